@@ -1,0 +1,407 @@
+"""Pins of the CPU oracle against facts fixed by the paper or by mathematics.
+
+Every test here checks the oracle (never the GPU library) against something
+other than itself: values printed in the paper (Fig. 'adj'), closed forms of
+the Euler recursion, published generator outputs, library distributions
+(scipy), brute force from the connection predicate, and hand-derived spike
+timings.  CPU only.
+"""
+import math
+
+import numpy as np
+import pytest
+from scipy import stats
+
+import inputs as I
+import oracle
+
+TAG = oracle.TAG
+
+
+# --------------------------------------------------------------- generator
+
+def test_splitmix64_published_outputs():
+    # First three outputs of the SplitMix64 reference generator started from
+    # state 0 (Steele, Lea & Flood 2014; the public-domain reference code
+    # splitmix64.c): the state advances by the golden gamma per call.
+    g = 0x9E3779B97F4A7C15
+    want = [0xE220A8397B1DCDAF, 0x6E789E6AA1B965F4, 0x06C45D188009454F]
+    got = [oracle.splitmix64((i * g) % 2**64) for i in range(3)]
+    assert got == want
+
+
+def test_hash_streams_are_uniform_and_distinct():
+    # u24 of the V0 stream is uniform on [0,1) (KS test) and distinct tags
+    # give uncorrelated streams.
+    n = 20000
+    u = np.array([oracle.hash64(7, TAG["V0"], i, 0) >> 40 for i in range(n)]) / 2.0**24
+    assert stats.kstest(u, "uniform").pvalue > 1e-3
+    v = np.array([oracle.hash64(7, TAG["POIS"], i, 0) >> 40 for i in range(n)]) / 2.0**24
+    assert abs(np.corrcoef(u, v)[0, 1]) < 5.0 / math.sqrt(n)
+
+
+# ------------------------------------------------------------ neuron model
+
+def _isolated(**over):
+    """One or more neurons without synapses (explicit empty adjacency)."""
+    n = over.pop("n", 1)
+    cfg = I.explicit_params(n, **over)
+    row_ptr = np.zeros(n + 1, dtype=np.uint64)
+    empty = np.zeros(0, dtype=np.uint32)
+    return oracle.Net(cfg, csr=(row_ptr, empty, np.zeros(0, np.float32), None))
+
+
+@pytest.mark.parametrize("v0", [-55.0, -50.5, -70.0, -60.0])
+def test_euler_decay_closed_form(v0):
+    # Without input, forward Euler of dV/dt = (V_rest - V)/tau gives
+    # V_n - V_rest = (V_0 - V_rest) (1 - k)^n exactly in real arithmetic,
+    # k the fp32 value of dt/tau.  fp32 rounding adds at most ~1.5 ulp per
+    # step, damped by (1-k) per step: total below (1/k) * 2 ulp(64).
+    net = _isolated(v0_lo=v0, v0_hi=v0)
+    k = float(np.float32(0.1 / 20.0))
+    assert net.derived()["k"] == np.float32(k)
+    bound = (1.0 / k) * 2.0 * np.spacing(np.float32(64.0))
+    for n in (1, 10, 100, 1000, 5000):
+        while net.t < n:
+            net.run(1)
+        v, _ = net.state()
+        exact = -60.0 + (v0 + 60.0) * (1.0 - k) ** n
+        assert abs(float(v[0]) - exact) <= bound, (n, v[0], exact)
+        if v0 == -60.0:
+            assert v[0] == np.float32(-60.0)  # V_rest is a fixed point, exactly
+
+
+def test_no_drive_literal_workloads_are_silent():
+    # V0 < V_th for every neuron and the leak pulls V towards V_rest < V_th,
+    # so without external drive nothing ever fires (C0 literal).
+    net = oracle.Net(I.config(0))
+    r = net.run(1000)
+    assert r["counts"].sum() == 0
+
+
+@pytest.mark.parametrize("ibias", [0.06, 0.1, 0.2])
+def test_constant_drive_period(ibias):
+    # With constant input I the Euler map V <- V + k (V_rest - V) + I has the
+    # fixed point V* = V_rest + I/k and V_m - V* = (V_reset - V*)(1-k)^m, so
+    # threshold is reached at update m = ceil(ln((V*-V_reset)/(V*-V_th)) / -ln(1-k)),
+    # and after each spike ref_steps held steps precede m more updates: the
+    # inter-spike interval is exactly ref_steps + m.  (The chosen drives put
+    # the real crossing at least 0.28 steps away from an integer, far beyond
+    # fp32 rounding.)
+    net = _isolated(v0_lo=-60.0, v0_hi=-60.0, i_bias=ibias)
+    d = net.derived()
+    k = float(d["k"])
+    vstar = -60.0 + ibias / k
+    x = math.log((vstar + 60.0) / (vstar + 50.0)) / -math.log(1.0 - k)
+    assert min(x - math.floor(x), math.ceil(x) - x) > 0.25
+    m = math.ceil(x)
+    r = net.run(2000)
+    times = np.nonzero(r["counts"])[0]
+    assert len(times) >= 3
+    assert times[0] == m - 1          # the m-th update happens at step m-1
+    assert d["ref_steps"] == 50       # round(5 ms / 0.1 ms)
+    assert np.all(np.diff(times) == d["ref_steps"] + m)
+
+
+def test_refractory_and_threshold_rules():
+    net = _isolated(v0_lo=-60.0, v0_hi=-60.0)
+    # inside the refractory period: counter decrements, V held at V_reset,
+    # input dropped
+    v, ref, sp = net.update_one(0, 0, -55.0, 3, isyn_f=100.0)
+    assert (v, ref, sp) == (np.float32(-60.0), 2, False)
+    # V == V_th exactly fires (threshold test is >=): V_rest + 0 + 10 = -50
+    v, ref, sp = net.update_one(0, 0, -60.0, 0, isyn_f=10.0)
+    assert sp and v == np.float32(-60.0) and ref == 50
+    # one fp32 step below threshold does not fire (-60 + below = -50 - ulp(50))
+    below = float(np.float32(10.0) - np.spacing(np.float32(50.0)))
+    v, ref, sp = net.update_one(0, 0, -60.0, 0, isyn_f=below)
+    assert not sp and v < -50.0 and ref == 0
+
+
+# ---------------------------------------------------------------- delivery
+
+def test_fig_adj_delivery_matches_paper_figure():
+    fx = I.fig_adj()
+    cfg = I.explicit_params(fx["n"])
+    net = oracle.Net(cfg, csr=(fx["row_ptr"], fx["col"], fx["w"], fx["delay"]))
+    out = net.deliver(fx["spikes"])
+    assert out.tolist() == [float(x) for x in fx["expect_input"]]
+    rp = fx["row_ptr"]
+    events = sum(int(rp[s + 1] - rp[s]) for s in fx["spikes"])
+    assert events == fx["expect_events"][0] == int(out.sum())
+    tgt, _, _ = net.row(9)
+    assert tgt.tolist() == fx["expect_row9"]
+    # fixed-point mode: the same sums in units of 2^-S
+    cfgq = I.explicit_params(fx["n"], acc_mode=I.ACC_FIXED, fixed_shift=20)
+    netq = oracle.Net(cfgq, csr=(fx["row_ptr"], fx["col"], fx["w"], fx["delay"]))
+    _, q = netq.deliver(fx["spikes"], fixed=True)
+    assert (q == np.array(fx["expect_input"]) * 2**20).all()
+
+
+def _brute_bernoulli(cfg, spikes, delay=0):
+    """I_j = sum_i spiked_i * [pair (i,j) connected] * w_i from the predicate."""
+    n, seed = cfg["n"], cfg["seed"]
+    thr = math.floor(cfg["p"] * 2**32)
+    ne = round(cfg["frac_exc"] * n)
+    span = cfg["delay_max"] - cfg["delay_min"] + 1
+    out = np.zeros(n)
+    for i in spikes:
+        wi = cfg["w_exc"] if i < ne else cfg["w_inh"]
+        for j in range(n):
+            if (oracle.hash64(seed, TAG["CONN"], int(i), j) >> 32) < thr:
+                d = cfg["delay_min"]
+                if span > 1:
+                    h = oracle.hash64(seed, TAG["DELAY"], int(i), j) >> 32
+                    d += (h * span) >> 32
+                if delay == 0 or d == delay:
+                    out[j] += wi
+    return out
+
+
+@pytest.mark.parametrize("seed", [1, 2, 3])
+def test_brute_force_bernoulli_delivery(seed):
+    cfg = I.config(0, seed=seed, n=48, p=0.3, delay_max=3)
+    net = oracle.Net(cfg)
+    spikes = I.spike_set(48, 12, seed=100 + seed)
+    for delay in (0, 1, 2, 3):
+        got = net.deliver(spikes, delay=delay)
+        want = _brute_bernoulli(cfg, spikes, delay)
+        np.testing.assert_allclose(got, want, rtol=0, atol=1e-12)
+
+
+def test_brute_force_fixed_out_delivery():
+    cfg = I.config(4, n=40, k_out=25, delay_max=4, seed=9)
+    net = oracle.Net(cfg)
+    spikes = I.spike_set(40, 10, seed=5)
+    want = np.zeros(40)
+    ne = round(0.8 * 40)
+    for s in spikes:
+        for j in range(25):
+            t = ((oracle.hash64(9, TAG["TGT"], int(s), j) >> 32) * 40) >> 32
+            want[t] += cfg["w_exc"] if s < ne else cfg["w_inh"]
+    np.testing.assert_allclose(net.deliver(spikes), want, rtol=0, atol=1e-12)
+
+
+def test_brute_force_fixed_in_delivery():
+    cfg = I.config(2, n=50, k_in_exc=6, k_in_inh=3, delay_min=2, delay_max=2, seed=4)
+    net = oracle.Net(cfg)
+    spikes = I.spike_set(50, 20, seed=8)
+    spiked = np.zeros(50, bool)
+    spiked[spikes] = True
+    ne = 40
+    want = np.zeros(50)
+    for j in range(50):
+        for k in range(6):
+            s = ((oracle.hash64(4, TAG["SRC_E"], j, k) >> 32) * ne) >> 32
+            want[j] += cfg["w_exc"] if spiked[s] else 0.0
+        for k in range(3):
+            s = ne + (((oracle.hash64(4, TAG["SRC_I"], j, k) >> 32) * 10) >> 32)
+            want[j] += cfg["w_inh"] if spiked[s] else 0.0
+    np.testing.assert_allclose(net.deliver(spikes), want, rtol=0, atol=1e-12)
+
+
+def test_delay_chain_spike_timing():
+    # Chain 0->1->2->3->4 with per-synapse delays; every neuron starts above
+    # threshold (all fire at step 0), no refractory period, weight 15 mV
+    # lifts a resting neuron above threshold.  Neuron j then fires at every
+    # step t_{j-1} + d_j for each firing step t_{j-1} of neuron j-1.
+    delays = [1, 3, 2, 5]
+    n = 5
+    row_ptr = np.array([0, 1, 2, 3, 4, 4], dtype=np.uint64)
+    col = np.array([1, 2, 3, 4], dtype=np.uint32)
+    w = np.full(4, 15.0, dtype=np.float32)
+    cfg = I.explicit_params(n, v0_lo=-49.0, v0_hi=-49.0, t_ref_ms=0.0, delay_min=1,
+                            delay_max=5)
+    net = oracle.Net(cfg, csr=(row_ptr, col, w, np.array(delays, dtype=np.uint8)))
+    fire = [{0}]
+    for j in range(1, n):
+        fire.append({0} | {t + delays[j - 1] for t in fire[j - 1]})
+    T = 20
+    r = net.run(T)
+    for t in range(T):
+        got = set(r["raster"][int(r["offs"][t]):int(r["offs"][t + 1])].tolist())
+        want = {j for j in range(n) if t in fire[j]}
+        assert got == want, (t, got, want)
+
+
+# -------------------------------------------------------- generator checks
+
+def _rows_sorted(row_ptr, col, delay, w):
+    for s in range(len(row_ptr) - 1):
+        a, b = int(row_ptr[s]), int(row_ptr[s + 1])
+        key = list(zip(col[a:b].tolist(), delay[a:b].tolist(), w[a:b].view(np.uint32).tolist()))
+        if key != sorted(key):
+            return False
+    return True
+
+
+def test_fixed_out_invariants():
+    cfg = I.config(4, n=3000, k_out=150, seed=2)
+    net = oracle.Net(cfg)
+    rp, col, w, d = net.csr()
+    assert (np.diff(rp) == 150).all()
+    assert col.max() < 3000 and d.min() >= 1 and d.max() <= 20
+    assert _rows_sorted(rp, col, d, w)
+    # targets uniform over [0, n): in-degree ~ Binomial(n*k, 1/n)
+    indeg = np.bincount(col, minlength=3000)
+    assert abs(indeg.mean() - 150) < 1e-9
+    assert abs(indeg.var() / 150 - 1) < 0.1
+    # delays uniform over 1..20
+    assert stats.chisquare(np.bincount(d, minlength=21)[1:]).pvalue > 1e-4
+
+
+def test_fixed_in_invariants():
+    cfg = I.config(2, n=2000, k_in_exc=160, k_in_inh=40, seed=3)
+    net = oracle.Net(cfg)
+    rp, col, w, d = net.csr()
+    ne = 1600
+    src = np.repeat(np.arange(2000), np.diff(rp).astype(np.int64))
+    from_exc = np.bincount(col[src < ne], minlength=2000)
+    from_inh = np.bincount(col[src >= ne], minlength=2000)
+    assert (from_exc == 160).all() and (from_inh == 40).all()
+    assert (d == 15).all()
+    assert set(np.unique(w[src < ne])) == {np.float32(0.1)}
+    assert set(np.unique(w[src >= ne])) == {np.float32(-0.5)}
+    assert _rows_sorted(rp, col, d, w)
+
+
+def test_bernoulli_invariants():
+    n, p = 2000, 0.02
+    cfg = I.config(0, n=n, p=p, seed=11)
+    net = oracle.Net(cfg)
+    rp, col, w, d = net.csr()
+    nnz = int(rp[-1])
+    mu, sd = n * n * p, math.sqrt(n * n * p * (1 - p))
+    assert abs(nnz - mu) < 5 * sd
+    deg = np.diff(rp).astype(np.float64)
+    # row lengths ~ Binomial(n, p)
+    assert abs(deg.mean() - n * p) < 5 * math.sqrt(p * (1 - p) / 1)  # per-row sd / sqrt(1)
+    assert abs(deg.var() / (n * p * (1 - p)) - 1) < 0.15
+    assert _rows_sorted(rp, col, d, w)
+    # at most one synapse per ordered pair, autapses allowed (Fig. 'adj')
+    pairs = np.repeat(np.arange(n), deg.astype(np.int64)) * n + col
+    assert len(np.unique(pairs)) == nnz
+
+
+def test_width_estimate_mu_plus_3_sigma_is_not_a_bound():
+    # Sec. III-B sizes the padded list as max(mu + 3 sigma); for Binomial row
+    # lengths about 0.135 % of rows exceed it (normal tail), so rows must be
+    # sized exactly.  Check the generator's tail matches the Binomial tail.
+    n, p = 4000, 0.05
+    net = oracle.Net(I.config(0, n=n, p=p, seed=5))
+    rp, _, _, _ = net.csr()
+    deg = np.diff(rp)
+    width = n * p + 3 * math.sqrt(n * p * (1 - p))
+    frac = (deg > width).mean()
+    want = stats.binom.sf(math.floor(width), n, p)
+    assert abs(frac - want) < 5 * math.sqrt(want / n) + 1e-4
+
+
+# ------------------------------------------------------------ Poisson drive
+
+@pytest.mark.parametrize("lam", [0.37, 1.0, 6.94, 23.15])
+def test_poisson_table_matches_scipy(lam):
+    thr = oracle.poisson_table(lam)
+    L = len(thr)
+    assert thr[-1] == 2**32
+    want = np.floor(stats.poisson.cdf(np.arange(L - 1), lam) * 2.0**32)
+    assert np.all(np.abs(thr[:-1].astype(np.float64) - want) <= 2.0)
+    assert stats.poisson.sf(L - 2, lam) < 1e-9
+
+
+def test_poisson_drive_moments():
+    # tau_m huge => leak contributes nothing at fp32 precision, so each step
+    # V grows by exactly K * w with w = 1: recover the counts K.
+    lam = 1.0
+    net = _isolated(n=400, v0_lo=0.0, v0_hi=0.0, v_rest=0.0, v_th=1e9, v_reset=0.0,
+                    tau_m_ms=1e30, ext_lambda=lam, ext_w=1.0)
+    prev = np.zeros(400)
+    ks = []
+    for _ in range(100):
+        net.run(1)
+        v, _ = net.state()
+        ks.append(v - prev)
+        prev = v.astype(np.float64)
+    K = np.concatenate(ks)
+    assert np.all(K == np.round(K)) and K.min() >= 0
+    m = K.size
+    assert abs(K.mean() - lam) < 5 * math.sqrt(lam / m)
+    assert abs(K.var() - lam) < 5 * lam * math.sqrt(2.0 / m) + 0.02
+
+
+def test_bernoulli_source_rate():
+    n, T = 5000, 200
+    cfg = I.config(3, n=n, k_out=0, rate_hz=10.0)  # p = 10 Hz * 1 ms = 0.01
+    net = oracle.Net(cfg)
+    r = net.run(T)
+    tot = int(r["counts"].sum())
+    mu = n * T * 0.01
+    assert abs(tot - mu) < 5 * math.sqrt(mu * 0.99)
+
+
+# ------------------------------------------------ whole-simulation checks
+
+def test_event_accounting_and_determinism():
+    cfg = I.config(0, driven=True, seed=2)
+    a = oracle.Net(cfg)
+    ra = a.run(300)
+    rp, _, _, _ = a.csr()
+    outdeg = np.diff(rp)
+    for t in range(300):
+        ids = ra["raster"][int(ra["offs"][t]):int(ra["offs"][t + 1])]
+        assert int(ra["events"][t]) == int(outdeg[ids].sum())
+        assert (np.diff(ids.astype(np.int64)) > 0).all()
+    assert ra["counts"].sum() > 0
+    b = oracle.Net(cfg)
+    rb = b.run(300)
+    assert (ra["raster"] == rb["raster"]).all()
+    c = oracle.Net(dict(cfg, seed=3))
+    assert not np.array_equal(c.csr()[1], a.csr()[1])
+
+
+@pytest.mark.parametrize("acc", [I.ACC_F32, I.ACC_FIXED])
+def test_resume_equals_single_run(acc):
+    cfg = I.config(0, driven=True, seed=1, acc_mode=acc)
+    a, b = oracle.Net(cfg), oracle.Net(cfg)
+    r1, r2 = a.run(50), a.run(50)
+    r = b.run(100)
+    assert np.array_equal(np.concatenate([r1["counts"], r2["counts"]]), r["counts"])
+    assert np.array_equal(np.concatenate([r1["raster"], r2["raster"]]), r["raster"])
+    va, ra_ = a.state()
+    vb, rb_ = b.state()
+    assert np.array_equal(va, vb) and np.array_equal(ra_, rb_)
+
+
+def test_fixed_point_close_to_fp32_and_quantisation_exact():
+    cfg = I.config(0, driven=True, seed=1, acc_mode=I.ACC_FIXED)
+    net = oracle.Net(cfg)
+    spikes = I.spike_set(1000, 100, seed=3)
+    f, q = net.deliver(spikes, fixed=True)
+    rp, col, w, _ = net.csr()
+    wq = np.rint(w.astype(np.float64) * 2**20).astype(np.int64)
+    want = np.zeros(1000, np.int64)
+    for s in spikes:
+        np.add.at(want, col[rp[s]:rp[s + 1]], wq[rp[s]:rp[s + 1]])
+    assert np.array_equal(q, want)
+    nterm = np.zeros(1000)
+    for s in spikes:
+        np.add.at(nterm, col[rp[s]:rp[s + 1]], 1)
+    assert np.all(np.abs(q * 2.0**-20 - f) <= nterm * 2.0**-21 + 1e-12)
+
+
+def test_fixed_point_overflow_guard():
+    # 40 in-synapses of 2000 mV each at S = 20: 40 * 2000 * 2^20 > 2^31
+    cfg = I.config(0, n=60, p=1.0, w_exc=2000.0, w_inh=-2000.0, acc_mode=I.ACC_FIXED,
+                   fixed_shift=20)
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.Net(cfg)
+    assert e.value.code == oracle.EOVERFLOW
+    cfg["fixed_shift"] = 8
+    oracle.Net(cfg)  # fits at a coarser shift
+
+
+def test_driven_workloads_are_active():
+    net = oracle.Net(I.config(0, driven=True, seed=1))
+    r = net.run(1000)
+    rate = r["counts"][200:].sum() / (1000 * 800 * 1e-4)
+    assert 5.0 < rate < 100.0
