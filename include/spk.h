@@ -1,0 +1,225 @@
+/*
+ * spk.h -- C ABI of libspk: spike transmission fused with the neuron update,
+ * for one AMD Instinct MI355X (gfx950).
+ *
+ * Method: Bautembach, Oikonomidis, Argyros, "Multi-GPU SNN Simulation with
+ * Static Load Balancing" (arXiv 2102.04681).
+ *   - Sec. III-A: neurons and synapses live in struct-of-arrays pools; the
+ *     topology is an adjacency list with sorted rows; spiking neuron IDs go
+ *     into one of 'delay' spike arrays and are delivered that many steps
+ *     later.
+ *   - Sec. III-B: the network is described by connectivity parameters and
+ *     expanded on the GPU ("uploaded to the GPU where it is expanded").
+ *   - Sec. III-C: every spike is delivered to all neighbours of its row.
+ *   - Sec. IV-A: single-precision forward Euler integration.
+ *   - Sec. V:    per-synapse delays through one adjacency list per delay.
+ *
+ * Conventions (all entry points):
+ *   - Every function returns spk_status (0 = SPK_OK, negative = error) and
+ *     never throws; spk_last_error() gives a message for the calling thread.
+ *   - The library owns all device memory of a network (allocated at create,
+ *     released by spk_destroy).  The caller owns every host buffer passed
+ *     in and passes its length explicitly; host buffers are only read or
+ *     written during the call.
+ *   - All device work of a network is ordered on one HIP stream: the one
+ *     given at creation (e.g. torch.cuda.current_stream().cuda_stream), or a
+ *     stream the library creates when NULL is given.  spk_step is
+ *     asynchronous; every spk_read_* / spk_export_* call synchronises that
+ *     stream before returning.
+ *   - A network is not thread-safe: calls on one network must not overlap.
+ *   - Errors: SPK_EINVAL bad argument or parameter, SPK_ENOMEM device or host
+ *     allocation failed, SPK_EHIP a HIP runtime error (message included),
+ *     SPK_EOVERFLOW a capacity or fixed-point range would be exceeded,
+ *     SPK_ESTATE call not valid in the network's current state.
+ */
+#ifndef SPK_H
+#define SPK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SPK_ABI_VERSION 1u
+#define SPK_MAX_DELAY_LISTS 64u  /* delay_max - delay_min + 1 must not exceed this */
+
+typedef enum {
+    SPK_OK = 0,
+    SPK_EINVAL = -1,
+    SPK_ENOMEM = -2,
+    SPK_EHIP = -3,
+    SPK_EOVERFLOW = -4,
+    SPK_ESTATE = -5
+} spk_status;
+
+enum { SPK_LIF = 0, SPK_SOURCE = 1 };
+enum { SPK_CONN_BERNOULLI = 0, SPK_CONN_FIXED_OUT = 1, SPK_CONN_FIXED_IN = 2,
+       SPK_CONN_EXPLICIT = 3 };
+enum { SPK_ACC_F32 = 0, SPK_ACC_FIXED = 1 };
+
+/* Network parameters (plain data).
+ *
+ * Neurons: IDs [0, n); excitatory = [0, round(frac_exc*n)), inhibitory = rest.
+ *   SPK_LIF: delta-current leaky integrate-and-fire, forward Euler in fp32
+ *     (Sec. IV-A), per step  V <- (V + k*(v_rest - V)) + I,  k = fp32(dt/tau),
+ *     spike when V >= v_th, then V = v_reset and round(t_ref/dt) steps held
+ *     at v_reset with arriving input dropped.  V0 ~ U[v0_lo, v0_hi).
+ *   SPK_SOURCE: fires independently with probability src_rate_hz*dt per
+ *     step; V integrates its input the same way (no threshold).
+ * Connectivity (Sec. III-B): Bernoulli(p) per ordered pair; fixed out-degree
+ *   k_out (uniform targets, with replacement); fixed in-degree k_in_exc from
+ *   the excitatory and k_in_inh from the inhibitory range (with
+ *   replacement); or explicit (spk_create_from_csr).  Self-connections are
+ *   allowed.  Weight = w_exc / w_inh by source population, or per synapse
+ *   w_lo + (w_hi-w_lo)*U[0,1) when w_uniform.  Delay (steps) uniform over
+ *   [delay_min, delay_max], delay_min >= 1.
+ * Drive: ext_lambda > 0 adds K*ext_w per neuron and step, K ~ Poisson(lambda);
+ *   i_bias is added every step.
+ * Accumulation: SPK_ACC_F32 sums inputs with fp32 atomics (order varies from
+ *   run to run); SPK_ACC_FIXED quantises weights to round(w * 2^fixed_shift)
+ *   and sums int32 exactly (deterministic, bit-reproducible).
+ * Every random draw is a pure function of (seed, stream, coordinates) via a
+ *   SplitMix64-based counter hash, so networks are reproducible exactly.
+ * Capacities: max_steps bounds the per-step records (counts, events) and the
+ *   total number of steps; raster_capacity bounds the recorded spike IDs
+ *   (0 = no raster). */
+typedef struct {
+    uint32_t abi_version;      /* must be SPK_ABI_VERSION */
+    uint32_t n;
+    uint64_t seed;
+    uint32_t neuron_kind;      /* SPK_LIF or SPK_SOURCE */
+    uint32_t conn_kind;        /* SPK_CONN_* */
+    double frac_exc;
+    double dt_ms, tau_m_ms, t_ref_ms;
+    float v_rest, v_th, v_reset, v0_lo, v0_hi, i_bias;
+    double p;
+    uint32_t k_out, k_in_exc, k_in_inh;
+    uint32_t w_uniform;
+    float w_exc, w_inh, w_lo, w_hi;
+    uint32_t delay_min, delay_max;
+    double ext_lambda;
+    float ext_w;
+    uint32_t acc_mode;         /* SPK_ACC_F32 or SPK_ACC_FIXED */
+    double src_rate_hz;
+    int32_t fixed_shift;       /* 0..30 */
+    uint32_t reserved0;
+    uint64_t max_steps;        /* >= 1 */
+    uint64_t raster_capacity;  /* spike IDs; 0 = no raster */
+} spk_params;
+
+typedef struct {
+    uint64_t n, nnz, steps;
+    uint64_t device_bytes;     /* device memory owned by the network */
+    uint32_t n_exc, ref_steps, ring_slots, delay_lists;
+    uint32_t max_piece;        /* longest (source, delay) synapse run */
+    uint32_t pois_len;
+    int32_t fixed_shift;
+    float k;
+    double bytes_per_synapse;  /* synapse storage / nnz (8 = int32 target + 32-bit weight) */
+} spk_stats_t;
+
+typedef struct spk_net spk_net;
+
+/* Fill *out with the parameters of workload `index` (0..4):
+ *   0  1 000 LIF, Bernoulli p=0.02, w +0.27/-4.5 mV, delay 1, 1 000 steps
+ *   1  250 000 LIF, p=0.02, weights x 80/(0.02 n), 10 000 steps
+ *   2  100 000 LIF, in-degree 8 000 exc + 2 000 inh, J=0.1, g=5, delay 15,
+ *      Poisson drive at twice threshold rate, 10 000 steps
+ *   3  1 000 000 Bernoulli sources at rate_hz, dt 1 ms, fan-out 1 000,
+ *      w ~ U[0,1e-3), 1 000 steps
+ *   4  2 000 000 LIF, fan-out 1 500, weights x 80/1500, delays 1..20, 5 000 steps
+ * driven != 0 adds an external Poisson drive at twice the threshold rate
+ * (lambda = 2*(v_th-v_rest)*(dt/tau)/w_exc, ext_w = w_exc) to LIF workloads
+ * that have none; without it workloads 0, 1 and 4 are silent.
+ * rate_hz is used by workload 3 only.  Errors: SPK_EINVAL for a bad index. */
+spk_status spk_preset(int index, int driven, double rate_hz, uint64_t seed, spk_params *out);
+
+/* Create a network and generate its connectivity on the GPU (Sec. III-B).
+ * stream: a hipStream_t, or NULL for a library-owned stream.  On success
+ * *out owns all device memory; release with spk_destroy.  Errors:
+ * SPK_EINVAL (parameters), SPK_ENOMEM, SPK_EHIP, SPK_EOVERFLOW (fixed-point
+ * range: the sum of |quantised weights| into one neuron plus the largest
+ * drive must fit in int32). */
+spk_status spk_create(const spk_params *params, void *stream, spk_net **out);
+
+/* Create a network from an explicit adjacency list (row per source neuron,
+ * any order inside rows; Fig. 'adj').  row_ptr: n+1 entries, row_ptr[0]=0;
+ * col, w: row_ptr[n] entries; delay: row_ptr[n] entries or NULL (= delay_min).
+ * params->n and params->conn_kind are ignored.  Host buffers, read only
+ * during the call. */
+spk_status spk_create_from_csr(const spk_params *params, uint32_t n, const uint64_t *row_ptr,
+                               const uint32_t *col, const float *w, const uint8_t *delay,
+                               void *stream, spk_net **out);
+
+/* Enqueue n_steps simulation steps on the network's stream (asynchronous).
+ * Each step t: deliver every synapse whose spike is due at t (source spiked
+ * at t - d for a synapse of delay d; Sec. III-A, III-C, V), update all
+ * neurons, compact the spiking IDs into the spike list of step t, record.
+ * Errors: SPK_EOVERFLOW if steps would exceed max_steps. */
+spk_status spk_step(spk_net *net, uint64_t n_steps);
+
+/* Wait for all enqueued work; reports device-side overflow flags. */
+spk_status spk_sync(spk_net *net);
+
+/* Per-step records for steps [t0, t0+n) (host output buffers of n entries):
+ * spike counts |S(t)|, synaptic events emitted at t (sum of the out-degrees
+ * of the neurons that spiked at t), synaptic events delivered at t (synapses
+ * whose spike arrived at t). */
+spk_status spk_read_spike_counts(spk_net *net, uint64_t t0, uint64_t n, uint32_t *out);
+spk_status spk_read_events(spk_net *net, uint64_t t0, uint64_t n, uint64_t *out);
+spk_status spk_read_delivered(spk_net *net, uint64_t t0, uint64_t n, uint64_t *out);
+
+/* Spike raster of steps [t0, t0+n): offs (n+1 entries, offs[0] = 0) and ids
+ * (cap entries); IDs of each step ascending.  SPK_EOVERFLOW if the raster
+ * capacity was exceeded during the run or cap is too small. */
+spk_status spk_read_raster(spk_net *net, uint64_t t0, uint64_t n, uint64_t *offs,
+                           uint32_t *ids, uint64_t cap);
+
+/* Membrane potentials and refractory counters (host buffers of n entries;
+ * either may be NULL). */
+spk_status spk_read_state(spk_net *net, float *v, uint8_t *ref);
+
+/* Deliver the listed spikes (IDs < n) through the synapses of delay `delay`
+ * (0 = every delay) with the same kernel the simulation uses, into a
+ * scratch input buffer that is copied to out_f32 (fp32 mode) or out_i32
+ * (fixed mode, units of 2^-fixed_shift); n entries.  Network state is not
+ * changed. */
+spk_status spk_debug_deliver(spk_net *net, const uint32_t *spikes, uint64_t n_spikes,
+                             uint32_t delay, float *out_f32, int32_t *out_i32);
+
+/* Export the rows (all synapses of the given source neurons), each row in
+ * canonical order (target, delay, weight bits).  offs: n_rows+1 entries;
+ * col/delay and w (fp32 mode) or wq (fixed mode) of cap entries; unused
+ * outputs may be NULL.  SPK_EOVERFLOW if cap is too small. */
+spk_status spk_export_rows(spk_net *net, const uint32_t *rows, uint64_t n_rows, uint64_t *offs,
+                           uint32_t *col, float *w, int32_t *wq, uint8_t *delay, uint64_t cap);
+
+/* The Poisson threshold table of the drive: thr[k] = floor(CDF(k) * 2^32),
+ * last entry 2^32; *len entries (0 without drive).  cap entries of thr. */
+spk_status spk_poisson_table(spk_net *net, uint64_t *thr, uint32_t cap, uint32_t *len);
+
+spk_status spk_stats(spk_net *net, spk_stats_t *out);
+
+/* Kernel timing: with profiling on, spk_step records HIP events around each
+ * launch of the delivery and update kernels on the network's stream, and
+ * spk_read_kernel_ms returns their summed durations (ms) and launch counts
+ * since the last reset.  Profiling off (default) records nothing. */
+spk_status spk_set_profiling(spk_net *net, int on);
+spk_status spk_read_kernel_ms(spk_net *net, double *deliver_ms, double *update_ms,
+                              uint64_t *launches);
+
+/* Plain device-to-device copy of `bytes` bytes (multiple of 16) through the
+ * library's streaming copy kernel on the network's stream, timed with HIP
+ * events: used to calibrate HBM traffic counters.  *ms may be NULL. */
+spk_status spk_hbm_copy(spk_net *net, uint64_t bytes, int reps, double *ms);
+
+void spk_destroy(spk_net *net);                 /* NULL-safe */
+const char *spk_last_error(void);               /* thread-local; never NULL */
+uint32_t spk_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

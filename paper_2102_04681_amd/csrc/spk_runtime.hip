@@ -1,0 +1,963 @@
+// spk_runtime.hip -- host runtime and C ABI of libspk (declared in spk.h).
+//
+// A network owns its device memory and orders all work on one HIP stream.
+// Creation expands the connectivity parameters on the GPU (paper Sec. III-B:
+// the layout description is expanded on the device), into one adjacency
+// list per distinct delay (Sec. V), each row sorted by target (Sec. III-A).
+// A step enqueues: delivery of the due spikes (Sec. III-C), the neuron
+// update with spike compaction, and optional raster recording.  Spike counts
+// stay on the device, so stepping never waits for the host.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "spk_internal.h"
+
+using namespace spk;
+
+namespace {
+
+thread_local std::string g_err;
+
+spk_status fail(spk_status st, const std::string &msg)
+{
+    g_err = msg;
+    return st;
+}
+
+#define SPK_HIP(expr)                                                                   \
+    do {                                                                                \
+        hipError_t e_ = (expr);                                                         \
+        if (e_ != hipSuccess)                                                           \
+            return fail(e_ == hipErrorOutOfMemory ? SPK_ENOMEM : SPK_EHIP,              \
+                        std::string(#expr) + ": " + hipGetErrorString(e_));             \
+    } while (0)
+
+#define SPK_TRY(expr)                   \
+    do {                                \
+        spk_status s_ = (expr);         \
+        if (s_ != SPK_OK) return s_;    \
+    } while (0)
+
+constexpr uint32_t kMaxPiece = 16384;    // longest (source, delay) run the sorter accepts
+constexpr uint32_t kPoisCap = 256;
+
+uint64_t prob_threshold(double p)
+{
+    if (!(p > 0.0)) return 0;
+    if (p >= 1.0) return 4294967296ull;
+    return (uint64_t)std::floor(p * 4294967296.0);
+}
+
+// Poisson(lambda) thresholds on a 32-bit uniform draw: T_k = floor(CDF(k)*2^32)
+// with the CDF summed in double from p_0 = exp(-lambda), p_k = p_{k-1}*lambda/k;
+// the table ends with 2^32 once the CDF reaches 1 - 2^-32.
+int poisson_thresholds(double lambda, std::vector<uint64_t> &thr)
+{
+    thr.clear();
+    if (!(lambda > 0.0) || lambda > 100.0) return -1;
+    double pk = std::exp(-lambda), cdf = pk;
+    for (uint32_t k = 0;; k++) {
+        const double T = std::floor(cdf * 4294967296.0);
+        if (T >= 4294967295.0 || k == kPoisCap - 1) {
+            thr.push_back(4294967296ull);
+            return (int)thr.size();
+        }
+        thr.push_back((uint64_t)T);
+        pk = (pk * lambda) / (double)(k + 1);
+        cdf = cdf + pk;
+    }
+}
+
+bool quantise(float w, int S, int32_t *out)
+{
+    const float x = std::rint(std::ldexp(w, S));
+    if (!(std::fabs(x) < 2147483648.0f)) return false;
+    *out = (int32_t)x;
+    return true;
+}
+
+}  // namespace
+
+struct spk_net {
+    spk_params P{};
+    // derived constants
+    uint32_t n = 0, n_exc = 0, lists = 1, dmin = 1, ring = 2, ref_steps = 0;
+    uint32_t pois_len = 0, max_piece = 0, bpp = 1;
+    float k = 0.f;
+    uint64_t conn_thr = 0, src_thr = 0, nnz = 0;
+    int32_t ext_wq = 0, bias_q = 0;
+    Keys keys{};
+    std::vector<uint64_t> pois;
+    // device
+    hipStream_t stream = nullptr;
+    bool own_stream = false;
+    int device = 0;
+    uint64_t *row_ptr = nullptr;
+    int2 *syn = nullptr;
+    uint32_t *outdeg = nullptr;
+    float *V = nullptr;
+    uint8_t *ref = nullptr;
+    void *acc = nullptr;
+    void *dbg_acc = nullptr;
+    uint32_t *ring_buf = nullptr, *ring_count = nullptr, *counts = nullptr, *flags = nullptr;
+    uint64_t *events = nullptr, *delivered = nullptr, *pois_dev = nullptr;
+    uint32_t *raster = nullptr;
+    uint64_t *raster_offs = nullptr;
+    uint32_t *dbg_count = nullptr;
+    uint64_t t = 0;
+    uint64_t device_bytes = 0;
+    std::vector<void *> allocs;
+    // profiling
+    bool profiling = false;
+    std::vector<hipEvent_t> ev_free;
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> ev_deliver, ev_update;
+    double ms_deliver = 0, ms_update = 0;
+    uint64_t launches = 0;
+};
+
+namespace {
+
+template <class T>
+spk_status dalloc(spk_net *net, T **p, size_t count)
+{
+    *p = nullptr;
+    const size_t bytes = (count ? count : 1) * sizeof(T);
+    void *q = nullptr;
+    hipError_t e = hipMalloc(&q, bytes);
+    if (e != hipSuccess)
+        return fail(SPK_ENOMEM, "hipMalloc of " + std::to_string(bytes) + " bytes: " +
+                                    hipGetErrorString(e));
+    net->allocs.push_back(q);
+    net->device_bytes += bytes;
+    *p = (T *)q;
+    return SPK_OK;
+}
+
+void dfree(spk_net *net, void *p)
+{
+    if (!p) return;
+    auto it = std::find(net->allocs.begin(), net->allocs.end(), p);
+    if (it != net->allocs.end()) net->allocs.erase(it);
+    (void)hipFree(p);
+}
+
+ModelArgs model_args(const spk_net *net)
+{
+    ModelArgs m{};
+    m.n = net->n;
+    m.kind = net->P.neuron_kind;
+    m.fixed = net->P.acc_mode == SPK_ACC_FIXED;
+    m.shift = net->P.fixed_shift;
+    m.k = net->k;
+    m.v_rest = net->P.v_rest;
+    m.v_th = net->P.v_th;
+    m.v_reset = net->P.v_reset;
+    m.i_bias = net->P.i_bias;
+    m.ext_w = net->P.ext_w;
+    m.ext_wq = net->ext_wq;
+    m.bias_q = net->bias_q;
+    m.ref_steps = net->ref_steps;
+    m.pois_len = net->pois_len;
+    m.src_thr = net->src_thr;
+    m.keys = net->keys;
+    return m;
+}
+
+NetDev net_dev(const spk_net *net)
+{
+    NetDev d{};
+    d.n = net->n;
+    d.lists = net->lists;
+    d.dmin = net->dmin;
+    d.ring_slots = net->ring;
+    d.cap = net->n;
+    d.row_ptr = net->row_ptr;
+    d.syn = net->syn;
+    d.outdeg = net->outdeg;
+    d.V = net->V;
+    d.ref = net->ref;
+    d.acc = net->acc;
+    d.ring = net->ring_buf;
+    d.ring_count = net->ring_count;
+    d.counts = net->counts;
+    d.events = net->events;
+    d.delivered = net->delivered;
+    d.pois = net->pois_dev;
+    d.flags = net->flags;
+    d.raster = net->raster;
+    d.raster_offs = net->raster_offs;
+    d.raster_cap = net->P.raster_capacity;
+    return d;
+}
+
+ConnArgs conn_args(const spk_net *net)
+{
+    ConnArgs c{};
+    c.n = net->n;
+    c.n_exc = net->n_exc;
+    c.kind = net->P.conn_kind;
+    c.lists = net->lists;
+    c.dmin = net->dmin;
+    c.k_out = net->P.k_out;
+    c.k_in_exc = net->P.k_in_exc;
+    c.k_in_inh = net->P.k_in_inh;
+    c.conn_thr = net->conn_thr;
+    c.w_uniform = net->P.w_uniform;
+    c.w_exc = net->P.w_exc;
+    c.w_inh = net->P.w_inh;
+    c.w_lo = net->P.w_lo;
+    c.w_hi = net->P.w_hi;
+    c.fixed = net->P.acc_mode == SPK_ACC_FIXED;
+    c.qscale = std::ldexp(1.0f, net->P.fixed_shift);
+    c.keys = net->keys;
+    return c;
+}
+
+// Validate parameters and compute the derived constants.
+spk_status derive(spk_net *net, bool explicit_csr)
+{
+    const spk_params &P = net->P;
+    if (P.abi_version != SPK_ABI_VERSION) return fail(SPK_EINVAL, "abi_version mismatch");
+    if (P.n == 0 || P.n > 2000000000u) return fail(SPK_EINVAL, "n must be in [1, 2e9]");
+    if (!(P.dt_ms > 0.0) || !(P.tau_m_ms > 0.0) || !(P.t_ref_ms >= 0.0))
+        return fail(SPK_EINVAL, "dt_ms, tau_m_ms must be > 0 and t_ref_ms >= 0");
+    if (P.delay_min < 1 || P.delay_max < P.delay_min || P.delay_max > 255)
+        return fail(SPK_EINVAL, "delays must satisfy 1 <= delay_min <= delay_max <= 255");
+    if (P.delay_max - P.delay_min + 1 > kMaxLists)
+        return fail(SPK_EINVAL, "at most 64 distinct delays");
+    if (!(P.frac_exc >= 0.0 && P.frac_exc <= 1.0)) return fail(SPK_EINVAL, "frac_exc in [0,1]");
+    if (P.neuron_kind > SPK_SOURCE) return fail(SPK_EINVAL, "neuron_kind");
+    if (P.acc_mode > SPK_ACC_FIXED) return fail(SPK_EINVAL, "acc_mode");
+    if (!explicit_csr && P.conn_kind > SPK_CONN_FIXED_IN) return fail(SPK_EINVAL, "conn_kind");
+    if (!(P.p >= 0.0 && P.p <= 1.0)) return fail(SPK_EINVAL, "p in [0,1]");
+    if (P.max_steps == 0) return fail(SPK_EINVAL, "max_steps must be >= 1");
+    if (!(P.ext_lambda >= 0.0) || P.ext_lambda > 100.0) return fail(SPK_EINVAL, "ext_lambda in [0,100]");
+    net->n = P.n;
+    net->n_exc = (uint32_t)std::llround(P.frac_exc * (double)P.n);
+    net->k = (float)(P.dt_ms / P.tau_m_ms);
+    const long long rs = std::llround(P.t_ref_ms / P.dt_ms);
+    if (rs < 0 || rs > 255) return fail(SPK_EINVAL, "t_ref/dt must round to 0..255 steps");
+    net->ref_steps = (uint32_t)rs;
+    net->dmin = P.delay_min;
+    net->lists = P.delay_max - P.delay_min + 1;
+    net->ring = P.delay_max + 1;
+    net->conn_thr = prob_threshold(P.p);
+    net->src_thr = prob_threshold(P.src_rate_hz * P.dt_ms * 1e-3);
+    if (!explicit_csr && P.conn_kind == SPK_CONN_FIXED_IN &&
+        ((P.k_in_exc > 0 && net->n_exc == 0) || (P.k_in_inh > 0 && net->n_exc == P.n)))
+        return fail(SPK_EINVAL, "fixed in-degree needs a non-empty source population");
+    if (P.ext_lambda > 0.0) {
+        const int L = poisson_thresholds(P.ext_lambda, net->pois);
+        if (L < 0) return fail(SPK_EINVAL, "ext_lambda");
+        net->pois_len = (uint32_t)L;
+    }
+    if (P.acc_mode == SPK_ACC_FIXED) {
+        if (P.fixed_shift < 0 || P.fixed_shift > 30) return fail(SPK_EINVAL, "fixed_shift in 0..30");
+        int32_t dummy;
+        const int S = P.fixed_shift;
+        if (!quantise(P.ext_w, S, &net->ext_wq) || !quantise(P.i_bias, S, &net->bias_q) ||
+            !quantise(P.w_exc, S, &dummy) || !quantise(P.w_inh, S, &dummy) ||
+            !quantise(P.w_lo, S, &dummy) || !quantise(P.w_hi, S, &dummy))
+            return fail(SPK_EOVERFLOW, "a weight does not fit int32 at this fixed_shift");
+    }
+    const uint64_t seed = P.seed;
+    net->keys.conn = stream_key(seed, TAG_CONN);
+    net->keys.tgt = stream_key(seed, TAG_TGT);
+    net->keys.src_e = stream_key(seed, TAG_SRC_E);
+    net->keys.src_i = stream_key(seed, TAG_SRC_I);
+    net->keys.w = stream_key(seed, TAG_W);
+    net->keys.delay = stream_key(seed, TAG_DELAY);
+    net->keys.v0 = stream_key(seed, TAG_V0);
+    net->keys.pois = stream_key(seed, TAG_POIS);
+    net->keys.bern = stream_key(seed, TAG_BERN);
+    return SPK_OK;
+}
+
+spk_status setup_stream(spk_net *net, void *stream)
+{
+    SPK_HIP(hipGetDevice(&net->device));
+    if (stream) {
+        net->stream = (hipStream_t)stream;
+    } else {
+        SPK_HIP(hipStreamCreateWithFlags(&net->stream, hipStreamNonBlocking));
+        net->own_stream = true;
+    }
+    return SPK_OK;
+}
+
+// State, spike ring and per-step records.
+spk_status alloc_state(spk_net *net)
+{
+    const uint32_t n = net->n;
+    const uint64_t T = net->P.max_steps;
+    hipStream_t s = net->stream;
+    SPK_TRY(dalloc(net, &net->V, n));
+    SPK_TRY(dalloc(net, &net->ref, n));
+    SPK_TRY(dalloc(net, (uint32_t **)&net->acc, n));
+    SPK_TRY(dalloc(net, (uint32_t **)&net->dbg_acc, n));
+    SPK_TRY(dalloc(net, &net->ring_buf, (size_t)net->ring * n));
+    SPK_TRY(dalloc(net, &net->ring_count, net->ring));
+    SPK_TRY(dalloc(net, &net->counts, T));
+    SPK_TRY(dalloc(net, &net->events, T));
+    SPK_TRY(dalloc(net, &net->delivered, T));
+    SPK_TRY(dalloc(net, &net->flags, 1));
+    SPK_TRY(dalloc(net, &net->dbg_count, 1));
+    SPK_TRY(dalloc(net, &net->raster_offs, T + 1));
+    SPK_TRY(dalloc(net, &net->raster, net->P.raster_capacity));
+    SPK_TRY(dalloc(net, &net->pois_dev, net->pois_len ? net->pois_len : 1));
+    SPK_HIP(hipMemsetAsync(net->acc, 0, (size_t)n * 4, s));
+    SPK_HIP(hipMemsetAsync(net->ring_count, 0, (size_t)net->ring * 4, s));
+    SPK_HIP(hipMemsetAsync(net->counts, 0, T * 4, s));
+    SPK_HIP(hipMemsetAsync(net->events, 0, T * 8, s));
+    SPK_HIP(hipMemsetAsync(net->delivered, 0, T * 8, s));
+    SPK_HIP(hipMemsetAsync(net->flags, 0, 4, s));
+    SPK_HIP(hipMemsetAsync(net->raster_offs, 0, (T + 1) * 8, s));
+    if (net->pois_len)
+        SPK_HIP(hipMemcpyAsync(net->pois_dev, net->pois.data(), net->pois_len * 8,
+                               hipMemcpyHostToDevice, s));
+    ModelArgs m = model_args(net);
+    SPK_HIP(init_state(m, net->P.v0_lo, net->P.v0_hi, net->V, net->ref, s));
+    return SPK_OK;
+}
+
+// After the piece counts are known: offsets, synapse storage.
+spk_status finish_counts(spk_net *net, uint32_t *cnt, uint64_t pieces)
+{
+    hipStream_t s = net->stream;
+    uint64_t *bsum = nullptr;
+    uint32_t *maxp = nullptr;
+    SPK_TRY(dalloc(net, &net->row_ptr, pieces + 1));
+    SPK_TRY(dalloc(net, &bsum, scan_scratch_elems(pieces) + 1));
+    SPK_TRY(dalloc(net, &maxp, 1));
+    SPK_HIP(hipMemsetAsync(maxp, 0, 4, s));
+    SPK_HIP(scan_counts(cnt, pieces, net->row_ptr, bsum, maxp, s));
+    uint64_t nnz = 0;
+    uint32_t mp = 0;
+    SPK_HIP(hipMemcpyAsync(&nnz, net->row_ptr + pieces, 8, hipMemcpyDeviceToHost, s));
+    SPK_HIP(hipMemcpyAsync(&mp, maxp, 4, hipMemcpyDeviceToHost, s));
+    SPK_HIP(hipStreamSynchronize(s));
+    dfree(net, bsum);
+    dfree(net, maxp);
+    net->nnz = nnz;
+    net->max_piece = mp;
+    net->bpp = std::max<uint32_t>(1, (mp + kWave - 1) / kWave);
+    if (mp > kMaxPiece)
+        return fail(SPK_EINVAL, "a (source, delay) synapse run of " + std::to_string(mp) +
+                                    " exceeds the supported " + std::to_string(kMaxPiece));
+    SPK_TRY(dalloc(net, &net->syn, nnz));
+    return SPK_OK;
+}
+
+// Sort every piece by (target, weight bits); out-degrees; fixed-point guard.
+spk_status finish_pieces(spk_net *net, uint64_t pieces)
+{
+    hipStream_t s = net->stream;
+    uint32_t *large = nullptr, *n_large = nullptr;
+    SPK_TRY(dalloc(net, &n_large, 1));
+    SPK_HIP(hipMemsetAsync(n_large, 0, 4, s));
+    // pieces longer than the small-sort limit: at most nnz / 257 of them
+    const uint64_t max_large = std::min<uint64_t>(pieces, net->nnz / 257 + 1);
+    SPK_TRY(dalloc(net, &large, max_large));
+    SPK_HIP(sort_small_pieces(net->row_ptr, net->syn, pieces, large, n_large, s));
+    uint32_t nl = 0;
+    SPK_HIP(hipMemcpyAsync(&nl, n_large, 4, hipMemcpyDeviceToHost, s));
+    SPK_HIP(hipStreamSynchronize(s));
+    if (nl > max_large) return fail(SPK_EHIP, "internal: large-piece list overflow");
+    uint32_t pow2 = 1;
+    while (pow2 < net->max_piece) pow2 <<= 1;
+    SPK_HIP(sort_large_pieces(net->row_ptr, net->syn, large, nl, pow2, s));
+    SPK_HIP(hipStreamSynchronize(s));
+    dfree(net, large);
+    dfree(net, n_large);
+    SPK_TRY(dalloc(net, &net->outdeg, net->n));
+    SPK_HIP(out_degree(net->row_ptr, net->n, net->lists, net->outdeg, s));
+    if (net->P.acc_mode == SPK_ACC_FIXED) {
+        // Guard: all in-synapses of one neuron at once, plus the largest
+        // Poisson count and the bias, must fit in int32.
+        uint64_t *insum = nullptr, *mx = nullptr;
+        SPK_TRY(dalloc(net, &insum, net->n));
+        SPK_TRY(dalloc(net, &mx, 1));
+        SPK_HIP(hipMemsetAsync(insum, 0, (size_t)net->n * 8, s));
+        SPK_HIP(hipMemsetAsync(mx, 0, 8, s));
+        SPK_HIP(in_abs_sum(net->syn, net->nnz, insum, s));
+        SPK_HIP(max_u64(insum, net->n, mx, s));
+        uint64_t m = 0;
+        SPK_HIP(hipMemcpyAsync(&m, mx, 8, hipMemcpyDeviceToHost, s));
+        SPK_HIP(hipStreamSynchronize(s));
+        dfree(net, insum);
+        dfree(net, mx);
+        const uint64_t kmax = net->pois_len ? net->pois_len - 1 : 0;
+        const uint64_t extra = kmax * (uint64_t)std::llabs((long long)net->ext_wq) +
+                               (uint64_t)std::llabs((long long)net->bias_q);
+        if (m + extra > 2147483647ull)
+            return fail(SPK_EOVERFLOW, "fixed-point inputs could exceed int32; lower fixed_shift");
+    }
+    return SPK_OK;
+}
+
+spk_status generate(spk_net *net)
+{
+    hipStream_t s = net->stream;
+    const uint64_t pieces = (uint64_t)net->lists * net->n;
+    uint32_t *cnt = nullptr;
+    SPK_TRY(dalloc(net, &cnt, pieces));
+    SPK_HIP(hipMemsetAsync(cnt, 0, pieces * 4, s));
+    ConnArgs c = conn_args(net);
+    const uint32_t kind = net->P.conn_kind;
+    if (kind == SPK_CONN_FIXED_IN) SPK_HIP(gen_in_count(c, cnt, s));
+    else SPK_HIP(gen_count_rows(c, cnt, s));
+    SPK_TRY(finish_counts(net, cnt, pieces));
+    if (kind == SPK_CONN_FIXED_IN) {
+        SPK_HIP(hipMemsetAsync(cnt, 0, pieces * 4, s));
+        SPK_HIP(gen_in_fill(c, net->row_ptr, cnt, net->syn, s));
+    } else {
+        SPK_HIP(gen_fill_rows(c, net->row_ptr, net->syn, s));
+    }
+    SPK_HIP(hipStreamSynchronize(s));
+    dfree(net, cnt);
+    return finish_pieces(net, pieces);
+}
+
+spk_status check_ready(spk_net *net)
+{
+    if (!net) return fail(SPK_EINVAL, "null network");
+    return SPK_OK;
+}
+
+spk_status sync_flags(spk_net *net, uint32_t *flags_out)
+{
+    SPK_HIP(hipStreamSynchronize(net->stream));
+    uint32_t f = 0;
+    SPK_HIP(hipMemcpy(&f, net->flags, 4, hipMemcpyDeviceToHost));
+    if (flags_out) *flags_out = f;
+    if (f & 1u) return fail(SPK_EOVERFLOW, "spike list overflow");
+    return SPK_OK;
+}
+
+spk_status collect_profile(spk_net *net)
+{
+    SPK_HIP(hipStreamSynchronize(net->stream));
+    for (auto *v : {&net->ev_deliver, &net->ev_update}) {
+        double &acc = v == &net->ev_deliver ? net->ms_deliver : net->ms_update;
+        for (auto &pr : *v) {
+            float ms = 0;
+            SPK_HIP(hipEventElapsedTime(&ms, pr.first, pr.second));
+            acc += ms;
+            net->ev_free.push_back(pr.first);
+            net->ev_free.push_back(pr.second);
+        }
+        v->clear();
+    }
+    return SPK_OK;
+}
+
+spk_status get_event(spk_net *net, hipEvent_t *e)
+{
+    if (!net->ev_free.empty()) {
+        *e = net->ev_free.back();
+        net->ev_free.pop_back();
+        return SPK_OK;
+    }
+    SPK_HIP(hipEventCreate(e));
+    return SPK_OK;
+}
+
+void destroy_net(spk_net *net)
+{
+    if (!net) return;
+    if (net->stream) (void)hipStreamSynchronize(net->stream);
+    for (auto &pr : net->ev_deliver) { (void)hipEventDestroy(pr.first); (void)hipEventDestroy(pr.second); }
+    for (auto &pr : net->ev_update) { (void)hipEventDestroy(pr.first); (void)hipEventDestroy(pr.second); }
+    for (auto e : net->ev_free) (void)hipEventDestroy(e);
+    for (void *p : net->allocs) (void)hipFree(p);
+    if (net->own_stream && net->stream) (void)hipStreamDestroy(net->stream);
+    delete net;
+}
+
+}  // namespace
+
+// ===================================================================== ABI
+
+extern "C" {
+
+uint32_t spk_abi_version(void) { return SPK_ABI_VERSION; }
+
+const char *spk_last_error(void) { return g_err.c_str(); }
+
+spk_status spk_preset(int index, int driven, double rate_hz, uint64_t seed, spk_params *out)
+{
+    if (!out) return fail(SPK_EINVAL, "null output");
+    spk_params p{};
+    p.abi_version = SPK_ABI_VERSION;
+    p.seed = seed;
+    p.neuron_kind = SPK_LIF;
+    p.frac_exc = 0.8;
+    p.dt_ms = 0.1;
+    p.tau_m_ms = 20.0;
+    p.t_ref_ms = 5.0;
+    p.v_rest = -60.0f;
+    p.v_th = -50.0f;
+    p.v_reset = -60.0f;
+    p.v0_lo = -60.0f;
+    p.v0_hi = -50.0f;
+    p.delay_min = p.delay_max = 1;
+    p.acc_mode = SPK_ACC_F32;
+    p.fixed_shift = 20;
+    switch (index) {
+    case 0:
+        p.n = 1000; p.conn_kind = SPK_CONN_BERNOULLI; p.p = 0.02;
+        p.w_exc = 0.27f; p.w_inh = -4.5f; p.max_steps = 1000;
+        break;
+    case 1: {
+        p.n = 250000; p.conn_kind = SPK_CONN_BERNOULLI; p.p = 0.02;
+        const double sc = 80.0 / (0.02 * p.n);
+        p.w_exc = (float)(0.27 * sc); p.w_inh = (float)(-4.5 * sc); p.max_steps = 10000;
+        break;
+    }
+    case 2:
+        p.n = 100000; p.conn_kind = SPK_CONN_FIXED_IN; p.k_in_exc = 8000; p.k_in_inh = 2000;
+        p.w_exc = 0.1f; p.w_inh = -0.5f; p.delay_min = p.delay_max = 15;
+        p.ext_lambda = 1.0; p.ext_w = 0.1f; p.max_steps = 10000;
+        break;
+    case 3:
+        p.n = 1000000; p.neuron_kind = SPK_SOURCE; p.frac_exc = 1.0; p.dt_ms = 1.0;
+        p.conn_kind = SPK_CONN_FIXED_OUT; p.k_out = 1000; p.w_uniform = 1; p.w_lo = 0.0f;
+        p.w_hi = 1e-3f; p.src_rate_hz = rate_hz; p.max_steps = 1000;
+        break;
+    case 4: {
+        p.n = 2000000; p.conn_kind = SPK_CONN_FIXED_OUT; p.k_out = 1500;
+        const double sc = 80.0 / 1500.0;
+        p.w_exc = (float)(0.27 * sc); p.w_inh = (float)(-4.5 * sc);
+        p.delay_min = 1; p.delay_max = 20; p.max_steps = 5000;
+        break;
+    }
+    default:
+        return fail(SPK_EINVAL, "preset index must be 0..4");
+    }
+    if (driven && p.neuron_kind == SPK_LIF && p.ext_lambda == 0.0) {
+        const double theta = (double)p.v_th - (double)p.v_rest;
+        p.ext_lambda = 2.0 * theta * (p.dt_ms / p.tau_m_ms) / (double)p.w_exc;
+        p.ext_w = p.w_exc;
+    }
+    *out = p;
+    return SPK_OK;
+}
+
+spk_status spk_create(const spk_params *params, void *stream, spk_net **out)
+{
+    if (!params || !out) return fail(SPK_EINVAL, "null argument");
+    *out = nullptr;
+    spk_net *net = new (std::nothrow) spk_net();
+    if (!net) return fail(SPK_ENOMEM, "host allocation");
+    net->P = *params;
+    spk_status st = derive(net, false);
+    if (st == SPK_OK) st = setup_stream(net, stream);
+    if (st == SPK_OK) st = generate(net);
+    if (st == SPK_OK) st = alloc_state(net);
+    if (st == SPK_OK) st = sync_flags(net, nullptr);
+    if (st != SPK_OK) {
+        std::string msg = g_err;
+        destroy_net(net);
+        g_err = msg;
+        return st;
+    }
+    *out = net;
+    return SPK_OK;
+}
+
+spk_status spk_create_from_csr(const spk_params *params, uint32_t n, const uint64_t *row_ptr,
+                               const uint32_t *col, const float *w, const uint8_t *delay,
+                               void *stream, spk_net **out)
+{
+    if (!params || !out || !row_ptr || (row_ptr[n] && (!col || !w)))
+        return fail(SPK_EINVAL, "null argument");
+    *out = nullptr;
+    spk_net *net = new (std::nothrow) spk_net();
+    if (!net) return fail(SPK_ENOMEM, "host allocation");
+    net->P = *params;
+    net->P.n = n;
+    net->P.conn_kind = SPK_CONN_EXPLICIT;
+    auto run = [&]() -> spk_status {
+        SPK_TRY(derive(net, true));
+        if (row_ptr[0] != 0) return fail(SPK_EINVAL, "row_ptr[0] must be 0");
+        for (uint32_t s = 0; s < n; s++)
+            if (row_ptr[s + 1] < row_ptr[s]) return fail(SPK_EINVAL, "row_ptr not monotone");
+        const uint64_t nnz = row_ptr[n];
+        for (uint64_t e = 0; e < nnz; e++) {
+            if (col[e] >= n) return fail(SPK_EINVAL, "target id out of range");
+            const uint32_t d = delay ? delay[e] : net->P.delay_min;
+            if (d < net->P.delay_min || d > net->P.delay_max)
+                return fail(SPK_EINVAL, "delay out of [delay_min, delay_max]");
+            if (net->P.acc_mode == SPK_ACC_FIXED) {
+                int32_t q;
+                if (!quantise(w[e], net->P.fixed_shift, &q))
+                    return fail(SPK_EOVERFLOW, "a weight does not fit int32 at this fixed_shift");
+            }
+        }
+        SPK_TRY(setup_stream(net, stream));
+        hipStream_t s = net->stream;
+        uint64_t *in_ptr = nullptr;
+        uint32_t *in_col = nullptr;
+        float *in_w = nullptr;
+        uint8_t *in_d = nullptr;
+        SPK_TRY(dalloc(net, &in_ptr, (size_t)n + 1));
+        SPK_TRY(dalloc(net, &in_col, nnz));
+        SPK_TRY(dalloc(net, &in_w, nnz));
+        SPK_HIP(hipMemcpyAsync(in_ptr, row_ptr, ((size_t)n + 1) * 8, hipMemcpyHostToDevice, s));
+        if (nnz) {
+            SPK_HIP(hipMemcpyAsync(in_col, col, nnz * 4, hipMemcpyHostToDevice, s));
+            SPK_HIP(hipMemcpyAsync(in_w, w, nnz * 4, hipMemcpyHostToDevice, s));
+        }
+        if (delay) {
+            SPK_TRY(dalloc(net, &in_d, nnz));
+            if (nnz) SPK_HIP(hipMemcpyAsync(in_d, delay, nnz, hipMemcpyHostToDevice, s));
+        }
+        const uint64_t pieces = (uint64_t)net->lists * n;
+        uint32_t *cnt = nullptr;
+        SPK_TRY(dalloc(net, &cnt, pieces));
+        SPK_HIP(hipMemsetAsync(cnt, 0, pieces * 4, s));
+        ConnArgs c = conn_args(net);
+        SPK_HIP(csr_count(c, in_ptr, in_d, cnt, s));
+        SPK_TRY(finish_counts(net, cnt, pieces));
+        SPK_HIP(csr_fill(c, in_ptr, in_col, in_w, in_d, net->row_ptr, net->syn, s));
+        SPK_HIP(hipStreamSynchronize(s));
+        dfree(net, cnt);
+        dfree(net, in_ptr);
+        dfree(net, in_col);
+        dfree(net, in_w);
+        dfree(net, in_d);
+        SPK_TRY(finish_pieces(net, pieces));
+        SPK_TRY(alloc_state(net));
+        return sync_flags(net, nullptr);
+    };
+    spk_status st = run();
+    if (st != SPK_OK) {
+        std::string msg = g_err;
+        destroy_net(net);
+        g_err = msg;
+        return st;
+    }
+    *out = net;
+    return SPK_OK;
+}
+
+spk_status spk_step(spk_net *net, uint64_t n_steps)
+{
+    SPK_TRY(check_ready(net));
+    if (net->t + n_steps > net->P.max_steps)
+        return fail(SPK_EOVERFLOW, "max_steps exceeded");
+    hipStream_t s = net->stream;
+    const ModelArgs m = model_args(net);
+    const NetDev nd = net_dev(net);
+    const int grid = deliver_grid();
+    for (uint64_t k = 0; k < n_steps; k++) {
+        const uint64_t t = net->t;
+        DeliverArgs a{};
+        a.net = nd;
+        a.fixed = m.fixed;
+        a.bpp = net->bpp;
+        a.t = t;
+        a.list_lo = 0;
+        a.list_hi = net->lists;
+        a.acc = net->acc;
+        a.delivered = net->delivered + t;
+        a.zero_count = net->ring_count + (t % net->ring);
+        hipEvent_t e0 = nullptr, e1 = nullptr, e2 = nullptr, e3 = nullptr;
+        if (net->profiling) {
+            SPK_TRY(get_event(net, &e0));
+            SPK_TRY(get_event(net, &e1));
+            SPK_TRY(get_event(net, &e2));
+            SPK_TRY(get_event(net, &e3));
+            SPK_HIP(hipEventRecord(e0, s));
+        }
+        SPK_HIP(deliver(a, grid, s));
+        if (net->profiling) {
+            SPK_HIP(hipEventRecord(e1, s));
+            SPK_HIP(hipEventRecord(e2, s));
+        }
+        SPK_HIP(update(m, nd, t, s));
+        if (net->profiling) {
+            SPK_HIP(hipEventRecord(e3, s));
+            net->ev_deliver.push_back({e0, e1});
+            net->ev_update.push_back({e2, e3});
+            net->launches++;
+        }
+        if (net->P.raster_capacity) SPK_HIP(record(nd, t, s));
+        net->t = t + 1;
+    }
+    return SPK_OK;
+}
+
+spk_status spk_sync(spk_net *net)
+{
+    SPK_TRY(check_ready(net));
+    return sync_flags(net, nullptr);
+}
+
+spk_status spk_read_spike_counts(spk_net *net, uint64_t t0, uint64_t n, uint32_t *out)
+{
+    SPK_TRY(check_ready(net));
+    if (t0 + n > net->P.max_steps || (n && !out)) return fail(SPK_EINVAL, "range");
+    SPK_TRY(sync_flags(net, nullptr));
+    if (n) SPK_HIP(hipMemcpy(out, net->counts + t0, n * 4, hipMemcpyDeviceToHost));
+    return SPK_OK;
+}
+
+spk_status spk_read_events(spk_net *net, uint64_t t0, uint64_t n, uint64_t *out)
+{
+    SPK_TRY(check_ready(net));
+    if (t0 + n > net->P.max_steps || (n && !out)) return fail(SPK_EINVAL, "range");
+    SPK_TRY(sync_flags(net, nullptr));
+    if (n) SPK_HIP(hipMemcpy(out, net->events + t0, n * 8, hipMemcpyDeviceToHost));
+    return SPK_OK;
+}
+
+spk_status spk_read_delivered(spk_net *net, uint64_t t0, uint64_t n, uint64_t *out)
+{
+    SPK_TRY(check_ready(net));
+    if (t0 + n > net->P.max_steps || (n && !out)) return fail(SPK_EINVAL, "range");
+    SPK_TRY(sync_flags(net, nullptr));
+    if (n) SPK_HIP(hipMemcpy(out, net->delivered + t0, n * 8, hipMemcpyDeviceToHost));
+    return SPK_OK;
+}
+
+spk_status spk_read_raster(spk_net *net, uint64_t t0, uint64_t n, uint64_t *offs, uint32_t *ids,
+                           uint64_t cap)
+{
+    SPK_TRY(check_ready(net));
+    if (!net->P.raster_capacity) return fail(SPK_ESTATE, "raster recording is off");
+    if (t0 + n > net->t || !offs) return fail(SPK_EINVAL, "range");
+    uint32_t f = 0;
+    SPK_TRY(sync_flags(net, &f));
+    if (f & 2u) return fail(SPK_EOVERFLOW, "raster capacity exceeded during the run");
+    std::vector<uint64_t> o(n + 1);
+    SPK_HIP(hipMemcpy(o.data(), net->raster_offs + t0, (n + 1) * 8, hipMemcpyDeviceToHost));
+    const uint64_t total = o[n] - o[0];
+    if (total > cap || (total && !ids)) return fail(SPK_EOVERFLOW, "ids buffer too small");
+    if (total) SPK_HIP(hipMemcpy(ids, net->raster + o[0], total * 4, hipMemcpyDeviceToHost));
+    for (uint64_t k = 0; k <= n; k++) offs[k] = o[k] - o[0];
+    for (uint64_t k = 0; k < n; k++) std::sort(ids + offs[k], ids + offs[k + 1]);
+    return SPK_OK;
+}
+
+spk_status spk_read_state(spk_net *net, float *v, uint8_t *ref)
+{
+    SPK_TRY(check_ready(net));
+    SPK_TRY(sync_flags(net, nullptr));
+    if (v) SPK_HIP(hipMemcpy(v, net->V, (size_t)net->n * 4, hipMemcpyDeviceToHost));
+    if (ref) SPK_HIP(hipMemcpy(ref, net->ref, net->n, hipMemcpyDeviceToHost));
+    return SPK_OK;
+}
+
+spk_status spk_debug_deliver(spk_net *net, const uint32_t *spikes, uint64_t n_spikes, uint32_t delay,
+                             float *out_f32, int32_t *out_i32)
+{
+    SPK_TRY(check_ready(net));
+    const bool fixed = net->P.acc_mode == SPK_ACC_FIXED;
+    if ((fixed && !out_i32) || (!fixed && !out_f32))
+        return fail(SPK_EINVAL, "output buffer for this accumulation mode is required");
+    if (n_spikes > 0xffffffffull || (n_spikes && !spikes)) return fail(SPK_EINVAL, "spikes");
+    for (uint64_t k = 0; k < n_spikes; k++)
+        if (spikes[k] >= net->n) return fail(SPK_EINVAL, "spike id out of range");
+    if (delay && (delay < net->dmin || delay >= net->dmin + net->lists))
+        return fail(SPK_EINVAL, "delay not in [delay_min, delay_max]");
+    hipStream_t s = net->stream;
+    SPK_TRY(sync_flags(net, nullptr));
+    uint32_t *d_sp = nullptr;
+    SPK_TRY(dalloc(net, &d_sp, n_spikes));
+    const uint32_t cnt = (uint32_t)n_spikes;
+    spk_status st = SPK_OK;
+    do {
+        hipError_t e = hipSuccess;
+        if (n_spikes) e = hipMemcpyAsync(d_sp, spikes, n_spikes * 4, hipMemcpyHostToDevice, s);
+        if (e == hipSuccess) e = hipMemcpyAsync(net->dbg_count, &cnt, 4, hipMemcpyHostToDevice, s);
+        if (e == hipSuccess) e = hipMemsetAsync(net->dbg_acc, 0, (size_t)net->n * 4, s);
+        if (e != hipSuccess) { st = fail(SPK_EHIP, hipGetErrorString(e)); break; }
+        DeliverArgs a{};
+        a.net = net_dev(net);
+        a.fixed = fixed;
+        a.bpp = net->bpp;
+        a.t = 0;
+        a.list_lo = delay ? delay - net->dmin : 0;
+        a.list_hi = delay ? a.list_lo + 1 : net->lists;
+        a.acc = net->dbg_acc;
+        a.dbg_spikes = d_sp;
+        a.dbg_count = net->dbg_count;
+        e = deliver(a, deliver_grid(), s);
+        if (e == hipSuccess) e = hipStreamSynchronize(s);
+        if (e == hipSuccess)
+            e = hipMemcpy(fixed ? (void *)out_i32 : (void *)out_f32, net->dbg_acc,
+                          (size_t)net->n * 4, hipMemcpyDeviceToHost);
+        if (e != hipSuccess) st = fail(SPK_EHIP, hipGetErrorString(e));
+    } while (0);
+    dfree(net, d_sp);
+    return st;
+}
+
+spk_status spk_export_rows(spk_net *net, const uint32_t *rows, uint64_t n_rows, uint64_t *offs,
+                           uint32_t *col, float *w, int32_t *wq, uint8_t *delay, uint64_t cap)
+{
+    SPK_TRY(check_ready(net));
+    if (!offs || (n_rows && !rows)) return fail(SPK_EINVAL, "null argument");
+    for (uint64_t r = 0; r < n_rows; r++)
+        if (rows[r] >= net->n) return fail(SPK_EINVAL, "row id out of range");
+    SPK_TRY(sync_flags(net, nullptr));
+    offs[0] = 0;
+    if (!n_rows) return SPK_OK;
+    hipStream_t s = net->stream;
+    const uint64_t pieces = n_rows * net->lists;
+    uint32_t *d_rows = nullptr;
+    uint64_t *d_lens = nullptr, *d_off = nullptr;
+    SPK_TRY(dalloc(net, &d_rows, n_rows));
+    SPK_TRY(dalloc(net, &d_lens, pieces));
+    SPK_TRY(dalloc(net, &d_off, pieces));
+    std::vector<uint64_t> lens(pieces), poff(pieces);
+    SPK_HIP(hipMemcpyAsync(d_rows, rows, n_rows * 4, hipMemcpyHostToDevice, s));
+    SPK_HIP(export_lens(net->row_ptr, net->n, net->lists, d_rows, n_rows, d_lens, s));
+    SPK_HIP(hipMemcpyAsync(lens.data(), d_lens, pieces * 8, hipMemcpyDeviceToHost, s));
+    SPK_HIP(hipStreamSynchronize(s));
+    uint64_t tot = 0;
+    for (uint64_t r = 0; r < n_rows; r++) {
+        for (uint32_t j = 0; j < net->lists; j++) {
+            poff[r * net->lists + j] = tot;
+            tot += lens[r * net->lists + j];
+        }
+        offs[r + 1] = tot;
+    }
+    if (tot > cap) {
+        dfree(net, d_rows); dfree(net, d_lens); dfree(net, d_off);
+        return fail(SPK_EOVERFLOW, "export buffers too small");
+    }
+    uint32_t *d_col = nullptr, *d_wb = nullptr;
+    uint8_t *d_del = nullptr;
+    SPK_TRY(dalloc(net, &d_col, tot));
+    SPK_TRY(dalloc(net, &d_wb, tot));
+    SPK_TRY(dalloc(net, &d_del, tot));
+    SPK_HIP(hipMemcpyAsync(d_off, poff.data(), pieces * 8, hipMemcpyHostToDevice, s));
+    SPK_HIP(export_gather(net->row_ptr, net->syn, net->n, net->lists, net->dmin, d_rows, n_rows, d_off,
+                          d_col, d_wb, d_del, s));
+    std::vector<uint32_t> hc(tot), hw(tot);
+    std::vector<uint8_t> hd(tot);
+    if (tot) {
+        SPK_HIP(hipMemcpyAsync(hc.data(), d_col, tot * 4, hipMemcpyDeviceToHost, s));
+        SPK_HIP(hipMemcpyAsync(hw.data(), d_wb, tot * 4, hipMemcpyDeviceToHost, s));
+        SPK_HIP(hipMemcpyAsync(hd.data(), d_del, tot, hipMemcpyDeviceToHost, s));
+    }
+    SPK_HIP(hipStreamSynchronize(s));
+    dfree(net, d_rows); dfree(net, d_lens); dfree(net, d_off);
+    dfree(net, d_col); dfree(net, d_wb); dfree(net, d_del);
+    // canonical order per row: (target, delay, stored weight bits)
+    std::vector<uint64_t> idx;
+    for (uint64_t r = 0; r < n_rows; r++) {
+        const uint64_t a = offs[r], b = offs[r + 1];
+        idx.resize(b - a);
+        for (uint64_t e = a; e < b; e++) idx[e - a] = e;
+        std::sort(idx.begin(), idx.end(), [&](uint64_t x, uint64_t y) {
+            if (hc[x] != hc[y]) return hc[x] < hc[y];
+            if (hd[x] != hd[y]) return hd[x] < hd[y];
+            return hw[x] < hw[y];
+        });
+        for (uint64_t e = a; e < b; e++) {
+            const uint64_t src = idx[e - a];
+            if (col) col[e] = hc[src];
+            if (delay) delay[e] = hd[src];
+            if (w) std::memcpy(&w[e], &hw[src], 4);
+            if (wq) wq[e] = (int32_t)hw[src];
+        }
+    }
+    return SPK_OK;
+}
+
+spk_status spk_poisson_table(spk_net *net, uint64_t *thr, uint32_t cap, uint32_t *len)
+{
+    SPK_TRY(check_ready(net));
+    if (!len) return fail(SPK_EINVAL, "null len");
+    *len = net->pois_len;
+    if (net->pois_len > cap || (net->pois_len && !thr)) return fail(SPK_EOVERFLOW, "cap");
+    for (uint32_t k = 0; k < net->pois_len; k++) thr[k] = net->pois[k];
+    return SPK_OK;
+}
+
+spk_status spk_stats(spk_net *net, spk_stats_t *out)
+{
+    SPK_TRY(check_ready(net));
+    if (!out) return fail(SPK_EINVAL, "null output");
+    spk_stats_t st{};
+    st.n = net->n;
+    st.nnz = net->nnz;
+    st.steps = net->t;
+    st.device_bytes = net->device_bytes;
+    st.n_exc = net->n_exc;
+    st.ref_steps = net->ref_steps;
+    st.ring_slots = net->ring;
+    st.delay_lists = net->lists;
+    st.max_piece = net->max_piece;
+    st.pois_len = net->pois_len;
+    st.fixed_shift = net->P.fixed_shift;
+    st.k = net->k;
+    st.bytes_per_synapse = (double)sizeof(int2);
+    *out = st;
+    return SPK_OK;
+}
+
+spk_status spk_set_profiling(spk_net *net, int on)
+{
+    SPK_TRY(check_ready(net));
+    SPK_TRY(collect_profile(net));
+    net->profiling = on != 0;
+    net->ms_deliver = net->ms_update = 0;
+    net->launches = 0;
+    return SPK_OK;
+}
+
+spk_status spk_read_kernel_ms(spk_net *net, double *deliver_ms, double *update_ms,
+                              uint64_t *launches)
+{
+    SPK_TRY(check_ready(net));
+    SPK_TRY(collect_profile(net));
+    if (deliver_ms) *deliver_ms = net->ms_deliver;
+    if (update_ms) *update_ms = net->ms_update;
+    if (launches) *launches = net->launches;
+    return SPK_OK;
+}
+
+spk_status spk_hbm_copy(spk_net *net, uint64_t bytes, int reps, double *ms)
+{
+    SPK_TRY(check_ready(net));
+    if (bytes == 0 || bytes % 16 || reps < 1) return fail(SPK_EINVAL, "bytes multiple of 16, reps >= 1");
+    hipStream_t s = net->stream;
+    void *a = nullptr, *b = nullptr;
+    SPK_TRY(dalloc(net, (uint8_t **)&a, bytes));
+    SPK_TRY(dalloc(net, (uint8_t **)&b, bytes));
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    spk_status st = SPK_OK;
+    do {
+        hipError_t e = hipMemsetAsync(a, 1, bytes, s);
+        if (e == hipSuccess) e = stream_copy(a, b, bytes, s);  // warm-up
+        if (e == hipSuccess) e = hipEventCreate(&e0);
+        if (e == hipSuccess) e = hipEventCreate(&e1);
+        if (e == hipSuccess) e = hipEventRecord(e0, s);
+        for (int r = 0; r < reps && e == hipSuccess; r++) e = stream_copy(a, b, bytes, s);
+        if (e == hipSuccess) e = hipEventRecord(e1, s);
+        if (e == hipSuccess) e = hipEventSynchronize(e1);
+        float t = 0;
+        if (e == hipSuccess) e = hipEventElapsedTime(&t, e0, e1);
+        if (e != hipSuccess) { st = fail(SPK_EHIP, hipGetErrorString(e)); break; }
+        if (ms) *ms = t;
+    } while (0);
+    if (e0) (void)hipEventDestroy(e0);
+    if (e1) (void)hipEventDestroy(e1);
+    dfree(net, a);
+    dfree(net, b);
+    return st;
+}
+
+void spk_destroy(spk_net *net) { destroy_net(net); }
+
+}  // extern "C"
