@@ -58,6 +58,10 @@ enum { SPK_LIF = 0, SPK_SOURCE = 1 };
 enum { SPK_CONN_BERNOULLI = 0, SPK_CONN_FIXED_OUT = 1, SPK_CONN_FIXED_IN = 2,
        SPK_CONN_EXPLICIT = 3 };
 enum { SPK_ACC_F32 = 0, SPK_ACC_FIXED = 1 };
+/* Delivery strategy (same results, different speed): AUTO picks from the
+ * network's shape; DIRECT makes each target tile read its runs of the due
+ * rows; BINNED first sorts the due events into per-tile bins. */
+enum { SPK_DELIVERY_AUTO = 0, SPK_DELIVERY_DIRECT = 1, SPK_DELIVERY_BINNED = 2 };
 
 /* Network parameters (plain data).
  *
@@ -74,12 +78,15 @@ enum { SPK_ACC_F32 = 0, SPK_ACC_FIXED = 1 };
  *   replacement); or explicit (spk_create_from_csr).  Self-connections are
  *   allowed.  Weight = w_exc / w_inh by source population, or per synapse
  *   w_lo + (w_hi-w_lo)*U[0,1) when w_uniform.  Delay (steps) uniform over
- *   [delay_min, delay_max], delay_min >= 1.
+ *   [delay_min, delay_max], 1 <= delay_min <= delay_max <= 253, at most 64
+ *   distinct delays.
  * Drive: ext_lambda > 0 adds K*ext_w per neuron and step, K ~ Poisson(lambda);
  *   i_bias is added every step.
- * Accumulation: SPK_ACC_F32 sums inputs with fp32 atomics (order varies from
- *   run to run); SPK_ACC_FIXED quantises weights to round(w * 2^fixed_shift)
- *   and sums int32 exactly (deterministic, bit-reproducible).
+ * Accumulation: SPK_ACC_F32 keeps fp32 weights and sums each neuron's input
+ *   exactly (64-bit fixed point whose unit is chosen at creation so that every
+ *   weight is an exact multiple), then rounds the sum once to fp32;
+ *   SPK_ACC_FIXED quantises weights to round(w * 2^fixed_shift) and sums
+ *   int32.  Both are deterministic and bit-reproducible.
  * Every random draw is a pure function of (seed, stream, coordinates) via a
  *   SplitMix64-based counter hash, so networks are reproducible exactly.
  * Capacities: max_steps bounds the per-step records (counts, events) and the
@@ -104,7 +111,7 @@ typedef struct {
     uint32_t acc_mode;         /* SPK_ACC_F32 or SPK_ACC_FIXED */
     double src_rate_hz;
     int32_t fixed_shift;       /* 0..30 */
-    uint32_t reserved0;
+    uint32_t delivery;         /* SPK_DELIVERY_*: how events reach their target tile */
     uint64_t max_steps;        /* >= 1 */
     uint64_t raster_capacity;  /* spike IDs; 0 = no raster */
 } spk_params;
@@ -115,9 +122,13 @@ typedef struct {
     uint32_t n_exc, ref_steps, ring_slots, delay_lists;
     uint32_t max_piece;        /* longest (source, delay) synapse run */
     uint32_t pois_len;
-    int32_t fixed_shift;
+    int32_t fixed_shift;       /* fixed mode: S; fp32 mode: the unit 2^-S64 of the exact sums */
     float k;
     double bytes_per_synapse;  /* synapse storage / nnz (8 = int32 target + 32-bit weight) */
+    uint32_t tile_width;       /* target neurons per tile (one workgroup each) */
+    uint32_t tiles;
+    uint32_t delivery;         /* SPK_DELIVERY_DIRECT or SPK_DELIVERY_BINNED as chosen */
+    uint32_t bin_chunk;        /* rows per binning chunk (binned delivery) */
 } spk_stats_t;
 
 typedef struct spk_net spk_net;
@@ -202,13 +213,14 @@ spk_status spk_poisson_table(spk_net *net, uint64_t *thr, uint32_t cap, uint32_t
 
 spk_status spk_stats(spk_net *net, spk_stats_t *out);
 
-/* Kernel timing: with profiling on, spk_step records HIP events around each
- * launch of the delivery and update kernels on the network's stream, and
- * spk_read_kernel_ms returns their summed durations (ms) and launch counts
- * since the last reset.  Profiling off (default) records nothing. */
+/* Kernel timing.  By default spk_step replays batches of steps captured in
+ * a HIP graph.  With profiling on, it launches each kernel directly with HIP
+ * events around the binning kernel (binned delivery only) and the tile
+ * kernel (delivery into LDS + neuron update) on the network's stream, and
+ * spk_read_kernel_ms returns their summed durations (ms) and the number of
+ * steps since the last spk_set_profiling call. */
 spk_status spk_set_profiling(spk_net *net, int on);
-spk_status spk_read_kernel_ms(spk_net *net, double *deliver_ms, double *update_ms,
-                              uint64_t *launches);
+spk_status spk_read_kernel_ms(spk_net *net, double *bin_ms, double *tile_ms, uint64_t *steps);
 
 /* Plain device-to-device copy of `bytes` bytes (multiple of 16) through the
  * library's streaming copy kernel on the network's stream, timed with HIP

@@ -77,6 +77,8 @@ def lib():
         L.orc_splitmix64.argtypes = [u64]
         L.orc_hash.restype = u64
         L.orc_hash.argtypes = [u64, u32, u64, u64]
+        L.orc_hash_step.restype = u64
+        L.orc_hash_step.argtypes = [u64, u32, u32, u32]
         L.orc_poisson_table.restype = i32
         L.orc_poisson_table.argtypes = [C.c_double, P, i32]
         L.orc_create.restype = i32
@@ -139,6 +141,10 @@ def splitmix64(z: int) -> int:
 
 def hash64(seed: int, tag: int, a: int, b: int) -> int:
     return lib().orc_hash(seed, tag, a, b)
+
+
+def hash_step(seed: int, tag: int, i: int, t: int) -> int:
+    return lib().orc_hash_step(seed, tag, i, t)
 
 
 def poisson_table(lam: float, cap: int = 256) -> np.ndarray:

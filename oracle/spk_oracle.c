@@ -77,6 +77,17 @@ uint64_t orc_hash(uint64_t seed, uint32_t tag, uint64_t a, uint64_t b)
     return orc_splitmix64(h ^ b);
 }
 
+/* Per-step draws (Poisson drive, Bernoulli firing of neuron i at step t):
+ * one mixer round over the stream key and the packed counter (t, i),
+ *     H_step(seed, tag, i, t) = mix(key(seed, tag) ^ (t * 2^32 + i)),
+ * key(seed, tag) = mix(mix(seed) ^ tag); distinct (i, t) give distinct
+ * counters and hence distinct outputs. */
+uint64_t orc_hash_step(uint64_t seed, uint32_t tag, uint32_t i, uint32_t t)
+{
+    uint64_t key = orc_splitmix64(orc_splitmix64(seed) ^ (uint64_t)tag);
+    return orc_splitmix64(key ^ (((uint64_t)t << 32) | (uint64_t)i));
+}
+
 static uint32_t hi32(uint64_t h) { return (uint32_t)(h >> 32); }
 
 /* uniform in [0,1): the top 24 bits scaled by 2^-24 (exact in fp32) */
@@ -612,7 +623,7 @@ static int update_neuron(const orc_net *net, uint64_t t, uint32_t i, float *v, u
     const orc_params *P = &net->P;
     const orc_derived *D = &net->D;
     uint32_t K = 0;
-    if (D->pois_len) K = poisson_draw(net, orc_hash(P->seed, ORC_TAG_POIS, i, t));
+    if (D->pois_len) K = poisson_draw(net, orc_hash_step(P->seed, ORC_TAG_POIS, i, (uint32_t)t));
     float I;
     if (P->acc_mode == ORC_ACC_FIXED) {
         int64_t q = isyn_q + (int64_t)K * D->ext_wq + D->bias_q;
@@ -628,7 +639,7 @@ static int update_neuron(const orc_net *net, uint64_t t, uint32_t i, float *v, u
         float b = D->k * a;
         float c = *v + b;
         *v = c + I;
-        return hi32(orc_hash(P->seed, ORC_TAG_BERN, i, t)) < D->src_thr ? 1 : 0;
+        return hi32(orc_hash_step(P->seed, ORC_TAG_BERN, i, (uint32_t)t)) < D->src_thr ? 1 : 0;
     }
     if (*ref > 0) {
         *ref = (uint8_t)(*ref - 1);

@@ -81,8 +81,11 @@ typedef struct orc_net orc_net;
 
 /* SplitMix64 (Steele, Lea, Flood 2014): the output function applied to state z. */
 uint64_t orc_splitmix64(uint64_t z);
-/* Counter-based hash H(seed, tag, a, b). */
+/* Counter-based hash H(seed, tag, a, b) (connectivity, weights, delays, V0). */
 uint64_t orc_hash(uint64_t seed, uint32_t tag, uint64_t a, uint64_t b);
+/* Per-step draw of neuron i at step t (< 2^32): one mixer round over the
+ * stream key and the counter t * 2^32 + i (Poisson drive, Bernoulli firing). */
+uint64_t orc_hash_step(uint64_t seed, uint32_t tag, uint32_t i, uint32_t t);
 /* Poisson CDF thresholds T_k (k = 0..len-1); returns len or <0 on error. */
 int orc_poisson_table(double lambda, uint64_t *thr, int cap);
 

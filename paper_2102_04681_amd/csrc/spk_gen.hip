@@ -363,15 +363,61 @@ __global__ __launch_bounds__(kBlock) void k_out_degree(const uint64_t *row_ptr, 
     outdeg[s] = (uint32_t)d;
 }
 
-__global__ __launch_bounds__(kBlock) void k_in_abs_sum(const int2 *syn, uint64_t nnz,
+// Per-target sum of |weight| over all in-synapses: exact in quantised units
+// (fixed mode), or an upper bound in units of 2^-24 (fp32 mode: each term
+// rounded up), used to size the accumulators.
+__global__ __launch_bounds__(kBlock) void k_in_abs_sum(const int2 *syn, uint64_t nnz, int fixed,
                                                       unsigned long long *insum)
 {
     for (uint64_t e = (uint64_t)blockIdx.x * kBlock + threadIdx.x; e < nnz;
          e += (uint64_t)gridDim.x * kBlock) {
         const int2 x = syn[e];
-        const long long q = x.y < 0 ? -(long long)x.y : (long long)x.y;
-        atomicAdd(&insum[(uint32_t)x.x], (unsigned long long)q);
+        unsigned long long q;
+        if (fixed) {
+            q = (unsigned long long)(x.y < 0 ? -(long long)x.y : (long long)x.y);
+        } else {
+            const float w = fabsf(__int_as_float(x.y));
+            q = (unsigned long long)ceil(ldexp((double)w, 24));
+        }
+        atomicAdd(&insum[(uint32_t)x.x], q);
     }
+}
+
+// Sub-piece boundaries of target-sorted pieces: off[p*bounds + b] is the
+// offset (from the piece start) of the first synapse with target >= b*width.
+// Also the longest sub-piece (targets in [b*width, (b+1)*width)).
+__global__ __launch_bounds__(kBlock) void k_piece_offsets(const uint64_t *row_ptr, const int2 *syn,
+                                                         uint64_t pieces, uint32_t bounds,
+                                                         uint32_t width, uint16_t *off,
+                                                         uint32_t *max_sub)
+{
+    uint32_t mx = 0;
+    for (uint64_t k = (uint64_t)blockIdx.x * kBlock + threadIdx.x; k < pieces * bounds;
+         k += (uint64_t)gridDim.x * kBlock) {
+        const uint64_t p = k / bounds;
+        const uint32_t b = (uint32_t)(k % bounds);
+        const uint64_t beg = row_ptr[p];
+        const uint32_t L = (uint32_t)(row_ptr[p + 1] - beg);
+        const uint64_t lo_t = (uint64_t)b * width, hi_t = lo_t + width;
+        uint32_t lo = 0, hi = L;  // first index with target >= lo_t
+        while (lo < hi) {
+            const uint32_t mid = (lo + hi) >> 1;
+            if ((uint64_t)(uint32_t)syn[beg + mid].x < lo_t) lo = mid + 1; else hi = mid;
+        }
+        const uint32_t first = lo;
+        hi = L;  // first index with target >= hi_t
+        while (lo < hi) {
+            const uint32_t mid = (lo + hi) >> 1;
+            if ((uint64_t)(uint32_t)syn[beg + mid].x < hi_t) lo = mid + 1; else hi = mid;
+        }
+        off[k] = (uint16_t)first;
+        mx = lo - first > mx ? lo - first : mx;
+    }
+    for (int o = 32; o > 0; o >>= 1) {
+        const uint32_t y = __shfl_xor(mx, o);
+        mx = y > mx ? y : mx;
+    }
+    if (lane_id() == 0 && mx) atomicMax(max_sub, mx);
 }
 
 __global__ __launch_bounds__(kBlock) void k_max_u64(const uint64_t *x, uint64_t m,
@@ -397,211 +443,6 @@ __global__ __launch_bounds__(kBlock) void k_init_state(ModelArgs m, float v0_lo,
     const float span = __fsub_rn(v0_hi, v0_lo);
     V[i] = __fadd_rn(v0_lo, __fmul_rn(span, u24(key_hash(m.keys.v0, i, 0))));
     ref[i] = 0;
-}
-
-// --------------------------------------------------------------- deliver
-// Spike transmission (Sec. III-C): every synapse of every due (spike,
-// delay-list) piece adds its weight into the input of its target.  Work
-// item = one 64-synapse column block of one piece; items are numbered
-// column-major (item = block * P + piece), so consecutively scheduled waves
-// walk the same column of many sorted rows, the paper's cache-aware order.
-// A wave sets up kIPW items lane-parallel (list search, spike ID, row
-// pointers), then streams them: one coalesced 8-byte load and one atomic
-// per lane and item.
-constexpr int kIPW = 16;
-
-template <bool FIXED>
-__global__ __launch_bounds__(kBlock) void k_deliver(DeliverArgs a)
-{
-    __shared__ uint64_t pre[kMaxLists + 1];
-    __shared__ uint32_t slot_of[kMaxLists];
-    __shared__ unsigned long long blk_ev;
-    const uint32_t tid = threadIdx.x, lane = lane_id(), wv = tid / kWave;
-    const uint32_t nl = a.list_hi - a.list_lo;
-    if (tid < kWave) {
-        uint32_t c = 0, slot = 0;
-        if (lane < nl) {
-            const uint64_t d = (uint64_t)a.net.dmin + a.list_lo + lane;
-            if (a.dbg_spikes) {
-                c = *a.dbg_count;  // the debug list holds exactly this many IDs
-            } else if (a.t >= d) {
-                slot = (uint32_t)((a.t - d) % a.net.ring_slots);
-                c = a.net.ring_count[slot];
-                if (c > a.net.cap) c = a.net.cap;
-            }
-            slot_of[lane] = slot;
-        }
-        uint64_t inc = c;
-        for (int o = 1; o < kWave; o <<= 1) {
-            uint64_t y = __shfl_up(inc, o);
-            if (lane >= (uint32_t)o) inc += y;
-        }
-        if (lane < nl) pre[lane + 1] = inc;
-        if (lane == 0) {
-            pre[0] = 0;
-            blk_ev = 0;
-        }
-    }
-    if (blockIdx.x == 0 && tid == 0 && a.zero_count) *a.zero_count = 0;
-    __syncthreads();
-
-    const uint64_t P = pre[nl];
-    const uint64_t items = P * a.bpp;
-    const uint64_t tasks = (items + kIPW - 1) / kIPW;
-    const uint64_t nwaves = (uint64_t)gridDim.x * (kBlock / kWave);
-    const int2 *__restrict__ syn = a.net.syn;
-    uint64_t my_ev = 0;
-    for (uint64_t task = (uint64_t)blockIdx.x * (kBlock / kWave) + wv; task < tasks; task += nwaves) {
-        uint64_t beg = 0, end = 0;
-        if (lane < (uint32_t)kIPW) {
-            const uint64_t item = task * kIPW + lane;
-            if (item < items) {
-                const uint64_t p = item % P, b = item / P;
-                uint32_t lo = 0, hi = nl - 1;  // largest j with pre[j] <= p
-                while (lo < hi) {
-                    const uint32_t mid = (lo + hi + 1) >> 1;
-                    if (pre[mid] <= p) lo = mid; else hi = mid - 1;
-                }
-                const uint32_t j = lo;
-                const uint32_t *sp = a.dbg_spikes
-                    ? a.dbg_spikes : a.net.ring + (uint64_t)slot_of[j] * a.net.cap;
-                const uint32_t s = sp[p - pre[j]];
-                const uint64_t row = (uint64_t)(a.list_lo + j) * a.net.n + s;
-                const uint64_t rb = a.net.row_ptr[row], re = a.net.row_ptr[row + 1];
-                beg = rb + b * kWave;
-                end = re < beg + kWave ? re : beg + kWave;
-                if (beg > end) beg = end;
-                my_ev += end - beg;
-            }
-        }
-#pragma unroll
-        for (int q0 = 0; q0 < kIPW; q0 += 4) {
-            int2 e[4];
-            bool ok[4];
-#pragma unroll
-            for (int u = 0; u < 4; u++) {
-                const uint64_t qb = __shfl(beg, q0 + u), qe = __shfl(end, q0 + u);
-                const uint64_t idx = qb + lane;
-                ok[u] = idx < qe;
-                if (ok[u]) e[u] = syn[idx];
-            }
-#pragma unroll
-            for (int u = 0; u < 4; u++) {
-                if (!ok[u]) continue;
-                if (FIXED) atomicAdd((int *)a.acc + (uint32_t)e[u].x, e[u].y);
-                else unsafeAtomicAdd((float *)a.acc + (uint32_t)e[u].x, __int_as_float(e[u].y));
-            }
-        }
-    }
-    if (a.delivered) {
-        my_ev = wave_sum_u64(my_ev);
-        if (lane == 0 && my_ev) atomicAdd(&blk_ev, (unsigned long long)my_ev);
-        __syncthreads();
-        if (tid == 0 && blk_ev) atomicAdd((unsigned long long *)a.delivered, blk_ev);
-    }
-}
-
-// ---------------------------------------------------------------- update
-// Neuron update (forward Euler, fp32, each operation rounded separately),
-// then wavefront-ballot compaction of the spiking IDs into the spike list
-// of step t: one atomic per wave reserves its slots.
-template <bool FIXED>
-__global__ __launch_bounds__(kBlock) void k_update(ModelArgs m, NetDev nd, uint64_t t, uint32_t slot)
-{
-    __shared__ uint64_t pois[256];
-    if (m.pois_len) {
-        for (uint32_t k = threadIdx.x; k < m.pois_len; k += kBlock) pois[k] = nd.pois[k];
-        __syncthreads();
-    }
-    const uint32_t i = blockIdx.x * kBlock + threadIdx.x;
-    const uint32_t lane = lane_id();
-    bool spk = false;
-    if (i < m.n) {
-        uint32_t K = 0;
-        if (m.pois_len) {  // K = min { k : hi32 < T_k }
-            const uint64_t x = hash_hi32(key_hash(m.keys.pois, i, t));
-            uint32_t lo = 0, hi = m.pois_len - 1;
-            while (lo < hi) {
-                const uint32_t mid = (lo + hi) >> 1;
-                if (x < pois[mid]) hi = mid; else lo = mid + 1;
-            }
-            K = lo;
-        }
-        float I;
-        if (FIXED) {
-            int32_t *acc = (int32_t *)nd.acc;
-            const int32_t q = acc[i];
-            acc[i] = 0;
-            const int32_t qt = q + (int32_t)K * m.ext_wq + m.bias_q;
-            I = ldexpf((float)qt, -m.shift);
-        } else {
-            float *acc = (float *)nd.acc;
-            const float x = acc[i];
-            acc[i] = 0.0f;
-            const float ext = __fmul_rn((float)K, m.ext_w);
-            I = __fadd_rn(__fadd_rn(x, ext), m.i_bias);
-        }
-        float V = nd.V[i];
-        if (m.kind == SPK_SOURCE) {
-            const float a = __fsub_rn(m.v_rest, V);
-            const float b = __fmul_rn(m.k, a);
-            const float c = __fadd_rn(V, b);
-            V = __fadd_rn(c, I);
-            spk = (uint64_t)hash_hi32(key_hash(m.keys.bern, i, t)) < m.src_thr;
-        } else {
-            uint32_t r = nd.ref[i];
-            if (r > 0) {
-                r -= 1;
-                V = m.v_reset;
-            } else {
-                const float a = __fsub_rn(m.v_rest, V);
-                const float b = __fmul_rn(m.k, a);
-                const float c = __fadd_rn(V, b);
-                V = __fadd_rn(c, I);
-                if (V >= m.v_th) {
-                    spk = true;
-                    V = m.v_reset;
-                    r = m.ref_steps;
-                }
-            }
-            nd.ref[i] = (uint8_t)r;
-        }
-        nd.V[i] = V;
-    }
-    const uint64_t mask = __ballot(spk);
-    if (mask) {
-        const uint32_t c = (uint32_t)__popcll(mask);
-        const int leader = __ffsll((long long)mask) - 1;
-        const uint64_t ev = wave_sum_u64(spk ? (uint64_t)nd.outdeg[i] : 0ull);
-        uint32_t base = 0;
-        if ((int)lane == leader) {
-            base = atomicAdd(&nd.ring_count[slot], c);
-            atomicAdd(&nd.counts[t], c);
-            atomicAdd((unsigned long long *)&nd.events[t], (unsigned long long)ev);
-        }
-        base = __shfl(base, leader);
-        if (spk) {
-            const uint32_t pos = base + mbcnt(mask);
-            if (pos < nd.cap) nd.ring[(uint64_t)slot * nd.cap + pos] = i;
-            else atomicOr(nd.flags, 1u);
-        }
-    }
-}
-
-// Append the spike list of step t to the raster.
-__global__ __launch_bounds__(kBlock) void k_record(NetDev nd, uint64_t t, uint32_t slot)
-{
-    uint32_t c = nd.ring_count[slot];
-    if (c > nd.cap) c = nd.cap;
-    const uint64_t base = nd.raster_offs[t];
-    const bool ok = base + c <= nd.raster_cap;
-    if (ok)
-        for (uint32_t k = threadIdx.x; k < c; k += kBlock)
-            nd.raster[base + k] = nd.ring[(uint64_t)slot * nd.cap + k];
-    if (threadIdx.x == 0) {
-        nd.raster_offs[t + 1] = ok ? base + c : base;
-        if (!ok) atomicOr(nd.flags, 2u);
-    }
 }
 
 // ---------------------------------------------------------------- export
@@ -636,28 +477,6 @@ __global__ __launch_bounds__(kBlock) void k_export_gather(const uint64_t *row_pt
     }
 }
 
-__global__ __launch_bounds__(kBlock) void k_stream_copy(const uint4 *src, uint4 *dst, uint64_t n16)
-{
-    for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < n16;
-         i += (uint64_t)gridDim.x * kBlock)
-        dst[i] = src[i];
-}
-
-int g_cus = 0;
-
-int cu_count()
-{
-    if (!g_cus) {
-        int dev = 0, v = 0;
-        if (hipGetDevice(&dev) == hipSuccess &&
-            hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
-            g_cus = v;
-        else
-            g_cus = 256;
-    }
-    return g_cus;
-}
-
 uint32_t grid_for(uint64_t threads, uint32_t cap = 1u << 20)
 {
     uint64_t g = (threads + kBlock - 1) / kBlock;
@@ -668,6 +487,20 @@ uint32_t grid_for(uint64_t threads, uint32_t cap = 1u << 20)
 }  // namespace
 
 // -------------------------------------------------------- launch wrappers
+
+int cu_count()
+{
+    static int cus = 0;
+    if (!cus) {
+        int dev = 0, v = 0;
+        if (hipGetDevice(&dev) == hipSuccess &&
+            hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0)
+            cus = v;
+        else
+            cus = 256;
+    }
+    return cus;
+}
 
 hipError_t gen_count_rows(const ConnArgs &c, uint32_t *cnt, hipStream_t s)
 {
@@ -760,11 +593,11 @@ hipError_t out_degree(const uint64_t *row_ptr, uint32_t n, uint32_t lists, uint3
     return hipGetLastError();
 }
 
-hipError_t in_abs_sum(const int2 *syn, uint64_t nnz, uint64_t *insum, hipStream_t s)
+hipError_t in_abs_sum(const int2 *syn, uint64_t nnz, bool fixed, uint64_t *insum, hipStream_t s)
 {
     if (!nnz) return hipSuccess;
     hipLaunchKernelGGL(k_in_abs_sum, dim3(grid_for(nnz, 65536)), dim3(kBlock), 0, s, syn, nnz,
-                       (unsigned long long *)insum);
+                       fixed ? 1 : 0, (unsigned long long *)insum);
     return hipGetLastError();
 }
 
@@ -782,32 +615,12 @@ hipError_t init_state(const ModelArgs &m, float v0_lo, float v0_hi, float *V, ui
     return hipGetLastError();
 }
 
-int deliver_grid() { return cu_count() * 8; }
-
-hipError_t deliver(const DeliverArgs &a, int grid, hipStream_t s)
+hipError_t piece_offsets(const uint64_t *row_ptr, const int2 *syn, uint64_t pieces, uint32_t bounds,
+                         uint32_t width, uint16_t *off, uint32_t *max_sub, hipStream_t s)
 {
-    if (a.list_hi <= a.list_lo || a.list_hi - a.list_lo > kMaxLists) return hipErrorInvalidValue;
-    if (a.fixed)
-        hipLaunchKernelGGL(k_deliver<true>, dim3(grid), dim3(kBlock), 0, s, a);
-    else
-        hipLaunchKernelGGL(k_deliver<false>, dim3(grid), dim3(kBlock), 0, s, a);
-    return hipGetLastError();
-}
-
-hipError_t update(const ModelArgs &m, const NetDev &net, uint64_t t, hipStream_t s)
-{
-    if (m.pois_len > 256) return hipErrorInvalidValue;
-    const uint32_t slot = (uint32_t)(t % net.ring_slots);
-    if (m.fixed)
-        hipLaunchKernelGGL(k_update<true>, dim3(grid_for(m.n)), dim3(kBlock), 0, s, m, net, t, slot);
-    else
-        hipLaunchKernelGGL(k_update<false>, dim3(grid_for(m.n)), dim3(kBlock), 0, s, m, net, t, slot);
-    return hipGetLastError();
-}
-
-hipError_t record(const NetDev &net, uint64_t t, hipStream_t s)
-{
-    hipLaunchKernelGGL(k_record, dim3(1), dim3(kBlock), 0, s, net, t, (uint32_t)(t % net.ring_slots));
+    if (!pieces) return hipSuccess;
+    hipLaunchKernelGGL(k_piece_offsets, dim3(grid_for(pieces * bounds, 1u << 22)), dim3(kBlock), 0, s,
+                       row_ptr, syn, pieces, bounds, width, off, max_sub);
     return hipGetLastError();
 }
 
@@ -829,14 +642,6 @@ hipError_t export_gather(const uint64_t *row_ptr, const int2 *syn, uint32_t n, u
     if (pieces > 0x7fffffffull) return hipErrorInvalidValue;
     hipLaunchKernelGGL(k_export_gather, dim3((uint32_t)pieces), dim3(kBlock), 0, s, row_ptr, syn, n,
                        lists, dmin, rows, piece_off, col, wbits, delay);
-    return hipGetLastError();
-}
-
-hipError_t stream_copy(const void *src, void *dst, uint64_t bytes, hipStream_t s)
-{
-    const uint64_t n16 = bytes / 16;
-    hipLaunchKernelGGL(k_stream_copy, dim3(cu_count() * 16), dim3(kBlock), 0, s, (const uint4 *)src,
-                       (uint4 *)dst, n16);
     return hipGetLastError();
 }
 

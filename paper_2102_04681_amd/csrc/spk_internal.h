@@ -12,6 +12,9 @@ namespace spk {
 
 constexpr uint32_t kMaxLists = SPK_MAX_DELAY_LISTS;
 constexpr int kWave = 64;
+constexpr uint32_t kGroups = 8;      // one target group per XCD (blockIdx % 8 == XCD)
+constexpr uint32_t kPad = 16;        // u32 counters padded to 64 B
+constexpr uint32_t kMaxTileW = 8192; // neurons per tile (LDS accumulators + spike list)
 
 // Stream tags of the counter-based hash: one independent stream per kind of
 // random decision (connection, target, source, weight, delay, initial V,
@@ -42,6 +45,12 @@ __host__ __device__ __forceinline__ uint64_t key_hash(uint64_t key, uint64_t a, 
 {
     return mix64(mix64(key ^ a) ^ b);
 }
+// Per-step draws of neuron i at step t (Poisson drive, Bernoulli firing):
+// one round over the stream key and the packed counter t * 2^32 + i.
+__host__ __device__ __forceinline__ uint64_t step_hash(uint64_t key, uint32_t i, uint64_t t)
+{
+    return mix64(key ^ ((t << 32) | (uint64_t)i));
+}
 __host__ __device__ __forceinline__ uint32_t hash_hi32(uint64_t h) { return (uint32_t)(h >> 32); }
 // integer in [0, n): multiply-shift of the high 32 bits (Lemire)
 __host__ __device__ __forceinline__ uint32_t hash_range(uint64_t h, uint32_t n)
@@ -51,6 +60,15 @@ __host__ __device__ __forceinline__ uint32_t hash_range(uint64_t h, uint32_t n)
 
 struct Keys {
     uint64_t conn, tgt, src_e, src_i, w, delay, v0, pois, bern;
+};
+
+// Target tiling.  Tile k covers neurons [k*W, (k+1)*W); group x (one per
+// XCD) covers tiles [x*T8, (x+1)*T8), i.e. neurons [x*Gw, (x+1)*Gw).
+struct Tiling {
+    uint32_t W, logW;   // tile width, a power of two
+    uint32_t T8;        // tiles per group
+    uint32_t T;         // tiles = 8 * T8
+    uint32_t Gw;        // group width = T8 * W
 };
 
 // Connectivity generation parameters.
@@ -68,12 +86,13 @@ struct ConnArgs {
     Keys keys;
 };
 
-// Everything the update kernel needs about the neuron model.
+// Neuron model constants for the update.
 struct ModelArgs {
     uint32_t n;
     uint32_t kind;          // SPK_LIF / SPK_SOURCE
-    uint32_t fixed;
+    uint32_t fixed;         // 1: int32 accumulators in units of 2^-shift
     int32_t shift;
+    int32_t shift64;        // fp32 mode: int64 accumulators in units of 2^-shift64
     float k, v_rest, v_th, v_reset, i_bias, ext_w;
     int32_t ext_wq, bias_q;
     uint32_t ref_steps;
@@ -82,42 +101,44 @@ struct ModelArgs {
     Keys keys;
 };
 
-struct NetDev {
-    uint32_t n, lists, dmin, ring_slots, cap;
-    const uint64_t *row_ptr;   // lists*n + 1: list j, source s -> row_ptr[j*n + s]
-    const int2 *syn;           // {target, weight bits (fp32 or quantised int32)}
-    const uint32_t *outdeg;    // n
-    float *V;                  // n
-    uint8_t *ref;              // n
-    void *acc;                 // n: fp32 or int32 input of the current step
-    uint32_t *ring;            // ring * cap spike IDs
-    uint32_t *ring_count;      // ring
-    uint32_t *counts;          // max_steps
-    uint64_t *events;          // max_steps
-    uint64_t *delivered;       // max_steps
-    const uint64_t *pois;      // pois_len thresholds
-    uint32_t *flags;           // bit 0: spike-list overflow, bit 1: raster overflow
-    uint32_t *raster;          // raster_cap
-    uint64_t *raster_offs;     // max_steps + 1
+// Everything the step kernels touch.
+struct StepArgs {
+    ModelArgs m;
+    Tiling tl;
+    uint32_t n, lists, dmin, ring_slots;
+    uint32_t direct;             // 1: tiles read their sub-pieces (no bins)
+    const uint64_t *row_ptr;     // lists*n + 1: piece (j, s) = [row_ptr[j*n+s], row_ptr[j*n+s+1])
+    const int2 *syn;             // {target, weight bits (fp32 or quantised int32)}
+    const uint16_t *goff;        // 8 per piece: group sub-piece starts (binned mode)
+    const uint16_t *toff;        // T+1 per piece: tile sub-piece starts (direct mode)
+    const uint32_t *outdeg;      // n
+    float *V;                    // n
+    uint8_t *ref;                // n
+    uint32_t *ring;              // ring_slots * 8 * Gw spike IDs, list (slot, group)
+    uint32_t *ring_count;        // ring_slots * 8 counters (padded)
+    uint32_t *counts8;           // max_steps * 8
+    uint64_t *events8;           // max_steps * 8: events emitted per group
+    uint64_t *delivered8;        // max_steps * 8: events delivered per group
+    int2 *bins;                  // T * bin_cap records {local target, weight bits}
+    uint32_t *bin_fill;          // T counters (padded)
+    uint64_t bin_cap;
+    void *acc_ovf;               // n accumulators for bin overflow (int64 or int32)
+    uint32_t *ovf_flag;          // T
+    const uint64_t *pois;        // pois_len thresholds
+    uint32_t *flags;             // bit 0: spike-list overflow, bit 1: raster overflow
+    uint32_t *raster;
+    uint64_t *raster_offs;       // max_steps + 1
     uint64_t raster_cap;
-};
-
-// Delivery work description: spike lists of lists [list_lo, list_hi) due
-// at step t, or a single debug spike list delivered through those lists.
-struct DeliverArgs {
-    NetDev net;
-    uint32_t fixed;
-    uint32_t bpp;              // 64-synapse column blocks per piece
-    uint64_t t;
-    uint32_t list_lo, list_hi;
-    void *acc;                 // accumulation target
-    const uint32_t *dbg_spikes;  // non-null: debug mode
+    const uint64_t *t_base;      // device step counter (steps completed before this batch)
+    // delivery selection
+    uint32_t list_lo, list_hi;   // delay lists delivered
+    const uint32_t *dbg_spikes;  // non-null: deliver this list instead of the ring
     const uint32_t *dbg_count;
-    uint64_t *delivered;       // per-step counter to add to, or null
-    uint32_t *zero_count;      // ring_count slot to clear, or null
+    void *dbg_out;               // debug: per-neuron input (fp32 or int32), no update
+    uint32_t bin_chunk;          // pieces per binning chunk
 };
 
-// kernels.hip -- launch wrappers (return the launch error)
+// spk_gen.hip -- connectivity expansion
 hipError_t gen_count_rows(const ConnArgs &c, uint32_t *cnt, hipStream_t s);
 hipError_t gen_fill_rows(const ConnArgs &c, const uint64_t *row_ptr, int2 *syn, hipStream_t s);
 hipError_t gen_in_count(const ConnArgs &c, uint32_t *cnt, hipStream_t s);
@@ -135,22 +156,30 @@ hipError_t sort_small_pieces(const uint64_t *row_ptr, int2 *syn, uint64_t m, uin
                              uint32_t *n_large, hipStream_t s);
 hipError_t sort_large_pieces(const uint64_t *row_ptr, int2 *syn, const uint32_t *large,
                              uint32_t n_large, uint32_t pow2, hipStream_t s);
+hipError_t piece_offsets(const uint64_t *row_ptr, const int2 *syn, uint64_t pieces, uint32_t bounds,
+                         uint32_t width, uint16_t *off, uint32_t *max_sub, hipStream_t s);
 hipError_t out_degree(const uint64_t *row_ptr, uint32_t n, uint32_t lists, uint32_t *outdeg,
                       hipStream_t s);
-hipError_t in_abs_sum(const int2 *syn, uint64_t nnz, uint64_t *insum, hipStream_t s);
+hipError_t in_abs_sum(const int2 *syn, uint64_t nnz, bool fixed, uint64_t *insum, hipStream_t s);
 hipError_t max_u64(const uint64_t *x, uint64_t m, uint64_t *out, hipStream_t s);
 hipError_t init_state(const ModelArgs &m, float v0_lo, float v0_hi, float *V, uint8_t *ref,
                       hipStream_t s);
-hipError_t deliver(const DeliverArgs &a, int grid, hipStream_t s);
-hipError_t update(const ModelArgs &m, const NetDev &net, uint64_t t, hipStream_t s);
-hipError_t record(const NetDev &net, uint64_t t, hipStream_t s);
 hipError_t export_lens(const uint64_t *row_ptr, uint32_t n, uint32_t lists, const uint32_t *rows,
                        uint64_t n_rows, uint64_t *lens, hipStream_t s);
 hipError_t export_gather(const uint64_t *row_ptr, const int2 *syn, uint32_t n, uint32_t lists,
                          uint32_t dmin, const uint32_t *rows, uint64_t n_rows,
                          const uint64_t *piece_off, uint32_t *col, uint32_t *wbits,
                          uint8_t *delay, hipStream_t s);
+int cu_count();
+
+// spk_step.hip -- one simulation step = [bin] + tile (+ record); i = step
+// index inside the current batch (t = *t_base + i), or explicit t when
+// t_explicit >= 0.
+hipError_t launch_bin(const StepArgs &a, uint32_t i, int64_t t_explicit, hipStream_t s);
+hipError_t launch_tile(const StepArgs &a, uint32_t i, int64_t t_explicit, hipStream_t s);
+hipError_t launch_record(const StepArgs &a, uint32_t i, int64_t t_explicit, hipStream_t s);
+hipError_t launch_advance(uint64_t *t_base, uint32_t steps, hipStream_t s);
 hipError_t stream_copy(const void *src, void *dst, uint64_t bytes, hipStream_t s);
-int deliver_grid();
+uint32_t bin_grid();
 
 }  // namespace spk

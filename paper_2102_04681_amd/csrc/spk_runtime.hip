@@ -2,17 +2,20 @@
 //
 // A network owns its device memory and orders all work on one HIP stream.
 // Creation expands the connectivity parameters on the GPU (paper Sec. III-B:
-// the layout description is expanded on the device), into one adjacency
-// list per distinct delay (Sec. V), each row sorted by target (Sec. III-A).
-// A step enqueues: delivery of the due spikes (Sec. III-C), the neuron
-// update with spike compaction, and optional raster recording.  Spike counts
-// stay on the device, so stepping never waits for the host.
+// the layout description is expanded on the device), into one adjacency list
+// per distinct delay (Sec. V), each row sorted by target (Sec. III-A), and
+// precomputes where every row crosses the target-tile boundaries.  A step is
+// [bin kernel] + tile kernel (+ raster record); batches of steps are captured
+// once into a HIP graph and replayed.  Spike counts stay on the device, so
+// stepping never waits for the host.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
 #include <cmath>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
+#include <map>
 #include <string>
 #include <vector>
 
@@ -44,8 +47,11 @@ spk_status fail(spk_status st, const std::string &msg)
         if (s_ != SPK_OK) return s_;    \
     } while (0)
 
-constexpr uint32_t kMaxPiece = 16384;    // longest (source, delay) run the sorter accepts
+constexpr uint32_t kMaxPiece = 16384;  // longest (source, delay) run the sorter accepts
 constexpr uint32_t kPoisCap = 256;
+constexpr uint32_t kBatch = 32;        // steps per captured graph
+constexpr uint32_t kChunkEvents = 4096;
+constexpr uint64_t kBinBudget = 96ull << 20;  // bin records across all tiles
 
 uint64_t prob_threshold(double p)
 {
@@ -82,42 +88,74 @@ bool quantise(float w, int S, int32_t *out)
     return true;
 }
 
+// Tiles of W neurons (a power of two, at most kMaxTileW), 8 groups of T8
+// tiles; the smallest W that keeps T8 <= max_t8 (default 32: one tile per
+// compute unit).  SPK_TILES_PER_XCD overrides max_t8 (a tuning knob).
+Tiling make_tiling(uint32_t n)
+{
+    uint32_t max_t8 = 32;
+    if (const char *e = std::getenv("SPK_TILES_PER_XCD")) {
+        const long v = std::strtol(e, nullptr, 10);
+        if (v >= 1 && v <= 256) max_t8 = (uint32_t)v;
+    }
+    Tiling tl{};
+    uint32_t W = 64, logW = 6;
+    while (W < kMaxTileW && (n + 8ull * W - 1) / (8ull * W) > max_t8) {
+        W <<= 1;
+        logW++;
+    }
+    tl.W = W;
+    tl.logW = logW;
+    tl.T8 = (uint32_t)((n + 8ull * W - 1) / (8ull * W));
+    tl.T = kGroups * tl.T8;
+    tl.Gw = tl.T8 * W;
+    return tl;
+}
+
 }  // namespace
 
 struct spk_net {
     spk_params P{};
     // derived constants
-    uint32_t n = 0, n_exc = 0, lists = 1, dmin = 1, ring = 2, ref_steps = 0;
-    uint32_t pois_len = 0, max_piece = 0, bpp = 1;
+    uint32_t n = 0, n_exc = 0, lists = 1, dmin = 1, ring = 3, ref_steps = 0;
+    uint32_t pois_len = 0, max_piece = 0;
     float k = 0.f;
     uint64_t conn_thr = 0, src_thr = 0, nnz = 0;
-    int32_t ext_wq = 0, bias_q = 0;
+    int32_t ext_wq = 0, bias_q = 0, shift64 = 0;
     Keys keys{};
     std::vector<uint64_t> pois;
+    Tiling tl{};
+    bool direct = false;
+    uint32_t bin_chunk = 1;
+    uint64_t bin_cap = 0;
     // device
-    hipStream_t stream = nullptr;
+    hipStream_t stream = nullptr, cap_stream = nullptr;
     bool own_stream = false;
     int device = 0;
     uint64_t *row_ptr = nullptr;
     int2 *syn = nullptr;
+    uint16_t *goff = nullptr, *toff = nullptr;
     uint32_t *outdeg = nullptr;
     float *V = nullptr;
     uint8_t *ref = nullptr;
-    void *acc = nullptr;
-    void *dbg_acc = nullptr;
-    uint32_t *ring_buf = nullptr, *ring_count = nullptr, *counts = nullptr, *flags = nullptr;
-    uint64_t *events = nullptr, *delivered = nullptr, *pois_dev = nullptr;
+    uint32_t *ring_buf = nullptr, *ring_count = nullptr, *counts8 = nullptr, *flags = nullptr;
+    uint64_t *events8 = nullptr, *delivered8 = nullptr, *pois_dev = nullptr, *t_base = nullptr;
+    int2 *bins = nullptr;
+    uint32_t *bin_fill = nullptr, *ovf_flag = nullptr;
+    void *acc_ovf = nullptr;
     uint32_t *raster = nullptr;
     uint64_t *raster_offs = nullptr;
     uint32_t *dbg_count = nullptr;
+    void *dbg_out = nullptr;
     uint64_t t = 0;
     uint64_t device_bytes = 0;
     std::vector<void *> allocs;
+    std::map<uint32_t, hipGraphExec_t> graphs;
     // profiling
     bool profiling = false;
     std::vector<hipEvent_t> ev_free;
-    std::vector<std::pair<hipEvent_t, hipEvent_t>> ev_deliver, ev_update;
-    double ms_deliver = 0, ms_update = 0;
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> ev_bin, ev_tile;
+    double ms_bin = 0, ms_tile = 0;
     uint64_t launches = 0;
 };
 
@@ -154,6 +192,7 @@ ModelArgs model_args(const spk_net *net)
     m.kind = net->P.neuron_kind;
     m.fixed = net->P.acc_mode == SPK_ACC_FIXED;
     m.shift = net->P.fixed_shift;
+    m.shift64 = net->shift64;
     m.k = net->k;
     m.v_rest = net->P.v_rest;
     m.v_th = net->P.v_th;
@@ -169,31 +208,43 @@ ModelArgs model_args(const spk_net *net)
     return m;
 }
 
-NetDev net_dev(const spk_net *net)
+StepArgs step_args(const spk_net *net)
 {
-    NetDev d{};
-    d.n = net->n;
-    d.lists = net->lists;
-    d.dmin = net->dmin;
-    d.ring_slots = net->ring;
-    d.cap = net->n;
-    d.row_ptr = net->row_ptr;
-    d.syn = net->syn;
-    d.outdeg = net->outdeg;
-    d.V = net->V;
-    d.ref = net->ref;
-    d.acc = net->acc;
-    d.ring = net->ring_buf;
-    d.ring_count = net->ring_count;
-    d.counts = net->counts;
-    d.events = net->events;
-    d.delivered = net->delivered;
-    d.pois = net->pois_dev;
-    d.flags = net->flags;
-    d.raster = net->raster;
-    d.raster_offs = net->raster_offs;
-    d.raster_cap = net->P.raster_capacity;
-    return d;
+    StepArgs a{};
+    a.m = model_args(net);
+    a.tl = net->tl;
+    a.n = net->n;
+    a.lists = net->lists;
+    a.dmin = net->dmin;
+    a.ring_slots = net->ring;
+    a.direct = net->direct ? 1u : 0u;
+    a.row_ptr = net->row_ptr;
+    a.syn = net->syn;
+    a.goff = net->goff;
+    a.toff = net->toff;
+    a.outdeg = net->outdeg;
+    a.V = net->V;
+    a.ref = net->ref;
+    a.ring = net->ring_buf;
+    a.ring_count = net->ring_count;
+    a.counts8 = net->counts8;
+    a.events8 = net->events8;
+    a.delivered8 = net->delivered8;
+    a.bins = net->bins;
+    a.bin_fill = net->bin_fill;
+    a.bin_cap = net->bin_cap;
+    a.acc_ovf = net->acc_ovf;
+    a.ovf_flag = net->ovf_flag;
+    a.pois = net->pois_dev;
+    a.flags = net->flags;
+    a.raster = net->raster;
+    a.raster_offs = net->raster_offs;
+    a.raster_cap = net->P.raster_capacity;
+    a.t_base = net->t_base;
+    a.list_lo = 0;
+    a.list_hi = net->lists;
+    a.bin_chunk = net->bin_chunk;
+    return a;
 }
 
 ConnArgs conn_args(const spk_net *net)
@@ -227,13 +278,14 @@ spk_status derive(spk_net *net, bool explicit_csr)
     if (P.n == 0 || P.n > 2000000000u) return fail(SPK_EINVAL, "n must be in [1, 2e9]");
     if (!(P.dt_ms > 0.0) || !(P.tau_m_ms > 0.0) || !(P.t_ref_ms >= 0.0))
         return fail(SPK_EINVAL, "dt_ms, tau_m_ms must be > 0 and t_ref_ms >= 0");
-    if (P.delay_min < 1 || P.delay_max < P.delay_min || P.delay_max > 255)
-        return fail(SPK_EINVAL, "delays must satisfy 1 <= delay_min <= delay_max <= 255");
+    if (P.delay_min < 1 || P.delay_max < P.delay_min || P.delay_max > 253)
+        return fail(SPK_EINVAL, "delays must satisfy 1 <= delay_min <= delay_max <= 253");
     if (P.delay_max - P.delay_min + 1 > kMaxLists)
         return fail(SPK_EINVAL, "at most 64 distinct delays");
     if (!(P.frac_exc >= 0.0 && P.frac_exc <= 1.0)) return fail(SPK_EINVAL, "frac_exc in [0,1]");
     if (P.neuron_kind > SPK_SOURCE) return fail(SPK_EINVAL, "neuron_kind");
     if (P.acc_mode > SPK_ACC_FIXED) return fail(SPK_EINVAL, "acc_mode");
+    if (P.delivery > SPK_DELIVERY_BINNED) return fail(SPK_EINVAL, "delivery");
     if (!explicit_csr && P.conn_kind > SPK_CONN_FIXED_IN) return fail(SPK_EINVAL, "conn_kind");
     if (!(P.p >= 0.0 && P.p <= 1.0)) return fail(SPK_EINVAL, "p in [0,1]");
     if (P.max_steps == 0) return fail(SPK_EINVAL, "max_steps must be >= 1");
@@ -246,9 +298,12 @@ spk_status derive(spk_net *net, bool explicit_csr)
     net->ref_steps = (uint32_t)rs;
     net->dmin = P.delay_min;
     net->lists = P.delay_max - P.delay_min + 1;
-    net->ring = P.delay_max + 1;
+    // dmax + 2 slots: the slot written at step t is neither read at t nor
+    // at t - 1, so it can be cleared one step ahead
+    net->ring = P.delay_max + 2;
     net->conn_thr = prob_threshold(P.p);
     net->src_thr = prob_threshold(P.src_rate_hz * P.dt_ms * 1e-3);
+    net->tl = make_tiling(P.n);
     if (!explicit_csr && P.conn_kind == SPK_CONN_FIXED_IN &&
         ((P.k_in_exc > 0 && net->n_exc == 0) || (P.k_in_inh > 0 && net->n_exc == P.n)))
         return fail(SPK_EINVAL, "fixed in-degree needs a non-empty source population");
@@ -288,41 +343,7 @@ spk_status setup_stream(spk_net *net, void *stream)
         SPK_HIP(hipStreamCreateWithFlags(&net->stream, hipStreamNonBlocking));
         net->own_stream = true;
     }
-    return SPK_OK;
-}
-
-// State, spike ring and per-step records.
-spk_status alloc_state(spk_net *net)
-{
-    const uint32_t n = net->n;
-    const uint64_t T = net->P.max_steps;
-    hipStream_t s = net->stream;
-    SPK_TRY(dalloc(net, &net->V, n));
-    SPK_TRY(dalloc(net, &net->ref, n));
-    SPK_TRY(dalloc(net, (uint32_t **)&net->acc, n));
-    SPK_TRY(dalloc(net, (uint32_t **)&net->dbg_acc, n));
-    SPK_TRY(dalloc(net, &net->ring_buf, (size_t)net->ring * n));
-    SPK_TRY(dalloc(net, &net->ring_count, net->ring));
-    SPK_TRY(dalloc(net, &net->counts, T));
-    SPK_TRY(dalloc(net, &net->events, T));
-    SPK_TRY(dalloc(net, &net->delivered, T));
-    SPK_TRY(dalloc(net, &net->flags, 1));
-    SPK_TRY(dalloc(net, &net->dbg_count, 1));
-    SPK_TRY(dalloc(net, &net->raster_offs, T + 1));
-    SPK_TRY(dalloc(net, &net->raster, net->P.raster_capacity));
-    SPK_TRY(dalloc(net, &net->pois_dev, net->pois_len ? net->pois_len : 1));
-    SPK_HIP(hipMemsetAsync(net->acc, 0, (size_t)n * 4, s));
-    SPK_HIP(hipMemsetAsync(net->ring_count, 0, (size_t)net->ring * 4, s));
-    SPK_HIP(hipMemsetAsync(net->counts, 0, T * 4, s));
-    SPK_HIP(hipMemsetAsync(net->events, 0, T * 8, s));
-    SPK_HIP(hipMemsetAsync(net->delivered, 0, T * 8, s));
-    SPK_HIP(hipMemsetAsync(net->flags, 0, 4, s));
-    SPK_HIP(hipMemsetAsync(net->raster_offs, 0, (T + 1) * 8, s));
-    if (net->pois_len)
-        SPK_HIP(hipMemcpyAsync(net->pois_dev, net->pois.data(), net->pois_len * 8,
-                               hipMemcpyHostToDevice, s));
-    ModelArgs m = model_args(net);
-    SPK_HIP(init_state(m, net->P.v0_lo, net->P.v0_hi, net->V, net->ref, s));
+    SPK_HIP(hipStreamCreateWithFlags(&net->cap_stream, hipStreamNonBlocking));
     return SPK_OK;
 }
 
@@ -346,7 +367,6 @@ spk_status finish_counts(spk_net *net, uint32_t *cnt, uint64_t pieces)
     dfree(net, maxp);
     net->nnz = nnz;
     net->max_piece = mp;
-    net->bpp = std::max<uint32_t>(1, (mp + kWave - 1) / kWave);
     if (mp > kMaxPiece)
         return fail(SPK_EINVAL, "a (source, delay) synapse run of " + std::to_string(mp) +
                                     " exceeds the supported " + std::to_string(kMaxPiece));
@@ -354,14 +374,14 @@ spk_status finish_counts(spk_net *net, uint32_t *cnt, uint64_t pieces)
     return SPK_OK;
 }
 
-// Sort every piece by (target, weight bits); out-degrees; fixed-point guard.
+// Sort every piece by (target, weight bits); tile/group offsets; out-degrees;
+// accumulator ranges; delivery strategy and its buffers.
 spk_status finish_pieces(spk_net *net, uint64_t pieces)
 {
     hipStream_t s = net->stream;
     uint32_t *large = nullptr, *n_large = nullptr;
     SPK_TRY(dalloc(net, &n_large, 1));
     SPK_HIP(hipMemsetAsync(n_large, 0, 4, s));
-    // pieces longer than the small-sort limit: at most nnz / 257 of them
     const uint64_t max_large = std::min<uint64_t>(pieces, net->nnz / 257 + 1);
     SPK_TRY(dalloc(net, &large, max_large));
     SPK_HIP(sort_small_pieces(net->row_ptr, net->syn, pieces, large, n_large, s));
@@ -377,26 +397,69 @@ spk_status finish_pieces(spk_net *net, uint64_t pieces)
     dfree(net, n_large);
     SPK_TRY(dalloc(net, &net->outdeg, net->n));
     SPK_HIP(out_degree(net->row_ptr, net->n, net->lists, net->outdeg, s));
-    if (net->P.acc_mode == SPK_ACC_FIXED) {
-        // Guard: all in-synapses of one neuron at once, plus the largest
-        // Poisson count and the bias, must fit in int32.
-        uint64_t *insum = nullptr, *mx = nullptr;
-        SPK_TRY(dalloc(net, &insum, net->n));
-        SPK_TRY(dalloc(net, &mx, 1));
-        SPK_HIP(hipMemsetAsync(insum, 0, (size_t)net->n * 8, s));
-        SPK_HIP(hipMemsetAsync(mx, 0, 8, s));
-        SPK_HIP(in_abs_sum(net->syn, net->nnz, insum, s));
-        SPK_HIP(max_u64(insum, net->n, mx, s));
-        uint64_t m = 0;
-        SPK_HIP(hipMemcpyAsync(&m, mx, 8, hipMemcpyDeviceToHost, s));
-        SPK_HIP(hipStreamSynchronize(s));
-        dfree(net, insum);
-        dfree(net, mx);
+
+    // Delivery strategy: tiles read their own runs when rows are long
+    // compared with the tile count (and the offsets stay small), otherwise
+    // the due events are binned per tile first.
+    const Tiling &tl = net->tl;
+    const double mean_piece = pieces ? (double)net->nnz / (double)pieces : 0.0;
+    const double toff_bytes = (double)pieces * (tl.T + 1) * 2.0;
+    bool direct = mean_piece >= 2.0 * tl.T && toff_bytes <= 0.5 * 8.0 * (double)net->nnz;
+    if (net->P.delivery == SPK_DELIVERY_DIRECT) direct = true;
+    if (net->P.delivery == SPK_DELIVERY_BINNED) direct = false;
+    net->direct = direct;
+    uint32_t *maxs = nullptr;
+    SPK_TRY(dalloc(net, &maxs, 1));
+    SPK_HIP(hipMemsetAsync(maxs, 0, 4, s));
+    if (direct) {
+        SPK_TRY(dalloc(net, &net->toff, pieces * (tl.T + 1)));
+        SPK_HIP(piece_offsets(net->row_ptr, net->syn, pieces, tl.T + 1, tl.W, net->toff, maxs, s));
+    } else {
+        SPK_TRY(dalloc(net, &net->goff, pieces * kGroups));
+        SPK_HIP(piece_offsets(net->row_ptr, net->syn, pieces, kGroups, tl.Gw, net->goff, maxs, s));
+        // binning chunk: enough pieces for ~kChunkEvents events of one group
+        const double mean_sub = std::max(1.0, mean_piece / kGroups);
+        net->bin_chunk = (uint32_t)std::min(512.0, std::max(1.0, std::floor(kChunkEvents / mean_sub)));
+        net->bin_cap = std::max<uint64_t>(4096, std::min<uint64_t>(net->nnz, kBinBudget) / tl.T + 1);
+        SPK_TRY(dalloc(net, &net->bins, tl.T * net->bin_cap));
+        SPK_TRY(dalloc(net, &net->bin_fill, (size_t)tl.T * kPad));
+        SPK_TRY(dalloc(net, &net->ovf_flag, tl.T));
+        SPK_TRY(dalloc(net, (uint64_t **)&net->acc_ovf, (size_t)tl.T * tl.W));
+        SPK_HIP(hipMemsetAsync(net->bin_fill, 0, (size_t)tl.T * kPad * 4, s));
+        SPK_HIP(hipMemsetAsync(net->ovf_flag, 0, (size_t)tl.T * 4, s));
+        SPK_HIP(hipMemsetAsync(net->acc_ovf, 0, (size_t)tl.T * tl.W * 8, s));
+    }
+    SPK_HIP(hipStreamSynchronize(s));
+    dfree(net, maxs);
+
+    // Accumulator range.  Fixed mode: all in-synapses of one neuron at once,
+    // plus the largest Poisson count and the bias, must fit in int32.  fp32
+    // mode: choose the 64-bit fixed-point unit 2^-S64 as fine as the largest
+    // possible sum allows.
+    const bool fixed = net->P.acc_mode == SPK_ACC_FIXED;
+    uint64_t *insum = nullptr, *mx = nullptr;
+    SPK_TRY(dalloc(net, &insum, net->n));
+    SPK_TRY(dalloc(net, &mx, 1));
+    SPK_HIP(hipMemsetAsync(insum, 0, (size_t)net->n * 8, s));
+    SPK_HIP(hipMemsetAsync(mx, 0, 8, s));
+    SPK_HIP(in_abs_sum(net->syn, net->nnz, fixed, insum, s));
+    SPK_HIP(max_u64(insum, net->n, mx, s));
+    uint64_t m = 0;
+    SPK_HIP(hipMemcpyAsync(&m, mx, 8, hipMemcpyDeviceToHost, s));
+    SPK_HIP(hipStreamSynchronize(s));
+    dfree(net, insum);
+    dfree(net, mx);
+    if (fixed) {
         const uint64_t kmax = net->pois_len ? net->pois_len - 1 : 0;
         const uint64_t extra = kmax * (uint64_t)std::llabs((long long)net->ext_wq) +
                                (uint64_t)std::llabs((long long)net->bias_q);
         if (m + extra > 2147483647ull)
             return fail(SPK_EOVERFLOW, "fixed-point inputs could exceed int32; lower fixed_shift");
+    } else {
+        // every reachable |sum| stays below 2^52 (M <= 2^e): exact in double
+        const double M = std::ldexp((double)m, -24);
+        const int e = M > 0.0 ? (int)std::ceil(std::log2(M)) : 0;
+        net->shift64 = std::max(0, std::min(100, 52 - e));
     }
     return SPK_OK;
 }
@@ -424,6 +487,42 @@ spk_status generate(spk_net *net)
     return finish_pieces(net, pieces);
 }
 
+// State, spike ring and per-step records.
+spk_status alloc_state(spk_net *net)
+{
+    const uint32_t n = net->n;
+    const uint64_t T = net->P.max_steps;
+    hipStream_t s = net->stream;
+    const uint64_t ring_ids = (uint64_t)net->ring * kGroups * net->tl.Gw;
+    SPK_TRY(dalloc(net, &net->V, n));
+    SPK_TRY(dalloc(net, &net->ref, n));
+    SPK_TRY(dalloc(net, &net->ring_buf, ring_ids));
+    SPK_TRY(dalloc(net, &net->ring_count, (size_t)net->ring * kGroups * kPad));
+    SPK_TRY(dalloc(net, &net->counts8, T * kGroups));
+    SPK_TRY(dalloc(net, &net->events8, T * kGroups));
+    SPK_TRY(dalloc(net, &net->delivered8, T * kGroups));
+    SPK_TRY(dalloc(net, &net->flags, 1));
+    SPK_TRY(dalloc(net, &net->dbg_count, 1));
+    SPK_TRY(dalloc(net, (uint32_t **)&net->dbg_out, n));
+    SPK_TRY(dalloc(net, &net->t_base, 1));
+    SPK_TRY(dalloc(net, &net->raster_offs, T + 1));
+    SPK_TRY(dalloc(net, &net->raster, net->P.raster_capacity));
+    SPK_TRY(dalloc(net, &net->pois_dev, net->pois_len ? net->pois_len : 1));
+    SPK_HIP(hipMemsetAsync(net->ring_count, 0, (size_t)net->ring * kGroups * kPad * 4, s));
+    SPK_HIP(hipMemsetAsync(net->counts8, 0, T * kGroups * 4, s));
+    SPK_HIP(hipMemsetAsync(net->events8, 0, T * kGroups * 8, s));
+    SPK_HIP(hipMemsetAsync(net->delivered8, 0, T * kGroups * 8, s));
+    SPK_HIP(hipMemsetAsync(net->flags, 0, 4, s));
+    SPK_HIP(hipMemsetAsync(net->t_base, 0, 8, s));
+    SPK_HIP(hipMemsetAsync(net->raster_offs, 0, (T + 1) * 8, s));
+    if (net->pois_len)
+        SPK_HIP(hipMemcpyAsync(net->pois_dev, net->pois.data(), net->pois_len * 8,
+                               hipMemcpyHostToDevice, s));
+    ModelArgs m = model_args(net);
+    SPK_HIP(init_state(m, net->P.v0_lo, net->P.v0_hi, net->V, net->ref, s));
+    return SPK_OK;
+}
+
 spk_status check_ready(spk_net *net)
 {
     if (!net) return fail(SPK_EINVAL, "null network");
@@ -443,16 +542,17 @@ spk_status sync_flags(spk_net *net, uint32_t *flags_out)
 spk_status collect_profile(spk_net *net)
 {
     SPK_HIP(hipStreamSynchronize(net->stream));
-    for (auto *v : {&net->ev_deliver, &net->ev_update}) {
-        double &acc = v == &net->ev_deliver ? net->ms_deliver : net->ms_update;
-        for (auto &pr : *v) {
+    for (int which = 0; which < 2; which++) {
+        auto &v = which ? net->ev_tile : net->ev_bin;
+        double &acc = which ? net->ms_tile : net->ms_bin;
+        for (auto &pr : v) {
             float ms = 0;
             SPK_HIP(hipEventElapsedTime(&ms, pr.first, pr.second));
             acc += ms;
             net->ev_free.push_back(pr.first);
             net->ev_free.push_back(pr.second);
         }
-        v->clear();
+        v.clear();
     }
     return SPK_OK;
 }
@@ -468,16 +568,85 @@ spk_status get_event(spk_net *net, hipEvent_t *e)
     return SPK_OK;
 }
 
+// One step's kernels on stream s (step i of a batch, or explicit t).
+spk_status enqueue_step(spk_net *net, const StepArgs &a, hipStream_t s, uint32_t i, int64_t t_explicit)
+{
+    if (!net->direct) SPK_HIP(launch_bin(a, i, t_explicit, s));
+    SPK_HIP(launch_tile(a, i, t_explicit, s));
+    if (net->P.raster_capacity) SPK_HIP(launch_record(a, i, t_explicit, s));
+    return SPK_OK;
+}
+
+// A graph of B steps followed by the step-counter advance, built once.
+spk_status batch_graph(spk_net *net, uint32_t B, hipGraphExec_t *out)
+{
+    auto it = net->graphs.find(B);
+    if (it != net->graphs.end()) {
+        *out = it->second;
+        return SPK_OK;
+    }
+    const StepArgs a = step_args(net);
+    hipStream_t cs = net->cap_stream;
+    SPK_HIP(hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal));
+    spk_status st = SPK_OK;
+    for (uint32_t i = 0; i < B && st == SPK_OK; i++) st = enqueue_step(net, a, cs, i, -1);
+    if (st == SPK_OK && launch_advance(net->t_base, B, cs) != hipSuccess)
+        st = fail(SPK_EHIP, "advance launch");
+    hipGraph_t g = nullptr;
+    hipError_t e = hipStreamEndCapture(cs, &g);
+    if (st != SPK_OK) {
+        if (g) (void)hipGraphDestroy(g);
+        return st;
+    }
+    SPK_HIP(e);
+    hipGraphExec_t ge = nullptr;
+    e = hipGraphInstantiate(&ge, g, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(g);
+    SPK_HIP(e);
+    net->graphs[B] = ge;
+    *out = ge;
+    return SPK_OK;
+}
+
 void destroy_net(spk_net *net)
 {
     if (!net) return;
     if (net->stream) (void)hipStreamSynchronize(net->stream);
-    for (auto &pr : net->ev_deliver) { (void)hipEventDestroy(pr.first); (void)hipEventDestroy(pr.second); }
-    for (auto &pr : net->ev_update) { (void)hipEventDestroy(pr.first); (void)hipEventDestroy(pr.second); }
+    for (auto &kv : net->graphs) (void)hipGraphExecDestroy(kv.second);
+    for (auto *v : {&net->ev_bin, &net->ev_tile})
+        for (auto &pr : *v) {
+            (void)hipEventDestroy(pr.first);
+            (void)hipEventDestroy(pr.second);
+        }
     for (auto e : net->ev_free) (void)hipEventDestroy(e);
     for (void *p : net->allocs) (void)hipFree(p);
+    if (net->cap_stream) (void)hipStreamDestroy(net->cap_stream);
     if (net->own_stream && net->stream) (void)hipStreamDestroy(net->stream);
     delete net;
+}
+
+spk_status read_groups(spk_net *net, const void *dev, size_t elem, uint64_t t0, uint64_t n, void *out)
+{
+    std::vector<uint8_t> buf(n * kGroups * elem);
+    if (n) SPK_HIP(hipMemcpy(buf.data(), (const uint8_t *)dev + t0 * kGroups * elem, buf.size(),
+                             hipMemcpyDeviceToHost));
+    for (uint64_t k = 0; k < n; k++) {
+        uint64_t sum = 0;
+        for (uint32_t x = 0; x < kGroups; x++) {
+            if (elem == 4) {
+                uint32_t v;
+                std::memcpy(&v, &buf[(k * kGroups + x) * 4], 4);
+                sum += v;
+            } else {
+                uint64_t v;
+                std::memcpy(&v, &buf[(k * kGroups + x) * 8], 8);
+                sum += v;
+            }
+        }
+        if (elem == 4) ((uint32_t *)out)[k] = (uint32_t)sum;
+        else ((uint64_t *)out)[k] = sum;
+    }
+    return SPK_OK;
 }
 
 }  // namespace
@@ -653,43 +822,43 @@ spk_status spk_step(spk_net *net, uint64_t n_steps)
     if (net->t + n_steps > net->P.max_steps)
         return fail(SPK_EOVERFLOW, "max_steps exceeded");
     hipStream_t s = net->stream;
-    const ModelArgs m = model_args(net);
-    const NetDev nd = net_dev(net);
-    const int grid = deliver_grid();
-    for (uint64_t k = 0; k < n_steps; k++) {
-        const uint64_t t = net->t;
-        DeliverArgs a{};
-        a.net = nd;
-        a.fixed = m.fixed;
-        a.bpp = net->bpp;
-        a.t = t;
-        a.list_lo = 0;
-        a.list_hi = net->lists;
-        a.acc = net->acc;
-        a.delivered = net->delivered + t;
-        a.zero_count = net->ring_count + (t % net->ring);
-        hipEvent_t e0 = nullptr, e1 = nullptr, e2 = nullptr, e3 = nullptr;
-        if (net->profiling) {
+    if (net->profiling) {  // plain launches with events around every kernel
+        const StepArgs a = step_args(net);
+        for (uint64_t k = 0; k < n_steps; k++) {
+            const int64_t t = (int64_t)(net->t + k);
+            hipEvent_t e0 = nullptr, e1 = nullptr, e2 = nullptr, e3 = nullptr;
             SPK_TRY(get_event(net, &e0));
             SPK_TRY(get_event(net, &e1));
             SPK_TRY(get_event(net, &e2));
             SPK_TRY(get_event(net, &e3));
-            SPK_HIP(hipEventRecord(e0, s));
-        }
-        SPK_HIP(deliver(a, grid, s));
-        if (net->profiling) {
-            SPK_HIP(hipEventRecord(e1, s));
+            if (!net->direct) {
+                SPK_HIP(hipEventRecord(e0, s));
+                SPK_HIP(launch_bin(a, 0, t, s));
+                SPK_HIP(hipEventRecord(e1, s));
+                net->ev_bin.push_back({e0, e1});
+            } else {
+                net->ev_free.push_back(e0);
+                net->ev_free.push_back(e1);
+            }
             SPK_HIP(hipEventRecord(e2, s));
-        }
-        SPK_HIP(update(m, nd, t, s));
-        if (net->profiling) {
+            SPK_HIP(launch_tile(a, 0, t, s));
             SPK_HIP(hipEventRecord(e3, s));
-            net->ev_deliver.push_back({e0, e1});
-            net->ev_update.push_back({e2, e3});
+            net->ev_tile.push_back({e2, e3});
+            if (net->P.raster_capacity) SPK_HIP(launch_record(a, 0, t, s));
             net->launches++;
         }
-        if (net->P.raster_capacity) SPK_HIP(record(nd, t, s));
-        net->t = t + 1;
+        if (n_steps) SPK_HIP(launch_advance(net->t_base, (uint32_t)n_steps, s));
+        net->t += n_steps;
+        return SPK_OK;
+    }
+    uint64_t left = n_steps;
+    while (left) {
+        const uint32_t B = (uint32_t)std::min<uint64_t>(left, kBatch);
+        hipGraphExec_t ge = nullptr;
+        SPK_TRY(batch_graph(net, B, &ge));
+        SPK_HIP(hipGraphLaunch(ge, s));
+        left -= B;
+        net->t += B;
     }
     return SPK_OK;
 }
@@ -705,8 +874,7 @@ spk_status spk_read_spike_counts(spk_net *net, uint64_t t0, uint64_t n, uint32_t
     SPK_TRY(check_ready(net));
     if (t0 + n > net->P.max_steps || (n && !out)) return fail(SPK_EINVAL, "range");
     SPK_TRY(sync_flags(net, nullptr));
-    if (n) SPK_HIP(hipMemcpy(out, net->counts + t0, n * 4, hipMemcpyDeviceToHost));
-    return SPK_OK;
+    return read_groups(net, net->counts8, 4, t0, n, out);
 }
 
 spk_status spk_read_events(spk_net *net, uint64_t t0, uint64_t n, uint64_t *out)
@@ -714,8 +882,7 @@ spk_status spk_read_events(spk_net *net, uint64_t t0, uint64_t n, uint64_t *out)
     SPK_TRY(check_ready(net));
     if (t0 + n > net->P.max_steps || (n && !out)) return fail(SPK_EINVAL, "range");
     SPK_TRY(sync_flags(net, nullptr));
-    if (n) SPK_HIP(hipMemcpy(out, net->events + t0, n * 8, hipMemcpyDeviceToHost));
-    return SPK_OK;
+    return read_groups(net, net->events8, 8, t0, n, out);
 }
 
 spk_status spk_read_delivered(spk_net *net, uint64_t t0, uint64_t n, uint64_t *out)
@@ -723,8 +890,7 @@ spk_status spk_read_delivered(spk_net *net, uint64_t t0, uint64_t n, uint64_t *o
     SPK_TRY(check_ready(net));
     if (t0 + n > net->P.max_steps || (n && !out)) return fail(SPK_EINVAL, "range");
     SPK_TRY(sync_flags(net, nullptr));
-    if (n) SPK_HIP(hipMemcpy(out, net->delivered + t0, n * 8, hipMemcpyDeviceToHost));
-    return SPK_OK;
+    return read_groups(net, net->delivered8, 8, t0, n, out);
 }
 
 spk_status spk_read_raster(spk_net *net, uint64_t t0, uint64_t n, uint64_t *offs, uint32_t *ids,
@@ -762,11 +928,13 @@ spk_status spk_debug_deliver(spk_net *net, const uint32_t *spikes, uint64_t n_sp
     const bool fixed = net->P.acc_mode == SPK_ACC_FIXED;
     if ((fixed && !out_i32) || (!fixed && !out_f32))
         return fail(SPK_EINVAL, "output buffer for this accumulation mode is required");
-    if (n_spikes > 0xffffffffull || (n_spikes && !spikes)) return fail(SPK_EINVAL, "spikes");
+    if (n_spikes > 0x3fffffffull || (n_spikes && !spikes)) return fail(SPK_EINVAL, "spikes");
     for (uint64_t k = 0; k < n_spikes; k++)
         if (spikes[k] >= net->n) return fail(SPK_EINVAL, "spike id out of range");
     if (delay && (delay < net->dmin || delay >= net->dmin + net->lists))
         return fail(SPK_EINVAL, "delay not in [delay_min, delay_max]");
+    const uint32_t nl = delay ? 1u : net->lists;
+    if ((uint64_t)n_spikes * nl > 0xffffffffull) return fail(SPK_EINVAL, "too many spikes");
     hipStream_t s = net->stream;
     SPK_TRY(sync_flags(net, nullptr));
     uint32_t *d_sp = nullptr;
@@ -777,22 +945,18 @@ spk_status spk_debug_deliver(spk_net *net, const uint32_t *spikes, uint64_t n_sp
         hipError_t e = hipSuccess;
         if (n_spikes) e = hipMemcpyAsync(d_sp, spikes, n_spikes * 4, hipMemcpyHostToDevice, s);
         if (e == hipSuccess) e = hipMemcpyAsync(net->dbg_count, &cnt, 4, hipMemcpyHostToDevice, s);
-        if (e == hipSuccess) e = hipMemsetAsync(net->dbg_acc, 0, (size_t)net->n * 4, s);
         if (e != hipSuccess) { st = fail(SPK_EHIP, hipGetErrorString(e)); break; }
-        DeliverArgs a{};
-        a.net = net_dev(net);
-        a.fixed = fixed;
-        a.bpp = net->bpp;
-        a.t = 0;
+        StepArgs a = step_args(net);
         a.list_lo = delay ? delay - net->dmin : 0;
-        a.list_hi = delay ? a.list_lo + 1 : net->lists;
-        a.acc = net->dbg_acc;
+        a.list_hi = a.list_lo + nl;
         a.dbg_spikes = d_sp;
         a.dbg_count = net->dbg_count;
-        e = deliver(a, deliver_grid(), s);
+        a.dbg_out = net->dbg_out;
+        if (!net->direct) e = launch_bin(a, 0, 0, s);
+        if (e == hipSuccess) e = launch_tile(a, 0, 0, s);
         if (e == hipSuccess) e = hipStreamSynchronize(s);
         if (e == hipSuccess)
-            e = hipMemcpy(fixed ? (void *)out_i32 : (void *)out_f32, net->dbg_acc,
+            e = hipMemcpy(fixed ? (void *)out_i32 : (void *)out_f32, net->dbg_out,
                           (size_t)net->n * 4, hipMemcpyDeviceToHost);
         if (e != hipSuccess) st = fail(SPK_EHIP, hipGetErrorString(e));
     } while (0);
@@ -899,9 +1063,13 @@ spk_status spk_stats(spk_net *net, spk_stats_t *out)
     st.delay_lists = net->lists;
     st.max_piece = net->max_piece;
     st.pois_len = net->pois_len;
-    st.fixed_shift = net->P.fixed_shift;
+    st.fixed_shift = net->P.acc_mode == SPK_ACC_FIXED ? net->P.fixed_shift : net->shift64;
     st.k = net->k;
     st.bytes_per_synapse = (double)sizeof(int2);
+    st.tile_width = net->tl.W;
+    st.tiles = net->tl.T;
+    st.delivery = net->direct ? SPK_DELIVERY_DIRECT : SPK_DELIVERY_BINNED;
+    st.bin_chunk = net->bin_chunk;
     *out = st;
     return SPK_OK;
 }
@@ -911,19 +1079,18 @@ spk_status spk_set_profiling(spk_net *net, int on)
     SPK_TRY(check_ready(net));
     SPK_TRY(collect_profile(net));
     net->profiling = on != 0;
-    net->ms_deliver = net->ms_update = 0;
+    net->ms_bin = net->ms_tile = 0;
     net->launches = 0;
     return SPK_OK;
 }
 
-spk_status spk_read_kernel_ms(spk_net *net, double *deliver_ms, double *update_ms,
-                              uint64_t *launches)
+spk_status spk_read_kernel_ms(spk_net *net, double *bin_ms, double *tile_ms, uint64_t *steps)
 {
     SPK_TRY(check_ready(net));
     SPK_TRY(collect_profile(net));
-    if (deliver_ms) *deliver_ms = net->ms_deliver;
-    if (update_ms) *update_ms = net->ms_update;
-    if (launches) *launches = net->launches;
+    if (bin_ms) *bin_ms = net->ms_bin;
+    if (tile_ms) *tile_ms = net->ms_tile;
+    if (steps) *steps = net->launches;
     return SPK_OK;
 }
 

@@ -23,6 +23,7 @@ SPK_ABI_VERSION = 1
 SPK_LIF, SPK_SOURCE = 0, 1
 SPK_CONN_BERNOULLI, SPK_CONN_FIXED_OUT, SPK_CONN_FIXED_IN, SPK_CONN_EXPLICIT = 0, 1, 2, 3
 SPK_ACC_F32, SPK_ACC_FIXED = 0, 1
+SPK_DELIVERY_AUTO, SPK_DELIVERY_DIRECT, SPK_DELIVERY_BINNED = 0, 1, 2
 
 EXPORTED = [
     "spk_preset", "spk_create", "spk_create_from_csr", "spk_step", "spk_sync",
@@ -46,7 +47,7 @@ class spk_params(C.Structure):
         ("w_exc", C.c_float), ("w_inh", C.c_float), ("w_lo", C.c_float), ("w_hi", C.c_float),
         ("delay_min", C.c_uint32), ("delay_max", C.c_uint32),
         ("ext_lambda", C.c_double), ("ext_w", C.c_float), ("acc_mode", C.c_uint32),
-        ("src_rate_hz", C.c_double), ("fixed_shift", C.c_int32), ("reserved0", C.c_uint32),
+        ("src_rate_hz", C.c_double), ("fixed_shift", C.c_int32), ("delivery", C.c_uint32),
         ("max_steps", C.c_uint64), ("raster_capacity", C.c_uint64),
     ]
 
@@ -58,6 +59,8 @@ class spk_stats_t(C.Structure):
         ("n_exc", C.c_uint32), ("ref_steps", C.c_uint32), ("ring_slots", C.c_uint32),
         ("delay_lists", C.c_uint32), ("max_piece", C.c_uint32), ("pois_len", C.c_uint32),
         ("fixed_shift", C.c_int32), ("k", C.c_float), ("bytes_per_synapse", C.c_double),
+        ("tile_width", C.c_uint32), ("tiles", C.c_uint32), ("delivery", C.c_uint32),
+        ("bin_chunk", C.c_uint32),
     ]
 
 

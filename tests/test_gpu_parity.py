@@ -4,13 +4,17 @@ Bar (per the method's two accumulation modes):
   - connectivity: every row identical (targets, delays, weight bits);
   - delivery of a given spike set: exact in fixed-point mode; in fp32 mode
     |I_gpu - I_ref| <= 1e-5 * max(|I_ref|, sum |w|) per target, I_ref summed
-    in double (fp32 atomics add in a run-dependent order);
+    in double (the bar for any fp32 summation order), and in addition
+    within one fp32 ulp of I_ref, since the library sums exactly and rounds
+    once;
   - whole simulation in fixed-point mode: bit-identical rasters, counts,
-    events and final state;
-  - fp32 mode: mean firing rate within 1 % (spike trains diverge chaotically
-    after the first rounding difference, so they are not compared).
-Sizes span several 64-synapse column blocks, many delay lists and ragged
-row lengths.
+    events, delivered events and final state, for both delivery strategies
+    and for graph replay as well as plain launches;
+  - fp32 mode: mean firing rate within 1 % (the oracle adds fp32 inputs one
+    by one in push order, the library rounds the exact sum once, so spike
+    trains diverge chaotically after the first difference).
+Sizes span several tiles, many delay lists, ragged row lengths and the bin
+overflow path.
 """
 import sys
 
@@ -35,6 +39,35 @@ def spk():
 def _say(*a):
     print(*a, flush=True)
     sys.stdout.flush()
+
+
+_ORACLE_NETS = {}
+_ORACLE_RUNS = {}
+
+
+def _key(cfg):
+    return tuple(sorted((k, v) for k, v in cfg.items() if k != "delivery"))
+
+
+def _oracle_net(cfg):
+    """Oracle network for cfg (the delivery strategy does not change it)."""
+    k = _key(cfg)
+    if k not in _ORACLE_NETS:
+        _ORACLE_NETS.clear()
+        _ORACLE_NETS[k] = oracle.Net(cfg)
+    return _ORACLE_NETS[k]
+
+
+def _oracle_run(cfg, T):
+    """(run record, final V, final ref, csr) of a fresh oracle network."""
+    k = (_key(cfg), T)
+    if k not in _ORACLE_RUNS:
+        _ORACLE_RUNS.clear()
+        o = oracle.Net(cfg)
+        r = o.run(T)
+        v, ref = o.state()
+        _ORACLE_RUNS[k] = (r, v, ref, o.csr())
+    return _ORACLE_RUNS[k]
 
 
 def _canon(col, d, wbits):
@@ -140,13 +173,19 @@ DELIVER_CASES = [
 ]
 
 
+DELIVERY = [(0, "auto"), (1, "direct"), (2, "binned")]
+
+
 @pytest.mark.parametrize("name,mk,delays", DELIVER_CASES, ids=[c[0] for c in DELIVER_CASES])
 @pytest.mark.parametrize("acc", [I.ACC_F32, I.ACC_FIXED], ids=["f32", "fixed"])
-def test_debug_deliver_matches_oracle(spk, name, mk, delays, acc):
+@pytest.mark.parametrize("delivery", [1, 2], ids=["direct", "binned"])
+def test_debug_deliver_matches_oracle(spk, name, mk, delays, acc, delivery):
     cfg = mk(acc)
+    cfg["delivery"] = delivery
     n = cfg["n"]
     g = spk.Net(cfg, max_steps=1)
-    o = oracle.Net(cfg)
+    assert g.stats()["delivery"] == delivery
+    o = _oracle_net(cfg)
     # spike-set sizes: empty, single, a typical step at ~10-50 Hz (n*r*dt with
     # r*dt ~ 0.005), a third of the network, every neuron, every neuron 3x
     for k, (count, uniq) in enumerate([(0, True), (1, True), (37, True), (max(1, n // 200), True),
@@ -167,6 +206,10 @@ def test_debug_deliver_matches_oracle(spk, name, mk, delays, acc):
                 assert np.all(err <= tol), f"max rel err {np.max(err / scale)}"
                 if terms.max() <= 168:  # the plain 1e-5 relative bar applies
                     assert np.all(err <= 1e-5 * scale)
+                # the library sums exactly and rounds once: within one fp32
+                # ulp of the double-precision reference sum
+                ulp = np.spacing(np.abs(want).astype(np.float32)).astype(np.float64)
+                assert np.all(err <= ulp), f"not the rounded exact sum: {np.max(err / ulp)} ulp"
 
 
 def test_debug_deliver_rejects_bad_input(spk):
@@ -190,21 +233,25 @@ RUN_CASES = [
 
 
 @pytest.mark.parametrize("name,mk,T", RUN_CASES, ids=[c[0] for c in RUN_CASES])
-def test_fixed_point_simulation_bit_identical(spk, name, mk, T):
+@pytest.mark.parametrize("delivery", [1, 2], ids=["direct", "binned"])
+@pytest.mark.parametrize("profiled", [False, True], ids=["graph", "launch"])
+def test_fixed_point_simulation_bit_identical(spk, name, mk, T, delivery, profiled):
     cfg = mk()
     cfg["acc_mode"] = I.ACC_FIXED
-    _say(f"[run] {name} n={cfg['n']} T={T}")
+    cfg["delivery"] = delivery
+    if profiled and name not in ("C0-driven", "C4-12000"):
+        pytest.skip("direct-launch path checked on two shapes")
+    _say(f"[run] {name} n={cfg['n']} T={T} delivery={delivery} profiled={profiled}")
     g = spk.Net(cfg, max_steps=T, raster_capacity=cfg["n"] * T)
+    g.set_profiling(profiled)
     g.step(T)
     offs, ids = g.raster()
-    o = oracle.Net(cfg)
-    r = o.run(T)
+    r, ov, orf, (rp, col, w, d) = _oracle_run(cfg, T)
     assert np.array_equal(g.spike_counts(), r["counts"]), "spike counts differ"
     assert np.array_equal(offs, r["offs"])
     assert np.array_equal(ids, r["raster"]), "rasters differ"
     assert np.array_equal(g.events(), r["events"]), "event counts differ"
     gv, gr = g.state()
-    ov, orf = o.state()
     assert np.array_equal(gv.view(np.uint32), ov.view(np.uint32)), "membrane potentials differ"
     assert np.array_equal(gr, orf)
     if name != "C0-literal":
@@ -213,13 +260,39 @@ def test_fixed_point_simulation_bit_identical(spk, name, mk, T):
         assert r["counts"].sum() == 0
     # delivered events: every spike emitted at t arrives at t + d
     dl = g.delivered()
-    rp, col, w, d = o.csr()
     want = np.zeros(T, np.uint64)
     for t in range(T):
         for s in r["raster"][int(r["offs"][t]):int(r["offs"][t + 1])]:
             dd = d[int(rp[s]):int(rp[s + 1])].astype(np.int64) + t
             np.add.at(want, dd[dd < T], 1)
     assert np.array_equal(dl, want), "delivered-event counts differ"
+    if profiled:
+        b, tile_ms, steps = g.kernel_ms()
+        assert steps == T and tile_ms > 0
+
+
+@pytest.mark.parametrize("acc", [I.ACC_F32, I.ACC_FIXED], ids=["f32", "fixed"])
+def test_bin_overflow_fallback(spk, acc):
+    # 64 neurons, 200 synapses each (multapses), all above threshold at t=0:
+    # one tile receives 12 800 events at step 1, more than its bin holds
+    # (4 096), so the global-atomic fallback must deliver the rest.
+    cfg = I.config(4, n=64, k_out=200, delay_min=1, delay_max=1, v0_lo=-49.0, v0_hi=-49.0,
+                   t_ref_ms=0.0, acc_mode=acc, delivery=2)
+    T = 6
+    g = spk.Net(cfg, max_steps=T, raster_capacity=64 * T)
+    spikes = np.arange(64, dtype=np.uint32)
+    got = g.debug_deliver(spikes)
+    o = oracle.Net(cfg)
+    if acc == I.ACC_FIXED:
+        assert np.array_equal(got.astype(np.int64), o.deliver(spikes, fixed=True)[1])
+        g.step(T)
+        r = o.run(T)
+        assert np.array_equal(g.raster()[1], r["raster"])
+        assert np.array_equal(g.state()[0].view(np.uint32), o.state()[0].view(np.uint32))
+    else:
+        want = o.deliver(spikes)
+        ulp = np.spacing(np.abs(want).astype(np.float32)).astype(np.float64)
+        assert np.all(np.abs(got - want) <= ulp)
 
 
 def test_resume_matches_single_run(spk):

@@ -5,6 +5,7 @@ call."""
 import ctypes as C
 import os
 import re
+import subprocess
 
 import numpy as np
 import pytest
@@ -32,11 +33,23 @@ def test_library_exports_every_declared_symbol():
     assert L.spk_abi_version() == spk.SPK_ABI_VERSION
 
 
-def test_params_struct_layout_matches_header():
-    # offsets of the C struct (x86-64 SysV): the ctypes mirror must agree
-    assert C.sizeof(spk.spk_params) == 176
-    assert spk.spk_params.max_steps.offset == 160
-    assert C.sizeof(spk.spk_stats_t) == 72
+@pytest.mark.parametrize("struct", [spk.spk_params, spk.spk_stats_t])
+def test_struct_layout_matches_header(struct, tmp_path):
+    # compile a probe against include/spk.h and compare every field offset
+    # and the size with the ctypes mirror used by the binding
+    name = struct.__name__
+    lines = ["#include <stdio.h>", "#include <stddef.h>", '#include "spk.h"', "int main(void){",
+             f'printf("%zu\\n", sizeof({name}));']
+    for f, _ in struct._fields_:
+        lines.append(f'printf("%zu\\n", offsetof({name}, {f}));')
+    lines.append("return 0;}")
+    src = tmp_path / "probe.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "probe"
+    subprocess.check_call(["gcc", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)])
+    out = [int(x) for x in subprocess.check_output([str(exe)]).split()]
+    assert out[0] == C.sizeof(struct)
+    assert out[1:] == [getattr(struct, f).offset for f, _ in struct._fields_]
 
 
 _FIELDS = ["n", "neuron_kind", "conn_kind", "frac_exc", "dt_ms", "tau_m_ms", "t_ref_ms", "v_rest",

@@ -40,6 +40,20 @@ def test_hash_streams_are_uniform_and_distinct():
     assert abs(np.corrcoef(u, v)[0, 1]) < 5.0 / math.sqrt(n)
 
 
+def test_step_stream_uniform_and_uncorrelated_in_time():
+    # per-step draws: uniform over neurons and steps, no correlation between
+    # consecutive steps of one neuron or neighbouring neurons of one step
+    ni, nt = 200, 100
+    u = np.array([[oracle.hash_step(3, TAG["POIS"], i, t) >> 40 for t in range(nt)]
+                  for i in range(ni)]) / 2.0**24
+    assert stats.kstest(u.ravel(), "uniform").pvalue > 1e-3
+    m = ni * (nt - 1)
+    assert abs(np.corrcoef(u[:, 1:].ravel(), u[:, :-1].ravel())[0, 1]) < 5.0 / math.sqrt(m)
+    assert abs(np.corrcoef(u[1:, :].ravel(), u[:-1, :].ravel())[0, 1]) < 5.0 / math.sqrt(m)
+    # the counter packs (t, i) into one 64-bit word: all draws distinct
+    assert len(set(u.ravel().tolist())) > 0.999 * u.size
+
+
 # ------------------------------------------------------------ neuron model
 
 def _isolated(**over):
