@@ -1,0 +1,242 @@
+#!/usr/bin/env python3
+"""Synaptic-event throughput of libspk on one MI355X.
+
+A step is one simulation timestep of the whole hot path: delivery of every
+due spike to its targets (binning + tile accumulation in LDS) and the update
+of every neuron with spike compaction.  The default workload is the
+3-billion-synapse one-GPU network (2 000 000 LIF neurons, fan-out 1 500,
+delays 1..20 steps) with the external Poisson drive that keeps it active
+(without drive every neuron decays to rest and no synaptic event happens).
+
+    python bench.py [--steps K] [--warmup W] [--config 4] [--acc f32|fixed]
+
+Prints one JSON line (the last line of stdout).  Timing: W untimed steps,
+then exactly K steps replayed from captured HIP graphs, bracketed by
+torch.cuda.synchronize(); events delivered are read from the device
+counters.  A second pass of K steps launches every kernel directly with HIP
+events around it (on the network's stream) to measure each kernel's average
+duration for the roofline figure.  The CPU oracle is timed on a bounded
+sample (reduced neuron count, same per-neuron statistics) for comparison.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+sys.path.insert(0, os.path.join(ROOT, "tests"))
+
+PEAK_HBM_GBS = 8000.0  # MI355X HBM3E, published
+METRIC = "synaptic events delivered/sec on 1 MI355X; % of HBM roofline"
+WORKLOAD_NAMES = {
+    0: "C0: 1,000 LIF, Bernoulli p=0.02, delay 1",
+    1: "C1: 250,000 LIF, Bernoulli p=0.02 (1.25e9 synapses), delay 1",
+    2: "C2: 100,000 LIF, in-degree 8,000 exc + 2,000 inh (1e9 synapses), delay 15, Poisson drive",
+    3: "C3: 1,000,000 Bernoulli sources, fan-out 1,000 (1e9 synapses), dt 1 ms",
+    4: "C4: 2,000,000 LIF, fan-out 1,500 (3e9 synapses), delays 1-20 steps",
+}
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=4500)
+    ap.add_argument("--warmup", type=int, default=500)
+    ap.add_argument("--config", type=int, default=4, choices=range(5))
+    ap.add_argument("--rate", type=float, default=10.0, help="source rate (Hz) for config 3")
+    ap.add_argument("--acc", choices=["f32", "fixed"], default="f32")
+    ap.add_argument("--delivery", choices=["auto", "direct", "binned"], default="auto")
+    ap.add_argument("--seed", type=int, default=1)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="target duration of the timed oracle sample")
+    ap.add_argument("--probe-copy", type=int, default=0, metavar="BYTES",
+                    help="only run the library's copy kernel on BYTES (counter calibration)")
+    return ap.parse_args()
+
+
+def workload(args):
+    import inputs as I
+    acc = I.ACC_FIXED if args.acc == "fixed" else I.ACC_F32
+    cfg = I.config(args.config, driven=True, seed=args.seed, rate_hz=args.rate, acc_mode=acc)
+    cfg["delivery"] = {"auto": 0, "direct": 1, "binned": 2}[args.delivery]
+    return cfg
+
+
+def algorithmic_bytes(n, kind, events, spikes):
+    """Bytes the hot path must move per the method: 8 B per delivered event
+    (int32 target + 32-bit weight read once), 10 B per LIF neuron and step
+    (V read + write, refractory counter read + write; 8 B for a source
+    neuron, which has no counter), 8 B per spike (ID written once, read
+    once).  Accumulators are on chip and cost nothing."""
+    per_neuron = 8 if kind == 1 else 10
+    return 8.0 * events, per_neuron * float(n) + 8.0 * spikes
+
+
+def step_source_sha():
+    h = hashlib.sha256()
+    with open(os.path.join(ROOT, "paper_2102_04681_amd", "csrc", "spk_step.hip"), "rb") as f:
+        h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(config, acc, kernel):
+    """HBM bytes per launch from the committed counter summary, or None when
+    the summary is missing or the step kernels changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"traffic_c{config}_{acc}.json")
+    try:
+        with open(path) as f:
+            d = json.load(f)
+    except OSError:
+        return None
+    if d.get("source_sha") != step_source_sha():
+        return None
+    k = d.get("kernels", {}).get(kernel)
+    if not k:
+        return None
+    return (k["fetch_kib"] * d["fetch_scale"] + k["write_kib"] * d["write_scale"]) * 1024.0
+
+
+def cpu_baseline(cfg, seconds):
+    """The oracle (single-threaded C, unchanged) on a bounded sample of the
+    workload: the same per-neuron statistics at a neuron count whose network
+    the oracle builds in seconds; only its step loop is timed."""
+    import oracle
+    import inputs as I
+    n_full = cfg["n"]
+    n = min(n_full, 20000)
+    sample = dict(cfg)
+    sample["n"] = n
+    if cfg["conn_kind"] == I.BERNOULLI and cfg["p"] * n_full > 0:
+        sample["p"] = min(1.0, cfg["p"] * n_full / n)  # keep the expected in-degree
+    if cfg["conn_kind"] == I.FIXED_IN:
+        ne = round(cfg["frac_exc"] * n)
+        sample["k_in_exc"] = min(cfg["k_in_exc"], ne)
+        sample["k_in_inh"] = min(cfg["k_in_inh"], n - ne)
+    net = oracle.Net(sample)
+    net.run(200)  # initial transient
+    events, steps, t0 = 0, 0, time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        r = net.run(100)
+        events += int(r["events"].sum())
+        steps += 100
+    dt = time.perf_counter() - t0
+    desc = (f"oracle step loop (single thread), {steps} steps of the same workload at n={n} "
+            f"(fan-in, fan-out, weights, delays and drive unchanged), network build and the "
+            f"first 200 steps excluded")
+    return {"value": events / dt, "unit": "events/s", "cores": 1, "kind": "oracle",
+            "sample": desc, "steps": steps, "seconds": round(dt, 2)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one MI355X: the simulated network is one GPU's share and "
+              "there is no multi-GPU path (run with --gpus 1).", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2102_04681_amd import spk
+
+    if not torch.cuda.is_available():
+        print("no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    stream = torch.cuda.Stream()
+    torch.cuda.set_stream(stream)
+
+    if args.probe_copy:
+        cfg = workload(args)
+        cfg["n"] = 1000
+        g = spk.Net(dict(cfg, conn_kind=0, p=0.0), stream=stream, max_steps=1)
+        ms = g.hbm_copy(args.probe_copy, reps=20)
+        print(json.dumps({"probe": "copy", "bytes": args.probe_copy, "reps": 20,
+                          "GB/s": 2 * args.probe_copy * 20 / (ms * 1e-3) / 1e9}))
+        return
+
+    cfg = workload(args)
+    W, K = args.warmup, args.steps
+    t_create = time.perf_counter()
+    net = spk.Net(cfg, stream=stream, max_steps=W + 2 * K)
+    torch.cuda.synchronize()
+    t_create = time.perf_counter() - t_create
+    st = net.stats()
+    print(f"[bench] {WORKLOAD_NAMES[args.config]}: nnz={st['nnz']} tiles={st['tiles']}x{st['tile_width']} "
+          f"delivery={'direct' if st['delivery'] == 1 else 'binned'} create={t_create:.2f}s",
+          file=sys.stderr, flush=True)
+
+    net.step(W)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    net.step(K)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    delivered = net.delivered(W, K).astype(float)
+    counts = net.spike_counts(W, K).astype(float)
+    events = float(delivered.sum())
+    spikes = float(counts.sum())
+    value = events / (ms * 1e-3)
+    ms_step = ms / K
+
+    # per-kernel durations, HIP events around every launch (second pass)
+    net.set_profiling(True)
+    net.step(K)
+    bin_ms, tile_ms, nsteps = net.kernel_ms()
+    net.set_profiling(False)
+    d2 = net.delivered(W + K, K).astype(float)
+    c2 = net.spike_counts(W + K, K).astype(float)
+    ev_b, ev_t = algorithmic_bytes(cfg["n"], cfg["neuron_kind"], float(d2.sum()), float(c2.sum()))
+    binned = st["delivery"] == 2
+    if binned:  # bin kernel reads the synapses; tile kernel updates the neurons
+        kernels = {"k_bin": (bin_ms / nsteps, ev_b / nsteps), "k_tile": (tile_ms / nsteps, ev_t / nsteps)}
+    else:       # tile kernel does both
+        kernels = {"k_tile": (tile_ms / nsteps, (ev_b + ev_t) / nsteps)}
+    dom = max(kernels, key=lambda k: kernels[k][0])
+    dom_ms, dom_bytes = kernels[dom]
+    achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
+    b_evt, b_neu = algorithmic_bytes(cfg["n"], cfg["neuron_kind"], events, spikes)
+    step_gbs = (b_evt + b_neu) / (ms * 1e-3) / 1e9
+    traffic = measured_traffic(args.config, args.acc, dom)
+    roofline = {
+        "bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+        "frac": round(achieved / PEAK_HBM_GBS, 4),
+        "traffic": None if traffic is None else round(traffic),
+        "kernel": dom, "kernel_us": round(dom_ms * 1e3, 2),
+        "kernel_alg_bytes": round(dom_bytes),
+        "step_alg_GBs": round(step_gbs, 1), "step_frac": round(step_gbs / PEAK_HBM_GBS, 4),
+        "events_only_frac": round(value / (PEAK_HBM_GBS * 1e9 / 8.0), 4),
+        "per_kernel_us": {k: round(v[0] * 1e3, 2) for k, v in kernels.items()},
+    }
+
+    rate_hz = spikes / (cfg["n"] * K * cfg["dt_ms"] * 1e-3)
+    out = {
+        "metric": METRIC, "value": value, "unit": "events/s", "n_gpus": 1, "steps": K,
+        "warmup": W, "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32" if args.acc == "f32" else "i32",
+        "data": "synthetic",
+        "config": {
+            "workload": WORKLOAD_NAMES[args.config] + (", Poisson drive at twice threshold rate"
+                                                       if cfg["ext_lambda"] and args.config != 2 else ""),
+            "n_neurons": cfg["n"], "synapses": int(st["nnz"]), "dt_ms": cfg["dt_ms"],
+            "delivery": "direct" if st["delivery"] == 1 else "binned",
+            "accumulation": "exact int64 fixed point, rounded once to fp32" if args.acc == "f32"
+                            else f"int32 fixed point 2^-{cfg['fixed_shift']}",
+            "mean_rate_hz": round(rate_hz, 3), "events_per_step": round(events / K, 1),
+            "seed": args.seed, "parallelism": "1 GPU",
+        },
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seconds)
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()
