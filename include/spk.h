@@ -12,7 +12,10 @@
  *     expanded on the GPU ("uploaded to the GPU where it is expanded").
  *   - Sec. III-C: every spike is delivered to all neighbours of its row.
  *   - Sec. IV-A: single-precision forward Euler integration.
- *   - Sec. V:    per-synapse delays through one adjacency list per delay.
+ *   - Sec. V:    per-synapse delays (the paper proposes one adjacency list
+ *                per delay; here every stored synapse carries its delay and
+ *                an event is filed under its arrival step when its source
+ *                fires -- the same deliveries).
  *
  * Conventions (all entry points):
  *   - Every function returns spk_status (0 = SPK_OK, negative = error) and
@@ -60,7 +63,10 @@ enum { SPK_CONN_BERNOULLI = 0, SPK_CONN_FIXED_OUT = 1, SPK_CONN_FIXED_IN = 2,
 enum { SPK_ACC_F32 = 0, SPK_ACC_FIXED = 1 };
 /* Delivery strategy (same results, different speed): AUTO picks from the
  * network's shape; DIRECT makes each target tile read its runs of the due
- * rows; BINNED first sorts the due events into per-tile bins. */
+ * rows at arrival (best for one delay and long rows); BINNED reads every
+ * fired row once, right after the spike, and files its events by (arrival
+ * step, target tile) in pages that the tile drains at arrival.  BINNED needs
+ * (delay_max - delay_min + 1) * tiles / 8 <= 4096. */
 enum { SPK_DELIVERY_AUTO = 0, SPK_DELIVERY_DIRECT = 1, SPK_DELIVERY_BINNED = 2 };
 
 /* Network parameters (plain data).
@@ -91,7 +97,11 @@ enum { SPK_DELIVERY_AUTO = 0, SPK_DELIVERY_DIRECT = 1, SPK_DELIVERY_BINNED = 2 }
  *   SplitMix64-based counter hash, so networks are reproducible exactly.
  * Capacities: max_steps bounds the per-step records (counts, events) and the
  *   total number of steps; raster_capacity bounds the recorded spike IDs
- *   (0 = no raster). */
+ *   (0 = no raster).  Limits: n <= 2^24, at most 65535 synapses per source
+ *   row.
+ * Tuning (environment, read at creation): SPK_TILES_PER_XCD caps the tiles
+ *   per XCD group (1..256, default 32); SPK_PAGE_CAP sets the records per
+ *   page of binned delivery (default: an equal share of 2 GiB). */
 typedef struct {
     uint32_t abi_version;      /* must be SPK_ABI_VERSION */
     uint32_t n;
@@ -120,7 +130,7 @@ typedef struct {
     uint64_t n, nnz, steps;
     uint64_t device_bytes;     /* device memory owned by the network */
     uint32_t n_exc, ref_steps, ring_slots, delay_lists;
-    uint32_t max_piece;        /* longest (source, delay) synapse run */
+    uint32_t max_row;          /* longest source row (synapses) */
     uint32_t pois_len;
     int32_t fixed_shift;       /* fixed mode: S; fp32 mode: the unit 2^-S64 of the exact sums */
     float k;
@@ -128,7 +138,7 @@ typedef struct {
     uint32_t tile_width;       /* target neurons per tile (one workgroup each) */
     uint32_t tiles;
     uint32_t delivery;         /* SPK_DELIVERY_DIRECT or SPK_DELIVERY_BINNED as chosen */
-    uint32_t bin_chunk;        /* rows per binning chunk (binned delivery) */
+    uint32_t page_cap;         /* binned delivery: records per page (beyond: global atomics) */
 } spk_stats_t;
 
 typedef struct spk_net spk_net;
@@ -215,12 +225,13 @@ spk_status spk_stats(spk_net *net, spk_stats_t *out);
 
 /* Kernel timing.  By default spk_step replays batches of steps captured in
  * a HIP graph.  With profiling on, it launches each kernel directly with HIP
- * events around the binning kernel (binned delivery only) and the tile
- * kernel (delivery into LDS + neuron update) on the network's stream, and
- * spk_read_kernel_ms returns their summed durations (ms) and the number of
- * steps since the last spk_set_profiling call. */
+ * events around the tile kernel (delivery into LDS + neuron update + spike
+ * list) and the push kernel (binned delivery only: the new spikes' events
+ * into arrival pages) on the network's stream, and spk_read_kernel_ms
+ * returns their summed durations (ms) and the number of steps since the
+ * last spk_set_profiling call. */
 spk_status spk_set_profiling(spk_net *net, int on);
-spk_status spk_read_kernel_ms(spk_net *net, double *bin_ms, double *tile_ms, uint64_t *steps);
+spk_status spk_read_kernel_ms(spk_net *net, double *push_ms, double *tile_ms, uint64_t *steps);
 
 /* Plain device-to-device copy of `bytes` bytes (multiple of 16) through the
  * library's streaming copy kernel on the network's stream, timed with HIP

@@ -1,9 +1,17 @@
-// spk_kernels.hip -- HIP kernels of libspk for gfx950 (MI355X, wave64).
+// spk_gen.hip -- connectivity expansion on the GPU (paper Sec. III-B: the
+// network description is expanded on the device, not uploaded synapse by
+// synapse) for gfx950 (MI355X, wave64).
 //
-// Build with -ffp-contract=off: the neuron update must round every fp32
-// operation separately (forward Euler in single precision, Sec. IV-A of the
-// paper), so no multiply-add may be fused.  The update additionally uses
-// the explicit _rn intrinsics.
+// Layout produced: one row per source neuron at [row_ptr[s], row_ptr[s+1]),
+// synapse = int2 {j << 24 | target, weight bits}, j = delay - delay_min.
+// Every row is grouped by target tile (the paper keeps rows sorted by target,
+// Sec. III-A, so that each target range of a row is one contiguous run; only
+// the grouping matters for delivery, the order inside a tile does not).  The
+// tile boundaries of every row are written alongside: per-tile starts for
+// direct delivery, per-XCD-group ends for binned delivery.
+//
+// Build with -ffp-contract=off: weights are computed with explicitly rounded
+// fp32 operations.
 #include <hip/hip_runtime.h>
 
 #include "spk_internal.h"
@@ -35,96 +43,161 @@ __device__ __forceinline__ int32_t weight_bits(const ConnArgs &c, float w)
     return __float_as_int(w);
 }
 
+__device__ __forceinline__ int2 make_syn(uint32_t j, uint32_t tgt, int32_t wbits)
+{
+    return make_int2((int)((j << kTargetBits) | tgt), wbits);
+}
+
 __device__ __forceinline__ uint32_t lane_id() { return threadIdx.x & (kWave - 1); }
 
-__device__ __forceinline__ uint32_t mbcnt(uint64_t mask)
+// Block-wide exclusive scan of one u32 per thread (kBlock threads).
+__device__ uint32_t block_scan_u32(uint32_t x, uint32_t *ws, uint32_t *total)
 {
-    return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
-                                     __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
-}
-
-__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t x)
-{
-    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
-    return x;
-}
-
-__device__ __forceinline__ uint64_t pack(int2 e)
-{
-    return ((uint64_t)(uint32_t)e.x << 32) | (uint64_t)(uint32_t)e.y;
-}
-__device__ __forceinline__ int2 unpack(uint64_t k)
-{
-    return make_int2((int)(uint32_t)(k >> 32), (int)(uint32_t)k);
-}
-
-// ------------------------------------------------------------ generation
-// Per-delay adjacency lists (Sec. V): list j holds the synapses of delay
-// dmin + j; "piece" (j, s) = the synapses of source s in list j, stored
-// contiguously at [row_ptr[j*n+s], row_ptr[j*n+s+1]).
-
-// Count pieces of Bernoulli / fixed out-degree rows: one block per source.
-__global__ __launch_bounds__(kBlock) void k_gen_count_rows(ConnArgs c, uint32_t *cnt)
-{
-    __shared__ uint32_t lc[kMaxLists];
-    const uint32_t s = blockIdx.x, tid = threadIdx.x;
-    for (uint32_t j = tid; j < c.lists; j += kBlock) lc[j] = 0;
+    const uint32_t lane = lane_id(), w = threadIdx.x / kWave;
+    uint32_t inc = x;
+    for (int o = 1; o < kWave; o <<= 1) {
+        const uint32_t y = __shfl_up(inc, o);
+        if (lane >= (uint32_t)o) inc += y;
+    }
+    if (lane == kWave - 1) ws[w] = inc;
     __syncthreads();
-    const uint64_t rd = mix64(c.keys.delay ^ (uint64_t)s);
-    uint32_t mine = 0;
-    if (c.kind == SPK_CONN_BERNOULLI) {
-        const uint64_t rk = mix64(c.keys.conn ^ (uint64_t)s);
-        for (uint32_t tgt = tid; tgt < c.n; tgt += kBlock) {
-            if ((uint64_t)hash_hi32(mix64(rk ^ (uint64_t)tgt)) < c.conn_thr) {
-                if (c.lists > 1) atomicAdd(&lc[hash_range(mix64(rd ^ (uint64_t)tgt), c.lists)], 1u);
-                else mine++;
-            }
-        }
-    } else {
-        for (uint32_t q = tid; q < c.k_out; q += kBlock) {
-            if (c.lists > 1) atomicAdd(&lc[hash_range(mix64(rd ^ (uint64_t)q), c.lists)], 1u);
-            else mine++;
+    uint32_t before = 0, tot = 0;
+    for (uint32_t k = 0; k < kBlock / kWave; k++) {
+        before += k < w ? ws[k] : 0u;
+        tot += ws[k];
+    }
+    __syncthreads();
+    *total = tot;
+    return before + inc - x;
+}
+
+// ------------------------------------------------------------ bucketing
+// Per-row counting sort by target tile in LDS: histogram, exclusive scan
+// (the tile starts), then every synapse goes to start[tile] + its rank.
+
+struct RowLDS {
+    uint32_t cur[kMaxTiles];
+    uint32_t ws[kBlock / kWave];
+};
+
+__device__ __forceinline__ void zero_tiles(RowLDS &L, uint32_t T)
+{
+    for (uint32_t k = threadIdx.x; k < T; k += kBlock) L.cur[k] = 0;
+    __syncthreads();
+}
+
+// histogram -> exclusive starts, in place
+__device__ void scan_tiles(RowLDS &L, uint32_t T)
+{
+    __syncthreads();
+    const uint32_t P = (T + kBlock - 1) / kBlock;
+    const uint32_t b = threadIdx.x * P;
+    uint32_t sum = 0;
+    for (uint32_t k = 0; k < P; k++)
+        if (b + k < T) sum += L.cur[b + k];
+    uint32_t tot;
+    uint32_t ex = block_scan_u32(sum, L.ws, &tot);
+    for (uint32_t k = 0; k < P; k++) {
+        if (b + k < T) {
+            const uint32_t v = L.cur[b + k];
+            L.cur[b + k] = ex;
+            ex += v;
         }
     }
-    if (c.lists == 1 && mine) atomicAdd(&lc[0], mine);
     __syncthreads();
-    for (uint32_t j = tid; j < c.lists; j += kBlock) cnt[(uint64_t)j * c.n + s] = lc[j];
 }
 
-// Fill pieces of Bernoulli / fixed out-degree rows (unordered inside a
-// piece; k_sort_* establish the order).
-__global__ __launch_bounds__(kBlock) void k_gen_fill_rows(ConnArgs c, const uint64_t *row_ptr,
-                                                         int2 *syn)
+// Tile boundaries of row s from the starts in L.cur (before placement).
+__device__ void write_row_index(const ConnArgs &c, const RowIndex &ix, RowLDS &L, uint32_t s,
+                                uint64_t start, uint32_t len)
 {
-    __shared__ uint32_t cur[kMaxLists];
-    const uint32_t s = blockIdx.x, tid = threadIdx.x;
-    for (uint32_t j = tid; j < c.lists; j += kBlock) cur[j] = 0;
+    const Tiling &tl = c.tl;
+    if (ix.toff) {
+        uint16_t *to = ix.toff + (uint64_t)s * (tl.T + 1);
+        for (uint32_t k = threadIdx.x; k <= tl.T; k += kBlock)
+            to[k] = (uint16_t)(k < tl.T ? L.cur[k] : len);
+    }
+    if (ix.desc && threadIdx.x == 0) {
+        RowDesc d;
+        d.start = start;
+        for (uint32_t x = 0; x < kGroups; x++)
+            d.gend[x] = (uint16_t)(x + 1 < kGroups ? L.cur[(x + 1) * tl.T8] : len);
+        d.spare = 0;
+        ix.desc[s] = d;
+    }
     __syncthreads();
+}
+
+__device__ __forceinline__ uint32_t tile_of(const ConnArgs &c, uint32_t tgt) { return tgt >> c.tl.logW; }
+
+// ----------------------------------------------- rows drawn per source
+// Bernoulli rows (one hash per ordered pair) and fixed out-degree rows
+// (k_out uniform targets with replacement): one block per source.
+
+__global__ __launch_bounds__(kBlock) void k_gen_count_rows(ConnArgs c, uint32_t *cnt)
+{
+    __shared__ uint32_t tot;
+    const uint32_t s = blockIdx.x;
+    if (c.kind != SPK_CONN_BERNOULLI) {
+        if (threadIdx.x == 0) cnt[s] = c.k_out;
+        return;
+    }
+    if (threadIdx.x == 0) tot = 0;
+    __syncthreads();
+    const uint64_t rk = mix64(c.keys.conn ^ (uint64_t)s);
+    uint32_t mine = 0;
+    for (uint32_t tgt = threadIdx.x; tgt < c.n; tgt += kBlock)
+        mine += (uint64_t)hash_hi32(mix64(rk ^ (uint64_t)tgt)) < c.conn_thr;
+    for (int o = 32; o > 0; o >>= 1) mine += __shfl_xor(mine, o);
+    if (lane_id() == 0 && mine) atomicAdd(&tot, mine);
+    __syncthreads();
+    if (threadIdx.x == 0) cnt[s] = tot;
+}
+
+// Draw the row twice: once to count per tile, once to place.
+__global__ __launch_bounds__(kBlock) void k_gen_fill_rows(ConnArgs c, const uint64_t *row_ptr,
+                                                         int2 *syn, RowIndex ix)
+{
+    __shared__ RowLDS L;
+    const uint32_t s = blockIdx.x, tid = threadIdx.x;
+    const uint64_t beg = row_ptr[s];
+    const uint32_t len = (uint32_t)(row_ptr[s + 1] - beg);
+    zero_tiles(L, c.tl.T);
     const uint64_t rd = mix64(c.keys.delay ^ (uint64_t)s);
     const uint64_t rw = mix64(c.keys.w ^ (uint64_t)s);
     if (c.kind == SPK_CONN_BERNOULLI) {
         const uint64_t rk = mix64(c.keys.conn ^ (uint64_t)s);
+        for (uint32_t tgt = tid; tgt < c.n; tgt += kBlock)
+            if ((uint64_t)hash_hi32(mix64(rk ^ (uint64_t)tgt)) < c.conn_thr)
+                atomicAdd(&L.cur[tile_of(c, tgt)], 1u);
+        scan_tiles(L, c.tl.T);
+        write_row_index(c, ix, L, s, beg, len);
         for (uint32_t tgt = tid; tgt < c.n; tgt += kBlock) {
             if (!((uint64_t)hash_hi32(mix64(rk ^ (uint64_t)tgt)) < c.conn_thr)) continue;
-            uint32_t j = c.lists > 1 ? hash_range(mix64(rd ^ (uint64_t)tgt), c.lists) : 0;
-            float w = syn_weight(c, s, mix64(rw ^ (uint64_t)tgt));
-            uint32_t pos = atomicAdd(&cur[j], 1u);
-            syn[row_ptr[(uint64_t)j * c.n + s] + pos] = make_int2((int)tgt, weight_bits(c, w));
+            const uint32_t j = c.lists > 1 ? hash_range(mix64(rd ^ (uint64_t)tgt), c.lists) : 0;
+            const float w = syn_weight(c, s, mix64(rw ^ (uint64_t)tgt));
+            const uint32_t pos = atomicAdd(&L.cur[tile_of(c, tgt)], 1u);
+            syn[beg + pos] = make_syn(j, tgt, weight_bits(c, w));
         }
     } else {
         const uint64_t rt = mix64(c.keys.tgt ^ (uint64_t)s);
+        for (uint32_t q = tid; q < c.k_out; q += kBlock)
+            atomicAdd(&L.cur[tile_of(c, hash_range(mix64(rt ^ (uint64_t)q), c.n))], 1u);
+        scan_tiles(L, c.tl.T);
+        write_row_index(c, ix, L, s, beg, len);
         for (uint32_t q = tid; q < c.k_out; q += kBlock) {
-            uint32_t tgt = hash_range(mix64(rt ^ (uint64_t)q), c.n);
-            uint32_t j = c.lists > 1 ? hash_range(mix64(rd ^ (uint64_t)q), c.lists) : 0;
-            float w = syn_weight(c, s, mix64(rw ^ (uint64_t)q));
-            uint32_t pos = atomicAdd(&cur[j], 1u);
-            syn[row_ptr[(uint64_t)j * c.n + s] + pos] = make_int2((int)tgt, weight_bits(c, w));
+            const uint32_t tgt = hash_range(mix64(rt ^ (uint64_t)q), c.n);
+            const uint32_t j = c.lists > 1 ? hash_range(mix64(rd ^ (uint64_t)q), c.lists) : 0;
+            const float w = syn_weight(c, s, mix64(rw ^ (uint64_t)q));
+            const uint32_t pos = atomicAdd(&L.cur[tile_of(c, tgt)], 1u);
+            syn[beg + pos] = make_syn(j, tgt, weight_bits(c, w));
         }
     }
 }
 
-// Fixed in-degree: one block per target draws its sources; the synapses
-// are regrouped by source through global atomic counters.
+// ------------------------------------------------- fixed in-degree rows
+// One block per target draws its sources; synapses are regrouped by source
+// through global atomic cursors (unordered), then bucketed by bucket_rows.
 __device__ __forceinline__ uint32_t in_source(const ConnArgs &c, uint64_t re, uint64_t ri,
                                               uint32_t q)
 {
@@ -137,13 +210,9 @@ __global__ __launch_bounds__(kBlock) void k_gen_in_count(ConnArgs c, uint32_t *c
     const uint32_t tgt = blockIdx.x;
     const uint64_t re = mix64(c.keys.src_e ^ (uint64_t)tgt);
     const uint64_t ri = mix64(c.keys.src_i ^ (uint64_t)tgt);
-    const uint64_t rd = mix64(c.keys.delay ^ (uint64_t)tgt);
     const uint32_t kin = c.k_in_exc + c.k_in_inh;
-    for (uint32_t q = threadIdx.x; q < kin; q += kBlock) {
-        uint32_t src = in_source(c, re, ri, q);
-        uint32_t j = c.lists > 1 ? hash_range(mix64(rd ^ (uint64_t)q), c.lists) : 0;
-        atomicAdd(&cnt[(uint64_t)j * c.n + src], 1u);
-    }
+    for (uint32_t q = threadIdx.x; q < kin; q += kBlock)
+        atomicAdd(&cnt[in_source(c, re, ri, q)], 1u);
 }
 
 __global__ __launch_bounds__(kBlock) void k_gen_in_fill(ConnArgs c, const uint64_t *row_ptr,
@@ -156,41 +225,46 @@ __global__ __launch_bounds__(kBlock) void k_gen_in_fill(ConnArgs c, const uint64
     const uint64_t rw = mix64(c.keys.w ^ (uint64_t)tgt);
     const uint32_t kin = c.k_in_exc + c.k_in_inh;
     for (uint32_t q = threadIdx.x; q < kin; q += kBlock) {
-        uint32_t src = in_source(c, re, ri, q);
-        uint32_t j = c.lists > 1 ? hash_range(mix64(rd ^ (uint64_t)q), c.lists) : 0;
-        float w = syn_weight(c, src, mix64(rw ^ (uint64_t)q));
-        uint64_t piece = (uint64_t)j * c.n + src;
-        uint32_t pos = atomicAdd(&cursor[piece], 1u);
-        syn[row_ptr[piece] + pos] = make_int2((int)tgt, weight_bits(c, w));
+        const uint32_t src = in_source(c, re, ri, q);
+        const uint32_t j = c.lists > 1 ? hash_range(mix64(rd ^ (uint64_t)q), c.lists) : 0;
+        const float w = syn_weight(c, src, mix64(rw ^ (uint64_t)q));
+        const uint32_t pos = atomicAdd(&cursor[src], 1u);
+        syn[row_ptr[src] + pos] = make_syn(j, tgt, weight_bits(c, w));
     }
 }
 
-// Explicit adjacency (host-given rows): one thread per source row.
-__global__ __launch_bounds__(kBlock) void k_csr_count(ConnArgs c, const uint64_t *in_ptr,
-                                                     const uint8_t *in_delay, uint32_t *cnt)
+// Explicit adjacency (host-given rows, already in row order): encode.
+__global__ __launch_bounds__(kBlock) void k_csr_fill(ConnArgs c, uint64_t nnz, const uint32_t *in_col,
+                                                    const float *in_w, const uint8_t *in_delay,
+                                                    int2 *syn)
 {
-    const uint32_t s = blockIdx.x * kBlock + threadIdx.x;
-    if (s >= c.n) return;
-    for (uint64_t e = in_ptr[s]; e < in_ptr[s + 1]; e++) {
-        uint32_t j = in_delay ? (uint32_t)in_delay[e] - c.dmin : 0;
-        cnt[(uint64_t)j * c.n + s] += 1;
+    for (uint64_t e = (uint64_t)blockIdx.x * kBlock + threadIdx.x; e < nnz;
+         e += (uint64_t)gridDim.x * kBlock) {
+        const uint32_t j = in_delay ? (uint32_t)in_delay[e] - c.dmin : 0u;
+        syn[e] = make_syn(j, in_col[e], weight_bits(c, in_w[e]));
     }
 }
 
-__global__ __launch_bounds__(kBlock) void k_csr_fill(ConnArgs c, const uint64_t *in_ptr,
-                                                    const uint32_t *in_col, const float *in_w,
-                                                    const uint8_t *in_delay,
-                                                    const uint64_t *row_ptr, int2 *syn)
+// Group the synapses of every row of src by target tile into dst (same
+// row_ptr) and write the row's tile boundaries.  Blocks stride over rows.
+__global__ __launch_bounds__(kBlock) void k_bucket_rows(ConnArgs c, const uint64_t *row_ptr,
+                                                       const int2 *src, int2 *dst, RowIndex ix)
 {
-    const uint32_t s = blockIdx.x * kBlock + threadIdx.x;
-    if (s >= c.n) return;
-    uint32_t fill[kMaxLists];
-    for (uint32_t j = 0; j < c.lists; j++) fill[j] = 0;
-    for (uint64_t e = in_ptr[s]; e < in_ptr[s + 1]; e++) {
-        uint32_t j = in_delay ? (uint32_t)in_delay[e] - c.dmin : 0;
-        uint64_t piece = (uint64_t)j * c.n + s;
-        syn[row_ptr[piece] + fill[j]] = make_int2((int)in_col[e], weight_bits(c, in_w[e]));
-        fill[j] += 1;
+    __shared__ RowLDS L;
+    for (uint32_t s = blockIdx.x; s < c.n; s += gridDim.x) {
+        const uint64_t beg = row_ptr[s];
+        const uint32_t len = (uint32_t)(row_ptr[s + 1] - beg);
+        zero_tiles(L, c.tl.T);
+        for (uint32_t e = threadIdx.x; e < len; e += kBlock)
+            atomicAdd(&L.cur[tile_of(c, (uint32_t)src[beg + e].x & kTargetMask)], 1u);
+        scan_tiles(L, c.tl.T);
+        write_row_index(c, ix, L, s, beg, len);
+        for (uint32_t e = threadIdx.x; e < len; e += kBlock) {
+            const int2 r = src[beg + e];
+            const uint32_t pos = atomicAdd(&L.cur[tile_of(c, (uint32_t)r.x & kTargetMask)], 1u);
+            dst[beg + pos] = r;
+        }
+        __syncthreads();
     }
 }
 
@@ -274,93 +348,13 @@ __global__ __launch_bounds__(kBlock) void k_scan3(uint64_t *out, uint64_t m, con
     if (blockIdx.x == 0 && threadIdx.x == 0) out[m] = bsum[nb];
 }
 
-// ------------------------------------------------------------------ sort
-// Every piece is sorted by (target, weight bits).  Pieces of up to
-// kSmallSort synapses: one wave each, rank by counting; longer pieces are
-// listed for a block-wide bitonic sort in LDS.
-constexpr uint32_t kSmallSort = 256;
-
-__global__ __launch_bounds__(kBlock) void k_sort_small(const uint64_t *row_ptr, int2 *syn, uint64_t m,
-                                                      uint32_t *large, uint32_t *n_large)
-{
-    __shared__ uint64_t keys[kBlock / kWave][kSmallSort];
-    const uint32_t lane = lane_id(), w = threadIdx.x / kWave;
-    for (uint64_t b0 = (uint64_t)blockIdx.x * (kBlock / kWave); b0 < m;
-         b0 += (uint64_t)gridDim.x * (kBlock / kWave)) {
-        const uint64_t piece = b0 + w;
-        uint64_t beg = 0;
-        uint32_t L = 0;
-        if (piece < m) {
-            beg = row_ptr[piece];
-            uint64_t len = row_ptr[piece + 1] - beg;
-            if (len > kSmallSort) {
-                if (lane == 0) large[atomicAdd(n_large, 1u)] = (uint32_t)piece;
-            } else {
-                L = (uint32_t)len;
-            }
-        }
-        if (L < 2) L = 0;
-        for (uint32_t e = lane; e < L; e += kWave) keys[w][e] = pack(syn[beg + e]);
-        __syncthreads();
-        for (uint32_t e = lane; e < L; e += kWave) {
-            const uint64_t k = keys[w][e];
-            uint32_t r = 0;
-            for (uint32_t q = 0; q < L; q++) {
-                const uint64_t kq = keys[w][q];
-                r += (kq < k) | ((kq == k) & (q < e));
-            }
-            syn[beg + r] = unpack(k);
-        }
-        __syncthreads();
-    }
-}
-
-constexpr int kSortThreads = 1024;
-
-__global__ __launch_bounds__(kSortThreads) void k_sort_large(const uint64_t *row_ptr, int2 *syn,
-                                                            const uint32_t *large)
-{
-    extern __shared__ uint64_t sk[];
-    const uint32_t piece = large[blockIdx.x];
-    const uint64_t beg = row_ptr[piece];
-    const uint32_t L = (uint32_t)(row_ptr[piece + 1] - beg);
-    uint32_t P2 = 1;
-    while (P2 < L) P2 <<= 1;
-    for (uint32_t e = threadIdx.x; e < P2; e += kSortThreads)
-        sk[e] = e < L ? pack(syn[beg + e]) : ~0ull;
-    __syncthreads();
-    for (uint32_t k = 2; k <= P2; k <<= 1) {
-        for (uint32_t j = k >> 1; j > 0; j >>= 1) {
-            for (uint32_t e = threadIdx.x; e < P2; e += kSortThreads) {
-                const uint32_t x = e ^ j;
-                if (x > e) {
-                    const uint64_t a = sk[e], b = sk[x];
-                    const bool up = (e & k) == 0;
-                    if ((a > b) == up) {
-                        sk[e] = b;
-                        sk[x] = a;
-                    }
-                }
-            }
-            __syncthreads();
-        }
-    }
-    for (uint32_t e = threadIdx.x; e < L; e += kSortThreads) syn[beg + e] = unpack(sk[e]);
-}
-
 // --------------------------------------------------------- bookkeeping
 
 __global__ __launch_bounds__(kBlock) void k_out_degree(const uint64_t *row_ptr, uint32_t n,
-                                                      uint32_t lists, uint32_t *outdeg)
+                                                      uint32_t *outdeg)
 {
     const uint32_t s = blockIdx.x * kBlock + threadIdx.x;
-    if (s >= n) return;
-    uint64_t d = 0;
-    for (uint32_t j = 0; j < lists; j++) {
-        const uint64_t r = (uint64_t)j * n + s;
-        d += row_ptr[r + 1] - row_ptr[r];
-    }
-    outdeg[s] = (uint32_t)d;
+    if (s < n) outdeg[s] = (uint32_t)(row_ptr[s + 1] - row_ptr[s]);
 }
 
 // Per-target sum of |weight| over all in-synapses: exact in quantised units
@@ -379,45 +373,8 @@ __global__ __launch_bounds__(kBlock) void k_in_abs_sum(const int2 *syn, uint64_t
             const float w = fabsf(__int_as_float(x.y));
             q = (unsigned long long)ceil(ldexp((double)w, 24));
         }
-        atomicAdd(&insum[(uint32_t)x.x], q);
+        atomicAdd(&insum[(uint32_t)x.x & kTargetMask], q);
     }
-}
-
-// Sub-piece boundaries of target-sorted pieces: off[p*bounds + b] is the
-// offset (from the piece start) of the first synapse with target >= b*width.
-// Also the longest sub-piece (targets in [b*width, (b+1)*width)).
-__global__ __launch_bounds__(kBlock) void k_piece_offsets(const uint64_t *row_ptr, const int2 *syn,
-                                                         uint64_t pieces, uint32_t bounds,
-                                                         uint32_t width, uint16_t *off,
-                                                         uint32_t *max_sub)
-{
-    uint32_t mx = 0;
-    for (uint64_t k = (uint64_t)blockIdx.x * kBlock + threadIdx.x; k < pieces * bounds;
-         k += (uint64_t)gridDim.x * kBlock) {
-        const uint64_t p = k / bounds;
-        const uint32_t b = (uint32_t)(k % bounds);
-        const uint64_t beg = row_ptr[p];
-        const uint32_t L = (uint32_t)(row_ptr[p + 1] - beg);
-        const uint64_t lo_t = (uint64_t)b * width, hi_t = lo_t + width;
-        uint32_t lo = 0, hi = L;  // first index with target >= lo_t
-        while (lo < hi) {
-            const uint32_t mid = (lo + hi) >> 1;
-            if ((uint64_t)(uint32_t)syn[beg + mid].x < lo_t) lo = mid + 1; else hi = mid;
-        }
-        const uint32_t first = lo;
-        hi = L;  // first index with target >= hi_t
-        while (lo < hi) {
-            const uint32_t mid = (lo + hi) >> 1;
-            if ((uint64_t)(uint32_t)syn[beg + mid].x < hi_t) lo = mid + 1; else hi = mid;
-        }
-        off[k] = (uint16_t)first;
-        mx = lo - first > mx ? lo - first : mx;
-    }
-    for (int o = 32; o > 0; o >>= 1) {
-        const uint32_t y = __shfl_xor(mx, o);
-        mx = y > mx ? y : mx;
-    }
-    if (lane_id() == 0 && mx) atomicMax(max_sub, mx);
 }
 
 __global__ __launch_bounds__(kBlock) void k_max_u64(const uint64_t *x, uint64_t m,
@@ -447,33 +404,21 @@ __global__ __launch_bounds__(kBlock) void k_init_state(ModelArgs m, float v0_lo,
 
 // ---------------------------------------------------------------- export
 
-__global__ __launch_bounds__(kBlock) void k_export_lens(const uint64_t *row_ptr, uint32_t n,
-                                                       uint32_t lists, const uint32_t *rows,
-                                                       uint64_t n_rows, uint64_t *lens)
-{
-    const uint64_t k = (uint64_t)blockIdx.x * kBlock + threadIdx.x;
-    if (k >= n_rows * lists) return;
-    const uint64_t r = k / lists, j = k % lists;
-    const uint64_t piece = j * n + rows[r];
-    lens[k] = row_ptr[piece + 1] - row_ptr[piece];
-}
-
+// One block per requested row: decode (target, delay, weight bits).
 __global__ __launch_bounds__(kBlock) void k_export_gather(const uint64_t *row_ptr, const int2 *syn,
-                                                         uint32_t n, uint32_t lists, uint32_t dmin,
-                                                         const uint32_t *rows,
-                                                         const uint64_t *piece_off, uint32_t *col,
+                                                         uint32_t dmin, const uint32_t *rows,
+                                                         const uint64_t *out_off, uint32_t *col,
                                                          uint32_t *wbits, uint8_t *delay)
 {
-    const uint64_t k = blockIdx.x;  // (row r, list j) = (k / lists, k % lists)
-    const uint64_t r = k / lists, j = k % lists;
-    const uint64_t piece = j * n + rows[r];
-    const uint64_t beg = row_ptr[piece], L = row_ptr[piece + 1] - beg;
-    const uint64_t o = piece_off[k];
+    const uint64_t r = blockIdx.x;
+    const uint32_t s = rows[r];
+    const uint64_t beg = row_ptr[s], L = row_ptr[s + 1] - beg;
+    const uint64_t o = out_off[r];
     for (uint64_t e = threadIdx.x; e < L; e += kBlock) {
         const int2 x = syn[beg + e];
-        col[o + e] = (uint32_t)x.x;
+        col[o + e] = (uint32_t)x.x & kTargetMask;
         wbits[o + e] = (uint32_t)x.y;
-        delay[o + e] = (uint8_t)(dmin + j);
+        delay[o + e] = (uint8_t)(dmin + ((uint32_t)x.x >> kTargetBits));
     }
 }
 
@@ -508,9 +453,11 @@ hipError_t gen_count_rows(const ConnArgs &c, uint32_t *cnt, hipStream_t s)
     return hipGetLastError();
 }
 
-hipError_t gen_fill_rows(const ConnArgs &c, const uint64_t *row_ptr, int2 *syn, hipStream_t s)
+hipError_t gen_fill_rows(const ConnArgs &c, const uint64_t *row_ptr, int2 *syn, RowIndex ix,
+                         hipStream_t s)
 {
-    hipLaunchKernelGGL(k_gen_fill_rows, dim3(c.n), dim3(kBlock), 0, s, c, row_ptr, syn);
+    if (c.tl.T > kMaxTiles) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_gen_fill_rows, dim3(c.n), dim3(kBlock), 0, s, c, row_ptr, syn, ix);
     return hipGetLastError();
 }
 
@@ -527,33 +474,35 @@ hipError_t gen_in_fill(const ConnArgs &c, const uint64_t *row_ptr, uint32_t *cur
     return hipGetLastError();
 }
 
-hipError_t csr_count(const ConnArgs &c, const uint64_t *in_ptr, const uint8_t *in_delay,
-                     uint32_t *cnt, hipStream_t s)
+hipError_t csr_fill(const ConnArgs &c, uint64_t nnz, const uint32_t *in_col, const float *in_w,
+                    const uint8_t *in_delay, int2 *syn, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_csr_count, dim3(grid_for(c.n)), dim3(kBlock), 0, s, c, in_ptr, in_delay, cnt);
+    if (!nnz) return hipSuccess;
+    hipLaunchKernelGGL(k_csr_fill, dim3(grid_for(nnz, 65536)), dim3(kBlock), 0, s, c, nnz, in_col,
+                       in_w, in_delay, syn);
     return hipGetLastError();
 }
 
-hipError_t csr_fill(const ConnArgs &c, const uint64_t *in_ptr, const uint32_t *in_col,
-                    const float *in_w, const uint8_t *in_delay, const uint64_t *row_ptr,
-                    int2 *syn, hipStream_t s)
+hipError_t bucket_rows(const ConnArgs &c, const uint64_t *row_ptr, const int2 *src, int2 *dst,
+                       RowIndex ix, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_csr_fill, dim3(grid_for(c.n)), dim3(kBlock), 0, s, c, in_ptr, in_col, in_w,
-                       in_delay, row_ptr, syn);
+    if (c.tl.T > kMaxTiles) return hipErrorInvalidValue;
+    const uint32_t g = c.n < 65536u ? c.n : 65536u;
+    hipLaunchKernelGGL(k_bucket_rows, dim3(g ? g : 1), dim3(kBlock), 0, s, c, row_ptr, src, dst, ix);
     return hipGetLastError();
 }
 
 size_t scan_scratch_elems(uint64_t m) { return (size_t)((m + kScanTile - 1) / kScanTile) + 1; }
 
 hipError_t scan_counts(const uint32_t *cnt, uint64_t m, uint64_t *out, uint64_t *block_sums,
-                       uint32_t *max_piece, hipStream_t s)
+                       uint32_t *max_count, hipStream_t s)
 {
     const uint64_t nb = (m + kScanTile - 1) / kScanTile;
     if (nb == 0) {
         return hipMemsetAsync(out, 0, sizeof(uint64_t), s);
     }
     hipLaunchKernelGGL(k_scan1, dim3((uint32_t)nb), dim3(kBlock), 0, s, cnt, m, out, block_sums,
-                       max_piece);
+                       max_count);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k_scan2, dim3(1), dim3(kBlock), 0, s, block_sums, nb);
@@ -563,33 +512,9 @@ hipError_t scan_counts(const uint32_t *cnt, uint64_t m, uint64_t *out, uint64_t 
     return hipGetLastError();
 }
 
-hipError_t sort_small_pieces(const uint64_t *row_ptr, int2 *syn, uint64_t m, uint32_t *large,
-                             uint32_t *n_large, hipStream_t s)
+hipError_t out_degree(const uint64_t *row_ptr, uint32_t n, uint32_t *outdeg, hipStream_t s)
 {
-    uint64_t g = (m + 3) / 4;
-    if (g > 65536) g = 65536;
-    if (g == 0) g = 1;
-    hipLaunchKernelGGL(k_sort_small, dim3((uint32_t)g), dim3(kBlock), 0, s, row_ptr, syn, m, large,
-                       n_large);
-    return hipGetLastError();
-}
-
-hipError_t sort_large_pieces(const uint64_t *row_ptr, int2 *syn, const uint32_t *large,
-                             uint32_t n_large, uint32_t pow2, hipStream_t s)
-{
-    if (!n_large) return hipSuccess;
-    const size_t lds = (size_t)pow2 * sizeof(uint64_t);
-    hipError_t e = hipFuncSetAttribute((const void *)k_sort_large,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_sort_large, dim3(n_large), dim3(kSortThreads), lds, s, row_ptr, syn, large);
-    return hipGetLastError();
-}
-
-hipError_t out_degree(const uint64_t *row_ptr, uint32_t n, uint32_t lists, uint32_t *outdeg,
-                      hipStream_t s)
-{
-    hipLaunchKernelGGL(k_out_degree, dim3(grid_for(n)), dim3(kBlock), 0, s, row_ptr, n, lists, outdeg);
+    hipLaunchKernelGGL(k_out_degree, dim3(grid_for(n)), dim3(kBlock), 0, s, row_ptr, n, outdeg);
     return hipGetLastError();
 }
 
@@ -615,33 +540,14 @@ hipError_t init_state(const ModelArgs &m, float v0_lo, float v0_hi, float *V, ui
     return hipGetLastError();
 }
 
-hipError_t piece_offsets(const uint64_t *row_ptr, const int2 *syn, uint64_t pieces, uint32_t bounds,
-                         uint32_t width, uint16_t *off, uint32_t *max_sub, hipStream_t s)
-{
-    if (!pieces) return hipSuccess;
-    hipLaunchKernelGGL(k_piece_offsets, dim3(grid_for(pieces * bounds, 1u << 22)), dim3(kBlock), 0, s,
-                       row_ptr, syn, pieces, bounds, width, off, max_sub);
-    return hipGetLastError();
-}
-
-hipError_t export_lens(const uint64_t *row_ptr, uint32_t n, uint32_t lists, const uint32_t *rows,
-                       uint64_t n_rows, uint64_t *lens, hipStream_t s)
-{
-    hipLaunchKernelGGL(k_export_lens, dim3(grid_for(n_rows * lists)), dim3(kBlock), 0, s, row_ptr, n,
-                       lists, rows, n_rows, lens);
-    return hipGetLastError();
-}
-
-hipError_t export_gather(const uint64_t *row_ptr, const int2 *syn, uint32_t n, uint32_t lists,
-                         uint32_t dmin, const uint32_t *rows, uint64_t n_rows,
-                         const uint64_t *piece_off, uint32_t *col, uint32_t *wbits,
+hipError_t export_gather(const uint64_t *row_ptr, const int2 *syn, uint32_t dmin, const uint32_t *rows,
+                         uint64_t n_rows, const uint64_t *out_off, uint32_t *col, uint32_t *wbits,
                          uint8_t *delay, hipStream_t s)
 {
-    const uint64_t pieces = n_rows * lists;
-    if (!pieces) return hipSuccess;
-    if (pieces > 0x7fffffffull) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_export_gather, dim3((uint32_t)pieces), dim3(kBlock), 0, s, row_ptr, syn, n,
-                       lists, dmin, rows, piece_off, col, wbits, delay);
+    if (!n_rows) return hipSuccess;
+    if (n_rows > 0x7fffffffull) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_export_gather, dim3((uint32_t)n_rows), dim3(kBlock), 0, s, row_ptr, syn, dmin,
+                       rows, out_off, col, wbits, delay);
     return hipGetLastError();
 }
 

@@ -12,9 +12,16 @@ namespace spk {
 
 constexpr uint32_t kMaxLists = SPK_MAX_DELAY_LISTS;
 constexpr int kWave = 64;
-constexpr uint32_t kGroups = 8;      // one target group per XCD (blockIdx % 8 == XCD)
-constexpr uint32_t kPad = 16;        // u32 counters padded to 64 B
-constexpr uint32_t kMaxTileW = 8192; // neurons per tile (LDS accumulators + spike list)
+constexpr uint32_t kGroups = 8;        // one target group per XCD (blockIdx % 8 == XCD)
+constexpr uint32_t kMaxTileW = 8192;   // neurons per tile (LDS accumulators + spike list)
+constexpr uint32_t kMaxT8 = 256;       // tiles per group
+constexpr uint32_t kMaxTiles = kGroups * kMaxT8;
+constexpr uint32_t kMaxBuckets = 4096; // (delay, tile) buckets of one group in the push kernel
+constexpr uint32_t kMaxRow = 65535;    // synapses per source row (16-bit run offsets)
+// A stored synapse is int2 {delay index << 24 | target, weight bits}: the
+// target needs at most 24 bits (n <= 2^24), the delay index j = d - dmin < 64.
+constexpr uint32_t kTargetBits = 24;
+constexpr uint32_t kTargetMask = (1u << kTargetBits) - 1u;
 
 // Stream tags of the counter-based hash: one independent stream per kind of
 // random decision (connection, target, source, weight, delay, initial V,
@@ -71,11 +78,21 @@ struct Tiling {
     uint32_t Gw;        // group width = T8 * W
 };
 
+// Where the runs of one source row start, per XCD group (binned delivery):
+// group x owns [start + (x ? gend[x-1] : 0), start + gend[x]); gend[7] is the
+// row length.
+struct RowDesc {
+    uint64_t start;
+    uint16_t gend[kGroups];
+    uint64_t spare;
+};
+static_assert(sizeof(RowDesc) == 32, "one row descriptor is 32 bytes");
+
 // Connectivity generation parameters.
 struct ConnArgs {
     uint32_t n, n_exc;
     uint32_t kind;          // SPK_CONN_*
-    uint32_t lists;         // D = delay_max - delay_min + 1
+    uint32_t lists;         // delay_max - delay_min + 1
     uint32_t dmin;
     uint32_t k_out, k_in_exc, k_in_inh;
     uint64_t conn_thr;      // Bernoulli: connect iff hi32 < conn_thr
@@ -84,6 +101,14 @@ struct ConnArgs {
     uint32_t fixed;         // store quantised weights
     float qscale;           // 2^fixed_shift
     Keys keys;
+    Tiling tl;
+};
+
+// Where a bucketing pass writes the tile boundaries of every row: per-tile
+// starts (direct delivery, T+1 per row) or per-group descriptors (binned).
+struct RowIndex {
+    uint16_t *toff;         // n * (T+1) or null
+    RowDesc *desc;          // n or null
 };
 
 // Neuron model constants for the update.
@@ -105,81 +130,79 @@ struct ModelArgs {
 struct StepArgs {
     ModelArgs m;
     Tiling tl;
-    uint32_t n, lists, dmin, ring_slots;
-    uint32_t direct;             // 1: tiles read their sub-pieces (no bins)
-    const uint64_t *row_ptr;     // lists*n + 1: piece (j, s) = [row_ptr[j*n+s], row_ptr[j*n+s+1])
-    const int2 *syn;             // {target, weight bits (fp32 or quantised int32)}
-    const uint16_t *goff;        // 8 per piece: group sub-piece starts (binned mode)
-    const uint16_t *toff;        // T+1 per piece: tile sub-piece starts (direct mode)
+    uint32_t n, lists, dmin;
+    uint32_t direct;             // 1: tiles read their runs of the due rows (one delay)
+    const uint64_t *row_ptr;     // n + 1
+    const int2 *syn;             // {j << 24 | target, weight bits (fp32 or quantised int32)}
+    const RowDesc *desc;         // binned: n
+    const uint16_t *toff;        // direct: T + 1 per row
     const uint32_t *outdeg;      // n
     float *V;                    // n
     uint8_t *ref;                // n
-    uint32_t *ring;              // ring_slots * 8 * Gw spike IDs, list (slot, group)
-    uint32_t *ring_count;        // ring_slots * 8 counters (padded)
+    // spike lists: one segment of W IDs per (slot, tile) and its count
+    uint32_t spk_slots;
+    uint32_t *spk_ids;           // spk_slots * T * W
+    uint32_t *spk_cnt;           // spk_slots * T
     uint32_t *counts8;           // max_steps * 8
     uint64_t *events8;           // max_steps * 8: events emitted per group
     uint64_t *delivered8;        // max_steps * 8: events delivered per group
-    int2 *bins;                  // T * bin_cap records {local target, weight bits}
-    uint32_t *bin_fill;          // T counters (padded)
-    uint64_t bin_cap;
-    void *acc_ovf;               // n accumulators for bin overflow (int64 or int32)
-    uint32_t *ovf_flag;          // T
+    // binned delivery: pages of {local target, weight bits} records, one per
+    // (group x, push block g1, arrival slot, tile of the group), each owned by
+    // its push block; fill counters in the same order
+    int2 *pages;
+    uint32_t *pfill;
+    uint32_t page_cap;           // records per page
+    uint32_t pslots;             // arrival slots (delay_max)
+    uint32_t pg1;                // push blocks per group
+    void *acc_ovf;               // pslots * T * W accumulators for page overflow (int64 or int32)
+    uint32_t *ovf_flag;          // pslots * T
     const uint64_t *pois;        // pois_len thresholds
-    uint32_t *flags;             // bit 0: spike-list overflow, bit 1: raster overflow
+    const uint16_t *pois_guide;  // 256: first k with T_k > b * 2^24
+    uint32_t *flags;             // bit 1: raster overflow
     uint32_t *raster;
     uint64_t *raster_offs;       // max_steps + 1
     uint64_t raster_cap;
     const uint64_t *t_base;      // device step counter (steps completed before this batch)
-    // delivery selection
-    uint32_t list_lo, list_hi;   // delay lists delivered
-    const uint32_t *dbg_spikes;  // non-null: deliver this list instead of the ring
-    const uint32_t *dbg_count;
-    void *dbg_out;               // debug: per-neuron input (fp32 or int32), no update
-    uint32_t bin_chunk;          // pieces per binning chunk
+    // debug delivery: deliver this spike list (only delay index dbg_j, or
+    // every delay when dbg_j < 0) into dbg_out, no update
+    const uint32_t *dbg_spikes;
+    uint32_t dbg_n;
+    int32_t dbg_j;
+    void *dbg_out;
 };
 
 // spk_gen.hip -- connectivity expansion
 hipError_t gen_count_rows(const ConnArgs &c, uint32_t *cnt, hipStream_t s);
-hipError_t gen_fill_rows(const ConnArgs &c, const uint64_t *row_ptr, int2 *syn, hipStream_t s);
+hipError_t gen_fill_rows(const ConnArgs &c, const uint64_t *row_ptr, int2 *syn, RowIndex ix,
+                         hipStream_t s);
 hipError_t gen_in_count(const ConnArgs &c, uint32_t *cnt, hipStream_t s);
 hipError_t gen_in_fill(const ConnArgs &c, const uint64_t *row_ptr, uint32_t *cursor, int2 *syn,
                        hipStream_t s);
-hipError_t csr_count(const ConnArgs &c, const uint64_t *in_ptr, const uint8_t *in_delay,
-                     uint32_t *cnt, hipStream_t s);
-hipError_t csr_fill(const ConnArgs &c, const uint64_t *in_ptr, const uint32_t *in_col,
-                    const float *in_w, const uint8_t *in_delay, const uint64_t *row_ptr,
-                    int2 *syn, hipStream_t s);
+hipError_t csr_fill(const ConnArgs &c, uint64_t nnz, const uint32_t *in_col, const float *in_w,
+                    const uint8_t *in_delay, int2 *syn, hipStream_t s);
+hipError_t bucket_rows(const ConnArgs &c, const uint64_t *row_ptr, const int2 *src, int2 *dst,
+                       RowIndex ix, hipStream_t s);
 hipError_t scan_counts(const uint32_t *cnt, uint64_t m, uint64_t *out, uint64_t *block_sums,
-                       uint32_t *max_piece, hipStream_t s);
+                       uint32_t *max_count, hipStream_t s);
 size_t scan_scratch_elems(uint64_t m);
-hipError_t sort_small_pieces(const uint64_t *row_ptr, int2 *syn, uint64_t m, uint32_t *large,
-                             uint32_t *n_large, hipStream_t s);
-hipError_t sort_large_pieces(const uint64_t *row_ptr, int2 *syn, const uint32_t *large,
-                             uint32_t n_large, uint32_t pow2, hipStream_t s);
-hipError_t piece_offsets(const uint64_t *row_ptr, const int2 *syn, uint64_t pieces, uint32_t bounds,
-                         uint32_t width, uint16_t *off, uint32_t *max_sub, hipStream_t s);
-hipError_t out_degree(const uint64_t *row_ptr, uint32_t n, uint32_t lists, uint32_t *outdeg,
-                      hipStream_t s);
+hipError_t out_degree(const uint64_t *row_ptr, uint32_t n, uint32_t *outdeg, hipStream_t s);
 hipError_t in_abs_sum(const int2 *syn, uint64_t nnz, bool fixed, uint64_t *insum, hipStream_t s);
 hipError_t max_u64(const uint64_t *x, uint64_t m, uint64_t *out, hipStream_t s);
 hipError_t init_state(const ModelArgs &m, float v0_lo, float v0_hi, float *V, uint8_t *ref,
                       hipStream_t s);
-hipError_t export_lens(const uint64_t *row_ptr, uint32_t n, uint32_t lists, const uint32_t *rows,
-                       uint64_t n_rows, uint64_t *lens, hipStream_t s);
-hipError_t export_gather(const uint64_t *row_ptr, const int2 *syn, uint32_t n, uint32_t lists,
-                         uint32_t dmin, const uint32_t *rows, uint64_t n_rows,
-                         const uint64_t *piece_off, uint32_t *col, uint32_t *wbits,
+hipError_t export_gather(const uint64_t *row_ptr, const int2 *syn, uint32_t dmin, const uint32_t *rows,
+                         uint64_t n_rows, const uint64_t *out_off, uint32_t *col, uint32_t *wbits,
                          uint8_t *delay, hipStream_t s);
 int cu_count();
 
-// spk_step.hip -- one simulation step = [bin] + tile (+ record); i = step
+// spk_step.hip -- one simulation step = tile (+ push) (+ record); i = step
 // index inside the current batch (t = *t_base + i), or explicit t when
 // t_explicit >= 0.
-hipError_t launch_bin(const StepArgs &a, uint32_t i, int64_t t_explicit, hipStream_t s);
 hipError_t launch_tile(const StepArgs &a, uint32_t i, int64_t t_explicit, hipStream_t s);
+hipError_t launch_push(const StepArgs &a, uint32_t i, int64_t t_explicit, hipStream_t s);
 hipError_t launch_record(const StepArgs &a, uint32_t i, int64_t t_explicit, hipStream_t s);
 hipError_t launch_advance(uint64_t *t_base, uint32_t steps, hipStream_t s);
 hipError_t stream_copy(const void *src, void *dst, uint64_t bytes, hipStream_t s);
-uint32_t bin_grid();
+uint32_t push_blocks_per_group();
 
 }  // namespace spk

@@ -2,12 +2,15 @@
 //
 // A network owns its device memory and orders all work on one HIP stream.
 // Creation expands the connectivity parameters on the GPU (paper Sec. III-B:
-// the layout description is expanded on the device), into one adjacency list
-// per distinct delay (Sec. V), each row sorted by target (Sec. III-A), and
-// precomputes where every row crosses the target-tile boundaries.  A step is
-// [bin kernel] + tile kernel (+ raster record); batches of steps are captured
-// once into a HIP graph and replayed.  Spike counts stay on the device, so
-// stepping never waits for the host.
+// the layout description is expanded on the device) into one row per source
+// neuron, grouped by target tile (Sec. III-A keeps rows sorted by target),
+// with each synapse carrying its delay (Sec. V), and records where every row
+// crosses the tile or XCD-group boundaries.  A step is the tile kernel
+// (delivery into LDS + update + spike list), then for binned delivery the
+// push kernel (the new spikes' events into per-arrival pages), then the
+// optional raster record; batches of steps are captured once into a HIP
+// graph and replayed.  Spike counts stay on the device, so stepping never
+// waits for the host.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -47,11 +50,10 @@ spk_status fail(spk_status st, const std::string &msg)
         if (s_ != SPK_OK) return s_;    \
     } while (0)
 
-constexpr uint32_t kMaxPiece = 16384;  // longest (source, delay) run the sorter accepts
 constexpr uint32_t kPoisCap = 256;
-constexpr uint32_t kBatch = 32;        // steps per captured graph
-constexpr uint32_t kChunkEvents = 4096;
-constexpr uint64_t kBinBudget = 96ull << 20;  // bin records across all tiles
+constexpr uint32_t kBatch = 32;                    // steps per captured graph
+constexpr uint64_t kPageBudget = 256ull << 20;     // page records across all pages (2 GiB)
+constexpr uint64_t kDebugPageCap = 4096;           // records per page for spk_debug_deliver
 
 uint64_t prob_threshold(double p)
 {
@@ -80,6 +82,21 @@ int poisson_thresholds(double lambda, std::vector<uint64_t> &thr)
     }
 }
 
+// Guide table of the indexed search (Chen & Asau 1974): for the 256 ranges of
+// the top 8 bits of the draw, the first k whose threshold exceeds the range
+// start; the search for K = min{k : h < T_k} starts there.
+std::vector<uint16_t> poisson_guide(const std::vector<uint64_t> &thr)
+{
+    std::vector<uint16_t> g(256, 0);
+    uint32_t k = 0;
+    for (uint32_t b = 0; b < 256; b++) {
+        const uint64_t lo = (uint64_t)b << 24;
+        while (k + 1 < thr.size() && thr[k] <= lo) k++;
+        g[b] = (uint16_t)k;
+    }
+    return g;
+}
+
 bool quantise(float w, int S, int32_t *out)
 {
     const float x = std::rint(std::ldexp(w, S));
@@ -96,7 +113,7 @@ Tiling make_tiling(uint32_t n)
     uint32_t max_t8 = 32;
     if (const char *e = std::getenv("SPK_TILES_PER_XCD")) {
         const long v = std::strtol(e, nullptr, 10);
-        if (v >= 1 && v <= 256) max_t8 = (uint32_t)v;
+        if (v >= 1 && v <= (long)kMaxT8) max_t8 = (uint32_t)v;
     }
     Tiling tl{};
     uint32_t W = 64, logW = 6;
@@ -117,35 +134,36 @@ Tiling make_tiling(uint32_t n)
 struct spk_net {
     spk_params P{};
     // derived constants
-    uint32_t n = 0, n_exc = 0, lists = 1, dmin = 1, ring = 3, ref_steps = 0;
-    uint32_t pois_len = 0, max_piece = 0;
+    uint32_t n = 0, n_exc = 0, lists = 1, dmin = 1, dmax = 1, ref_steps = 0;
+    uint32_t pois_len = 0, max_row = 0;
     float k = 0.f;
     uint64_t conn_thr = 0, src_thr = 0, nnz = 0;
     int32_t ext_wq = 0, bias_q = 0, shift64 = 0;
     Keys keys{};
     std::vector<uint64_t> pois;
+    std::vector<uint16_t> guide;
     Tiling tl{};
     bool direct = false;
-    uint32_t bin_chunk = 1;
-    uint64_t bin_cap = 0;
+    uint32_t spk_slots = 1, pslots = 1, pg1 = 1, page_cap = 0;
     // device
     hipStream_t stream = nullptr, cap_stream = nullptr;
     bool own_stream = false;
     int device = 0;
     uint64_t *row_ptr = nullptr;
     int2 *syn = nullptr;
-    uint16_t *goff = nullptr, *toff = nullptr;
+    RowDesc *desc = nullptr;
+    uint16_t *toff = nullptr;
     uint32_t *outdeg = nullptr;
     float *V = nullptr;
     uint8_t *ref = nullptr;
-    uint32_t *ring_buf = nullptr, *ring_count = nullptr, *counts8 = nullptr, *flags = nullptr;
+    uint32_t *spk_ids = nullptr, *spk_cnt = nullptr, *counts8 = nullptr, *flags = nullptr;
     uint64_t *events8 = nullptr, *delivered8 = nullptr, *pois_dev = nullptr, *t_base = nullptr;
-    int2 *bins = nullptr;
-    uint32_t *bin_fill = nullptr, *ovf_flag = nullptr;
+    uint16_t *guide_dev = nullptr;
+    int2 *pages = nullptr;
+    uint32_t *pfill = nullptr, *ovf_flag = nullptr;
     void *acc_ovf = nullptr;
     uint32_t *raster = nullptr;
     uint64_t *raster_offs = nullptr;
-    uint32_t *dbg_count = nullptr;
     void *dbg_out = nullptr;
     uint64_t t = 0;
     uint64_t device_bytes = 0;
@@ -154,8 +172,8 @@ struct spk_net {
     // profiling
     bool profiling = false;
     std::vector<hipEvent_t> ev_free;
-    std::vector<std::pair<hipEvent_t, hipEvent_t>> ev_bin, ev_tile;
-    double ms_bin = 0, ms_tile = 0;
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> ev_push, ev_tile;
+    double ms_push = 0, ms_tile = 0;
     uint64_t launches = 0;
 };
 
@@ -216,34 +234,35 @@ StepArgs step_args(const spk_net *net)
     a.n = net->n;
     a.lists = net->lists;
     a.dmin = net->dmin;
-    a.ring_slots = net->ring;
     a.direct = net->direct ? 1u : 0u;
     a.row_ptr = net->row_ptr;
     a.syn = net->syn;
-    a.goff = net->goff;
+    a.desc = net->desc;
     a.toff = net->toff;
     a.outdeg = net->outdeg;
     a.V = net->V;
     a.ref = net->ref;
-    a.ring = net->ring_buf;
-    a.ring_count = net->ring_count;
+    a.spk_slots = net->spk_slots;
+    a.spk_ids = net->spk_ids;
+    a.spk_cnt = net->spk_cnt;
     a.counts8 = net->counts8;
     a.events8 = net->events8;
     a.delivered8 = net->delivered8;
-    a.bins = net->bins;
-    a.bin_fill = net->bin_fill;
-    a.bin_cap = net->bin_cap;
+    a.pages = net->pages;
+    a.pfill = net->pfill;
+    a.page_cap = net->page_cap;
+    a.pslots = net->pslots;
+    a.pg1 = net->pg1;
     a.acc_ovf = net->acc_ovf;
     a.ovf_flag = net->ovf_flag;
     a.pois = net->pois_dev;
+    a.pois_guide = net->guide_dev;
     a.flags = net->flags;
     a.raster = net->raster;
     a.raster_offs = net->raster_offs;
     a.raster_cap = net->P.raster_capacity;
     a.t_base = net->t_base;
-    a.list_lo = 0;
-    a.list_hi = net->lists;
-    a.bin_chunk = net->bin_chunk;
+    a.dbg_j = -1;
     return a;
 }
 
@@ -267,6 +286,7 @@ ConnArgs conn_args(const spk_net *net)
     c.fixed = net->P.acc_mode == SPK_ACC_FIXED;
     c.qscale = std::ldexp(1.0f, net->P.fixed_shift);
     c.keys = net->keys;
+    c.tl = net->tl;
     return c;
 }
 
@@ -275,7 +295,8 @@ spk_status derive(spk_net *net, bool explicit_csr)
 {
     const spk_params &P = net->P;
     if (P.abi_version != SPK_ABI_VERSION) return fail(SPK_EINVAL, "abi_version mismatch");
-    if (P.n == 0 || P.n > 2000000000u) return fail(SPK_EINVAL, "n must be in [1, 2e9]");
+    if (P.n == 0 || P.n > (1u << kTargetBits))
+        return fail(SPK_EINVAL, "n must be in [1, 2^24]");
     if (!(P.dt_ms > 0.0) || !(P.tau_m_ms > 0.0) || !(P.t_ref_ms >= 0.0))
         return fail(SPK_EINVAL, "dt_ms, tau_m_ms must be > 0 and t_ref_ms >= 0");
     if (P.delay_min < 1 || P.delay_max < P.delay_min || P.delay_max > 253)
@@ -290,6 +311,8 @@ spk_status derive(spk_net *net, bool explicit_csr)
     if (!(P.p >= 0.0 && P.p <= 1.0)) return fail(SPK_EINVAL, "p in [0,1]");
     if (P.max_steps == 0) return fail(SPK_EINVAL, "max_steps must be >= 1");
     if (!(P.ext_lambda >= 0.0) || P.ext_lambda > 100.0) return fail(SPK_EINVAL, "ext_lambda in [0,100]");
+    if (!explicit_csr && P.conn_kind == SPK_CONN_FIXED_OUT && P.k_out > kMaxRow)
+        return fail(SPK_EINVAL, "k_out exceeds the longest supported row (65535)");
     net->n = P.n;
     net->n_exc = (uint32_t)std::llround(P.frac_exc * (double)P.n);
     net->k = (float)(P.dt_ms / P.tau_m_ms);
@@ -297,10 +320,8 @@ spk_status derive(spk_net *net, bool explicit_csr)
     if (rs < 0 || rs > 255) return fail(SPK_EINVAL, "t_ref/dt must round to 0..255 steps");
     net->ref_steps = (uint32_t)rs;
     net->dmin = P.delay_min;
+    net->dmax = P.delay_max;
     net->lists = P.delay_max - P.delay_min + 1;
-    // dmax + 2 slots: the slot written at step t is neither read at t nor
-    // at t - 1, so it can be cleared one step ahead
-    net->ring = P.delay_max + 2;
     net->conn_thr = prob_threshold(P.p);
     net->src_thr = prob_threshold(P.src_rate_hz * P.dt_ms * 1e-3);
     net->tl = make_tiling(P.n);
@@ -311,6 +332,7 @@ spk_status derive(spk_net *net, bool explicit_csr)
         const int L = poisson_thresholds(P.ext_lambda, net->pois);
         if (L < 0) return fail(SPK_EINVAL, "ext_lambda");
         net->pois_len = (uint32_t)L;
+        net->guide = poisson_guide(net->pois);
     }
     if (P.acc_mode == SPK_ACC_FIXED) {
         if (P.fixed_shift < 0 || P.fixed_shift > 30) return fail(SPK_EINVAL, "fixed_shift in 0..30");
@@ -347,90 +369,69 @@ spk_status setup_stream(spk_net *net, void *stream)
     return SPK_OK;
 }
 
-// After the piece counts are known: offsets, synapse storage.
-spk_status finish_counts(spk_net *net, uint32_t *cnt, uint64_t pieces)
+// Row offsets from per-row counts.
+spk_status finish_counts(spk_net *net, const uint32_t *cnt)
 {
     hipStream_t s = net->stream;
+    const uint64_t n = net->n;
     uint64_t *bsum = nullptr;
     uint32_t *maxp = nullptr;
-    SPK_TRY(dalloc(net, &net->row_ptr, pieces + 1));
-    SPK_TRY(dalloc(net, &bsum, scan_scratch_elems(pieces) + 1));
+    SPK_TRY(dalloc(net, &net->row_ptr, n + 1));
+    SPK_TRY(dalloc(net, &bsum, scan_scratch_elems(n) + 1));
     SPK_TRY(dalloc(net, &maxp, 1));
     SPK_HIP(hipMemsetAsync(maxp, 0, 4, s));
-    SPK_HIP(scan_counts(cnt, pieces, net->row_ptr, bsum, maxp, s));
+    SPK_HIP(scan_counts(cnt, n, net->row_ptr, bsum, maxp, s));
     uint64_t nnz = 0;
-    uint32_t mp = 0;
-    SPK_HIP(hipMemcpyAsync(&nnz, net->row_ptr + pieces, 8, hipMemcpyDeviceToHost, s));
-    SPK_HIP(hipMemcpyAsync(&mp, maxp, 4, hipMemcpyDeviceToHost, s));
+    uint32_t mr = 0;
+    SPK_HIP(hipMemcpyAsync(&nnz, net->row_ptr + n, 8, hipMemcpyDeviceToHost, s));
+    SPK_HIP(hipMemcpyAsync(&mr, maxp, 4, hipMemcpyDeviceToHost, s));
     SPK_HIP(hipStreamSynchronize(s));
     dfree(net, bsum);
     dfree(net, maxp);
     net->nnz = nnz;
-    net->max_piece = mp;
-    if (mp > kMaxPiece)
-        return fail(SPK_EINVAL, "a (source, delay) synapse run of " + std::to_string(mp) +
-                                    " exceeds the supported " + std::to_string(kMaxPiece));
-    SPK_TRY(dalloc(net, &net->syn, nnz));
+    net->max_row = mr;
     return SPK_OK;
 }
 
-// Sort every piece by (target, weight bits); tile/group offsets; out-degrees;
-// accumulator ranges; delivery strategy and its buffers.
-spk_status finish_pieces(spk_net *net, uint64_t pieces)
+// Delivery strategy and the row index it needs.  Direct: every tile reads
+// its run of each due row (rows long compared with the tile count, one
+// delay, offsets small next to the synapses).  Binned: the push kernel sorts
+// each fired row's events by (arrival step, tile) into pages.
+spk_status choose_delivery(spk_net *net, RowIndex *ix)
+{
+    if (net->max_row > kMaxRow)
+        return fail(SPK_EINVAL, "a source row of " + std::to_string(net->max_row) +
+                                    " synapses exceeds the supported " + std::to_string(kMaxRow));
+    const Tiling &tl = net->tl;
+    const double mean_row = (double)net->nnz / (double)net->n;
+    const double toff_bytes = (double)net->n * (tl.T + 1) * 2.0;
+    const bool binned_ok = (uint64_t)net->lists * tl.T8 <= kMaxBuckets;
+    bool direct = net->lists == 1 && mean_row >= 2.0 * tl.T && toff_bytes <= 0.5 * 8.0 * (double)net->nnz;
+    if (!binned_ok || net->P.delivery == SPK_DELIVERY_DIRECT) direct = true;
+    if (net->P.delivery == SPK_DELIVERY_BINNED) {
+        if (!binned_ok)
+            return fail(SPK_EINVAL, "binned delivery supports at most 4096 (delay, tile) buckets per "
+                                    "XCD group; use fewer delays or direct delivery");
+        direct = false;
+    }
+    net->direct = direct;
+    *ix = RowIndex{};
+    if (direct) {
+        SPK_TRY(dalloc(net, &net->toff, (size_t)net->n * (tl.T + 1)));
+        ix->toff = net->toff;
+    } else {
+        SPK_TRY(dalloc(net, &net->desc, net->n));
+        ix->desc = net->desc;
+    }
+    return SPK_OK;
+}
+
+// Out-degrees, accumulator range, delivery buffers.
+spk_status finish_rows(spk_net *net)
 {
     hipStream_t s = net->stream;
-    uint32_t *large = nullptr, *n_large = nullptr;
-    SPK_TRY(dalloc(net, &n_large, 1));
-    SPK_HIP(hipMemsetAsync(n_large, 0, 4, s));
-    const uint64_t max_large = std::min<uint64_t>(pieces, net->nnz / 257 + 1);
-    SPK_TRY(dalloc(net, &large, max_large));
-    SPK_HIP(sort_small_pieces(net->row_ptr, net->syn, pieces, large, n_large, s));
-    uint32_t nl = 0;
-    SPK_HIP(hipMemcpyAsync(&nl, n_large, 4, hipMemcpyDeviceToHost, s));
-    SPK_HIP(hipStreamSynchronize(s));
-    if (nl > max_large) return fail(SPK_EHIP, "internal: large-piece list overflow");
-    uint32_t pow2 = 1;
-    while (pow2 < net->max_piece) pow2 <<= 1;
-    SPK_HIP(sort_large_pieces(net->row_ptr, net->syn, large, nl, pow2, s));
-    SPK_HIP(hipStreamSynchronize(s));
-    dfree(net, large);
-    dfree(net, n_large);
     SPK_TRY(dalloc(net, &net->outdeg, net->n));
-    SPK_HIP(out_degree(net->row_ptr, net->n, net->lists, net->outdeg, s));
-
-    // Delivery strategy: tiles read their own runs when rows are long
-    // compared with the tile count (and the offsets stay small), otherwise
-    // the due events are binned per tile first.
-    const Tiling &tl = net->tl;
-    const double mean_piece = pieces ? (double)net->nnz / (double)pieces : 0.0;
-    const double toff_bytes = (double)pieces * (tl.T + 1) * 2.0;
-    bool direct = mean_piece >= 2.0 * tl.T && toff_bytes <= 0.5 * 8.0 * (double)net->nnz;
-    if (net->P.delivery == SPK_DELIVERY_DIRECT) direct = true;
-    if (net->P.delivery == SPK_DELIVERY_BINNED) direct = false;
-    net->direct = direct;
-    uint32_t *maxs = nullptr;
-    SPK_TRY(dalloc(net, &maxs, 1));
-    SPK_HIP(hipMemsetAsync(maxs, 0, 4, s));
-    if (direct) {
-        SPK_TRY(dalloc(net, &net->toff, pieces * (tl.T + 1)));
-        SPK_HIP(piece_offsets(net->row_ptr, net->syn, pieces, tl.T + 1, tl.W, net->toff, maxs, s));
-    } else {
-        SPK_TRY(dalloc(net, &net->goff, pieces * kGroups));
-        SPK_HIP(piece_offsets(net->row_ptr, net->syn, pieces, kGroups, tl.Gw, net->goff, maxs, s));
-        // binning chunk: enough pieces for ~kChunkEvents events of one group
-        const double mean_sub = std::max(1.0, mean_piece / kGroups);
-        net->bin_chunk = (uint32_t)std::min(512.0, std::max(1.0, std::floor(kChunkEvents / mean_sub)));
-        net->bin_cap = std::max<uint64_t>(4096, std::min<uint64_t>(net->nnz, kBinBudget) / tl.T + 1);
-        SPK_TRY(dalloc(net, &net->bins, tl.T * net->bin_cap));
-        SPK_TRY(dalloc(net, &net->bin_fill, (size_t)tl.T * kPad));
-        SPK_TRY(dalloc(net, &net->ovf_flag, tl.T));
-        SPK_TRY(dalloc(net, (uint64_t **)&net->acc_ovf, (size_t)tl.T * tl.W));
-        SPK_HIP(hipMemsetAsync(net->bin_fill, 0, (size_t)tl.T * kPad * 4, s));
-        SPK_HIP(hipMemsetAsync(net->ovf_flag, 0, (size_t)tl.T * 4, s));
-        SPK_HIP(hipMemsetAsync(net->acc_ovf, 0, (size_t)tl.T * tl.W * 8, s));
-    }
-    SPK_HIP(hipStreamSynchronize(s));
-    dfree(net, maxs);
+    SPK_HIP(out_degree(net->row_ptr, net->n, net->outdeg, s));
 
     // Accumulator range.  Fixed mode: all in-synapses of one neuron at once,
     // plus the largest Poisson count and the bias, must fit in int32.  fp32
@@ -461,65 +462,107 @@ spk_status finish_pieces(spk_net *net, uint64_t pieces)
         const int e = M > 0.0 ? (int)std::ceil(std::log2(M)) : 0;
         net->shift64 = std::max(0, std::min(100, 52 - e));
     }
+
+    // Spike lists: direct delivery reads the lists of steps t - dmax .. t - dmin
+    // while writing that of t; binned delivery consumes the list of t within t.
+    const Tiling &tl = net->tl;
+    net->spk_slots = net->direct ? net->dmax + 1 : 1;
+    if (!net->direct) {
+        // Pages: (group, push block, arrival slot, tile).  A page never holds
+        // more than nnz records (each synapse arrives at most once per slot),
+        // so small networks never overflow; large ones get an equal share of
+        // the budget and fall back to global atomics beyond it.
+        net->pslots = net->dmax;
+        net->pg1 = push_blocks_per_group();
+        const uint64_t n_pages = (uint64_t)kGroups * net->pg1 * net->pslots * tl.T8;
+        uint64_t cap = std::min<uint64_t>(kPageBudget / n_pages, std::max<uint64_t>(net->nnz, 1));
+        if (const char *e = std::getenv("SPK_PAGE_CAP")) {
+            const long long v = std::strtoll(e, nullptr, 10);
+            if (v >= 1 && v <= (1ll << 30)) cap = (uint64_t)v;
+        }
+        cap = std::max<uint64_t>(16, (cap + 15) / 16 * 16);
+        net->page_cap = (uint32_t)cap;
+        const size_t acc_elems = (size_t)net->pslots * tl.T * tl.W;
+        SPK_TRY(dalloc(net, &net->pages, n_pages * cap));
+        SPK_TRY(dalloc(net, &net->pfill, n_pages));
+        SPK_TRY(dalloc(net, &net->ovf_flag, (size_t)net->pslots * tl.T));
+        SPK_TRY(dalloc(net, (uint64_t **)&net->acc_ovf, acc_elems));
+        SPK_HIP(hipMemsetAsync(net->pfill, 0, n_pages * 4, s));
+        SPK_HIP(hipMemsetAsync(net->ovf_flag, 0, (size_t)net->pslots * tl.T * 4, s));
+        SPK_HIP(hipMemsetAsync(net->acc_ovf, 0, acc_elems * 8, s));
+    }
+    SPK_HIP(hipStreamSynchronize(s));
     return SPK_OK;
 }
 
 spk_status generate(spk_net *net)
 {
     hipStream_t s = net->stream;
-    const uint64_t pieces = (uint64_t)net->lists * net->n;
     uint32_t *cnt = nullptr;
-    SPK_TRY(dalloc(net, &cnt, pieces));
-    SPK_HIP(hipMemsetAsync(cnt, 0, pieces * 4, s));
+    SPK_TRY(dalloc(net, &cnt, net->n));
+    SPK_HIP(hipMemsetAsync(cnt, 0, (size_t)net->n * 4, s));
     ConnArgs c = conn_args(net);
-    const uint32_t kind = net->P.conn_kind;
-    if (kind == SPK_CONN_FIXED_IN) SPK_HIP(gen_in_count(c, cnt, s));
+    const bool in_rows = net->P.conn_kind == SPK_CONN_FIXED_IN;
+    if (in_rows) SPK_HIP(gen_in_count(c, cnt, s));
     else SPK_HIP(gen_count_rows(c, cnt, s));
-    SPK_TRY(finish_counts(net, cnt, pieces));
-    if (kind == SPK_CONN_FIXED_IN) {
-        SPK_HIP(hipMemsetAsync(cnt, 0, pieces * 4, s));
-        SPK_HIP(gen_in_fill(c, net->row_ptr, cnt, net->syn, s));
-    } else {
-        SPK_HIP(gen_fill_rows(c, net->row_ptr, net->syn, s));
+    SPK_TRY(finish_counts(net, cnt));
+    RowIndex ix{};
+    SPK_TRY(choose_delivery(net, &ix));
+    SPK_TRY(dalloc(net, &net->syn, net->nnz));
+    if (in_rows) {  // drawn per target: regroup by source, then bucket
+        int2 *tmp = nullptr;
+        SPK_TRY(dalloc(net, &tmp, net->nnz));
+        SPK_HIP(hipMemsetAsync(cnt, 0, (size_t)net->n * 4, s));
+        SPK_HIP(gen_in_fill(c, net->row_ptr, cnt, tmp, s));
+        SPK_HIP(bucket_rows(c, net->row_ptr, tmp, net->syn, ix, s));
+        SPK_HIP(hipStreamSynchronize(s));
+        dfree(net, tmp);
+    } else {        // drawn per source, bucketed while drawn
+        SPK_HIP(gen_fill_rows(c, net->row_ptr, net->syn, ix, s));
     }
     SPK_HIP(hipStreamSynchronize(s));
     dfree(net, cnt);
-    return finish_pieces(net, pieces);
+    return finish_rows(net);
 }
 
-// State, spike ring and per-step records.
+// State, spike lists and per-step records.
 spk_status alloc_state(spk_net *net)
 {
     const uint32_t n = net->n;
     const uint64_t T = net->P.max_steps;
+    const Tiling &tl = net->tl;
     hipStream_t s = net->stream;
-    const uint64_t ring_ids = (uint64_t)net->ring * kGroups * net->tl.Gw;
+    const uint64_t segs = (uint64_t)net->spk_slots * tl.T;
     SPK_TRY(dalloc(net, &net->V, n));
     SPK_TRY(dalloc(net, &net->ref, n));
-    SPK_TRY(dalloc(net, &net->ring_buf, ring_ids));
-    SPK_TRY(dalloc(net, &net->ring_count, (size_t)net->ring * kGroups * kPad));
+    SPK_TRY(dalloc(net, &net->spk_ids, segs * tl.W));
+    SPK_TRY(dalloc(net, &net->spk_cnt, segs));
     SPK_TRY(dalloc(net, &net->counts8, T * kGroups));
     SPK_TRY(dalloc(net, &net->events8, T * kGroups));
     SPK_TRY(dalloc(net, &net->delivered8, T * kGroups));
     SPK_TRY(dalloc(net, &net->flags, 1));
-    SPK_TRY(dalloc(net, &net->dbg_count, 1));
     SPK_TRY(dalloc(net, (uint32_t **)&net->dbg_out, n));
     SPK_TRY(dalloc(net, &net->t_base, 1));
     SPK_TRY(dalloc(net, &net->raster_offs, T + 1));
     SPK_TRY(dalloc(net, &net->raster, net->P.raster_capacity));
     SPK_TRY(dalloc(net, &net->pois_dev, net->pois_len ? net->pois_len : 1));
-    SPK_HIP(hipMemsetAsync(net->ring_count, 0, (size_t)net->ring * kGroups * kPad * 4, s));
+    SPK_TRY(dalloc(net, &net->guide_dev, 256));
+    SPK_HIP(hipMemsetAsync(net->spk_cnt, 0, segs * 4, s));
     SPK_HIP(hipMemsetAsync(net->counts8, 0, T * kGroups * 4, s));
     SPK_HIP(hipMemsetAsync(net->events8, 0, T * kGroups * 8, s));
     SPK_HIP(hipMemsetAsync(net->delivered8, 0, T * kGroups * 8, s));
     SPK_HIP(hipMemsetAsync(net->flags, 0, 4, s));
     SPK_HIP(hipMemsetAsync(net->t_base, 0, 8, s));
     SPK_HIP(hipMemsetAsync(net->raster_offs, 0, (T + 1) * 8, s));
-    if (net->pois_len)
+    SPK_HIP(hipMemsetAsync(net->guide_dev, 0, 512, s));
+    if (net->pois_len) {
         SPK_HIP(hipMemcpyAsync(net->pois_dev, net->pois.data(), net->pois_len * 8,
                                hipMemcpyHostToDevice, s));
+        SPK_HIP(hipMemcpyAsync(net->guide_dev, net->guide.data(), 512, hipMemcpyHostToDevice, s));
+    }
     ModelArgs m = model_args(net);
     SPK_HIP(init_state(m, net->P.v0_lo, net->P.v0_hi, net->V, net->ref, s));
+    SPK_HIP(hipStreamSynchronize(s));  // host tables above are stack/vector memory
     return SPK_OK;
 }
 
@@ -535,7 +578,6 @@ spk_status sync_flags(spk_net *net, uint32_t *flags_out)
     uint32_t f = 0;
     SPK_HIP(hipMemcpy(&f, net->flags, 4, hipMemcpyDeviceToHost));
     if (flags_out) *flags_out = f;
-    if (f & 1u) return fail(SPK_EOVERFLOW, "spike list overflow");
     return SPK_OK;
 }
 
@@ -543,8 +585,8 @@ spk_status collect_profile(spk_net *net)
 {
     SPK_HIP(hipStreamSynchronize(net->stream));
     for (int which = 0; which < 2; which++) {
-        auto &v = which ? net->ev_tile : net->ev_bin;
-        double &acc = which ? net->ms_tile : net->ms_bin;
+        auto &v = which ? net->ev_tile : net->ev_push;
+        double &acc = which ? net->ms_tile : net->ms_push;
         for (auto &pr : v) {
             float ms = 0;
             SPK_HIP(hipEventElapsedTime(&ms, pr.first, pr.second));
@@ -571,8 +613,8 @@ spk_status get_event(spk_net *net, hipEvent_t *e)
 // One step's kernels on stream s (step i of a batch, or explicit t).
 spk_status enqueue_step(spk_net *net, const StepArgs &a, hipStream_t s, uint32_t i, int64_t t_explicit)
 {
-    if (!net->direct) SPK_HIP(launch_bin(a, i, t_explicit, s));
     SPK_HIP(launch_tile(a, i, t_explicit, s));
+    if (!net->direct) SPK_HIP(launch_push(a, i, t_explicit, s));
     if (net->P.raster_capacity) SPK_HIP(launch_record(a, i, t_explicit, s));
     return SPK_OK;
 }
@@ -613,7 +655,7 @@ void destroy_net(spk_net *net)
     if (!net) return;
     if (net->stream) (void)hipStreamSynchronize(net->stream);
     for (auto &kv : net->graphs) (void)hipGraphExecDestroy(kv.second);
-    for (auto *v : {&net->ev_bin, &net->ev_tile})
+    for (auto *v : {&net->ev_push, &net->ev_tile})
         for (auto &pr : *v) {
             (void)hipEventDestroy(pr.first);
             (void)hipEventDestroy(pr.second);
@@ -627,6 +669,7 @@ void destroy_net(spk_net *net)
 
 spk_status read_groups(spk_net *net, const void *dev, size_t elem, uint64_t t0, uint64_t n, void *out)
 {
+    (void)net;
     std::vector<uint8_t> buf(n * kGroups * elem);
     if (n) SPK_HIP(hipMemcpy(buf.data(), (const uint8_t *)dev + t0 * kGroups * elem, buf.size(),
                              hipMemcpyDeviceToHost));
@@ -755,8 +798,11 @@ spk_status spk_create_from_csr(const spk_params *params, uint32_t n, const uint6
     auto run = [&]() -> spk_status {
         SPK_TRY(derive(net, true));
         if (row_ptr[0] != 0) return fail(SPK_EINVAL, "row_ptr[0] must be 0");
-        for (uint32_t s = 0; s < n; s++)
+        uint64_t max_row = 0;
+        for (uint32_t s = 0; s < n; s++) {
             if (row_ptr[s + 1] < row_ptr[s]) return fail(SPK_EINVAL, "row_ptr not monotone");
+            max_row = std::max<uint64_t>(max_row, row_ptr[s + 1] - row_ptr[s]);
+        }
         const uint64_t nnz = row_ptr[n];
         for (uint64_t e = 0; e < nnz; e++) {
             if (col[e] >= n) return fail(SPK_EINVAL, "target id out of range");
@@ -769,16 +815,22 @@ spk_status spk_create_from_csr(const spk_params *params, uint32_t n, const uint6
                     return fail(SPK_EOVERFLOW, "a weight does not fit int32 at this fixed_shift");
             }
         }
+        net->nnz = nnz;
+        net->max_row = (uint32_t)std::min<uint64_t>(max_row, 0xffffffffull);
         SPK_TRY(setup_stream(net, stream));
         hipStream_t s = net->stream;
-        uint64_t *in_ptr = nullptr;
+        RowIndex ix{};
+        SPK_TRY(choose_delivery(net, &ix));
         uint32_t *in_col = nullptr;
         float *in_w = nullptr;
         uint8_t *in_d = nullptr;
-        SPK_TRY(dalloc(net, &in_ptr, (size_t)n + 1));
+        int2 *tmp = nullptr;
+        SPK_TRY(dalloc(net, &net->row_ptr, (size_t)n + 1));
+        SPK_TRY(dalloc(net, &net->syn, nnz));
+        SPK_TRY(dalloc(net, &tmp, nnz));
         SPK_TRY(dalloc(net, &in_col, nnz));
         SPK_TRY(dalloc(net, &in_w, nnz));
-        SPK_HIP(hipMemcpyAsync(in_ptr, row_ptr, ((size_t)n + 1) * 8, hipMemcpyHostToDevice, s));
+        SPK_HIP(hipMemcpyAsync(net->row_ptr, row_ptr, ((size_t)n + 1) * 8, hipMemcpyHostToDevice, s));
         if (nnz) {
             SPK_HIP(hipMemcpyAsync(in_col, col, nnz * 4, hipMemcpyHostToDevice, s));
             SPK_HIP(hipMemcpyAsync(in_w, w, nnz * 4, hipMemcpyHostToDevice, s));
@@ -787,21 +839,15 @@ spk_status spk_create_from_csr(const spk_params *params, uint32_t n, const uint6
             SPK_TRY(dalloc(net, &in_d, nnz));
             if (nnz) SPK_HIP(hipMemcpyAsync(in_d, delay, nnz, hipMemcpyHostToDevice, s));
         }
-        const uint64_t pieces = (uint64_t)net->lists * n;
-        uint32_t *cnt = nullptr;
-        SPK_TRY(dalloc(net, &cnt, pieces));
-        SPK_HIP(hipMemsetAsync(cnt, 0, pieces * 4, s));
         ConnArgs c = conn_args(net);
-        SPK_HIP(csr_count(c, in_ptr, in_d, cnt, s));
-        SPK_TRY(finish_counts(net, cnt, pieces));
-        SPK_HIP(csr_fill(c, in_ptr, in_col, in_w, in_d, net->row_ptr, net->syn, s));
+        SPK_HIP(csr_fill(c, nnz, in_col, in_w, in_d, tmp, s));
+        SPK_HIP(bucket_rows(c, net->row_ptr, tmp, net->syn, ix, s));
         SPK_HIP(hipStreamSynchronize(s));
-        dfree(net, cnt);
-        dfree(net, in_ptr);
+        dfree(net, tmp);
         dfree(net, in_col);
         dfree(net, in_w);
         dfree(net, in_d);
-        SPK_TRY(finish_pieces(net, pieces));
+        SPK_TRY(finish_rows(net));
         SPK_TRY(alloc_state(net));
         return sync_flags(net, nullptr);
     };
@@ -829,21 +875,18 @@ spk_status spk_step(spk_net *net, uint64_t n_steps)
             hipEvent_t e0 = nullptr, e1 = nullptr, e2 = nullptr, e3 = nullptr;
             SPK_TRY(get_event(net, &e0));
             SPK_TRY(get_event(net, &e1));
-            SPK_TRY(get_event(net, &e2));
-            SPK_TRY(get_event(net, &e3));
-            if (!net->direct) {
-                SPK_HIP(hipEventRecord(e0, s));
-                SPK_HIP(launch_bin(a, 0, t, s));
-                SPK_HIP(hipEventRecord(e1, s));
-                net->ev_bin.push_back({e0, e1});
-            } else {
-                net->ev_free.push_back(e0);
-                net->ev_free.push_back(e1);
-            }
-            SPK_HIP(hipEventRecord(e2, s));
+            SPK_HIP(hipEventRecord(e0, s));
             SPK_HIP(launch_tile(a, 0, t, s));
-            SPK_HIP(hipEventRecord(e3, s));
-            net->ev_tile.push_back({e2, e3});
+            SPK_HIP(hipEventRecord(e1, s));
+            net->ev_tile.push_back({e0, e1});
+            if (!net->direct) {
+                SPK_TRY(get_event(net, &e2));
+                SPK_TRY(get_event(net, &e3));
+                SPK_HIP(hipEventRecord(e2, s));
+                SPK_HIP(launch_push(a, 0, t, s));
+                SPK_HIP(hipEventRecord(e3, s));
+                net->ev_push.push_back({e2, e3});
+            }
             if (net->P.raster_capacity) SPK_HIP(launch_record(a, 0, t, s));
             net->launches++;
         }
@@ -933,26 +976,46 @@ spk_status spk_debug_deliver(spk_net *net, const uint32_t *spikes, uint64_t n_sp
         if (spikes[k] >= net->n) return fail(SPK_EINVAL, "spike id out of range");
     if (delay && (delay < net->dmin || delay >= net->dmin + net->lists))
         return fail(SPK_EINVAL, "delay not in [delay_min, delay_max]");
-    const uint32_t nl = delay ? 1u : net->lists;
-    if ((uint64_t)n_spikes * nl > 0xffffffffull) return fail(SPK_EINVAL, "too many spikes");
     hipStream_t s = net->stream;
     SPK_TRY(sync_flags(net, nullptr));
-    uint32_t *d_sp = nullptr;
-    SPK_TRY(dalloc(net, &d_sp, n_spikes));
-    const uint32_t cnt = (uint32_t)n_spikes;
+    const Tiling &tl = net->tl;
+    // scratch: the spike list, and for binned delivery pages of one arrival
+    // slot with their fill counters and overflow accumulators, so that the
+    // network's own pages (events in flight) are left untouched
+    std::vector<void *> tmp;
+    auto scratch = [&](void **p, size_t bytes) -> spk_status {
+        uint8_t *q = nullptr;
+        SPK_TRY(dalloc(net, &q, bytes));
+        tmp.push_back(q);
+        *p = q;
+        return SPK_OK;
+    };
     spk_status st = SPK_OK;
     do {
+        uint32_t *d_sp = nullptr;
+        if ((st = scratch((void **)&d_sp, n_spikes * 4 + 4)) != SPK_OK) break;
+        StepArgs a = step_args(net);
+        a.dbg_spikes = d_sp;
+        a.dbg_n = (uint32_t)n_spikes;
+        a.dbg_j = delay ? (int32_t)(delay - net->dmin) : -1;
+        a.dbg_out = net->dbg_out;
         hipError_t e = hipSuccess;
         if (n_spikes) e = hipMemcpyAsync(d_sp, spikes, n_spikes * 4, hipMemcpyHostToDevice, s);
-        if (e == hipSuccess) e = hipMemcpyAsync(net->dbg_count, &cnt, 4, hipMemcpyHostToDevice, s);
-        if (e != hipSuccess) { st = fail(SPK_EHIP, hipGetErrorString(e)); break; }
-        StepArgs a = step_args(net);
-        a.list_lo = delay ? delay - net->dmin : 0;
-        a.list_hi = a.list_lo + nl;
-        a.dbg_spikes = d_sp;
-        a.dbg_count = net->dbg_count;
-        a.dbg_out = net->dbg_out;
-        if (!net->direct) e = launch_bin(a, 0, 0, s);
+        if (e == hipSuccess && !net->direct) {
+            const uint64_t n_pages = (uint64_t)kGroups * net->pg1 * tl.T8;
+            const uint64_t cap = std::min<uint64_t>(kDebugPageCap, std::max<uint64_t>(16, net->page_cap));
+            const size_t acc_elems = (size_t)tl.T * tl.W;
+            if ((st = scratch((void **)&a.pages, n_pages * cap * 8)) != SPK_OK) break;
+            if ((st = scratch((void **)&a.pfill, n_pages * 4)) != SPK_OK) break;
+            if ((st = scratch((void **)&a.ovf_flag, (size_t)tl.T * 4)) != SPK_OK) break;
+            if ((st = scratch(&a.acc_ovf, acc_elems * 8)) != SPK_OK) break;
+            a.page_cap = (uint32_t)cap;
+            a.pslots = 1;
+            e = hipMemsetAsync(a.pfill, 0, n_pages * 4, s);
+            if (e == hipSuccess) e = hipMemsetAsync(a.ovf_flag, 0, (size_t)tl.T * 4, s);
+            if (e == hipSuccess) e = hipMemsetAsync(a.acc_ovf, 0, acc_elems * 8, s);
+            if (e == hipSuccess) e = launch_push(a, 0, 0, s);
+        }
         if (e == hipSuccess) e = launch_tile(a, 0, 0, s);
         if (e == hipSuccess) e = hipStreamSynchronize(s);
         if (e == hipSuccess)
@@ -960,7 +1023,8 @@ spk_status spk_debug_deliver(spk_net *net, const uint32_t *spikes, uint64_t n_sp
                           (size_t)net->n * 4, hipMemcpyDeviceToHost);
         if (e != hipSuccess) st = fail(SPK_EHIP, hipGetErrorString(e));
     } while (0);
-    dfree(net, d_sp);
+    (void)hipStreamSynchronize(s);
+    for (void *p : tmp) dfree(net, p);
     return st;
 }
 
@@ -975,37 +1039,25 @@ spk_status spk_export_rows(spk_net *net, const uint32_t *rows, uint64_t n_rows, 
     offs[0] = 0;
     if (!n_rows) return SPK_OK;
     hipStream_t s = net->stream;
-    const uint64_t pieces = n_rows * net->lists;
-    uint32_t *d_rows = nullptr;
-    uint64_t *d_lens = nullptr, *d_off = nullptr;
-    SPK_TRY(dalloc(net, &d_rows, n_rows));
-    SPK_TRY(dalloc(net, &d_lens, pieces));
-    SPK_TRY(dalloc(net, &d_off, pieces));
-    std::vector<uint64_t> lens(pieces), poff(pieces);
-    SPK_HIP(hipMemcpyAsync(d_rows, rows, n_rows * 4, hipMemcpyHostToDevice, s));
-    SPK_HIP(export_lens(net->row_ptr, net->n, net->lists, d_rows, n_rows, d_lens, s));
-    SPK_HIP(hipMemcpyAsync(lens.data(), d_lens, pieces * 8, hipMemcpyDeviceToHost, s));
-    SPK_HIP(hipStreamSynchronize(s));
+    std::vector<uint32_t> deg(net->n);
+    SPK_HIP(hipMemcpy(deg.data(), net->outdeg, (size_t)net->n * 4, hipMemcpyDeviceToHost));
     uint64_t tot = 0;
     for (uint64_t r = 0; r < n_rows; r++) {
-        for (uint32_t j = 0; j < net->lists; j++) {
-            poff[r * net->lists + j] = tot;
-            tot += lens[r * net->lists + j];
-        }
+        tot += deg[rows[r]];
         offs[r + 1] = tot;
     }
-    if (tot > cap) {
-        dfree(net, d_rows); dfree(net, d_lens); dfree(net, d_off);
-        return fail(SPK_EOVERFLOW, "export buffers too small");
-    }
-    uint32_t *d_col = nullptr, *d_wb = nullptr;
+    if (tot > cap) return fail(SPK_EOVERFLOW, "export buffers too small");
+    uint32_t *d_rows = nullptr, *d_col = nullptr, *d_wb = nullptr;
+    uint64_t *d_off = nullptr;
     uint8_t *d_del = nullptr;
+    SPK_TRY(dalloc(net, &d_rows, n_rows));
+    SPK_TRY(dalloc(net, &d_off, n_rows));
     SPK_TRY(dalloc(net, &d_col, tot));
     SPK_TRY(dalloc(net, &d_wb, tot));
     SPK_TRY(dalloc(net, &d_del, tot));
-    SPK_HIP(hipMemcpyAsync(d_off, poff.data(), pieces * 8, hipMemcpyHostToDevice, s));
-    SPK_HIP(export_gather(net->row_ptr, net->syn, net->n, net->lists, net->dmin, d_rows, n_rows, d_off,
-                          d_col, d_wb, d_del, s));
+    SPK_HIP(hipMemcpyAsync(d_rows, rows, n_rows * 4, hipMemcpyHostToDevice, s));
+    SPK_HIP(hipMemcpyAsync(d_off, offs, n_rows * 8, hipMemcpyHostToDevice, s));
+    SPK_HIP(export_gather(net->row_ptr, net->syn, net->dmin, d_rows, n_rows, d_off, d_col, d_wb, d_del, s));
     std::vector<uint32_t> hc(tot), hw(tot);
     std::vector<uint8_t> hd(tot);
     if (tot) {
@@ -1014,7 +1066,7 @@ spk_status spk_export_rows(spk_net *net, const uint32_t *rows, uint64_t n_rows, 
         SPK_HIP(hipMemcpyAsync(hd.data(), d_del, tot, hipMemcpyDeviceToHost, s));
     }
     SPK_HIP(hipStreamSynchronize(s));
-    dfree(net, d_rows); dfree(net, d_lens); dfree(net, d_off);
+    dfree(net, d_rows); dfree(net, d_off);
     dfree(net, d_col); dfree(net, d_wb); dfree(net, d_del);
     // canonical order per row: (target, delay, stored weight bits)
     std::vector<uint64_t> idx;
@@ -1059,9 +1111,9 @@ spk_status spk_stats(spk_net *net, spk_stats_t *out)
     st.device_bytes = net->device_bytes;
     st.n_exc = net->n_exc;
     st.ref_steps = net->ref_steps;
-    st.ring_slots = net->ring;
+    st.ring_slots = net->spk_slots;
     st.delay_lists = net->lists;
-    st.max_piece = net->max_piece;
+    st.max_row = net->max_row;
     st.pois_len = net->pois_len;
     st.fixed_shift = net->P.acc_mode == SPK_ACC_FIXED ? net->P.fixed_shift : net->shift64;
     st.k = net->k;
@@ -1069,7 +1121,7 @@ spk_status spk_stats(spk_net *net, spk_stats_t *out)
     st.tile_width = net->tl.W;
     st.tiles = net->tl.T;
     st.delivery = net->direct ? SPK_DELIVERY_DIRECT : SPK_DELIVERY_BINNED;
-    st.bin_chunk = net->bin_chunk;
+    st.page_cap = net->page_cap;
     *out = st;
     return SPK_OK;
 }
@@ -1079,16 +1131,16 @@ spk_status spk_set_profiling(spk_net *net, int on)
     SPK_TRY(check_ready(net));
     SPK_TRY(collect_profile(net));
     net->profiling = on != 0;
-    net->ms_bin = net->ms_tile = 0;
+    net->ms_push = net->ms_tile = 0;
     net->launches = 0;
     return SPK_OK;
 }
 
-spk_status spk_read_kernel_ms(spk_net *net, double *bin_ms, double *tile_ms, uint64_t *steps)
+spk_status spk_read_kernel_ms(spk_net *net, double *push_ms, double *tile_ms, uint64_t *steps)
 {
     SPK_TRY(check_ready(net));
     SPK_TRY(collect_profile(net));
-    if (bin_ms) *bin_ms = net->ms_bin;
+    if (push_ms) *push_ms = net->ms_push;
     if (tile_ms) *tile_ms = net->ms_tile;
     if (steps) *steps = net->launches;
     return SPK_OK;

@@ -12,20 +12,23 @@
 //     the sum is therefore exact and is rounded once to fp32.
 // The target neurons are cut into tiles of W neurons, one workgroup per tile
 // ("tile" kernel); each XCD owns a contiguous group of T8 tiles (blockIdx % 8
-// selects the XCD).  Events reach their tile in one of two ways:
-//   - direct: the tile reads, for every due spike, the run of that spike's
-//     target-sorted row that falls into the tile (per-piece tile offsets);
-//     used when rows are long compared with the tile count;
-//   - binned: a "bin" kernel reads each due row's run for the XCD's group
-//     (per-piece group offsets), counting-sorts it by tile in LDS and appends
-//     coalesced runs to per-tile bins that the tile kernel then drains.
-// The rows are sorted by target (Sec. III-A), so both runs are contiguous:
-// this is the paper's cache-aware transmission, with the locality made
-// explicit as LDS tiles instead of left to the cache.
+// selects the XCD).  A step t is:
+//   1. tile kernel: accumulate the events arriving at t in LDS, update the
+//      tile's neurons, compact the spikes of t into the tile's own segment of
+//      the spike list (no global atomics);
+//   2. push kernel (binned delivery): read the row of every neuron that fired
+//      at t once, and sort its events by (arrival step t + d, target tile) in
+//      LDS into pages owned by the block (no global atomics); the tile kernel
+//      of step t + d drains them.
+// With a single delay and long rows the tile kernel instead reads, for every
+// spike due at t, the run of that spike's row that falls into its tile
+// ("direct" delivery, per-row tile offsets).  Rows are grouped by target tile
+// (Sec. III-A keeps them sorted by target), so both runs are contiguous: the
+// paper's cache-aware transmission, with the locality made explicit as LDS
+// tiles instead of left to the cache.
 //
-// Per-delay adjacency lists (Sec. V): at step t, list j (delay dmin+j)
-// delivers the spikes of step t - dmin - j.  Spike lists live in a ring of
-// dmax + 2 slots, one list per (slot, XCD group); counts stay on the device.
+// Delays (Sec. V): each stored synapse carries its delay index; an event of
+// delay d from a spike at t lands in the page of arrival slot (t + d) mod dmax.
 #include <hip/hip_runtime.h>
 
 #include "spk_internal.h"
@@ -34,13 +37,36 @@ namespace spk {
 
 namespace {
 
-constexpr int kBinThreads = 512;
+constexpr int kPushThreads = 1024;
 constexpr int kTileThreads = 1024;
-constexpr uint32_t kChunk = 4096;              // events staged per binning round
-constexpr uint32_t kMaxChunkPieces = 512;      // pieces resolved per binning chunk
-constexpr uint32_t kDue = kMaxLists * kGroups; // (list, source group) spike lists
+constexpr int kPushR = 16;                                // events per thread per load phase
+constexpr uint32_t kLoadPhase = kPushR * kPushThreads;    // events loaded at once
+constexpr uint32_t kStage = kLoadPhase / 2;               // events bucket-sorted at once
+constexpr uint32_t kMaxChunkSpikes = 1024;                // rows resolved per push chunk
+constexpr uint32_t kMaxSrcTiles = 64;                     // source tiles per push block
+constexpr int kRounds = kMaxTileW / kTileThreads;         // neurons per tile thread
+static_assert(kMaxTiles <= 2 * kTileThreads, "spike-count prefix takes at most two tiles per thread");
 
 __device__ __forceinline__ uint32_t lane_id() { return threadIdx.x & (kWave - 1); }
+
+// Workgroup barrier that orders LDS traffic only.  __syncthreads() also
+// waits for every outstanding global load and store of the thread, which
+// would turn each phase of these kernels into a full memory round trip;
+// here global loads issued before the barrier stay in flight across it.
+// Used wherever threads of a block communicate through LDS alone.
+__device__ __forceinline__ void lds_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+__device__ __forceinline__ void lds_wave_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
 
 __device__ __forceinline__ uint64_t step_index(const StepArgs &a, uint32_t i, int64_t t_explicit)
 {
@@ -57,14 +83,14 @@ __device__ uint32_t block_scan_u32(uint32_t x, uint32_t *ws /*>=16*/, uint32_t *
         if (lane >= (uint32_t)o) inc += y;
     }
     if (lane == kWave - 1) ws[w] = inc;
-    __syncthreads();
+    lds_sync();
     uint32_t before = 0, tot = 0;
     for (uint32_t k = 0; k < nw; k++) {
         const uint32_t v = ws[k];
         before += k < w ? v : 0u;
         tot += v;
     }
-    __syncthreads();
+    lds_sync();
     *total = tot;
     return before + inc - x;
 }
@@ -74,63 +100,72 @@ __device__ __forceinline__ uint64_t block_sum_u64(uint64_t x, unsigned long long
     const uint32_t lane = lane_id(), w = threadIdx.x / kWave, nw = blockDim.x / kWave;
     for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
     if (lane == 0) ws[w] = x;
-    __syncthreads();
+    lds_sync();
     uint64_t tot = 0;
     for (uint32_t k = 0; k < nw; k++) tot += ws[k];
-    __syncthreads();
+    lds_sync();
     return tot;
 }
 
-// The spike lists due at step t: one entry per (delay list, source group).
-struct Due {
-    uint32_t pre[kDue + 1];   // exclusive prefix of the entry counts
-    uint64_t base[kDue];      // offset of the entry's spike list in the ring
-    uint32_t list[kDue];      // delay list of the entry
-    uint32_t ne;
-};
-
-__device__ void build_due(const StepArgs &a, uint64_t t, Due &d, uint32_t *ws)
+// Block-wide exclusive max-scan of one u32 per thread.
+__device__ uint32_t block_scan_max_u32(uint32_t x, uint32_t *ws)
 {
-    const uint32_t nl = a.list_hi - a.list_lo;
-    const uint32_t ne = nl * kGroups;
-    uint32_t c = 0;
-    const uint32_t e = threadIdx.x;
-    if (e < ne) {
-        const uint32_t jj = a.list_lo + e / kGroups, xs = e % kGroups;
-        const uint64_t del = (uint64_t)a.dmin + jj;
-        uint64_t base = 0;
-        if (a.dbg_spikes) {
-            c = xs == 0 ? *a.dbg_count : 0u;
-        } else if (t >= del) {
-            const uint64_t slot = (t - del) % a.ring_slots;
-            c = a.ring_count[(slot * kGroups + xs) * kPad];
-            if (c > a.tl.Gw) c = a.tl.Gw;
-            base = (slot * kGroups + xs) * (uint64_t)a.tl.Gw;
-        }
-        d.base[e] = base;
-        d.list[e] = jj;
+    const uint32_t lane = lane_id(), w = threadIdx.x / kWave;
+    uint32_t inc = x;
+    for (int o = 1; o < kWave; o <<= 1) {
+        const uint32_t y = __shfl_up(inc, o);
+        if (lane >= (uint32_t)o) inc = y > inc ? y : inc;
     }
-    uint32_t tot;
-    const uint32_t ex = block_scan_u32(e < ne ? c : 0u, ws, &tot);
-    if (e < ne) d.pre[e] = ex;
-    if (threadIdx.x == 0) {
-        d.pre[ne] = tot;
-        d.ne = ne;
-    }
-    __syncthreads();
+    const uint32_t ex_w = __shfl_up(inc, 1);
+    if (lane == kWave - 1) ws[w] = inc;
+    lds_sync();
+    uint32_t before = 0;
+    for (uint32_t k = 0; k < w; k++) before = ws[k] > before ? ws[k] : before;
+    lds_sync();
+    return lane ? (ex_w > before ? ex_w : before) : before;
 }
 
-// piece p of the due set -> (row index j*n + s); p < d.pre[d.ne]
-__device__ __forceinline__ uint64_t due_row(const StepArgs &a, const Due &d, uint32_t p)
+// The spike list of one slot is spread over per-tile segments: pre[] gets
+// the exclusive prefix of the T segment counts; returns the total.
+__device__ uint32_t load_spike_set(const StepArgs &a, uint32_t slot, uint32_t *pre, uint32_t *ws)
 {
-    uint32_t lo = 0, hi = d.ne - 1;  // largest e with pre[e] <= p
+    const uint32_t T = a.tl.T, W = a.tl.W;
+    const uint32_t b = threadIdx.x * 2;
+    const uint32_t *cnt = a.spk_cnt + (uint64_t)slot * T;
+    uint32_t c0 = cnt[b < T ? b : 0], c1 = cnt[b + 1 < T ? b + 1 : 0];
+    c0 = b < T ? (c0 < W ? c0 : W) : 0u;
+    c1 = b + 1 < T ? (c1 < W ? c1 : W) : 0u;
+    uint32_t tot;
+    const uint32_t ex = block_scan_u32(c0 + c1, ws, &tot);
+    if (b < T) pre[b] = ex;
+    if (b + 1 < T) pre[b + 1] = ex + c0;
+    if (threadIdx.x == 0) pre[T] = tot;
+    lds_sync();
+    return tot;
+}
+
+// k-th spike of the slot (k < total): largest tile with pre[tile] <= k.
+__device__ __forceinline__ uint32_t spike_at(const StepArgs &a, const uint32_t *pre, uint32_t slot,
+                                             uint32_t k)
+{
+    uint32_t lo = 0, hi = a.tl.T - 1;
     while (lo < hi) {
         const uint32_t mid = (lo + hi + 1) >> 1;
-        if (d.pre[mid] <= p) lo = mid; else hi = mid - 1;
+        if (pre[mid] <= k) lo = mid; else hi = mid - 1;
     }
-    const uint32_t k = p - d.pre[lo];
-    const uint32_t s = a.dbg_spikes ? a.dbg_spikes[k] : a.ring[d.base[lo] + k];
-    return (uint64_t)d.list[lo] * a.n + s;
+    return a.spk_ids[((uint64_t)slot * a.tl.T + lo) * a.tl.W + (k - pre[lo])];
+}
+
+// Page (x, g1, slot, c) of the binned delivery; records at page * page_cap.
+__device__ __forceinline__ uint32_t page_of(const StepArgs &a, uint32_t x, uint32_t g1, uint32_t slot,
+                                            uint32_t c)
+{
+    return ((x * a.pg1 + g1) * a.pslots + slot) * a.tl.T8 + c;
+}
+
+__device__ __forceinline__ uint32_t arrival_slot(const StepArgs &a, uint64_t t, uint32_t j, bool dbg)
+{
+    return dbg ? 0u : (uint32_t)((t + a.dmin + j) % a.pslots);
 }
 
 // Accumulator conversions.  fp32 mode: exact int64 multiple of 2^-S64.
@@ -158,174 +193,223 @@ template <> struct Acc<false> {
     }
 };
 
-// Global fallback for bin overflow (rare): same units as the LDS accumulator.
+// Global fallback for a full page (rare): same units as the LDS accumulator,
+// one accumulator per (arrival slot, neuron).
 template <bool FIXED>
-__device__ __forceinline__ void overflow_add(const StepArgs &a, uint32_t tile, uint32_t local, int32_t wbits)
+__device__ __forceinline__ void overflow_add(const StepArgs &a, uint32_t slot, uint32_t tile,
+                                             uint32_t local, int32_t wbits)
 {
-    const uint64_t i = (uint64_t)tile * a.tl.W + local;
+    const uint64_t st = (uint64_t)slot * a.tl.T + tile;
+    const uint64_t i = st * a.tl.W + local;
     if (FIXED) atomicAdd((int32_t *)a.acc_ovf + i, wbits);
     else atomicAdd((unsigned long long *)a.acc_ovf + i, (unsigned long long)to_fixed64(wbits, a.m.shift64));
-    if (a.ovf_flag[tile] == 0) atomicOr(&a.ovf_flag[tile], 1u);
+    if (a.ovf_flag[st] == 0) atomicOr(&a.ovf_flag[st], 1u);
 }
 
-// ------------------------------------------------------------- bin kernel
+// ------------------------------------------------------------ push kernel
 
-struct BinLDS {
-    Due due;
-    union {
-        int2 stage[kChunk];        // tile-sorted events {tile<<16 | local, weight}
-        uint16_t pmap[kChunk];     // piece of every event of the round
-    } u;
-    uint32_t poff[kMaxChunkPieces + 1];
-    uint64_t pbase[kMaxChunkPieces];
-    uint32_t tcnt[256], tst[256];
-    uint64_t gbase[256];
+struct PushLDS {
+    int2 stage[kStage];              // bucket-sorted events {bucket << 16 | local, weight}
+    uint32_t spec[kPushThreads];     // spike IDs fetched with the counts
+    uint32_t tpre[kMaxSrcTiles + 1]; // prefix of the source tiles' spike counts
+    uint32_t cpre[kMaxChunkSpikes + 1];  // prefix of the rows' 64-event chunk counts
+    uint16_t crow[kPushR * (kPushThreads / kWave)];  // row of every chunk of the window
+    uint32_t plen[kMaxChunkSpikes];
+    uint64_t pbase[kMaxChunkSpikes];
+    uint32_t bcnt[kMaxBuckets];      // events per bucket in this half, then rank cursor
+    uint32_t bst[kMaxBuckets];       // bucket starts in the stage
+    uint32_t fill[kMaxBuckets];      // records already in the bucket's page
+    uint32_t pidx[kMaxBuckets];      // page of the bucket
     uint32_t ws[16];
+    unsigned long long ws64[16];
 };
 
-// Block-wide exclusive max-scan of one u32 per thread.
-__device__ uint32_t block_scan_max_u32(uint32_t x, uint32_t *ws)
-{
-    const uint32_t lane = lane_id(), w = threadIdx.x / kWave, nw = blockDim.x / kWave;
-    uint32_t inc = x;
-    for (int o = 1; o < kWave; o <<= 1) {
-        const uint32_t y = __shfl_up(inc, o);
-        if (lane >= (uint32_t)o) inc = y > inc ? y : inc;
-    }
-    const uint32_t ex_w = __shfl_up(inc, 1);
-    if (lane == kWave - 1) ws[w] = inc;
-    __syncthreads();
-    uint32_t before = 0;
-    for (uint32_t k = 0; k < w; k++) before = ws[k] > before ? ws[k] : before;
-    __syncthreads();
-    const uint32_t ex = lane ? (ex_w > before ? ex_w : before) : before;
-    (void)nw;
-    return ex;
-}
-
+// Block (x, g1) takes the spikes of step t of the source tiles g1, g1 + G1,
+// ..., reads the runs of their rows that target group x, and appends the
+// events to its own pages, bucket b = j * T8 + c (delay index j, tile c of
+// the group).  Dependent memory round trips: spike counts and IDs (together),
+// row descriptors, synapses; the page writes are not waited for.
 template <bool FIXED>
-__global__ __launch_bounds__(kBinThreads) void k_bin(StepArgs a, uint32_t i, int64_t t_explicit)
+__global__ __launch_bounds__(kPushThreads) void k_push(StepArgs a, uint32_t i, int64_t t_explicit)
 {
-    __shared__ BinLDS L;
+    __shared__ PushLDS L;
     const uint64_t t = step_index(a, i, t_explicit);
-    const uint32_t x = blockIdx.x % kGroups, g = blockIdx.x / kGroups;
-    const uint32_t G1 = gridDim.x / kGroups;
+    const uint32_t x = blockIdx.x % kGroups, g1 = blockIdx.x / kGroups, G1 = a.pg1;
     const uint32_t tid = threadIdx.x;
     const Tiling tl = a.tl;
-    build_due(a, t, L.due, L.ws);
-    const uint32_t P = L.due.pre[L.due.ne];
-    // pieces per chunk: one chunk per block when possible
-    uint32_t K = (P + G1 - 1) / G1;
-    K = K < 1 ? 1 : (K > a.bin_chunk ? a.bin_chunk : K);
-    const uint32_t chunks = (P + K - 1) / K;
+    const bool dbg = a.dbg_spikes != nullptr;
+    const uint32_t NB = (dbg ? 1u : a.lists) * tl.T8;
+    const uint32_t sslot = (uint32_t)(t % a.spk_slots);
+
+    // 0. counts of this block's source tiles and, in the same round trip,
+    //    the first S spike IDs of each; fill counters of the block's pages
+    const uint32_t ntb = dbg ? 0u : (tl.T > g1 ? (tl.T - g1 + G1 - 1) / G1 : 0u);
+    const uint32_t S = ntb ? kPushThreads / ntb : 0u;
+    {
+        const uint32_t si = S ? tid / S : 0u, sk = S ? tid % S : 0u;
+        const bool mine = si < ntb;
+        const uint64_t seg = (uint64_t)sslot * tl.T + (mine ? g1 + si * G1 : 0u);
+        const uint32_t c = a.spk_cnt[seg];
+        const uint32_t id = a.spk_ids[seg * tl.W + (sk < tl.W ? sk : 0u)];
+        L.spec[tid] = id;
+        if (mine && sk == 0) L.tpre[si + 1] = c < tl.W ? c : tl.W;
+    }
+    for (uint32_t b = tid; b < NB; b += kPushThreads) {
+        const uint32_t p = page_of(a, x, g1, arrival_slot(a, t, b / tl.T8, dbg), b % tl.T8);
+        L.pidx[b] = p;
+        L.fill[b] = a.pfill[p];
+        L.bcnt[b] = 0;
+    }
+    lds_sync();
+    if (tid < kWave) {  // inclusive scan of at most 64 tile counts
+        uint32_t v = tid < ntb ? L.tpre[tid + 1] : 0u;
+        for (int o = 1; o < kWave; o <<= 1) {
+            const uint32_t y = __shfl_up(v, o);
+            if (tid >= (uint32_t)o) v += y;
+        }
+        if (tid < ntb) L.tpre[tid + 1] = v;
+        if (tid == 0) L.tpre[0] = 0;
+    }
+    lds_sync();
+    uint32_t k0 = 0, k1 = L.tpre[ntb];
+    if (dbg) {
+        k0 = (uint32_t)((uint64_t)a.dbg_n * g1 / G1);
+        k1 = (uint32_t)((uint64_t)a.dbg_n * (g1 + 1) / G1);
+    }
     const uint32_t xlo = x * tl.Gw;
-    for (uint32_t c = g; c < chunks; c += G1) {
-        // 1. this XCD's run of every piece of the chunk
+    const uint64_t cap = a.page_cap;
+    uint64_t emitted = 0;
+    for (uint32_t c0 = k0; c0 < k1; c0 += kMaxChunkSpikes) {
+        const uint32_t K = k1 - c0 < kMaxChunkSpikes ? k1 - c0 : kMaxChunkSpikes;
+        // 1. this group's run of every row of the chunk
         uint32_t len = 0;
         uint64_t base = 0;
-        if (tid < K && c * K + tid < P) {
-            const uint64_t row = due_row(a, L.due, c * K + tid);
-            const uint64_t pb = a.row_ptr[row];
-            const uint32_t plen = (uint32_t)(a.row_ptr[row + 1] - pb);
-            const uint32_t gl = a.goff[row * kGroups + x];
-            const uint32_t gh = x + 1 < kGroups ? a.goff[row * kGroups + x + 1] : plen;
-            len = gh - gl;
-            base = pb + gl;
-        }
-        uint32_t E;
-        const uint32_t off = block_scan_u32(len, L.ws, &E);
         if (tid < K) {
-            L.poff[tid] = off;
+            const uint32_t k = c0 + tid;
+            uint32_t s;
+            if (dbg) {
+                s = a.dbg_spikes[k];
+            } else {
+                uint32_t si = 0;
+                while (si + 1 < ntb && L.tpre[si + 1] <= k) si++;
+                const uint32_t r = k - L.tpre[si];
+                s = r < S ? L.spec[si * S + r]
+                          : a.spk_ids[((uint64_t)sslot * tl.T + g1 + si * G1) * tl.W + r];
+            }
+            const RowDesc *d = a.desc + s;
+            const uint32_t lo = x ? d->gend[x - 1] : 0u, hi = d->gend[x];
+            len = hi - lo;
+            base = d->start + lo;
+            emitted += d->gend[kGroups - 1];
+        }
+        // rows are cut into chunks of 64 events; wave w takes chunks w, w + nw,
+        // ...: lane l reads event l of the chunk (one uniform lookup per chunk)
+        uint32_t C;
+        const uint32_t nch = (len + kWave - 1) / kWave;
+        const uint32_t coff = block_scan_u32(nch, L.ws, &C);
+        if (tid < K) {
+            L.cpre[tid] = coff;
+            L.plen[tid] = len;
             L.pbase[tid] = base;
         }
-        if (tid == 0) L.poff[K] = E;
-        __syncthreads();
-        // 2. in rounds of kChunk events: map events to pieces, count by tile,
-        //    reserve bin space, stage tile-sorted in LDS, write coalesced runs
-        for (uint32_t e0 = 0; e0 < E; e0 += kChunk) {
-            const uint32_t nsub = E - e0 < kChunk ? E - e0 : kChunk;
-            constexpr int R = kChunk / kBinThreads;
-            // piece map: mark each piece's first event of the round, then a
-            // max-scan spreads the mark over the piece's events
-            for (uint32_t q = tid; q < nsub; q += kBinThreads) L.u.pmap[q] = 0;
-            for (uint32_t q = tid; q < tl.T8; q += kBinThreads) L.tcnt[q] = 0;
-            __syncthreads();
+        lds_sync();
+        const uint32_t lane = lane_id(), w = tid / kWave;
+        constexpr uint32_t nw = kPushThreads / kWave;
+        // 2. load phases of kPushR chunks per wave: issue every load, then
+        //    bucket-sort and append in two halves (the second half's loads
+        //    land while the first is sorted)
+        constexpr uint32_t kWin = kPushR * nw;  // chunks per load phase
+        for (uint32_t i0 = 0; i0 < C; i0 += kWin) {
+            // chunk -> row map of the window, written by each row's thread
             if (tid < K) {
-                const uint32_t ps = L.poff[tid], pe = L.poff[tid + 1];
-                const uint32_t st = ps > e0 ? ps : e0;
-                if (st < pe && st < e0 + nsub) L.u.pmap[st - e0] = (uint16_t)tid;
+                const uint32_t cb = coff > i0 ? coff : i0, ce = coff + nch < i0 + kWin ? coff + nch : i0 + kWin;
+                for (uint32_t c = cb; c < ce; c++) L.crow[c - i0] = (uint16_t)tid;
             }
-            __syncthreads();
-            {
-                uint32_t v[R], mx = 0;
+            lds_sync();
+            // every load is issued unconditionally (lanes past the end read
+            // synapse 0 and drop it): a load under a branch would get its own
+            // wait for all earlier loads
+            int2 rec[kPushR];
+            uint32_t okm = 0;  // bit u: rec[u] is an event
 #pragma unroll
-                for (int r = 0; r < R; r++) {
-                    const uint32_t q = tid * R + r;
-                    v[r] = q < nsub ? L.u.pmap[q] : 0u;
-                    mx = v[r] > mx ? v[r] : mx;
+            for (int u = 0; u < kPushR; u++) {
+                const uint32_t cl = u * nw + w, ci = i0 + cl;
+                uint64_t idx = 0;
+                if (ci < C) {
+                    const uint32_t k = L.crow[cl];
+                    const uint32_t o = (ci - L.cpre[k]) * kWave + lane;
+                    if (o < L.plen[k]) {
+                        idx = L.pbase[k] + o;
+                        okm |= 1u << u;
+                    }
                 }
-                uint32_t run = block_scan_max_u32(mx, L.ws);
+                rec[u] = a.syn[idx];
+            }
 #pragma unroll
-                for (int r = 0; r < R; r++) {
-                    const uint32_t q = tid * R + r;
-                    run = v[r] > run ? v[r] : run;
-                    if (q < nsub) L.u.pmap[q] = (uint16_t)run;
+            for (int h = 0; h < 2; h++) {
+                if (i0 + (uint32_t)h * (kPushR / 2) * nw >= C) break;
+                constexpr int R = kPushR / 2;
+                uint32_t tr[R];
+#pragma unroll
+                for (int rr = 0; rr < R; rr++) {
+                    const int r = h * R + rr;
+                    tr[rr] = 0xffffffffu;
+                    if (!((okm >> r) & 1u)) continue;
+                    const uint32_t j = (uint32_t)rec[r].x >> kTargetBits;
+                    if (dbg && a.dbg_j >= 0 && (int32_t)j != a.dbg_j) continue;
+                    const uint32_t local = ((uint32_t)rec[r].x & kTargetMask) - xlo;
+                    const uint32_t b = (dbg ? 0u : j) * tl.T8 + (local >> tl.logW);
+                    const uint32_t rank = atomicAdd(&L.bcnt[b], 1u);
+                    tr[rr] = (b << 16) | rank;
+                    rec[r].x = (int)((b << 16) | (local & (tl.W - 1)));
                 }
-            }
-            __syncthreads();
-            int2 rec[R];
-            uint32_t tr[R];
-            uint64_t idx[R];
-#pragma unroll
-            for (int r = 0; r < R; r++) {
-                const uint32_t f = r * kBinThreads + tid;
-                idx[r] = ~0ull;
-                if (f < nsub) {
-                    const uint32_t k = L.u.pmap[f];
-                    idx[r] = L.pbase[k] + (e0 + f - L.poff[k]);
+                lds_sync();
+                uint32_t staged;
+                {   // bucket starts: exclusive scan of the half's counts
+                    const uint32_t P = (NB + kPushThreads - 1) / kPushThreads;
+                    const uint32_t b0 = tid * P;
+                    uint32_t sum = 0;
+                    for (uint32_t k = 0; k < P; k++)
+                        if (b0 + k < NB) sum += L.bcnt[b0 + k];
+                    uint32_t ex = block_scan_u32(sum, L.ws, &staged);
+                    for (uint32_t k = 0; k < P; k++) {
+                        if (b0 + k < NB) {
+                            L.bst[b0 + k] = ex;
+                            ex += L.bcnt[b0 + k];
+                        }
+                    }
                 }
-            }
+                lds_sync();
 #pragma unroll
-            for (int r = 0; r < R; r++)
-                if (idx[r] != ~0ull) rec[r] = a.syn[idx[r]];
-#pragma unroll
-            for (int r = 0; r < R; r++) {
-                tr[r] = 0xffffffffu;
-                if (idx[r] != ~0ull) {
-                    const uint32_t local = (uint32_t)rec[r].x - xlo;
-                    const uint32_t tc = local >> tl.logW;
-                    const uint32_t rank = atomicAdd(&L.tcnt[tc], 1u);
-                    tr[r] = (tc << 16) | rank;
-                    rec[r].x = (int)((tc << 16) | (local & (tl.W - 1)));
+                for (int rr = 0; rr < R; rr++) {
+                    if (tr[rr] == 0xffffffffu) continue;
+                    L.stage[L.bst[tr[rr] >> 16] + (tr[rr] & 0xffffu)] = rec[h * R + rr];
                 }
-            }
-            __syncthreads();
-            {
-                uint32_t cnt = tid < tl.T8 ? L.tcnt[tid] : 0u, tot;
-                const uint32_t st = block_scan_u32(cnt, L.ws, &tot);
-                if (tid < tl.T8) {
-                    L.tst[tid] = st;
-                    L.gbase[tid] = cnt ? atomicAdd(&a.bin_fill[(x * tl.T8 + tid) * kPad], cnt) : 0u;
+                lds_sync();
+                for (uint32_t q = tid; q < staged; q += kPushThreads) {
+                    const int2 r2 = L.stage[q];
+                    const uint32_t b = (uint32_t)r2.x >> 16, local = (uint32_t)r2.x & 0xffffu;
+                    const uint64_t pos = (uint64_t)L.fill[b] + (q - L.bst[b]);
+                    if (pos < cap) {
+                        a.pages[(uint64_t)L.pidx[b] * cap + pos] = make_int2((int)local, r2.y);
+                    } else {
+                        const uint32_t c = b % tl.T8;
+                        overflow_add<FIXED>(a, arrival_slot(a, t, b / tl.T8, dbg), x * tl.T8 + c, local, r2.y);
+                    }
                 }
+                lds_sync();
+                for (uint32_t b = tid; b < NB; b += kPushThreads) {
+                    L.fill[b] += L.bcnt[b];
+                    L.bcnt[b] = 0;
+                }
+                lds_sync();
             }
-            __syncthreads();
-#pragma unroll
-            for (int r = 0; r < R; r++) {
-                if (tr[r] == 0xffffffffu) continue;
-                L.u.stage[L.tst[tr[r] >> 16] + (tr[r] & 0xffffu)] = rec[r];
-            }
-            __syncthreads();
-            for (uint32_t q = tid; q < nsub; q += kBinThreads) {
-                int2 r2 = L.u.stage[q];
-                const uint32_t tc = (uint32_t)r2.x >> 16;
-                r2.x &= 0xffff;
-                const uint32_t tile = x * tl.T8 + tc;
-                const uint64_t pos = L.gbase[tc] + (q - L.tst[tc]);
-                if (pos < a.bin_cap) a.bins[(uint64_t)tile * a.bin_cap + pos] = r2;
-                else overflow_add<FIXED>(a, tile, (uint32_t)r2.x, r2.y);
-            }
-            __syncthreads();
         }
+    }
+    for (uint32_t b = tid; b < NB; b += kPushThreads) a.pfill[L.pidx[b]] = L.fill[b];
+    if (!dbg && x == 0) {  // events emitted at t, counted once per spike
+        const uint64_t tot = block_sum_u64(emitted, L.ws64);
+        if (tid == 0 && tot) atomicAdd((unsigned long long *)&a.events8[t * kGroups], (unsigned long long)tot);
     }
 }
 
@@ -335,33 +419,37 @@ template <bool FIXED>
 struct TileLDS {
     typename Acc<FIXED>::T acc[kMaxTileW];
     uint16_t spk[kMaxTileW];
-    Due due;
+    uint32_t pre[kMaxTiles + 1];   // direct: spike-count prefix; binned: page prefix
+    uint16_t cpage[kTileThreads / kWave * 16];  // binned: page of every chunk of the window
     uint32_t wpre[kTileThreads / kWave][kWave + 1];
     uint64_t wbeg[kTileThreads / kWave][kWave];
     uint32_t ws[16];
     unsigned long long ws64[16];
-    uint32_t nspk, base;
+    uint32_t nspk;
     uint64_t pois[256];
+    uint16_t guide[256];
 };
 
-// Accumulate the tile's events directly from the due rows (direct mode):
-// each wave takes 64 pieces at a time, lane l resolving piece l's run for
-// this tile; the 64 runs are then streamed lane-parallel.
+// Accumulate the tile's events directly from the rows of the given spikes
+// (direct mode): each wave takes 64 spikes at a time, lane l resolving spike
+// l's run for this tile; the 64 runs are then streamed lane-parallel.  With
+// jf >= 0 only synapses of delay index jf are delivered.  Returns the number
+// of events this thread delivered.
 template <bool FIXED>
-__device__ uint64_t gather_direct(const StepArgs &a, TileLDS<FIXED> &L, uint32_t tile, uint32_t tile_lo)
+__device__ uint32_t gather_direct(const StepArgs &a, TileLDS<FIXED> &L, uint32_t tile, uint32_t tile_lo,
+                                  uint32_t P, uint32_t slot, int32_t jf)
 {
     const uint32_t lane = lane_id(), w = threadIdx.x / kWave, nw = kTileThreads / kWave;
-    const uint32_t P = L.due.pre[L.due.ne];
     const uint32_t T1 = a.tl.T + 1;
-    uint64_t mine = 0;
+    uint32_t mine = 0;
     for (uint32_t p0 = w * kWave; p0 < P; p0 += nw * kWave) {
         uint32_t len = 0;
         uint64_t beg = 0;
         if (p0 + lane < P) {
-            const uint64_t row = due_row(a, L.due, p0 + lane);
-            const uint16_t *to = a.toff + row * T1 + tile;
+            const uint32_t s = a.dbg_spikes ? a.dbg_spikes[p0 + lane] : spike_at(a, L.pre, slot, p0 + lane);
+            const uint16_t *to = a.toff + (uint64_t)s * T1 + tile;
             const uint32_t b = to[0], e = to[1];
-            beg = a.row_ptr[row] + b;
+            beg = a.row_ptr[s] + b;
             len = e - b;
         }
         uint32_t inc = len;
@@ -373,34 +461,32 @@ __device__ uint64_t gather_direct(const StepArgs &a, TileLDS<FIXED> &L, uint32_t
         L.wpre[w][lane] = inc - len;
         L.wbeg[w][lane] = beg;
         if (lane == 0) L.wpre[w][kWave] = tot;
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-        constexpr int U = 4;  // loads in flight per lane
+        lds_wave_sync();
+        constexpr int U = 8;  // loads in flight per lane
         for (uint32_t f0 = 0; f0 < tot; f0 += kWave * U) {
             uint64_t idx[U];
 #pragma unroll
             for (int u = 0; u < U; u++) {
                 const uint32_t f = f0 + u * kWave + lane;
-                idx[u] = ~0ull;
-                if (f < tot) {
-                    uint32_t lo = 0, hi = kWave - 1;
-                    while (lo < hi) {
-                        const uint32_t mid = (lo + hi + 1) >> 1;
-                        if (L.wpre[w][mid] <= f) lo = mid; else hi = mid - 1;
-                    }
-                    idx[u] = L.wbeg[w][lo] + (f - L.wpre[w][lo]);
+                const uint32_t fc = f < tot ? f : 0u;
+                uint32_t lo = 0, hi = kWave - 1;
+                while (lo < hi) {
+                    const uint32_t mid = (lo + hi + 1) >> 1;
+                    if (L.wpre[w][mid] <= fc) lo = mid; else hi = mid - 1;
                 }
+                idx[u] = f < tot ? L.wbeg[w][lo] + (fc - L.wpre[w][lo]) : 0ull;
             }
             int2 r[U];
 #pragma unroll
-            for (int u = 0; u < U; u++)
-                if (idx[u] != ~0ull) r[u] = a.syn[idx[u]];
+            for (int u = 0; u < U; u++) r[u] = a.syn[idx[u]];  // unconditional, see push
 #pragma unroll
-            for (int u = 0; u < U; u++)
-                if (idx[u] != ~0ull) Acc<FIXED>::add(&L.acc[(uint32_t)r[u].x - tile_lo], r[u].y, a.m.shift64);
+            for (int u = 0; u < U; u++) {
+                if (f0 + u * kWave + lane >= tot) continue;
+                if (jf >= 0 && (int32_t)((uint32_t)r[u].x >> kTargetBits) != jf) continue;
+                Acc<FIXED>::add(&L.acc[((uint32_t)r[u].x & kTargetMask) - tile_lo], r[u].y, a.m.shift64);
+                mine++;
+            }
         }
-        mine += lane == 0 ? tot : 0u;
         __builtin_amdgcn_wave_barrier();
     }
     return mine;
@@ -419,41 +505,114 @@ __global__ __launch_bounds__(kTileThreads) void k_tile(StepArgs a, uint32_t i, i
     const uint32_t tile_n = tile_lo < a.n ? (a.n - tile_lo < tl.W ? a.n - tile_lo : tl.W) : 0u;
     const ModelArgs &m = a.m;
     const bool debug = a.dbg_out != nullptr;
+    const uint32_t pslot = debug || a.direct ? 0u : (uint32_t)(t % a.pslots);
 
+    // 0. loads that do not depend on delivery are issued first.  Loads
+    //    complete in issue order, so the small ones that are waited for soon
+    //    (drive table, page fill counts, overflow flag) go before the tile's
+    //    neuron state, which stays in flight until the update needs it.
+    //    All are unconditional loads from clamped indices (see the push kernel).
+    uint64_t pz = 0;
+    uint16_t gz = 0;
+    const bool drive = m.pois_len && !debug;
+    if (drive) {
+        pz = a.pois[tid < m.pois_len ? tid : 0u];
+        gz = a.pois_guide[tid & 255u];
+    }
+    uint32_t pf = 0, ovf = 0;
+    if (!a.direct) {
+        pf = a.pfill[page_of(a, x, tid < a.pg1 ? tid : 0u, pslot, cl)];  // masked where used
+        ovf = a.ovf_flag[(uint64_t)pslot * tl.T + tile];
+    }
+    float Vr[kRounds];
+    uint32_t Rr[kRounds];
+#pragma unroll
+    for (int u = 0; u < kRounds; u++) {
+        const uint32_t q = u * kTileThreads + tid;
+        const uint32_t gi = q < tile_n ? tile_lo + q : 0u;
+        Vr[u] = a.V[gi];
+        Rr[u] = a.ref[gi];
+    }
     for (uint32_t q = tid; q < tl.W; q += kTileThreads) L.acc[q] = 0;
-    if (m.pois_len && !debug)
-        for (uint32_t k = tid; k < m.pois_len; k += kTileThreads) L.pois[k] = a.pois[k];
+    if (drive) {
+        if (tid < m.pois_len) L.pois[tid] = pz;
+        if (tid < 256) L.guide[tid] = gz;
+    }
     if (tid == 0) L.nspk = 0;
-    if (a.direct) build_due(a, t, L.due, L.ws);
-    __syncthreads();
 
-    // 1. accumulate every event due at t for this tile
+    // 1. accumulate every event arriving at t (the state loads above stay
+    //    in flight: the barriers below order LDS traffic only)
     uint64_t delivered = 0;
+    lds_sync();
     if (a.direct) {
-        delivered = block_sum_u64(gather_direct<FIXED>(a, L, tile, tile_lo), L.ws64);
+        // spikes of step t - d for every delay d, through the runs of their
+        // rows in this tile (only the synapses of delay d when there are several)
+        uint64_t mine = 0;
+        if (debug) {
+            mine = gather_direct<FIXED>(a, L, tile, tile_lo, a.dbg_n, 0, a.dbg_j);
+        } else {
+            for (uint32_t j = 0; j < a.lists; j++) {
+                const uint64_t d = (uint64_t)a.dmin + j;
+                if (t < d) break;
+                const uint32_t dslot = (uint32_t)((t - d) % a.spk_slots);
+                const uint32_t P = load_spike_set(a, dslot, L.pre, L.ws);
+                mine += gather_direct<FIXED>(a, L, tile, tile_lo, P, dslot, a.lists > 1 ? (int32_t)j : -1);
+                lds_sync();
+            }
+        }
+        delivered = block_sum_u64(mine, L.ws64);
     } else {
-        const uint32_t filled = a.bin_fill[tile * kPad];
-        const uint32_t nb = filled < a.bin_cap ? filled : (uint32_t)a.bin_cap;
-        const int2 *bin = a.bins + (uint64_t)tile * a.bin_cap;
-        // kDrain independent loads in flight per thread before their atomics
-        constexpr int kDrain = 8;
-        for (uint32_t q0 = tid; q0 < nb; q0 += kTileThreads * kDrain) {
+        // pages cut into chunks of 64 records; wave w drains chunks w, w + nw, ...
+        const uint32_t cap = a.page_cap, G1 = a.pg1;
+        pf = tid < G1 ? pf : 0u;
+        const uint32_t ne = pf < cap ? pf : cap;  // records stored in page tid
+        uint32_t C;
+        const uint32_t cex = block_scan_u32((ne + kWave - 1) / kWave, L.ws, &C);
+        uint32_t *pn = L.pre + kTileThreads;      // record counts after the chunk prefix
+        if (tid < G1) {
+            L.pre[tid] = cex;
+            pn[tid] = ne;
+        }
+        delivered = block_sum_u64(pf, L.ws64);  // includes events that overflowed
+        const uint32_t w = tid / kWave;
+        constexpr uint32_t nw = kTileThreads / kWave;
+        constexpr int kDrain = 16;  // loads in flight per lane before their atomics
+        constexpr uint32_t kWin = kDrain * nw;
+        const uint32_t nchp = (ne + kWave - 1) / kWave;
+        for (uint32_t i0 = 0; i0 < C; i0 += kWin) {
+            // chunk -> page map of the window, written by each page's thread
+            if (tid < G1) {
+                const uint32_t cb = cex > i0 ? cex : i0, ce = cex + nchp < i0 + kWin ? cex + nchp : i0 + kWin;
+                for (uint32_t c = cb; c < ce; c++) L.cpage[c - i0] = (uint16_t)tid;
+            }
+            lds_sync();
             int2 r[kDrain];
+            uint32_t okm = 0;
 #pragma unroll
             for (int u = 0; u < kDrain; u++) {
-                const uint32_t q = q0 + u * kTileThreads;
-                r[u] = q < nb ? bin[q] : make_int2(-1, 0);
+                const uint32_t cw = u * nw + w, ci = i0 + cw;
+                uint64_t idx = 0;
+                if (ci < C) {
+                    const uint32_t g = L.cpage[cw];
+                    const uint32_t o = (ci - L.pre[g]) * kWave + lane;
+                    if (o < pn[g]) {
+                        idx = (uint64_t)page_of(a, x, g, pslot, cl) * cap + o;
+                        okm |= 1u << u;
+                    }
+                }
+                r[u] = a.pages[idx];  // unconditional, see the push kernel
             }
 #pragma unroll
             for (int u = 0; u < kDrain; u++)
-                if (r[u].x >= 0) Acc<FIXED>::add(&L.acc[(uint32_t)r[u].x], r[u].y, m.shift64);
+                if ((okm >> u) & 1u) Acc<FIXED>::add(&L.acc[(uint32_t)r[u].x], r[u].y, m.shift64);
+            lds_sync();  // the window's map is read before the next one is written
         }
-        delivered = filled;
-        __syncthreads();
-        if (tid == 0) a.bin_fill[tile * kPad] = 0;
-        if (a.ovf_flag[tile]) {  // events that did not fit the bin (global fallback)
+        if (tid < G1) a.pfill[page_of(a, x, tid, pslot, cl)] = 0;
+        lds_sync();
+        if (ovf) {  // events that did not fit their page (global fallback)
+            const uint64_t st = (uint64_t)pslot * tl.T + tile;
             for (uint32_t q = tid; q < tile_n; q += kTileThreads) {
-                const uint64_t gi = (uint64_t)tile * tl.W + q;
+                const uint64_t gi = st * tl.W + q;
                 if (FIXED) {
                     int32_t *o = (int32_t *)a.acc_ovf + gi;
                     L.acc[q] += *o;
@@ -464,11 +623,10 @@ __global__ __launch_bounds__(kTileThreads) void k_tile(StepArgs a, uint32_t i, i
                     *o = 0;
                 }
             }
-            __syncthreads();
-            if (tid == 0) a.ovf_flag[tile] = 0;
+            if (tid == 0) a.ovf_flag[st] = 0;
         }
     }
-    __syncthreads();
+    lds_sync();
 
     if (debug) {  // delivery check: hand the accumulated input back, no update
         for (uint32_t q = tid; q < tile_n; q += kTileThreads) {
@@ -480,38 +638,19 @@ __global__ __launch_bounds__(kTileThreads) void k_tile(StepArgs a, uint32_t i, i
 
     // 2. neuron update (forward Euler in fp32, every operation rounded on its
     //    own), spikes collected in LDS
-    const uint32_t slot = (uint32_t)(t % a.ring_slots);
     uint64_t ev = 0;
-    constexpr int kRounds = kMaxTileW / kTileThreads;  // neurons per thread
-    for (uint32_t q00 = 0; q00 < tile_n; q00 += kTileThreads * kRounds) {
-    // all state loads of this thread's neurons are issued before any update
-    float Vr[kRounds];
-    uint32_t Rr[kRounds];
 #pragma unroll
     for (int u = 0; u < kRounds; u++) {
-        const uint32_t q = q00 + u * kTileThreads + tid;
-        Vr[u] = 0.0f;
-        Rr[u] = 0;
-        if (q < tile_n) {
-            Vr[u] = a.V[tile_lo + q];
-            if (m.kind != SPK_SOURCE) Rr[u] = a.ref[tile_lo + q];
-        }
-    }
-#pragma unroll
-    for (int u = 0; u < kRounds; u++) {
-        const uint32_t q = q00 + u * kTileThreads + tid;
+        const uint32_t q = u * kTileThreads + tid;
         bool spk = false;
         if (q < tile_n) {
             const uint32_t gi = tile_lo + q;
             uint32_t K = 0;
-            if (m.pois_len) {  // K = min { k : hi32 < T_k }
-                const uint64_t h = hash_hi32(step_hash(m.keys.pois, gi, t));
-                uint32_t lo = 0, hi = m.pois_len - 1;
-                while (lo < hi) {
-                    const uint32_t mid = (lo + hi) >> 1;
-                    if (h < L.pois[mid]) hi = mid; else lo = mid + 1;
-                }
-                K = lo;
+            if (m.pois_len) {  // K = min { k : hi32 < T_k }, searched from the guide entry
+                const uint32_t h = hash_hi32(step_hash(m.keys.pois, gi, t));
+                uint32_t k = L.guide[h >> 24];
+                while ((uint64_t)h >= L.pois[k]) k++;
+                K = k;
             }
             float I;
             if (FIXED) {
@@ -548,7 +687,7 @@ __global__ __launch_bounds__(kTileThreads) void k_tile(StepArgs a, uint32_t i, i
                 a.ref[gi] = (uint8_t)r;
             }
             a.V[gi] = V;
-            if (spk) ev += a.outdeg[gi];
+            if (spk && a.direct) ev += a.outdeg[gi];  // binned: counted by the push kernel
         }
         const uint64_t mask = __ballot(spk);
         if (mask) {  // wavefront-ballot compaction into the tile's LDS list
@@ -563,54 +702,38 @@ __global__ __launch_bounds__(kTileThreads) void k_tile(StepArgs a, uint32_t i, i
             }
         }
     }
-    }
-    ev = block_sum_u64(ev, L.ws64);
+    if (a.direct) ev = block_sum_u64(ev, L.ws64);
+    else lds_sync();
 
-    // 3. publish: one reservation per tile in the XCD group's spike list
+    // 3. publish into the tile's own segment of the spike list of t
+    const uint32_t ns = L.nspk;
+    const uint64_t seg = (uint64_t)(t % a.spk_slots) * tl.T + tile;
+    uint32_t *dst = a.spk_ids + seg * tl.W;
+    for (uint32_t q = tid; q < ns; q += kTileThreads) dst[q] = tile_lo + L.spk[q];
     if (tid == 0) {
-        const uint32_t ns = L.nspk;
-        uint32_t base = 0;
-        if (ns) {
-            base = atomicAdd(&a.ring_count[((uint64_t)slot * kGroups + x) * kPad], ns);
-            atomicAdd(&a.counts8[t * kGroups + x], ns);
-            atomicAdd((unsigned long long *)&a.events8[t * kGroups + x], (unsigned long long)ev);
-        }
+        a.spk_cnt[seg] = ns;
+        if (ns) atomicAdd(&a.counts8[t * kGroups + x], ns);
+        if (ev) atomicAdd((unsigned long long *)&a.events8[t * kGroups + x], (unsigned long long)ev);
         if (delivered)
             atomicAdd((unsigned long long *)&a.delivered8[t * kGroups + x], (unsigned long long)delivered);
-        L.base = base;
-    }
-    if (blockIdx.x == 0 && tid < kGroups)  // next step's lists start empty
-        a.ring_count[(((t + 1) % a.ring_slots) * kGroups + tid) * kPad] = 0;
-    __syncthreads();
-    const uint32_t ns = L.nspk, base = L.base;
-    uint32_t *dst = a.ring + ((uint64_t)slot * kGroups + x) * tl.Gw;
-    for (uint32_t q = tid; q < ns; q += kTileThreads) {
-        if (base + q < tl.Gw) dst[base + q] = tile_lo + L.spk[q];
-        else atomicOr(a.flags, 1u);
     }
 }
 
 // ---------------------------------------------------------------- record
 
-__global__ __launch_bounds__(256) void k_record(StepArgs a, uint32_t i, int64_t t_explicit)
+__global__ __launch_bounds__(kTileThreads) void k_record(StepArgs a, uint32_t i, int64_t t_explicit)
 {
+    __shared__ uint32_t pre[kMaxTiles + 1];
+    __shared__ uint32_t ws[16];
     const uint64_t t = step_index(a, i, t_explicit);
-    const uint64_t slot = t % a.ring_slots;
-    uint64_t base = a.raster_offs[t];
-    bool ok = true;
-    for (uint32_t xs = 0; xs < kGroups; xs++) {
-        uint32_t c = a.ring_count[(slot * kGroups + xs) * kPad];
-        if (c > a.tl.Gw) c = a.tl.Gw;
-        if (base + c > a.raster_cap) {
-            ok = false;
-            break;
-        }
-        const uint32_t *src = a.ring + (slot * kGroups + xs) * a.tl.Gw;
-        for (uint32_t k = threadIdx.x; k < c; k += blockDim.x) a.raster[base + k] = src[k];
-        base += c;
-    }
+    const uint32_t slot = (uint32_t)(t % a.spk_slots);
+    const uint32_t M = load_spike_set(a, slot, pre, ws);
+    const uint64_t base = a.raster_offs[t];
+    const bool ok = base + M <= a.raster_cap;
+    if (ok)
+        for (uint32_t k = threadIdx.x; k < M; k += kTileThreads) a.raster[base + k] = spike_at(a, pre, slot, k);
     if (threadIdx.x == 0) {
-        a.raster_offs[t + 1] = ok ? base : a.raster_offs[t];
+        a.raster_offs[t + 1] = ok ? base + M : base;
         if (!ok) atomicOr(a.flags, 2u);
     }
 }
@@ -628,24 +751,32 @@ __global__ __launch_bounds__(256) void k_stream_copy(const uint4 *src, uint4 *ds
 
 }  // namespace
 
-uint32_t bin_grid() { return (uint32_t)(kGroups * ((3 * cu_count() + kGroups - 1) / kGroups)); }
-
-hipError_t launch_bin(const StepArgs &a, uint32_t i, int64_t t_explicit, hipStream_t s)
+uint32_t push_blocks_per_group()
 {
-    if (a.tl.T8 > 256 || a.bin_chunk == 0 || a.bin_chunk > kMaxChunkPieces ||
-        a.list_hi <= a.list_lo || a.list_hi - a.list_lo > kMaxLists || a.tl.W > 65536)
+    const int g = cu_count() / (int)kGroups;
+    return g < 1 ? 1u : (uint32_t)g;
+}
+
+hipError_t launch_push(const StepArgs &a, uint32_t i, int64_t t_explicit, hipStream_t s)
+{
+    const uint32_t nj = a.dbg_spikes ? 1u : a.lists;
+    if (a.direct || a.tl.T > kMaxTiles || a.tl.T != kGroups * a.tl.T8 || nj * a.tl.T8 > kMaxBuckets ||
+        a.tl.W > 65536 || a.pg1 == 0 || a.pg1 > kPushThreads || a.pslots == 0 || a.page_cap == 0 ||
+        (a.tl.T + a.pg1 - 1) / a.pg1 > kMaxSrcTiles)
         return hipErrorInvalidValue;
+    const dim3 grid(kGroups * a.pg1);
     if (a.m.fixed)
-        hipLaunchKernelGGL(k_bin<true>, dim3(bin_grid()), dim3(kBinThreads), 0, s, a, i, t_explicit);
+        hipLaunchKernelGGL(k_push<true>, grid, dim3(kPushThreads), 0, s, a, i, t_explicit);
     else
-        hipLaunchKernelGGL(k_bin<false>, dim3(bin_grid()), dim3(kBinThreads), 0, s, a, i, t_explicit);
+        hipLaunchKernelGGL(k_push<false>, grid, dim3(kPushThreads), 0, s, a, i, t_explicit);
     return hipGetLastError();
 }
 
 hipError_t launch_tile(const StepArgs &a, uint32_t i, int64_t t_explicit, hipStream_t s)
 {
-    if (a.tl.W > kMaxTileW || a.m.pois_len > 256 || a.list_hi <= a.list_lo ||
-        a.list_hi - a.list_lo > kMaxLists || a.tl.T != kGroups * a.tl.T8)
+    if (a.tl.W > kMaxTileW || a.m.pois_len > 256 || a.tl.T != kGroups * a.tl.T8 || a.tl.T > kMaxTiles ||
+        (!a.direct && (a.pg1 == 0 || a.pg1 > kTileThreads || a.pslots == 0)) || a.spk_slots == 0 ||
+        (a.direct && a.spk_slots <= a.dmin && !a.dbg_out))
         return hipErrorInvalidValue;
     if (a.m.fixed)
         hipLaunchKernelGGL(k_tile<true>, dim3(a.tl.T), dim3(kTileThreads), 0, s, a, i, t_explicit);
@@ -656,7 +787,8 @@ hipError_t launch_tile(const StepArgs &a, uint32_t i, int64_t t_explicit, hipStr
 
 hipError_t launch_record(const StepArgs &a, uint32_t i, int64_t t_explicit, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_record, dim3(1), dim3(256), 0, s, a, i, t_explicit);
+    if (a.tl.T > kMaxTiles) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_record, dim3(1), dim3(kTileThreads), 0, s, a, i, t_explicit);
     return hipGetLastError();
 }
 

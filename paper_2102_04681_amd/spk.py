@@ -57,10 +57,10 @@ class spk_stats_t(C.Structure):
         ("n", C.c_uint64), ("nnz", C.c_uint64), ("steps", C.c_uint64),
         ("device_bytes", C.c_uint64),
         ("n_exc", C.c_uint32), ("ref_steps", C.c_uint32), ("ring_slots", C.c_uint32),
-        ("delay_lists", C.c_uint32), ("max_piece", C.c_uint32), ("pois_len", C.c_uint32),
+        ("delay_lists", C.c_uint32), ("max_row", C.c_uint32), ("pois_len", C.c_uint32),
         ("fixed_shift", C.c_int32), ("k", C.c_float), ("bytes_per_synapse", C.c_double),
         ("tile_width", C.c_uint32), ("tiles", C.c_uint32), ("delivery", C.c_uint32),
-        ("bin_chunk", C.c_uint32),
+        ("page_cap", C.c_uint32),
     ]
 
 
@@ -259,7 +259,7 @@ class Net:
         st = self.stats()
         if cap is None:
             cap = max(1, int(st["nnz"]) if len(rows) > 64 else
-                      len(rows) * max(1, int(st["max_piece"])) * int(st["delay_lists"]))
+                      len(rows) * max(1, int(st["max_row"])))
         offs = np.zeros(len(rows) + 1, dtype=np.uint64)
         col = np.zeros(cap, dtype=np.uint32)
         w = np.zeros(cap, dtype=np.float32)

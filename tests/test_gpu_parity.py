@@ -119,7 +119,7 @@ def test_generator_equals_oracle(spk, name, mk):
     fixed = cfg["acc_mode"] == I.ACC_FIXED
     _compare_rows(offs, col, w, d, o_rp, o_col, o_w, o_d, range(cfg["n"]), fixed)
     # out-degree bookkeeping and the maximum run length
-    assert st["max_piece"] >= 1
+    assert st["max_row"] >= 1
 
 
 def test_fig_adj_delivery(spk):
