@@ -66,7 +66,7 @@ enum { SPK_ACC_F32 = 0, SPK_ACC_FIXED = 1 };
  * rows at arrival (best for one delay and long rows); BINNED reads every
  * fired row once, right after the spike, and files its events by (arrival
  * step, target tile) in pages that the tile drains at arrival.  BINNED needs
- * (delay_max - delay_min + 1) * tiles / 8 <= 4096. */
+ * (delay_max - delay_min + 1) * tiles / 8 <= 2048. */
 enum { SPK_DELIVERY_AUTO = 0, SPK_DELIVERY_DIRECT = 1, SPK_DELIVERY_BINNED = 2 };
 
 /* Network parameters (plain data).

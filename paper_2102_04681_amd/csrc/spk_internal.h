@@ -16,7 +16,7 @@ constexpr uint32_t kGroups = 8;        // one target group per XCD (blockIdx % 8
 constexpr uint32_t kMaxTileW = 8192;   // neurons per tile (LDS accumulators + spike list)
 constexpr uint32_t kMaxT8 = 256;       // tiles per group
 constexpr uint32_t kMaxTiles = kGroups * kMaxT8;
-constexpr uint32_t kMaxBuckets = 4096; // (delay, tile) buckets of one group in the push kernel
+constexpr uint32_t kMaxBuckets = 2048; // (delay, tile) buckets of one group in the push kernel
 constexpr uint32_t kMaxRow = 65535;    // synapses per source row (16-bit run offsets)
 // A stored synapse is int2 {delay index << 24 | target, weight bits}: the
 // target needs at most 24 bits (n <= 2^24), the delay index j = d - dmin < 64.

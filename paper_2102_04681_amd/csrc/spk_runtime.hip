@@ -410,7 +410,7 @@ spk_status choose_delivery(spk_net *net, RowIndex *ix)
     if (!binned_ok || net->P.delivery == SPK_DELIVERY_DIRECT) direct = true;
     if (net->P.delivery == SPK_DELIVERY_BINNED) {
         if (!binned_ok)
-            return fail(SPK_EINVAL, "binned delivery supports at most 4096 (delay, tile) buckets per "
+            return fail(SPK_EINVAL, "binned delivery supports at most 2048 (delay, tile) buckets per "
                                     "XCD group; use fewer delays or direct delivery");
         direct = false;
     }

@@ -43,7 +43,6 @@ constexpr int kPushR = 16;                                // events per thread p
 constexpr uint32_t kLoadPhase = kPushR * kPushThreads;    // events loaded at once
 constexpr uint32_t kStage = kLoadPhase / 2;               // events bucket-sorted at once
 constexpr uint32_t kMaxChunkSpikes = 1024;                // rows resolved per push chunk
-constexpr uint32_t kMaxSrcTiles = 64;                     // source tiles per push block
 constexpr int kRounds = kMaxTileW / kTileThreads;         // neurons per tile thread
 static_assert(kMaxTiles <= 2 * kTileThreads, "spike-count prefix takes at most two tiles per thread");
 
@@ -91,6 +90,28 @@ __device__ uint32_t block_scan_u32(uint32_t x, uint32_t *ws /*>=16*/, uint32_t *
         tot += v;
     }
     lds_sync();
+    *total = tot;
+    return before + inc - x;
+}
+
+// Same, without the trailing barrier: ws must not be written again before
+// the caller's next barrier.
+__device__ uint32_t block_scan_u32_open(uint32_t x, uint32_t *ws /*>=16*/, uint32_t *total)
+{
+    const uint32_t lane = lane_id(), w = threadIdx.x / kWave, nw = blockDim.x / kWave;
+    uint32_t inc = x;
+    for (int o = 1; o < kWave; o <<= 1) {
+        const uint32_t y = __shfl_up(inc, o);
+        if (lane >= (uint32_t)o) inc += y;
+    }
+    if (lane == kWave - 1) ws[w] = inc;
+    lds_sync();
+    uint32_t before = 0, tot = 0;
+    for (uint32_t k = 0; k < nw; k++) {
+        const uint32_t v = ws[k];
+        before += k < w ? v : 0u;
+        tot += v;
+    }
     *total = tot;
     return before + inc - x;
 }
@@ -210,25 +231,25 @@ __device__ __forceinline__ void overflow_add(const StepArgs &a, uint32_t slot, u
 
 struct PushLDS {
     int2 stage[kStage];              // bucket-sorted events {bucket << 16 | local, weight}
-    uint32_t spec[kPushThreads];     // spike IDs fetched with the counts
-    uint32_t tpre[kMaxSrcTiles + 1]; // prefix of the source tiles' spike counts
+    uint32_t pre[kMaxTiles + 1];     // prefix of the source tiles' spike counts
     uint32_t cpre[kMaxChunkSpikes + 1];  // prefix of the rows' 64-event chunk counts
     uint16_t crow[kPushR * (kPushThreads / kWave)];  // row of every chunk of the window
     uint32_t plen[kMaxChunkSpikes];
     uint64_t pbase[kMaxChunkSpikes];
     uint32_t bcnt[kMaxBuckets];      // events per bucket in this half, then rank cursor
     uint32_t bst[kMaxBuckets];       // bucket starts in the stage
+    uint32_t wb[kMaxBuckets];        // page position of stage entry q is wb[b] + q
     uint32_t fill[kMaxBuckets];      // records already in the bucket's page
     uint32_t pidx[kMaxBuckets];      // page of the bucket
-    uint32_t ws[16];
+    uint32_t ws[16], ws2[16];
     unsigned long long ws64[16];
 };
 
-// Block (x, g1) takes the spikes of step t of the source tiles g1, g1 + G1,
-// ..., reads the runs of their rows that target group x, and appends the
-// events to its own pages, bucket b = j * T8 + c (delay index j, tile c of
-// the group).  Dependent memory round trips: spike counts and IDs (together),
-// row descriptors, synapses; the page writes are not waited for.
+// Block (x, g1) takes the g1-th equal share of the spikes of step t, reads
+// the runs of their rows that target group x, and appends the events to its
+// own pages, bucket b = j * T8 + c (delay index j, tile c of the group).
+// Dependent memory round trips: spike counts, spike IDs, row descriptors,
+// synapses; the page writes are not waited for.
 template <bool FIXED>
 __global__ __launch_bounds__(kPushThreads) void k_push(StepArgs a, uint32_t i, int64_t t_explicit)
 {
@@ -241,41 +262,16 @@ __global__ __launch_bounds__(kPushThreads) void k_push(StepArgs a, uint32_t i, i
     const uint32_t NB = (dbg ? 1u : a.lists) * tl.T8;
     const uint32_t sslot = (uint32_t)(t % a.spk_slots);
 
-    // 0. counts of this block's source tiles and, in the same round trip,
-    //    the first S spike IDs of each; fill counters of the block's pages
-    const uint32_t ntb = dbg ? 0u : (tl.T > g1 ? (tl.T - g1 + G1 - 1) / G1 : 0u);
-    const uint32_t S = ntb ? kPushThreads / ntb : 0u;
-    {
-        const uint32_t si = S ? tid / S : 0u, sk = S ? tid % S : 0u;
-        const bool mine = si < ntb;
-        const uint64_t seg = (uint64_t)sslot * tl.T + (mine ? g1 + si * G1 : 0u);
-        const uint32_t c = a.spk_cnt[seg];
-        const uint32_t id = a.spk_ids[seg * tl.W + (sk < tl.W ? sk : 0u)];
-        L.spec[tid] = id;
-        if (mine && sk == 0) L.tpre[si + 1] = c < tl.W ? c : tl.W;
-    }
+    // 0. the spike counts of every source tile (their prefix gives each
+    //    block an equal share of the spikes) and the block's fill counters
     for (uint32_t b = tid; b < NB; b += kPushThreads) {
         const uint32_t p = page_of(a, x, g1, arrival_slot(a, t, b / tl.T8, dbg), b % tl.T8);
         L.pidx[b] = p;
         L.fill[b] = a.pfill[p];
         L.bcnt[b] = 0;
     }
-    lds_sync();
-    if (tid < kWave) {  // inclusive scan of at most 64 tile counts
-        uint32_t v = tid < ntb ? L.tpre[tid + 1] : 0u;
-        for (int o = 1; o < kWave; o <<= 1) {
-            const uint32_t y = __shfl_up(v, o);
-            if (tid >= (uint32_t)o) v += y;
-        }
-        if (tid < ntb) L.tpre[tid + 1] = v;
-        if (tid == 0) L.tpre[0] = 0;
-    }
-    lds_sync();
-    uint32_t k0 = 0, k1 = L.tpre[ntb];
-    if (dbg) {
-        k0 = (uint32_t)((uint64_t)a.dbg_n * g1 / G1);
-        k1 = (uint32_t)((uint64_t)a.dbg_n * (g1 + 1) / G1);
-    }
+    const uint32_t M = dbg ? a.dbg_n : load_spike_set(a, sslot, L.pre, L.ws);
+    const uint32_t k0 = (uint32_t)((uint64_t)M * g1 / G1), k1 = (uint32_t)((uint64_t)M * (g1 + 1) / G1);
     const uint32_t xlo = x * tl.Gw;
     const uint64_t cap = a.page_cap;
     uint64_t emitted = 0;
@@ -286,16 +282,7 @@ __global__ __launch_bounds__(kPushThreads) void k_push(StepArgs a, uint32_t i, i
         uint64_t base = 0;
         if (tid < K) {
             const uint32_t k = c0 + tid;
-            uint32_t s;
-            if (dbg) {
-                s = a.dbg_spikes[k];
-            } else {
-                uint32_t si = 0;
-                while (si + 1 < ntb && L.tpre[si + 1] <= k) si++;
-                const uint32_t r = k - L.tpre[si];
-                s = r < S ? L.spec[si * S + r]
-                          : a.spk_ids[((uint64_t)sslot * tl.T + g1 + si * G1) * tl.W + r];
-            }
+            const uint32_t s = dbg ? a.dbg_spikes[k] : spike_at(a, L.pre, sslot, k);
             const RowDesc *d = a.desc + s;
             const uint32_t lo = x ? d->gend[x - 1] : 0u, hi = d->gend[x];
             len = hi - lo;
@@ -364,18 +351,24 @@ __global__ __launch_bounds__(kPushThreads) void k_push(StepArgs a, uint32_t i, i
                     rec[r].x = (int)((b << 16) | (local & (tl.W - 1)));
                 }
                 lds_sync();
+                // bucket starts in the stage; the page position of staged event
+                // q of bucket b is wb[b] + q (mod 2^32); the fill counters advance
                 uint32_t staged;
-                {   // bucket starts: exclusive scan of the half's counts
+                {
                     const uint32_t P = (NB + kPushThreads - 1) / kPushThreads;
                     const uint32_t b0 = tid * P;
                     uint32_t sum = 0;
                     for (uint32_t k = 0; k < P; k++)
                         if (b0 + k < NB) sum += L.bcnt[b0 + k];
-                    uint32_t ex = block_scan_u32(sum, L.ws, &staged);
+                    uint32_t ex = block_scan_u32_open(sum, h ? L.ws : L.ws2, &staged);
                     for (uint32_t k = 0; k < P; k++) {
                         if (b0 + k < NB) {
-                            L.bst[b0 + k] = ex;
-                            ex += L.bcnt[b0 + k];
+                            const uint32_t bb = b0 + k, cnt = L.bcnt[bb], f = L.fill[bb];
+                            L.bst[bb] = ex;
+                            L.wb[bb] = f - ex;
+                            L.fill[bb] = f + cnt;
+                            L.bcnt[bb] = 0;
+                            ex += cnt;
                         }
                     }
                 }
@@ -386,10 +379,13 @@ __global__ __launch_bounds__(kPushThreads) void k_push(StepArgs a, uint32_t i, i
                     L.stage[L.bst[tr[rr] >> 16] + (tr[rr] & 0xffffu)] = rec[h * R + rr];
                 }
                 lds_sync();
+                // no barrier after the write-out: the next half's first barrier
+                // follows every thread's write-out, and only then are wb and the
+                // stage rewritten
                 for (uint32_t q = tid; q < staged; q += kPushThreads) {
                     const int2 r2 = L.stage[q];
                     const uint32_t b = (uint32_t)r2.x >> 16, local = (uint32_t)r2.x & 0xffffu;
-                    const uint64_t pos = (uint64_t)L.fill[b] + (q - L.bst[b]);
+                    const uint32_t pos = L.wb[b] + q;
                     if (pos < cap) {
                         a.pages[(uint64_t)L.pidx[b] * cap + pos] = make_int2((int)local, r2.y);
                     } else {
@@ -397,15 +393,10 @@ __global__ __launch_bounds__(kPushThreads) void k_push(StepArgs a, uint32_t i, i
                         overflow_add<FIXED>(a, arrival_slot(a, t, b / tl.T8, dbg), x * tl.T8 + c, local, r2.y);
                     }
                 }
-                lds_sync();
-                for (uint32_t b = tid; b < NB; b += kPushThreads) {
-                    L.fill[b] += L.bcnt[b];
-                    L.bcnt[b] = 0;
-                }
-                lds_sync();
             }
         }
     }
+    lds_sync();
     for (uint32_t b = tid; b < NB; b += kPushThreads) a.pfill[L.pidx[b]] = L.fill[b];
     if (!dbg && x == 0) {  // events emitted at t, counted once per spike
         const uint64_t tot = block_sum_u64(emitted, L.ws64);
@@ -761,8 +752,7 @@ hipError_t launch_push(const StepArgs &a, uint32_t i, int64_t t_explicit, hipStr
 {
     const uint32_t nj = a.dbg_spikes ? 1u : a.lists;
     if (a.direct || a.tl.T > kMaxTiles || a.tl.T != kGroups * a.tl.T8 || nj * a.tl.T8 > kMaxBuckets ||
-        a.tl.W > 65536 || a.pg1 == 0 || a.pg1 > kPushThreads || a.pslots == 0 || a.page_cap == 0 ||
-        (a.tl.T + a.pg1 - 1) / a.pg1 > kMaxSrcTiles)
+        a.tl.W > 65536 || a.pg1 == 0 || a.pg1 > kPushThreads || a.pslots == 0 || a.page_cap == 0)
         return hipErrorInvalidValue;
     const dim3 grid(kGroups * a.pg1);
     if (a.m.fixed)
