@@ -481,6 +481,8 @@ spk_status finish_rows(spk_net *net)
             if (v >= 1 && v <= (1ll << 30)) cap = (uint64_t)v;
         }
         cap = std::max<uint64_t>(16, (cap + 15) / 16 * 16);
+        if (n_pages * cap >= (1ull << 32))  // page records are addressed with 32-bit indices
+            return fail(SPK_EINVAL, "page capacity too large: pages x records must stay below 2^32");
         net->page_cap = (uint32_t)cap;
         const size_t acc_elems = (size_t)net->pslots * tl.T * tl.W;
         SPK_TRY(dalloc(net, &net->pages, n_pages * cap));

@@ -233,7 +233,8 @@ struct PushLDS {
     int2 stage[kStage];              // bucket-sorted events {bucket << 16 | local, weight}
     uint32_t pre[kMaxTiles + 1];     // prefix of the source tiles' spike counts
     uint32_t cpre[kMaxChunkSpikes + 1];  // prefix of the rows' 64-event chunk counts
-    uint16_t crow[kPushR * (kPushThreads / kWave)];  // row of every chunk of the window
+    uint64_t cbase[kPushR * (kPushThreads / kWave)];  // first synapse of every chunk of the window
+    uint32_t clen[kPushR * (kPushThreads / kWave)];   // its number of events (0 past the end)
     uint32_t plen[kMaxChunkSpikes];
     uint64_t pbase[kMaxChunkSpikes];
     uint32_t bcnt[kMaxBuckets];      // events per bucket in this half, then rank cursor
@@ -307,10 +308,16 @@ __global__ __launch_bounds__(kPushThreads) void k_push(StepArgs a, uint32_t i, i
         //    land while the first is sorted)
         constexpr uint32_t kWin = kPushR * nw;  // chunks per load phase
         for (uint32_t i0 = 0; i0 < C; i0 += kWin) {
-            // chunk -> row map of the window, written by each row's thread
+            // the window's chunks (start, length), written by each row's thread
+            for (uint32_t c = tid; c < kWin; c += kPushThreads) L.clen[c] = 0;
+            lds_sync();
             if (tid < K) {
                 const uint32_t cb = coff > i0 ? coff : i0, ce = coff + nch < i0 + kWin ? coff + nch : i0 + kWin;
-                for (uint32_t c = cb; c < ce; c++) L.crow[c - i0] = (uint16_t)tid;
+                for (uint32_t c = cb; c < ce; c++) {
+                    const uint32_t o = (c - coff) * kWave;
+                    L.cbase[c - i0] = base + o;
+                    L.clen[c - i0] = len - o < kWave ? len - o : kWave;
+                }
             }
             lds_sync();
             // every load is issued unconditionally (lanes past the end read
@@ -320,16 +327,10 @@ __global__ __launch_bounds__(kPushThreads) void k_push(StepArgs a, uint32_t i, i
             uint32_t okm = 0;  // bit u: rec[u] is an event
 #pragma unroll
             for (int u = 0; u < kPushR; u++) {
-                const uint32_t cl = u * nw + w, ci = i0 + cl;
-                uint64_t idx = 0;
-                if (ci < C) {
-                    const uint32_t k = L.crow[cl];
-                    const uint32_t o = (ci - L.cpre[k]) * kWave + lane;
-                    if (o < L.plen[k]) {
-                        idx = L.pbase[k] + o;
-                        okm |= 1u << u;
-                    }
-                }
+                const uint32_t cl = u * nw + w;
+                const bool ok = lane < L.clen[cl];
+                const uint64_t idx = ok ? L.cbase[cl] + lane : 0ull;
+                okm |= (uint32_t)ok << u;
                 rec[u] = a.syn[idx];
             }
 #pragma unroll
@@ -411,7 +412,8 @@ struct TileLDS {
     typename Acc<FIXED>::T acc[kMaxTileW];
     uint16_t spk[kMaxTileW];
     uint32_t pre[kMaxTiles + 1];   // direct: spike-count prefix; binned: page prefix
-    uint16_t cpage[kTileThreads / kWave * 16];  // binned: page of every chunk of the window
+    uint32_t cbase[kTileThreads / kWave * 16];  // binned: first record of every chunk of the window
+    uint32_t clen[kTileThreads / kWave * 16];   // its number of records (0 past the end)
     uint32_t wpre[kTileThreads / kWave][kWave + 1];
     uint64_t wbeg[kTileThreads / kWave][kWave];
     uint32_t ws[16];
@@ -571,26 +573,27 @@ __global__ __launch_bounds__(kTileThreads) void k_tile(StepArgs a, uint32_t i, i
         constexpr uint32_t kWin = kDrain * nw;
         const uint32_t nchp = (ne + kWave - 1) / kWave;
         for (uint32_t i0 = 0; i0 < C; i0 += kWin) {
-            // chunk -> page map of the window, written by each page's thread
+            // the window's chunks (first record, length), written by each page's thread
+            for (uint32_t c = tid; c < kWin; c += kTileThreads) L.clen[c] = 0;
+            lds_sync();
             if (tid < G1) {
                 const uint32_t cb = cex > i0 ? cex : i0, ce = cex + nchp < i0 + kWin ? cex + nchp : i0 + kWin;
-                for (uint32_t c = cb; c < ce; c++) L.cpage[c - i0] = (uint16_t)tid;
+                const uint32_t pbase = page_of(a, x, tid, pslot, cl) * cap;
+                for (uint32_t c = cb; c < ce; c++) {
+                    const uint32_t o = (c - cex) * kWave;
+                    L.cbase[c - i0] = pbase + o;
+                    L.clen[c - i0] = ne - o < kWave ? ne - o : kWave;
+                }
             }
             lds_sync();
             int2 r[kDrain];
             uint32_t okm = 0;
 #pragma unroll
             for (int u = 0; u < kDrain; u++) {
-                const uint32_t cw = u * nw + w, ci = i0 + cw;
-                uint64_t idx = 0;
-                if (ci < C) {
-                    const uint32_t g = L.cpage[cw];
-                    const uint32_t o = (ci - L.pre[g]) * kWave + lane;
-                    if (o < pn[g]) {
-                        idx = (uint64_t)page_of(a, x, g, pslot, cl) * cap + o;
-                        okm |= 1u << u;
-                    }
-                }
+                const uint32_t cw = u * nw + w;
+                const bool ok = lane < L.clen[cw];
+                const uint32_t idx = ok ? L.cbase[cw] + lane : 0u;
+                okm |= (uint32_t)ok << u;
                 r[u] = a.pages[idx];  // unconditional, see the push kernel
             }
 #pragma unroll

@@ -272,14 +272,17 @@ def test_fixed_point_simulation_bit_identical(spk, name, mk, T, delivery, profil
 
 
 @pytest.mark.parametrize("acc", [I.ACC_F32, I.ACC_FIXED], ids=["f32", "fixed"])
-def test_bin_overflow_fallback(spk, acc):
+def test_bin_overflow_fallback(spk, acc, monkeypatch):
     # 64 neurons, 200 synapses each (multapses), all above threshold at t=0:
-    # one tile receives 12 800 events at step 1, more than its bin holds
-    # (4 096), so the global-atomic fallback must deliver the rest.
+    # the one tile receives 12 800 events at step 1, ~400 per push block,
+    # while every page is capped at 64 records, so the global-atomic
+    # fallback must deliver the rest (in the simulation and in debug_deliver).
+    monkeypatch.setenv("SPK_PAGE_CAP", "64")
     cfg = I.config(4, n=64, k_out=200, delay_min=1, delay_max=1, v0_lo=-49.0, v0_hi=-49.0,
                    t_ref_ms=0.0, acc_mode=acc, delivery=2)
     T = 6
     g = spk.Net(cfg, max_steps=T, raster_capacity=64 * T)
+    assert g.stats()["page_cap"] == 64
     spikes = np.arange(64, dtype=np.uint32)
     got = g.debug_deliver(spikes)
     o = oracle.Net(cfg)
