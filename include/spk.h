@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define SPK_ABI_VERSION 1u
+#define SPK_ABI_VERSION 2u
 #define SPK_MAX_DELAY_LISTS 64u  /* delay_max - delay_min + 1 must not exceed this */
 
 typedef enum {
@@ -68,6 +68,14 @@ enum { SPK_ACC_F32 = 0, SPK_ACC_FIXED = 1 };
  * step, target tile) in pages that the tile drains at arrival.  BINNED needs
  * (delay_max - delay_min + 1) * tiles / 8 <= 2048. */
 enum { SPK_DELIVERY_AUTO = 0, SPK_DELIVERY_DIRECT = 1, SPK_DELIVERY_BINNED = 2 };
+/* Synapse storage (same results, different size): FULL keeps 8 bytes per
+ * synapse (delay index and target in 32 bits, the 32-bit weight beside them);
+ * COMPACT keeps 4 (delay index, target and a 2-bit weight class; the weight of
+ * each class is held once), which needs a network with at most 4 distinct
+ * weights: population weights (the paper's static models keep one weight per
+ * source population, Sec. III-A), or an explicit adjacency with at most 4
+ * distinct weights.  AUTO picks COMPACT whenever it applies. */
+enum { SPK_FORMAT_AUTO = 0, SPK_FORMAT_FULL = 1, SPK_FORMAT_COMPACT = 2 };
 
 /* Network parameters (plain data).
  *
@@ -122,6 +130,7 @@ typedef struct {
     double src_rate_hz;
     int32_t fixed_shift;       /* 0..30 */
     uint32_t delivery;         /* SPK_DELIVERY_*: how events reach their target tile */
+    uint32_t syn_format;       /* SPK_FORMAT_*: synapse storage */
     uint64_t max_steps;        /* >= 1 */
     uint64_t raster_capacity;  /* spike IDs; 0 = no raster */
 } spk_params;
@@ -134,7 +143,7 @@ typedef struct {
     uint32_t pois_len;
     int32_t fixed_shift;       /* fixed mode: S; fp32 mode: the unit 2^-S64 of the exact sums */
     float k;
-    double bytes_per_synapse;  /* synapse storage / nnz (8 = int32 target + 32-bit weight) */
+    double bytes_per_synapse;  /* synapse storage / nnz: 8 (FULL) or 4 (COMPACT) */
     uint32_t tile_width;       /* target neurons per tile (one workgroup each) */
     uint32_t tiles;
     uint32_t delivery;         /* SPK_DELIVERY_DIRECT or SPK_DELIVERY_BINNED as chosen */

@@ -3,7 +3,9 @@
 // synapse) for gfx950 (MI355X, wave64).
 //
 // Layout produced: one row per source neuron at [row_ptr[s], row_ptr[s+1]),
-// synapse = int2 {j << 24 | target, weight bits}, j = delay - delay_min.
+// synapse = int2 {j << 24 | target, weight bits} (full format) or u32
+// {class << 30 | j << 24 | target} (compact format: at most four distinct
+// weights, looked up by class), j = delay - delay_min.
 // Every row is grouped by target tile (the paper keeps rows sorted by target,
 // Sec. III-A, so that each target range of a row is one contiguous run; only
 // the grouping matters for delivery, the order inside a tile does not).  The
@@ -46,6 +48,25 @@ __device__ __forceinline__ int32_t weight_bits(const ConnArgs &c, float w)
 __device__ __forceinline__ int2 make_syn(uint32_t j, uint32_t tgt, int32_t wbits)
 {
     return make_int2((int)((j << kTargetBits) | tgt), wbits);
+}
+
+// Synapse e of a row, in the format of the network.  Compact classes:
+// generated rows have one weight per source population (class 0 excitatory,
+// 1 inhibitory); explicit rows name their weight's class in cls_w.
+__device__ __forceinline__ void put_syn(const ConnArgs &c, void *syn, uint64_t e, uint32_t j, uint32_t tgt,
+                                        uint32_t src, float w)
+{
+    if (c.compact) {
+        uint32_t cls = src < c.n_exc ? 0u : 1u;
+        if (c.kind == SPK_CONN_EXPLICIT) {
+            cls = 0;
+            for (uint32_t k = 1; k < kMaxClasses; k++)
+                if (c.cls_w[k] == __float_as_uint(w)) cls = k;
+        }
+        ((uint32_t *)syn)[e] = (cls << kClassShift) | (j << kTargetBits) | tgt;
+    } else {
+        ((int2 *)syn)[e] = make_syn(j, tgt, weight_bits(c, w));
+    }
 }
 
 __device__ __forceinline__ uint32_t lane_id() { return threadIdx.x & (kWave - 1); }
@@ -156,7 +177,7 @@ __global__ __launch_bounds__(kBlock) void k_gen_count_rows(ConnArgs c, uint32_t 
 
 // Draw the row twice: once to count per tile, once to place.
 __global__ __launch_bounds__(kBlock) void k_gen_fill_rows(ConnArgs c, const uint64_t *row_ptr,
-                                                         int2 *syn, RowIndex ix)
+                                                         void *syn, RowIndex ix)
 {
     __shared__ RowLDS L;
     const uint32_t s = blockIdx.x, tid = threadIdx.x;
@@ -177,7 +198,7 @@ __global__ __launch_bounds__(kBlock) void k_gen_fill_rows(ConnArgs c, const uint
             const uint32_t j = c.lists > 1 ? hash_range(mix64(rd ^ (uint64_t)tgt), c.lists) : 0;
             const float w = syn_weight(c, s, mix64(rw ^ (uint64_t)tgt));
             const uint32_t pos = atomicAdd(&L.cur[tile_of(c, tgt)], 1u);
-            syn[beg + pos] = make_syn(j, tgt, weight_bits(c, w));
+            put_syn(c, syn, beg + pos, j, tgt, s, w);
         }
     } else {
         const uint64_t rt = mix64(c.keys.tgt ^ (uint64_t)s);
@@ -190,7 +211,7 @@ __global__ __launch_bounds__(kBlock) void k_gen_fill_rows(ConnArgs c, const uint
             const uint32_t j = c.lists > 1 ? hash_range(mix64(rd ^ (uint64_t)q), c.lists) : 0;
             const float w = syn_weight(c, s, mix64(rw ^ (uint64_t)q));
             const uint32_t pos = atomicAdd(&L.cur[tile_of(c, tgt)], 1u);
-            syn[beg + pos] = make_syn(j, tgt, weight_bits(c, w));
+            put_syn(c, syn, beg + pos, j, tgt, s, w);
         }
     }
 }
@@ -216,7 +237,7 @@ __global__ __launch_bounds__(kBlock) void k_gen_in_count(ConnArgs c, uint32_t *c
 }
 
 __global__ __launch_bounds__(kBlock) void k_gen_in_fill(ConnArgs c, const uint64_t *row_ptr,
-                                                       uint32_t *cursor, int2 *syn)
+                                                       uint32_t *cursor, void *syn)
 {
     const uint32_t tgt = blockIdx.x;
     const uint64_t re = mix64(c.keys.src_e ^ (uint64_t)tgt);
@@ -229,26 +250,27 @@ __global__ __launch_bounds__(kBlock) void k_gen_in_fill(ConnArgs c, const uint64
         const uint32_t j = c.lists > 1 ? hash_range(mix64(rd ^ (uint64_t)q), c.lists) : 0;
         const float w = syn_weight(c, src, mix64(rw ^ (uint64_t)q));
         const uint32_t pos = atomicAdd(&cursor[src], 1u);
-        syn[row_ptr[src] + pos] = make_syn(j, tgt, weight_bits(c, w));
+        put_syn(c, syn, row_ptr[src] + pos, j, tgt, src, w);
     }
 }
 
 // Explicit adjacency (host-given rows, already in row order): encode.
 __global__ __launch_bounds__(kBlock) void k_csr_fill(ConnArgs c, uint64_t nnz, const uint32_t *in_col,
                                                     const float *in_w, const uint8_t *in_delay,
-                                                    int2 *syn)
+                                                    void *syn)
 {
     for (uint64_t e = (uint64_t)blockIdx.x * kBlock + threadIdx.x; e < nnz;
          e += (uint64_t)gridDim.x * kBlock) {
         const uint32_t j = in_delay ? (uint32_t)in_delay[e] - c.dmin : 0u;
-        syn[e] = make_syn(j, in_col[e], weight_bits(c, in_w[e]));
+        put_syn(c, syn, e, j, in_col[e], 0u, in_w[e]);
     }
 }
 
 // Group the synapses of every row of src by target tile into dst (same
 // row_ptr) and write the row's tile boundaries.  Blocks stride over rows.
+template <class R>
 __global__ __launch_bounds__(kBlock) void k_bucket_rows(ConnArgs c, const uint64_t *row_ptr,
-                                                       const int2 *src, int2 *dst, RowIndex ix)
+                                                       const R *src, R *dst, RowIndex ix)
 {
     __shared__ RowLDS L;
     for (uint32_t s = blockIdx.x; s < c.n; s += gridDim.x) {
@@ -256,12 +278,12 @@ __global__ __launch_bounds__(kBlock) void k_bucket_rows(ConnArgs c, const uint64
         const uint32_t len = (uint32_t)(row_ptr[s + 1] - beg);
         zero_tiles(L, c.tl.T);
         for (uint32_t e = threadIdx.x; e < len; e += kBlock)
-            atomicAdd(&L.cur[tile_of(c, (uint32_t)src[beg + e].x & kTargetMask)], 1u);
+            atomicAdd(&L.cur[tile_of(c, rec_target(rec_key(src[beg + e])))], 1u);
         scan_tiles(L, c.tl.T);
         write_row_index(c, ix, L, s, beg, len);
         for (uint32_t e = threadIdx.x; e < len; e += kBlock) {
-            const int2 r = src[beg + e];
-            const uint32_t pos = atomicAdd(&L.cur[tile_of(c, (uint32_t)r.x & kTargetMask)], 1u);
+            const R r = src[beg + e];
+            const uint32_t pos = atomicAdd(&L.cur[tile_of(c, rec_target(rec_key(r)))], 1u);
             dst[beg + pos] = r;
         }
         __syncthreads();
@@ -359,13 +381,20 @@ __global__ __launch_bounds__(kBlock) void k_out_degree(const uint64_t *row_ptr, 
 
 // Per-target sum of |weight| over all in-synapses: exact in quantised units
 // (fixed mode), or an upper bound in units of 2^-24 (fp32 mode: each term
-// rounded up), used to size the accumulators.
-__global__ __launch_bounds__(kBlock) void k_in_abs_sum(const int2 *syn, uint64_t nnz, int fixed,
+// rounded up), used to size the accumulators.  Compact synapses take the
+// term of their class from the table (the same value).
+__global__ __launch_bounds__(kBlock) void k_in_abs_sum(const void *syn, uint64_t nnz, int fixed,
+                                                      int compact, ClassTab tab,
                                                       unsigned long long *insum)
 {
     for (uint64_t e = (uint64_t)blockIdx.x * kBlock + threadIdx.x; e < nnz;
          e += (uint64_t)gridDim.x * kBlock) {
-        const int2 x = syn[e];
+        if (compact) {
+            const uint32_t x = ((const uint32_t *)syn)[e];
+            atomicAdd(&insum[rec_target(x)], (unsigned long long)tab.abs[rec_class(x)]);
+            continue;
+        }
+        const int2 x = ((const int2 *)syn)[e];
         unsigned long long q;
         if (fixed) {
             q = (unsigned long long)(x.y < 0 ? -(long long)x.y : (long long)x.y);
@@ -405,20 +434,28 @@ __global__ __launch_bounds__(kBlock) void k_init_state(ModelArgs m, float v0_lo,
 // ---------------------------------------------------------------- export
 
 // One block per requested row: decode (target, delay, weight bits).
-__global__ __launch_bounds__(kBlock) void k_export_gather(const uint64_t *row_ptr, const int2 *syn,
-                                                         uint32_t dmin, const uint32_t *rows,
-                                                         const uint64_t *out_off, uint32_t *col,
-                                                         uint32_t *wbits, uint8_t *delay)
+__global__ __launch_bounds__(kBlock) void k_export_gather(const uint64_t *row_ptr, const void *syn,
+                                                         int compact, ClassTab tab, uint32_t dmin,
+                                                         const uint32_t *rows, const uint64_t *out_off,
+                                                         uint32_t *col, uint32_t *wbits, uint8_t *delay)
 {
     const uint64_t r = blockIdx.x;
     const uint32_t s = rows[r];
     const uint64_t beg = row_ptr[s], L = row_ptr[s + 1] - beg;
     const uint64_t o = out_off[r];
     for (uint64_t e = threadIdx.x; e < L; e += kBlock) {
-        const int2 x = syn[beg + e];
-        col[o + e] = (uint32_t)x.x & kTargetMask;
-        wbits[o + e] = (uint32_t)x.y;
-        delay[o + e] = (uint8_t)(dmin + ((uint32_t)x.x >> kTargetBits));
+        uint32_t key, wb;
+        if (compact) {
+            key = ((const uint32_t *)syn)[beg + e];
+            wb = tab.bits[rec_class(key)];
+        } else {
+            const int2 x = ((const int2 *)syn)[beg + e];
+            key = (uint32_t)x.x;
+            wb = (uint32_t)x.y;
+        }
+        col[o + e] = rec_target(key);
+        wbits[o + e] = wb;
+        delay[o + e] = (uint8_t)(dmin + rec_delay(key));
     }
 }
 
@@ -453,7 +490,7 @@ hipError_t gen_count_rows(const ConnArgs &c, uint32_t *cnt, hipStream_t s)
     return hipGetLastError();
 }
 
-hipError_t gen_fill_rows(const ConnArgs &c, const uint64_t *row_ptr, int2 *syn, RowIndex ix,
+hipError_t gen_fill_rows(const ConnArgs &c, const uint64_t *row_ptr, void *syn, RowIndex ix,
                          hipStream_t s)
 {
     if (c.tl.T > kMaxTiles) return hipErrorInvalidValue;
@@ -467,7 +504,7 @@ hipError_t gen_in_count(const ConnArgs &c, uint32_t *cnt, hipStream_t s)
     return hipGetLastError();
 }
 
-hipError_t gen_in_fill(const ConnArgs &c, const uint64_t *row_ptr, uint32_t *cursor, int2 *syn,
+hipError_t gen_in_fill(const ConnArgs &c, const uint64_t *row_ptr, uint32_t *cursor, void *syn,
                        hipStream_t s)
 {
     hipLaunchKernelGGL(k_gen_in_fill, dim3(c.n), dim3(kBlock), 0, s, c, row_ptr, cursor, syn);
@@ -475,7 +512,7 @@ hipError_t gen_in_fill(const ConnArgs &c, const uint64_t *row_ptr, uint32_t *cur
 }
 
 hipError_t csr_fill(const ConnArgs &c, uint64_t nnz, const uint32_t *in_col, const float *in_w,
-                    const uint8_t *in_delay, int2 *syn, hipStream_t s)
+                    const uint8_t *in_delay, void *syn, hipStream_t s)
 {
     if (!nnz) return hipSuccess;
     hipLaunchKernelGGL(k_csr_fill, dim3(grid_for(nnz, 65536)), dim3(kBlock), 0, s, c, nnz, in_col,
@@ -483,12 +520,17 @@ hipError_t csr_fill(const ConnArgs &c, uint64_t nnz, const uint32_t *in_col, con
     return hipGetLastError();
 }
 
-hipError_t bucket_rows(const ConnArgs &c, const uint64_t *row_ptr, const int2 *src, int2 *dst,
+hipError_t bucket_rows(const ConnArgs &c, const uint64_t *row_ptr, const void *src, void *dst,
                        RowIndex ix, hipStream_t s)
 {
     if (c.tl.T > kMaxTiles) return hipErrorInvalidValue;
     const uint32_t g = c.n < 65536u ? c.n : 65536u;
-    hipLaunchKernelGGL(k_bucket_rows, dim3(g ? g : 1), dim3(kBlock), 0, s, c, row_ptr, src, dst, ix);
+    if (c.compact)
+        hipLaunchKernelGGL(k_bucket_rows<uint32_t>, dim3(g ? g : 1), dim3(kBlock), 0, s, c, row_ptr,
+                           (const uint32_t *)src, (uint32_t *)dst, ix);
+    else
+        hipLaunchKernelGGL(k_bucket_rows<int2>, dim3(g ? g : 1), dim3(kBlock), 0, s, c, row_ptr,
+                           (const int2 *)src, (int2 *)dst, ix);
     return hipGetLastError();
 }
 
@@ -518,11 +560,12 @@ hipError_t out_degree(const uint64_t *row_ptr, uint32_t n, uint32_t *outdeg, hip
     return hipGetLastError();
 }
 
-hipError_t in_abs_sum(const int2 *syn, uint64_t nnz, bool fixed, uint64_t *insum, hipStream_t s)
+hipError_t in_abs_sum(const void *syn, uint64_t nnz, bool fixed, bool compact, const ClassTab &tab,
+                      uint64_t *insum, hipStream_t s)
 {
     if (!nnz) return hipSuccess;
     hipLaunchKernelGGL(k_in_abs_sum, dim3(grid_for(nnz, 65536)), dim3(kBlock), 0, s, syn, nnz,
-                       fixed ? 1 : 0, (unsigned long long *)insum);
+                       fixed ? 1 : 0, compact ? 1 : 0, tab, (unsigned long long *)insum);
     return hipGetLastError();
 }
 
@@ -540,14 +583,14 @@ hipError_t init_state(const ModelArgs &m, float v0_lo, float v0_hi, float *V, ui
     return hipGetLastError();
 }
 
-hipError_t export_gather(const uint64_t *row_ptr, const int2 *syn, uint32_t dmin, const uint32_t *rows,
-                         uint64_t n_rows, const uint64_t *out_off, uint32_t *col, uint32_t *wbits,
-                         uint8_t *delay, hipStream_t s)
+hipError_t export_gather(const uint64_t *row_ptr, const void *syn, bool compact, const ClassTab &tab,
+                         uint32_t dmin, const uint32_t *rows, uint64_t n_rows, const uint64_t *out_off,
+                         uint32_t *col, uint32_t *wbits, uint8_t *delay, hipStream_t s)
 {
     if (!n_rows) return hipSuccess;
     if (n_rows > 0x7fffffffull) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_export_gather, dim3((uint32_t)n_rows), dim3(kBlock), 0, s, row_ptr, syn, dmin,
-                       rows, out_off, col, wbits, delay);
+    hipLaunchKernelGGL(k_export_gather, dim3((uint32_t)n_rows), dim3(kBlock), 0, s, row_ptr, syn,
+                       compact ? 1 : 0, tab, dmin, rows, out_off, col, wbits, delay);
     return hipGetLastError();
 }
 

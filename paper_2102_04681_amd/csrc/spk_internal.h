@@ -18,10 +18,25 @@ constexpr uint32_t kMaxT8 = 256;       // tiles per group
 constexpr uint32_t kMaxTiles = kGroups * kMaxT8;
 constexpr uint32_t kMaxBuckets = 2048; // (delay, tile) buckets of one group in the push kernel
 constexpr uint32_t kMaxRow = 65535;    // synapses per source row (16-bit run offsets)
-// A stored synapse is int2 {delay index << 24 | target, weight bits}: the
+// Two synapse formats.  Full: int2 {j << 24 | target, weight bits}.  Compact
+// (networks with at most kMaxClasses distinct weights, e.g. one weight per
+// source population, as in the paper's static models): u32
+// {class << 30 | j << 24 | target}, the weight taken from a table.  The
 // target needs at most 24 bits (n <= 2^24), the delay index j = d - dmin < 64.
 constexpr uint32_t kTargetBits = 24;
 constexpr uint32_t kTargetMask = (1u << kTargetBits) - 1u;
+constexpr uint32_t kDelayMask = 0x3fu;
+constexpr uint32_t kMaxClasses = 4;
+constexpr uint32_t kClassShift = 30;
+__host__ __device__ __forceinline__ uint32_t rec_target(uint32_t x) { return x & kTargetMask; }
+__host__ __device__ __forceinline__ uint32_t rec_delay(uint32_t x) { return (x >> kTargetBits) & kDelayMask; }
+__host__ __device__ __forceinline__ uint32_t rec_class(uint32_t x) { return x >> kClassShift; }
+__host__ __device__ __forceinline__ uint32_t rec_key(int2 r) { return (uint32_t)r.x; }
+__host__ __device__ __forceinline__ uint32_t rec_key(uint32_t r) { return r; }
+
+// A compact page record (u16): class << 13 | local target (W <= 8192).
+constexpr uint32_t kPageClassShift = 13;
+constexpr uint32_t kPageLocalMask = (1u << kPageClassShift) - 1u;
 
 // Stream tags of the counter-based hash: one independent stream per kind of
 // random decision (connection, target, source, weight, delay, initial V,
@@ -100,6 +115,9 @@ struct ConnArgs {
     float w_exc, w_inh, w_lo, w_hi;
     uint32_t fixed;         // store quantised weights
     float qscale;           // 2^fixed_shift
+    uint32_t compact;       // write u32 records; generated rows: class = source population
+                            // (0 exc, 1 inh); explicit rows: class k where cls_w[k] = weight bits
+    uint32_t cls_w[kMaxClasses];
     Keys keys;
     Tiling tl;
 };
@@ -132,8 +150,11 @@ struct StepArgs {
     Tiling tl;
     uint32_t n, lists, dmin;
     uint32_t direct;             // 1: tiles read their runs of the due rows (one delay)
+    uint32_t compact;            // 1: u32 synapses and u16 page records, weights from wval
+    int64_t wval[kMaxClasses];   // compact: weight of each class in accumulator units
     const uint64_t *row_ptr;     // n + 1
-    const int2 *syn;             // {j << 24 | target, weight bits (fp32 or quantised int32)}
+    const int2 *syn;             // full: {j << 24 | target, weight bits (fp32 or quantised int32)}
+    const uint32_t *syn32;       // compact: class << 30 | j << 24 | target
     const RowDesc *desc;         // binned: n
     const uint16_t *toff;        // direct: T + 1 per row
     const uint32_t *outdeg;      // n
@@ -149,7 +170,8 @@ struct StepArgs {
     // binned delivery: pages of {local target, weight bits} records, one per
     // (group x, push block g1, arrival slot, tile of the group), each owned by
     // its push block; fill counters in the same order
-    int2 *pages;
+    int2 *pages;                 // full records {local target, weight bits}
+    uint16_t *pages16;           // compact records class << 13 | local target
     uint32_t *pfill;
     uint32_t page_cap;           // records per page
     uint32_t pslots;             // arrival slots (delay_max)
@@ -173,26 +195,33 @@ struct StepArgs {
 
 // spk_gen.hip -- connectivity expansion
 hipError_t gen_count_rows(const ConnArgs &c, uint32_t *cnt, hipStream_t s);
-hipError_t gen_fill_rows(const ConnArgs &c, const uint64_t *row_ptr, int2 *syn, RowIndex ix,
+hipError_t gen_fill_rows(const ConnArgs &c, const uint64_t *row_ptr, void *syn, RowIndex ix,
                          hipStream_t s);
 hipError_t gen_in_count(const ConnArgs &c, uint32_t *cnt, hipStream_t s);
-hipError_t gen_in_fill(const ConnArgs &c, const uint64_t *row_ptr, uint32_t *cursor, int2 *syn,
+hipError_t gen_in_fill(const ConnArgs &c, const uint64_t *row_ptr, uint32_t *cursor, void *syn,
                        hipStream_t s);
 hipError_t csr_fill(const ConnArgs &c, uint64_t nnz, const uint32_t *in_col, const float *in_w,
-                    const uint8_t *in_delay, int2 *syn, hipStream_t s);
-hipError_t bucket_rows(const ConnArgs &c, const uint64_t *row_ptr, const int2 *src, int2 *dst,
+                    const uint8_t *in_delay, void *syn, hipStream_t s);
+hipError_t bucket_rows(const ConnArgs &c, const uint64_t *row_ptr, const void *src, void *dst,
                        RowIndex ix, hipStream_t s);
 hipError_t scan_counts(const uint32_t *cnt, uint64_t m, uint64_t *out, uint64_t *block_sums,
                        uint32_t *max_count, hipStream_t s);
 size_t scan_scratch_elems(uint64_t m);
 hipError_t out_degree(const uint64_t *row_ptr, uint32_t n, uint32_t *outdeg, hipStream_t s);
-hipError_t in_abs_sum(const int2 *syn, uint64_t nnz, bool fixed, uint64_t *insum, hipStream_t s);
+// Per-class values of compact synapses: the stored weight bits (fp32, or the
+// quantised int32 in fixed mode) and the |weight| term of in_abs_sum.
+struct ClassTab {
+    uint32_t bits[kMaxClasses];
+    uint64_t abs[kMaxClasses];
+};
+hipError_t in_abs_sum(const void *syn, uint64_t nnz, bool fixed, bool compact, const ClassTab &tab,
+                      uint64_t *insum, hipStream_t s);
 hipError_t max_u64(const uint64_t *x, uint64_t m, uint64_t *out, hipStream_t s);
 hipError_t init_state(const ModelArgs &m, float v0_lo, float v0_hi, float *V, uint8_t *ref,
                       hipStream_t s);
-hipError_t export_gather(const uint64_t *row_ptr, const int2 *syn, uint32_t dmin, const uint32_t *rows,
-                         uint64_t n_rows, const uint64_t *out_off, uint32_t *col, uint32_t *wbits,
-                         uint8_t *delay, hipStream_t s);
+hipError_t export_gather(const uint64_t *row_ptr, const void *syn, bool compact, const ClassTab &tab,
+                         uint32_t dmin, const uint32_t *rows, uint64_t n_rows, const uint64_t *out_off,
+                         uint32_t *col, uint32_t *wbits, uint8_t *delay, hipStream_t s);
 int cu_count();
 
 // spk_step.hip -- one simulation step = tile (+ push) (+ record); i = step

@@ -150,7 +150,14 @@ struct spk_net {
     bool own_stream = false;
     int device = 0;
     uint64_t *row_ptr = nullptr;
+    // synapses: full (int2) or compact (u32 with a weight class)
+    bool compact = false;
+    uint32_t n_cls = 0;
+    float cls_w[kMaxClasses] = {};
+    ClassTab ctab{};
+    long long wval[kMaxClasses] = {};
     int2 *syn = nullptr;
+    uint32_t *syn32 = nullptr;
     RowDesc *desc = nullptr;
     uint16_t *toff = nullptr;
     uint32_t *outdeg = nullptr;
@@ -160,6 +167,7 @@ struct spk_net {
     uint64_t *events8 = nullptr, *delivered8 = nullptr, *pois_dev = nullptr, *t_base = nullptr;
     uint16_t *guide_dev = nullptr;
     int2 *pages = nullptr;
+    uint16_t *pages16 = nullptr;
     uint32_t *pfill = nullptr, *ovf_flag = nullptr;
     void *acc_ovf = nullptr;
     uint32_t *raster = nullptr;
@@ -236,7 +244,10 @@ StepArgs step_args(const spk_net *net)
     a.dmin = net->dmin;
     a.direct = net->direct ? 1u : 0u;
     a.row_ptr = net->row_ptr;
+    a.compact = net->compact ? 1u : 0u;
+    for (uint32_t k = 0; k < kMaxClasses; k++) a.wval[k] = net->wval[k];
     a.syn = net->syn;
+    a.syn32 = net->syn32;
     a.desc = net->desc;
     a.toff = net->toff;
     a.outdeg = net->outdeg;
@@ -249,6 +260,7 @@ StepArgs step_args(const spk_net *net)
     a.events8 = net->events8;
     a.delivered8 = net->delivered8;
     a.pages = net->pages;
+    a.pages16 = net->pages16;
     a.pfill = net->pfill;
     a.page_cap = net->page_cap;
     a.pslots = net->pslots;
@@ -285,9 +297,78 @@ ConnArgs conn_args(const spk_net *net)
     c.w_hi = net->P.w_hi;
     c.fixed = net->P.acc_mode == SPK_ACC_FIXED;
     c.qscale = std::ldexp(1.0f, net->P.fixed_shift);
+    c.compact = net->compact ? 1u : 0u;
+    for (uint32_t k = 0; k < kMaxClasses; k++) {
+        float w = net->cls_w[k < net->n_cls ? k : 0];
+        std::memcpy(&c.cls_w[k], &w, 4);
+    }
     c.keys = net->keys;
     c.tl = net->tl;
     return c;
+}
+
+// Synapse format.  classes = the distinct weights (null: per-synapse weights).
+// Class k stores its weight bits (fp32, or the quantised int32 in fixed mode)
+// and the |weight| term of the accumulator-range bound, both as the full
+// format would per synapse.
+spk_status choose_format(spk_net *net, const float *classes, uint32_t n_cls)
+{
+    const uint32_t f = net->P.syn_format;
+    const bool ok = classes && n_cls >= 1 && n_cls <= kMaxClasses;
+    if (f == SPK_FORMAT_COMPACT && !ok)
+        return fail(SPK_EINVAL, "the compact synapse format needs at most 4 distinct weights");
+    net->compact = ok && f != SPK_FORMAT_FULL;
+    net->n_cls = 0;
+    net->ctab = ClassTab{};
+    if (!net->compact) return SPK_OK;
+    const bool fixed = net->P.acc_mode == SPK_ACC_FIXED;
+    net->n_cls = n_cls;
+    for (uint32_t k = 0; k < kMaxClasses; k++) {
+        const float w = classes[k < n_cls ? k : 0];
+        net->cls_w[k] = w;
+        if (fixed) {
+            int32_t q = 0;
+            if (!quantise(w, net->P.fixed_shift, &q))
+                return fail(SPK_EOVERFLOW, "a weight does not fit int32 at this fixed_shift");
+            net->ctab.bits[k] = (uint32_t)q;
+            net->ctab.abs[k] = (uint64_t)std::llabs((long long)q);
+        } else {
+            std::memcpy(&net->ctab.bits[k], &w, 4);
+            net->ctab.abs[k] = (uint64_t)std::ceil(std::ldexp((double)std::fabs(w), 24));
+        }
+    }
+    return SPK_OK;
+}
+
+// Per-class accumulator units, once the unit is known.
+void class_units(spk_net *net)
+{
+    const bool fixed = net->P.acc_mode == SPK_ACC_FIXED;
+    for (uint32_t k = 0; k < kMaxClasses; k++) {
+        if (!net->compact) {
+            net->wval[k] = 0;
+        } else if (fixed) {
+            net->wval[k] = (long long)(int32_t)net->ctab.bits[k];
+        } else {
+            // exact: every weight is a multiple of the unit 2^-S64 (as the
+            // per-event conversion of the full format, rounded to nearest)
+            net->wval[k] = std::llrint(std::ldexp((double)net->cls_w[k], net->shift64));
+        }
+    }
+}
+
+// Synapse storage of the chosen format.
+spk_status alloc_syn(spk_net *net, void **p, uint64_t nnz)
+{
+    uint8_t *q = nullptr;
+    SPK_TRY(dalloc(net, &q, (size_t)nnz * (net->compact ? 4 : 8)));
+    *p = q;
+    return SPK_OK;
+}
+
+const void *syn_ptr(const spk_net *net)
+{
+    return net->compact ? (const void *)net->syn32 : (const void *)net->syn;
 }
 
 // Validate parameters and compute the derived constants.
@@ -307,6 +388,7 @@ spk_status derive(spk_net *net, bool explicit_csr)
     if (P.neuron_kind > SPK_SOURCE) return fail(SPK_EINVAL, "neuron_kind");
     if (P.acc_mode > SPK_ACC_FIXED) return fail(SPK_EINVAL, "acc_mode");
     if (P.delivery > SPK_DELIVERY_BINNED) return fail(SPK_EINVAL, "delivery");
+    if (P.syn_format > SPK_FORMAT_COMPACT) return fail(SPK_EINVAL, "syn_format");
     if (!explicit_csr && P.conn_kind > SPK_CONN_FIXED_IN) return fail(SPK_EINVAL, "conn_kind");
     if (!(P.p >= 0.0 && P.p <= 1.0)) return fail(SPK_EINVAL, "p in [0,1]");
     if (P.max_steps == 0) return fail(SPK_EINVAL, "max_steps must be >= 1");
@@ -342,6 +424,10 @@ spk_status derive(spk_net *net, bool explicit_csr)
             !quantise(P.w_exc, S, &dummy) || !quantise(P.w_inh, S, &dummy) ||
             !quantise(P.w_lo, S, &dummy) || !quantise(P.w_hi, S, &dummy))
             return fail(SPK_EOVERFLOW, "a weight does not fit int32 at this fixed_shift");
+    }
+    if (!explicit_csr) {  // population weights: class 0 excitatory, 1 inhibitory
+        const float w[2] = {P.w_exc, P.w_inh};
+        SPK_TRY(choose_format(net, P.w_uniform ? nullptr : w, 2));
     }
     const uint64_t seed = P.seed;
     net->keys.conn = stream_key(seed, TAG_CONN);
@@ -443,7 +529,7 @@ spk_status finish_rows(spk_net *net)
     SPK_TRY(dalloc(net, &mx, 1));
     SPK_HIP(hipMemsetAsync(insum, 0, (size_t)net->n * 8, s));
     SPK_HIP(hipMemsetAsync(mx, 0, 8, s));
-    SPK_HIP(in_abs_sum(net->syn, net->nnz, fixed, insum, s));
+    SPK_HIP(in_abs_sum(syn_ptr(net), net->nnz, fixed, net->compact, net->ctab, insum, s));
     SPK_HIP(max_u64(insum, net->n, mx, s));
     uint64_t m = 0;
     SPK_HIP(hipMemcpyAsync(&m, mx, 8, hipMemcpyDeviceToHost, s));
@@ -462,6 +548,7 @@ spk_status finish_rows(spk_net *net)
         const int e = M > 0.0 ? (int)std::ceil(std::log2(M)) : 0;
         net->shift64 = std::max(0, std::min(100, 52 - e));
     }
+    class_units(net);
 
     // Spike lists: direct delivery reads the lists of steps t - dmax .. t - dmin
     // while writing that of t; binned delivery consumes the list of t within t.
@@ -485,7 +572,8 @@ spk_status finish_rows(spk_net *net)
             return fail(SPK_EINVAL, "page capacity too large: pages x records must stay below 2^32");
         net->page_cap = (uint32_t)cap;
         const size_t acc_elems = (size_t)net->pslots * tl.T * tl.W;
-        SPK_TRY(dalloc(net, &net->pages, n_pages * cap));
+        if (net->compact) SPK_TRY(dalloc(net, &net->pages16, n_pages * cap));
+        else SPK_TRY(dalloc(net, &net->pages, n_pages * cap));
         SPK_TRY(dalloc(net, &net->pfill, n_pages));
         SPK_TRY(dalloc(net, &net->ovf_flag, (size_t)net->pslots * tl.T));
         SPK_TRY(dalloc(net, (uint64_t **)&net->acc_ovf, acc_elems));
@@ -510,17 +598,20 @@ spk_status generate(spk_net *net)
     SPK_TRY(finish_counts(net, cnt));
     RowIndex ix{};
     SPK_TRY(choose_delivery(net, &ix));
-    SPK_TRY(dalloc(net, &net->syn, net->nnz));
+    void *syn = nullptr;
+    SPK_TRY(alloc_syn(net, &syn, net->nnz));
+    if (net->compact) net->syn32 = (uint32_t *)syn;
+    else net->syn = (int2 *)syn;
     if (in_rows) {  // drawn per target: regroup by source, then bucket
-        int2 *tmp = nullptr;
-        SPK_TRY(dalloc(net, &tmp, net->nnz));
+        void *tmp = nullptr;
+        SPK_TRY(alloc_syn(net, &tmp, net->nnz));
         SPK_HIP(hipMemsetAsync(cnt, 0, (size_t)net->n * 4, s));
         SPK_HIP(gen_in_fill(c, net->row_ptr, cnt, tmp, s));
-        SPK_HIP(bucket_rows(c, net->row_ptr, tmp, net->syn, ix, s));
+        SPK_HIP(bucket_rows(c, net->row_ptr, tmp, syn, ix, s));
         SPK_HIP(hipStreamSynchronize(s));
         dfree(net, tmp);
     } else {        // drawn per source, bucketed while drawn
-        SPK_HIP(gen_fill_rows(c, net->row_ptr, net->syn, ix, s));
+        SPK_HIP(gen_fill_rows(c, net->row_ptr, syn, ix, s));
     }
     SPK_HIP(hipStreamSynchronize(s));
     dfree(net, cnt);
@@ -806,6 +897,20 @@ spk_status spk_create_from_csr(const spk_params *params, uint32_t n, const uint6
             max_row = std::max<uint64_t>(max_row, row_ptr[s + 1] - row_ptr[s]);
         }
         const uint64_t nnz = row_ptr[n];
+        std::vector<uint32_t> distinct;  // weight bit patterns, first-seen order, up to 5
+        for (uint64_t e = 0; e < nnz && distinct.size() <= kMaxClasses; e++) {
+            uint32_t b;
+            std::memcpy(&b, &w[e], 4);
+            if (std::find(distinct.begin(), distinct.end(), b) == distinct.end()) distinct.push_back(b);
+        }
+        {
+            float cls[kMaxClasses] = {};
+            const bool fits = distinct.size() <= kMaxClasses;
+            for (size_t k = 0; fits && k < distinct.size(); k++) std::memcpy(&cls[k], &distinct[k], 4);
+            if (fits && distinct.empty()) cls[0] = 0.0f;
+            SPK_TRY(choose_format(net, fits ? cls : nullptr,
+                                  fits ? std::max<uint32_t>(1, (uint32_t)distinct.size()) : 0));
+        }
         for (uint64_t e = 0; e < nnz; e++) {
             if (col[e] >= n) return fail(SPK_EINVAL, "target id out of range");
             const uint32_t d = delay ? delay[e] : net->P.delay_min;
@@ -826,10 +931,12 @@ spk_status spk_create_from_csr(const spk_params *params, uint32_t n, const uint6
         uint32_t *in_col = nullptr;
         float *in_w = nullptr;
         uint8_t *in_d = nullptr;
-        int2 *tmp = nullptr;
+        void *tmp = nullptr, *syn = nullptr;
         SPK_TRY(dalloc(net, &net->row_ptr, (size_t)n + 1));
-        SPK_TRY(dalloc(net, &net->syn, nnz));
-        SPK_TRY(dalloc(net, &tmp, nnz));
+        SPK_TRY(alloc_syn(net, &syn, nnz));
+        if (net->compact) net->syn32 = (uint32_t *)syn;
+        else net->syn = (int2 *)syn;
+        SPK_TRY(alloc_syn(net, &tmp, nnz));
         SPK_TRY(dalloc(net, &in_col, nnz));
         SPK_TRY(dalloc(net, &in_w, nnz));
         SPK_HIP(hipMemcpyAsync(net->row_ptr, row_ptr, ((size_t)n + 1) * 8, hipMemcpyHostToDevice, s));
@@ -843,7 +950,7 @@ spk_status spk_create_from_csr(const spk_params *params, uint32_t n, const uint6
         }
         ConnArgs c = conn_args(net);
         SPK_HIP(csr_fill(c, nnz, in_col, in_w, in_d, tmp, s));
-        SPK_HIP(bucket_rows(c, net->row_ptr, tmp, net->syn, ix, s));
+        SPK_HIP(bucket_rows(c, net->row_ptr, tmp, syn, ix, s));
         SPK_HIP(hipStreamSynchronize(s));
         dfree(net, tmp);
         dfree(net, in_col);
@@ -1007,7 +1114,10 @@ spk_status spk_debug_deliver(spk_net *net, const uint32_t *spikes, uint64_t n_sp
             const uint64_t n_pages = (uint64_t)kGroups * net->pg1 * tl.T8;
             const uint64_t cap = std::min<uint64_t>(kDebugPageCap, std::max<uint64_t>(16, net->page_cap));
             const size_t acc_elems = (size_t)tl.T * tl.W;
-            if ((st = scratch((void **)&a.pages, n_pages * cap * 8)) != SPK_OK) break;
+            void *pg = nullptr;
+            if ((st = scratch(&pg, n_pages * cap * (net->compact ? 2 : 8))) != SPK_OK) break;
+            a.pages = net->compact ? nullptr : (int2 *)pg;
+            a.pages16 = net->compact ? (uint16_t *)pg : nullptr;
             if ((st = scratch((void **)&a.pfill, n_pages * 4)) != SPK_OK) break;
             if ((st = scratch((void **)&a.ovf_flag, (size_t)tl.T * 4)) != SPK_OK) break;
             if ((st = scratch(&a.acc_ovf, acc_elems * 8)) != SPK_OK) break;
@@ -1059,7 +1169,8 @@ spk_status spk_export_rows(spk_net *net, const uint32_t *rows, uint64_t n_rows, 
     SPK_TRY(dalloc(net, &d_del, tot));
     SPK_HIP(hipMemcpyAsync(d_rows, rows, n_rows * 4, hipMemcpyHostToDevice, s));
     SPK_HIP(hipMemcpyAsync(d_off, offs, n_rows * 8, hipMemcpyHostToDevice, s));
-    SPK_HIP(export_gather(net->row_ptr, net->syn, net->dmin, d_rows, n_rows, d_off, d_col, d_wb, d_del, s));
+    SPK_HIP(export_gather(net->row_ptr, syn_ptr(net), net->compact, net->ctab, net->dmin, d_rows, n_rows, d_off,
+                          d_col, d_wb, d_del, s));
     std::vector<uint32_t> hc(tot), hw(tot);
     std::vector<uint8_t> hd(tot);
     if (tot) {
@@ -1119,7 +1230,7 @@ spk_status spk_stats(spk_net *net, spk_stats_t *out)
     st.pois_len = net->pois_len;
     st.fixed_shift = net->P.acc_mode == SPK_ACC_FIXED ? net->P.fixed_shift : net->shift64;
     st.k = net->k;
-    st.bytes_per_synapse = (double)sizeof(int2);
+    st.bytes_per_synapse = net->compact ? 4.0 : 8.0;
     st.tile_width = net->tl.W;
     st.tiles = net->tl.T;
     st.delivery = net->direct ? SPK_DELIVERY_DIRECT : SPK_DELIVERY_BINNED;

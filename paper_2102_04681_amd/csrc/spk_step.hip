@@ -201,36 +201,63 @@ __device__ __forceinline__ float fixed64_to_float(unsigned long long acc, int32_
     return (float)ldexp((double)(long long)acc, -s64);
 }
 
+// Accumulator units of one event: the stored weight bits converted
+// (full format), or the class's precomputed value (compact format).
+template <bool FIXED>
+__device__ __forceinline__ long long units_of(int32_t wbits, int32_t s64)
+{
+    return FIXED ? (long long)wbits : to_fixed64(wbits, s64);
+}
+// Selected without a dynamic index into the kernel arguments (which would
+// go through scratch memory).
+__device__ __forceinline__ long long class_units(const StepArgs &a, uint32_t cls)
+{
+    const long long w01 = cls & 1u ? a.wval[1] : a.wval[0];
+    const long long w23 = cls & 1u ? a.wval[3] : a.wval[2];
+    return cls & 2u ? w23 : w01;
+}
+
 template <bool FIXED> struct Acc;
 template <> struct Acc<true> {
     using T = int32_t;
-    static __device__ __forceinline__ void add(T *p, int32_t wbits, int32_t) { atomicAdd(p, wbits); }
+    static __device__ __forceinline__ void add(T *p, long long units) { atomicAdd(p, (int32_t)units); }
 };
 template <> struct Acc<false> {
     using T = unsigned long long;
-    static __device__ __forceinline__ void add(T *p, int32_t wbits, int32_t s64)
+    static __device__ __forceinline__ void add(T *p, long long units)
     {
-        atomicAdd(p, (unsigned long long)to_fixed64(wbits, s64));
+        atomicAdd(p, (unsigned long long)units);
     }
 };
 
+// Synapse record of each format, and its key (class, delay index, target).
+template <bool CMP> struct SynRec;
+template <> struct SynRec<false> {
+    using T = int2;
+    static __device__ __forceinline__ T load(const StepArgs &a, uint64_t e) { return a.syn[e]; }
+};
+template <> struct SynRec<true> {
+    using T = uint32_t;
+    static __device__ __forceinline__ T load(const StepArgs &a, uint64_t e) { return a.syn32[e]; }
+};
 // Global fallback for a full page (rare): same units as the LDS accumulator,
 // one accumulator per (arrival slot, neuron).
 template <bool FIXED>
 __device__ __forceinline__ void overflow_add(const StepArgs &a, uint32_t slot, uint32_t tile,
-                                             uint32_t local, int32_t wbits)
+                                             uint32_t local, long long units)
 {
     const uint64_t st = (uint64_t)slot * a.tl.T + tile;
     const uint64_t i = st * a.tl.W + local;
-    if (FIXED) atomicAdd((int32_t *)a.acc_ovf + i, wbits);
-    else atomicAdd((unsigned long long *)a.acc_ovf + i, (unsigned long long)to_fixed64(wbits, a.m.shift64));
+    if (FIXED) atomicAdd((int32_t *)a.acc_ovf + i, (int32_t)units);
+    else atomicAdd((unsigned long long *)a.acc_ovf + i, (unsigned long long)units);
     if (a.ovf_flag[st] == 0) atomicOr(&a.ovf_flag[st], 1u);
 }
 
 // ------------------------------------------------------------ push kernel
 
 struct PushLDS {
-    int2 stage[kStage];              // bucket-sorted events {bucket << 16 | local, weight}
+    int2 stage[kStage];              // bucket-sorted events {bucket << 16 | local, weight}; compact
+                                     // format: u32 bucket << 16 | class << 13 | local
     uint32_t pre[kMaxTiles + 1];     // prefix of the source tiles' spike counts
     uint32_t cpre[kMaxChunkSpikes + 1];  // prefix of the rows' 64-event chunk counts
     uint64_t cbase[kPushR * (kPushThreads / kWave)];  // first synapse of every chunk of the window
@@ -250,10 +277,12 @@ struct PushLDS {
 // the runs of their rows that target group x, and appends the events to its
 // own pages, bucket b = j * T8 + c (delay index j, tile c of the group).
 // Dependent memory round trips: spike counts, spike IDs, row descriptors,
-// synapses; the page writes are not waited for.
-template <bool FIXED>
+// synapses; the page writes are not waited for.  Compact synapses (CMP) give
+// 2-byte page records class << 13 | local.
+template <bool FIXED, bool CMP>
 __global__ __launch_bounds__(kPushThreads) void k_push(StepArgs a, uint32_t i, int64_t t_explicit)
 {
+    using Rec = typename SynRec<CMP>::T;
     __shared__ PushLDS L;
     const uint64_t t = step_index(a, i, t_explicit);
     const uint32_t x = blockIdx.x % kGroups, g1 = blockIdx.x / kGroups, G1 = a.pg1;
@@ -323,7 +352,7 @@ __global__ __launch_bounds__(kPushThreads) void k_push(StepArgs a, uint32_t i, i
             // every load is issued unconditionally (lanes past the end read
             // synapse 0 and drop it): a load under a branch would get its own
             // wait for all earlier loads
-            int2 rec[kPushR];
+            Rec rec[kPushR];
             uint32_t okm = 0;  // bit u: rec[u] is an event
 #pragma unroll
             for (int u = 0; u < kPushR; u++) {
@@ -331,7 +360,7 @@ __global__ __launch_bounds__(kPushThreads) void k_push(StepArgs a, uint32_t i, i
                 const bool ok = lane < L.clen[cl];
                 const uint64_t idx = ok ? L.cbase[cl] + lane : 0ull;
                 okm |= (uint32_t)ok << u;
-                rec[u] = a.syn[idx];
+                rec[u] = SynRec<CMP>::load(a, idx);
             }
 #pragma unroll
             for (int h = 0; h < 2; h++) {
@@ -343,13 +372,16 @@ __global__ __launch_bounds__(kPushThreads) void k_push(StepArgs a, uint32_t i, i
                     const int r = h * R + rr;
                     tr[rr] = 0xffffffffu;
                     if (!((okm >> r) & 1u)) continue;
-                    const uint32_t j = (uint32_t)rec[r].x >> kTargetBits;
+                    const uint32_t key = rec_key(rec[r]);
+                    const uint32_t j = rec_delay(key);
                     if (dbg && a.dbg_j >= 0 && (int32_t)j != a.dbg_j) continue;
-                    const uint32_t local = ((uint32_t)rec[r].x & kTargetMask) - xlo;
+                    const uint32_t local = rec_target(key) - xlo;
                     const uint32_t b = (dbg ? 0u : j) * tl.T8 + (local >> tl.logW);
                     const uint32_t rank = atomicAdd(&L.bcnt[b], 1u);
                     tr[rr] = (b << 16) | rank;
-                    rec[r].x = (int)((b << 16) | (local & (tl.W - 1)));
+                    const uint32_t sv = (b << 16) | (local & (tl.W - 1));
+                    if constexpr (CMP) rec[r] = sv | (rec_class(key) << kPageClassShift);
+                    else rec[r].x = (int)sv;
                 }
                 lds_sync();
                 // bucket starts in the stage; the page position of staged event
@@ -374,24 +406,37 @@ __global__ __launch_bounds__(kPushThreads) void k_push(StepArgs a, uint32_t i, i
                     }
                 }
                 lds_sync();
+                Rec *stage = (Rec *)L.stage;
 #pragma unroll
                 for (int rr = 0; rr < R; rr++) {
                     if (tr[rr] == 0xffffffffu) continue;
-                    L.stage[L.bst[tr[rr] >> 16] + (tr[rr] & 0xffffu)] = rec[h * R + rr];
+                    stage[L.bst[tr[rr] >> 16] + (tr[rr] & 0xffffu)] = rec[h * R + rr];
                 }
                 lds_sync();
                 // no barrier after the write-out: the next half's first barrier
                 // follows every thread's write-out, and only then are wb and the
                 // stage rewritten
                 for (uint32_t q = tid; q < staged; q += kPushThreads) {
-                    const int2 r2 = L.stage[q];
-                    const uint32_t b = (uint32_t)r2.x >> 16, local = (uint32_t)r2.x & 0xffffu;
+                    const Rec r2 = stage[q];
+                    const uint32_t key = rec_key(r2);
+                    const uint32_t b = key >> 16, low = key & 0xffffu;
                     const uint32_t pos = L.wb[b] + q;
                     if (pos < cap) {
-                        a.pages[(uint64_t)L.pidx[b] * cap + pos] = make_int2((int)local, r2.y);
+                        const uint64_t e = (uint64_t)L.pidx[b] * cap + pos;
+                        if constexpr (CMP) a.pages16[e] = (uint16_t)low;
+                        else a.pages[e] = make_int2((int)low, r2.y);
                     } else {
                         const uint32_t c = b % tl.T8;
-                        overflow_add<FIXED>(a, arrival_slot(a, t, b / tl.T8, dbg), x * tl.T8 + c, local, r2.y);
+                        long long units;
+                        uint32_t local;
+                        if constexpr (CMP) {
+                            units = class_units(a, low >> kPageClassShift);
+                            local = low & kPageLocalMask;
+                        } else {
+                            units = units_of<FIXED>(r2.y, a.m.shift64);
+                            local = low;
+                        }
+                        overflow_add<FIXED>(a, arrival_slot(a, t, b / tl.T8, dbg), x * tl.T8 + c, local, units);
                     }
                 }
             }
@@ -428,10 +473,11 @@ struct TileLDS {
 // l's run for this tile; the 64 runs are then streamed lane-parallel.  With
 // jf >= 0 only synapses of delay index jf are delivered.  Returns the number
 // of events this thread delivered.
-template <bool FIXED>
+template <bool FIXED, bool CMP>
 __device__ uint32_t gather_direct(const StepArgs &a, TileLDS<FIXED> &L, uint32_t tile, uint32_t tile_lo,
                                   uint32_t P, uint32_t slot, int32_t jf)
 {
+    using Rec = typename SynRec<CMP>::T;
     const uint32_t lane = lane_id(), w = threadIdx.x / kWave, nw = kTileThreads / kWave;
     const uint32_t T1 = a.tl.T + 1;
     uint32_t mine = 0;
@@ -469,14 +515,18 @@ __device__ uint32_t gather_direct(const StepArgs &a, TileLDS<FIXED> &L, uint32_t
                 }
                 idx[u] = f < tot ? L.wbeg[w][lo] + (fc - L.wpre[w][lo]) : 0ull;
             }
-            int2 r[U];
+            Rec r[U];
 #pragma unroll
-            for (int u = 0; u < U; u++) r[u] = a.syn[idx[u]];  // unconditional, see push
+            for (int u = 0; u < U; u++) r[u] = SynRec<CMP>::load(a, idx[u]);  // unconditional, see push
 #pragma unroll
             for (int u = 0; u < U; u++) {
                 if (f0 + u * kWave + lane >= tot) continue;
-                if (jf >= 0 && (int32_t)((uint32_t)r[u].x >> kTargetBits) != jf) continue;
-                Acc<FIXED>::add(&L.acc[((uint32_t)r[u].x & kTargetMask) - tile_lo], r[u].y, a.m.shift64);
+                const uint32_t key = rec_key(r[u]);
+                if (jf >= 0 && (int32_t)rec_delay(key) != jf) continue;
+                long long units;
+                if constexpr (CMP) units = class_units(a, rec_class(key));
+                else units = units_of<FIXED>(r[u].y, a.m.shift64);
+                Acc<FIXED>::add(&L.acc[rec_target(key) - tile_lo], units);
                 mine++;
             }
         }
@@ -485,7 +535,7 @@ __device__ uint32_t gather_direct(const StepArgs &a, TileLDS<FIXED> &L, uint32_t
     return mine;
 }
 
-template <bool FIXED>
+template <bool FIXED, bool CMP>
 __global__ __launch_bounds__(kTileThreads) void k_tile(StepArgs a, uint32_t i, int64_t t_explicit)
 {
     __shared__ TileLDS<FIXED> L;
@@ -542,25 +592,29 @@ __global__ __launch_bounds__(kTileThreads) void k_tile(StepArgs a, uint32_t i, i
         // rows in this tile (only the synapses of delay d when there are several)
         uint64_t mine = 0;
         if (debug) {
-            mine = gather_direct<FIXED>(a, L, tile, tile_lo, a.dbg_n, 0, a.dbg_j);
+            mine = gather_direct<FIXED, CMP>(a, L, tile, tile_lo, a.dbg_n, 0, a.dbg_j);
         } else {
             for (uint32_t j = 0; j < a.lists; j++) {
                 const uint64_t d = (uint64_t)a.dmin + j;
                 if (t < d) break;
                 const uint32_t dslot = (uint32_t)((t - d) % a.spk_slots);
                 const uint32_t P = load_spike_set(a, dslot, L.pre, L.ws);
-                mine += gather_direct<FIXED>(a, L, tile, tile_lo, P, dslot, a.lists > 1 ? (int32_t)j : -1);
+                mine += gather_direct<FIXED, CMP>(a, L, tile, tile_lo, P, dslot, a.lists > 1 ? (int32_t)j : -1);
                 lds_sync();
             }
         }
         delivered = block_sum_u64(mine, L.ws64);
     } else {
-        // pages cut into chunks of 64 records; wave w drains chunks w, w + nw, ...
+        // pages cut into chunks of 64 loads (a load is one full record, or two
+        // compact ones: page capacities are multiples of 16 records, so a pair
+        // never straddles pages); wave w drains chunks w, w + nw, ...
+        constexpr uint32_t kPer = CMP ? 2u : 1u;
+        constexpr uint32_t kChunk = kPer * kWave;
         const uint32_t cap = a.page_cap, G1 = a.pg1;
         pf = tid < G1 ? pf : 0u;
         const uint32_t ne = pf < cap ? pf : cap;  // records stored in page tid
         uint32_t C;
-        const uint32_t cex = block_scan_u32((ne + kWave - 1) / kWave, L.ws, &C);
+        const uint32_t cex = block_scan_u32((ne + kChunk - 1) / kChunk, L.ws, &C);
         uint32_t *pn = L.pre + kTileThreads;      // record counts after the chunk prefix
         if (tid < G1) {
             L.pre[tid] = cex;
@@ -571,7 +625,7 @@ __global__ __launch_bounds__(kTileThreads) void k_tile(StepArgs a, uint32_t i, i
         constexpr uint32_t nw = kTileThreads / kWave;
         constexpr int kDrain = 16;  // loads in flight per lane before their atomics
         constexpr uint32_t kWin = kDrain * nw;
-        const uint32_t nchp = (ne + kWave - 1) / kWave;
+        const uint32_t nchp = (ne + kChunk - 1) / kChunk;
         for (uint32_t i0 = 0; i0 < C; i0 += kWin) {
             // the window's chunks (first record, length), written by each page's thread
             for (uint32_t c = tid; c < kWin; c += kTileThreads) L.clen[c] = 0;
@@ -580,25 +634,49 @@ __global__ __launch_bounds__(kTileThreads) void k_tile(StepArgs a, uint32_t i, i
                 const uint32_t cb = cex > i0 ? cex : i0, ce = cex + nchp < i0 + kWin ? cex + nchp : i0 + kWin;
                 const uint32_t pbase = page_of(a, x, tid, pslot, cl) * cap;
                 for (uint32_t c = cb; c < ce; c++) {
-                    const uint32_t o = (c - cex) * kWave;
-                    L.cbase[c - i0] = pbase + o;
-                    L.clen[c - i0] = ne - o < kWave ? ne - o : kWave;
+                    const uint32_t o = (c - cex) * kChunk;
+                    L.cbase[c - i0] = (pbase + o) / kPer;
+                    L.clen[c - i0] = ne - o < kChunk ? ne - o : kChunk;
                 }
             }
             lds_sync();
-            int2 r[kDrain];
-            uint32_t okm = 0;
+            if constexpr (CMP) {
+                const uint32_t *pw = (const uint32_t *)a.pages16;
+                uint32_t r[kDrain];
+                uint32_t okm = 0;  // bits 2u, 2u + 1: the two records of r[u]
 #pragma unroll
-            for (int u = 0; u < kDrain; u++) {
-                const uint32_t cw = u * nw + w;
-                const bool ok = lane < L.clen[cw];
-                const uint32_t idx = ok ? L.cbase[cw] + lane : 0u;
-                okm |= (uint32_t)ok << u;
-                r[u] = a.pages[idx];  // unconditional, see the push kernel
+                for (int u = 0; u < kDrain; u++) {
+                    const uint32_t cw = u * nw + w;
+                    const uint32_t len = L.clen[cw];
+                    const bool ok = 2 * lane < len;
+                    const uint32_t idx = ok ? L.cbase[cw] + lane : 0u;
+                    okm |= ((uint32_t)ok | (uint32_t)(2 * lane + 1 < len) << 1) << (2 * u);
+                    r[u] = pw[idx];  // unconditional, see the push kernel
+                }
+#pragma unroll
+                for (int u = 0; u < kDrain; u++) {
+#pragma unroll
+                    for (int hf = 0; hf < 2; hf++) {
+                        if (!((okm >> (2 * u + hf)) & 1u)) continue;
+                        const uint32_t rec = hf ? r[u] >> 16 : r[u] & 0xffffu;
+                        Acc<FIXED>::add(&L.acc[rec & kPageLocalMask], class_units(a, rec >> kPageClassShift));
+                    }
+                }
+            } else {
+                int2 r[kDrain];
+                uint32_t okm = 0;
+#pragma unroll
+                for (int u = 0; u < kDrain; u++) {
+                    const uint32_t cw = u * nw + w;
+                    const bool ok = lane < L.clen[cw];
+                    const uint32_t idx = ok ? L.cbase[cw] + lane : 0u;
+                    okm |= (uint32_t)ok << u;
+                    r[u] = a.pages[idx];  // unconditional, see the push kernel
+                }
+#pragma unroll
+                for (int u = 0; u < kDrain; u++)
+                    if ((okm >> u) & 1u) Acc<FIXED>::add(&L.acc[(uint32_t)r[u].x], units_of<FIXED>(r[u].y, m.shift64));
             }
-#pragma unroll
-            for (int u = 0; u < kDrain; u++)
-                if ((okm >> u) & 1u) Acc<FIXED>::add(&L.acc[(uint32_t)r[u].x], r[u].y, m.shift64);
             lds_sync();  // the window's map is read before the next one is written
         }
         if (tid < G1) a.pfill[page_of(a, x, tid, pslot, cl)] = 0;
@@ -757,11 +835,15 @@ hipError_t launch_push(const StepArgs &a, uint32_t i, int64_t t_explicit, hipStr
     if (a.direct || a.tl.T > kMaxTiles || a.tl.T != kGroups * a.tl.T8 || nj * a.tl.T8 > kMaxBuckets ||
         a.tl.W > 65536 || a.pg1 == 0 || a.pg1 > kPushThreads || a.pslots == 0 || a.page_cap == 0)
         return hipErrorInvalidValue;
-    const dim3 grid(kGroups * a.pg1);
-    if (a.m.fixed)
-        hipLaunchKernelGGL(k_push<true>, grid, dim3(kPushThreads), 0, s, a, i, t_explicit);
-    else
-        hipLaunchKernelGGL(k_push<false>, grid, dim3(kPushThreads), 0, s, a, i, t_explicit);
+    if (a.compact ? (!a.syn32 || !a.pages16) : (!a.syn || !a.pages)) return hipErrorInvalidValue;
+    const dim3 grid(kGroups * a.pg1), block(kPushThreads);
+    if (a.compact) {
+        if (a.m.fixed) hipLaunchKernelGGL((k_push<true, true>), grid, block, 0, s, a, i, t_explicit);
+        else hipLaunchKernelGGL((k_push<false, true>), grid, block, 0, s, a, i, t_explicit);
+    } else {
+        if (a.m.fixed) hipLaunchKernelGGL((k_push<true, false>), grid, block, 0, s, a, i, t_explicit);
+        else hipLaunchKernelGGL((k_push<false, false>), grid, block, 0, s, a, i, t_explicit);
+    }
     return hipGetLastError();
 }
 
@@ -771,10 +853,17 @@ hipError_t launch_tile(const StepArgs &a, uint32_t i, int64_t t_explicit, hipStr
         (!a.direct && (a.pg1 == 0 || a.pg1 > kTileThreads || a.pslots == 0)) || a.spk_slots == 0 ||
         (a.direct && a.spk_slots <= a.dmin && !a.dbg_out))
         return hipErrorInvalidValue;
-    if (a.m.fixed)
-        hipLaunchKernelGGL(k_tile<true>, dim3(a.tl.T), dim3(kTileThreads), 0, s, a, i, t_explicit);
-    else
-        hipLaunchKernelGGL(k_tile<false>, dim3(a.tl.T), dim3(kTileThreads), 0, s, a, i, t_explicit);
+    if (a.compact ? !a.syn32 || (!a.direct && !a.pages16) : !a.syn || (!a.direct && !a.pages))
+        return hipErrorInvalidValue;
+    if (!a.direct && (a.page_cap % 16)) return hipErrorInvalidValue;  // record pairs stay in their page
+    const dim3 grid(a.tl.T), block(kTileThreads);
+    if (a.compact) {
+        if (a.m.fixed) hipLaunchKernelGGL((k_tile<true, true>), grid, block, 0, s, a, i, t_explicit);
+        else hipLaunchKernelGGL((k_tile<false, true>), grid, block, 0, s, a, i, t_explicit);
+    } else {
+        if (a.m.fixed) hipLaunchKernelGGL((k_tile<true, false>), grid, block, 0, s, a, i, t_explicit);
+        else hipLaunchKernelGGL((k_tile<false, false>), grid, block, 0, s, a, i, t_explicit);
+    }
     return hipGetLastError();
 }
 

@@ -19,11 +19,12 @@ import numpy as np
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libspk.so")
 
 SPK_OK, SPK_EINVAL, SPK_ENOMEM, SPK_EHIP, SPK_EOVERFLOW, SPK_ESTATE = 0, -1, -2, -3, -4, -5
-SPK_ABI_VERSION = 1
+SPK_ABI_VERSION = 2
 SPK_LIF, SPK_SOURCE = 0, 1
 SPK_CONN_BERNOULLI, SPK_CONN_FIXED_OUT, SPK_CONN_FIXED_IN, SPK_CONN_EXPLICIT = 0, 1, 2, 3
 SPK_ACC_F32, SPK_ACC_FIXED = 0, 1
 SPK_DELIVERY_AUTO, SPK_DELIVERY_DIRECT, SPK_DELIVERY_BINNED = 0, 1, 2
+SPK_FORMAT_AUTO, SPK_FORMAT_FULL, SPK_FORMAT_COMPACT = 0, 1, 2
 
 EXPORTED = [
     "spk_preset", "spk_create", "spk_create_from_csr", "spk_step", "spk_sync",
@@ -48,7 +49,7 @@ class spk_params(C.Structure):
         ("delay_min", C.c_uint32), ("delay_max", C.c_uint32),
         ("ext_lambda", C.c_double), ("ext_w", C.c_float), ("acc_mode", C.c_uint32),
         ("src_rate_hz", C.c_double), ("fixed_shift", C.c_int32), ("delivery", C.c_uint32),
-        ("max_steps", C.c_uint64), ("raster_capacity", C.c_uint64),
+        ("syn_format", C.c_uint32), ("max_steps", C.c_uint64), ("raster_capacity", C.c_uint64),
     ]
 
 

@@ -13,6 +13,8 @@ Bar (per the method's two accumulation modes):
   - fp32 mode: mean firing rate within 1 % (the oracle adds fp32 inputs one
     by one in push order, the library rounds the exact sum once, so spike
     trains diverge chaotically after the first difference).
+Both synapse formats (8-byte full records, 4-byte compact records with a
+weight class) are held to the same bar.
 Sizes span several tiles, many delay lists, ragged row lengths and the bin
 overflow path.
 """
@@ -46,11 +48,11 @@ _ORACLE_RUNS = {}
 
 
 def _key(cfg):
-    return tuple(sorted((k, v) for k, v in cfg.items() if k != "delivery"))
+    return tuple(sorted((k, v) for k, v in cfg.items() if k not in ("delivery", "syn_format")))
 
 
 def _oracle_net(cfg):
-    """Oracle network for cfg (the delivery strategy does not change it)."""
+    """Oracle network for cfg (delivery strategy and synapse format do not change it)."""
     k = _key(cfg)
     if k not in _ORACLE_NETS:
         _ORACLE_NETS.clear()
@@ -106,14 +108,21 @@ GEN_CASES = [
 ]
 
 
+FORMATS = [(1, "full"), (0, "auto")]
+
+
 @pytest.mark.parametrize("name,mk", GEN_CASES, ids=[c[0] for c in GEN_CASES])
-def test_generator_equals_oracle(spk, name, mk):
+@pytest.mark.parametrize("fmt", [f for f, _ in FORMATS], ids=[n for _, n in FORMATS])
+def test_generator_equals_oracle(spk, name, mk, fmt):
     cfg = mk()
-    _say(f"[gen] {name} n={cfg['n']}")
+    cfg["syn_format"] = fmt
+    _say(f"[gen] {name} n={cfg['n']} format={fmt}")
     g = spk.Net(cfg, max_steps=1)
     o = oracle.Net(cfg)
     o_rp, o_col, o_w, o_d = o.csr()
     st = g.stats()
+    # population weights are stored compactly unless the full format is asked for
+    assert st["bytes_per_synapse"] == (4.0 if fmt == 0 and not cfg["w_uniform"] else 8.0)
     assert st["nnz"] == len(o_col)
     offs, col, w, d = g.csr()
     fixed = cfg["acc_mode"] == I.ACC_FIXED
@@ -125,9 +134,11 @@ def test_generator_equals_oracle(spk, name, mk):
 def test_fig_adj_delivery(spk):
     fx = I.fig_adj()
     for acc in (I.ACC_F32, I.ACC_FIXED):
-        cfg = I.explicit_params(fx["n"], acc_mode=acc)
-        _say(f"[fig_adj] acc={acc}")
+      for fmt in (1, 2):
+        cfg = I.explicit_params(fx["n"], acc_mode=acc, syn_format=fmt)
+        _say(f"[fig_adj] acc={acc} format={fmt}")
         g = spk.Net(cfg, max_steps=1, csr=(fx["row_ptr"], fx["col"], fx["w"], fx["delay"]))
+        assert g.stats()["bytes_per_synapse"] == (8.0 if fmt == 1 else 4.0)
         out = g.debug_deliver(fx["spikes"])
         want = np.array(fx["expect_input"], dtype=np.float64)
         if acc == I.ACC_FIXED:
@@ -179,9 +190,11 @@ DELIVERY = [(0, "auto"), (1, "direct"), (2, "binned")]
 @pytest.mark.parametrize("name,mk,delays", DELIVER_CASES, ids=[c[0] for c in DELIVER_CASES])
 @pytest.mark.parametrize("acc", [I.ACC_F32, I.ACC_FIXED], ids=["f32", "fixed"])
 @pytest.mark.parametrize("delivery", [1, 2], ids=["direct", "binned"])
-def test_debug_deliver_matches_oracle(spk, name, mk, delays, acc, delivery):
+@pytest.mark.parametrize("fmt", [f for f, _ in FORMATS], ids=[n for _, n in FORMATS])
+def test_debug_deliver_matches_oracle(spk, name, mk, delays, acc, delivery, fmt):
     cfg = mk(acc)
     cfg["delivery"] = delivery
+    cfg["syn_format"] = fmt
     n = cfg["n"]
     g = spk.Net(cfg, max_steps=1)
     assert g.stats()["delivery"] == delivery
@@ -235,13 +248,15 @@ RUN_CASES = [
 @pytest.mark.parametrize("name,mk,T", RUN_CASES, ids=[c[0] for c in RUN_CASES])
 @pytest.mark.parametrize("delivery", [1, 2], ids=["direct", "binned"])
 @pytest.mark.parametrize("profiled", [False, True], ids=["graph", "launch"])
-def test_fixed_point_simulation_bit_identical(spk, name, mk, T, delivery, profiled):
+@pytest.mark.parametrize("fmt", [f for f, _ in FORMATS], ids=[n for _, n in FORMATS])
+def test_fixed_point_simulation_bit_identical(spk, name, mk, T, delivery, profiled, fmt):
     cfg = mk()
     cfg["acc_mode"] = I.ACC_FIXED
     cfg["delivery"] = delivery
+    cfg["syn_format"] = fmt
     if profiled and name not in ("C0-driven", "C4-12000"):
         pytest.skip("direct-launch path checked on two shapes")
-    _say(f"[run] {name} n={cfg['n']} T={T} delivery={delivery} profiled={profiled}")
+    _say(f"[run] {name} n={cfg['n']} T={T} delivery={delivery} profiled={profiled} format={fmt}")
     g = spk.Net(cfg, max_steps=T, raster_capacity=cfg["n"] * T)
     g.set_profiling(profiled)
     g.step(T)
@@ -272,14 +287,15 @@ def test_fixed_point_simulation_bit_identical(spk, name, mk, T, delivery, profil
 
 
 @pytest.mark.parametrize("acc", [I.ACC_F32, I.ACC_FIXED], ids=["f32", "fixed"])
-def test_bin_overflow_fallback(spk, acc, monkeypatch):
+@pytest.mark.parametrize("fmt", [f for f, _ in FORMATS], ids=[n for _, n in FORMATS])
+def test_bin_overflow_fallback(spk, acc, fmt, monkeypatch):
     # 64 neurons, 200 synapses each (multapses), all above threshold at t=0:
     # the one tile receives 12 800 events at step 1, ~400 per push block,
     # while every page is capped at 64 records, so the global-atomic
     # fallback must deliver the rest (in the simulation and in debug_deliver).
     monkeypatch.setenv("SPK_PAGE_CAP", "64")
     cfg = I.config(4, n=64, k_out=200, delay_min=1, delay_max=1, v0_lo=-49.0, v0_hi=-49.0,
-                   t_ref_ms=0.0, acc_mode=acc, delivery=2)
+                   t_ref_ms=0.0, acc_mode=acc, delivery=2, syn_format=fmt)
     T = 6
     g = spk.Net(cfg, max_steps=T, raster_capacity=64 * T)
     assert g.stats()["page_cap"] == 64
@@ -378,3 +394,64 @@ def test_fp32_mode_mean_rate_within_one_percent(spk, seed):
     _say(f"[rate] seed={seed} gpu={rg} oracle={ro}")
     assert ro > 1e5
     assert abs(rg - ro) / ro < 0.01
+
+
+def _random_csr(n, n_w, seed):
+    """Ragged random adjacency (0..250 synapses per row, multapses allowed),
+    delays 1..12, weights drawn from n_w distinct values (n_w = 0: every
+    synapse its own weight)."""
+    rng = np.random.default_rng(seed)
+    deg = rng.integers(0, 251, n)
+    deg[rng.choice(n, n // 10, replace=False)] = 0
+    row_ptr = np.zeros(n + 1, np.uint64)
+    row_ptr[1:] = np.cumsum(deg)
+    nnz = int(row_ptr[-1])
+    col = rng.integers(0, n, nnz).astype(np.uint32)
+    delay = rng.integers(1, 13, nnz).astype(np.uint8)
+    if n_w:
+        vals = np.array([0.37, -1.25, 0.05, 2.0, -0.61][:n_w], np.float32)
+        w = vals[rng.integers(0, n_w, nnz)]
+    else:
+        w = rng.uniform(-1.0, 1.0, nnz).astype(np.float32)
+    return row_ptr, col, w, delay
+
+
+@pytest.mark.parametrize("n_w", [1, 3, 4, 5, 0], ids=["1w", "3w", "4w", "5w", "perw"])
+@pytest.mark.parametrize("fmt", [0, 1, 2], ids=["auto", "full", "compact"])
+def test_explicit_adjacency_formats(spk, n_w, fmt):
+    n = 3000
+    row_ptr, col, w, delay = _random_csr(n, n_w, seed=40 + n_w)
+    fits = 1 <= n_w <= 4
+    for acc in (I.ACC_FIXED, I.ACC_F32):
+        cfg = I.explicit_params(n, acc_mode=acc, delay_min=1, delay_max=12, syn_format=fmt,
+                                i_bias=1.2, v0_lo=-65.0, v0_hi=-50.0)
+        _say(f"[explicit] n_w={n_w} format={fmt} acc={acc}")
+        if fmt == 2 and not fits:
+            with pytest.raises(spk.SpkError) as e:
+                spk.Net(cfg, max_steps=1, csr=(row_ptr, col, w, delay))
+            assert e.value.code == spk.SPK_EINVAL
+            return
+        T = 60
+        g = spk.Net(cfg, max_steps=T, raster_capacity=n * T, csr=(row_ptr, col, w, delay))
+        compact = fmt == 2 or (fmt == 0 and fits)
+        assert g.stats()["bytes_per_synapse"] == (4.0 if compact else 8.0)
+        o = oracle.Net(cfg, csr=(row_ptr, col, w, delay))
+        rows = np.arange(0, n, 7, dtype=np.uint32)
+        offs, gc, gw, gd = g.export_rows(rows)
+        o_rp, o_col, o_w, o_d = o.csr()
+        _compare_rows(offs, gc, gw, gd, o_rp, o_col, o_w, o_d, rows, acc == I.ACC_FIXED)
+        spikes = I.spike_set(n, n // 3, seed=5, unique=True)
+        for dl in (0, 1, 12):
+            got = g.debug_deliver(spikes, delay=dl)
+            if acc == I.ACC_FIXED:
+                assert np.array_equal(got.astype(np.int64), o.deliver(spikes, delay=dl, fixed=True)[1])
+            else:
+                want = o.deliver(spikes, delay=dl)
+                ulp = np.spacing(np.abs(want).astype(np.float32)).astype(np.float64)
+                assert np.all(np.abs(got.astype(np.float64) - want) <= ulp)
+        if acc == I.ACC_FIXED:
+            g.step(T)
+            r = o.run(T)
+            assert r["counts"].sum() > 0
+            assert np.array_equal(g.raster()[1], r["raster"]), "rasters differ"
+            assert np.array_equal(g.state()[0].view(np.uint32), o.state()[0].view(np.uint32))
