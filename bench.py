@@ -3,20 +3,22 @@
 
 A step is one simulation timestep of the whole hot path: delivery of every
 event arriving at the step into LDS, the update of every neuron with spike
-compaction, and the filing of the new spikes' events by arrival step.  The default workload is the
-3-billion-synapse one-GPU network (2 000 000 LIF neurons, fan-out 1 500,
-delays 1..20 steps) with the external Poisson drive that keeps it active
-(without drive every neuron decays to rest and no synaptic event happens).
+compaction, and the filing of the new spikes' events by arrival step.  The
+default workload is the 3-billion-synapse one-GPU network (2 000 000 LIF
+neurons, fan-out 1 500, delays 1..20 steps) with the external Poisson drive
+that keeps it active (without drive every neuron decays to rest and no
+synaptic event happens).
 
     python bench.py [--steps K] [--warmup W] [--config 4] [--acc f32|fixed]
+                    [--mode auto|graph|persistent] [--format auto|full|compact]
 
 Prints one JSON line (the last line of stdout).  Timing: W untimed steps,
-then exactly K steps replayed from captured HIP graphs, bracketed by
-torch.cuda.synchronize(); events delivered are read from the device
-counters.  A second pass of K steps launches every kernel directly with HIP
-events around it (on the network's stream) to measure each kernel's average
-duration for the roofline figure.  The CPU oracle is timed on a bounded
-sample (reduced neuron count, same per-neuron statistics) for comparison.
+then exactly K steps (one persistent-kernel launch, or graph replays),
+bracketed by torch.cuda.synchronize(); events delivered are read from the
+device counters.  A second pass of K steps runs with HIP events around every
+kernel launch (on the network's stream) to measure the dominant kernel's
+average launch duration for the roofline figure.  The CPU oracle is timed on
+a bounded sample (reduced neuron count, same per-neuron statistics).
 """
 from __future__ import annotations
 
@@ -51,6 +53,10 @@ def parse():
     ap.add_argument("--rate", type=float, default=10.0, help="source rate (Hz) for config 3")
     ap.add_argument("--acc", choices=["f32", "fixed"], default="f32")
     ap.add_argument("--delivery", choices=["auto", "direct", "binned"], default="auto")
+    ap.add_argument("--mode", choices=["auto", "graph", "persistent"], default="auto",
+                    help="how steps are launched (spk_params.step_mode)")
+    ap.add_argument("--format", choices=["auto", "full", "compact"], default="auto",
+                    help="synapse storage (spk_params.syn_format)")
     ap.add_argument("--seed", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
@@ -65,23 +71,35 @@ def workload(args):
     acc = I.ACC_FIXED if args.acc == "fixed" else I.ACC_F32
     cfg = I.config(args.config, driven=True, seed=args.seed, rate_hz=args.rate, acc_mode=acc)
     cfg["delivery"] = {"auto": 0, "direct": 1, "binned": 2}[args.delivery]
+    cfg["step_mode"] = {"auto": 0, "graph": 1, "persistent": 2}[args.mode]
+    cfg["syn_format"] = {"auto": 0, "full": 1, "compact": 2}[args.format]
     return cfg
 
 
-def algorithmic_bytes(n, kind, events, spikes):
-    """Bytes the hot path must move per the method: 8 B per delivered event
-    (int32 target + 32-bit weight read once), 10 B per LIF neuron and step
-    (V read + write, refractory counter read + write; 8 B for a source
-    neuron, which has no counter), 8 B per spike (ID written once, read
-    once).  Accumulators are on chip and cost nothing."""
+def algorithmic_bytes(n, kind, events, spikes, per_event, steps):
+    """Bytes the hot path must move per the method: one stored synapse per
+    delivered event, read once (per_event: 8 B for a 32-bit target + 32-bit
+    weight, 4 B where the network has per-population weights and only the
+    target is stored, as the paper's adjacency list does), 10 B per LIF
+    neuron and step (V read + write, refractory counter read + write; 8 B
+    for a source neuron, which has no counter), 8 B per spike (ID written
+    once, read once).  Accumulators are on chip and cost nothing.  events and
+    spikes are totals over `steps` steps; returns (event bytes, neuron and
+    spike bytes) over those steps."""
     per_neuron = 8 if kind == 1 else 10
-    return 8.0 * events, per_neuron * float(n) + 8.0 * spikes
+    return per_event * events, per_neuron * float(n) * steps + 8.0 * spikes
+
+
+STEP_SOURCES = ("spk_internal.h", "spk_dev.h", "spk_step.hip", "spk_run.hip")
 
 
 def step_source_sha():
+    """Hash of the sources of the step kernels (counter summaries are valid
+    only for the code they were taken on)."""
     h = hashlib.sha256()
-    with open(os.path.join(ROOT, "paper_2102_04681_amd", "csrc", "spk_step.hip"), "rb") as f:
-        h.update(f.read())
+    for name in STEP_SOURCES:
+        with open(os.path.join(ROOT, "paper_2102_04681_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
     return h.hexdigest()[:16]
 
 
@@ -165,8 +183,11 @@ def main():
     torch.cuda.synchronize()
     t_create = time.perf_counter() - t_create
     st = net.stats()
+    persistent = st["step_mode"] == spk.SPK_STEP_PERSISTENT
+    bpe = float(st["bytes_per_synapse"])
     print(f"[bench] {WORKLOAD_NAMES[args.config]}: nnz={st['nnz']} tiles={st['tiles']}x{st['tile_width']} "
-          f"delivery={'direct' if st['delivery'] == 1 else 'binned'} create={t_create:.2f}s",
+          f"delivery={'direct' if st['delivery'] == 1 else 'binned'} "
+          f"steps={'persistent' if persistent else 'graph'} bytes/synapse={bpe:g} create={t_create:.2f}s",
           file=sys.stderr, flush=True)
 
     net.step(W)
@@ -188,22 +209,28 @@ def main():
     # per-kernel durations, HIP events around every launch (second pass)
     net.set_profiling(True)
     net.step(K)
-    push_ms, tile_ms, nsteps = net.kernel_ms()
+    km = net.kernel_ms()
     net.set_profiling(False)
+    nsteps = km["steps"]
     d2 = float(net.delivered(W + K, K).astype(float).sum())
     e2 = float(net.events(W + K, K).astype(float).sum())
     c2 = float(net.spike_counts(W + K, K).astype(float).sum())
     binned = st["delivery"] == 2
-    if binned:  # push kernel reads the fired rows; tile kernel updates the neurons
-        b_push, b_tile = algorithmic_bytes(cfg["n"], cfg["neuron_kind"], e2, c2)
-        kernels = {"k_push": (push_ms / nsteps, b_push / nsteps), "k_tile": (tile_ms / nsteps, b_tile / nsteps)}
-    else:       # tile kernel does both
-        b_ev, b_neu = algorithmic_bytes(cfg["n"], cfg["neuron_kind"], d2, c2)
-        kernels = {"k_tile": (tile_ms / nsteps, (b_ev + b_neu) / nsteps)}
+    if persistent:  # one launch runs all K steps: every byte of the step is its
+        b_ev, b_neu = algorithmic_bytes(cfg["n"], cfg["neuron_kind"], d2, c2, bpe, nsteps)
+        nl = km["run_launches"]
+        kernels = {"k_run": (km["run_ms"] / nl, (b_ev + b_neu) / nl)}
+    elif binned:  # push kernel reads the fired rows; tile kernel updates the neurons
+        b_push, b_tile = algorithmic_bytes(cfg["n"], cfg["neuron_kind"], e2, c2, bpe, nsteps)
+        kernels = {"k_push": (km["push_ms"] / nsteps, b_push / nsteps),
+                   "k_tile": (km["tile_ms"] / nsteps, b_tile / nsteps)}
+    else:         # tile kernel does both
+        b_ev, b_neu = algorithmic_bytes(cfg["n"], cfg["neuron_kind"], d2, c2, bpe, nsteps)
+        kernels = {"k_tile": (km["tile_ms"] / nsteps, (b_ev + b_neu) / nsteps)}
     dom = max(kernels, key=lambda k: kernels[k][0])
     dom_ms, dom_bytes = kernels[dom]
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
-    b_evt, b_neu = algorithmic_bytes(cfg["n"], cfg["neuron_kind"], events, spikes)
+    b_evt, b_neu = algorithmic_bytes(cfg["n"], cfg["neuron_kind"], events, spikes, bpe, K)
     step_gbs = (b_evt + b_neu) / (ms * 1e-3) / 1e9
     traffic = measured_traffic(args.config, args.acc, dom)
     roofline = {
@@ -213,8 +240,10 @@ def main():
         "kernel": dom, "kernel_us": round(dom_ms * 1e3, 2),
         "kernel_alg_bytes": round(dom_bytes),
         "step_alg_GBs": round(step_gbs, 1), "step_frac": round(step_gbs / PEAK_HBM_GBS, 4),
-        "events_only_frac": round(value / (PEAK_HBM_GBS * 1e9 / 8.0), 4),
-        "per_kernel_us": {k: round(v[0] * 1e3, 2) for k, v in kernels.items()},
+        "events_only_frac": round(value / (PEAK_HBM_GBS * 1e9 / bpe), 4),
+        "bytes_per_event": bpe,
+        "per_launch_us": {k: round(v[0] * 1e3, 2) for k, v in kernels.items()},
+        "steps_per_launch": nsteps / km["run_launches"] if persistent else 1,
     }
 
     rate_hz = spikes / (cfg["n"] * K * cfg["dt_ms"] * 1e-3)
@@ -228,6 +257,8 @@ def main():
                                                        if cfg["ext_lambda"] and args.config != 2 else ""),
             "n_neurons": cfg["n"], "synapses": int(st["nnz"]), "dt_ms": cfg["dt_ms"],
             "delivery": "direct" if st["delivery"] == 1 else "binned",
+            "steps": "one persistent launch" if persistent else "HIP graphs of 32 steps",
+            "synapse_bytes": bpe,
             "accumulation": "exact int64 fixed point, rounded once to fp32" if args.acc == "f32"
                             else f"int32 fixed point 2^-{cfg['fixed_shift']}",
             "mean_rate_hz": round(rate_hz, 3), "events_per_step": round(events / K, 1),

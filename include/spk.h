@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define SPK_ABI_VERSION 2u
+#define SPK_ABI_VERSION 3u
 #define SPK_MAX_DELAY_LISTS 64u  /* delay_max - delay_min + 1 must not exceed this */
 
 typedef enum {
@@ -76,6 +76,17 @@ enum { SPK_DELIVERY_AUTO = 0, SPK_DELIVERY_DIRECT = 1, SPK_DELIVERY_BINNED = 2 }
  * source population, Sec. III-A), or an explicit adjacency with at most 4
  * distinct weights.  AUTO picks COMPACT whenever it applies. */
 enum { SPK_FORMAT_AUTO = 0, SPK_FORMAT_FULL = 1, SPK_FORMAT_COMPACT = 2 };
+/* How spk_step runs the steps (same results, different speed).  GRAPH: each
+ * step is a tile kernel (+ push kernel for binned delivery), batches of steps
+ * replayed from captured HIP graphs.  PERSISTENT: all steps of one spk_step
+ * call in a single cooperative launch of one workgroup per compute unit that
+ * keeps the neuron state in LDS and hands each step over through barriers
+ * inside the kernel; it needs one tile per compute unit or fewer (n <= 2^21
+ * on MI355X), direct delivery with a single delay, or binned delivery with
+ * delay_max * tiles / 8 <= 2048.  AUTO takes PERSISTENT where it applies and
+ * the device runs it (checked once at creation), else GRAPH; asking for
+ * PERSISTENT where it does not apply is SPK_EINVAL at creation. */
+enum { SPK_STEP_AUTO = 0, SPK_STEP_GRAPH = 1, SPK_STEP_PERSISTENT = 2 };
 
 /* Network parameters (plain data).
  *
@@ -131,6 +142,7 @@ typedef struct {
     int32_t fixed_shift;       /* 0..30 */
     uint32_t delivery;         /* SPK_DELIVERY_*: how events reach their target tile */
     uint32_t syn_format;       /* SPK_FORMAT_*: synapse storage */
+    uint32_t step_mode;        /* SPK_STEP_*: how steps are launched */
     uint64_t max_steps;        /* >= 1 */
     uint64_t raster_capacity;  /* spike IDs; 0 = no raster */
 } spk_params;
@@ -148,6 +160,7 @@ typedef struct {
     uint32_t tiles;
     uint32_t delivery;         /* SPK_DELIVERY_DIRECT or SPK_DELIVERY_BINNED as chosen */
     uint32_t page_cap;         /* binned delivery: records per page (beyond: global atomics) */
+    uint32_t step_mode;        /* SPK_STEP_GRAPH or SPK_STEP_PERSISTENT as chosen */
 } spk_stats_t;
 
 typedef struct spk_net spk_net;
@@ -190,7 +203,9 @@ spk_status spk_create_from_csr(const spk_params *params, uint32_t n, const uint6
  * Errors: SPK_EOVERFLOW if steps would exceed max_steps. */
 spk_status spk_step(spk_net *net, uint64_t n_steps);
 
-/* Wait for all enqueued work; reports device-side overflow flags. */
+/* Wait for all enqueued work; reports device-side overflow flags, and
+ * SPK_EHIP if a persistent launch stopped early (a barrier wait exceeded its
+ * 10 s bound): the state is then undefined. */
 spk_status spk_sync(spk_net *net);
 
 /* Per-step records for steps [t0, t0+n) (host output buffers of n entries):
@@ -232,15 +247,18 @@ spk_status spk_poisson_table(spk_net *net, uint64_t *thr, uint32_t cap, uint32_t
 
 spk_status spk_stats(spk_net *net, spk_stats_t *out);
 
-/* Kernel timing.  By default spk_step replays batches of steps captured in
- * a HIP graph.  With profiling on, it launches each kernel directly with HIP
- * events around the tile kernel (delivery into LDS + neuron update + spike
- * list) and the push kernel (binned delivery only: the new spikes' events
- * into arrival pages) on the network's stream, and spk_read_kernel_ms
- * returns their summed durations (ms) and the number of steps since the
- * last spk_set_profiling call. */
+/* Kernel timing.  With profiling on, spk_step records HIP events on the
+ * network's stream around every kernel it launches: in GRAPH mode it launches
+ * each step's kernels directly (no graph) -- the tile kernel (delivery into
+ * LDS + neuron update + spike list) and, for binned delivery, the push kernel
+ * (the new spikes' events into arrival pages); in PERSISTENT mode the one
+ * launch of each spk_step call.  spk_read_kernel_ms returns the summed
+ * durations (ms) of push, tile and persistent launches, the number of steps
+ * and the number of persistent launches since the last spk_set_profiling
+ * call; outputs may be NULL. */
 spk_status spk_set_profiling(spk_net *net, int on);
-spk_status spk_read_kernel_ms(spk_net *net, double *push_ms, double *tile_ms, uint64_t *steps);
+spk_status spk_read_kernel_ms(spk_net *net, double *push_ms, double *tile_ms, double *run_ms,
+                              uint64_t *steps, uint64_t *run_launches);
 
 /* Plain device-to-device copy of `bytes` bytes (multiple of 16) through the
  * library's streaming copy kernel on the network's stream, timed with HIP

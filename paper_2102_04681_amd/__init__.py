@@ -7,6 +7,6 @@ script; PyTorch is only used by callers for streams and device memory.
 from .spk import (Net, SpkError, lib, make_params, preset, SPK_ACC_F32, SPK_ACC_FIXED,  # noqa: F401
                   SPK_LIF, SPK_SOURCE, SPK_CONN_BERNOULLI, SPK_CONN_FIXED_OUT, SPK_CONN_FIXED_IN,
                   SPK_CONN_EXPLICIT, SPK_OK, SPK_EINVAL, SPK_ENOMEM, SPK_EHIP, SPK_EOVERFLOW,
-                  SPK_ESTATE, EXPORTED)
+                  SPK_ESTATE, SPK_STEP_AUTO, SPK_STEP_GRAPH, SPK_STEP_PERSISTENT, EXPORTED)
 
 __all__ = ["Net", "SpkError", "lib", "make_params", "preset"]

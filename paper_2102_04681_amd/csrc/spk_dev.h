@@ -1,0 +1,320 @@
+// spk_dev.h -- device helpers shared by the step kernels (spk_step.hip) and
+// the persistent step kernel (spk_run.hip): workgroup barriers and scans,
+// spike-list and page addressing, accumulator units, synapse records.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "spk_internal.h"
+
+namespace spk {
+namespace {
+
+
+// Loads and stores at agent scope (the sc1 cache policy): they do not hit in
+// the non-coherent per-XCD caches, so data written this way by one workgroup
+// is seen by a workgroup on another XCD once the writer's store has completed
+// (vmcnt) and the reader has observed that through an atomic.  Used by the
+// persistent kernel for the spike lists, which every XCD reads.
+__device__ __forceinline__ uint32_t ld_ag(const uint32_t *p)
+{
+    return __hip_atomic_load(const_cast<uint32_t *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_ag(uint32_t *p, uint32_t v)
+{
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+template <bool COH>
+__device__ __forceinline__ uint32_t ld_u32(const uint32_t *p)
+{
+    if constexpr (COH) return ld_ag(p);
+    else return *p;
+}
+
+__device__ __forceinline__ uint32_t lane_id() { return threadIdx.x & (kWave - 1); }
+
+// Workgroup barrier that orders LDS traffic only.  __syncthreads() carries
+// workgroup-scope fences on global memory as well, which can make a wave
+// wait for its outstanding global loads (one full memory round trip per
+// phase); here global loads issued before the barrier stay in flight across
+// it.  Used wherever threads of a block communicate through LDS alone.
+// Neither barrier waits for global stores to complete: code that hands
+// global data to other workgroups waits for them explicitly (s_waitcnt).
+__device__ __forceinline__ void lds_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+__device__ __forceinline__ void lds_wave_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+__device__ __forceinline__ uint64_t step_index(const StepArgs &a, uint32_t i, int64_t t_explicit)
+{
+    return t_explicit >= 0 ? (uint64_t)t_explicit : *a.t_base + i;
+}
+
+// Block-wide exclusive scan of one u32 per thread (blockDim <= 1024).
+__device__ uint32_t block_scan_u32(uint32_t x, uint32_t *ws /*>=16*/, uint32_t *total)
+{
+    const uint32_t lane = lane_id(), w = threadIdx.x / kWave, nw = blockDim.x / kWave;
+    uint32_t inc = x;
+    for (int o = 1; o < kWave; o <<= 1) {
+        const uint32_t y = __shfl_up(inc, o);
+        if (lane >= (uint32_t)o) inc += y;
+    }
+    if (lane == kWave - 1) ws[w] = inc;
+    lds_sync();
+    uint32_t before = 0, tot = 0;
+    for (uint32_t k = 0; k < nw; k++) {
+        const uint32_t v = ws[k];
+        before += k < w ? v : 0u;
+        tot += v;
+    }
+    lds_sync();
+    *total = tot;
+    return before + inc - x;
+}
+
+// Same, without the trailing barrier: ws must not be written again before
+// the caller's next barrier.
+__device__ uint32_t block_scan_u32_open(uint32_t x, uint32_t *ws /*>=16*/, uint32_t *total)
+{
+    const uint32_t lane = lane_id(), w = threadIdx.x / kWave, nw = blockDim.x / kWave;
+    uint32_t inc = x;
+    for (int o = 1; o < kWave; o <<= 1) {
+        const uint32_t y = __shfl_up(inc, o);
+        if (lane >= (uint32_t)o) inc += y;
+    }
+    if (lane == kWave - 1) ws[w] = inc;
+    lds_sync();
+    uint32_t before = 0, tot = 0;
+    for (uint32_t k = 0; k < nw; k++) {
+        const uint32_t v = ws[k];
+        before += k < w ? v : 0u;
+        tot += v;
+    }
+    *total = tot;
+    return before + inc - x;
+}
+
+__device__ __forceinline__ uint64_t block_sum_u64(uint64_t x, unsigned long long *ws /*>=16*/)
+{
+    const uint32_t lane = lane_id(), w = threadIdx.x / kWave, nw = blockDim.x / kWave;
+    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
+    if (lane == 0) ws[w] = x;
+    lds_sync();
+    uint64_t tot = 0;
+    for (uint32_t k = 0; k < nw; k++) tot += ws[k];
+    lds_sync();
+    return tot;
+}
+
+// Block-wide exclusive max-scan of one u32 per thread.
+__device__ uint32_t block_scan_max_u32(uint32_t x, uint32_t *ws)
+{
+    const uint32_t lane = lane_id(), w = threadIdx.x / kWave;
+    uint32_t inc = x;
+    for (int o = 1; o < kWave; o <<= 1) {
+        const uint32_t y = __shfl_up(inc, o);
+        if (lane >= (uint32_t)o) inc = y > inc ? y : inc;
+    }
+    const uint32_t ex_w = __shfl_up(inc, 1);
+    if (lane == kWave - 1) ws[w] = inc;
+    lds_sync();
+    uint32_t before = 0;
+    for (uint32_t k = 0; k < w; k++) before = ws[k] > before ? ws[k] : before;
+    lds_sync();
+    return lane ? (ex_w > before ? ex_w : before) : before;
+}
+
+// The spike list of one slot is spread over per-tile segments: pre[] gets
+// the exclusive prefix of the T segment counts (T <= 2048, two per thread of
+// a 1024-thread block); returns the total.  COH: agent-scope loads.
+template <bool COH = false>
+__device__ uint32_t load_spike_set(const StepArgs &a, uint32_t slot, uint32_t *pre, uint32_t *ws)
+{
+    const uint32_t T = a.tl.T, W = a.tl.W;
+    const uint32_t b = threadIdx.x * 2;
+    const uint32_t *cnt = a.spk_cnt + (uint64_t)slot * T;
+    uint32_t c0 = ld_u32<COH>(cnt + (b < T ? b : 0)), c1 = ld_u32<COH>(cnt + (b + 1 < T ? b + 1 : 0));
+    c0 = b < T ? (c0 < W ? c0 : W) : 0u;
+    c1 = b + 1 < T ? (c1 < W ? c1 : W) : 0u;
+    uint32_t tot;
+    const uint32_t ex = block_scan_u32(c0 + c1, ws, &tot);
+    if (b < T) pre[b] = ex;
+    if (b + 1 < T) pre[b + 1] = ex + c0;
+    if (threadIdx.x == 0) pre[T] = tot;
+    lds_sync();
+    return tot;
+}
+
+// k-th spike of the slot (k < total): largest tile with pre[tile] <= k.
+template <bool COH = false>
+__device__ __forceinline__ uint32_t spike_at(const StepArgs &a, const uint32_t *pre, uint32_t slot,
+                                             uint32_t k)
+{
+    uint32_t lo = 0, hi = a.tl.T - 1;
+    while (lo < hi) {
+        const uint32_t mid = (lo + hi + 1) >> 1;
+        if (pre[mid] <= k) lo = mid; else hi = mid - 1;
+    }
+    return ld_u32<COH>(a.spk_ids + ((uint64_t)slot * a.tl.T + lo) * a.tl.W + (k - pre[lo]));
+}
+
+// Page (x, g1, slot, c) of the binned delivery; records at page * page_cap.
+__device__ __forceinline__ uint32_t page_of(const StepArgs &a, uint32_t x, uint32_t g1, uint32_t slot,
+                                            uint32_t c)
+{
+    return ((x * a.pg1 + g1) * a.pslots + slot) * a.tl.T8 + c;
+}
+
+__device__ __forceinline__ uint32_t arrival_slot(const StepArgs &a, uint64_t t, uint32_t j, bool dbg)
+{
+    return dbg ? 0u : (uint32_t)((t + a.dmin + j) % a.pslots);
+}
+
+// Accumulator conversions.  fp32 mode: exact int64 multiple of 2^-S64.
+__device__ __forceinline__ long long to_fixed64(int32_t wbits, int32_t s64)
+{
+    return __double2ll_rn(ldexp((double)__int_as_float(wbits), s64));
+}
+// The unit is chosen so that |acc| < 2^53: the conversion to double is
+// exact, the scaling by 2^-S64 is exact, and the one rounding is to fp32.
+__device__ __forceinline__ float fixed64_to_float(unsigned long long acc, int32_t s64)
+{
+    return (float)ldexp((double)(long long)acc, -s64);
+}
+
+// Accumulator units of one event: the stored weight bits converted
+// (full format), or the class's precomputed value (compact format).
+template <bool FIXED>
+__device__ __forceinline__ long long units_of(int32_t wbits, int32_t s64)
+{
+    return FIXED ? (long long)wbits : to_fixed64(wbits, s64);
+}
+// Selected without a dynamic index into the kernel arguments (which would
+// go through scratch memory).
+__device__ __forceinline__ long long class_units(const StepArgs &a, uint32_t cls)
+{
+    const long long w01 = cls & 1u ? a.wval[1] : a.wval[0];
+    const long long w23 = cls & 1u ? a.wval[3] : a.wval[2];
+    return cls & 2u ? w23 : w01;
+}
+
+template <bool FIXED> struct Acc;
+template <> struct Acc<true> {
+    using T = int32_t;
+    static __device__ __forceinline__ void add(T *p, long long units) { atomicAdd(p, (int32_t)units); }
+};
+template <> struct Acc<false> {
+    using T = unsigned long long;
+    static __device__ __forceinline__ void add(T *p, long long units)
+    {
+        atomicAdd(p, (unsigned long long)units);
+    }
+};
+
+// Synapse record of each format, and its key (class, delay index, target).
+template <bool CMP> struct SynRec;
+template <> struct SynRec<false> {
+    using T = int2;
+    static __device__ __forceinline__ T load(const StepArgs &a, uint64_t e) { return a.syn[e]; }
+};
+template <> struct SynRec<true> {
+    using T = uint32_t;
+    static __device__ __forceinline__ T load(const StepArgs &a, uint64_t e) { return a.syn32[e]; }
+};
+// Global fallback for a full page (rare): same units as the LDS accumulator,
+// one accumulator per (arrival slot, neuron).
+// COH: the flag is read with an agent-scope load (persistent kernel, where
+// the tile resets it during the launch).
+template <bool FIXED, bool COH = false>
+__device__ __forceinline__ void overflow_add(const StepArgs &a, uint32_t slot, uint32_t tile,
+                                             uint32_t local, long long units)
+{
+    const uint64_t st = (uint64_t)slot * a.tl.T + tile;
+    const uint64_t i = st * a.tl.W + local;
+    if (FIXED) atomicAdd((int32_t *)a.acc_ovf + i, (int32_t)units);
+    else atomicAdd((unsigned long long *)a.acc_ovf + i, (unsigned long long)units);
+    if (ld_u32<COH>(&a.ovf_flag[st]) == 0) atomicOr(&a.ovf_flag[st], 1u);
+}
+
+// Accumulate the tile's events directly from the rows of the given spikes
+// (direct mode): each wave takes 64 spikes at a time, lane l resolving spike
+// l's run for this tile; the 64 runs are then streamed lane-parallel.  With
+// jf >= 0 only synapses of delay index jf are delivered.  Returns the number
+// of events this thread delivered.
+//   acc: the tile's LDS accumulators; pre: the spike-count prefix of the slot
+//   (load_spike_set); wpre, wbeg: per-wave scratch.  COH: spike IDs are read
+//   with agent-scope loads (persistent kernel).
+template <bool FIXED, bool CMP, bool COH>
+__device__ uint32_t gather_direct(const StepArgs &a, typename Acc<FIXED>::T *acc, const uint32_t *pre,
+                                  uint32_t (*wpre)[kWave + 1], uint64_t (*wbeg)[kWave], uint32_t tile,
+                                  uint32_t tile_lo, uint32_t P, uint32_t slot, int32_t jf)
+{
+    using Rec = typename SynRec<CMP>::T;
+    const uint32_t lane = lane_id(), w = threadIdx.x / kWave, nw = blockDim.x / kWave;
+    const uint32_t T1 = a.tl.T + 1;
+    uint32_t mine = 0;
+    for (uint32_t p0 = w * kWave; p0 < P; p0 += nw * kWave) {
+        uint32_t len = 0;
+        uint64_t beg = 0;
+        if (p0 + lane < P) {
+            const uint32_t s = a.dbg_spikes ? a.dbg_spikes[p0 + lane] : spike_at<COH>(a, pre, slot, p0 + lane);
+            const uint16_t *to = a.toff + (uint64_t)s * T1 + tile;
+            const uint32_t b = to[0], e = to[1];
+            beg = a.row_ptr[s] + b;
+            len = e - b;
+        }
+        uint32_t inc = len;
+        for (int o = 1; o < kWave; o <<= 1) {
+            const uint32_t y = __shfl_up(inc, o);
+            if (lane >= (uint32_t)o) inc += y;
+        }
+        const uint32_t tot = __shfl(inc, kWave - 1);
+        wpre[w][lane] = inc - len;
+        wbeg[w][lane] = beg;
+        if (lane == 0) wpre[w][kWave] = tot;
+        lds_wave_sync();
+        constexpr int U = 8;  // loads in flight per lane
+        for (uint32_t f0 = 0; f0 < tot; f0 += kWave * U) {
+            uint64_t idx[U];
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                const uint32_t f = f0 + u * kWave + lane;
+                const uint32_t fc = f < tot ? f : 0u;
+                uint32_t lo = 0, hi = kWave - 1;
+                while (lo < hi) {
+                    const uint32_t mid = (lo + hi + 1) >> 1;
+                    if (wpre[w][mid] <= fc) lo = mid; else hi = mid - 1;
+                }
+                idx[u] = f < tot ? wbeg[w][lo] + (fc - wpre[w][lo]) : 0ull;
+            }
+            Rec r[U];
+#pragma unroll
+            for (int u = 0; u < U; u++) r[u] = SynRec<CMP>::load(a, idx[u]);  // unconditional, see push
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                if (f0 + u * kWave + lane >= tot) continue;
+                const uint32_t key = rec_key(r[u]);
+                if (jf >= 0 && (int32_t)rec_delay(key) != jf) continue;
+                long long units;
+                if constexpr (CMP) units = class_units(a, rec_class(key));
+                else units = units_of<FIXED>(r[u].y, a.m.shift64);
+                Acc<FIXED>::add(&acc[rec_target(key) - tile_lo], units);
+                mine++;
+            }
+        }
+        __builtin_amdgcn_wave_barrier();
+    }
+    return mine;
+}
+
+}  // namespace
+}  // namespace spk

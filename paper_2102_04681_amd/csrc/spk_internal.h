@@ -193,6 +193,30 @@ struct StepArgs {
     void *dbg_out;
 };
 
+// Persistent step kernel (spk_run.hip): one cooperative launch of R
+// workgroups per XCD runs many steps.  Control words, zeroed before every
+// launch; each counter sits on its own 128-byte line.
+constexpr uint32_t kCtlStride = 32;
+constexpr uint32_t kRunMaxR = 32;          // workgroups per XCD (one per compute unit)
+constexpr uint32_t kRunMaxFill = 2048;     // pages per push block: arrival slots x tiles of a group
+constexpr uint32_t kRunAbortTimeout = 1u;  // a barrier wait gave up
+constexpr uint32_t kRunAbortPlacement = 2u;  // workgroups not spread R per XCD: nothing was run
+struct RunCtl {
+    uint32_t ticket[kGroups * kCtlStride];  // workgroups placed on each XCD
+    uint32_t gx[kGroups * kCtlStride];      // grid barrier: arrivals per XCD
+    uint32_t lx[kGroups * kCtlStride];      // XCD barrier: arrivals per XCD
+    uint32_t start, pad0[kCtlStride - 1];   // placement barrier
+    uint32_t gcnt, pad1[kCtlStride - 1];    // grid barrier: XCDs complete
+    uint32_t gen, pad2[kCtlStride - 1];     // grid barrier: released epoch
+    uint32_t abort_flag, pad3[kCtlStride - 1];
+};
+struct RunArgs {
+    StepArgs s;
+    RunCtl *ctl;
+    uint64_t t0, n_steps;   // steps [t0, t0 + n_steps)
+    uint32_t R;             // workgroups per XCD
+};
+
 // spk_gen.hip -- connectivity expansion
 hipError_t gen_count_rows(const ConnArgs &c, uint32_t *cnt, hipStream_t s);
 hipError_t gen_fill_rows(const ConnArgs &c, const uint64_t *row_ptr, void *syn, RowIndex ix,
@@ -233,5 +257,9 @@ hipError_t launch_record(const StepArgs &a, uint32_t i, int64_t t_explicit, hipS
 hipError_t launch_advance(uint64_t *t_base, uint32_t steps, hipStream_t s);
 hipError_t stream_copy(const void *src, void *dst, uint64_t bytes, hipStream_t s);
 uint32_t push_blocks_per_group();
+
+// spk_run.hip -- the persistent step kernel (all steps of a call in one launch)
+bool run_supported(const StepArgs &a, uint32_t R);
+hipError_t launch_run(const RunArgs &ra, hipStream_t s);
 
 }  // namespace spk

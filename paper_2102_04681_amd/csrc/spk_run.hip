@@ -1,0 +1,697 @@
+// spk_run.hip -- the persistent step kernel: many simulation steps in one
+// cooperative launch of one workgroup per compute unit.
+//
+// The step is the same as the graph path's (spk_step.hip): the events that
+// arrive at t are summed in LDS, the neurons are updated, the spikes of t are
+// compacted, and (binned delivery) the rows of the neurons that fired are read
+// once and their events filed by (arrival step, target tile) into pages.  The
+// difference is what persists between steps and how the hand-offs happen:
+//   - each workgroup keeps its tile's membrane potentials, refractory
+//     counters and the next step's Poisson draws in LDS for the whole launch,
+//     and (as a push block) the fill counters of the pages it owns;
+//   - the two hand-offs of a step are barriers inside the kernel instead of
+//     kernel boundaries.  After the tiles publish the spike list of t, a grid
+//     barrier; after the push blocks of an XCD have filed their events, a
+//     barrier of that XCD's workgroups only, because every page is written
+//     and read on one XCD (its L2 is the point of coherence, so only the
+//     compute units' L1 caches are invalidated there).
+// Workgroups find their XCD from the hardware register and take a ticket
+// within it, so the group of tiles a workgroup serves is always on the XCD it
+// runs on.  Spike lists cross XCDs through agent-scope loads and stores.
+//
+// Every wait is bounded (10 s of the real-time clock); a workgroup that gives
+// up sets an abort flag that every other waiter also polls, so the grid
+// always drains.  The host reads the flag after the launch.
+#include <hip/hip_runtime.h>
+
+#include "spk_dev.h"
+
+namespace spk {
+
+namespace {
+
+constexpr int kRunThreads = 1024;
+constexpr int kRunRounds = kMaxTileW / kRunThreads;      // neurons per thread
+constexpr uint32_t kRunChunk = 256;                      // spikes resolved per push chunk
+constexpr uint32_t kRunMaxT = kGroups * kRunMaxR;        // tiles
+constexpr uint64_t kSpinTicks = 10ull * 100000000ull;    // 10 s of the 100 MHz clock
+constexpr uint32_t kRunStoppedFlag = 4u;                 // sticky in the network's device flags
+
+__device__ __forceinline__ uint32_t xcc_id()
+{
+    return __builtin_amdgcn_s_getreg((20) | (0 << 6) | ((4 - 1) << 11)) & 0xfu;  // HW_REG_XCC_ID[3:0]
+}
+
+// Wait until *p >= target; false if the wait gave up or another workgroup did.
+__device__ bool spin_ge(const uint32_t *p, uint32_t target, uint32_t *abort_flag)
+{
+    const uint64_t t0 = wall_clock64();
+    for (uint32_t k = 0;; k++) {
+        if (ld_ag(p) >= target) return true;
+        if ((k & 31u) == 31u) {
+            if (ld_ag(abort_flag)) return false;
+            if (wall_clock64() - t0 > kSpinTicks) {
+                atomicOr(abort_flag, kRunAbortTimeout);
+                return false;
+            }
+        }
+        __builtin_amdgcn_s_sleep(1);
+    }
+}
+
+template <bool FIXED, bool CMP>
+struct RunLDS {
+    using AccT = typename Acc<FIXED>::T;
+    using Rec = typename SynRec<CMP>::T;
+    static constexpr int R = CMP ? 16 : 8;                    // events per thread per load phase
+    static constexpr uint32_t kStageN = R * kRunThreads / 2;  // events bucket-sorted at once
+    // persistent for the whole launch
+    float V[kMaxTileW];
+    uint8_t ref[kMaxTileW];     // LIF: refractory steps left; source: fires at the current step
+    uint8_t kp[kMaxTileW];      // Poisson count of the current step
+    uint64_t pois[256];
+    uint16_t guide[256];
+    uint32_t fill[kRunMaxFill]; // push block: records in each of its pages, (arrival slot, tile)
+    union {
+        struct {
+            AccT acc[kMaxTileW];
+            uint16_t spk[kMaxTileW];
+            uint32_t pre[kRunMaxT + 1];                      // binned: chunk prefix; direct: spike prefix
+            uint32_t cbase[kRunThreads / kWave * 16];
+            uint32_t clen[kRunThreads / kWave * 16];
+            uint32_t wpre[kRunThreads / kWave][kWave + 1];
+            uint64_t wbeg[kRunThreads / kWave][kWave];
+        } t;
+        struct {
+            Rec stage[kStageN];
+            uint32_t pre[kRunMaxT + 1];
+            uint32_t cpre[kRunChunk + 1];
+            uint32_t plen[kRunChunk];
+            uint64_t pbase[kRunChunk];
+            uint64_t cbase[R * (kRunThreads / kWave)];
+            uint32_t clen[R * (kRunThreads / kWave)];
+            uint32_t bcnt[kMaxBuckets];   // events per bucket in this half, then rank cursor
+            uint32_t bst[kMaxBuckets];    // bucket starts in the stage
+            uint32_t wb[kMaxBuckets];     // page position of stage entry q is wb[b] + q
+        } p;
+    } u;
+    uint32_t ws[16], ws2[16];
+    unsigned long long ws64[16];
+    uint32_t nspk, x, r, stop;
+};
+
+// Per-step draws of the tile's neurons for step t: the Poisson count and, for
+// source neurons, whether they fire.  They do not depend on the network's
+// activity, so they are computed while the workgroup waits at a barrier.
+template <bool FIXED, bool CMP>
+__device__ void run_draws(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t tile_lo, uint32_t tile_n,
+                          uint64_t t)
+{
+    const ModelArgs &m = a.m;
+#pragma unroll
+    for (int u = 0; u < kRunRounds; u++) {
+        const uint32_t q = u * kRunThreads + threadIdx.x;
+        if (q >= tile_n) continue;
+        const uint32_t gi = tile_lo + q;
+        if (m.pois_len) {  // K = min { k : hi32 < T_k }, searched from the guide entry
+            const uint32_t h = hash_hi32(step_hash(m.keys.pois, gi, t));
+            uint32_t k = L.guide[h >> 24];
+            while ((uint64_t)h >= L.pois[k]) k++;
+            L.kp[q] = (uint8_t)k;
+        }
+        if (m.kind == SPK_SOURCE)
+            L.ref[q] = (uint64_t)hash_hi32(step_hash(m.keys.bern, gi, t)) < m.src_thr ? 1 : 0;
+    }
+}
+
+// Grid barrier: every workgroup's stores have completed before it arrives.
+// The last arrival of an XCD counts the XCD; the last XCD releases epoch e.
+// Between arriving and waiting, the workgroup computes the next step's draws.
+template <bool FIXED, bool CMP>
+__device__ bool grid_sync(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x, uint32_t e, bool draws,
+                          uint32_t tile_lo, uint32_t tile_n, uint64_t t_draw)
+{
+    RunCtl *c = ra.ctl;
+    __builtin_amdgcn_s_waitcnt(0);  // this thread's stores have completed
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const uint32_t o = atomicAdd(&c->gx[x * kCtlStride], 1u);
+        if (o == ra.R * e - 1) {
+            const uint32_t g = atomicAdd(&c->gcnt, 1u);
+            if (g == kGroups * e - 1) st_ag(&c->gen, e);
+        }
+    }
+    if (draws) run_draws(ra.s, L, tile_lo, tile_n, t_draw);
+    if (threadIdx.x == 0) {
+        L.stop = spin_ge(&c->gen, e, &c->abort_flag) ? 0u : 1u;
+        if (L.stop) atomicOr(ra.s.flags, kRunStoppedFlag);
+    }
+    __syncthreads();
+    return L.stop == 0;
+}
+
+// Barrier of the workgroups of one XCD; afterwards the compute unit's L1 is
+// invalidated so that plain loads see what the others stored in the L2.
+template <bool FIXED, bool CMP>
+__device__ bool xcd_sync(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x, uint32_t e)
+{
+    RunCtl *c = ra.ctl;
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        atomicAdd(&c->lx[x * kCtlStride], 1u);
+        L.stop = spin_ge(&c->lx[x * kCtlStride], ra.R * e, &c->abort_flag) ? 0u : 1u;
+        if (L.stop) atomicOr(ra.s.flags, kRunStoppedFlag);
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        __builtin_amdgcn_s_waitcnt(0);
+    }
+    __syncthreads();
+    return L.stop == 0;
+}
+
+// Tile phase, binned delivery: sum the records of the arrival step's pages
+// (one per push block of the group) into LDS.  Returns the events delivered
+// (including any that overflowed into the global accumulators).
+template <bool FIXED, bool CMP>
+__device__ uint64_t run_drain(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t x, uint32_t c, uint32_t tile,
+                              uint32_t tile_n, uint64_t t)
+{
+    const uint32_t tid = threadIdx.x;
+    const Tiling tl = a.tl;
+    const uint32_t pslot = (uint32_t)(t % a.pslots);
+    constexpr uint32_t kPer = CMP ? 2u : 1u;
+    constexpr uint32_t kChunk = kPer * kWave;
+    const uint32_t cap = a.page_cap, G1 = a.pg1;
+    uint32_t pf = a.pfill[page_of(a, x, tid < G1 ? tid : 0u, pslot, c)];
+    const uint32_t ovf = ld_ag(&a.ovf_flag[(uint64_t)pslot * tl.T + tile]);
+    pf = tid < G1 ? pf : 0u;
+    const uint32_t ne = pf < cap ? pf : cap;
+    uint32_t C;
+    const uint32_t cex = block_scan_u32((ne + kChunk - 1) / kChunk, L.ws, &C);
+    const uint64_t delivered = block_sum_u64(pf, L.ws64);
+    // the wave index is uniform: held in a scalar register, the chunk-table
+    // addresses below cost no vector registers
+    const uint32_t w = __builtin_amdgcn_readfirstlane(tid / kWave), lane = lane_id();
+    constexpr uint32_t nw = kRunThreads / kWave;
+    constexpr int kDrain = 16;
+    constexpr uint32_t kWin = kDrain * nw;
+    const uint32_t nchp = (ne + kChunk - 1) / kChunk;
+    for (uint32_t i0 = 0; i0 < C; i0 += kWin) {
+        for (uint32_t q = tid; q < kWin; q += kRunThreads) L.u.t.clen[q] = 0;
+        lds_sync();
+        if (tid < G1) {
+            const uint32_t cb = cex > i0 ? cex : i0, ce = cex + nchp < i0 + kWin ? cex + nchp : i0 + kWin;
+            const uint32_t pbase = page_of(a, x, tid, pslot, c) * cap;
+            for (uint32_t q = cb; q < ce; q++) {
+                const uint32_t o = (q - cex) * kChunk;
+                L.u.t.cbase[q - i0] = (pbase + o) / kPer;
+                L.u.t.clen[q - i0] = ne - o < kChunk ? ne - o : kChunk;
+            }
+        }
+        lds_sync();
+        if constexpr (CMP) {
+            const uint32_t *pw = (const uint32_t *)a.pages16;
+            uint32_t rr[kDrain];
+            uint32_t okm = 0;
+#pragma unroll
+            for (int u = 0; u < kDrain; u++) {
+                const uint32_t cw = u * nw + w;
+                const uint32_t len = L.u.t.clen[cw], cb = L.u.t.cbase[cw];
+                const bool ok = 2 * lane < len;
+                const uint32_t idx = ok ? cb + lane : 0u;
+                okm |= ((uint32_t)ok | (uint32_t)(2 * lane + 1 < len) << 1) << (2 * u);
+                rr[u] = pw[idx];  // unconditional load from a clamped index
+            }
+#pragma unroll
+            for (int u = 0; u < kDrain; u++) {
+#pragma unroll
+                for (int hf = 0; hf < 2; hf++) {
+                    if (!((okm >> (2 * u + hf)) & 1u)) continue;
+                    const uint32_t rec = hf ? rr[u] >> 16 : rr[u] & 0xffffu;
+                    Acc<FIXED>::add(&L.u.t.acc[rec & kPageLocalMask], class_units(a, rec >> kPageClassShift));
+                }
+            }
+        } else {
+            int2 rr[kDrain];
+            uint32_t okm = 0;
+#pragma unroll
+            for (int u = 0; u < kDrain; u++) {
+                const uint32_t cw = u * nw + w;
+                const uint32_t len = L.u.t.clen[cw], cb = L.u.t.cbase[cw];
+                const bool ok = lane < len;
+                const uint32_t idx = ok ? cb + lane : 0u;
+                okm |= (uint32_t)ok << u;
+                rr[u] = a.pages[idx];
+            }
+#pragma unroll
+            for (int u = 0; u < kDrain; u++)
+                if ((okm >> u) & 1u)
+                    Acc<FIXED>::add(&L.u.t.acc[(uint32_t)rr[u].x], units_of<FIXED>(rr[u].y, a.m.shift64));
+        }
+        lds_sync();
+    }
+    if (ovf) {  // events that did not fit their page, accumulated by global atomics
+        const uint64_t st = (uint64_t)pslot * tl.T + tile;
+        for (uint32_t q = tid; q < tile_n; q += kRunThreads) {
+            const uint64_t gi = st * tl.W + q;
+            if (FIXED) {
+                int32_t *o = (int32_t *)a.acc_ovf + gi;
+                L.u.t.acc[q] += (int32_t)ld_ag((const uint32_t *)o);
+                st_ag((uint32_t *)o, 0u);
+            } else {
+                unsigned long long *o = (unsigned long long *)a.acc_ovf + gi;
+                L.u.t.acc[q] += __hip_atomic_load(o, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(o, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+        if (tid == 0) st_ag(&a.ovf_flag[st], 0u);
+    }
+    lds_sync();
+    return delivered;
+}
+
+// Tile phase: the update of the tile's neurons from the LDS accumulators, the
+// state and the draws in LDS; spikes compacted by wavefront ballots into the
+// LDS list, then published to the tile's segment of the spike list of t.
+template <bool FIXED, bool CMP, bool DIRECT>
+__device__ void run_update(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x, uint32_t tile,
+                           uint32_t tile_lo, uint32_t tile_n, uint64_t t, uint64_t delivered)
+{
+    const StepArgs &a = ra.s;
+    const ModelArgs &m = a.m;
+    const uint32_t tid = threadIdx.x, lane = lane_id();
+    uint64_t ev = 0;
+#pragma unroll
+    for (int u = 0; u < kRunRounds; u++) {
+        const uint32_t q = u * kRunThreads + tid;
+        bool spk = false;
+        if (q < tile_n) {
+            const uint32_t K = m.pois_len ? L.kp[q] : 0u;
+            float I;
+            if (FIXED) {
+                const int32_t qt = (int32_t)L.u.t.acc[q] + (int32_t)K * m.ext_wq + m.bias_q;
+                I = ldexpf((float)qt, -m.shift);
+            } else {
+                const float isyn = fixed64_to_float(L.u.t.acc[q], m.shift64);
+                const float ext = __fmul_rn((float)K, m.ext_w);
+                I = __fadd_rn(__fadd_rn(isyn, ext), m.i_bias);
+            }
+            float V = L.V[q];
+            if (m.kind == SPK_SOURCE) {
+                const float av = __fsub_rn(m.v_rest, V);
+                const float bv = __fmul_rn(m.k, av);
+                const float cv = __fadd_rn(V, bv);
+                V = __fadd_rn(cv, I);
+                spk = L.ref[q] != 0;
+            } else {
+                uint32_t r = L.ref[q];
+                if (r > 0) {
+                    r -= 1;
+                    V = m.v_reset;
+                } else {
+                    const float av = __fsub_rn(m.v_rest, V);
+                    const float bv = __fmul_rn(m.k, av);
+                    const float cv = __fadd_rn(V, bv);
+                    V = __fadd_rn(cv, I);
+                    if (V >= m.v_th) {
+                        spk = true;
+                        V = m.v_reset;
+                        r = m.ref_steps;
+                    }
+                }
+                L.ref[q] = (uint8_t)r;
+            }
+            L.V[q] = V;
+            if (spk && DIRECT) ev += a.outdeg[tile_lo + q];
+        }
+        const uint64_t mask = __ballot(spk);
+        if (mask) {
+            const int leader = __ffsll((unsigned long long)mask) - 1;
+            uint32_t wb = 0;
+            if ((int)lane == leader) wb = atomicAdd(&L.nspk, (uint32_t)__popcll(mask));
+            wb = __shfl(wb, leader);
+            if (spk) {
+                const uint32_t rank = __builtin_amdgcn_mbcnt_hi(
+                    (uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+                L.u.t.spk[wb + rank] = (uint16_t)q;
+            }
+        }
+    }
+    if (DIRECT) ev = block_sum_u64(ev, L.ws64);
+    else lds_sync();
+    const uint32_t ns = L.nspk;
+    const uint64_t seg = (uint64_t)(t % a.spk_slots) * a.tl.T + tile;
+    uint32_t *dst = a.spk_ids + seg * a.tl.W;
+    for (uint32_t q = tid; q < ns; q += kRunThreads) st_ag(dst + q, tile_lo + L.u.t.spk[q]);
+    if (tid == 0) {
+        st_ag(&a.spk_cnt[seg], ns);
+        if (ns) atomicAdd(&a.counts8[t * kGroups + x], ns);
+        if (ev) atomicAdd((unsigned long long *)&a.events8[t * kGroups + x], (unsigned long long)ev);
+        if (delivered)
+            atomicAdd((unsigned long long *)&a.delivered8[t * kGroups + x], (unsigned long long)delivered);
+    }
+}
+
+// Push phase (binned delivery): push block (x, r) takes the r-th equal share
+// of the spikes of t, reads the runs of their rows that target group x and
+// appends the events to its own pages: bucket b = j * T8 + c (delay index j,
+// tile c of the group), page (arrival slot (t + dmin + j) mod pslots, c).
+// Also appends its share of the spike IDs to the raster (group 0).  Returns
+// the step's spike count (every push block sees the whole list).
+template <bool FIXED, bool CMP>
+__device__ uint32_t run_push(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x, uint32_t r, uint64_t t,
+                             uint64_t rbase)
+{
+    using Rec = typename SynRec<CMP>::T;
+    using LT = RunLDS<FIXED, CMP>;
+    constexpr int R = LT::R;
+    const StepArgs &a = ra.s;
+    const uint32_t tid = threadIdx.x, lane = lane_id(), w = __builtin_amdgcn_readfirstlane(tid / kWave);
+    constexpr uint32_t nw = kRunThreads / kWave;
+    const Tiling tl = a.tl;
+    const uint32_t NB = a.lists * tl.T8, G1 = ra.R;
+    const uint32_t sslot = (uint32_t)(t % a.spk_slots);
+    const uint32_t s0 = (uint32_t)(t % a.pslots);
+    // the pages of arrival slot t were drained at t: they restart empty
+    for (uint32_t c = tid; c < tl.T8; c += kRunThreads) L.fill[s0 * tl.T8 + c] = 0;
+    for (uint32_t b = tid; b < NB; b += kRunThreads) L.u.p.bcnt[b] = 0;
+    const uint32_t M = load_spike_set<true>(a, sslot, L.u.p.pre, L.ws);
+    const uint32_t k0 = (uint32_t)((uint64_t)M * r / G1), k1 = (uint32_t)((uint64_t)M * (r + 1) / G1);
+    const bool rec_raster = a.raster_cap && x == 0 && rbase + M <= a.raster_cap;
+    const uint32_t xlo = x * tl.Gw;
+    const uint64_t cap = a.page_cap;
+    const uint32_t slot_of_j0 = (uint32_t)((t + a.dmin) % a.pslots);
+    uint64_t emitted = 0;
+    for (uint32_t c0 = k0; c0 < k1; c0 += kRunChunk) {
+        const uint32_t K = k1 - c0 < kRunChunk ? k1 - c0 : kRunChunk;
+        uint32_t len = 0;
+        uint64_t base = 0;
+        if (tid < K) {
+            const uint32_t k = c0 + tid;
+            const uint32_t s = spike_at<true>(a, L.u.p.pre, sslot, k);
+            if (rec_raster) a.raster[rbase + k] = s;
+            const RowDesc *d = a.desc + s;
+            const uint32_t lo = x ? d->gend[x - 1] : 0u, hi = d->gend[x];
+            len = hi - lo;
+            base = d->start + lo;
+            emitted += d->gend[kGroups - 1];
+        }
+        uint32_t C;
+        const uint32_t nch = (len + kWave - 1) / kWave;
+        const uint32_t coff = block_scan_u32(nch, L.ws, &C);
+        if (tid < K) {
+            L.u.p.cpre[tid] = coff;
+            L.u.p.plen[tid] = len;
+            L.u.p.pbase[tid] = base;
+        }
+        lds_sync();
+        constexpr uint32_t kWin = R * nw;
+        for (uint32_t i0 = 0; i0 < C; i0 += kWin) {
+            for (uint32_t q = tid; q < kWin; q += kRunThreads) L.u.p.clen[q] = 0;
+            lds_sync();
+            if (tid < K) {
+                const uint32_t cb = coff > i0 ? coff : i0, ce = coff + nch < i0 + kWin ? coff + nch : i0 + kWin;
+                for (uint32_t q = cb; q < ce; q++) {
+                    const uint32_t o = (q - coff) * kWave;
+                    L.u.p.cbase[q - i0] = base + o;
+                    L.u.p.clen[q - i0] = len - o < kWave ? len - o : kWave;
+                }
+            }
+            lds_sync();
+            Rec rec[R];
+            uint32_t okm = 0;
+#pragma unroll
+            for (int u = 0; u < R; u++) {
+                const uint32_t cl = u * nw + w;
+                const uint32_t len = L.u.p.clen[cl];
+                const uint64_t cb = L.u.p.cbase[cl];
+                const bool ok = lane < len;
+                const uint64_t idx = ok ? cb + lane : 0ull;
+                okm |= (uint32_t)ok << u;
+                rec[u] = SynRec<CMP>::load(a, idx);  // unconditional load from a clamped index
+            }
+#pragma unroll
+            for (int h = 0; h < 2; h++) {
+                if (i0 + (uint32_t)h * (R / 2) * nw >= C) break;
+                constexpr int RH = R / 2;
+                uint32_t tr[RH];
+#pragma unroll
+                for (int rr = 0; rr < RH; rr++) {
+                    const int q = h * RH + rr;
+                    tr[rr] = 0xffffffffu;
+                    if (!((okm >> q) & 1u)) continue;
+                    const uint32_t key = rec_key(rec[q]);
+                    const uint32_t j = rec_delay(key);
+                    const uint32_t local = rec_target(key) - xlo;
+                    const uint32_t b = j * tl.T8 + (local >> tl.logW);
+                    const uint32_t rank = atomicAdd(&L.u.p.bcnt[b], 1u);
+                    tr[rr] = (b << 16) | rank;
+                    const uint32_t sv = (b << 16) | (local & (tl.W - 1));
+                    if constexpr (CMP) rec[q] = sv | (rec_class(key) << kPageClassShift);
+                    else rec[q].x = (int)sv;
+                }
+                lds_sync();
+                uint32_t staged;
+                {
+                    const uint32_t P = (NB + kRunThreads - 1) / kRunThreads;
+                    const uint32_t b0 = tid * P;
+                    uint32_t sum = 0;
+                    for (uint32_t k = 0; k < P; k++)
+                        if (b0 + k < NB) sum += L.u.p.bcnt[b0 + k];
+                    uint32_t ex = block_scan_u32_open(sum, h ? L.ws : L.ws2, &staged);
+                    for (uint32_t k = 0; k < P; k++) {
+                        if (b0 + k < NB) {
+                            const uint32_t bb = b0 + k, cnt = L.u.p.bcnt[bb];
+                            const uint32_t j = bb / tl.T8, cc = bb - j * tl.T8;
+                            uint32_t sl = slot_of_j0 + j;
+                            sl = sl >= a.pslots ? sl - a.pslots : sl;
+                            uint32_t &f = L.fill[sl * tl.T8 + cc];
+                            L.u.p.bst[bb] = ex;
+                            L.u.p.wb[bb] = f - ex;
+                            f += cnt;
+                            L.u.p.bcnt[bb] = 0;
+                            ex += cnt;
+                        }
+                    }
+                }
+                lds_sync();
+                Rec *stage = L.u.p.stage;
+#pragma unroll
+                for (int rr = 0; rr < RH; rr++) {
+                    if (tr[rr] == 0xffffffffu) continue;
+                    stage[L.u.p.bst[tr[rr] >> 16] + (tr[rr] & 0xffffu)] = rec[h * RH + rr];
+                }
+                lds_sync();
+                for (uint32_t q = tid; q < staged; q += kRunThreads) {
+                    const Rec r2 = stage[q];
+                    const uint32_t key = rec_key(r2);
+                    const uint32_t b = key >> 16, low = key & 0xffffu;
+                    const uint32_t pos = L.u.p.wb[b] + q;
+                    const uint32_t j = b / tl.T8, cc = b - j * tl.T8;
+                    uint32_t sl = slot_of_j0 + j;
+                    sl = sl >= a.pslots ? sl - a.pslots : sl;
+                    if (pos < cap) {
+                        const uint64_t e = (uint64_t)page_of(a, x, r, sl, cc) * cap + pos;
+                        if constexpr (CMP) a.pages16[e] = (uint16_t)low;
+                        else a.pages[e] = make_int2((int)low, r2.y);
+                    } else {
+                        long long units;
+                        uint32_t local;
+                        if constexpr (CMP) {
+                            units = class_units(a, low >> kPageClassShift);
+                            local = low & kPageLocalMask;
+                        } else {
+                            units = units_of<FIXED>(r2.y, a.m.shift64);
+                            local = low;
+                        }
+                        overflow_add<FIXED, true>(a, sl, x * tl.T8 + cc, local, units);
+                    }
+                }
+            }
+        }
+        lds_sync();  // the chunk tables are rewritten by the next chunk
+    }
+    lds_sync();
+    // publish the fill counters of all pages of this block
+    const uint32_t NF = a.pslots * tl.T8;
+    for (uint32_t f = tid; f < NF; f += kRunThreads) {
+        const uint32_t sl = f / tl.T8;
+        a.pfill[page_of(a, x, r, sl, f - sl * tl.T8)] = L.fill[f];
+    }
+    if (x == 0) {  // events emitted at t, counted once per spike
+        const uint64_t tot = block_sum_u64(emitted, L.ws64);
+        if (tid == 0 && tot) atomicAdd((unsigned long long *)&a.events8[t * kGroups], (unsigned long long)tot);
+    }
+    return M;
+}
+
+// Direct delivery (one delay): the tile reads, for every spike of t - dmin,
+// the run of its row that falls into the tile.
+template <bool FIXED, bool CMP>
+__device__ uint64_t run_gather(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t tile, uint32_t tile_lo,
+                               uint64_t t)
+{
+    uint64_t mine = 0;
+    if (t >= a.dmin) {
+        const uint32_t dslot = (uint32_t)((t - a.dmin) % a.spk_slots);
+        const uint32_t P = load_spike_set<true>(a, dslot, L.u.t.pre, L.ws);
+        mine = gather_direct<FIXED, CMP, true>(a, L.u.t.acc, L.u.t.pre, L.u.t.wpre, L.u.t.wbeg, tile, tile_lo, P,
+                                               dslot, -1);
+    }
+    const uint64_t tot = block_sum_u64(mine, L.ws64);
+    return tot;
+}
+
+// Raster bookkeeping shared by both deliveries: offsets of step t + 1 and the
+// capacity flag, by one workgroup; every workgroup advances its own copy of
+// the running base.
+__device__ __forceinline__ uint64_t raster_advance(const StepArgs &a, uint64_t t, uint64_t rbase, uint32_t M,
+                                                   bool writer)
+{
+    const bool ok = rbase + M <= a.raster_cap;
+    if (writer && threadIdx.x == 0) {
+        a.raster_offs[t + 1] = ok ? rbase + M : rbase;
+        if (!ok) atomicOr(a.flags, 2u);
+    }
+    return ok ? rbase + M : rbase;
+}
+
+template <bool FIXED, bool CMP, bool DIRECT>
+__global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
+{
+    __shared__ RunLDS<FIXED, CMP> L;
+    const StepArgs &a = ra.s;
+    RunCtl *ctl = ra.ctl;
+    const uint32_t tid = threadIdx.x;
+
+    // placement: the XCD this workgroup runs on, and a ticket within it
+    if (tid == 0) {
+        const uint32_t raw = xcc_id();
+        const uint32_t x = raw & (kGroups - 1);
+        if (raw >= kGroups) atomicOr(&ctl->abort_flag, kRunAbortPlacement);
+        L.x = x;
+        L.r = atomicAdd(&ctl->ticket[x * kCtlStride], 1u);
+        L.nspk = 0;
+        atomicAdd(&ctl->start, 1u);
+        L.stop = spin_ge(&ctl->start, gridDim.x, &ctl->abort_flag) ? 0u : 1u;
+        if (L.stop) atomicOr(a.flags, kRunStoppedFlag);
+    }
+    __syncthreads();
+    if (L.stop) return;
+    if (tid < kGroups && ld_ag(&ctl->ticket[tid * kCtlStride]) != ra.R) atomicOr(&L.stop, 1u);
+    if (tid == 0 && ld_ag(&ctl->abort_flag)) atomicOr(&L.stop, 1u);
+    __syncthreads();
+    if (L.stop) {  // every workgroup reads the same tickets: all leave here together
+        if (tid == 0) {
+            atomicOr(&ctl->abort_flag, kRunAbortPlacement);
+            atomicOr(a.flags, kRunStoppedFlag);
+        }
+        return;
+    }
+    const uint32_t x = L.x, r = L.r;
+    const Tiling tl = a.tl;
+    const bool has_tile = r < tl.T8;
+    const uint32_t tile = x * tl.T8 + r;
+    const uint32_t tile_lo = tile * tl.W;
+    const uint32_t tile_n = has_tile && tile_lo < a.n ? (a.n - tile_lo < tl.W ? a.n - tile_lo : tl.W) : 0u;
+    const ModelArgs &m = a.m;
+
+    // persistent LDS state
+    for (uint32_t q = tid; q < tile_n; q += kRunThreads) {
+        L.V[q] = a.V[tile_lo + q];
+        L.ref[q] = a.ref[tile_lo + q];
+    }
+    if (m.pois_len)
+        for (uint32_t q = tid; q < 256; q += kRunThreads) {
+            L.pois[q] = a.pois[q < m.pois_len ? q : 0u];
+            L.guide[q] = a.pois_guide[q];
+        }
+    if (!DIRECT) {
+        const uint32_t NF = a.pslots * tl.T8;
+        for (uint32_t f = tid; f < NF; f += kRunThreads) {
+            const uint32_t sl = f / tl.T8;
+            L.fill[f] = a.pfill[page_of(a, x, r, sl, f - sl * tl.T8)];
+        }
+    }
+    __syncthreads();
+    if (ra.n_steps) run_draws(a, L, tile_lo, tile_n, ra.t0);
+    uint64_t rbase = a.raster_cap ? a.raster_offs[ra.t0] : 0;
+    uint32_t eg = 0, ex = 0;
+    __syncthreads();
+
+    for (uint64_t s = 0; s < ra.n_steps; s++) {
+        const uint64_t t = ra.t0 + s;
+        const bool more = s + 1 < ra.n_steps;
+        if (has_tile) {
+            // the push phase reused this LDS: accumulators restart at zero, and
+            // the spike count of the previous step has been read by every thread
+            for (uint32_t q = tid; q < tl.W; q += kRunThreads) L.u.t.acc[q] = 0;
+            if (tid == 0) L.nspk = 0;
+            const uint64_t delivered = DIRECT ? run_gather(a, L, tile, tile_lo, t)
+                                              : run_drain(a, L, x, r, tile, tile_n, t);
+            run_update<FIXED, CMP, DIRECT>(ra, L, x, tile, tile_lo, tile_n, t, delivered);
+        }
+        if (!grid_sync(ra, L, x, ++eg, has_tile && more, tile_lo, tile_n, t + 1)) return;
+        if (DIRECT) {
+            if (a.raster_cap) {  // the spike list of t is complete: workgroup (0, 0) records it
+                const bool writer = x == 0 && r == 0;
+                const uint32_t M = load_spike_set<true>(a, (uint32_t)(t % a.spk_slots), L.u.p.pre, L.ws);
+                if (writer && rbase + M <= a.raster_cap)
+                    for (uint32_t k = tid; k < M; k += kRunThreads)
+                        a.raster[rbase + k] = spike_at<true>(a, L.u.p.pre, (uint32_t)(t % a.spk_slots), k);
+                rbase = raster_advance(a, t, rbase, M, writer);
+                __syncthreads();  // pre[] is the tile's scratch again
+            }
+        } else {
+            const uint32_t M = run_push(ra, L, x, r, t, rbase);
+            if (a.raster_cap) rbase = raster_advance(a, t, rbase, M, x == 0 && r == 0);
+            if (!xcd_sync(ra, L, x, ++ex)) return;
+        }
+    }
+
+    for (uint32_t q = tid; q < tile_n; q += kRunThreads) {
+        a.V[tile_lo + q] = L.V[q];
+        if (m.kind != SPK_SOURCE) a.ref[tile_lo + q] = L.ref[q];
+    }
+    if (tid == 0 && x == 0 && r == 0) *(uint64_t *)a.t_base = ra.t0 + ra.n_steps;
+}
+
+template <bool FIXED, bool CMP, bool DIRECT>
+hipError_t launch_run_t(const RunArgs &ra, hipStream_t s)
+{
+    RunArgs arg = ra;
+    void *args[] = {&arg};
+    return hipLaunchCooperativeKernel((const void *)k_run<FIXED, CMP, DIRECT>, dim3(kGroups * ra.R),
+                                      dim3(kRunThreads), args, 0, s);
+}
+
+}  // namespace
+
+bool run_supported(const StepArgs &a, uint32_t R)
+{
+    const Tiling &tl = a.tl;
+    if (R == 0 || R > kRunMaxR || tl.T8 > R || tl.T != kGroups * tl.T8 || tl.W > kMaxTileW) return false;
+    if (a.m.pois_len > 256) return false;
+    if (a.direct) return a.lists == 1 && a.spk_slots > a.dmin;
+    return a.pg1 == R && a.pslots * tl.T8 <= kRunMaxFill && a.lists * tl.T8 <= kMaxBuckets && a.spk_slots >= 2 &&
+           a.page_cap % 16 == 0 && tl.W <= 65536;
+}
+
+hipError_t launch_run(const RunArgs &ra, hipStream_t s)
+{
+    if (!run_supported(ra.s, ra.R)) return hipErrorInvalidValue;
+    const StepArgs &a = ra.s;
+    if (a.compact ? !a.syn32 || (!a.direct && !a.pages16) : !a.syn || (!a.direct && !a.pages))
+        return hipErrorInvalidValue;
+    const bool F = a.m.fixed, C = a.compact, D = a.direct;
+    if (F && C && D) return launch_run_t<true, true, true>(ra, s);
+    if (F && C && !D) return launch_run_t<true, true, false>(ra, s);
+    if (F && !C && D) return launch_run_t<true, false, true>(ra, s);
+    if (F && !C && !D) return launch_run_t<true, false, false>(ra, s);
+    if (!F && C && D) return launch_run_t<false, true, true>(ra, s);
+    if (!F && C && !D) return launch_run_t<false, true, false>(ra, s);
+    if (!F && !C && D) return launch_run_t<false, false, true>(ra, s);
+    return launch_run_t<false, false, false>(ra, s);
+}
+
+}  // namespace spk

@@ -5,10 +5,11 @@
 // the layout description is expanded on the device) into one row per source
 // neuron, grouped by target tile (Sec. III-A keeps rows sorted by target),
 // with each synapse carrying its delay (Sec. V), and records where every row
-// crosses the tile or XCD-group boundaries.  A step is the tile kernel
-// (delivery into LDS + update + spike list), then for binned delivery the
-// push kernel (the new spikes' events into per-arrival pages), then the
-// optional raster record; batches of steps are captured once into a HIP
+// crosses the tile or XCD-group boundaries.  Steps run either as one
+// persistent cooperative launch per spk_step call (spk_run.hip), or as the
+// tile kernel (delivery into LDS + update + spike list), then for binned
+// delivery the push kernel (the new spikes' events into per-arrival pages),
+// then the optional raster record, batches of steps captured once into a HIP
 // graph and replayed.  Spike counts stay on the device, so stepping never
 // waits for the host.
 #include <hip/hip_runtime.h>
@@ -54,6 +55,8 @@ constexpr uint32_t kPoisCap = 256;
 constexpr uint32_t kBatch = 32;                    // steps per captured graph
 constexpr uint64_t kPageBudget = 256ull << 20;     // page records across all pages (2 GiB)
 constexpr uint64_t kDebugPageCap = 4096;           // records per page for spk_debug_deliver
+constexpr uint64_t kRunMaxSteps = 1ull << 24;      // steps per persistent launch (barrier epochs fit u32)
+constexpr uint32_t kFlagRunStopped = 4u;           // device flag: a persistent launch stopped early
 
 uint64_t prob_threshold(double p)
 {
@@ -177,12 +180,16 @@ struct spk_net {
     uint64_t device_bytes = 0;
     std::vector<void *> allocs;
     std::map<uint32_t, hipGraphExec_t> graphs;
+    // persistent step kernel
+    bool persistent = false;
+    uint32_t run_R = 0;
+    RunCtl *ctl = nullptr;
     // profiling
     bool profiling = false;
     std::vector<hipEvent_t> ev_free;
-    std::vector<std::pair<hipEvent_t, hipEvent_t>> ev_push, ev_tile;
-    double ms_push = 0, ms_tile = 0;
-    uint64_t launches = 0;
+    std::vector<std::pair<hipEvent_t, hipEvent_t>> ev_push, ev_tile, ev_run;
+    double ms_push = 0, ms_tile = 0, ms_run = 0;
+    uint64_t launches = 0, run_launches = 0;
 };
 
 namespace {
@@ -389,6 +396,7 @@ spk_status derive(spk_net *net, bool explicit_csr)
     if (P.acc_mode > SPK_ACC_FIXED) return fail(SPK_EINVAL, "acc_mode");
     if (P.delivery > SPK_DELIVERY_BINNED) return fail(SPK_EINVAL, "delivery");
     if (P.syn_format > SPK_FORMAT_COMPACT) return fail(SPK_EINVAL, "syn_format");
+    if (P.step_mode > SPK_STEP_PERSISTENT) return fail(SPK_EINVAL, "step_mode");
     if (!explicit_csr && P.conn_kind > SPK_CONN_FIXED_IN) return fail(SPK_EINVAL, "conn_kind");
     if (!(P.p >= 0.0 && P.p <= 1.0)) return fail(SPK_EINVAL, "p in [0,1]");
     if (P.max_steps == 0) return fail(SPK_EINVAL, "max_steps must be >= 1");
@@ -551,9 +559,11 @@ spk_status finish_rows(spk_net *net)
     class_units(net);
 
     // Spike lists: direct delivery reads the lists of steps t - dmax .. t - dmin
-    // while writing that of t; binned delivery consumes the list of t within t.
+    // while writing that of t; binned delivery consumes the list of t within t,
+    // but in the persistent kernel one XCD may publish t + 1 while another
+    // still reads t, so there are two.
     const Tiling &tl = net->tl;
-    net->spk_slots = net->direct ? net->dmax + 1 : 1;
+    net->spk_slots = net->direct ? net->dmax + 1 : 2;
     if (!net->direct) {
         // Pages: (group, push block, arrival slot, tile).  A page never holds
         // more than nnz records (each synapse arrives at most once per slot),
@@ -671,15 +681,72 @@ spk_status sync_flags(spk_net *net, uint32_t *flags_out)
     uint32_t f = 0;
     SPK_HIP(hipMemcpy(&f, net->flags, 4, hipMemcpyDeviceToHost));
     if (flags_out) *flags_out = f;
+    if (f & kFlagRunStopped)
+        return fail(SPK_EHIP, "a persistent step launch stopped early (a barrier wait exceeded its "
+                              "bound); the network state is undefined");
+    return SPK_OK;
+}
+
+RunArgs run_args(const spk_net *net, uint64_t t0, uint64_t n_steps)
+{
+    RunArgs ra{};
+    ra.s = step_args(net);
+    ra.ctl = net->ctl;
+    ra.t0 = t0;
+    ra.n_steps = n_steps;
+    ra.R = net->run_R;
+    return ra;
+}
+
+// Step mode.  The persistent kernel needs a cooperative launch of one
+// workgroup per compute unit spread evenly over the XCDs; a launch of zero
+// steps checks that once (it only loads and stores back the state).
+spk_status choose_step_mode(spk_net *net)
+{
+    net->persistent = false;
+    const uint32_t mode = net->P.step_mode;
+    if (mode == SPK_STEP_GRAPH) return SPK_OK;
+    int coop = 0;
+    SPK_HIP(hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, net->device));
+    const int cus = cu_count();
+    net->run_R = cus > 0 && cus % (int)kGroups == 0 ? (uint32_t)(cus / (int)kGroups) : 0u;
+    const StepArgs a = step_args(net);
+    const bool fits = coop && run_supported(a, net->run_R);
+    if (!fits) {
+        if (mode == SPK_STEP_PERSISTENT)
+            return fail(SPK_EINVAL, "the persistent step kernel does not apply to this network or device "
+                                    "(tiles per XCD, delays, or cooperative launch)");
+        return SPK_OK;
+    }
+    hipStream_t s = net->stream;
+    SPK_TRY(dalloc(net, &net->ctl, 1));
+    SPK_HIP(hipMemsetAsync(net->ctl, 0, sizeof(RunCtl), s));
+    hipError_t e = launch_run(run_args(net, net->t, 0), s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    uint32_t abort_flag = 1;
+    if (e == hipSuccess) e = hipMemcpy(&abort_flag, &net->ctl->abort_flag, 4, hipMemcpyDeviceToHost);
+    if (e == hipSuccess && abort_flag == 0) {
+        net->persistent = true;
+        return SPK_OK;
+    }
+    (void)hipGetLastError();
+    (void)hipStreamSynchronize(s);
+    SPK_HIP(hipMemsetAsync(net->flags, 0, 4, s));  // the probe's stop flag
+    SPK_HIP(hipStreamSynchronize(s));
+    dfree(net, net->ctl);
+    net->ctl = nullptr;
+    if (mode == SPK_STEP_PERSISTENT)
+        return fail(SPK_EHIP, std::string("the persistent step kernel could not be placed: ") +
+                                  (e != hipSuccess ? hipGetErrorString(e) : "uneven workgroup placement"));
     return SPK_OK;
 }
 
 spk_status collect_profile(spk_net *net)
 {
     SPK_HIP(hipStreamSynchronize(net->stream));
-    for (int which = 0; which < 2; which++) {
-        auto &v = which ? net->ev_tile : net->ev_push;
-        double &acc = which ? net->ms_tile : net->ms_push;
+    for (int which = 0; which < 3; which++) {
+        auto &v = which == 2 ? net->ev_run : which ? net->ev_tile : net->ev_push;
+        double &acc = which == 2 ? net->ms_run : which ? net->ms_tile : net->ms_push;
         for (auto &pr : v) {
             float ms = 0;
             SPK_HIP(hipEventElapsedTime(&ms, pr.first, pr.second));
@@ -748,7 +815,7 @@ void destroy_net(spk_net *net)
     if (!net) return;
     if (net->stream) (void)hipStreamSynchronize(net->stream);
     for (auto &kv : net->graphs) (void)hipGraphExecDestroy(kv.second);
-    for (auto *v : {&net->ev_push, &net->ev_tile})
+    for (auto *v : {&net->ev_push, &net->ev_tile, &net->ev_run})
         for (auto &pr : *v) {
             (void)hipEventDestroy(pr.first);
             (void)hipEventDestroy(pr.second);
@@ -865,6 +932,7 @@ spk_status spk_create(const spk_params *params, void *stream, spk_net **out)
     if (st == SPK_OK) st = setup_stream(net, stream);
     if (st == SPK_OK) st = generate(net);
     if (st == SPK_OK) st = alloc_state(net);
+    if (st == SPK_OK) st = choose_step_mode(net);
     if (st == SPK_OK) st = sync_flags(net, nullptr);
     if (st != SPK_OK) {
         std::string msg = g_err;
@@ -958,6 +1026,7 @@ spk_status spk_create_from_csr(const spk_params *params, uint32_t n, const uint6
         dfree(net, in_d);
         SPK_TRY(finish_rows(net));
         SPK_TRY(alloc_state(net));
+        SPK_TRY(choose_step_mode(net));
         return sync_flags(net, nullptr);
     };
     spk_status st = run();
@@ -977,6 +1046,29 @@ spk_status spk_step(spk_net *net, uint64_t n_steps)
     if (net->t + n_steps > net->P.max_steps)
         return fail(SPK_EOVERFLOW, "max_steps exceeded");
     hipStream_t s = net->stream;
+    if (net->persistent) {  // one cooperative launch per (at most 2^24) steps
+        uint64_t left = n_steps;
+        while (left) {
+            const uint64_t B = std::min<uint64_t>(left, kRunMaxSteps);
+            hipEvent_t e0 = nullptr, e1 = nullptr;
+            if (net->profiling) {
+                SPK_TRY(get_event(net, &e0));
+                SPK_TRY(get_event(net, &e1));
+            }
+            SPK_HIP(hipMemsetAsync(net->ctl, 0, sizeof(RunCtl), s));
+            if (e0) SPK_HIP(hipEventRecord(e0, s));
+            SPK_HIP(launch_run(run_args(net, net->t, B), s));
+            if (e1) {
+                SPK_HIP(hipEventRecord(e1, s));
+                net->ev_run.push_back({e0, e1});
+                net->run_launches++;
+                net->launches += B;
+            }
+            left -= B;
+            net->t += B;
+        }
+        return SPK_OK;
+    }
     if (net->profiling) {  // plain launches with events around every kernel
         const StepArgs a = step_args(net);
         for (uint64_t k = 0; k < n_steps; k++) {
@@ -1235,6 +1327,7 @@ spk_status spk_stats(spk_net *net, spk_stats_t *out)
     st.tiles = net->tl.T;
     st.delivery = net->direct ? SPK_DELIVERY_DIRECT : SPK_DELIVERY_BINNED;
     st.page_cap = net->page_cap;
+    st.step_mode = net->persistent ? SPK_STEP_PERSISTENT : SPK_STEP_GRAPH;
     *out = st;
     return SPK_OK;
 }
@@ -1244,18 +1337,21 @@ spk_status spk_set_profiling(spk_net *net, int on)
     SPK_TRY(check_ready(net));
     SPK_TRY(collect_profile(net));
     net->profiling = on != 0;
-    net->ms_push = net->ms_tile = 0;
-    net->launches = 0;
+    net->ms_push = net->ms_tile = net->ms_run = 0;
+    net->launches = net->run_launches = 0;
     return SPK_OK;
 }
 
-spk_status spk_read_kernel_ms(spk_net *net, double *push_ms, double *tile_ms, uint64_t *steps)
+spk_status spk_read_kernel_ms(spk_net *net, double *push_ms, double *tile_ms, double *run_ms,
+                              uint64_t *steps, uint64_t *run_launches)
 {
     SPK_TRY(check_ready(net));
     SPK_TRY(collect_profile(net));
     if (push_ms) *push_ms = net->ms_push;
     if (tile_ms) *tile_ms = net->ms_tile;
+    if (run_ms) *run_ms = net->ms_run;
     if (steps) *steps = net->launches;
+    if (run_launches) *run_launches = net->run_launches;
     return SPK_OK;
 }
 

@@ -31,7 +31,7 @@
 // delay d from a spike at t lands in the page of arrival slot (t + d) mod dmax.
 #include <hip/hip_runtime.h>
 
-#include "spk_internal.h"
+#include "spk_dev.h"
 
 namespace spk {
 
@@ -45,213 +45,6 @@ constexpr uint32_t kStage = kLoadPhase / 2;               // events bucket-sorte
 constexpr uint32_t kMaxChunkSpikes = 1024;                // rows resolved per push chunk
 constexpr int kRounds = kMaxTileW / kTileThreads;         // neurons per tile thread
 static_assert(kMaxTiles <= 2 * kTileThreads, "spike-count prefix takes at most two tiles per thread");
-
-__device__ __forceinline__ uint32_t lane_id() { return threadIdx.x & (kWave - 1); }
-
-// Workgroup barrier that orders LDS traffic only.  __syncthreads() also
-// waits for every outstanding global load and store of the thread, which
-// would turn each phase of these kernels into a full memory round trip;
-// here global loads issued before the barrier stay in flight across it.
-// Used wherever threads of a block communicate through LDS alone.
-__device__ __forceinline__ void lds_sync()
-{
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
-
-__device__ __forceinline__ void lds_wave_sync()
-{
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
-
-__device__ __forceinline__ uint64_t step_index(const StepArgs &a, uint32_t i, int64_t t_explicit)
-{
-    return t_explicit >= 0 ? (uint64_t)t_explicit : *a.t_base + i;
-}
-
-// Block-wide exclusive scan of one u32 per thread (blockDim <= 1024).
-__device__ uint32_t block_scan_u32(uint32_t x, uint32_t *ws /*>=16*/, uint32_t *total)
-{
-    const uint32_t lane = lane_id(), w = threadIdx.x / kWave, nw = blockDim.x / kWave;
-    uint32_t inc = x;
-    for (int o = 1; o < kWave; o <<= 1) {
-        const uint32_t y = __shfl_up(inc, o);
-        if (lane >= (uint32_t)o) inc += y;
-    }
-    if (lane == kWave - 1) ws[w] = inc;
-    lds_sync();
-    uint32_t before = 0, tot = 0;
-    for (uint32_t k = 0; k < nw; k++) {
-        const uint32_t v = ws[k];
-        before += k < w ? v : 0u;
-        tot += v;
-    }
-    lds_sync();
-    *total = tot;
-    return before + inc - x;
-}
-
-// Same, without the trailing barrier: ws must not be written again before
-// the caller's next barrier.
-__device__ uint32_t block_scan_u32_open(uint32_t x, uint32_t *ws /*>=16*/, uint32_t *total)
-{
-    const uint32_t lane = lane_id(), w = threadIdx.x / kWave, nw = blockDim.x / kWave;
-    uint32_t inc = x;
-    for (int o = 1; o < kWave; o <<= 1) {
-        const uint32_t y = __shfl_up(inc, o);
-        if (lane >= (uint32_t)o) inc += y;
-    }
-    if (lane == kWave - 1) ws[w] = inc;
-    lds_sync();
-    uint32_t before = 0, tot = 0;
-    for (uint32_t k = 0; k < nw; k++) {
-        const uint32_t v = ws[k];
-        before += k < w ? v : 0u;
-        tot += v;
-    }
-    *total = tot;
-    return before + inc - x;
-}
-
-__device__ __forceinline__ uint64_t block_sum_u64(uint64_t x, unsigned long long *ws /*>=16*/)
-{
-    const uint32_t lane = lane_id(), w = threadIdx.x / kWave, nw = blockDim.x / kWave;
-    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
-    if (lane == 0) ws[w] = x;
-    lds_sync();
-    uint64_t tot = 0;
-    for (uint32_t k = 0; k < nw; k++) tot += ws[k];
-    lds_sync();
-    return tot;
-}
-
-// Block-wide exclusive max-scan of one u32 per thread.
-__device__ uint32_t block_scan_max_u32(uint32_t x, uint32_t *ws)
-{
-    const uint32_t lane = lane_id(), w = threadIdx.x / kWave;
-    uint32_t inc = x;
-    for (int o = 1; o < kWave; o <<= 1) {
-        const uint32_t y = __shfl_up(inc, o);
-        if (lane >= (uint32_t)o) inc = y > inc ? y : inc;
-    }
-    const uint32_t ex_w = __shfl_up(inc, 1);
-    if (lane == kWave - 1) ws[w] = inc;
-    lds_sync();
-    uint32_t before = 0;
-    for (uint32_t k = 0; k < w; k++) before = ws[k] > before ? ws[k] : before;
-    lds_sync();
-    return lane ? (ex_w > before ? ex_w : before) : before;
-}
-
-// The spike list of one slot is spread over per-tile segments: pre[] gets
-// the exclusive prefix of the T segment counts; returns the total.
-__device__ uint32_t load_spike_set(const StepArgs &a, uint32_t slot, uint32_t *pre, uint32_t *ws)
-{
-    const uint32_t T = a.tl.T, W = a.tl.W;
-    const uint32_t b = threadIdx.x * 2;
-    const uint32_t *cnt = a.spk_cnt + (uint64_t)slot * T;
-    uint32_t c0 = cnt[b < T ? b : 0], c1 = cnt[b + 1 < T ? b + 1 : 0];
-    c0 = b < T ? (c0 < W ? c0 : W) : 0u;
-    c1 = b + 1 < T ? (c1 < W ? c1 : W) : 0u;
-    uint32_t tot;
-    const uint32_t ex = block_scan_u32(c0 + c1, ws, &tot);
-    if (b < T) pre[b] = ex;
-    if (b + 1 < T) pre[b + 1] = ex + c0;
-    if (threadIdx.x == 0) pre[T] = tot;
-    lds_sync();
-    return tot;
-}
-
-// k-th spike of the slot (k < total): largest tile with pre[tile] <= k.
-__device__ __forceinline__ uint32_t spike_at(const StepArgs &a, const uint32_t *pre, uint32_t slot,
-                                             uint32_t k)
-{
-    uint32_t lo = 0, hi = a.tl.T - 1;
-    while (lo < hi) {
-        const uint32_t mid = (lo + hi + 1) >> 1;
-        if (pre[mid] <= k) lo = mid; else hi = mid - 1;
-    }
-    return a.spk_ids[((uint64_t)slot * a.tl.T + lo) * a.tl.W + (k - pre[lo])];
-}
-
-// Page (x, g1, slot, c) of the binned delivery; records at page * page_cap.
-__device__ __forceinline__ uint32_t page_of(const StepArgs &a, uint32_t x, uint32_t g1, uint32_t slot,
-                                            uint32_t c)
-{
-    return ((x * a.pg1 + g1) * a.pslots + slot) * a.tl.T8 + c;
-}
-
-__device__ __forceinline__ uint32_t arrival_slot(const StepArgs &a, uint64_t t, uint32_t j, bool dbg)
-{
-    return dbg ? 0u : (uint32_t)((t + a.dmin + j) % a.pslots);
-}
-
-// Accumulator conversions.  fp32 mode: exact int64 multiple of 2^-S64.
-__device__ __forceinline__ long long to_fixed64(int32_t wbits, int32_t s64)
-{
-    return __double2ll_rn(ldexp((double)__int_as_float(wbits), s64));
-}
-// The unit is chosen so that |acc| < 2^53: the conversion to double is
-// exact, the scaling by 2^-S64 is exact, and the one rounding is to fp32.
-__device__ __forceinline__ float fixed64_to_float(unsigned long long acc, int32_t s64)
-{
-    return (float)ldexp((double)(long long)acc, -s64);
-}
-
-// Accumulator units of one event: the stored weight bits converted
-// (full format), or the class's precomputed value (compact format).
-template <bool FIXED>
-__device__ __forceinline__ long long units_of(int32_t wbits, int32_t s64)
-{
-    return FIXED ? (long long)wbits : to_fixed64(wbits, s64);
-}
-// Selected without a dynamic index into the kernel arguments (which would
-// go through scratch memory).
-__device__ __forceinline__ long long class_units(const StepArgs &a, uint32_t cls)
-{
-    const long long w01 = cls & 1u ? a.wval[1] : a.wval[0];
-    const long long w23 = cls & 1u ? a.wval[3] : a.wval[2];
-    return cls & 2u ? w23 : w01;
-}
-
-template <bool FIXED> struct Acc;
-template <> struct Acc<true> {
-    using T = int32_t;
-    static __device__ __forceinline__ void add(T *p, long long units) { atomicAdd(p, (int32_t)units); }
-};
-template <> struct Acc<false> {
-    using T = unsigned long long;
-    static __device__ __forceinline__ void add(T *p, long long units)
-    {
-        atomicAdd(p, (unsigned long long)units);
-    }
-};
-
-// Synapse record of each format, and its key (class, delay index, target).
-template <bool CMP> struct SynRec;
-template <> struct SynRec<false> {
-    using T = int2;
-    static __device__ __forceinline__ T load(const StepArgs &a, uint64_t e) { return a.syn[e]; }
-};
-template <> struct SynRec<true> {
-    using T = uint32_t;
-    static __device__ __forceinline__ T load(const StepArgs &a, uint64_t e) { return a.syn32[e]; }
-};
-// Global fallback for a full page (rare): same units as the LDS accumulator,
-// one accumulator per (arrival slot, neuron).
-template <bool FIXED>
-__device__ __forceinline__ void overflow_add(const StepArgs &a, uint32_t slot, uint32_t tile,
-                                             uint32_t local, long long units)
-{
-    const uint64_t st = (uint64_t)slot * a.tl.T + tile;
-    const uint64_t i = st * a.tl.W + local;
-    if (FIXED) atomicAdd((int32_t *)a.acc_ovf + i, (int32_t)units);
-    else atomicAdd((unsigned long long *)a.acc_ovf + i, (unsigned long long)units);
-    if (a.ovf_flag[st] == 0) atomicOr(&a.ovf_flag[st], 1u);
-}
 
 // ------------------------------------------------------------ push kernel
 
@@ -468,73 +261,6 @@ struct TileLDS {
     uint16_t guide[256];
 };
 
-// Accumulate the tile's events directly from the rows of the given spikes
-// (direct mode): each wave takes 64 spikes at a time, lane l resolving spike
-// l's run for this tile; the 64 runs are then streamed lane-parallel.  With
-// jf >= 0 only synapses of delay index jf are delivered.  Returns the number
-// of events this thread delivered.
-template <bool FIXED, bool CMP>
-__device__ uint32_t gather_direct(const StepArgs &a, TileLDS<FIXED> &L, uint32_t tile, uint32_t tile_lo,
-                                  uint32_t P, uint32_t slot, int32_t jf)
-{
-    using Rec = typename SynRec<CMP>::T;
-    const uint32_t lane = lane_id(), w = threadIdx.x / kWave, nw = kTileThreads / kWave;
-    const uint32_t T1 = a.tl.T + 1;
-    uint32_t mine = 0;
-    for (uint32_t p0 = w * kWave; p0 < P; p0 += nw * kWave) {
-        uint32_t len = 0;
-        uint64_t beg = 0;
-        if (p0 + lane < P) {
-            const uint32_t s = a.dbg_spikes ? a.dbg_spikes[p0 + lane] : spike_at(a, L.pre, slot, p0 + lane);
-            const uint16_t *to = a.toff + (uint64_t)s * T1 + tile;
-            const uint32_t b = to[0], e = to[1];
-            beg = a.row_ptr[s] + b;
-            len = e - b;
-        }
-        uint32_t inc = len;
-        for (int o = 1; o < kWave; o <<= 1) {
-            const uint32_t y = __shfl_up(inc, o);
-            if (lane >= (uint32_t)o) inc += y;
-        }
-        const uint32_t tot = __shfl(inc, kWave - 1);
-        L.wpre[w][lane] = inc - len;
-        L.wbeg[w][lane] = beg;
-        if (lane == 0) L.wpre[w][kWave] = tot;
-        lds_wave_sync();
-        constexpr int U = 8;  // loads in flight per lane
-        for (uint32_t f0 = 0; f0 < tot; f0 += kWave * U) {
-            uint64_t idx[U];
-#pragma unroll
-            for (int u = 0; u < U; u++) {
-                const uint32_t f = f0 + u * kWave + lane;
-                const uint32_t fc = f < tot ? f : 0u;
-                uint32_t lo = 0, hi = kWave - 1;
-                while (lo < hi) {
-                    const uint32_t mid = (lo + hi + 1) >> 1;
-                    if (L.wpre[w][mid] <= fc) lo = mid; else hi = mid - 1;
-                }
-                idx[u] = f < tot ? L.wbeg[w][lo] + (fc - L.wpre[w][lo]) : 0ull;
-            }
-            Rec r[U];
-#pragma unroll
-            for (int u = 0; u < U; u++) r[u] = SynRec<CMP>::load(a, idx[u]);  // unconditional, see push
-#pragma unroll
-            for (int u = 0; u < U; u++) {
-                if (f0 + u * kWave + lane >= tot) continue;
-                const uint32_t key = rec_key(r[u]);
-                if (jf >= 0 && (int32_t)rec_delay(key) != jf) continue;
-                long long units;
-                if constexpr (CMP) units = class_units(a, rec_class(key));
-                else units = units_of<FIXED>(r[u].y, a.m.shift64);
-                Acc<FIXED>::add(&L.acc[rec_target(key) - tile_lo], units);
-                mine++;
-            }
-        }
-        __builtin_amdgcn_wave_barrier();
-    }
-    return mine;
-}
-
 template <bool FIXED, bool CMP>
 __global__ __launch_bounds__(kTileThreads) void k_tile(StepArgs a, uint32_t i, int64_t t_explicit)
 {
@@ -592,14 +318,15 @@ __global__ __launch_bounds__(kTileThreads) void k_tile(StepArgs a, uint32_t i, i
         // rows in this tile (only the synapses of delay d when there are several)
         uint64_t mine = 0;
         if (debug) {
-            mine = gather_direct<FIXED, CMP>(a, L, tile, tile_lo, a.dbg_n, 0, a.dbg_j);
+            mine = gather_direct<FIXED, CMP, false>(a, L.acc, L.pre, L.wpre, L.wbeg, tile, tile_lo, a.dbg_n, 0, a.dbg_j);
         } else {
             for (uint32_t j = 0; j < a.lists; j++) {
                 const uint64_t d = (uint64_t)a.dmin + j;
                 if (t < d) break;
                 const uint32_t dslot = (uint32_t)((t - d) % a.spk_slots);
                 const uint32_t P = load_spike_set(a, dslot, L.pre, L.ws);
-                mine += gather_direct<FIXED, CMP>(a, L, tile, tile_lo, P, dslot, a.lists > 1 ? (int32_t)j : -1);
+                mine += gather_direct<FIXED, CMP, false>(a, L.acc, L.pre, L.wpre, L.wbeg, tile, tile_lo, P, dslot,
+                                                         a.lists > 1 ? (int32_t)j : -1);
                 lds_sync();
             }
         }

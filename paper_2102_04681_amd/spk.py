@@ -19,12 +19,13 @@ import numpy as np
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libspk.so")
 
 SPK_OK, SPK_EINVAL, SPK_ENOMEM, SPK_EHIP, SPK_EOVERFLOW, SPK_ESTATE = 0, -1, -2, -3, -4, -5
-SPK_ABI_VERSION = 2
+SPK_ABI_VERSION = 3
 SPK_LIF, SPK_SOURCE = 0, 1
 SPK_CONN_BERNOULLI, SPK_CONN_FIXED_OUT, SPK_CONN_FIXED_IN, SPK_CONN_EXPLICIT = 0, 1, 2, 3
 SPK_ACC_F32, SPK_ACC_FIXED = 0, 1
 SPK_DELIVERY_AUTO, SPK_DELIVERY_DIRECT, SPK_DELIVERY_BINNED = 0, 1, 2
 SPK_FORMAT_AUTO, SPK_FORMAT_FULL, SPK_FORMAT_COMPACT = 0, 1, 2
+SPK_STEP_AUTO, SPK_STEP_GRAPH, SPK_STEP_PERSISTENT = 0, 1, 2
 
 EXPORTED = [
     "spk_preset", "spk_create", "spk_create_from_csr", "spk_step", "spk_sync",
@@ -49,7 +50,8 @@ class spk_params(C.Structure):
         ("delay_min", C.c_uint32), ("delay_max", C.c_uint32),
         ("ext_lambda", C.c_double), ("ext_w", C.c_float), ("acc_mode", C.c_uint32),
         ("src_rate_hz", C.c_double), ("fixed_shift", C.c_int32), ("delivery", C.c_uint32),
-        ("syn_format", C.c_uint32), ("max_steps", C.c_uint64), ("raster_capacity", C.c_uint64),
+        ("syn_format", C.c_uint32), ("step_mode", C.c_uint32), ("max_steps", C.c_uint64),
+        ("raster_capacity", C.c_uint64),
     ]
 
 
@@ -61,7 +63,7 @@ class spk_stats_t(C.Structure):
         ("delay_lists", C.c_uint32), ("max_row", C.c_uint32), ("pois_len", C.c_uint32),
         ("fixed_shift", C.c_int32), ("k", C.c_float), ("bytes_per_synapse", C.c_double),
         ("tile_width", C.c_uint32), ("tiles", C.c_uint32), ("delivery", C.c_uint32),
-        ("page_cap", C.c_uint32),
+        ("page_cap", C.c_uint32), ("step_mode", C.c_uint32),
     ]
 
 
@@ -94,7 +96,7 @@ def lib():
             "spk_stats": (i32, [P, C.POINTER(spk_stats_t)]),
             "spk_set_profiling": (i32, [P, i32]),
             "spk_read_kernel_ms": (i32, [P, C.POINTER(C.c_double), C.POINTER(C.c_double),
-                                         C.POINTER(u64)]),
+                                         C.POINTER(C.c_double), C.POINTER(u64), C.POINTER(u64)]),
             "spk_hbm_copy": (i32, [P, u64, i32, C.POINTER(C.c_double)]),
             "spk_destroy": (None, [P]),
             "spk_last_error": (C.c_char_p, []),
@@ -286,11 +288,15 @@ class Net:
     def set_profiling(self, on: bool):
         _check(lib().spk_set_profiling(self._h, 1 if on else 0), "spk_set_profiling")
 
-    def kernel_ms(self):
-        d, u, n = C.c_double(), C.c_double(), C.c_uint64()
-        _check(lib().spk_read_kernel_ms(self._h, C.byref(d), C.byref(u), C.byref(n)),
-               "spk_read_kernel_ms")
-        return d.value, u.value, n.value
+    def kernel_ms(self) -> dict:
+        """Summed kernel durations (ms) since set_profiling: push, tile and
+        persistent launches, with the step and persistent-launch counts."""
+        d, u, r = C.c_double(), C.c_double(), C.c_double()
+        n, nr = C.c_uint64(), C.c_uint64()
+        _check(lib().spk_read_kernel_ms(self._h, C.byref(d), C.byref(u), C.byref(r), C.byref(n),
+                                        C.byref(nr)), "spk_read_kernel_ms")
+        return {"push_ms": d.value, "tile_ms": u.value, "run_ms": r.value, "steps": n.value,
+                "run_launches": nr.value}
 
     def hbm_copy(self, nbytes: int, reps: int = 10) -> float:
         ms = C.c_double()

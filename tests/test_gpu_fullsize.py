@@ -2,9 +2,10 @@
 
 Workload: 2,000,000 LIF neurons, fixed out-degree 1,500 (3.0e9 synapses),
 delays 1..20 steps, external Poisson drive at twice the threshold rate,
-fp32 accumulation, binned delivery, steps replayed from HIP graphs.  The
-oracle cannot simulate this network step by step in test time, so it checks
-sampled outputs it can compute one by one:
+fp32 accumulation, binned delivery, steps run by the persistent kernel (as
+bench.py times them) and replayed from HIP graphs.  The oracle cannot
+simulate this network step by step in test time, so it checks sampled
+outputs it can compute one by one:
 
   - sampled rows, generated lazily by the oracle, equal the library's rows;
   - after 300 steps, the input of sampled neurons at the next step is the
@@ -41,14 +42,16 @@ def _say(*a):
     sys.stdout.flush()
 
 
-def test_full_size_bench_configuration_sampled(spk_full):
+@pytest.mark.parametrize("step_mode", [2, 1], ids=["persist", "graph"])
+def test_full_size_bench_configuration_sampled(spk_full, step_mode):
     spk = spk_full
-    cfg = I.config(4, driven=True)
+    cfg = I.config(4, driven=True, step_mode=step_mode)
     n, K, dmax = cfg["n"], cfg["k_out"], cfg["delay_max"]
     T0 = 300
     _say(f"[full] create n={n} k_out={K}")
     g = spk.Net(cfg, max_steps=T0 + 1, raster_capacity=4_000_000)
     st = g.stats()
+    assert st["step_mode"] == step_mode
     assert st["nnz"] == n * K
     assert st["delivery"] == spk.SPK_DELIVERY_BINNED
     s64 = int(st["fixed_shift"])
@@ -68,7 +71,7 @@ def test_full_size_bench_configuration_sampled(spk_full):
         assert np.array_equal(w[a:b][gi].view(np.uint32), ow[oi].view(np.uint32)), f"row {s}: weights"
     _say("[full] rows ok")
 
-    # 2. run as the benchmark does (graph replay), then one more step
+    # 2. run as the benchmark does, then one more step
     g.step(T0)
     V0, R0 = g.state()
     g.step(1)

@@ -9,7 +9,10 @@ Bar (per the method's two accumulation modes):
     once;
   - whole simulation in fixed-point mode: bit-identical rasters, counts,
     events, delivered events and final state, for both delivery strategies
-    and for graph replay as well as plain launches;
+    and for every way of running the steps (graph replay, plain launches,
+    the persistent kernel);
+  - the persistent kernel and the graph path: bit-identical in fp32 mode
+    too (both sum exactly and round once);
   - fp32 mode: mean firing rate within 1 % (the oracle adds fp32 inputs one
     by one in push order, the library rounds the exact sum once, so spike
     trains diverge chaotically after the first difference).
@@ -48,7 +51,7 @@ _ORACLE_RUNS = {}
 
 
 def _key(cfg):
-    return tuple(sorted((k, v) for k, v in cfg.items() if k not in ("delivery", "syn_format")))
+    return tuple(sorted((k, v) for k, v in cfg.items() if k not in ("delivery", "syn_format", "step_mode")))
 
 
 def _oracle_net(cfg):
@@ -245,19 +248,34 @@ RUN_CASES = [
 ]
 
 
+# how the steps run: graph replay, plain launches with events (profiling),
+# the persistent kernel, and the persistent kernel with events around it
+MODES = [("graph", 1, False), ("launch", 1, True), ("persist", 2, False), ("persist-prof", 2, True)]
+
+
+def _persistent_applies(cfg, delivery):
+    """Shapes the persistent kernel takes: direct delivery with one delay,
+    or binned delivery (the test shapes are all small enough)."""
+    return delivery == 2 or cfg["delay_min"] == cfg["delay_max"]
+
+
 @pytest.mark.parametrize("name,mk,T", RUN_CASES, ids=[c[0] for c in RUN_CASES])
 @pytest.mark.parametrize("delivery", [1, 2], ids=["direct", "binned"])
-@pytest.mark.parametrize("profiled", [False, True], ids=["graph", "launch"])
+@pytest.mark.parametrize("mode,step_mode,profiled", MODES, ids=[m[0] for m in MODES])
 @pytest.mark.parametrize("fmt", [f for f, _ in FORMATS], ids=[n for _, n in FORMATS])
-def test_fixed_point_simulation_bit_identical(spk, name, mk, T, delivery, profiled, fmt):
+def test_fixed_point_simulation_bit_identical(spk, name, mk, T, delivery, mode, step_mode, profiled, fmt):
     cfg = mk()
     cfg["acc_mode"] = I.ACC_FIXED
     cfg["delivery"] = delivery
     cfg["syn_format"] = fmt
+    cfg["step_mode"] = step_mode
     if profiled and name not in ("C0-driven", "C4-12000"):
-        pytest.skip("direct-launch path checked on two shapes")
-    _say(f"[run] {name} n={cfg['n']} T={T} delivery={delivery} profiled={profiled} format={fmt}")
+        pytest.skip("profiled paths checked on two shapes")
+    if step_mode == 2 and not _persistent_applies(cfg, delivery):
+        pytest.skip("the persistent kernel takes direct delivery with one delay only")
+    _say(f"[run] {name} n={cfg['n']} T={T} delivery={delivery} mode={mode} format={fmt}")
     g = spk.Net(cfg, max_steps=T, raster_capacity=cfg["n"] * T)
+    assert g.stats()["step_mode"] == step_mode
     g.set_profiling(profiled)
     g.step(T)
     offs, ids = g.raster()
@@ -282,20 +300,25 @@ def test_fixed_point_simulation_bit_identical(spk, name, mk, T, delivery, profil
             np.add.at(want, dd[dd < T], 1)
     assert np.array_equal(dl, want), "delivered-event counts differ"
     if profiled:
-        b, tile_ms, steps = g.kernel_ms()
-        assert steps == T and tile_ms > 0
+        km = g.kernel_ms()
+        assert km["steps"] == T
+        if step_mode == 2:
+            assert km["run_launches"] == 1 and km["run_ms"] > 0 and km["tile_ms"] == 0
+        else:
+            assert km["tile_ms"] > 0 and km["run_launches"] == 0
 
 
 @pytest.mark.parametrize("acc", [I.ACC_F32, I.ACC_FIXED], ids=["f32", "fixed"])
 @pytest.mark.parametrize("fmt", [f for f, _ in FORMATS], ids=[n for _, n in FORMATS])
-def test_bin_overflow_fallback(spk, acc, fmt, monkeypatch):
+@pytest.mark.parametrize("step_mode", [1, 2], ids=["graph", "persist"])
+def test_bin_overflow_fallback(spk, acc, fmt, step_mode, monkeypatch):
     # 64 neurons, 200 synapses each (multapses), all above threshold at t=0:
     # the one tile receives 12 800 events at step 1, ~400 per push block,
     # while every page is capped at 64 records, so the global-atomic
     # fallback must deliver the rest (in the simulation and in debug_deliver).
     monkeypatch.setenv("SPK_PAGE_CAP", "64")
     cfg = I.config(4, n=64, k_out=200, delay_min=1, delay_max=1, v0_lo=-49.0, v0_hi=-49.0,
-                   t_ref_ms=0.0, acc_mode=acc, delivery=2, syn_format=fmt)
+                   t_ref_ms=0.0, acc_mode=acc, delivery=2, syn_format=fmt, step_mode=step_mode)
     T = 6
     g = spk.Net(cfg, max_steps=T, raster_capacity=64 * T)
     assert g.stats()["page_cap"] == 64
@@ -314,8 +337,9 @@ def test_bin_overflow_fallback(spk, acc, fmt, monkeypatch):
         assert np.all(np.abs(got - want) <= ulp)
 
 
-def test_resume_matches_single_run(spk):
-    cfg = I.scaled(4, 5000, k_out=500, acc_mode=I.ACC_FIXED)
+@pytest.mark.parametrize("step_mode", [1, 2], ids=["graph", "persist"])
+def test_resume_matches_single_run(spk, step_mode):
+    cfg = I.scaled(4, 5000, k_out=500, acc_mode=I.ACC_FIXED, step_mode=step_mode)
     a = spk.Net(cfg, max_steps=120, raster_capacity=5000 * 120)
     b = spk.Net(cfg, max_steps=120, raster_capacity=5000 * 120)
     a.step(50)
@@ -324,15 +348,18 @@ def test_resume_matches_single_run(spk):
         b.step(1)
     assert np.array_equal(a.raster()[1], b.raster()[1])
     assert np.array_equal(a.state()[0].view(np.uint32), b.state()[0].view(np.uint32))
+    assert np.array_equal(a.delivered(), b.delivered())
 
 
-def test_delay_chain_spike_timing(spk):
+@pytest.mark.parametrize("step_mode", [1, 2], ids=["graph", "persist"])
+def test_delay_chain_spike_timing(spk, step_mode):
     delays = [1, 3, 2, 5]
     n = 5
     row_ptr = np.array([0, 1, 2, 3, 4, 4], dtype=np.uint64)
     col = np.array([1, 2, 3, 4], dtype=np.uint32)
     w = np.full(4, 15.0, dtype=np.float32)
-    cfg = I.explicit_params(n, v0_lo=-49.0, v0_hi=-49.0, t_ref_ms=0.0, delay_min=1, delay_max=5)
+    cfg = I.explicit_params(n, v0_lo=-49.0, v0_hi=-49.0, t_ref_ms=0.0, delay_min=1, delay_max=5,
+                            step_mode=step_mode)
     g = spk.Net(cfg, max_steps=20, raster_capacity=100,
                 csr=(row_ptr, col, w, np.array(delays, dtype=np.uint8)))
     g.step(20)
@@ -455,3 +482,45 @@ def test_explicit_adjacency_formats(spk, n_w, fmt):
             assert r["counts"].sum() > 0
             assert np.array_equal(g.raster()[1], r["raster"]), "rasters differ"
             assert np.array_equal(g.state()[0].view(np.uint32), o.state()[0].view(np.uint32))
+
+
+@pytest.mark.parametrize("name,mk,T", [
+    ("C4-20000", lambda: I.scaled(4, 20000, k_out=1500), 1500),
+    ("C1-8000", lambda: I.scaled(1, 8000), 800),
+    ("C3-30000", lambda: I.scaled(3, 30000, k_out=1000), 200),
+    ("C2-8000", lambda: I.scaled(2, 8000, k_in_exc=640, k_in_inh=160), 800),
+], ids=["C4-20000", "C1-8000", "C3-30000", "C2-8000"])
+@pytest.mark.parametrize("fmt", [f for f, _ in FORMATS], ids=[n for _, n in FORMATS])
+def test_persistent_equals_graph_fp32(spk, name, mk, T, fmt):
+    # fp32 mode is deterministic (exact sums, one rounding): the two ways of
+    # running the steps must agree bit for bit over a long active run
+    cfg = mk()
+    cfg["syn_format"] = fmt
+    runs = []
+    for step_mode in (1, 2):
+        c = dict(cfg, step_mode=step_mode)
+        g = spk.Net(c, max_steps=T, raster_capacity=cfg["n"] * T)
+        assert g.stats()["step_mode"] == step_mode
+        _say(f"[persist=graph] {name} T={T} mode={step_mode} format={fmt}")
+        g.step(T // 3)
+        g.step(T - T // 3)
+        runs.append((g.spike_counts(), g.raster()[1], g.delivered(), g.events(), g.state()))
+    (c1, r1, d1, e1, (v1, f1)), (c2, r2, d2, e2, (v2, f2)) = runs
+    assert c1.sum() > 0
+    assert np.array_equal(c1, c2) and np.array_equal(r1, r2), "rasters differ"
+    assert np.array_equal(d1, d2) and np.array_equal(e1, e2)
+    assert np.array_equal(v1.view(np.uint32), v2.view(np.uint32)) and np.array_equal(f1, f2)
+
+
+def test_step_mode_selection(spk):
+    # AUTO takes the persistent kernel where it applies; asking for it where
+    # it does not (direct delivery with several delays) is an error
+    g = spk.Net(I.scaled(4, 8000, k_out=300), max_steps=1)
+    assert g.stats()["step_mode"] == spk.SPK_STEP_PERSISTENT
+    g = spk.Net(I.scaled(4, 8000, k_out=300, step_mode=1), max_steps=1)
+    assert g.stats()["step_mode"] == spk.SPK_STEP_GRAPH
+    cfg = I.scaled(4, 8000, k_out=300, delivery=1)
+    assert spk.Net(cfg, max_steps=1).stats()["step_mode"] == spk.SPK_STEP_GRAPH
+    with pytest.raises(spk.SpkError) as e:
+        spk.Net(dict(cfg, step_mode=2), max_steps=1)
+    assert e.value.code == spk.SPK_EINVAL
