@@ -103,9 +103,11 @@ def step_source_sha():
     return h.hexdigest()[:16]
 
 
-def measured_traffic(config, acc, kernel):
-    """HBM bytes per launch from the committed counter summary, or None when
-    the summary is missing or the step kernels changed since it was taken."""
+def measured_traffic(config, acc, kernel, steps_per_launch):
+    """HBM bytes per launch from the committed counter summary (calibrated
+    FETCH_SIZE + WRITE_SIZE per step of the kernel, times the steps of one
+    launch), or None when the summary is missing or the step kernels changed
+    since it was taken."""
     path = os.path.join(ROOT, "profiles", f"traffic_c{config}_{acc}.json")
     try:
         with open(path) as f:
@@ -117,7 +119,7 @@ def measured_traffic(config, acc, kernel):
     k = d.get("kernels", {}).get(kernel)
     if not k:
         return None
-    return (k["fetch_kib"] * d["fetch_scale"] + k["write_kib"] * d["write_scale"]) * 1024.0
+    return k["hbm_bytes_per_step"] * steps_per_launch
 
 
 def cpu_baseline(cfg, seconds):
@@ -232,7 +234,8 @@ def main():
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
     b_evt, b_neu = algorithmic_bytes(cfg["n"], cfg["neuron_kind"], events, spikes, bpe, K)
     step_gbs = (b_evt + b_neu) / (ms * 1e-3) / 1e9
-    traffic = measured_traffic(args.config, args.acc, dom)
+    spl = nsteps / km["run_launches"] if persistent else 1
+    traffic = measured_traffic(args.config, args.acc, dom, spl)
     roofline = {
         "bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
         "frac": round(achieved / PEAK_HBM_GBS, 4),
@@ -243,7 +246,7 @@ def main():
         "events_only_frac": round(value / (PEAK_HBM_GBS * 1e9 / bpe), 4),
         "bytes_per_event": bpe,
         "per_launch_us": {k: round(v[0] * 1e3, 2) for k, v in kernels.items()},
-        "steps_per_launch": nsteps / km["run_launches"] if persistent else 1,
+        "steps_per_launch": spl,
     }
 
     rate_hz = spikes / (cfg["n"] * K * cfg["dt_ms"] * 1e-3)
