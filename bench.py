@@ -221,7 +221,8 @@ def main():
     if persistent:  # one launch runs all K steps: every byte of the step is its
         b_ev, b_neu = algorithmic_bytes(cfg["n"], cfg["neuron_kind"], d2, c2, bpe, nsteps)
         nl = km["run_launches"]
-        kernels = {"k_run": (km["run_ms"] / nl, (b_ev + b_neu) / nl)}
+        kname = "k_split" if st["persistent_split"] else "k_run"
+        kernels = {kname: (km["run_ms"] / nl, (b_ev + b_neu) / nl)}
     elif binned:  # push kernel reads the fired rows; tile kernel updates the neurons
         b_push, b_tile = algorithmic_bytes(cfg["n"], cfg["neuron_kind"], e2, c2, bpe, nsteps)
         kernels = {"k_push": (km["push_ms"] / nsteps, b_push / nsteps),
@@ -260,7 +261,8 @@ def main():
                                                        if cfg["ext_lambda"] and args.config != 2 else ""),
             "n_neurons": cfg["n"], "synapses": int(st["nnz"]), "dt_ms": cfg["dt_ms"],
             "delivery": "direct" if st["delivery"] == 1 else "binned",
-            "steps": "one persistent launch" if persistent else "HIP graphs of 32 steps",
+            "steps": ("one persistent launch" + (" (filing beside the updates)" if st["persistent_split"] else ""))
+                     if persistent else "HIP graphs of 32 steps",
             "synapse_bytes": bpe,
             "accumulation": "exact int64 fixed point, rounded once to fp32" if args.acc == "f32"
                             else f"int32 fixed point 2^-{cfg['fixed_shift']}",

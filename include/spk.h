@@ -120,7 +120,9 @@ enum { SPK_STEP_AUTO = 0, SPK_STEP_GRAPH = 1, SPK_STEP_PERSISTENT = 2 };
  *   row.
  * Tuning (environment, read at creation): SPK_TILES_PER_XCD caps the tiles
  *   per XCD group (1..256, default 32); SPK_PAGE_CAP sets the records per
- *   page of binned delivery (default: an equal share of 2 GiB). */
+ *   page of binned delivery (default: an equal share of 2 GiB);
+ *   SPK_PERSISTENT_SPLIT=0 / 1 forces the persistent kernel's variant (see
+ *   spk_stats_t.persistent_split; default: split iff delay_min >= 2). */
 typedef struct {
     uint32_t abi_version;      /* must be SPK_ABI_VERSION */
     uint32_t n;
@@ -161,6 +163,10 @@ typedef struct {
     uint32_t delivery;         /* SPK_DELIVERY_DIRECT or SPK_DELIVERY_BINNED as chosen */
     uint32_t page_cap;         /* binned delivery: records per page (beyond: global atomics) */
     uint32_t step_mode;        /* SPK_STEP_GRAPH or SPK_STEP_PERSISTENT as chosen */
+    uint32_t persistent_split; /* 1: the persistent kernel runs filing and updates side by
+                                  side, the events that arrive at the next step first (binned
+                                  delivery, 4-byte synapses or fixed-point accumulation);
+                                  chosen when the smallest delay is >= 2 steps */
 } spk_stats_t;
 
 typedef struct spk_net spk_net;

@@ -6,11 +6,13 @@
 // synapse = int2 {j << 24 | target, weight bits} (full format) or u32
 // {class << 30 | j << 24 | target} (compact format: at most four distinct
 // weights, looked up by class), j = delay - delay_min.
-// Every row is grouped by target tile (the paper keeps rows sorted by target,
+// Every row is grouped by target range (the paper keeps rows sorted by target,
 // Sec. III-A, so that each target range of a row is one contiguous run; only
-// the grouping matters for delivery, the order inside a tile does not).  The
-// tile boundaries of every row are written alongside: per-tile starts for
-// direct delivery, per-XCD-group ends for binned delivery.
+// the grouping matters for delivery, the order inside a range does not).
+// Direct delivery groups by target tile and writes per-tile starts.  Binned
+// delivery groups by XCD group and, inside each group's run, puts the
+// synapses of the smallest delay first; it writes per-group ends and the end
+// of each group's smallest-delay part (the events that arrive soonest).
 //
 // Build with -ffp-contract=off: weights are computed with explicitly rounded
 // fp32 operations.
@@ -93,8 +95,10 @@ __device__ uint32_t block_scan_u32(uint32_t x, uint32_t *ws, uint32_t *total)
 }
 
 // ------------------------------------------------------------ bucketing
-// Per-row counting sort by target tile in LDS: histogram, exclusive scan
-// (the tile starts), then every synapse goes to start[tile] + its rank.
+// Per-row counting sort in LDS: histogram, exclusive scan (the bucket
+// starts), then every synapse goes to start[bucket] + its rank.  Buckets:
+// target tiles (direct delivery) or (XCD group, smallest delay or not)
+// (binned delivery).
 
 struct RowLDS {
     uint32_t cur[kMaxTiles];
@@ -128,7 +132,7 @@ __device__ void scan_tiles(RowLDS &L, uint32_t T)
     __syncthreads();
 }
 
-// Tile boundaries of row s from the starts in L.cur (before placement).
+// Range boundaries of row s from the bucket starts in L.cur (before placement).
 __device__ void write_row_index(const ConnArgs &c, const RowIndex &ix, RowLDS &L, uint32_t s,
                                 uint64_t start, uint32_t len)
 {
@@ -139,17 +143,28 @@ __device__ void write_row_index(const ConnArgs &c, const RowIndex &ix, RowLDS &L
             to[k] = (uint16_t)(k < tl.T ? L.cur[k] : len);
     }
     if (ix.desc && threadIdx.x == 0) {
-        RowDesc d;
+        RowDesc d{};
         d.start = start;
-        for (uint32_t x = 0; x < kGroups; x++)
-            d.gend[x] = (uint16_t)(x + 1 < kGroups ? L.cur[(x + 1) * tl.T8] : len);
-        d.spare = 0;
+        for (uint32_t x = 0; x < kGroups; x++) {
+            d.gend[x] = (uint16_t)(x + 1 < kGroups ? L.cur[2 * (x + 1)] : len);
+            d.dend[x] = (uint16_t)L.cur[2 * x + 1];
+        }
         ix.desc[s] = d;
     }
     __syncthreads();
 }
 
-__device__ __forceinline__ uint32_t tile_of(const ConnArgs &c, uint32_t tgt) { return tgt >> c.tl.logW; }
+// Bucket of a synapse (target tgt, delay index j) in its row.
+__device__ __forceinline__ uint32_t bucket_of(const ConnArgs &c, const RowIndex &ix, uint32_t tgt, uint32_t j)
+{
+    const uint32_t tile = tgt >> c.tl.logW;
+    if (ix.desc) return 2 * (tile / c.tl.T8) + (j != 0 ? 1u : 0u);
+    return tile;
+}
+__device__ __forceinline__ uint32_t n_buckets(const ConnArgs &c, const RowIndex &ix)
+{
+    return ix.desc ? 2 * kGroups : c.tl.T;
+}
 
 // ----------------------------------------------- rows drawn per source
 // Bernoulli rows (one hash per ordered pair) and fixed out-degree rows
@@ -183,34 +198,40 @@ __global__ __launch_bounds__(kBlock) void k_gen_fill_rows(ConnArgs c, const uint
     const uint32_t s = blockIdx.x, tid = threadIdx.x;
     const uint64_t beg = row_ptr[s];
     const uint32_t len = (uint32_t)(row_ptr[s + 1] - beg);
-    zero_tiles(L, c.tl.T);
+    const uint32_t nb = n_buckets(c, ix);
+    zero_tiles(L, nb);
     const uint64_t rd = mix64(c.keys.delay ^ (uint64_t)s);
     const uint64_t rw = mix64(c.keys.w ^ (uint64_t)s);
     if (c.kind == SPK_CONN_BERNOULLI) {
         const uint64_t rk = mix64(c.keys.conn ^ (uint64_t)s);
-        for (uint32_t tgt = tid; tgt < c.n; tgt += kBlock)
-            if ((uint64_t)hash_hi32(mix64(rk ^ (uint64_t)tgt)) < c.conn_thr)
-                atomicAdd(&L.cur[tile_of(c, tgt)], 1u);
-        scan_tiles(L, c.tl.T);
+        for (uint32_t tgt = tid; tgt < c.n; tgt += kBlock) {
+            if (!((uint64_t)hash_hi32(mix64(rk ^ (uint64_t)tgt)) < c.conn_thr)) continue;
+            const uint32_t j = c.lists > 1 ? hash_range(mix64(rd ^ (uint64_t)tgt), c.lists) : 0;
+            atomicAdd(&L.cur[bucket_of(c, ix, tgt, j)], 1u);
+        }
+        scan_tiles(L, nb);
         write_row_index(c, ix, L, s, beg, len);
         for (uint32_t tgt = tid; tgt < c.n; tgt += kBlock) {
             if (!((uint64_t)hash_hi32(mix64(rk ^ (uint64_t)tgt)) < c.conn_thr)) continue;
             const uint32_t j = c.lists > 1 ? hash_range(mix64(rd ^ (uint64_t)tgt), c.lists) : 0;
             const float w = syn_weight(c, s, mix64(rw ^ (uint64_t)tgt));
-            const uint32_t pos = atomicAdd(&L.cur[tile_of(c, tgt)], 1u);
+            const uint32_t pos = atomicAdd(&L.cur[bucket_of(c, ix, tgt, j)], 1u);
             put_syn(c, syn, beg + pos, j, tgt, s, w);
         }
     } else {
         const uint64_t rt = mix64(c.keys.tgt ^ (uint64_t)s);
-        for (uint32_t q = tid; q < c.k_out; q += kBlock)
-            atomicAdd(&L.cur[tile_of(c, hash_range(mix64(rt ^ (uint64_t)q), c.n))], 1u);
-        scan_tiles(L, c.tl.T);
+        for (uint32_t q = tid; q < c.k_out; q += kBlock) {
+            const uint32_t tgt = hash_range(mix64(rt ^ (uint64_t)q), c.n);
+            const uint32_t j = c.lists > 1 ? hash_range(mix64(rd ^ (uint64_t)q), c.lists) : 0;
+            atomicAdd(&L.cur[bucket_of(c, ix, tgt, j)], 1u);
+        }
+        scan_tiles(L, nb);
         write_row_index(c, ix, L, s, beg, len);
         for (uint32_t q = tid; q < c.k_out; q += kBlock) {
             const uint32_t tgt = hash_range(mix64(rt ^ (uint64_t)q), c.n);
             const uint32_t j = c.lists > 1 ? hash_range(mix64(rd ^ (uint64_t)q), c.lists) : 0;
             const float w = syn_weight(c, s, mix64(rw ^ (uint64_t)q));
-            const uint32_t pos = atomicAdd(&L.cur[tile_of(c, tgt)], 1u);
+            const uint32_t pos = atomicAdd(&L.cur[bucket_of(c, ix, tgt, j)], 1u);
             put_syn(c, syn, beg + pos, j, tgt, s, w);
         }
     }
@@ -266,8 +287,8 @@ __global__ __launch_bounds__(kBlock) void k_csr_fill(ConnArgs c, uint64_t nnz, c
     }
 }
 
-// Group the synapses of every row of src by target tile into dst (same
-// row_ptr) and write the row's tile boundaries.  Blocks stride over rows.
+// Group the synapses of every row of src by bucket into dst (same row_ptr)
+// and write the row's range boundaries.  Blocks stride over rows.
 template <class R>
 __global__ __launch_bounds__(kBlock) void k_bucket_rows(ConnArgs c, const uint64_t *row_ptr,
                                                        const R *src, R *dst, RowIndex ix)
@@ -276,14 +297,18 @@ __global__ __launch_bounds__(kBlock) void k_bucket_rows(ConnArgs c, const uint64
     for (uint32_t s = blockIdx.x; s < c.n; s += gridDim.x) {
         const uint64_t beg = row_ptr[s];
         const uint32_t len = (uint32_t)(row_ptr[s + 1] - beg);
-        zero_tiles(L, c.tl.T);
-        for (uint32_t e = threadIdx.x; e < len; e += kBlock)
-            atomicAdd(&L.cur[tile_of(c, rec_target(rec_key(src[beg + e])))], 1u);
-        scan_tiles(L, c.tl.T);
+        const uint32_t nb = n_buckets(c, ix);
+        zero_tiles(L, nb);
+        for (uint32_t e = threadIdx.x; e < len; e += kBlock) {
+            const uint32_t key = rec_key(src[beg + e]);
+            atomicAdd(&L.cur[bucket_of(c, ix, rec_target(key), rec_delay(key))], 1u);
+        }
+        scan_tiles(L, nb);
         write_row_index(c, ix, L, s, beg, len);
         for (uint32_t e = threadIdx.x; e < len; e += kBlock) {
             const R r = src[beg + e];
-            const uint32_t pos = atomicAdd(&L.cur[tile_of(c, rec_target(rec_key(r)))], 1u);
+            const uint32_t key = rec_key(r);
+            const uint32_t pos = atomicAdd(&L.cur[bucket_of(c, ix, rec_target(key), rec_delay(key))], 1u);
             dst[beg + pos] = r;
         }
         __syncthreads();

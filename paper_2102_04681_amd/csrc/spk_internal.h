@@ -95,13 +95,15 @@ struct Tiling {
 
 // Where the runs of one source row start, per XCD group (binned delivery):
 // group x owns [start + (x ? gend[x-1] : 0), start + gend[x]); gend[7] is the
-// row length.
-struct RowDesc {
+// row length.  Inside group x's run the synapses of the smallest delay come
+// first, up to start + dend[x].  One cache line per row.
+struct alignas(64) RowDesc {
     uint64_t start;
     uint16_t gend[kGroups];
-    uint64_t spare;
+    uint16_t dend[kGroups];
+    uint64_t spare[3];
 };
-static_assert(sizeof(RowDesc) == 32, "one row descriptor is 32 bytes");
+static_assert(sizeof(RowDesc) == 64, "one row descriptor is 64 bytes");
 
 // Connectivity generation parameters.
 struct ConnArgs {
@@ -205,6 +207,8 @@ struct RunCtl {
     uint32_t ticket[kGroups * kCtlStride];  // workgroups placed on each XCD
     uint32_t gx[kGroups * kCtlStride];      // grid barrier: arrivals per XCD
     uint32_t lx[kGroups * kCtlStride];      // XCD barrier: arrivals per XCD
+    uint32_t critp[kGroups * kRunMaxR];     // split kernel: critical phases finished, per push block
+    uint32_t bulkp[kGroups * kRunMaxR];     // split kernel: bulk phases finished, per push block
     uint32_t start, pad0[kCtlStride - 1];   // placement barrier
     uint32_t gcnt, pad1[kCtlStride - 1];    // grid barrier: XCDs complete
     uint32_t gen, pad2[kCtlStride - 1];     // grid barrier: released epoch
@@ -215,7 +219,13 @@ struct RunArgs {
     RunCtl *ctl;
     uint64_t t0, n_steps;   // steps [t0, t0 + n_steps)
     uint32_t R;             // workgroups per XCD
+    // split kernel: critical pages (events of delay 1), one per (XCD group,
+    // push block, tile of the group), page_cap records each, and their fills
+    uint16_t *cpages16;
+    int2 *cpages;
+    uint32_t *cfill;
 };
+constexpr uint32_t kSplitMaxBuckets = 1024;  // split kernel: (delay, tile) buckets and (slot, tile) pages
 
 // spk_gen.hip -- connectivity expansion
 hipError_t gen_count_rows(const ConnArgs &c, uint32_t *cnt, hipStream_t s);
@@ -261,5 +271,10 @@ uint32_t push_blocks_per_group();
 // spk_run.hip -- the persistent step kernel (all steps of a call in one launch)
 bool run_supported(const StepArgs &a, uint32_t R);
 hipError_t launch_run(const RunArgs &ra, hipStream_t s);
+
+// spk_split.hip -- the persistent kernel that files each step's delay-1
+// events before the rest (binned delivery)
+bool split_supported(const StepArgs &a, uint32_t R);
+hipError_t launch_split(const RunArgs &ra, hipStream_t s);
 
 }  // namespace spk

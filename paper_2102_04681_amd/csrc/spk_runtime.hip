@@ -180,10 +180,13 @@ struct spk_net {
     uint64_t device_bytes = 0;
     std::vector<void *> allocs;
     std::map<uint32_t, hipGraphExec_t> graphs;
-    // persistent step kernel
-    bool persistent = false;
+    // persistent step kernel; split: the variant that files delay-1 events first
+    bool persistent = false, split = false;
     uint32_t run_R = 0;
     RunCtl *ctl = nullptr;
+    uint16_t *cpages16 = nullptr;
+    int2 *cpages = nullptr;
+    uint32_t *cfill = nullptr;
     // profiling
     bool profiling = false;
     std::vector<hipEvent_t> ev_free;
@@ -491,6 +494,17 @@ spk_status finish_counts(spk_net *net, const uint32_t *cnt)
 // its run of each due row (rows long compared with the tile count, one
 // delay, offsets small next to the synapses).  Binned: the push kernel sorts
 // each fired row's events by (arrival step, tile) into pages.
+// Whether the split persistent kernel's layout limits hold for binned
+// delivery of this network (the device check comes later).
+bool split_layout_fits(const spk_net *net)
+{
+    const Tiling &tl = net->tl;
+    const int cus = cu_count();
+    const uint32_t R = cus > 0 && cus % (int)kGroups == 0 ? (uint32_t)(cus / (int)kGroups) : 0u;
+    return R && tl.T8 <= R && R <= kRunMaxR && (net->compact || net->P.acc_mode == SPK_ACC_FIXED) &&
+           (uint64_t)net->lists * tl.T8 <= kSplitMaxBuckets && (uint64_t)net->dmax * tl.T8 <= kSplitMaxBuckets;
+}
+
 spk_status choose_delivery(spk_net *net, RowIndex *ix)
 {
     if (net->max_row > kMaxRow)
@@ -501,6 +515,11 @@ spk_status choose_delivery(spk_net *net, RowIndex *ix)
     const double toff_bytes = (double)net->n * (tl.T + 1) * 2.0;
     const bool binned_ok = (uint64_t)net->lists * tl.T8 <= kMaxBuckets;
     bool direct = net->lists == 1 && mean_row >= 2.0 * tl.T && toff_bytes <= 0.5 * 8.0 * (double)net->nnz;
+    // With a smallest delay of two steps or more, no event filed at t is
+    // needed at t + 1: binned delivery lets the persistent kernel file them
+    // beside the updates (split kernel), which beats reading the due rows
+    // at arrival.
+    if (direct && net->dmin >= 2 && net->P.step_mode != SPK_STEP_GRAPH && split_layout_fits(net)) direct = false;
     if (!binned_ok || net->P.delivery == SPK_DELIVERY_DIRECT) direct = true;
     if (net->P.delivery == SPK_DELIVERY_BINNED) {
         if (!binned_ok)
@@ -560,10 +579,10 @@ spk_status finish_rows(spk_net *net)
 
     // Spike lists: direct delivery reads the lists of steps t - dmax .. t - dmin
     // while writing that of t; binned delivery consumes the list of t within t,
-    // but in the persistent kernel one XCD may publish t + 1 while another
-    // still reads t, so there are two.
+    // but in the persistent kernels one XCD may publish t + 1 (split kernel:
+    // t + 2) while another still reads t, so there are three.
     const Tiling &tl = net->tl;
-    net->spk_slots = net->direct ? net->dmax + 1 : 2;
+    net->spk_slots = net->direct ? net->dmax + 1 : 3;
     if (!net->direct) {
         // Pages: (group, push block, arrival slot, tile).  A page never holds
         // more than nnz records (each synapse arrives at most once per slot),
@@ -585,6 +604,12 @@ spk_status finish_rows(spk_net *net)
         if (net->compact) SPK_TRY(dalloc(net, &net->pages16, n_pages * cap));
         else SPK_TRY(dalloc(net, &net->pages, n_pages * cap));
         SPK_TRY(dalloc(net, &net->pfill, n_pages));
+        // critical pages of the split persistent kernel: (group, push block, tile)
+        const uint64_t n_cpages = (uint64_t)kGroups * net->pg1 * tl.T8;
+        if (net->compact) SPK_TRY(dalloc(net, &net->cpages16, n_cpages * cap));
+        else SPK_TRY(dalloc(net, &net->cpages, n_cpages * cap));
+        SPK_TRY(dalloc(net, &net->cfill, n_cpages));
+        SPK_HIP(hipMemsetAsync(net->cfill, 0, n_cpages * 4, s));
         SPK_TRY(dalloc(net, &net->ovf_flag, (size_t)net->pslots * tl.T));
         SPK_TRY(dalloc(net, (uint64_t **)&net->acc_ovf, acc_elems));
         SPK_HIP(hipMemsetAsync(net->pfill, 0, n_pages * 4, s));
@@ -695,7 +720,37 @@ RunArgs run_args(const spk_net *net, uint64_t t0, uint64_t n_steps)
     ra.t0 = t0;
     ra.n_steps = n_steps;
     ra.R = net->run_R;
+    ra.cpages16 = net->cpages16;
+    ra.cpages = net->cpages;
+    ra.cfill = net->cfill;
     return ra;
+}
+
+hipError_t launch_persistent(const spk_net *net, const RunArgs &ra, hipStream_t s)
+{
+    return net->split ? launch_split(ra, s) : launch_run(ra, s);
+}
+
+// A zero-step launch of the persistent kernel: checks that the workgroups
+// were placed evenly over the XCDs (it only loads and stores back state).
+spk_status probe_persistent(spk_net *net, bool *ok)
+{
+    hipStream_t s = net->stream;
+    *ok = false;
+    SPK_HIP(hipMemsetAsync(net->ctl, 0, sizeof(RunCtl), s));
+    hipError_t e = launch_persistent(net, run_args(net, net->t, 0), s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    uint32_t abort_flag = 1;
+    if (e == hipSuccess) e = hipMemcpy(&abort_flag, &net->ctl->abort_flag, 4, hipMemcpyDeviceToHost);
+    if (e == hipSuccess && abort_flag == 0) {
+        *ok = true;
+        return SPK_OK;
+    }
+    (void)hipGetLastError();
+    (void)hipStreamSynchronize(s);
+    SPK_HIP(hipMemsetAsync(net->flags, 0, 4, s));  // the probe's stop flag
+    SPK_HIP(hipStreamSynchronize(s));
+    return SPK_OK;
 }
 
 // Step mode.  The persistent kernel needs a cooperative launch of one
@@ -711,33 +766,39 @@ spk_status choose_step_mode(spk_net *net)
     const int cus = cu_count();
     net->run_R = cus > 0 && cus % (int)kGroups == 0 ? (uint32_t)(cus / (int)kGroups) : 0u;
     const StepArgs a = step_args(net);
-    const bool fits = coop && run_supported(a, net->run_R);
-    if (!fits) {
+    // The split kernel runs filing and updates side by side on half the waves
+    // each: it wins when nothing filed at t is needed at t + 1 (smallest delay
+    // >= 2); with delay-1 events the unsplit kernel is faster on MI355X.
+    // SPK_PERSISTENT_SPLIT=0 / 1 forces the choice (a tuning knob).
+    bool want_split = net->dmin >= 2;
+    if (const char *e = std::getenv("SPK_PERSISTENT_SPLIT")) want_split = std::strcmp(e, "0") != 0;
+    const bool split_fits = coop && want_split && split_supported(a, net->run_R);
+    const bool run_fits = coop && run_supported(a, net->run_R);
+    if (!split_fits && !run_fits) {
         if (mode == SPK_STEP_PERSISTENT)
             return fail(SPK_EINVAL, "the persistent step kernel does not apply to this network or device "
                                     "(tiles per XCD, delays, or cooperative launch)");
         return SPK_OK;
     }
-    hipStream_t s = net->stream;
     SPK_TRY(dalloc(net, &net->ctl, 1));
-    SPK_HIP(hipMemsetAsync(net->ctl, 0, sizeof(RunCtl), s));
-    hipError_t e = launch_run(run_args(net, net->t, 0), s);
-    if (e == hipSuccess) e = hipStreamSynchronize(s);
-    uint32_t abort_flag = 1;
-    if (e == hipSuccess) e = hipMemcpy(&abort_flag, &net->ctl->abort_flag, 4, hipMemcpyDeviceToHost);
-    if (e == hipSuccess && abort_flag == 0) {
+    bool ok = false;
+    if (split_fits) {
+        net->split = true;
+        SPK_TRY(probe_persistent(net, &ok));
+    }
+    if (!ok && run_fits) {
+        net->split = false;
+        SPK_TRY(probe_persistent(net, &ok));
+    }
+    if (ok) {
         net->persistent = true;
         return SPK_OK;
     }
-    (void)hipGetLastError();
-    (void)hipStreamSynchronize(s);
-    SPK_HIP(hipMemsetAsync(net->flags, 0, 4, s));  // the probe's stop flag
-    SPK_HIP(hipStreamSynchronize(s));
+    net->split = false;
     dfree(net, net->ctl);
     net->ctl = nullptr;
     if (mode == SPK_STEP_PERSISTENT)
-        return fail(SPK_EHIP, std::string("the persistent step kernel could not be placed: ") +
-                                  (e != hipSuccess ? hipGetErrorString(e) : "uneven workgroup placement"));
+        return fail(SPK_EHIP, "the persistent step kernel could not be placed evenly over the XCDs");
     return SPK_OK;
 }
 
@@ -1057,7 +1118,7 @@ spk_status spk_step(spk_net *net, uint64_t n_steps)
             }
             SPK_HIP(hipMemsetAsync(net->ctl, 0, sizeof(RunCtl), s));
             if (e0) SPK_HIP(hipEventRecord(e0, s));
-            SPK_HIP(launch_run(run_args(net, net->t, B), s));
+            SPK_HIP(launch_persistent(net, run_args(net, net->t, B), s));
             if (e1) {
                 SPK_HIP(hipEventRecord(e1, s));
                 net->ev_run.push_back({e0, e1});
@@ -1328,6 +1389,7 @@ spk_status spk_stats(spk_net *net, spk_stats_t *out)
     st.delivery = net->direct ? SPK_DELIVERY_DIRECT : SPK_DELIVERY_BINNED;
     st.page_cap = net->page_cap;
     st.step_mode = net->persistent ? SPK_STEP_PERSISTENT : SPK_STEP_GRAPH;
+    st.persistent_split = net->split ? 1u : 0u;
     *out = st;
     return SPK_OK;
 }

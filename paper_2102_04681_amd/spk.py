@@ -63,7 +63,7 @@ class spk_stats_t(C.Structure):
         ("delay_lists", C.c_uint32), ("max_row", C.c_uint32), ("pois_len", C.c_uint32),
         ("fixed_shift", C.c_int32), ("k", C.c_float), ("bytes_per_synapse", C.c_double),
         ("tile_width", C.c_uint32), ("tiles", C.c_uint32), ("delivery", C.c_uint32),
-        ("page_cap", C.c_uint32), ("step_mode", C.c_uint32),
+        ("page_cap", C.c_uint32), ("step_mode", C.c_uint32), ("persistent_split", C.c_uint32),
     ]
 
 

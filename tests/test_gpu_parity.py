@@ -249,8 +249,11 @@ RUN_CASES = [
 
 
 # how the steps run: graph replay, plain launches with events (profiling),
-# the persistent kernel, and the persistent kernel with events around it
-MODES = [("graph", 1, False), ("launch", 1, True), ("persist", 2, False), ("persist-prof", 2, True)]
+# the persistent kernel (binned delivery: the split variant that files delay-1
+# events first), the same with events around it, and the unsplit persistent
+# kernel (SPK_PERSISTENT_SPLIT=0)
+MODES = [("graph", 1, False, "auto"), ("launch", 1, True, "auto"), ("persist", 2, False, "auto"),
+         ("persist-prof", 2, True, "auto"), ("persist-split", 2, False, "1"), ("persist-unsplit", 2, False, "0")]
 
 
 def _persistent_applies(cfg, delivery):
@@ -261,9 +264,10 @@ def _persistent_applies(cfg, delivery):
 
 @pytest.mark.parametrize("name,mk,T", RUN_CASES, ids=[c[0] for c in RUN_CASES])
 @pytest.mark.parametrize("delivery", [1, 2], ids=["direct", "binned"])
-@pytest.mark.parametrize("mode,step_mode,profiled", MODES, ids=[m[0] for m in MODES])
+@pytest.mark.parametrize("mode,step_mode,profiled,split", MODES, ids=[m[0] for m in MODES])
 @pytest.mark.parametrize("fmt", [f for f, _ in FORMATS], ids=[n for _, n in FORMATS])
-def test_fixed_point_simulation_bit_identical(spk, name, mk, T, delivery, mode, step_mode, profiled, fmt):
+def test_fixed_point_simulation_bit_identical(spk, name, mk, T, delivery, mode, step_mode, profiled, split, fmt,
+                                              monkeypatch):
     cfg = mk()
     cfg["acc_mode"] = I.ACC_FIXED
     cfg["delivery"] = delivery
@@ -273,9 +277,16 @@ def test_fixed_point_simulation_bit_identical(spk, name, mk, T, delivery, mode, 
         pytest.skip("profiled paths checked on two shapes")
     if step_mode == 2 and not _persistent_applies(cfg, delivery):
         pytest.skip("the persistent kernel takes direct delivery with one delay only")
+    if split != "auto" and delivery == 1:
+        pytest.skip("direct delivery has no split variant")
+    if split != "auto":
+        monkeypatch.setenv("SPK_PERSISTENT_SPLIT", split)
     _say(f"[run] {name} n={cfg['n']} T={T} delivery={delivery} mode={mode} format={fmt}")
     g = spk.Net(cfg, max_steps=T, raster_capacity=cfg["n"] * T)
-    assert g.stats()["step_mode"] == step_mode
+    st = g.stats()
+    assert st["step_mode"] == step_mode
+    want_split = step_mode == 2 and delivery == 2 and (split == "1" or (split == "auto" and cfg["delay_min"] >= 2))
+    assert st["persistent_split"] == (1 if want_split else 0)
     g.set_profiling(profiled)
     g.step(T)
     offs, ids = g.raster()
@@ -310,13 +321,14 @@ def test_fixed_point_simulation_bit_identical(spk, name, mk, T, delivery, mode, 
 
 @pytest.mark.parametrize("acc", [I.ACC_F32, I.ACC_FIXED], ids=["f32", "fixed"])
 @pytest.mark.parametrize("fmt", [f for f, _ in FORMATS], ids=[n for _, n in FORMATS])
-@pytest.mark.parametrize("step_mode", [1, 2], ids=["graph", "persist"])
-def test_bin_overflow_fallback(spk, acc, fmt, step_mode, monkeypatch):
+@pytest.mark.parametrize("step_mode,split", [(1, "1"), (2, "1"), (2, "0")], ids=["graph", "persist", "unsplit"])
+def test_bin_overflow_fallback(spk, acc, fmt, step_mode, split, monkeypatch):
     # 64 neurons, 200 synapses each (multapses), all above threshold at t=0:
     # the one tile receives 12 800 events at step 1, ~400 per push block,
     # while every page is capped at 64 records, so the global-atomic
     # fallback must deliver the rest (in the simulation and in debug_deliver).
     monkeypatch.setenv("SPK_PAGE_CAP", "64")
+    monkeypatch.setenv("SPK_PERSISTENT_SPLIT", split)
     cfg = I.config(4, n=64, k_out=200, delay_min=1, delay_max=1, v0_lo=-49.0, v0_hi=-49.0,
                    t_ref_ms=0.0, acc_mode=acc, delivery=2, syn_format=fmt, step_mode=step_mode)
     T = 6
@@ -337,8 +349,9 @@ def test_bin_overflow_fallback(spk, acc, fmt, step_mode, monkeypatch):
         assert np.all(np.abs(got - want) <= ulp)
 
 
-@pytest.mark.parametrize("step_mode", [1, 2], ids=["graph", "persist"])
-def test_resume_matches_single_run(spk, step_mode):
+@pytest.mark.parametrize("step_mode,split", [(1, "1"), (2, "1"), (2, "0")], ids=["graph", "persist", "unsplit"])
+def test_resume_matches_single_run(spk, step_mode, split, monkeypatch):
+    monkeypatch.setenv("SPK_PERSISTENT_SPLIT", split)
     cfg = I.scaled(4, 5000, k_out=500, acc_mode=I.ACC_FIXED, step_mode=step_mode)
     a = spk.Net(cfg, max_steps=120, raster_capacity=5000 * 120)
     b = spk.Net(cfg, max_steps=120, raster_capacity=5000 * 120)
@@ -346,8 +359,14 @@ def test_resume_matches_single_run(spk, step_mode):
     a.step(70)
     for _ in range(120):
         b.step(1)
-    assert np.array_equal(a.raster()[1], b.raster()[1])
-    assert np.array_equal(a.state()[0].view(np.uint32), b.state()[0].view(np.uint32))
+    # events filed near a launch boundary arrive up to 20 steps later: both
+    # must equal the oracle's single run, raster and state
+    r, ov, orf, _ = _oracle_run(cfg, 120)
+    assert r["counts"].sum() > 0
+    for g in (a, b):
+        assert np.array_equal(g.raster()[1], r["raster"]), "raster differs from the oracle"
+        assert np.array_equal(g.state()[0].view(np.uint32), ov.view(np.uint32))
+        assert np.array_equal(g.state()[1], orf)
     assert np.array_equal(a.delivered(), b.delivered())
 
 
@@ -491,32 +510,54 @@ def test_explicit_adjacency_formats(spk, n_w, fmt):
     ("C2-8000", lambda: I.scaled(2, 8000, k_in_exc=640, k_in_inh=160), 800),
 ], ids=["C4-20000", "C1-8000", "C3-30000", "C2-8000"])
 @pytest.mark.parametrize("fmt", [f for f, _ in FORMATS], ids=[n for _, n in FORMATS])
-def test_persistent_equals_graph_fp32(spk, name, mk, T, fmt):
-    # fp32 mode is deterministic (exact sums, one rounding): the two ways of
+@pytest.mark.parametrize("delivery", [0, 2], ids=["auto", "binned"])
+def test_persistent_equals_graph_fp32(spk, name, mk, T, fmt, delivery, monkeypatch):
+    # fp32 mode is deterministic (exact sums, one rounding): every way of
     # running the steps must agree bit for bit over a long active run
     cfg = mk()
     cfg["syn_format"] = fmt
+    cfg["delivery"] = delivery
     runs = []
-    for step_mode in (1, 2):
+    for step_mode, split in ((1, True), (2, True), (2, False)):
+        monkeypatch.setenv("SPK_PERSISTENT_SPLIT", "1" if split else "0")
+        if step_mode == 1:
+            monkeypatch.delenv("SPK_PERSISTENT_SPLIT")
         c = dict(cfg, step_mode=step_mode)
         g = spk.Net(c, max_steps=T, raster_capacity=cfg["n"] * T)
-        assert g.stats()["step_mode"] == step_mode
-        _say(f"[persist=graph] {name} T={T} mode={step_mode} format={fmt}")
+        st = g.stats()
+        assert st["step_mode"] == step_mode
+        _say(f"[persist=graph] {name} T={T} mode={step_mode} split={st['persistent_split']} format={fmt}")
         g.step(T // 3)
         g.step(T - T // 3)
         runs.append((g.spike_counts(), g.raster()[1], g.delivered(), g.events(), g.state()))
-    (c1, r1, d1, e1, (v1, f1)), (c2, r2, d2, e2, (v2, f2)) = runs
+    c1, r1, d1, e1, (v1, f1) = runs[0]
     assert c1.sum() > 0
-    assert np.array_equal(c1, c2) and np.array_equal(r1, r2), "rasters differ"
-    assert np.array_equal(d1, d2) and np.array_equal(e1, e2)
-    assert np.array_equal(v1.view(np.uint32), v2.view(np.uint32)) and np.array_equal(f1, f2)
+    for c2, r2, d2, e2, (v2, f2) in runs[1:]:
+        assert np.array_equal(c1, c2) and np.array_equal(r1, r2), "rasters differ"
+        assert np.array_equal(d1, d2) and np.array_equal(e1, e2)
+        assert np.array_equal(v1.view(np.uint32), v2.view(np.uint32)) and np.array_equal(f1, f2)
 
 
-def test_step_mode_selection(spk):
+def test_step_mode_selection(spk, monkeypatch):
     # AUTO takes the persistent kernel where it applies; asking for it where
     # it does not (direct delivery with several delays) is an error
-    g = spk.Net(I.scaled(4, 8000, k_out=300), max_steps=1)
-    assert g.stats()["step_mode"] == spk.SPK_STEP_PERSISTENT
+    # delay-1 events: the unsplit kernel
+    st = spk.Net(I.scaled(4, 8000, k_out=300), max_steps=1).stats()
+    assert st["step_mode"] == spk.SPK_STEP_PERSISTENT and st["persistent_split"] == 0
+    # smallest delay 15: binned delivery and the split kernel
+    st = spk.Net(I.scaled(2, 8000, k_in_exc=640, k_in_inh=160), max_steps=1).stats()
+    assert st["step_mode"] == spk.SPK_STEP_PERSISTENT and st["persistent_split"] == 1
+    assert st["delivery"] == spk.SPK_DELIVERY_BINNED
+    # ... but direct delivery when steps run as graphs
+    st = spk.Net(I.scaled(2, 8000, k_in_exc=640, k_in_inh=160, step_mode=1), max_steps=1).stats()
+    assert st["delivery"] == spk.SPK_DELIVERY_DIRECT
+    # fp32 sums with 8-byte synapses: the unsplit kernel even when asked (LDS)
+    monkeypatch.setenv("SPK_PERSISTENT_SPLIT", "1")
+    st = spk.Net(I.scaled(4, 8000, k_out=300, syn_format=1), max_steps=1).stats()
+    assert st["step_mode"] == spk.SPK_STEP_PERSISTENT and st["persistent_split"] == 0
+    st = spk.Net(I.scaled(4, 8000, k_out=300), max_steps=1).stats()
+    assert st["persistent_split"] == 1
+    monkeypatch.delenv("SPK_PERSISTENT_SPLIT")
     g = spk.Net(I.scaled(4, 8000, k_out=300, step_mode=1), max_steps=1)
     assert g.stats()["step_mode"] == spk.SPK_STEP_GRAPH
     cfg = I.scaled(4, 8000, k_out=300, delivery=1)
