@@ -61,6 +61,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target duration of the timed oracle sample")
+    ap.add_argument("--setup", action="store_true",
+                    help="setup-time study instead of the step benchmark: create Synth networks "
+                         "(density 5%%) of growing size and C2/C4, print one JSON line")
     ap.add_argument("--probe-copy", type=int, default=0, metavar="BYTES",
                     help="only run the library's copy kernel on BYTES (counter calibration)")
     return ap.parse_args()
@@ -149,8 +152,51 @@ def cpu_baseline(cfg, seconds):
     desc = (f"oracle step loop (single thread), {steps} steps of the same workload at n={n} "
             f"(fan-in, fan-out, weights, delays and drive unchanged), network build and the "
             f"first 200 steps excluded")
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), model)
+    except OSError:
+        pass
     return {"value": events / dt, "unit": "events/s", "cores": 1, "kind": "oracle",
-            "sample": desc, "steps": steps, "seconds": round(dt, 2)}
+            "sample": desc, "steps": steps, "seconds": round(dt, 2),
+            "wall_per_bio_time": round(dt / (steps * cfg["dt_ms"] * 1e-3), 2),
+            "cpu_model": model, "host_cpus": os.cpu_count()}
+
+
+SETUP_SYNTH_N = (10_000, 20_000, 50_000, 100_000, 200_000, 300_000)
+
+
+def setup_study(stream, seed):
+    """Setup time as a function of network size (Sec. IV-C): Synth networks of
+    density 5 % and the C2 and C4 networks, created on the GPU.  Reports the
+    wall time of the creating call and the GPU time of the generation
+    kernels (rows counted, drawn, grouped) and of the accumulator-range pass."""
+    import torch
+    import inputs as I
+    from paper_2102_04681_amd import spk
+    cases = [(f"synth n={n:,}", I.synth(n, 0.05, seed=seed)) for n in SETUP_SYNTH_N]
+    cases += [("C2", I.config(2, driven=True, seed=seed)), ("C4", I.config(4, driven=True, seed=seed))]
+    points = []
+    for name, cfg in cases:
+        net = spk.Net(cfg, stream=stream, max_steps=1)
+        st = net.stats()
+        nnz = int(st["nnz"])
+        points.append({"network": name, "n": cfg["n"], "synapses": nnz,
+                       "setup_ms": round(st["setup_ms"], 2), "gen_ms": round(st["gen_ms"], 3),
+                       "range_ms": round(st["range_ms"], 3),
+                       "gen_synapses_per_ms": round(nnz / st["gen_ms"]) if st["gen_ms"] > 0 else None,
+                       "setup_synapses_per_ms": round(nnz / st["setup_ms"]) if st["setup_ms"] > 0 else None})
+        print(f"[setup] {name}: {nnz:,} synapses, create {st['setup_ms']:.1f} ms, generation kernels "
+              f"{st['gen_ms']:.2f} ms, range pass {st['range_ms']:.2f} ms", file=sys.stderr, flush=True)
+        del net
+        torch.cuda.synchronize()
+    synth = [p_ for p_ in points if p_["network"].startswith("synth")]
+    best = max(synth, key=lambda p_: p_["synapses"])
+    return {"metric": "setup: synapses generated per ms (GPU generation kernels), Synth density 5%",
+            "value": best["gen_synapses_per_ms"], "unit": "synapses/ms", "n_gpus": 1,
+            "higher_is_better": True, "data": "synthetic", "seed": seed,
+            "config": {"workload": f"Synth density 5%, n={best['n']:,}"}, "points": points}
 
 
 def main():
@@ -168,6 +214,10 @@ def main():
     torch.cuda.set_device(0)
     stream = torch.cuda.Stream()
     torch.cuda.set_stream(stream)
+
+    if args.setup:
+        print(json.dumps(setup_study(stream, args.seed)))
+        return
 
     if args.probe_copy:
         cfg = workload(args)
@@ -230,6 +280,10 @@ def main():
     else:         # tile kernel does both
         b_ev, b_neu = algorithmic_bytes(cfg["n"], cfg["neuron_kind"], d2, c2, bpe, nsteps)
         kernels = {"k_tile": (km["tile_ms"] / nsteps, (b_ev + b_neu) / nsteps)}
+    # measured copy bandwidth of this device (the library's streaming copy
+    # kernel, 1 GiB read + 1 GiB written per repetition), for a second ratio
+    probe_ms = net.hbm_copy(1 << 30, reps=10)
+    probe_gbs = 2 * (1 << 30) * 10 / (probe_ms * 1e-3) / 1e9
     dom = max(kernels, key=lambda k: kernels[k][0])
     dom_ms, dom_bytes = kernels[dom]
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
@@ -248,6 +302,7 @@ def main():
         "bytes_per_event": bpe,
         "per_launch_us": {k: round(v[0] * 1e3, 2) for k, v in kernels.items()},
         "steps_per_launch": spl,
+        "probe_GBs": round(probe_gbs, 1), "frac_vs_probe": round(achieved / probe_gbs, 4),
     }
 
     rate_hz = spikes / (cfg["n"] * K * cfg["dt_ms"] * 1e-3)
@@ -270,6 +325,7 @@ def main():
             "seed": args.seed, "parallelism": "1 GPU",
         },
         "roofline": roofline,
+        "wall_per_bio_time": round(ms_step / cfg["dt_ms"], 4),
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, args.cpu_seconds)

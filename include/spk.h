@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define SPK_ABI_VERSION 3u
+#define SPK_ABI_VERSION 4u
 #define SPK_MAX_DELAY_LISTS 64u  /* delay_max - delay_min + 1 must not exceed this */
 
 typedef enum {
@@ -122,7 +122,9 @@ enum { SPK_STEP_AUTO = 0, SPK_STEP_GRAPH = 1, SPK_STEP_PERSISTENT = 2 };
  *   per XCD group (1..256, default 32); SPK_PAGE_CAP sets the records per
  *   page of binned delivery (default: an equal share of 2 GiB);
  *   SPK_PERSISTENT_SPLIT=0 / 1 forces the persistent kernel's variant (see
- *   spk_stats_t.persistent_split; default: split iff delay_min >= 2). */
+ *   spk_stats_t.persistent_split; default: split only when the smallest
+ *   delay is >= 2 and steps cannot be batched); SPK_BATCH_STEPS caps the
+ *   steps per batch (spk_stats_t.batch_steps). */
 typedef struct {
     uint32_t abi_version;      /* must be SPK_ABI_VERSION */
     uint32_t n;
@@ -167,6 +169,16 @@ typedef struct {
                                   side, the events that arrive at the next step first (binned
                                   delivery, 4-byte synapses or fixed-point accumulation);
                                   chosen when the smallest delay is >= 2 steps */
+    uint32_t batch_steps;      /* persistent kernel, binned delivery, unsplit: steps run as
+                                  one batch (tile phases back to back, then one filing pass);
+                                  up to the smallest delay (at most 16), 1 otherwise */
+    /* Setup timing (Sec. IV-C): host wall time of the creating call, GPU time
+     * (HIP events on the network's stream) of the connectivity generation
+     * kernels (row counts, fill and regrouping; excludes allocation), and of the
+     * accumulator-range pass (largest sum of |weights| into one neuron).
+     * gen_ms is zero for networks made by spk_create_from_csr (rows are
+     * uploaded and grouped there, not generated). */
+    double setup_ms, gen_ms, range_ms;
 } spk_stats_t;
 
 typedef struct spk_net spk_net;

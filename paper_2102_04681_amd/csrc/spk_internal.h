@@ -201,6 +201,7 @@ struct StepArgs {
 constexpr uint32_t kCtlStride = 32;
 constexpr uint32_t kRunMaxR = 32;          // workgroups per XCD (one per compute unit)
 constexpr uint32_t kRunMaxFill = 2048;     // pages per push block: arrival slots x tiles of a group
+constexpr uint32_t kRunMaxD = 16;          // steps per batch of the unsplit kernel (binned delivery)
 constexpr uint32_t kRunAbortTimeout = 1u;  // a barrier wait gave up
 constexpr uint32_t kRunAbortPlacement = 2u;  // workgroups not spread R per XCD: nothing was run
 struct RunCtl {
@@ -219,6 +220,7 @@ struct RunArgs {
     RunCtl *ctl;
     uint64_t t0, n_steps;   // steps [t0, t0 + n_steps)
     uint32_t R;             // workgroups per XCD
+    uint32_t D;             // unsplit kernel, binned delivery: steps per batch (1 .. min(d_min, kRunMaxD))
     // split kernel: critical pages (events of delay 1), one per (XCD group,
     // push block, tile of the group), page_cap records each, and their fills
     uint16_t *cpages16;
@@ -270,6 +272,7 @@ uint32_t push_blocks_per_group();
 
 // spk_run.hip -- the persistent step kernel (all steps of a call in one launch)
 bool run_supported(const StepArgs &a, uint32_t R);
+bool run_batch_supported(const StepArgs &a, uint32_t D);  // steps per batch D is valid for this network
 hipError_t launch_run(const RunArgs &ra, hipStream_t s);
 
 // spk_split.hip -- the persistent kernel that files each step's delay-1

@@ -81,10 +81,16 @@ struct RunLDS {
             uint32_t clen[kRunThreads / kWave * 16];
             uint32_t wpre[kRunThreads / kWave][kWave + 1];
             uint64_t wbeg[kRunThreads / kWave][kWave];
+            unsigned long long dlv[kRunMaxD];  // binned: events delivered at each step of the batch
+            uint32_t ovfm;                     // binned: bit u: step u of the batch has overflowed events
         } t;
         struct {
             Rec stage[kStageN];
-            uint32_t pre[kRunMaxT + 1];
+            uint32_t pre[kRunMaxT * kRunMaxD + 1];  // spikes before segment (step of the batch, tile)
+            uint32_t uslot[kRunMaxD];               // spike-list slot of each step of the batch
+            unsigned long long emit[kRunMaxD];      // events emitted per step of the batch
+            unsigned long long rbu[kRunMaxD];       // raster position of spike k of step u: rbu[u] + k
+            uint32_t rokm;                          // bit u: the spikes of step u fit in the raster
             uint32_t cpre[kRunChunk + 1];
             uint32_t plen[kRunChunk];
             uint64_t pbase[kRunChunk];
@@ -97,6 +103,7 @@ struct RunLDS {
     } u;
     uint32_t ws[16], ws2[16];
     unsigned long long ws64[16];
+    uint32_t mstep[kRunMaxD];   // spikes of each step of the last pushed batch
     uint32_t nspk, x, r, stop;
 };
 
@@ -169,26 +176,41 @@ __device__ bool xcd_sync(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x, u
     return L.stop == 0;
 }
 
-// Tile phase, binned delivery: sum the records of the arrival step's pages
-// (one per push block of the group) into LDS.  Returns the events delivered
-// (including any that overflowed into the global accumulators).
+// Tile phase, binned delivery: sum the records of the pages of the Db
+// arrival steps t_first .. t_first + Db - 1 (one page per push block of the
+// group and step) into the LDS accumulators, those of step u at
+// acc[u * W ...].  A table of 64-record chunks of all the pages is built per
+// window of kDrain chunks per wave; every wave loads its chunks at once.
+// The caller has zeroed acc[0 .. Db * W).  Leaves in L.u.t.dlv the events
+// delivered at each step, including any that overflowed into the global
+// accumulators (merged here).
 template <bool FIXED, bool CMP>
-__device__ uint64_t run_drain(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t x, uint32_t c, uint32_t tile,
-                              uint32_t tile_n, uint64_t t)
+__device__ void run_drain(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t x, uint32_t c, uint32_t tile,
+                          uint32_t tile_n, uint64_t t_first, uint32_t Db)
 {
     const uint32_t tid = threadIdx.x;
     const Tiling tl = a.tl;
-    const uint32_t pslot = (uint32_t)(t % a.pslots);
     constexpr uint32_t kPer = CMP ? 2u : 1u;
     constexpr uint32_t kChunk = kPer * kWave;
-    const uint32_t cap = a.page_cap, G1 = a.pg1;
-    uint32_t pf = a.pfill[page_of(a, x, tid < G1 ? tid : 0u, pslot, c)];
-    const uint32_t ovf = ld_ag(&a.ovf_flag[(uint64_t)pslot * tl.T + tile]);
-    pf = tid < G1 ? pf : 0u;
+    const uint32_t cap = a.page_cap, G1 = a.pg1, P = Db * G1;
+    const uint32_t pslot0 = (uint32_t)(t_first % a.pslots);  // Db <= pslots: one wrap at most
+    // thread p < P: page p = u * G1 + g, push block g's page of arrival step t_first + u
+    const uint32_t pu = tid < P ? tid / G1 : 0u, pg = tid < P ? tid - pu * G1 : 0u;
+    const uint32_t psl = pslot0 + pu < a.pslots ? pslot0 + pu : pslot0 + pu - a.pslots;
+    const uint32_t page = page_of(a, x, pg, psl, c);
+    uint32_t pf = a.pfill[page];
+    // thread u < Db: the overflow flag of (arrival step t_first + u, tile)
+    const uint32_t osl = tid < Db ? (pslot0 + tid < a.pslots ? pslot0 + tid : pslot0 + tid - a.pslots) : 0u;
+    uint32_t ovf = ld_ag(&a.ovf_flag[(uint64_t)osl * tl.T + tile]);
+    ovf = tid < Db ? ovf : 0u;
+    if (tid < Db) L.u.t.dlv[tid] = 0;
+    if (tid == 0) L.u.t.ovfm = 0;
+    pf = tid < P ? pf : 0u;
     const uint32_t ne = pf < cap ? pf : cap;
     uint32_t C;
-    const uint32_t cex = block_scan_u32((ne + kChunk - 1) / kChunk, L.ws, &C);
-    const uint64_t delivered = block_sum_u64(pf, L.ws64);
+    const uint32_t cex = block_scan_u32((ne + kChunk - 1) / kChunk, L.ws, &C);  // (publishes the resets)
+    if (pf) atomicAdd(&L.u.t.dlv[pu], (unsigned long long)pf);
+    if (ovf) atomicOr(&L.u.t.ovfm, 1u << tid);
     // the wave index is uniform: held in a scalar register, the chunk-table
     // addresses below cost no vector registers
     const uint32_t w = __builtin_amdgcn_readfirstlane(tid / kWave), lane = lane_id();
@@ -196,16 +218,17 @@ __device__ uint64_t run_drain(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t
     constexpr int kDrain = 16;
     constexpr uint32_t kWin = kDrain * nw;
     const uint32_t nchp = (ne + kChunk - 1) / kChunk;
+    const uint32_t W = tl.W;
     for (uint32_t i0 = 0; i0 < C; i0 += kWin) {
         for (uint32_t q = tid; q < kWin; q += kRunThreads) L.u.t.clen[q] = 0;
         lds_sync();
-        if (tid < G1) {
+        if (tid < P) {
             const uint32_t cb = cex > i0 ? cex : i0, ce = cex + nchp < i0 + kWin ? cex + nchp : i0 + kWin;
-            const uint32_t pbase = page_of(a, x, tid, pslot, c) * cap;
+            const uint32_t pbase = page * cap;
             for (uint32_t q = cb; q < ce; q++) {
                 const uint32_t o = (q - cex) * kChunk;
                 L.u.t.cbase[q - i0] = (pbase + o) / kPer;
-                L.u.t.clen[q - i0] = ne - o < kChunk ? ne - o : kChunk;
+                L.u.t.clen[q - i0] = (ne - o < kChunk ? ne - o : kChunk) | (pu << 8);
             }
         }
         lds_sync();
@@ -216,7 +239,7 @@ __device__ uint64_t run_drain(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t
 #pragma unroll
             for (int u = 0; u < kDrain; u++) {
                 const uint32_t cw = u * nw + w;
-                const uint32_t len = L.u.t.clen[cw], cb = L.u.t.cbase[cw];
+                const uint32_t len = L.u.t.clen[cw] & 0xffu, cb = L.u.t.cbase[cw];
                 const bool ok = 2 * lane < len;
                 const uint32_t idx = ok ? cb + lane : 0u;
                 okm |= ((uint32_t)ok | (uint32_t)(2 * lane + 1 < len) << 1) << (2 * u);
@@ -224,11 +247,12 @@ __device__ uint64_t run_drain(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t
             }
 #pragma unroll
             for (int u = 0; u < kDrain; u++) {
+                const uint32_t ao = (L.u.t.clen[u * nw + w] >> 8) * W;
 #pragma unroll
                 for (int hf = 0; hf < 2; hf++) {
                     if (!((okm >> (2 * u + hf)) & 1u)) continue;
                     const uint32_t rec = hf ? rr[u] >> 16 : rr[u] & 0xffffu;
-                    Acc<FIXED>::add(&L.u.t.acc[rec & kPageLocalMask], class_units(a, rec >> kPageClassShift));
+                    Acc<FIXED>::add(&L.u.t.acc[ao + (rec & kPageLocalMask)], class_units(a, rec >> kPageClassShift));
                 }
             }
         } else {
@@ -237,7 +261,7 @@ __device__ uint64_t run_drain(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t
 #pragma unroll
             for (int u = 0; u < kDrain; u++) {
                 const uint32_t cw = u * nw + w;
-                const uint32_t len = L.u.t.clen[cw], cb = L.u.t.cbase[cw];
+                const uint32_t len = L.u.t.clen[cw] & 0xffu, cb = L.u.t.cbase[cw];
                 const bool ok = lane < len;
                 const uint32_t idx = ok ? cb + lane : 0u;
                 okm |= (uint32_t)ok << u;
@@ -245,37 +269,44 @@ __device__ uint64_t run_drain(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t
             }
 #pragma unroll
             for (int u = 0; u < kDrain; u++)
-                if ((okm >> u) & 1u)
-                    Acc<FIXED>::add(&L.u.t.acc[(uint32_t)rr[u].x], units_of<FIXED>(rr[u].y, a.m.shift64));
+                if ((okm >> u) & 1u) {
+                    const uint32_t ao = (L.u.t.clen[u * nw + w] >> 8) * W;
+                    Acc<FIXED>::add(&L.u.t.acc[ao + (uint32_t)rr[u].x], units_of<FIXED>(rr[u].y, a.m.shift64));
+                }
         }
         lds_sync();
     }
-    if (ovf) {  // events that did not fit their page, accumulated by global atomics
-        const uint64_t st = (uint64_t)pslot * tl.T + tile;
-        for (uint32_t q = tid; q < tile_n; q += kRunThreads) {
-            const uint64_t gi = st * tl.W + q;
-            if (FIXED) {
-                int32_t *o = (int32_t *)a.acc_ovf + gi;
-                L.u.t.acc[q] += (int32_t)ld_ag((const uint32_t *)o);
-                st_ag((uint32_t *)o, 0u);
-            } else {
-                unsigned long long *o = (unsigned long long *)a.acc_ovf + gi;
-                L.u.t.acc[q] += __hip_atomic_load(o, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                __hip_atomic_store(o, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    lds_sync();  // the counts and flags above are complete (also when there was no chunk)
+    const uint32_t om = L.u.t.ovfm;
+    if (om) {  // events that did not fit their page, accumulated by global atomics
+        for (uint32_t u = 0; u < Db; u++) {
+            if (!((om >> u) & 1u)) continue;
+            const uint32_t sl = pslot0 + u < a.pslots ? pslot0 + u : pslot0 + u - a.pslots;
+            const uint64_t st = (uint64_t)sl * tl.T + tile;
+            for (uint32_t q = tid; q < tile_n; q += kRunThreads) {
+                const uint64_t gi = st * tl.W + q;
+                if (FIXED) {
+                    int32_t *o = (int32_t *)a.acc_ovf + gi;
+                    L.u.t.acc[u * W + q] += (int32_t)ld_ag((const uint32_t *)o);
+                    st_ag((uint32_t *)o, 0u);
+                } else {
+                    unsigned long long *o = (unsigned long long *)a.acc_ovf + gi;
+                    L.u.t.acc[u * W + q] += __hip_atomic_load(o, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    __hip_atomic_store(o, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
             }
+            if (tid == 0) st_ag(&a.ovf_flag[st], 0u);
         }
-        if (tid == 0) st_ag(&a.ovf_flag[st], 0u);
     }
-    lds_sync();
-    return delivered;
 }
 
 // Tile phase: the update of the tile's neurons from the LDS accumulators, the
-// state and the draws in LDS; spikes compacted by wavefront ballots into the
-// LDS list, then published to the tile's segment of the spike list of t.
+// state and the draws in LDS (input: the accumulators from acc[aoff] on);
+// spikes compacted by wavefront ballots into the LDS list, then published to
+// the tile's segment of the spike list of t.
 template <bool FIXED, bool CMP, bool DIRECT>
 __device__ void run_update(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x, uint32_t tile,
-                           uint32_t tile_lo, uint32_t tile_n, uint64_t t, uint64_t delivered)
+                           uint32_t tile_lo, uint32_t tile_n, uint64_t t, uint64_t delivered, uint32_t aoff)
 {
     const StepArgs &a = ra.s;
     const ModelArgs &m = a.m;
@@ -289,10 +320,10 @@ __device__ void run_update(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x,
             const uint32_t K = m.pois_len ? L.kp[q] : 0u;
             float I;
             if (FIXED) {
-                const int32_t qt = (int32_t)L.u.t.acc[q] + (int32_t)K * m.ext_wq + m.bias_q;
+                const int32_t qt = (int32_t)L.u.t.acc[aoff + q] + (int32_t)K * m.ext_wq + m.bias_q;
                 I = ldexpf((float)qt, -m.shift);
             } else {
-                const float isyn = fixed64_to_float(L.u.t.acc[q], m.shift64);
+                const float isyn = fixed64_to_float(L.u.t.acc[aoff + q], m.shift64);
                 const float ext = __fmul_rn((float)K, m.ext_w);
                 I = __fadd_rn(__fadd_rn(isyn, ext), m.i_bias);
             }
@@ -352,15 +383,74 @@ __device__ void run_update(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x,
     }
 }
 
-// Push phase (binned delivery): push block (x, r) takes the r-th equal share
-// of the spikes of t, reads the runs of their rows that target group x and
-// appends the events to its own pages: bucket b = j * T8 + c (delay index j,
-// tile c of the group), page (arrival slot (t + dmin + j) mod pslots, c).
-// Also appends its share of the spike IDs to the raster (group 0).  Returns
-// the step's spike count (every push block sees the whole list).
+// Spike counts of the Db steps t_first .. t_first + Db - 1 as one list in
+// (step, tile) order: pre[u * T + tile] = spikes before segment (u, tile),
+// pre[Db * T] = all of them; uslot[u] = the spike-list slot of step u.
 template <bool FIXED, bool CMP>
-__device__ uint32_t run_push(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x, uint32_t r, uint64_t t,
-                             uint64_t rbase)
+__device__ uint32_t load_spike_batch(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint64_t t_first, uint32_t Db)
+{
+    const uint32_t T = a.tl.T, W = a.tl.W, NS = Db * T;
+    constexpr uint32_t kPerMax = kRunMaxT * kRunMaxD / kRunThreads;  // segments per thread, at most
+    const uint32_t per = (NS + kRunThreads - 1) / kRunThreads;
+    const uint32_t b0 = threadIdx.x * per;
+    const uint32_t slot0 = (uint32_t)(t_first % a.spk_slots);  // Db <= spk_slots / 2: one wrap at most
+    uint32_t c[kPerMax], sum = 0;
+#pragma unroll
+    for (uint32_t k = 0; k < kPerMax; k++) {  // unconditional loads from clamped indices
+        const uint32_t seg = b0 + k < NS && k < per ? b0 + k : 0u;
+        const uint32_t u = seg / T, tile = seg - u * T;
+        const uint32_t slot = slot0 + u < a.spk_slots ? slot0 + u : slot0 + u - a.spk_slots;
+        const uint32_t v = ld_u32<true>(a.spk_cnt + (uint64_t)slot * T + tile);
+        c[k] = b0 + k < NS && k < per ? (v < W ? v : W) : 0u;
+        sum += c[k];
+    }
+    if (threadIdx.x < Db) {
+        const uint32_t u = threadIdx.x;
+        L.u.p.uslot[u] = slot0 + u < a.spk_slots ? slot0 + u : slot0 + u - a.spk_slots;
+    }
+    uint32_t tot;
+    uint32_t ex = block_scan_u32(sum, L.ws, &tot);
+#pragma unroll
+    for (uint32_t k = 0; k < kPerMax; k++)
+        if (k < per && b0 + k < NS) {
+            L.u.p.pre[b0 + k] = ex;
+            ex += c[k];
+        }
+    if (threadIdx.x == 0) L.u.p.pre[NS] = tot;
+    lds_sync();
+    return tot;
+}
+
+// k-th spike of the batch (k < total): its neuron, and in *u the step of the
+// batch it belongs to.
+template <bool FIXED, bool CMP>
+__device__ __forceinline__ uint32_t spike_at_batch(const StepArgs &a, const RunLDS<FIXED, CMP> &L, uint32_t NS,
+                                                   uint32_t k, uint32_t *u)
+{
+    const uint32_t *pre = L.u.p.pre;
+    uint32_t lo = 0, hi = NS - 1;
+    while (lo < hi) {
+        const uint32_t mid = (lo + hi + 1) >> 1;
+        if (pre[mid] <= k) lo = mid; else hi = mid - 1;
+    }
+    const uint32_t T = a.tl.T, uu = lo / T, tile = lo - uu * T;
+    *u = uu;
+    return ld_u32<true>(a.spk_ids + ((uint64_t)L.u.p.uslot[uu] * T + tile) * a.tl.W + (k - pre[lo]));
+}
+
+// Push phase (binned delivery): push block (x, r) takes the r-th equal share
+// of the spikes of the Db steps t_first .. t_first + Db - 1 (Db = 1 unless
+// the smallest delay allows batches: every event of these spikes arrives
+// after the batch), reads the runs of their rows that target group x and
+// appends the events to its own pages: bucket b = a_off * T8 + c with the
+// arrival offset a_off = (step of the batch) + (delay index j) and c the tile
+// of the group; page (arrival slot (t_first + dmin + a_off) mod pslots, c).
+// Also appends its share of the spike IDs to the raster (group 0).  Returns
+// the batch's spike count (every push block sees the whole list) and, for
+// batches of several steps, leaves each step's count in L.mstep.
+template <bool FIXED, bool CMP>
+__device__ uint32_t run_push(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x, uint32_t r, uint64_t t_first,
+                             uint32_t Db, uint64_t rbase)
 {
     using Rec = typename SynRec<CMP>::T;
     using LT = RunLDS<FIXED, CMP>;
@@ -369,32 +459,52 @@ __device__ uint32_t run_push(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t 
     const uint32_t tid = threadIdx.x, lane = lane_id(), w = __builtin_amdgcn_readfirstlane(tid / kWave);
     constexpr uint32_t nw = kRunThreads / kWave;
     const Tiling tl = a.tl;
-    const uint32_t NB = a.lists * tl.T8, G1 = ra.R;
-    const uint32_t sslot = (uint32_t)(t % a.spk_slots);
-    const uint32_t s0 = (uint32_t)(t % a.pslots);
-    // the pages of arrival slot t were drained at t: they restart empty
-    for (uint32_t c = tid; c < tl.T8; c += kRunThreads) L.fill[s0 * tl.T8 + c] = 0;
+    const uint32_t NB = (Db + a.lists - 1) * tl.T8, G1 = ra.R, NS = Db * tl.T;
+    // the pages of the batch's arrival slots were drained in the batch: they restart empty
+    for (uint32_t q = tid; q < Db * tl.T8; q += kRunThreads) {
+        const uint32_t u = q / tl.T8, c = q - u * tl.T8;
+        L.fill[(uint32_t)((t_first + u) % a.pslots) * tl.T8 + c] = 0;
+    }
     for (uint32_t b = tid; b < NB; b += kRunThreads) L.u.p.bcnt[b] = 0;
-    const uint32_t M = load_spike_set<true>(a, sslot, L.u.p.pre, L.ws);
+    if (tid < Db) L.u.p.emit[tid] = 0;
+    const uint32_t M = load_spike_batch(a, L, t_first, Db);  // (its barriers publish the resets)
+    if (Db > 1) {
+        if (tid == 0) {  // each step's count, and where its spikes go in the raster (if they fit)
+            uint64_t rb = rbase;
+            uint32_t okm = 0;
+            for (uint32_t u = 0; u < Db; u++) {
+                const uint32_t Mu = L.u.p.pre[(u + 1) * tl.T] - L.u.p.pre[u * tl.T];
+                const bool ok = a.raster_cap && rb + Mu <= a.raster_cap;
+                L.u.p.rbu[u] = rb - L.u.p.pre[u * tl.T];  // (mod 2^64)
+                okm |= (uint32_t)ok << u;
+                rb = ok ? rb + Mu : rb;
+                L.mstep[u] = Mu;
+            }
+            L.u.p.rokm = okm;
+        }
+        lds_sync();
+    }
+    // one step: its spikes go to the raster from rbase on, if they fit
+    const bool one_fits = a.raster_cap && rbase + M <= a.raster_cap;
     const uint32_t k0 = (uint32_t)((uint64_t)M * r / G1), k1 = (uint32_t)((uint64_t)M * (r + 1) / G1);
-    const bool rec_raster = a.raster_cap && x == 0 && rbase + M <= a.raster_cap;
+    const bool rec_raster = a.raster_cap && x == 0;
     const uint32_t xlo = x * tl.Gw;
     const uint64_t cap = a.page_cap;
-    const uint32_t slot_of_j0 = (uint32_t)((t + a.dmin) % a.pslots);
-    uint64_t emitted = 0;
+    const uint32_t slot_of_a0 = (uint32_t)((t_first + a.dmin) % a.pslots);
     for (uint32_t c0 = k0; c0 < k1; c0 += kRunChunk) {
         const uint32_t K = k1 - c0 < kRunChunk ? k1 - c0 : kRunChunk;
-        uint32_t len = 0;
+        uint32_t len = 0, uo = 0;
         uint64_t base = 0;
         if (tid < K) {
             const uint32_t k = c0 + tid;
-            const uint32_t s = spike_at<true>(a, L.u.p.pre, sslot, k);
-            if (rec_raster) a.raster[rbase + k] = s;
+            const uint32_t s = spike_at_batch(a, L, NS, k, &uo);
+            if (rec_raster && (Db == 1 ? one_fits : ((L.u.p.rokm >> uo) & 1u) != 0))
+                a.raster[(Db == 1 ? rbase : L.u.p.rbu[uo]) + k] = s;
             const RowDesc *d = a.desc + s;
             const uint32_t lo = x ? d->gend[x - 1] : 0u, hi = d->gend[x];
             len = hi - lo;
             base = d->start + lo;
-            emitted += d->gend[kGroups - 1];
+            if (x == 0) atomicAdd(&L.u.p.emit[uo], (unsigned long long)d->gend[kGroups - 1]);
         }
         uint32_t C;
         const uint32_t nch = (len + kWave - 1) / kWave;
@@ -414,20 +524,23 @@ __device__ uint32_t run_push(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t 
                 for (uint32_t q = cb; q < ce; q++) {
                     const uint32_t o = (q - coff) * kWave;
                     L.u.p.cbase[q - i0] = base + o;
-                    L.u.p.clen[q - i0] = len - o < kWave ? len - o : kWave;
+                    L.u.p.clen[q - i0] = (len - o < kWave ? len - o : kWave) | (uo << 8);
                 }
             }
             lds_sync();
             Rec rec[R];
             uint32_t okm = 0;
+            uint64_t uom = 0;  // step of the batch of each chunk, 4 bits each
 #pragma unroll
             for (int u = 0; u < R; u++) {
                 const uint32_t cl = u * nw + w;
-                const uint32_t len = L.u.p.clen[cl];
+                const uint32_t lw = L.u.p.clen[cl];
+                const uint32_t len = lw & 0xffu;
                 const uint64_t cb = L.u.p.cbase[cl];
                 const bool ok = lane < len;
                 const uint64_t idx = ok ? cb + lane : 0ull;
                 okm |= (uint32_t)ok << u;
+                uom |= (uint64_t)(lw >> 8) << (4 * u);
                 rec[u] = SynRec<CMP>::load(a, idx);  // unconditional load from a clamped index
             }
 #pragma unroll
@@ -441,9 +554,9 @@ __device__ uint32_t run_push(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t 
                     tr[rr] = 0xffffffffu;
                     if (!((okm >> q) & 1u)) continue;
                     const uint32_t key = rec_key(rec[q]);
-                    const uint32_t j = rec_delay(key);
+                    const uint32_t ao = rec_delay(key) + (uint32_t)((uom >> (4 * q)) & 0xfu);
                     const uint32_t local = rec_target(key) - xlo;
-                    const uint32_t b = j * tl.T8 + (local >> tl.logW);
+                    const uint32_t b = ao * tl.T8 + (local >> tl.logW);
                     const uint32_t rank = atomicAdd(&L.u.p.bcnt[b], 1u);
                     tr[rr] = (b << 16) | rank;
                     const uint32_t sv = (b << 16) | (local & (tl.W - 1));
@@ -462,8 +575,8 @@ __device__ uint32_t run_push(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t 
                     for (uint32_t k = 0; k < P; k++) {
                         if (b0 + k < NB) {
                             const uint32_t bb = b0 + k, cnt = L.u.p.bcnt[bb];
-                            const uint32_t j = bb / tl.T8, cc = bb - j * tl.T8;
-                            uint32_t sl = slot_of_j0 + j;
+                            const uint32_t ao = bb / tl.T8, cc = bb - ao * tl.T8;
+                            uint32_t sl = slot_of_a0 + ao;
                             sl = sl >= a.pslots ? sl - a.pslots : sl;
                             uint32_t &f = L.fill[sl * tl.T8 + cc];
                             L.u.p.bst[bb] = ex;
@@ -487,8 +600,8 @@ __device__ uint32_t run_push(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t 
                     const uint32_t key = rec_key(r2);
                     const uint32_t b = key >> 16, low = key & 0xffffu;
                     const uint32_t pos = L.u.p.wb[b] + q;
-                    const uint32_t j = b / tl.T8, cc = b - j * tl.T8;
-                    uint32_t sl = slot_of_j0 + j;
+                    const uint32_t ao = b / tl.T8, cc = b - ao * tl.T8;
+                    uint32_t sl = slot_of_a0 + ao;
                     sl = sl >= a.pslots ? sl - a.pslots : sl;
                     if (pos < cap) {
                         const uint64_t e = (uint64_t)page_of(a, x, r, sl, cc) * cap + pos;
@@ -518,10 +631,9 @@ __device__ uint32_t run_push(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t 
         const uint32_t sl = f / tl.T8;
         a.pfill[page_of(a, x, r, sl, f - sl * tl.T8)] = L.fill[f];
     }
-    if (x == 0) {  // events emitted at t, counted once per spike
-        const uint64_t tot = block_sum_u64(emitted, L.ws64);
-        if (tid == 0 && tot) atomicAdd((unsigned long long *)&a.events8[t * kGroups], (unsigned long long)tot);
-    }
+    // events emitted at each step of the batch, counted once per spike (group 0)
+    if (x == 0 && tid < Db && L.u.p.emit[tid])
+        atomicAdd((unsigned long long *)&a.events8[(t_first + tid) * kGroups], L.u.p.emit[tid]);
     return M;
 }
 
@@ -619,20 +731,38 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
     uint32_t eg = 0, ex = 0;
     __syncthreads();
 
-    for (uint64_t s = 0; s < ra.n_steps; s++) {
-        const uint64_t t = ra.t0 + s;
-        const bool more = s + 1 < ra.n_steps;
+    // Steps run in batches of D (binned delivery with a smallest delay >= D;
+    // D = 1 otherwise): the tile phases of the batch back to back, then one
+    // push phase for all of the batch's spikes.  Every event that arrives
+    // within a batch comes from a spike before it, so it has been filed.
+    const uint32_t D = DIRECT ? 1u : ra.D;
+    uint64_t s = 0;
+    while (s < ra.n_steps) {
+        const uint32_t Db = (uint32_t)(ra.n_steps - s < D ? ra.n_steps - s : D);
+        const uint64_t t_first = ra.t0 + s;
+        s += Db;
+        const bool more = s < ra.n_steps;
         if (has_tile) {
             // the push phase reused this LDS: accumulators restart at zero, and
             // the spike count of the previous step has been read by every thread
-            for (uint32_t q = tid; q < tl.W; q += kRunThreads) L.u.t.acc[q] = 0;
+            for (uint32_t q = tid; q < Db * tl.W; q += kRunThreads) L.u.t.acc[q] = 0;
             if (tid == 0) L.nspk = 0;
-            const uint64_t delivered = DIRECT ? run_gather(a, L, tile, tile_lo, t)
-                                              : run_drain(a, L, x, r, tile, tile_n, t);
-            run_update<FIXED, CMP, DIRECT>(ra, L, x, tile, tile_lo, tile_n, t, delivered);
+            if (!DIRECT) run_drain(a, L, x, r, tile, tile_n, t_first, Db);  // all steps of the batch
+            for (uint32_t u = 0; u < Db; u++) {
+                const uint64_t t = t_first + u;
+                if (u) {  // the draws of t; the spike list of t - 1 has been read by every thread
+                    run_draws(a, L, tile_lo, tile_n, t);
+                    __syncthreads();
+                    if (tid == 0) L.nspk = 0;
+                    __syncthreads();
+                }
+                const uint64_t delivered = DIRECT ? run_gather(a, L, tile, tile_lo, t) : L.u.t.dlv[u];
+                run_update<FIXED, CMP, DIRECT>(ra, L, x, tile, tile_lo, tile_n, t, delivered, u * tl.W);
+            }
         }
-        if (!grid_sync(ra, L, x, ++eg, has_tile && more, tile_lo, tile_n, t + 1)) return;
+        if (!grid_sync(ra, L, x, ++eg, has_tile && more, tile_lo, tile_n, t_first + Db)) return;
         if (DIRECT) {
+            const uint64_t t = t_first;
             if (a.raster_cap) {  // the spike list of t is complete: workgroup (0, 0) records it
                 const bool writer = x == 0 && r == 0;
                 const uint32_t M = load_spike_set<true>(a, (uint32_t)(t % a.spk_slots), L.u.p.pre, L.ws);
@@ -643,8 +773,10 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
                 __syncthreads();  // pre[] is the tile's scratch again
             }
         } else {
-            const uint32_t M = run_push(ra, L, x, r, t, rbase);
-            if (a.raster_cap) rbase = raster_advance(a, t, rbase, M, x == 0 && r == 0);
+            const uint32_t M = run_push(ra, L, x, r, t_first, Db, rbase);
+            if (a.raster_cap)
+                for (uint32_t u = 0; u < Db; u++)
+                    rbase = raster_advance(a, t_first + u, rbase, Db == 1 ? M : L.mstep[u], x == 0 && r == 0);
             if (!xcd_sync(ra, L, x, ++ex)) return;
         }
     }
@@ -677,9 +809,17 @@ bool run_supported(const StepArgs &a, uint32_t R)
            a.page_cap % 16 == 0 && tl.W <= 65536;
 }
 
+bool run_batch_supported(const StepArgs &a, uint32_t D)
+{
+    if (a.direct) return D == 1;
+    return D >= 1 && D <= kRunMaxD && D <= a.dmin && a.spk_slots >= 2 * D && a.tl.T <= kRunMaxT &&
+           (D + a.lists - 1) * a.tl.T8 <= kMaxBuckets && D + a.lists - 1 <= a.pslots &&
+           D * a.tl.W <= kMaxTileW && D * a.pg1 <= kRunThreads;
+}
+
 hipError_t launch_run(const RunArgs &ra, hipStream_t s)
 {
-    if (!run_supported(ra.s, ra.R)) return hipErrorInvalidValue;
+    if (!run_supported(ra.s, ra.R) || !run_batch_supported(ra.s, ra.D)) return hipErrorInvalidValue;
     const StepArgs &a = ra.s;
     if (a.compact ? !a.syn32 || (!a.direct && !a.pages16) : !a.syn || (!a.direct && !a.pages))
         return hipErrorInvalidValue;

@@ -15,6 +15,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <chrono>
 #include <cmath>
 #include <cstdio>
 #include <cstdlib>
@@ -183,6 +184,7 @@ struct spk_net {
     // persistent step kernel; split: the variant that files delay-1 events first
     bool persistent = false, split = false;
     uint32_t run_R = 0;
+    uint32_t run_D = 1;  // unsplit persistent kernel, binned delivery: steps per batch
     RunCtl *ctl = nullptr;
     uint16_t *cpages16 = nullptr;
     int2 *cpages = nullptr;
@@ -193,9 +195,40 @@ struct spk_net {
     std::vector<std::pair<hipEvent_t, hipEvent_t>> ev_push, ev_tile, ev_run;
     double ms_push = 0, ms_tile = 0, ms_run = 0;
     uint64_t launches = 0, run_launches = 0;
+    // setup timing
+    double setup_ms = 0, gen_ms = 0, range_ms = 0;
 };
 
 namespace {
+
+// GPU time of the work enqueued on a stream between start() and stop(),
+// added to *acc by stop() (which waits for the work).
+struct SegTimer {
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    SegTimer() = default;
+    SegTimer(const SegTimer &) = delete;
+    SegTimer &operator=(const SegTimer &) = delete;
+    ~SegTimer()
+    {
+        if (e0) (void)hipEventDestroy(e0);
+        if (e1) (void)hipEventDestroy(e1);
+    }
+    hipError_t start(hipStream_t s)
+    {
+        hipError_t e = e0 ? hipSuccess : hipEventCreate(&e0);
+        if (e == hipSuccess && !e1) e = hipEventCreate(&e1);
+        return e == hipSuccess ? hipEventRecord(e0, s) : e;
+    }
+    hipError_t stop(hipStream_t s, double *acc)
+    {
+        hipError_t e = hipEventRecord(e1, s);
+        if (e == hipSuccess) e = hipEventSynchronize(e1);
+        float t = 0.f;
+        if (e == hipSuccess) e = hipEventElapsedTime(&t, e0, e1);
+        if (e == hipSuccess) *acc += t;
+        return e;
+    }
+};
 
 template <class T>
 spk_status dalloc(spk_net *net, T **p, size_t count)
@@ -477,7 +510,10 @@ spk_status finish_counts(spk_net *net, const uint32_t *cnt)
     SPK_TRY(dalloc(net, &bsum, scan_scratch_elems(n) + 1));
     SPK_TRY(dalloc(net, &maxp, 1));
     SPK_HIP(hipMemsetAsync(maxp, 0, 4, s));
+    SegTimer tm;
+    SPK_HIP(tm.start(s));
     SPK_HIP(scan_counts(cnt, n, net->row_ptr, bsum, maxp, s));
+    SPK_HIP(tm.stop(s, &net->gen_ms));
     uint64_t nnz = 0;
     uint32_t mr = 0;
     SPK_HIP(hipMemcpyAsync(&nnz, net->row_ptr + n, 8, hipMemcpyDeviceToHost, s));
@@ -494,17 +530,6 @@ spk_status finish_counts(spk_net *net, const uint32_t *cnt)
 // its run of each due row (rows long compared with the tile count, one
 // delay, offsets small next to the synapses).  Binned: the push kernel sorts
 // each fired row's events by (arrival step, tile) into pages.
-// Whether the split persistent kernel's layout limits hold for binned
-// delivery of this network (the device check comes later).
-bool split_layout_fits(const spk_net *net)
-{
-    const Tiling &tl = net->tl;
-    const int cus = cu_count();
-    const uint32_t R = cus > 0 && cus % (int)kGroups == 0 ? (uint32_t)(cus / (int)kGroups) : 0u;
-    return R && tl.T8 <= R && R <= kRunMaxR && (net->compact || net->P.acc_mode == SPK_ACC_FIXED) &&
-           (uint64_t)net->lists * tl.T8 <= kSplitMaxBuckets && (uint64_t)net->dmax * tl.T8 <= kSplitMaxBuckets;
-}
-
 spk_status choose_delivery(spk_net *net, RowIndex *ix)
 {
     if (net->max_row > kMaxRow)
@@ -516,10 +541,10 @@ spk_status choose_delivery(spk_net *net, RowIndex *ix)
     const bool binned_ok = (uint64_t)net->lists * tl.T8 <= kMaxBuckets;
     bool direct = net->lists == 1 && mean_row >= 2.0 * tl.T && toff_bytes <= 0.5 * 8.0 * (double)net->nnz;
     // With a smallest delay of two steps or more, no event filed at t is
-    // needed at t + 1: binned delivery lets the persistent kernel file them
-    // beside the updates (split kernel), which beats reading the due rows
-    // at arrival.
-    if (direct && net->dmin >= 2 && net->P.step_mode != SPK_STEP_GRAPH && split_layout_fits(net)) direct = false;
+    // needed at t + 1: binned delivery lets the persistent kernel run steps
+    // in batches and file a whole batch's events at once (or file them beside
+    // the updates, split kernel), which beats reading the due rows at arrival.
+    if (direct && net->dmin >= 2 && net->P.step_mode != SPK_STEP_GRAPH && binned_ok) direct = false;
     if (!binned_ok || net->P.delivery == SPK_DELIVERY_DIRECT) direct = true;
     if (net->P.delivery == SPK_DELIVERY_BINNED) {
         if (!binned_ok)
@@ -556,8 +581,11 @@ spk_status finish_rows(spk_net *net)
     SPK_TRY(dalloc(net, &mx, 1));
     SPK_HIP(hipMemsetAsync(insum, 0, (size_t)net->n * 8, s));
     SPK_HIP(hipMemsetAsync(mx, 0, 8, s));
+    SegTimer tm;
+    SPK_HIP(tm.start(s));
     SPK_HIP(in_abs_sum(syn_ptr(net), net->nnz, fixed, net->compact, net->ctab, insum, s));
     SPK_HIP(max_u64(insum, net->n, mx, s));
+    SPK_HIP(tm.stop(s, &net->range_ms));
     uint64_t m = 0;
     SPK_HIP(hipMemcpyAsync(&m, mx, 8, hipMemcpyDeviceToHost, s));
     SPK_HIP(hipStreamSynchronize(s));
@@ -577,12 +605,27 @@ spk_status finish_rows(spk_net *net)
     }
     class_units(net);
 
+    // Steps per batch of the unsplit persistent kernel (binned delivery): up
+    // to the smallest delay, so that nothing a batch files arrives within it,
+    // and within the bucket and slot limits.  SPK_BATCH_STEPS lowers it.
+    const Tiling &tl = net->tl;
+    net->run_D = 1;
+    if (!net->direct) {
+        uint32_t D = std::min<uint32_t>(net->dmin, kRunMaxD);
+        if (const char *e = std::getenv("SPK_BATCH_STEPS")) {
+            const long v = std::strtol(e, nullptr, 10);
+            if (v >= 1) D = std::min<uint32_t>(D, (uint32_t)v);
+        }
+        // the tile keeps one accumulator array per step of the batch in LDS
+        while (D > 1 && ((uint64_t)(D + net->lists - 1) * tl.T8 > kMaxBuckets || D * tl.W > kMaxTileW)) D--;
+        net->run_D = D;
+    }
     // Spike lists: direct delivery reads the lists of steps t - dmax .. t - dmin
     // while writing that of t; binned delivery consumes the list of t within t,
     // but in the persistent kernels one XCD may publish t + 1 (split kernel:
-    // t + 2) while another still reads t, so there are three.
-    const Tiling &tl = net->tl;
-    net->spk_slots = net->direct ? net->dmax + 1 : 3;
+    // t + 2) while another still reads t, so there are three; with batches of
+    // D steps, one XCD may publish the next batch while another reads this one.
+    net->spk_slots = net->direct ? net->dmax + 1 : std::max<uint32_t>(3, 2 * net->run_D);
     if (!net->direct) {
         // Pages: (group, push block, arrival slot, tile).  A page never holds
         // more than nnz records (each synapse arrives at most once per slot),
@@ -628,8 +671,11 @@ spk_status generate(spk_net *net)
     SPK_HIP(hipMemsetAsync(cnt, 0, (size_t)net->n * 4, s));
     ConnArgs c = conn_args(net);
     const bool in_rows = net->P.conn_kind == SPK_CONN_FIXED_IN;
+    SegTimer tm;
+    SPK_HIP(tm.start(s));
     if (in_rows) SPK_HIP(gen_in_count(c, cnt, s));
     else SPK_HIP(gen_count_rows(c, cnt, s));
+    SPK_HIP(tm.stop(s, &net->gen_ms));
     SPK_TRY(finish_counts(net, cnt));
     RowIndex ix{};
     SPK_TRY(choose_delivery(net, &ix));
@@ -641,12 +687,15 @@ spk_status generate(spk_net *net)
         void *tmp = nullptr;
         SPK_TRY(alloc_syn(net, &tmp, net->nnz));
         SPK_HIP(hipMemsetAsync(cnt, 0, (size_t)net->n * 4, s));
+        SPK_HIP(tm.start(s));
         SPK_HIP(gen_in_fill(c, net->row_ptr, cnt, tmp, s));
         SPK_HIP(bucket_rows(c, net->row_ptr, tmp, syn, ix, s));
-        SPK_HIP(hipStreamSynchronize(s));
+        SPK_HIP(tm.stop(s, &net->gen_ms));
         dfree(net, tmp);
     } else {        // drawn per source, bucketed while drawn
+        SPK_HIP(tm.start(s));
         SPK_HIP(gen_fill_rows(c, net->row_ptr, syn, ix, s));
+        SPK_HIP(tm.stop(s, &net->gen_ms));
     }
     SPK_HIP(hipStreamSynchronize(s));
     dfree(net, cnt);
@@ -720,6 +769,7 @@ RunArgs run_args(const spk_net *net, uint64_t t0, uint64_t n_steps)
     ra.t0 = t0;
     ra.n_steps = n_steps;
     ra.R = net->run_R;
+    ra.D = net->direct ? 1u : net->run_D;
     ra.cpages16 = net->cpages16;
     ra.cpages = net->cpages;
     ra.cfill = net->cfill;
@@ -767,13 +817,14 @@ spk_status choose_step_mode(spk_net *net)
     net->run_R = cus > 0 && cus % (int)kGroups == 0 ? (uint32_t)(cus / (int)kGroups) : 0u;
     const StepArgs a = step_args(net);
     // The split kernel runs filing and updates side by side on half the waves
-    // each: it wins when nothing filed at t is needed at t + 1 (smallest delay
-    // >= 2); with delay-1 events the unsplit kernel is faster on MI355X.
-    // SPK_PERSISTENT_SPLIT=0 / 1 forces the choice (a tuning knob).
-    bool want_split = net->dmin >= 2;
+    // each: it is taken when nothing filed at t is needed at t + 1 (smallest
+    // delay >= 2) but the unsplit kernel cannot batch steps; with delay-1
+    // events, or with batches of several steps, the unsplit kernel is faster
+    // on MI355X.  SPK_PERSISTENT_SPLIT=0 / 1 forces the choice (a tuning knob).
+    bool want_split = net->dmin >= 2 && net->run_D < 2;
     if (const char *e = std::getenv("SPK_PERSISTENT_SPLIT")) want_split = std::strcmp(e, "0") != 0;
     const bool split_fits = coop && want_split && split_supported(a, net->run_R);
-    const bool run_fits = coop && run_supported(a, net->run_R);
+    const bool run_fits = coop && run_supported(a, net->run_R) && run_batch_supported(a, net->direct ? 1u : net->run_D);
     if (!split_fits && !run_fits) {
         if (mode == SPK_STEP_PERSISTENT)
             return fail(SPK_EINVAL, "the persistent step kernel does not apply to this network or device "
@@ -986,6 +1037,7 @@ spk_status spk_create(const spk_params *params, void *stream, spk_net **out)
 {
     if (!params || !out) return fail(SPK_EINVAL, "null argument");
     *out = nullptr;
+    const auto t_begin = std::chrono::steady_clock::now();
     spk_net *net = new (std::nothrow) spk_net();
     if (!net) return fail(SPK_ENOMEM, "host allocation");
     net->P = *params;
@@ -1001,6 +1053,7 @@ spk_status spk_create(const spk_params *params, void *stream, spk_net **out)
         g_err = msg;
         return st;
     }
+    net->setup_ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t_begin).count();
     *out = net;
     return SPK_OK;
 }
@@ -1012,6 +1065,7 @@ spk_status spk_create_from_csr(const spk_params *params, uint32_t n, const uint6
     if (!params || !out || !row_ptr || (row_ptr[n] && (!col || !w)))
         return fail(SPK_EINVAL, "null argument");
     *out = nullptr;
+    const auto t_begin = std::chrono::steady_clock::now();
     spk_net *net = new (std::nothrow) spk_net();
     if (!net) return fail(SPK_ENOMEM, "host allocation");
     net->P = *params;
@@ -1097,6 +1151,7 @@ spk_status spk_create_from_csr(const spk_params *params, uint32_t n, const uint6
         g_err = msg;
         return st;
     }
+    net->setup_ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - t_begin).count();
     *out = net;
     return SPK_OK;
 }
@@ -1390,6 +1445,10 @@ spk_status spk_stats(spk_net *net, spk_stats_t *out)
     st.page_cap = net->page_cap;
     st.step_mode = net->persistent ? SPK_STEP_PERSISTENT : SPK_STEP_GRAPH;
     st.persistent_split = net->split ? 1u : 0u;
+    st.batch_steps = net->persistent && !net->split && !net->direct ? net->run_D : 1u;
+    st.setup_ms = net->setup_ms;
+    st.gen_ms = net->gen_ms;
+    st.range_ms = net->range_ms;
     *out = st;
     return SPK_OK;
 }

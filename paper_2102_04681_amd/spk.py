@@ -19,7 +19,7 @@ import numpy as np
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libspk.so")
 
 SPK_OK, SPK_EINVAL, SPK_ENOMEM, SPK_EHIP, SPK_EOVERFLOW, SPK_ESTATE = 0, -1, -2, -3, -4, -5
-SPK_ABI_VERSION = 3
+SPK_ABI_VERSION = 4
 SPK_LIF, SPK_SOURCE = 0, 1
 SPK_CONN_BERNOULLI, SPK_CONN_FIXED_OUT, SPK_CONN_FIXED_IN, SPK_CONN_EXPLICIT = 0, 1, 2, 3
 SPK_ACC_F32, SPK_ACC_FIXED = 0, 1
@@ -64,6 +64,7 @@ class spk_stats_t(C.Structure):
         ("fixed_shift", C.c_int32), ("k", C.c_float), ("bytes_per_synapse", C.c_double),
         ("tile_width", C.c_uint32), ("tiles", C.c_uint32), ("delivery", C.c_uint32),
         ("page_cap", C.c_uint32), ("step_mode", C.c_uint32), ("persistent_split", C.c_uint32),
+        ("batch_steps", C.c_uint32), ("setup_ms", C.c_double), ("gen_ms", C.c_double), ("range_ms", C.c_double),
     ]
 
 

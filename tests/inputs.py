@@ -94,6 +94,20 @@ def config(index: int, driven: bool = False, seed: int = 1, rate_hz: float = 10.
     return c
 
 
+def synth(n: int, density: float = 0.05, seed: int = 1, **over) -> dict:
+    """The Synth shape of the setup-time study (Sec. IV-C): one intra-connected
+    LIF population, Bernoulli connectivity of the given density, delay 1,
+    weights scaled by 80/(density n) as in C1."""
+    s = 80.0 / (density * n)
+    c = dict(_MEMBRANE, seed=seed, n=n, frac_exc=1.0, conn_kind=BERNOULLI, p=density,
+             w_exc=_f32(0.27 * s), w_inh=_f32(-4.5 * s), steps=1000)
+    c.update(over)
+    for k in ("v_rest", "v_th", "v_reset", "v0_lo", "v0_hi", "i_bias", "w_exc", "w_inh",
+              "w_lo", "w_hi", "ext_w"):
+        c[k] = _f32(c[k])
+    return c
+
+
 def scaled(index: int, n: int, driven: bool = True, **over) -> dict:
     """A reduced-size network with the per-neuron statistics of C<index>:
     Bernoulli p is rescaled to keep the expected in-degree when n is small

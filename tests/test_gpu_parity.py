@@ -244,16 +244,25 @@ RUN_CASES = [
     ("C2-6000", lambda: I.scaled(2, 6000, k_in_exc=480, k_in_inh=120), 300),
     ("C3-20000", lambda: I.scaled(3, 20000, k_out=1000), 100),
     ("C4-12000", lambda: I.scaled(4, 12000, k_out=1500), 400),
+    ("C4-d3-9", lambda: I.scaled(4, 12000, k_out=1500, delay_min=3, delay_max=9), 300),
     ("C0-literal", lambda: I.config(0, seed=1), 200),
 ]
 
 
 # how the steps run: graph replay, plain launches with events (profiling),
-# the persistent kernel (binned delivery: the split variant that files delay-1
-# events first), the same with events around it, and the unsplit persistent
-# kernel (SPK_PERSISTENT_SPLIT=0)
-MODES = [("graph", 1, False, "auto"), ("launch", 1, True, "auto"), ("persist", 2, False, "auto"),
-         ("persist-prof", 2, True, "auto"), ("persist-split", 2, False, "1"), ("persist-unsplit", 2, False, "0")]
+# the persistent kernel as chosen (binned delivery with a smallest delay >= 2:
+# the unsplit kernel in batches of up to 16 steps), the same with events
+# around it, the split variant (SPK_PERSISTENT_SPLIT=1), the unsplit kernel,
+# and the unsplit kernel with batches capped at 1 and 4 steps
+# (SPK_BATCH_STEPS)
+MODES = [("graph", 1, False, "auto", None), ("launch", 1, True, "auto", None), ("persist", 2, False, "auto", None),
+         ("persist-prof", 2, True, "auto", None), ("persist-split", 2, False, "1", None),
+         ("persist-unsplit", 2, False, "0", None), ("persist-batch1", 2, False, "0", "1"),
+         ("persist-batch4", 2, False, "0", "4")]
+
+
+def _expected_batch(cfg, batch):
+    return min(cfg["delay_min"], 16, int(batch) if batch else 16)
 
 
 def _persistent_applies(cfg, delivery):
@@ -264,10 +273,10 @@ def _persistent_applies(cfg, delivery):
 
 @pytest.mark.parametrize("name,mk,T", RUN_CASES, ids=[c[0] for c in RUN_CASES])
 @pytest.mark.parametrize("delivery", [1, 2], ids=["direct", "binned"])
-@pytest.mark.parametrize("mode,step_mode,profiled,split", MODES, ids=[m[0] for m in MODES])
+@pytest.mark.parametrize("mode,step_mode,profiled,split,batch", MODES, ids=[m[0] for m in MODES])
 @pytest.mark.parametrize("fmt", [f for f, _ in FORMATS], ids=[n for _, n in FORMATS])
-def test_fixed_point_simulation_bit_identical(spk, name, mk, T, delivery, mode, step_mode, profiled, split, fmt,
-                                              monkeypatch):
+def test_fixed_point_simulation_bit_identical(spk, name, mk, T, delivery, mode, step_mode, profiled, split, batch,
+                                              fmt, monkeypatch):
     cfg = mk()
     cfg["acc_mode"] = I.ACC_FIXED
     cfg["delivery"] = delivery
@@ -279,14 +288,20 @@ def test_fixed_point_simulation_bit_identical(spk, name, mk, T, delivery, mode, 
         pytest.skip("the persistent kernel takes direct delivery with one delay only")
     if split != "auto" and delivery == 1:
         pytest.skip("direct delivery has no split variant")
+    if batch and (delivery == 1 or cfg["delay_min"] < 2):
+        pytest.skip("steps are batched only with binned delivery and a smallest delay >= 2")
     if split != "auto":
         monkeypatch.setenv("SPK_PERSISTENT_SPLIT", split)
+    if batch:
+        monkeypatch.setenv("SPK_BATCH_STEPS", batch)
     _say(f"[run] {name} n={cfg['n']} T={T} delivery={delivery} mode={mode} format={fmt}")
     g = spk.Net(cfg, max_steps=T, raster_capacity=cfg["n"] * T)
     st = g.stats()
     assert st["step_mode"] == step_mode
-    want_split = step_mode == 2 and delivery == 2 and (split == "1" or (split == "auto" and cfg["delay_min"] >= 2))
+    want_split = step_mode == 2 and delivery == 2 and split == "1"
     assert st["persistent_split"] == (1 if want_split else 0)
+    unsplit_binned = step_mode == 2 and delivery == 2 and not want_split
+    assert st["batch_steps"] == (_expected_batch(cfg, batch) if unsplit_binned else 1)
     g.set_profiling(profiled)
     g.step(T)
     offs, ids = g.raster()
@@ -349,10 +364,14 @@ def test_bin_overflow_fallback(spk, acc, fmt, step_mode, split, monkeypatch):
         assert np.all(np.abs(got - want) <= ulp)
 
 
+@pytest.mark.parametrize("delays", [(1, 20), (3, 9), (15, 15)], ids=["d1-20", "d3-9", "d15"])
 @pytest.mark.parametrize("step_mode,split", [(1, "1"), (2, "1"), (2, "0")], ids=["graph", "persist", "unsplit"])
-def test_resume_matches_single_run(spk, step_mode, split, monkeypatch):
+def test_resume_matches_single_run(spk, step_mode, split, delays, monkeypatch):
+    # calls of 50 and 70 steps, and of one step each: batches of several steps
+    # (smallest delay 3 or 15) end early at the end of a call
     monkeypatch.setenv("SPK_PERSISTENT_SPLIT", split)
-    cfg = I.scaled(4, 5000, k_out=500, acc_mode=I.ACC_FIXED, step_mode=step_mode)
+    cfg = I.scaled(4, 5000, k_out=500, acc_mode=I.ACC_FIXED, step_mode=step_mode,
+                   delay_min=delays[0], delay_max=delays[1])
     a = spk.Net(cfg, max_steps=120, raster_capacity=5000 * 120)
     b = spk.Net(cfg, max_steps=120, raster_capacity=5000 * 120)
     a.step(50)
@@ -538,16 +557,48 @@ def test_persistent_equals_graph_fp32(spk, name, mk, T, fmt, delivery, monkeypat
         assert np.array_equal(v1.view(np.uint32), v2.view(np.uint32)) and np.array_equal(f1, f2)
 
 
+def test_setup_timing_stats(spk):
+    # creation reports its wall time and the GPU time of the generation
+    # kernels and of the accumulator-range pass (Sec. IV-C); uploaded rows are
+    # not generated
+    for cfg in (I.synth(4000, 0.05), I.scaled(2, 8000, k_in_exc=640, k_in_inh=160),
+                I.scaled(4, 8000, k_out=300)):
+        _say(f"[setup] n={cfg['n']} conn={cfg['conn_kind']}")
+        st = spk.Net(cfg, max_steps=1).stats()
+        assert st["gen_ms"] > 0 and st["range_ms"] > 0
+        assert st["setup_ms"] >= st["gen_ms"] + st["range_ms"]
+    n = 2000
+    row_ptr, col, w, delay = _random_csr(n, 2, seed=3)
+    cfg = I.explicit_params(n, delay_min=1, delay_max=12)
+    st = spk.Net(cfg, max_steps=1, csr=(row_ptr, col, w, delay)).stats()
+    assert st["gen_ms"] == 0 and st["range_ms"] > 0 and st["setup_ms"] > 0
+
+
 def test_step_mode_selection(spk, monkeypatch):
     # AUTO takes the persistent kernel where it applies; asking for it where
     # it does not (direct delivery with several delays) is an error
     # delay-1 events: the unsplit kernel
     st = spk.Net(I.scaled(4, 8000, k_out=300), max_steps=1).stats()
     assert st["step_mode"] == spk.SPK_STEP_PERSISTENT and st["persistent_split"] == 0
-    # smallest delay 15: binned delivery and the split kernel
-    st = spk.Net(I.scaled(2, 8000, k_in_exc=640, k_in_inh=160), max_steps=1).stats()
-    assert st["step_mode"] == spk.SPK_STEP_PERSISTENT and st["persistent_split"] == 1
-    assert st["delivery"] == spk.SPK_DELIVERY_BINNED
+    st = spk.Net(I.scaled(4, 8000, k_out=300), max_steps=1).stats()
+    assert st["batch_steps"] == 1
+    # smallest delay 15: binned delivery and the unsplit kernel in batches of
+    # 15 steps; the split kernel when asked for, or when batches are capped at 1
+    c2 = I.scaled(2, 8000, k_in_exc=640, k_in_inh=160)
+    st = spk.Net(c2, max_steps=1).stats()
+    assert st["step_mode"] == spk.SPK_STEP_PERSISTENT and st["persistent_split"] == 0
+    assert st["delivery"] == spk.SPK_DELIVERY_BINNED and st["batch_steps"] == 15
+    monkeypatch.setenv("SPK_BATCH_STEPS", "1")
+    st = spk.Net(c2, max_steps=1).stats()
+    assert st["persistent_split"] == 1 and st["batch_steps"] == 1
+    monkeypatch.delenv("SPK_BATCH_STEPS")
+    monkeypatch.setenv("SPK_PERSISTENT_SPLIT", "1")
+    st = spk.Net(c2, max_steps=1).stats()
+    assert st["persistent_split"] == 1 and st["batch_steps"] == 1
+    monkeypatch.delenv("SPK_PERSISTENT_SPLIT")
+    # delays 3..9: batches of 3 steps
+    st = spk.Net(I.scaled(4, 8000, k_out=300, delay_min=3, delay_max=9), max_steps=1).stats()
+    assert st["persistent_split"] == 0 and st["batch_steps"] == 3
     # ... but direct delivery when steps run as graphs
     st = spk.Net(I.scaled(2, 8000, k_in_exc=640, k_in_inh=160, step_mode=1), max_steps=1).stats()
     assert st["delivery"] == spk.SPK_DELIVERY_DIRECT
