@@ -202,6 +202,7 @@ constexpr uint32_t kCtlStride = 32;
 constexpr uint32_t kRunMaxR = 32;          // workgroups per XCD (one per compute unit)
 constexpr uint32_t kRunMaxFill = 2048;     // pages per push block: arrival slots x tiles of a group
 constexpr uint32_t kRunMaxD = 16;          // steps per batch of the unsplit kernel (binned delivery)
+constexpr uint32_t kRunMaxBuckets = 1024;  // unsplit kernel: (arrival offset, tile) buckets of a push block
 constexpr uint32_t kRunAbortTimeout = 1u;  // a barrier wait gave up
 constexpr uint32_t kRunAbortPlacement = 2u;  // workgroups not spread R per XCD: nothing was run
 struct RunCtl {

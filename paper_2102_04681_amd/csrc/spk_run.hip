@@ -63,8 +63,8 @@ template <bool FIXED, bool CMP>
 struct RunLDS {
     using AccT = typename Acc<FIXED>::T;
     using Rec = typename SynRec<CMP>::T;
-    static constexpr int R = CMP ? 16 : 8;                    // events per thread per load phase
-    static constexpr uint32_t kStageN = R * kRunThreads / 2;  // events bucket-sorted at once
+    static constexpr int R = CMP ? 16 : 8;                // events per thread per window
+    static constexpr uint32_t kStageN = R * kRunThreads;  // events bucket-sorted at once (a window)
     // persistent for the whole launch
     float V[kMaxTileW];
     uint8_t ref[kMaxTileW];     // LIF: refractory steps left; source: fires at the current step
@@ -96,9 +96,9 @@ struct RunLDS {
             uint64_t pbase[kRunChunk];
             uint64_t cbase[R * (kRunThreads / kWave)];
             uint32_t clen[R * (kRunThreads / kWave)];
-            uint32_t bcnt[kMaxBuckets];   // events per bucket in this half, then rank cursor
-            uint32_t bst[kMaxBuckets];    // bucket starts in the stage
-            uint32_t wb[kMaxBuckets];     // page position of stage entry q is wb[b] + q
+            uint32_t bcnt[kRunMaxBuckets];  // events per bucket in this window, then rank cursor
+            uint32_t bst[kRunMaxBuckets];   // bucket starts in the stage
+            uint32_t wb[kRunMaxBuckets];    // page position of stage entry q is wb[b] + q
         } p;
     } u;
     uint32_t ws[16], ws2[16];
@@ -543,84 +543,84 @@ __device__ uint32_t run_push(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t 
                 uom |= (uint64_t)(lw >> 8) << (4 * u);
                 rec[u] = SynRec<CMP>::load(a, idx);  // unconditional load from a clamped index
             }
+            // rank every event of the window within its bucket (LDS counters)
+            uint32_t tr[R];
 #pragma unroll
-            for (int h = 0; h < 2; h++) {
-                if (i0 + (uint32_t)h * (R / 2) * nw >= C) break;
-                constexpr int RH = R / 2;
-                uint32_t tr[RH];
-#pragma unroll
-                for (int rr = 0; rr < RH; rr++) {
-                    const int q = h * RH + rr;
-                    tr[rr] = 0xffffffffu;
-                    if (!((okm >> q) & 1u)) continue;
-                    const uint32_t key = rec_key(rec[q]);
-                    const uint32_t ao = rec_delay(key) + (uint32_t)((uom >> (4 * q)) & 0xfu);
-                    const uint32_t local = rec_target(key) - xlo;
-                    const uint32_t b = ao * tl.T8 + (local >> tl.logW);
-                    const uint32_t rank = atomicAdd(&L.u.p.bcnt[b], 1u);
-                    tr[rr] = (b << 16) | rank;
-                    const uint32_t sv = (b << 16) | (local & (tl.W - 1));
-                    if constexpr (CMP) rec[q] = sv | (rec_class(key) << kPageClassShift);
-                    else rec[q].x = (int)sv;
-                }
-                lds_sync();
-                uint32_t staged;
-                {
-                    const uint32_t P = (NB + kRunThreads - 1) / kRunThreads;
-                    const uint32_t b0 = tid * P;
-                    uint32_t sum = 0;
-                    for (uint32_t k = 0; k < P; k++)
-                        if (b0 + k < NB) sum += L.u.p.bcnt[b0 + k];
-                    uint32_t ex = block_scan_u32_open(sum, h ? L.ws : L.ws2, &staged);
-                    for (uint32_t k = 0; k < P; k++) {
-                        if (b0 + k < NB) {
-                            const uint32_t bb = b0 + k, cnt = L.u.p.bcnt[bb];
-                            const uint32_t ao = bb / tl.T8, cc = bb - ao * tl.T8;
-                            uint32_t sl = slot_of_a0 + ao;
-                            sl = sl >= a.pslots ? sl - a.pslots : sl;
-                            uint32_t &f = L.fill[sl * tl.T8 + cc];
-                            L.u.p.bst[bb] = ex;
-                            L.u.p.wb[bb] = f - ex;
-                            f += cnt;
-                            L.u.p.bcnt[bb] = 0;
-                            ex += cnt;
-                        }
-                    }
-                }
-                lds_sync();
-                Rec *stage = L.u.p.stage;
-#pragma unroll
-                for (int rr = 0; rr < RH; rr++) {
-                    if (tr[rr] == 0xffffffffu) continue;
-                    stage[L.u.p.bst[tr[rr] >> 16] + (tr[rr] & 0xffffu)] = rec[h * RH + rr];
-                }
-                lds_sync();
-                for (uint32_t q = tid; q < staged; q += kRunThreads) {
-                    const Rec r2 = stage[q];
-                    const uint32_t key = rec_key(r2);
-                    const uint32_t b = key >> 16, low = key & 0xffffu;
-                    const uint32_t pos = L.u.p.wb[b] + q;
-                    const uint32_t ao = b / tl.T8, cc = b - ao * tl.T8;
-                    uint32_t sl = slot_of_a0 + ao;
-                    sl = sl >= a.pslots ? sl - a.pslots : sl;
-                    if (pos < cap) {
-                        const uint64_t e = (uint64_t)page_of(a, x, r, sl, cc) * cap + pos;
-                        if constexpr (CMP) a.pages16[e] = (uint16_t)low;
-                        else a.pages[e] = make_int2((int)low, r2.y);
-                    } else {
-                        long long units;
-                        uint32_t local;
-                        if constexpr (CMP) {
-                            units = class_units(a, low >> kPageClassShift);
-                            local = low & kPageLocalMask;
-                        } else {
-                            units = units_of<FIXED>(r2.y, a.m.shift64);
-                            local = low;
-                        }
-                        overflow_add<FIXED, true>(a, sl, x * tl.T8 + cc, local, units);
+            for (int q = 0; q < R; q++) {
+                tr[q] = 0xffffffffu;
+                if (!((okm >> q) & 1u)) continue;
+                const uint32_t key = rec_key(rec[q]);
+                const uint32_t ao = rec_delay(key) + (uint32_t)((uom >> (4 * q)) & 0xfu);
+                const uint32_t local = rec_target(key) - xlo;
+                const uint32_t b = ao * tl.T8 + (local >> tl.logW);
+                const uint32_t rank = atomicAdd(&L.u.p.bcnt[b], 1u);
+                tr[q] = (b << 16) | rank;
+                const uint32_t sv = (b << 16) | (local & (tl.W - 1));
+                if constexpr (CMP) rec[q] = sv | (rec_class(key) << kPageClassShift);
+                else rec[q].x = (int)sv;
+            }
+            lds_sync();
+            // bucket starts in the stage; the page position of staged event q
+            // of bucket b is wb[b] + q (mod 2^32); the fill counters advance
+            uint32_t staged;
+            {
+                const uint32_t P = (NB + kRunThreads - 1) / kRunThreads;
+                const uint32_t b0 = tid * P;
+                uint32_t sum = 0;
+                for (uint32_t k = 0; k < P; k++)
+                    if (b0 + k < NB) sum += L.u.p.bcnt[b0 + k];
+                uint32_t ex = block_scan_u32_open(sum, L.ws2, &staged);
+                for (uint32_t k = 0; k < P; k++) {
+                    if (b0 + k < NB) {
+                        const uint32_t bb = b0 + k, cnt = L.u.p.bcnt[bb];
+                        const uint32_t ao = bb / tl.T8, cc = bb - ao * tl.T8;
+                        uint32_t sl = slot_of_a0 + ao;
+                        sl = sl >= a.pslots ? sl - a.pslots : sl;
+                        uint32_t &f = L.fill[sl * tl.T8 + cc];
+                        L.u.p.bst[bb] = ex;
+                        L.u.p.wb[bb] = f - ex;
+                        f += cnt;
+                        L.u.p.bcnt[bb] = 0;
+                        ex += cnt;
                     }
                 }
             }
+            lds_sync();
+            Rec *stage = L.u.p.stage;
+#pragma unroll
+            for (int q = 0; q < R; q++) {
+                if (tr[q] == 0xffffffffu) continue;
+                stage[L.u.p.bst[tr[q] >> 16] + (tr[q] & 0xffffu)] = rec[q];
+            }
+            lds_sync();
+            // coalesced appends: consecutive staged events of a bucket go to
+            // consecutive page positions
+            for (uint32_t q = tid; q < staged; q += kRunThreads) {
+                const Rec r2 = stage[q];
+                const uint32_t key = rec_key(r2);
+                const uint32_t b = key >> 16, low = key & 0xffffu;
+                const uint32_t pos = L.u.p.wb[b] + q;
+                const uint32_t ao = b / tl.T8, cc = b - ao * tl.T8;
+                uint32_t sl = slot_of_a0 + ao;
+                sl = sl >= a.pslots ? sl - a.pslots : sl;
+                if (pos < cap) {
+                    const uint64_t e = (uint64_t)page_of(a, x, r, sl, cc) * cap + pos;
+                    if constexpr (CMP) a.pages16[e] = (uint16_t)low;
+                    else a.pages[e] = make_int2((int)low, r2.y);
+                } else {
+                    long long units;
+                    uint32_t local;
+                    if constexpr (CMP) {
+                        units = class_units(a, low >> kPageClassShift);
+                        local = low & kPageLocalMask;
+                    } else {
+                        units = units_of<FIXED>(r2.y, a.m.shift64);
+                        local = low;
+                    }
+                    overflow_add<FIXED, true>(a, sl, x * tl.T8 + cc, local, units);
+                }
+            }
+            lds_sync();  // the stage and wb are rewritten by the next window
         }
         lds_sync();  // the chunk tables are rewritten by the next chunk
     }
@@ -805,7 +805,7 @@ bool run_supported(const StepArgs &a, uint32_t R)
     if (R == 0 || R > kRunMaxR || tl.T8 > R || tl.T != kGroups * tl.T8 || tl.W > kMaxTileW) return false;
     if (a.m.pois_len > 256) return false;
     if (a.direct) return a.lists == 1 && a.spk_slots > a.dmin;
-    return a.pg1 == R && a.pslots * tl.T8 <= kRunMaxFill && a.lists * tl.T8 <= kMaxBuckets && a.spk_slots >= 2 &&
+    return a.pg1 == R && a.pslots * tl.T8 <= kRunMaxFill && a.lists * tl.T8 <= kRunMaxBuckets && a.spk_slots >= 2 &&
            a.page_cap % 16 == 0 && tl.W <= 65536;
 }
 
@@ -813,7 +813,7 @@ bool run_batch_supported(const StepArgs &a, uint32_t D)
 {
     if (a.direct) return D == 1;
     return D >= 1 && D <= kRunMaxD && D <= a.dmin && a.spk_slots >= 2 * D && a.tl.T <= kRunMaxT &&
-           (D + a.lists - 1) * a.tl.T8 <= kMaxBuckets && D + a.lists - 1 <= a.pslots &&
+           (D + a.lists - 1) * a.tl.T8 <= kRunMaxBuckets && D + a.lists - 1 <= a.pslots &&
            D * a.tl.W <= kMaxTileW && D * a.pg1 <= kRunThreads;
 }
 

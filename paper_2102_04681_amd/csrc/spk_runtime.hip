@@ -617,7 +617,7 @@ spk_status finish_rows(spk_net *net)
             if (v >= 1) D = std::min<uint32_t>(D, (uint32_t)v);
         }
         // the tile keeps one accumulator array per step of the batch in LDS
-        while (D > 1 && ((uint64_t)(D + net->lists - 1) * tl.T8 > kMaxBuckets || D * tl.W > kMaxTileW)) D--;
+        while (D > 1 && ((uint64_t)(D + net->lists - 1) * tl.T8 > kRunMaxBuckets || D * tl.W > kMaxTileW)) D--;
         net->run_D = D;
     }
     // Spike lists: direct delivery reads the lists of steps t - dmax .. t - dmin
