@@ -91,9 +91,6 @@ struct RunLDS {
             unsigned long long emit[kRunMaxD];      // events emitted per step of the batch
             unsigned long long rbu[kRunMaxD];       // raster position of spike k of step u: rbu[u] + k
             uint32_t rokm;                          // bit u: the spikes of step u fit in the raster
-            uint32_t cpre[kRunChunk + 1];
-            uint32_t plen[kRunChunk];
-            uint64_t pbase[kRunChunk];
             uint64_t cbase[R * (kRunThreads / kWave)];
             uint32_t clen[R * (kRunThreads / kWave)];
             uint32_t bcnt[kRunMaxBuckets];  // events per bucket in this window, then rank cursor
@@ -312,6 +309,8 @@ __device__ void run_update(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x,
     const ModelArgs &m = a.m;
     const uint32_t tid = threadIdx.x, lane = lane_id();
     uint64_t ev = 0;
+    uint64_t bal[kRunRounds];  // per round: the wave's firing lanes (wave-uniform)
+    uint32_t nw_spk = 0;       // the wave's spikes over all rounds
 #pragma unroll
     for (int u = 0; u < kRunRounds; u++) {
         const uint32_t q = u * kRunThreads + tid;
@@ -355,17 +354,24 @@ __device__ void run_update(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x,
             L.V[q] = V;
             if (spk && DIRECT) ev += a.outdeg[tile_lo + q];
         }
-        const uint64_t mask = __ballot(spk);
-        if (mask) {
-            const int leader = __ffsll((unsigned long long)mask) - 1;
-            uint32_t wb = 0;
-            if ((int)lane == leader) wb = atomicAdd(&L.nspk, (uint32_t)__popcll(mask));
-            wb = __shfl(wb, leader);
-            if (spk) {
+        bal[u] = __ballot(spk);
+        nw_spk += (uint32_t)__popcll(bal[u]);
+    }
+    // compaction: one LDS counter update per wave, then every round's firing
+    // lanes at consecutive positions
+    if (nw_spk) {
+        uint32_t wb = 0;
+        if (lane == 0) wb = atomicAdd(&L.nspk, nw_spk);
+        wb = __shfl(wb, 0);
+#pragma unroll
+        for (int u = 0; u < kRunRounds; u++) {
+            const uint64_t mask = bal[u];
+            if ((mask >> lane) & 1ull) {
                 const uint32_t rank = __builtin_amdgcn_mbcnt_hi(
                     (uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
-                L.u.t.spk[wb + rank] = (uint16_t)q;
+                L.u.t.spk[wb + rank] = (uint16_t)(u * kRunThreads + tid);
             }
+            wb += (uint32_t)__popcll(mask);
         }
     }
     if (DIRECT) ev = block_sum_u64(ev, L.ws64);
@@ -508,13 +514,7 @@ __device__ uint32_t run_push(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t 
         }
         uint32_t C;
         const uint32_t nch = (len + kWave - 1) / kWave;
-        const uint32_t coff = block_scan_u32(nch, L.ws, &C);
-        if (tid < K) {
-            L.u.p.cpre[tid] = coff;
-            L.u.p.plen[tid] = len;
-            L.u.p.pbase[tid] = base;
-        }
-        lds_sync();
+        const uint32_t coff = block_scan_u32(nch, L.ws, &C);  // this thread's row: chunks [coff, coff + nch)
         constexpr uint32_t kWin = R * nw;
         for (uint32_t i0 = 0; i0 < C; i0 += kWin) {
             for (uint32_t q = tid; q < kWin; q += kRunThreads) L.u.p.clen[q] = 0;
