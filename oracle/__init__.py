@@ -95,6 +95,8 @@ def lib():
         L.orc_get_csr.argtypes = [P, P, P, P, P]
         L.orc_row.restype = i32
         L.orc_row.argtypes = [P, u32, P, P, P, u64, C.POINTER(u64)]
+        L.orc_in_row.restype = i32
+        L.orc_in_row.argtypes = [P, u32, P, P, P, u64, C.POINTER(u64)]
         L.orc_deliver.restype = i32
         L.orc_deliver.argtypes = [P, P, u64, u32, P, P]
         L.orc_run.restype = i32
@@ -214,6 +216,18 @@ class Net:
         _check(lib().orc_row(self._h, s, _ptr(tgt), _ptr(w), _ptr(d), cap, C.byref(L)), "row")
         L = L.value
         return tgt[:L].copy(), w[:L].copy(), d[:L].copy()
+
+    def in_row(self, tgt: int):
+        """Fixed in-degree: the in-synapses of target tgt (source, weight,
+        delay) in draw order (Sec. III-B), without the CSR."""
+        cap = int(self.cfg["k_in_exc"]) + int(self.cfg["k_in_inh"])
+        src = np.zeros(max(cap, 1), dtype=np.uint32)
+        w = np.zeros(max(cap, 1), dtype=np.float32)
+        d = np.zeros(max(cap, 1), dtype=np.uint8)
+        L = C.c_uint64()
+        _check(lib().orc_in_row(self._h, tgt, _ptr(src), _ptr(w), _ptr(d), cap, C.byref(L)), "in_row")
+        L = L.value
+        return src[:L].copy(), w[:L].copy(), d[:L].copy()
 
     def deliver(self, spikes, delay: int = 0, fixed: bool = False):
         spikes = np.ascontiguousarray(spikes, dtype=np.uint32)

@@ -314,22 +314,29 @@ static int build_rows(orc_net *net)
  * range and k_in_inh from the inhibitory range (with replacement); the
  * synapses are then regrouped by source row (counting sort) and each row
  * is sorted canonically. */
+/* Fixed in-degree (Sec. III-B): in-synapse j of target tgt.  The first
+ * k_in_exc draw their source uniformly from the excitatory range, the rest
+ * from the inhibitory range (with replacement). */
+static uint32_t fixed_in_src(const orc_net *net, uint32_t tgt, uint32_t j)
+{
+    const orc_params *P = &net->P;
+    uint32_t ne = net->D.n_exc, ni = P->n - ne;
+    return j < P->k_in_exc
+        ? range_n(orc_hash(P->seed, ORC_TAG_SRC_E, tgt, j), ne)
+        : ne + range_n(orc_hash(P->seed, ORC_TAG_SRC_I, tgt, j - P->k_in_exc), ni);
+}
+
 static int build_fixed_in(orc_net *net)
 {
     const orc_params *P = &net->P;
-    uint32_t n = P->n, ne = net->D.n_exc, ni = n - ne;
+    uint32_t n = P->n;
     uint32_t kin = P->k_in_exc + P->k_in_inh;
     uint64_t nnz = (uint64_t)n * kin;
     uint64_t *cnt = (uint64_t *)calloc((size_t)n + 1, sizeof(uint64_t));
     net->row_ptr = (uint64_t *)malloc(((size_t)n + 1) * sizeof(uint64_t));
     if (!cnt || !net->row_ptr) { free(cnt); return ORC_ENOMEM; }
     for (uint32_t tgt = 0; tgt < n; tgt++)
-        for (uint32_t j = 0; j < kin; j++) {
-            uint32_t src = j < P->k_in_exc
-                ? range_n(orc_hash(P->seed, ORC_TAG_SRC_E, tgt, j), ne)
-                : ne + range_n(orc_hash(P->seed, ORC_TAG_SRC_I, tgt, j - P->k_in_exc), ni);
-            cnt[src]++;
-        }
+        for (uint32_t j = 0; j < kin; j++) cnt[fixed_in_src(net, tgt, j)]++;
     net->row_ptr[0] = 0;
     for (uint32_t s = 0; s < n; s++) net->row_ptr[s + 1] = net->row_ptr[s] + cnt[s];
     int rc = alloc_csr(net, nnz);
@@ -337,9 +344,7 @@ static int build_fixed_in(orc_net *net)
     for (uint32_t s = 0; s < n; s++) cnt[s] = net->row_ptr[s];
     for (uint32_t tgt = 0; tgt < n; tgt++)
         for (uint32_t j = 0; j < kin; j++) {
-            uint32_t src = j < P->k_in_exc
-                ? range_n(orc_hash(P->seed, ORC_TAG_SRC_E, tgt, j), ne)
-                : ne + range_n(orc_hash(P->seed, ORC_TAG_SRC_I, tgt, j - P->k_in_exc), ni);
+            uint32_t src = fixed_in_src(net, tgt, j);
             uint64_t o = cnt[src]++;
             net->col[o] = tgt;
             net->delay[o] = syn_delay(net, orc_hash(P->seed, ORC_TAG_DELAY, tgt, j));
@@ -567,6 +572,22 @@ int orc_row(orc_net *net, uint32_t s, uint32_t *tgt, float *w, uint8_t *delay,
 }
 
 /* ------------------------------------------------------------ delivery */
+
+int orc_in_row(const orc_net *net, uint32_t tgt, uint32_t *src, float *w, uint8_t *delay,
+               uint64_t cap, uint64_t *len)
+{
+    const orc_params *P = &net->P;
+    if (P->conn_kind != ORC_CONN_FIXED_IN || tgt >= P->n) return ORC_EINVAL;
+    uint32_t kin = P->k_in_exc + P->k_in_inh;
+    *len = kin;
+    if (kin > cap) return ORC_EOVERFLOW;
+    for (uint32_t j = 0; j < kin; j++) {
+        src[j] = fixed_in_src(net, tgt, j);
+        delay[j] = syn_delay(net, orc_hash(P->seed, ORC_TAG_DELAY, tgt, j));
+        w[j] = syn_weight(net, src[j], orc_hash(P->seed, ORC_TAG_W, tgt, j));
+    }
+    return ORC_OK;
+}
 
 int orc_deliver(orc_net *net, const uint32_t *spikes, uint64_t n_spikes,
                 uint32_t delay, double *out_f, int64_t *out_q)

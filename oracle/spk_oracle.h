@@ -104,6 +104,10 @@ int orc_get_csr(const orc_net *net, uint64_t *row_ptr, uint32_t *col, float *w,
 /* Canonical row s (sorted by target, delay, weight bits). */
 int orc_row(orc_net *net, uint32_t s, uint32_t *tgt, float *w, uint8_t *delay,
             uint64_t cap, uint64_t *len);
+/* Fixed in-degree networks: the in-synapses of target tgt in draw order
+ * (source, weight, delay), generated on their own (no CSR needed). */
+int orc_in_row(const orc_net *net, uint32_t tgt, uint32_t *src, float *w, uint8_t *delay,
+               uint64_t cap, uint64_t *len);
 /* Delivery definition: out[i] = sum over listed spikes s, over synapses
  * s->i whose delay equals 'delay' (0 = any delay), of w (double) and of the
  * quantised weight (int64).  Either output may be NULL. */

@@ -1,4 +1,4 @@
-"""GPU parity at the full benchmark size, in the configuration bench.py times.
+"""GPU parity at the full benchmark sizes, in the configurations bench.py times.
 
 Workload: 2,000,000 LIF neurons, fixed out-degree 1,500 (3.0e9 synapses),
 delays 1..20 steps, external Poisson drive at twice the threshold rate,
@@ -114,3 +114,55 @@ def test_full_size_bench_configuration_sampled(spk_full, step_mode, split, monke
         assert r == int(R1[i]), f"neuron {i}: refractory counter"
         assert sp == (int(i) in spiked_t), f"neuron {i}: spike decision"
     _say("[full] sampled update ok")
+
+
+def test_full_size_delay15_batch_sampled(spk_full):
+    """The 1e9-synapse network with delay 15 (100,000 LIF, in-degree 8,000
+    excitatory + 2,000 inhibitory, Poisson drive, fp32 accumulation) in the
+    configuration bench.py --config 2 times: the persistent kernel in batches
+    of 15 steps.  After 300 steps, one more batch of 15 steps; for sampled
+    neurons the oracle draws the in-synapses (its per-target generator), sums
+    the weights of those whose source fired 15 steps earlier exactly, and
+    runs its single-neuron update 15 times: every spike decision of the batch
+    and the final state must equal the library's bit for bit."""
+    spk = spk_full
+    cfg = I.config(2, driven=True)
+    n, D, d = cfg["n"], 15, cfg["delay_min"]
+    T0 = 300
+    _say(f"[full c2] create n={n}")
+    g = spk.Net(cfg, max_steps=T0 + D, raster_capacity=2_000_000)
+    st = g.stats()
+    assert st["step_mode"] == spk.SPK_STEP_PERSISTENT and st["persistent_split"] == 0
+    assert st["delivery"] == spk.SPK_DELIVERY_BINNED and st["batch_steps"] == D
+    assert st["nnz"] == n * (cfg["k_in_exc"] + cfg["k_in_inh"])
+    s64 = int(st["fixed_shift"])
+    g.step(T0)
+    V0, R0 = g.state()
+    g.step(D)
+    V1, R1 = g.state()
+    offs, ids = g.raster()
+    spikes = [set(ids[int(offs[t]):int(offs[t + 1])].tolist()) for t in range(T0 + D)]
+    fired = np.zeros((D, n), dtype=bool)  # fired[k, s]: s spiked at step T0 + k - 15
+    for k in range(D):
+        fired[k, ids[int(offs[T0 + k - d]):int(offs[T0 + k - d + 1])]] = True
+    assert 0 < sum(len(spikes[t]) for t in range(T0, T0 + D)) < n
+    # every synapse has delay 15: events arriving at t are those emitted at t - 15
+    dl, ev = g.delivered(T0, D), g.events(T0 - d, D)
+    assert np.array_equal(dl, ev)
+
+    o = oracle.Net(cfg, build_csr=False)
+    rng = np.random.default_rng(11)
+    targets = rng.choice(n, 256, replace=False).astype(np.uint32)
+    for i in targets:
+        src, w, dd = o.in_row(int(i))
+        assert (dd == d).all()
+        units = np.rint(np.ldexp(w.astype(np.float64), s64)).astype(np.int64)
+        v, r = float(V0[i]), int(R0[i])
+        for t in range(T0, T0 + D):
+            acc = int(units[fired[t - T0, src]].sum())
+            isyn = np.float32(np.ldexp(np.float64(acc), -s64))
+            v, r, sp = o.update_one(t, int(i), v, r, isyn_f=float(isyn))
+            assert sp == (int(i) in spikes[t]), f"neuron {i}: spike decision at step {t}"
+        assert np.float32(v).view(np.uint32) == V1[i].view(np.uint32), f"neuron {i}: V {v} vs {V1[i]}"
+        assert r == int(R1[i]), f"neuron {i}: refractory counter"
+    _say("[full c2] sampled batch ok")

@@ -196,6 +196,23 @@ def test_brute_force_fixed_out_delivery():
     np.testing.assert_allclose(net.deliver(spikes), want, rtol=0, atol=1e-12)
 
 
+def test_fixed_in_rows_per_target_match_the_csr():
+    # the per-target generator (used where the whole network is too large to
+    # build) gives every target exactly its column of the CSR
+    cfg = I.config(2, n=300, k_in_exc=24, k_in_inh=6, delay_min=2, delay_max=6, seed=6)
+    net = oracle.Net(cfg)
+    rp, col, w, d = net.csr()
+    src = np.repeat(np.arange(300), np.diff(rp).astype(np.int64))
+    lazy = oracle.Net(cfg, build_csr=False)
+    for tgt in range(300):
+        ls, lw, ld = lazy.in_row(tgt)
+        assert len(ls) == 30
+        m = col == tgt
+        a = sorted(zip(src[m].tolist(), d[m].tolist(), w[m].view(np.uint32).tolist()))
+        b = sorted(zip(ls.tolist(), ld.tolist(), lw.view(np.uint32).tolist()))
+        assert a == b, tgt
+
+
 def test_brute_force_fixed_in_delivery():
     cfg = I.config(2, n=50, k_in_exc=6, k_in_inh=3, delay_min=2, delay_max=2, seed=4)
     net = oracle.Net(cfg)
