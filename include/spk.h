@@ -177,7 +177,9 @@ typedef struct {
      * kernels (row counts, fill and regrouping; excludes allocation), and of the
      * accumulator-range pass (largest sum of |weights| into one neuron).
      * gen_ms is zero for networks made by spk_create_from_csr (rows are
-     * uploaded and grouped there, not generated). */
+     * uploaded and grouped there, not generated); range_ms is zero for fixed
+     * in-degree networks with population weights, whose range is known
+     * without a pass (every neuron has the same in-synapses' weights). */
     double setup_ms, gen_ms, range_ms;
 } spk_stats_t;
 

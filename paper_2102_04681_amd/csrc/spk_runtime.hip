@@ -383,6 +383,22 @@ spk_status choose_format(spk_net *net, const float *classes, uint32_t n_cls)
     return SPK_OK;
 }
 
+// The term of one synapse of weight w in the accumulator-range bound, as the
+// range pass computes it: |quantised w| (fixed mode) or |w| in units of
+// 2^-24 rounded up (fp32 mode).
+spk_status abs_term(const spk_net *net, float w, uint64_t *out)
+{
+    if (net->P.acc_mode == SPK_ACC_FIXED) {
+        int32_t q = 0;
+        if (!quantise(w, net->P.fixed_shift, &q))
+            return fail(SPK_EOVERFLOW, "a weight does not fit int32 at this fixed_shift");
+        *out = (uint64_t)std::llabs((long long)q);
+    } else {
+        *out = (uint64_t)std::ceil(std::ldexp((double)std::fabs(w), 24));
+    }
+    return SPK_OK;
+}
+
 // Per-class accumulator units, once the unit is known.
 void class_units(spk_net *net)
 {
@@ -576,21 +592,31 @@ spk_status finish_rows(spk_net *net)
     // mode: choose the 64-bit fixed-point unit 2^-S64 as fine as the largest
     // possible sum allows.
     const bool fixed = net->P.acc_mode == SPK_ACC_FIXED;
-    uint64_t *insum = nullptr, *mx = nullptr;
-    SPK_TRY(dalloc(net, &insum, net->n));
-    SPK_TRY(dalloc(net, &mx, 1));
-    SPK_HIP(hipMemsetAsync(insum, 0, (size_t)net->n * 8, s));
-    SPK_HIP(hipMemsetAsync(mx, 0, 8, s));
-    SegTimer tm;
-    SPK_HIP(tm.start(s));
-    SPK_HIP(in_abs_sum(syn_ptr(net), net->nnz, fixed, net->compact, net->ctab, insum, s));
-    SPK_HIP(max_u64(insum, net->n, mx, s));
-    SPK_HIP(tm.stop(s, &net->range_ms));
     uint64_t m = 0;
-    SPK_HIP(hipMemcpyAsync(&m, mx, 8, hipMemcpyDeviceToHost, s));
-    SPK_HIP(hipStreamSynchronize(s));
-    dfree(net, insum);
-    dfree(net, mx);
+    if (net->P.conn_kind == SPK_CONN_FIXED_IN && !net->P.w_uniform) {
+        // every neuron has exactly k_in_exc excitatory and k_in_inh
+        // inhibitory in-synapses, each with its population's weight: the
+        // largest sum is every neuron's, no pass over the synapses needed
+        uint64_t te = 0, ti = 0;
+        SPK_TRY(abs_term(net, net->P.w_exc, &te));
+        SPK_TRY(abs_term(net, net->P.w_inh, &ti));
+        m = (uint64_t)net->P.k_in_exc * te + (uint64_t)net->P.k_in_inh * ti;
+    } else {
+        uint64_t *insum = nullptr, *mx = nullptr;
+        SPK_TRY(dalloc(net, &insum, net->n));
+        SPK_TRY(dalloc(net, &mx, 1));
+        SPK_HIP(hipMemsetAsync(insum, 0, (size_t)net->n * 8, s));
+        SPK_HIP(hipMemsetAsync(mx, 0, 8, s));
+        SegTimer tm;
+        SPK_HIP(tm.start(s));
+        SPK_HIP(in_abs_sum(syn_ptr(net), net->nnz, fixed, net->compact, net->ctab, insum, s));
+        SPK_HIP(max_u64(insum, net->n, mx, s));
+        SPK_HIP(tm.stop(s, &net->range_ms));
+        SPK_HIP(hipMemcpyAsync(&m, mx, 8, hipMemcpyDeviceToHost, s));
+        SPK_HIP(hipStreamSynchronize(s));
+        dfree(net, insum);
+        dfree(net, mx);
+    }
     if (fixed) {
         const uint64_t kmax = net->pois_len ? net->pois_len - 1 : 0;
         const uint64_t extra = kmax * (uint64_t)std::llabs((long long)net->ext_wq) +

@@ -442,6 +442,26 @@ def test_fixed_point_guard_matches_oracle(spk):
     spk.Net(cfg, max_steps=1)
 
 
+def test_fixed_point_guard_fixed_in_degree(spk):
+    # fixed in-degree with population weights: the range is known without a
+    # pass over the synapses; the library refuses exactly the networks the
+    # oracle refuses (largest per-neuron sum of |quantised weights| beyond
+    # int32: 50 x 42,949,672 fits, 50 x 42,960,159 does not)
+    for w, fits in ((40.95, True), (40.97, False)):
+        cfg = I.config(2, n=400, k_in_exc=40, k_in_inh=10, w_exc=w, w_inh=-w, ext_lambda=0.0,
+                       ext_w=0.0, acc_mode=I.ACC_FIXED, fixed_shift=20)
+        if fits:
+            assert int(oracle.Net(cfg).in_abs_sum_q().max()) <= 2**31 - 1
+            spk.Net(cfg, max_steps=1)
+        else:
+            with pytest.raises(oracle.OracleError) as eo:
+                oracle.Net(cfg)
+            assert eo.value.code == -4  # the oracle's overflow status
+            with pytest.raises(spk.SpkError) as e:
+                spk.Net(cfg, max_steps=1)
+            assert e.value.code == spk.SPK_EOVERFLOW
+
+
 @pytest.mark.parametrize("seed", [1, 2])
 def test_fp32_mode_mean_rate_within_one_percent(spk, seed):
     # fp32 atomics: spike trains diverge after the first rounding
@@ -565,7 +585,9 @@ def test_setup_timing_stats(spk):
                 I.scaled(4, 8000, k_out=300)):
         _say(f"[setup] n={cfg['n']} conn={cfg['conn_kind']}")
         st = spk.Net(cfg, max_steps=1).stats()
-        assert st["gen_ms"] > 0 and st["range_ms"] > 0
+        assert st["gen_ms"] > 0
+        # fixed in-degree with population weights: the range needs no pass
+        assert (st["range_ms"] == 0) == (cfg["conn_kind"] == I.FIXED_IN)
         assert st["setup_ms"] >= st["gen_ms"] + st["range_ms"]
     n = 2000
     row_ptr, col, w, delay = _random_csr(n, 2, seed=3)
