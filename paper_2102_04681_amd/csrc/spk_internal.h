@@ -208,9 +208,9 @@ constexpr uint32_t kRunAbortPlacement = 2u;  // workgroups not spread R per XCD:
 struct RunCtl {
     uint32_t ticket[kGroups * kCtlStride];  // workgroups placed on each XCD
     uint32_t gx[kGroups * kCtlStride];      // grid barrier: arrivals per XCD
-    uint32_t lx[kGroups * kCtlStride];      // XCD barrier: arrivals per XCD
     uint32_t critp[kGroups * kRunMaxR];     // split kernel: critical phases finished, per push block
     uint32_t bulkp[kGroups * kRunMaxR];     // split kernel: bulk phases finished, per push block
+    uint32_t pushp[kGroups * kRunMaxR];     // unsplit kernel: push phases finished, per push block
     uint32_t start, pad0[kCtlStride - 1];   // placement barrier
     uint32_t gcnt, pad1[kCtlStride - 1];    // grid barrier: XCDs complete
     uint32_t gen, pad2[kCtlStride - 1];     // grid barrier: released epoch

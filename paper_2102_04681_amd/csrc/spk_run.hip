@@ -59,6 +59,26 @@ __device__ bool spin_ge(const uint32_t *p, uint32_t target, uint32_t *abort_flag
     }
 }
 
+// Wait (one wave) until every one of the n <= 64 words p[0..n) has reached
+// target (wrap-safe); false if the wait gave up or another workgroup did.
+__device__ bool spin_all_ge(const uint32_t *p, uint32_t n, uint32_t target, uint32_t *abort_flag)
+{
+    const uint32_t lane = lane_id();
+    const uint64_t t0 = wall_clock64();
+    for (uint32_t k = 0;; k++) {
+        const uint32_t v = ld_ag(p + (lane < n ? lane : 0u));
+        if (__all(lane >= n || (int32_t)(v - target) >= 0)) return true;
+        if ((k & 31u) == 31u) {
+            if (ld_ag(abort_flag)) return false;
+            if (wall_clock64() - t0 > kSpinTicks) {
+                if (lane == 0) atomicOr(abort_flag, kRunAbortTimeout);
+                return false;
+            }
+        }
+        __builtin_amdgcn_s_sleep(1);
+    }
+}
+
 template <bool FIXED, bool CMP>
 struct RunLDS {
     using AccT = typename Acc<FIXED>::T;
@@ -154,18 +174,28 @@ __device__ bool grid_sync(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x, 
     return L.stop == 0;
 }
 
-// Barrier of the workgroups of one XCD; afterwards the compute unit's L1 is
-// invalidated so that plain loads see what the others stored in the L2.
-template <bool FIXED, bool CMP>
-__device__ bool xcd_sync(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x, uint32_t e)
+// End of a push phase (binned delivery): every thread's page and fill
+// stores have completed, then the block's progress word advances to e.
+__device__ void publish_push(const RunArgs &ra, uint32_t x, uint32_t r, uint32_t e)
 {
-    RunCtl *c = ra.ctl;
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    if (threadIdx.x == 0) {
-        atomicAdd(&c->lx[x * kCtlStride], 1u);
-        L.stop = spin_ge(&c->lx[x * kCtlStride], ra.R * e, &c->abort_flag) ? 0u : 1u;
-        if (L.stop) atomicOr(ra.s.flags, kRunStoppedFlag);
+    if (threadIdx.x == 0) st_ag(&ra.ctl->pushp[x * kRunMaxR + r], e);
+}
+
+// Start of a tile phase (binned delivery): the first wave waits until every
+// push block of the XCD has finished push phase e; then the compute unit's L1
+// is invalidated so that plain loads see the pages in the XCD's L2.
+template <bool FIXED, bool CMP>
+__device__ bool wait_pushes(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x, uint32_t e)
+{
+    RunCtl *c = ra.ctl;
+    if (threadIdx.x < kWave) {
+        const bool ok = spin_all_ge(&c->pushp[x * kRunMaxR], ra.R, e, &c->abort_flag);
+        if (threadIdx.x == 0) {
+            L.stop = ok ? 0u : 1u;
+            if (!ok) atomicOr(ra.s.flags, kRunStoppedFlag);
+        }
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
         __builtin_amdgcn_s_waitcnt(0);
     }
@@ -743,6 +773,8 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
         s += Db;
         const bool more = s < ra.n_steps;
         if (has_tile) {
+            // binned: every push block of the XCD has filed the previous batch
+            if (!DIRECT && !wait_pushes(ra, L, x, ex)) return;
             // the push phase reused this LDS: accumulators restart at zero, and
             // the spike count of the previous step has been read by every thread
             for (uint32_t q = tid; q < Db * tl.W; q += kRunThreads) L.u.t.acc[q] = 0;
@@ -777,7 +809,7 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
             if (a.raster_cap)
                 for (uint32_t u = 0; u < Db; u++)
                     rbase = raster_advance(a, t_first + u, rbase, Db == 1 ? M : L.mstep[u], x == 0 && r == 0);
-            if (!xcd_sync(ra, L, x, ++ex)) return;
+            publish_push(ra, x, r, ++ex);  // the tiles of the XCD wait for it (wait_pushes)
         }
     }
 
