@@ -88,7 +88,7 @@ struct RunLDS {
     // persistent for the whole launch
     float V[kMaxTileW];
     uint8_t ref[kMaxTileW];     // LIF: refractory steps left; source: fires at the current step
-    uint8_t kp[kMaxTileW];      // Poisson count of the current step
+    uint8_t kp[kMaxTileW];      // Poisson counts: of the current step, or of step u of a batch at u * W
     uint64_t pois[256];
     uint16_t guide[256];
     uint32_t fill[kRunMaxFill]; // push block: records in each of its pages, (arrival slot, tile)
@@ -121,27 +121,34 @@ struct RunLDS {
     uint32_t ws[16], ws2[16];
     unsigned long long ws64[16];
     uint32_t mstep[kRunMaxD];   // spikes of each step of the last pushed batch
-    uint32_t nspk, x, r, stop;
+    uint32_t nspk2[2];          // spike counters of the update, alternating between steps
+    uint32_t x, r, stop;
+    // the neuron model's constants, read by the update from here into vector
+    // registers (kept in scalar registers they spill across the long kernel)
+    float mk, v_rest, v_th, v_reset, i_bias, ext_w;
+    int32_t ext_wq, bias_q, shift, shift64;
+    uint32_t ref_steps, pois_len;
 };
 
-// Per-step draws of the tile's neurons for step t: the Poisson count and, for
-// source neurons, whether they fire.  They do not depend on the network's
+// Per-step draws of the tile's neurons for steps t .. t + nsteps - 1: the
+// Poisson count of step t + u at kp[u * W + q] and, for source neurons (one
+// step at a time), whether they fire.  They do not depend on the network's
 // activity, so they are computed while the workgroup waits at a barrier.
 template <bool FIXED, bool CMP>
 __device__ void run_draws(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t tile_lo, uint32_t tile_n,
-                          uint64_t t)
+                          uint64_t t, uint32_t nsteps)
 {
     const ModelArgs &m = a.m;
-#pragma unroll
-    for (int u = 0; u < kRunRounds; u++) {
-        const uint32_t q = u * kRunThreads + threadIdx.x;
+    const uint32_t logW = a.tl.logW, W = a.tl.W;
+    for (uint32_t e = threadIdx.x; e < nsteps * W; e += kRunThreads) {
+        const uint32_t u = e >> logW, q = e & (W - 1);
         if (q >= tile_n) continue;
         const uint32_t gi = tile_lo + q;
         if (m.pois_len) {  // K = min { k : hi32 < T_k }, searched from the guide entry
-            const uint32_t h = hash_hi32(step_hash(m.keys.pois, gi, t));
+            const uint32_t h = hash_hi32(step_hash(m.keys.pois, gi, t + u));
             uint32_t k = L.guide[h >> 24];
             while ((uint64_t)h >= L.pois[k]) k++;
-            L.kp[q] = (uint8_t)k;
+            L.kp[e] = (uint8_t)k;
         }
         if (m.kind == SPK_SOURCE)
             L.ref[q] = (uint64_t)hash_hi32(step_hash(m.keys.bern, gi, t)) < m.src_thr ? 1 : 0;
@@ -153,7 +160,7 @@ __device__ void run_draws(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t til
 // Between arriving and waiting, the workgroup computes the next step's draws.
 template <bool FIXED, bool CMP>
 __device__ bool grid_sync(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x, uint32_t e, bool draws,
-                          uint32_t tile_lo, uint32_t tile_n, uint64_t t_draw)
+                          uint32_t tile_lo, uint32_t tile_n, uint64_t t_draw, uint32_t n_draw)
 {
     RunCtl *c = ra.ctl;
     __builtin_amdgcn_s_waitcnt(0);  // this thread's stores have completed
@@ -165,7 +172,7 @@ __device__ bool grid_sync(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x, 
             if (g == kGroups * e - 1) st_ag(&c->gen, e);
         }
     }
-    if (draws) run_draws(ra.s, L, tile_lo, tile_n, t_draw);
+    if (draws) run_draws(ra.s, L, tile_lo, tile_n, t_draw, n_draw);
     if (threadIdx.x == 0) {
         L.stop = spin_ge(&c->gen, e, &c->abort_flag) ? 0u : 1u;
         if (L.stop) atomicOr(ra.s.flags, kRunStoppedFlag);
@@ -333,11 +340,17 @@ __device__ void run_drain(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t x, 
 // the tile's segment of the spike list of t.
 template <bool FIXED, bool CMP, bool DIRECT>
 __device__ void run_update(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x, uint32_t tile,
-                           uint32_t tile_lo, uint32_t tile_n, uint64_t t, uint64_t delivered, uint32_t aoff)
+                           uint32_t tile_lo, uint32_t tile_n, uint64_t t, uint64_t delivered, uint32_t aoff,
+                           uint32_t kpoff, uint32_t *cnt, uint32_t *cnt_next)
 {
     const StepArgs &a = ra.s;
     const ModelArgs &m = a.m;
     const uint32_t tid = threadIdx.x, lane = lane_id();
+    // the model's constants from LDS (vector registers), see RunLDS
+    const float mk = L.mk, v_rest = L.v_rest, v_th = L.v_th, v_reset = L.v_reset, i_bias = L.i_bias,
+                ext_w = L.ext_w;
+    const int32_t ext_wq = L.ext_wq, bias_q = L.bias_q, shift = L.shift, shift64 = L.shift64;
+    const uint32_t ref_steps = L.ref_steps, pois_len = L.pois_len;
     uint64_t ev = 0;
     uint64_t bal[kRunRounds];  // per round: the wave's firing lanes (wave-uniform)
     uint32_t nw_spk = 0;       // the wave's spikes over all rounds
@@ -346,20 +359,20 @@ __device__ void run_update(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x,
         const uint32_t q = u * kRunThreads + tid;
         bool spk = false;
         if (q < tile_n) {
-            const uint32_t K = m.pois_len ? L.kp[q] : 0u;
+            const uint32_t K = pois_len ? L.kp[kpoff + q] : 0u;
             float I;
             if (FIXED) {
-                const int32_t qt = (int32_t)L.u.t.acc[aoff + q] + (int32_t)K * m.ext_wq + m.bias_q;
-                I = ldexpf((float)qt, -m.shift);
+                const int32_t qt = (int32_t)L.u.t.acc[aoff + q] + (int32_t)K * ext_wq + bias_q;
+                I = ldexpf((float)qt, -shift);
             } else {
-                const float isyn = fixed64_to_float(L.u.t.acc[aoff + q], m.shift64);
-                const float ext = __fmul_rn((float)K, m.ext_w);
-                I = __fadd_rn(__fadd_rn(isyn, ext), m.i_bias);
+                const float isyn = fixed64_to_float(L.u.t.acc[aoff + q], shift64);
+                const float ext = __fmul_rn((float)K, ext_w);
+                I = __fadd_rn(__fadd_rn(isyn, ext), i_bias);
             }
             float V = L.V[q];
             if (m.kind == SPK_SOURCE) {
-                const float av = __fsub_rn(m.v_rest, V);
-                const float bv = __fmul_rn(m.k, av);
+                const float av = __fsub_rn(v_rest, V);
+                const float bv = __fmul_rn(mk, av);
                 const float cv = __fadd_rn(V, bv);
                 V = __fadd_rn(cv, I);
                 spk = L.ref[q] != 0;
@@ -367,16 +380,16 @@ __device__ void run_update(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x,
                 uint32_t r = L.ref[q];
                 if (r > 0) {
                     r -= 1;
-                    V = m.v_reset;
+                    V = v_reset;
                 } else {
-                    const float av = __fsub_rn(m.v_rest, V);
-                    const float bv = __fmul_rn(m.k, av);
+                    const float av = __fsub_rn(v_rest, V);
+                    const float bv = __fmul_rn(mk, av);
                     const float cv = __fadd_rn(V, bv);
                     V = __fadd_rn(cv, I);
-                    if (V >= m.v_th) {
+                    if (V >= v_th) {
                         spk = true;
-                        V = m.v_reset;
-                        r = m.ref_steps;
+                        V = v_reset;
+                        r = ref_steps;
                     }
                 }
                 L.ref[q] = (uint8_t)r;
@@ -391,7 +404,7 @@ __device__ void run_update(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x,
     // lanes at consecutive positions
     if (nw_spk) {
         uint32_t wb = 0;
-        if (lane == 0) wb = atomicAdd(&L.nspk, nw_spk);
+        if (lane == 0) wb = atomicAdd(cnt, nw_spk);
         wb = __shfl(wb, 0);
 #pragma unroll
         for (int u = 0; u < kRunRounds; u++) {
@@ -406,7 +419,10 @@ __device__ void run_update(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x,
     }
     if (DIRECT) ev = block_sum_u64(ev, L.ws64);
     else lds_sync();
-    const uint32_t ns = L.nspk;
+    const uint32_t ns = *cnt;
+    // the other counter, last read before the barrier that began this step,
+    // restarts at zero for the next step
+    if (tid == 0) *cnt_next = 0;
     const uint64_t seg = (uint64_t)(t % a.spk_slots) * a.tl.T + tile;
     uint32_t *dst = a.spk_ids + seg * a.tl.W;
     for (uint32_t q = tid; q < ns; q += kRunThreads) st_ag(dst + q, tile_lo + L.u.t.spk[q]);
@@ -708,12 +724,25 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
 
     // placement: the XCD this workgroup runs on, and a ticket within it
     if (tid == 0) {
+        const ModelArgs &mm = ra.s.m;
+        L.mk = mm.k;
+        L.v_rest = mm.v_rest;
+        L.v_th = mm.v_th;
+        L.v_reset = mm.v_reset;
+        L.i_bias = mm.i_bias;
+        L.ext_w = mm.ext_w;
+        L.ext_wq = mm.ext_wq;
+        L.bias_q = mm.bias_q;
+        L.shift = mm.shift;
+        L.shift64 = mm.shift64;
+        L.ref_steps = mm.ref_steps;
+        L.pois_len = mm.pois_len;
         const uint32_t raw = xcc_id();
         const uint32_t x = raw & (kGroups - 1);
         if (raw >= kGroups) atomicOr(&ctl->abort_flag, kRunAbortPlacement);
         L.x = x;
         L.r = atomicAdd(&ctl->ticket[x * kCtlStride], 1u);
-        L.nspk = 0;
+        L.nspk2[0] = 0;
         atomicAdd(&ctl->start, 1u);
         L.stop = spin_ge(&ctl->start, gridDim.x, &ctl->abort_flag) ? 0u : 1u;
         if (L.stop) atomicOr(a.flags, kRunStoppedFlag);
@@ -756,7 +785,10 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
         }
     }
     __syncthreads();
-    if (ra.n_steps) run_draws(a, L, tile_lo, tile_n, ra.t0);
+    // LIF neurons: the draws of a whole batch at once (source neurons: of one step)
+    const bool lif = m.kind != SPK_SOURCE;
+    const uint32_t Dd = DIRECT || !lif ? 1u : ra.D;
+    if (ra.n_steps) run_draws(a, L, tile_lo, tile_n, ra.t0, (uint32_t)(ra.n_steps < Dd ? ra.n_steps : Dd));
     uint64_t rbase = a.raster_cap ? a.raster_offs[ra.t0] : 0;
     uint32_t eg = 0, ex = 0;
     __syncthreads();
@@ -778,21 +810,21 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
             // the push phase reused this LDS: accumulators restart at zero, and
             // the spike count of the previous step has been read by every thread
             for (uint32_t q = tid; q < Db * tl.W; q += kRunThreads) L.u.t.acc[q] = 0;
-            if (tid == 0) L.nspk = 0;
+            if (tid == 0) L.nspk2[0] = 0;
             if (!DIRECT) run_drain(a, L, x, r, tile, tile_n, t_first, Db);  // all steps of the batch
             for (uint32_t u = 0; u < Db; u++) {
                 const uint64_t t = t_first + u;
-                if (u) {  // the draws of t; the spike list of t - 1 has been read by every thread
-                    run_draws(a, L, tile_lo, tile_n, t);
-                    __syncthreads();
-                    if (tid == 0) L.nspk = 0;
+                if (u) {  // the spike list of t - 1 (LDS) has been published by every thread
+                    if (!lif) run_draws(a, L, tile_lo, tile_n, t, 1);
                     __syncthreads();
                 }
                 const uint64_t delivered = DIRECT ? run_gather(a, L, tile, tile_lo, t) : L.u.t.dlv[u];
-                run_update<FIXED, CMP, DIRECT>(ra, L, x, tile, tile_lo, tile_n, t, delivered, u * tl.W);
+                run_update<FIXED, CMP, DIRECT>(ra, L, x, tile, tile_lo, tile_n, t, delivered, u * tl.W,
+                                               lif ? u * tl.W : 0u, &L.nspk2[u & 1u], &L.nspk2[(u + 1u) & 1u]);
             }
         }
-        if (!grid_sync(ra, L, x, ++eg, has_tile && more, tile_lo, tile_n, t_first + Db)) return;
+        const uint32_t Dn = (uint32_t)(ra.n_steps - s < Dd ? ra.n_steps - s : Dd);  // (0 after the last batch)
+        if (!grid_sync(ra, L, x, ++eg, has_tile && more, tile_lo, tile_n, t_first + Db, Dn)) return;
         if (DIRECT) {
             const uint64_t t = t_first;
             if (a.raster_cap) {  // the spike list of t is complete: workgroup (0, 0) records it

@@ -243,6 +243,7 @@ RUN_CASES = [
     ("C1-6000", lambda: I.scaled(1, 6000), 300),
     ("C2-6000", lambda: I.scaled(2, 6000, k_in_exc=480, k_in_inh=120), 300),
     ("C3-20000", lambda: I.scaled(3, 20000, k_out=1000), 100),
+    ("C3-d4-6", lambda: I.scaled(3, 20000, k_out=1000, delay_min=4, delay_max=6), 100),
     ("C4-12000", lambda: I.scaled(4, 12000, k_out=1500), 400),
     ("C4-d3-9", lambda: I.scaled(4, 12000, k_out=1500, delay_min=3, delay_max=9), 300),
     ("C0-literal", lambda: I.config(0, seed=1), 200),
