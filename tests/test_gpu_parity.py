@@ -338,18 +338,23 @@ def test_fixed_point_simulation_bit_identical(spk, name, mk, T, delivery, mode, 
 @pytest.mark.parametrize("acc", [I.ACC_F32, I.ACC_FIXED], ids=["f32", "fixed"])
 @pytest.mark.parametrize("fmt", [f for f, _ in FORMATS], ids=[n for _, n in FORMATS])
 @pytest.mark.parametrize("step_mode,split", [(1, "1"), (2, "1"), (2, "0")], ids=["graph", "persist", "unsplit"])
-def test_bin_overflow_fallback(spk, acc, fmt, step_mode, split, monkeypatch):
+@pytest.mark.parametrize("delays", [(1, 1), (2, 4)], ids=["d1", "d2-4"])
+def test_bin_overflow_fallback(spk, acc, fmt, step_mode, split, delays, monkeypatch):
     # 64 neurons, 200 synapses each (multapses), all above threshold at t=0:
-    # the one tile receives 12 800 events at step 1, ~400 per push block,
-    # while every page is capped at 64 records, so the global-atomic
-    # fallback must deliver the rest (in the simulation and in debug_deliver).
+    # the one tile receives 12 800 events (delay 1; with delays 2-4, spread
+    # over three arrival steps of batches of 2), ~400 per push block, while
+    # every page is capped at 64 records, so the global-atomic fallback must
+    # deliver the rest (in the simulation and in debug_deliver).
     monkeypatch.setenv("SPK_PAGE_CAP", "64")
     monkeypatch.setenv("SPK_PERSISTENT_SPLIT", split)
-    cfg = I.config(4, n=64, k_out=200, delay_min=1, delay_max=1, v0_lo=-49.0, v0_hi=-49.0,
+    cfg = I.config(4, n=64, k_out=200, delay_min=delays[0], delay_max=delays[1], v0_lo=-49.0, v0_hi=-49.0,
                    t_ref_ms=0.0, acc_mode=acc, delivery=2, syn_format=fmt, step_mode=step_mode)
-    T = 6
+    T = 9
     g = spk.Net(cfg, max_steps=T, raster_capacity=64 * T)
-    assert g.stats()["page_cap"] == 64
+    st = g.stats()
+    assert st["page_cap"] == 64
+    if step_mode == 2 and split == "0":
+        assert st["batch_steps"] == delays[0]
     spikes = np.arange(64, dtype=np.uint32)
     got = g.debug_deliver(spikes)
     o = oracle.Net(cfg)
@@ -363,6 +368,12 @@ def test_bin_overflow_fallback(spk, acc, fmt, step_mode, split, monkeypatch):
         want = o.deliver(spikes)
         ulp = np.spacing(np.abs(want).astype(np.float32)).astype(np.float64)
         assert np.all(np.abs(got - want) <= ulp)
+        # fp32 sums are exact: the simulation equals the graph path's bit for bit
+        g.step(T)
+        ref = spk.Net(dict(cfg, step_mode=1), max_steps=T, raster_capacity=64 * T)
+        ref.step(T)
+        assert np.array_equal(g.raster()[1], ref.raster()[1])
+        assert np.array_equal(g.state()[0].view(np.uint32), ref.state()[0].view(np.uint32))
 
 
 @pytest.mark.parametrize("delays", [(1, 20), (3, 9), (15, 15)], ids=["d1-20", "d3-9", "d15"])
