@@ -431,6 +431,65 @@ __global__ __launch_bounds__(kBlock) void k_in_abs_sum(const void *syn, uint64_t
     }
 }
 
+// Largest sum of |weight| into any neuron of a Bernoulli network, with no
+// atomic per synapse: thread j evaluates the connection predicate of every
+// source s of its block's source range into j (the generator's hash of the
+// pair) and adds the term of each synapse it finds, in the units of
+// k_in_abs_sum; the sources' row keys are staged in LDS.  One source range
+// (grid.y = 1): a block's largest sum goes to *out by one atomic; several
+// (small networks, to fill the device): partial sums go to insum[j].
+// Cost: n^2 hashes (one pass of the generator), against nnz global atomics.
+__device__ __forceinline__ unsigned long long abs_term(const ConnArgs &c, uint32_t src, uint64_t hw)
+{
+    const float w = syn_weight(c, src, hw);
+    if (c.fixed) {
+        const int32_t q = weight_bits(c, w);
+        return (unsigned long long)(q < 0 ? -(long long)q : (long long)q);
+    }
+    return (unsigned long long)ceil(ldexp((double)fabsf(w), 24));
+}
+
+__global__ __launch_bounds__(kBlock) void k_bern_in_abs_max(ConnArgs c, uint32_t src_chunk, unsigned long long *out,
+                                                           unsigned long long *insum)
+{
+    __shared__ uint64_t rk[kBlock], rw[kBlock];
+    __shared__ unsigned long long wmax[kBlock / kWave];
+    const uint32_t j = blockIdx.x * kBlock + threadIdx.x;
+    const uint32_t sb = blockIdx.y * src_chunk;
+    const uint32_t se = c.n - sb < src_chunk ? c.n : sb + src_chunk;
+    const unsigned long long te = abs_term(c, 0, 0), ti = abs_term(c, c.n_exc, 0);  // population weights
+    unsigned long long sum = 0;
+    for (uint32_t s0 = sb; s0 < se; s0 += kBlock) {
+        __syncthreads();
+        const uint64_t sl = (uint64_t)s0 + threadIdx.x;
+        rk[threadIdx.x] = mix64(c.keys.conn ^ sl);
+        rw[threadIdx.x] = mix64(c.keys.w ^ sl);
+        __syncthreads();
+        const uint32_t ns = se - s0 < kBlock ? se - s0 : kBlock;
+        if (j >= c.n) continue;
+        for (uint32_t k = 0; k < ns; k++) {
+            if (!((uint64_t)hash_hi32(mix64(rk[k] ^ (uint64_t)j)) < c.conn_thr)) continue;
+            const uint32_t src = s0 + k;
+            sum += c.w_uniform ? abs_term(c, src, mix64(rw[k] ^ (uint64_t)j)) : (src < c.n_exc ? te : ti);
+        }
+    }
+    if (gridDim.y > 1) {
+        if (j < c.n && sum) atomicAdd(&insum[j], sum);
+        return;
+    }
+    for (int o = 32; o > 0; o >>= 1) {
+        const unsigned long long y = __shfl_xor(sum, o);
+        sum = y > sum ? y : sum;
+    }
+    if (lane_id() == 0) wmax[threadIdx.x / kWave] = sum;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        unsigned long long mx = 0;
+        for (uint32_t k = 0; k < kBlock / kWave; k++) mx = wmax[k] > mx ? wmax[k] : mx;
+        if (mx) atomicMax(out, mx);
+    }
+}
+
 __global__ __launch_bounds__(kBlock) void k_max_u64(const uint64_t *x, uint64_t m,
                                                    unsigned long long *out)
 {
@@ -592,6 +651,29 @@ hipError_t in_abs_sum(const void *syn, uint64_t nnz, bool fixed, bool compact, c
     hipLaunchKernelGGL(k_in_abs_sum, dim3(grid_for(nnz, 65536)), dim3(kBlock), 0, s, syn, nnz,
                        fixed ? 1 : 0, compact ? 1 : 0, tab, (unsigned long long *)insum);
     return hipGetLastError();
+}
+
+uint32_t bern_src_ranges(uint32_t n)
+{
+    // about 4096 blocks: split the sources when the targets alone give fewer
+    const uint32_t tb = (n + kBlock - 1) / kBlock;
+    uint32_t S = (4096 + tb - 1) / tb;
+    S = S < 1 ? 1 : (S > 64 ? 64 : S);
+    return S;
+}
+
+hipError_t bern_in_abs_max(const ConnArgs &c, uint64_t *out, uint64_t *insum, hipStream_t s)
+{
+    if (c.kind != SPK_CONN_BERNOULLI) return hipErrorInvalidValue;
+    const uint32_t S = bern_src_ranges(c.n);
+    const uint32_t chunk = ((c.n + S - 1) / S + kBlock - 1) / kBlock * kBlock;
+    const uint32_t Sused = chunk ? (c.n + chunk - 1) / chunk : 1;
+    if (Sused > 1 && !insum) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_bern_in_abs_max, dim3(grid_for(c.n), Sused ? Sused : 1), dim3(kBlock), 0, s, c, chunk,
+                       (unsigned long long *)out, (unsigned long long *)insum);
+    hipError_t e = hipGetLastError();
+    if (e == hipSuccess && Sused > 1) e = max_u64(insum, c.n, out, s);
+    return e;
 }
 
 hipError_t max_u64(const uint64_t *x, uint64_t m, uint64_t *out, hipStream_t s)

@@ -254,6 +254,11 @@ struct ClassTab {
 hipError_t in_abs_sum(const void *syn, uint64_t nnz, bool fixed, bool compact, const ClassTab &tab,
                       uint64_t *insum, hipStream_t s);
 hipError_t max_u64(const uint64_t *x, uint64_t m, uint64_t *out, hipStream_t s);
+// Bernoulli networks: the largest in_abs_sum over neurons, by evaluating the
+// pair predicate per target (no atomic per synapse); *out must be zero on
+// entry, and so must insum (n entries), needed when bern_src_ranges(n) > 1.
+uint32_t bern_src_ranges(uint32_t n);
+hipError_t bern_in_abs_max(const ConnArgs &c, uint64_t *out, uint64_t *insum, hipStream_t s);
 hipError_t init_state(const ModelArgs &m, float v0_lo, float v0_hi, float *V, uint8_t *ref,
                       hipStream_t s);
 hipError_t export_gather(const uint64_t *row_ptr, const void *syn, bool compact, const ClassTab &tab,

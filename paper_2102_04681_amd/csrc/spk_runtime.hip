@@ -383,6 +383,17 @@ spk_status choose_format(spk_net *net, const float *classes, uint32_t n_cls)
     return SPK_OK;
 }
 
+// How the accumulator range of a generated Bernoulli network is found: per
+// target from the pair predicate (n^2 hashes, ~1.7e12 per s) when that costs
+// less than one global atomic per synapse (~2.4e10 per s).
+// SPK_RANGE_PASS=targets / atomics forces either (a tuning knob, for tests).
+bool range_by_targets(const spk_net *net)
+{
+    if (net->P.conn_kind != SPK_CONN_BERNOULLI) return false;
+    if (const char *e = std::getenv("SPK_RANGE_PASS")) return std::strcmp(e, "targets") == 0;
+    return (double)net->nnz * 70.0 > (double)net->n * (double)net->n;
+}
+
 // The term of one synapse of weight w in the accumulator-range bound, as the
 // range pass computes it: |quantised w| (fixed mode) or |w| in units of
 // 2^-24 rounded up (fp32 mode).
@@ -601,6 +612,24 @@ spk_status finish_rows(spk_net *net)
         SPK_TRY(abs_term(net, net->P.w_exc, &te));
         SPK_TRY(abs_term(net, net->P.w_inh, &ti));
         m = (uint64_t)net->P.k_in_exc * te + (uint64_t)net->P.k_in_inh * ti;
+    } else if (range_by_targets(net)) {
+        // Bernoulli: the pair predicate evaluated per target (n^2 hashes)
+        // costs less than a global atomic per synapse above ~1.4 % density
+        uint64_t *mx = nullptr, *insum = nullptr;
+        SPK_TRY(dalloc(net, &mx, 1));
+        SPK_HIP(hipMemsetAsync(mx, 0, 8, s));
+        if (bern_src_ranges(net->n) > 1) {
+            SPK_TRY(dalloc(net, &insum, net->n));
+            SPK_HIP(hipMemsetAsync(insum, 0, (size_t)net->n * 8, s));
+        }
+        SegTimer tm;
+        SPK_HIP(tm.start(s));
+        SPK_HIP(bern_in_abs_max(conn_args(net), mx, insum, s));
+        SPK_HIP(tm.stop(s, &net->range_ms));
+        SPK_HIP(hipMemcpyAsync(&m, mx, 8, hipMemcpyDeviceToHost, s));
+        SPK_HIP(hipStreamSynchronize(s));
+        dfree(net, mx);
+        if (insum) dfree(net, insum);
     } else {
         uint64_t *insum = nullptr, *mx = nullptr;
         SPK_TRY(dalloc(net, &insum, net->n));

@@ -474,6 +474,39 @@ def test_fixed_point_guard_fixed_in_degree(spk):
             assert e.value.code == spk.SPK_EOVERFLOW
 
 
+@pytest.mark.parametrize("w_uniform", [0, 1], ids=["population", "per-synapse"])
+def test_range_pass_per_target_matches_oracle(spk, w_uniform, monkeypatch):
+    # Bernoulli networks: the largest per-neuron sum of |quantised weights|
+    # is found per target from the pair predicate (no atomics) or with one
+    # atomic per synapse; both must refuse exactly the networks the oracle
+    # refuses.  Weights are scaled so that the oracle's largest sum lands
+    # just inside and just outside int32.
+    base = dict(n=800, p=0.05, acc_mode=I.ACC_FIXED, fixed_shift=20, ext_lambda=0.0, ext_w=0.0)
+    if w_uniform:
+        base.update(w_uniform=1, w_lo=-1.0, w_hi=1.0)
+    probe = oracle.Net(I.config(0, **base))
+    m1 = int(probe.in_abs_sum_q().max())  # at unit scale
+    assert m1 > 0
+    for scale, fits in ((0.999, True), (1.001, False)):
+        f = scale * (2**31 - 1) / m1
+        over = dict(base, w_lo=-f, w_hi=f) if w_uniform else dict(base, w_exc=0.27 * f, w_inh=-4.5 * f)
+        cfg = I.config(0, **over)
+        try:
+            ok = int(oracle.Net(cfg).in_abs_sum_q().max()) <= 2**31 - 1
+        except oracle.OracleError as e:
+            assert e.code == -4
+            ok = False
+        assert ok == fits
+        for mode in ("targets", "atomics"):
+            monkeypatch.setenv("SPK_RANGE_PASS", mode)
+            if fits:
+                spk.Net(cfg, max_steps=1)
+            else:
+                with pytest.raises(spk.SpkError) as e:
+                    spk.Net(cfg, max_steps=1)
+                assert e.value.code == spk.SPK_EOVERFLOW
+
+
 @pytest.mark.parametrize("seed", [1, 2])
 def test_fp32_mode_mean_rate_within_one_percent(spk, seed):
     # fp32 atomics: spike trains diverge after the first rounding
