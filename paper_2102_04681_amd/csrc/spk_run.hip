@@ -9,12 +9,17 @@
 //   - each workgroup keeps its tile's membrane potentials, refractory
 //     counters and the next step's Poisson draws in LDS for the whole launch,
 //     and (as a push block) the fill counters of the pages it owns;
-//   - the two hand-offs of a step are barriers inside the kernel instead of
+//   - the two hand-offs of a step happen inside the kernel instead of at
 //     kernel boundaries.  After the tiles publish the spike list of t, a grid
-//     barrier; after the push blocks of an XCD have filed their events, a
-//     barrier of that XCD's workgroups only, because every page is written
-//     and read on one XCD (its L2 is the point of coherence, so only the
-//     compute units' L1 caches are invalidated there).
+//     barrier; after a push block of an XCD has filed its events, it advances
+//     its progress word, and a tile starts its next drain once the 32 words
+//     of its XCD have advanced: every page is written and read on one XCD
+//     (its L2 is the point of coherence, so only the compute unit's L1 is
+//     invalidated there);
+//   - with binned delivery and a smallest delay of D >= 2 steps, steps run in
+//     batches of D: nothing filed in a batch arrives within it, so the tile
+//     drains the batch's D arrival slots at once and runs its D updates back
+//     to back, and one push phase files the events of all D steps' spikes.
 // Workgroups find their XCD from the hardware register and take a ticket
 // within it, so the group of tiles a workgroup serves is always on the XCD it
 // runs on.  Spike lists cross XCDs through agent-scope loads and stores.
