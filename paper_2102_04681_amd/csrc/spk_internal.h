@@ -211,6 +211,7 @@ struct RunCtl {
     uint32_t critp[kGroups * kRunMaxR];     // split kernel: critical phases finished, per push block
     uint32_t bulkp[kGroups * kRunMaxR];     // split kernel: bulk phases finished, per push block
     uint32_t pushp[kGroups * kRunMaxR];     // unsplit kernel: push phases finished, per push block
+    uint32_t tilep[kGroups * kRunMaxR];     // unsplit kernel, binned: tile phases published, per tile
     uint32_t start, pad0[kCtlStride - 1];   // placement barrier
     uint32_t gcnt, pad1[kCtlStride - 1];    // grid barrier: XCDs complete
     uint32_t gen, pad2[kCtlStride - 1];     // grid barrier: released epoch

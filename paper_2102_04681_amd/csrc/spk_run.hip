@@ -10,12 +10,14 @@
 //     counters and the next step's Poisson draws in LDS for the whole launch,
 //     and (as a push block) the fill counters of the pages it owns;
 //   - the two hand-offs of a step happen inside the kernel instead of at
-//     kernel boundaries.  After the tiles publish the spike list of t, a grid
-//     barrier; after a push block of an XCD has filed its events, it advances
-//     its progress word, and a tile starts its next drain once the 32 words
-//     of its XCD have advanced: every page is written and read on one XCD
-//     (its L2 is the point of coherence, so only the compute unit's L1 is
-//     invalidated there);
+//     kernel boundaries, through progress words (binned delivery): a tile
+//     advances its word once it has published its spike list of t, and the
+//     push blocks start once every tile's word has advanced; a push block
+//     advances its word once it has filed its events, and a tile starts its
+//     next drain once the 32 words of its XCD have advanced: every page is
+//     written and read on one XCD (its L2 is the point of coherence, so only
+//     the compute unit's L1 is invalidated there).  Direct delivery has one
+//     hand-off per step, a grid barrier;
 //   - with binned delivery and a smallest delay of D >= 2 steps, steps run in
 //     batches of D: nothing filed in a batch arrives within it, so the tile
 //     drains the batch's D arrival slots at once and runs its D updates back
@@ -127,6 +129,7 @@ struct RunLDS {
     unsigned long long ws64[16];
     uint32_t mstep[kRunMaxD];   // spikes of each step of the last pushed batch
     uint32_t nspk2[2];          // spike counters of the update, alternating between steps
+    uint32_t pstop[4];          // wait_tiles: a polling wave gave up
     uint32_t x, r, stop;
     // the neuron model's constants, read by the update from here into vector
     // registers (kept in scalar registers they spill across the long kernel)
@@ -193,6 +196,38 @@ __device__ void publish_push(const RunArgs &ra, uint32_t x, uint32_t r, uint32_t
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (threadIdx.x == 0) st_ag(&ra.ctl->pushp[x * kRunMaxR + r], e);
+}
+
+// End of a tile phase (binned delivery): every thread's spike-list stores
+// have completed, then the tile's progress word advances to e.
+__device__ void publish_tile(const RunArgs &ra, uint32_t tile, uint32_t e)
+{
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0) st_ag(&ra.ctl->tilep[tile], e);
+}
+
+// Start of a push phase (binned delivery): waves 0-3 wait until the progress
+// word of every tile (64 per wave) has reached e: then every spike list of
+// the batch is complete, and every tile has drained the pages of the batch's
+// arrival steps, which this push phase may start to refill.
+template <bool FIXED, bool CMP>
+__device__ bool wait_tiles(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t e)
+{
+    RunCtl *c = ra.ctl;
+    const uint32_t T = ra.s.tl.T, w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+    if (w * kWave < T) {
+        const uint32_t n = T - w * kWave < kWave ? T - w * kWave : kWave;
+        const bool ok = spin_all_ge(&c->tilep[w * kWave], n, e, &c->abort_flag);
+        if (lane_id() == 0) {
+            L.pstop[w] = ok ? 0u : 1u;
+            if (!ok) atomicOr(ra.s.flags, kRunStoppedFlag);
+        }
+    }
+    __syncthreads();
+    uint32_t stop = 0;
+    for (uint32_t k = 0; k * kWave < T; k++) stop |= L.pstop[k];
+    return stop == 0;
 }
 
 // Start of a tile phase (binned delivery): the first wave waits until every
@@ -829,7 +864,14 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
             }
         }
         const uint32_t Dn = (uint32_t)(ra.n_steps - s < Dd ? ra.n_steps - s : Dd);  // (0 after the last batch)
-        if (!grid_sync(ra, L, x, ++eg, has_tile && more, tile_lo, tile_n, t_first + Db, Dn)) return;
+        if (DIRECT) {
+            if (!grid_sync(ra, L, x, ++eg, has_tile && more, tile_lo, tile_n, t_first + Db, Dn)) return;
+        } else {  // binned: the tiles' progress words instead of a grid barrier
+            ++eg;
+            if (has_tile) publish_tile(ra, tile, eg);
+            if (has_tile && more) run_draws(a, L, tile_lo, tile_n, t_first + Db, Dn);  // while the others finish
+            if (!wait_tiles(ra, L, eg)) return;
+        }
         if (DIRECT) {
             const uint64_t t = t_first;
             if (a.raster_cap) {  // the spike list of t is complete: workgroup (0, 0) records it
