@@ -147,19 +147,22 @@ __device__ void run_draws(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t til
                           uint64_t t, uint32_t nsteps)
 {
     const ModelArgs &m = a.m;
-    const uint32_t logW = a.tl.logW, W = a.tl.W;
-    for (uint32_t e = threadIdx.x; e < nsteps * W; e += kRunThreads) {
-        const uint32_t u = e >> logW, q = e & (W - 1);
-        if (q >= tile_n) continue;
-        const uint32_t gi = tile_lo + q;
-        if (m.pois_len) {  // K = min { k : hi32 < T_k }, searched from the guide entry
-            const uint32_t h = hash_hi32(step_hash(m.keys.pois, gi, t + u));
-            uint32_t k = L.guide[h >> 24];
-            while ((uint64_t)h >= L.pois[k]) k++;
-            L.kp[e] = (uint8_t)k;
+    const uint32_t W = a.tl.W;
+    for (uint32_t u = 0; u < nsteps; u++) {
+#pragma unroll
+        for (int r = 0; r < kRunRounds; r++) {  // (unrolled: the rounds' hashes are independent)
+            const uint32_t q = r * kRunThreads + threadIdx.x;
+            if (q >= tile_n) continue;
+            const uint32_t gi = tile_lo + q;
+            if (m.pois_len) {  // K = min { k : hi32 < T_k }, searched from the guide entry
+                const uint32_t h = hash_hi32(step_hash(m.keys.pois, gi, t + u));
+                uint32_t k = L.guide[h >> 24];
+                while ((uint64_t)h >= L.pois[k]) k++;
+                L.kp[u * W + q] = (uint8_t)k;
+            }
+            if (m.kind == SPK_SOURCE)
+                L.ref[q] = (uint64_t)hash_hi32(step_hash(m.keys.bern, gi, t)) < m.src_thr ? 1 : 0;
         }
-        if (m.kind == SPK_SOURCE)
-            L.ref[q] = (uint64_t)hash_hi32(step_hash(m.keys.bern, gi, t)) < m.src_thr ? 1 : 0;
     }
 }
 
