@@ -124,7 +124,7 @@ enum { SPK_STEP_AUTO = 0, SPK_STEP_GRAPH = 1, SPK_STEP_PERSISTENT = 2 };
  *   SPK_PERSISTENT_SPLIT=0 / 1 forces the persistent kernel's variant (see
  *   spk_stats_t.persistent_split; default: split only when the smallest
  *   delay is >= 2 and steps cannot be batched); SPK_BATCH_STEPS caps the
- *   steps per batch (spk_stats_t.batch_steps). */
+ *   steps per batch (1..16, default 8; spk_stats_t.batch_steps). */
 typedef struct {
     uint32_t abi_version;      /* must be SPK_ABI_VERSION */
     uint32_t n;
@@ -171,7 +171,8 @@ typedef struct {
                                   chosen when the smallest delay is >= 2 steps */
     uint32_t batch_steps;      /* persistent kernel, binned delivery, unsplit: steps run as
                                   one batch (tile phases back to back, then one filing pass);
-                                  up to the smallest delay (at most 16), 1 otherwise */
+                                  up to the smallest delay (at most 8, or SPK_BATCH_STEPS up
+                                  to 16), 1 otherwise */
     /* Setup timing (Sec. IV-C): host wall time of the creating call, GPU time
      * (HIP events on the network's stream) of the connectivity generation
      * kernels (row counts, fill and regrouping; excludes allocation), and of the

@@ -120,14 +120,14 @@ def test_full_size_delay15_batch_sampled(spk_full):
     """The 1e9-synapse network with delay 15 (100,000 LIF, in-degree 8,000
     excitatory + 2,000 inhibitory, Poisson drive, fp32 accumulation) in the
     configuration bench.py --config 2 times: the persistent kernel in batches
-    of 15 steps.  After 300 steps, one more batch of 15 steps; for sampled
+    of 8 steps.  After 300 steps, one more batch; for sampled
     neurons the oracle draws the in-synapses (its per-target generator), sums
     the weights of those whose source fired 15 steps earlier exactly, and
-    runs its single-neuron update 15 times: every spike decision of the batch
+    runs its single-neuron update for each step: every spike decision of the batch
     and the final state must equal the library's bit for bit."""
     spk = spk_full
     cfg = I.config(2, driven=True)
-    n, D, d = cfg["n"], 15, cfg["delay_min"]
+    n, D, d = cfg["n"], 8, cfg["delay_min"]
     T0 = 300
     _say(f"[full c2] create n={n}")
     g = spk.Net(cfg, max_steps=T0 + D, raster_capacity=2_000_000)

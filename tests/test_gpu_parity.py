@@ -252,18 +252,18 @@ RUN_CASES = [
 
 # how the steps run: graph replay, plain launches with events (profiling),
 # the persistent kernel as chosen (binned delivery with a smallest delay >= 2:
-# the unsplit kernel in batches of up to 16 steps), the same with events
+# the unsplit kernel in batches of up to 8 steps), the same with events
 # around it, the split variant (SPK_PERSISTENT_SPLIT=1), the unsplit kernel,
-# and the unsplit kernel with batches capped at 1 and 4 steps
+# and the unsplit kernel with batches capped at 1, 4 and 16 steps
 # (SPK_BATCH_STEPS)
 MODES = [("graph", 1, False, "auto", None), ("launch", 1, True, "auto", None), ("persist", 2, False, "auto", None),
          ("persist-prof", 2, True, "auto", None), ("persist-split", 2, False, "1", None),
          ("persist-unsplit", 2, False, "0", None), ("persist-batch1", 2, False, "0", "1"),
-         ("persist-batch4", 2, False, "0", "4")]
+         ("persist-batch4", 2, False, "0", "4"), ("persist-batch16", 2, False, "0", "16")]
 
 
 def _expected_batch(cfg, batch):
-    return min(cfg["delay_min"], 16, int(batch) if batch else 16)
+    return min(cfg["delay_min"], int(batch) if batch else 8)
 
 
 def _persistent_applies(cfg, delivery):
@@ -650,11 +650,14 @@ def test_step_mode_selection(spk, monkeypatch):
     st = spk.Net(I.scaled(4, 8000, k_out=300), max_steps=1).stats()
     assert st["batch_steps"] == 1
     # smallest delay 15: binned delivery and the unsplit kernel in batches of
-    # 15 steps; the split kernel when asked for, or when batches are capped at 1
+    # 8 steps (15 when asked for); the split kernel when asked for, or when
+    # batches are capped at 1
     c2 = I.scaled(2, 8000, k_in_exc=640, k_in_inh=160)
     st = spk.Net(c2, max_steps=1).stats()
     assert st["step_mode"] == spk.SPK_STEP_PERSISTENT and st["persistent_split"] == 0
-    assert st["delivery"] == spk.SPK_DELIVERY_BINNED and st["batch_steps"] == 15
+    assert st["delivery"] == spk.SPK_DELIVERY_BINNED and st["batch_steps"] == 8
+    monkeypatch.setenv("SPK_BATCH_STEPS", "16")
+    assert spk.Net(c2, max_steps=1).stats()["batch_steps"] == 15
     monkeypatch.setenv("SPK_BATCH_STEPS", "1")
     st = spk.Net(c2, max_steps=1).stats()
     assert st["persistent_split"] == 1 and st["batch_steps"] == 1
