@@ -14,6 +14,7 @@ constexpr uint32_t kMaxLists = SPK_MAX_DELAY_LISTS;
 constexpr int kWave = 64;
 constexpr uint32_t kGroups = 8;        // one target group per XCD (blockIdx % 8 == XCD)
 constexpr uint32_t kMaxTileW = 8192;   // neurons per tile (LDS accumulators + spike list)
+constexpr uint32_t kTileCntBits = 14;  // a tile's spike count (<= kMaxTileW) in a progress word
 constexpr uint32_t kMaxT8 = 256;       // tiles per group
 constexpr uint32_t kMaxTiles = kGroups * kMaxT8;
 constexpr uint32_t kMaxBuckets = 2048; // (delay, tile) buckets of one group in the push kernel
@@ -211,7 +212,10 @@ struct RunCtl {
     uint32_t critp[kGroups * kRunMaxR];     // split kernel: critical phases finished, per push block
     uint32_t bulkp[kGroups * kRunMaxR];     // split kernel: bulk phases finished, per push block
     uint32_t pushp[kGroups * kRunMaxR];     // unsplit kernel: push phases finished, per push block
-    uint32_t tilep[kGroups * kRunMaxR];     // unsplit kernel, binned: tile phases published, per tile
+    // unsplit kernel, binned: per batch parity and tile, the batch published
+    // (epoch in bits kTileCntBits and up) with, for a one-step batch, the
+    // tile's spike count of that step (bits below)
+    uint32_t tilep[2][kGroups * kRunMaxR];
     uint32_t start, pad0[kCtlStride - 1];   // placement barrier
     uint32_t gcnt, pad1[kCtlStride - 1];    // grid barrier: XCDs complete
     uint32_t gen, pad2[kCtlStride - 1];     // grid barrier: released epoch

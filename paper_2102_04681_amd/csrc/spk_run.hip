@@ -128,7 +128,7 @@ struct RunLDS {
     uint32_t ws[16], ws2[16];
     unsigned long long ws64[16];
     uint32_t mstep[kRunMaxD];   // spikes of each step of the last pushed batch
-    uint32_t nspk2[2];          // spike counters of the update, alternating between steps
+    uint32_t nspk2[3];          // spike counters of the update, alternating between steps; [2] = 0
     uint32_t pstop[4];          // wait_tiles: a polling wave gave up
     uint32_t x, r, stop;
     // the neuron model's constants, read by the update from here into vector
@@ -202,27 +202,57 @@ __device__ void publish_push(const RunArgs &ra, uint32_t x, uint32_t r, uint32_t
 }
 
 // End of a tile phase (binned delivery): every thread's spike-list stores
-// have completed, then the tile's progress word advances to e.
-__device__ void publish_tile(const RunArgs &ra, uint32_t tile, uint32_t e)
+// have completed, then the tile's progress word of batch parity e & 1 takes
+// the stamp of batch e and the spike count ns of its step (one-step batches;
+// 0 otherwise).
+__device__ void publish_tile(const RunArgs &ra, uint32_t tile, uint32_t e, const uint32_t *ns)
 {
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    if (threadIdx.x == 0) st_ag(&ra.ctl->tilep[tile], e);
+    if (threadIdx.x == 0) st_ag(&ra.ctl->tilep[e & 1u][tile], e << kTileCntBits | *ns);
+}
+
+// Wait (one wave) until each of the n <= 64 words p[0..n) carries the stamp e
+// in its bits kTileCntBits and up; leaves lane k's word in *v.  False if the
+// wait gave up or another workgroup did.
+__device__ bool spin_all_stamp(const uint32_t *p, uint32_t n, uint32_t e, uint32_t *abort_flag, uint32_t *v)
+{
+    const uint32_t lane = lane_id(), want = e & (0xffffffffu >> kTileCntBits);
+    const uint64_t t0 = wall_clock64();
+    for (uint32_t k = 0;; k++) {
+        *v = ld_ag(p + (lane < n ? lane : 0u));
+        if (__all(lane >= n || (*v >> kTileCntBits) == want)) return true;
+        if ((k & 31u) == 31u) {
+            if (ld_ag(abort_flag)) return false;
+            if (wall_clock64() - t0 > kSpinTicks) {
+                if (lane == 0) atomicOr(abort_flag, kRunAbortTimeout);
+                return false;
+            }
+        }
+        __builtin_amdgcn_s_sleep(1);
+    }
 }
 
 // Start of a push phase (binned delivery): waves 0-3 wait until the progress
-// word of every tile (64 per wave) has reached e: then every spike list of
+// word of every tile (64 per wave) carries batch e: then every spike list of
 // the batch is complete, and every tile has drained the pages of the batch's
-// arrival steps, which this push phase may start to refill.
+// arrival steps, which this push phase may start to refill.  For a one-step
+// batch the words' spike counts go to pre[tile] (the push phase's LDS).
+// Words are kept per batch parity: a tile publishes batch e + 1 only after
+// the push phases of batch e of its own XCD, and batch e + 2 only after
+// those of batch e + 1 of every XCD, so the words of parity e & 1 still hold
+// batch e for every push block that waits for it.
 template <bool FIXED, bool CMP>
-__device__ bool wait_tiles(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t e)
+__device__ bool wait_tiles(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t e, bool counts)
 {
     RunCtl *c = ra.ctl;
     const uint32_t T = ra.s.tl.T, w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     if (w * kWave < T) {
-        const uint32_t n = T - w * kWave < kWave ? T - w * kWave : kWave;
-        const bool ok = spin_all_ge(&c->tilep[w * kWave], n, e, &c->abort_flag);
-        if (lane_id() == 0) {
+        const uint32_t n = T - w * kWave < kWave ? T - w * kWave : kWave, lane = lane_id();
+        uint32_t v;
+        const bool ok = spin_all_stamp(&c->tilep[e & 1u][w * kWave], n, e, &c->abort_flag, &v);
+        if (counts && ok && lane < n) L.u.p.pre[w * kWave + lane] = v & ((1u << kTileCntBits) - 1u);
+        if (lane == 0) {
             L.pstop[w] = ok ? 0u : 1u;
             if (!ok) atomicOr(ra.s.flags, kRunStoppedFlag);
         }
@@ -480,7 +510,8 @@ __device__ void run_update(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x,
 
 // Spike counts of the Db steps t_first .. t_first + Db - 1 as one list in
 // (step, tile) order: pre[u * T + tile] = spikes before segment (u, tile),
-// pre[Db * T] = all of them; uslot[u] = the spike-list slot of step u.
+// pre[Db * T] = all of them; uslot[u] = the spike-list slot of step u.  A
+// one-step batch finds the counts in pre[tile] already (wait_tiles).
 template <bool FIXED, bool CMP>
 __device__ uint32_t load_spike_batch(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint64_t t_first, uint32_t Db)
 {
@@ -495,7 +526,7 @@ __device__ uint32_t load_spike_batch(const StepArgs &a, RunLDS<FIXED, CMP> &L, u
         const uint32_t seg = b0 + k < NS && k < per ? b0 + k : 0u;
         const uint32_t u = seg / T, tile = seg - u * T;
         const uint32_t slot = slot0 + u < a.spk_slots ? slot0 + u : slot0 + u - a.spk_slots;
-        const uint32_t v = ld_u32<true>(a.spk_cnt + (uint64_t)slot * T + tile);
+        const uint32_t v = Db == 1 ? L.u.p.pre[seg] : ld_u32<true>(a.spk_cnt + (uint64_t)slot * T + tile);
         c[k] = b0 + k < NS && k < per ? (v < W ? v : W) : 0u;
         sum += c[k];
     }
@@ -786,6 +817,7 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
         L.x = x;
         L.r = atomicAdd(&ctl->ticket[x * kCtlStride], 1u);
         L.nspk2[0] = 0;
+        L.nspk2[2] = 0;
         atomicAdd(&ctl->start, 1u);
         L.stop = spin_ge(&ctl->start, gridDim.x, &ctl->abort_flag) ? 0u : 1u;
         if (L.stop) atomicOr(a.flags, kRunStoppedFlag);
@@ -871,9 +903,9 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
             if (!grid_sync(ra, L, x, ++eg, has_tile && more, tile_lo, tile_n, t_first + Db, Dn)) return;
         } else {  // binned: the tiles' progress words instead of a grid barrier
             ++eg;
-            if (has_tile) publish_tile(ra, tile, eg);
+            if (has_tile) publish_tile(ra, tile, eg, &L.nspk2[Db == 1 ? 0u : 2u]);
             if (has_tile && more) run_draws(a, L, tile_lo, tile_n, t_first + Db, Dn);  // while the others finish
-            if (!wait_tiles(ra, L, eg)) return;
+            if (!wait_tiles(ra, L, eg, Db == 1)) return;
         }
         if (DIRECT) {
             const uint64_t t = t_first;
