@@ -129,6 +129,7 @@ struct RunLDS {
     unsigned long long ws64[16];
     uint32_t mstep[kRunMaxD];   // spikes of each step of the last pushed batch
     uint32_t nspk2[3];          // spike counters of the update, alternating between steps; [2] = 0
+    uint32_t nb[kRunMaxD];      // batched update: spikes of each step of the batch
     uint32_t pstop[4];          // wait_tiles: a polling wave gave up
     uint32_t x, r, stop;
     // the neuron model's constants, read by the update from here into vector
@@ -512,6 +513,99 @@ __device__ void run_update(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x,
 // (step, tile) order: pre[u * T + tile] = spikes before segment (u, tile),
 // pre[Db * T] = all of them; uslot[u] = the spike-list slot of step u.  A
 // one-step batch finds the counts in pre[tile] already (wait_tiles).
+// Tile phase of a batch of Db >= 2 steps of LIF neurons (binned delivery):
+// the inputs of every step of the batch are in the accumulators already
+// (acc[u * W ...], the smallest delay is at least Db), so each thread takes
+// its neurons through the Db steps in registers, with the arithmetic of
+// run_update, and compacts each step's spikes into that step's LDS list
+// spk[u * W ...] (one counter nb[u] per step: no barrier between steps).
+// Then one barrier, and every step's list is published to its slot.
+template <bool FIXED, bool CMP>
+__device__ void run_update_batch(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x, uint32_t tile,
+                                 uint32_t tile_lo, uint32_t tile_n, uint64_t t_first, uint32_t Db)
+{
+    using AccT = typename RunLDS<FIXED, CMP>::AccT;
+    const StepArgs &a = ra.s;
+    const uint32_t tid = threadIdx.x, lane = lane_id(), W = a.tl.W;
+    const float mk = L.mk, v_rest = L.v_rest, v_th = L.v_th, v_reset = L.v_reset, i_bias = L.i_bias,
+                ext_w = L.ext_w;
+    const int32_t ext_wq = L.ext_wq, bias_q = L.bias_q, shift = L.shift, shift64 = L.shift64;
+    const uint32_t ref_steps = L.ref_steps, pois_len = L.pois_len;
+    for (uint32_t q0 = 0; q0 < tile_n; q0 += kRunThreads) {  // (uniform trip count: ballots below)
+        const uint32_t q = q0 + tid;
+        const bool live = q < tile_n;
+        const uint32_t qc = live ? q : 0u;
+        float V = L.V[qc];
+        uint32_t r = L.ref[qc];
+        AccT acc_n = L.u.t.acc[qc];  // step u + 1's input, loaded one step ahead
+        uint32_t K_n = pois_len ? L.kp[qc] : 0u;
+        for (uint32_t u = 0; u < Db; u++) {
+            const AccT acc = acc_n;
+            const uint32_t K = K_n;
+            if (u + 1 < Db) {
+                acc_n = L.u.t.acc[(u + 1) * W + qc];
+                K_n = pois_len ? L.kp[(u + 1) * W + qc] : 0u;
+            }
+            float I;
+            if (FIXED) {
+                const int32_t qt = (int32_t)acc + (int32_t)K * ext_wq + bias_q;
+                I = ldexpf((float)qt, -shift);
+            } else {
+                const float isyn = fixed64_to_float(acc, shift64);
+                const float ext = __fmul_rn((float)K, ext_w);
+                I = __fadd_rn(__fadd_rn(isyn, ext), i_bias);
+            }
+            bool spk = false;
+            if (r > 0) {
+                r -= 1;
+                V = v_reset;
+            } else {
+                const float av = __fsub_rn(v_rest, V);
+                const float bv = __fmul_rn(mk, av);
+                const float cv = __fadd_rn(V, bv);
+                V = __fadd_rn(cv, I);
+                if (V >= v_th) {
+                    spk = true;
+                    V = v_reset;
+                    r = ref_steps;
+                }
+            }
+            spk = spk && live;
+            const uint64_t bal = __ballot(spk);
+            if (bal) {  // (uniform) one counter update per wave and step
+                uint32_t wb = 0;
+                if (lane == 0) wb = atomicAdd(&L.nb[u], (uint32_t)__popcll(bal));
+                wb = __shfl(wb, 0);
+                if (spk) {
+                    const uint32_t rank =
+                        __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+                    L.u.t.spk[u * W + wb + rank] = (uint16_t)q;
+                }
+            }
+        }
+        if (live) {
+            L.V[q] = V;
+            L.ref[q] = (uint8_t)r;
+        }
+    }
+    lds_sync();
+    const uint64_t T = a.tl.T;
+    for (uint32_t u = 0; u < Db; u++) {
+        const uint32_t ns = L.nb[u];
+        const uint64_t seg = ((t_first + u) % a.spk_slots) * T + tile;
+        uint32_t *dst = a.spk_ids + seg * W;
+        for (uint32_t k = tid; k < ns; k += kRunThreads) st_ag(dst + k, tile_lo + L.u.t.spk[u * W + k]);
+    }
+    if (tid < Db) {
+        const uint64_t t = t_first + tid;
+        const uint32_t ns = L.nb[tid];
+        st_ag(&a.spk_cnt[(t % a.spk_slots) * T + tile], ns);
+        if (ns) atomicAdd(&a.counts8[t * kGroups + x], ns);
+        const unsigned long long delivered = L.u.t.dlv[tid];
+        if (delivered) atomicAdd((unsigned long long *)&a.delivered8[t * kGroups + x], delivered);
+    }
+}
+
 template <bool FIXED, bool CMP>
 __device__ uint32_t load_spike_batch(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint64_t t_first, uint32_t Db)
 {
@@ -886,8 +980,11 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
             // the spike count of the previous step has been read by every thread
             for (uint32_t q = tid; q < Db * tl.W; q += kRunThreads) L.u.t.acc[q] = 0;
             if (tid == 0) L.nspk2[0] = 0;
+            if (tid < Db) L.nb[tid] = 0;
             if (!DIRECT) run_drain(a, L, x, r, tile, tile_n, t_first, Db);  // all steps of the batch
-            for (uint32_t u = 0; u < Db; u++) {
+            if (!DIRECT && lif && Db > 1)
+                run_update_batch(ra, L, x, tile, tile_lo, tile_n, t_first, Db);
+            else for (uint32_t u = 0; u < Db; u++) {
                 const uint64_t t = t_first + u;
                 if (u) {  // the spike list of t - 1 (LDS) has been published by every thread
                     if (!lif) run_draws(a, L, tile_lo, tile_n, t, 1);
