@@ -93,7 +93,8 @@ def algorithmic_bytes(n, kind, events, spikes, per_event, steps):
     return per_event * events, per_neuron * float(n) * steps + 8.0 * spikes
 
 
-STEP_SOURCES = ("spk_internal.h", "spk_dev.h", "spk_step.hip", "spk_run.hip", "spk_split.hip", "spk_runtime.hip")
+STEP_SOURCES = ("spk_internal.h", "spk_dev.h", "spk_step.hip", "spk_run.hip", "spk_run_batch.hip", "spk_split.hip",
+                "spk_runtime.hip")
 
 
 def step_source_sha():

@@ -285,6 +285,7 @@ uint32_t push_blocks_per_group();
 bool run_supported(const StepArgs &a, uint32_t R);
 bool run_batch_supported(const StepArgs &a, uint32_t D);  // steps per batch D is valid for this network
 hipError_t launch_run(const RunArgs &ra, hipStream_t s);
+hipError_t launch_run_batched(const RunArgs &ra, hipStream_t s);  // spk_run_batch.hip
 
 // spk_split.hip -- the persistent kernel that files each step's delay-1
 // events before the rest (binned delivery)

@@ -29,7 +29,16 @@
 // Every wait is bounded (10 s of the real-time clock); a workgroup that gives
 // up sets an abort flag that every other waiter also polls, so the grid
 // always drains.  The host reads the flag after the launch.
+//
+// The variants for batches of several LIF steps (updates in registers) are
+// compiled from this file in a translation unit of their own
+// (spk_run_batch.hip, SPK_RUN_BATCH = 1): instantiated beside the one-step
+// variants, they changed the compiler's register allocation of those.
 #include <hip/hip_runtime.h>
+
+#ifndef SPK_RUN_BATCH
+#define SPK_RUN_BATCH 0
+#endif
 
 #include "spk_dev.h"
 
@@ -110,6 +119,7 @@ struct RunLDS {
             uint64_t wbeg[kRunThreads / kWave][kWave];
             unsigned long long dlv[kRunMaxD];  // binned: events delivered at each step of the batch
             uint32_t ovfm;                     // binned: bit u: step u of the batch has overflowed events
+            uint32_t nb[kRunMaxD];             // batched update: spikes of each step of the batch
         } t;
         struct {
             Rec stage[kStageN];
@@ -129,7 +139,6 @@ struct RunLDS {
     unsigned long long ws64[16];
     uint32_t mstep[kRunMaxD];   // spikes of each step of the last pushed batch
     uint32_t nspk2[3];          // spike counters of the update, alternating between steps; [2] = 0
-    uint32_t nb[kRunMaxD];      // batched update: spikes of each step of the batch
     uint32_t pstop[4];          // wait_tiles: a polling wave gave up
     uint32_t x, r, stop;
     // the neuron model's constants, read by the update from here into vector
@@ -574,7 +583,7 @@ __device__ void run_update_batch(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint3
             const uint64_t bal = __ballot(spk);
             if (bal) {  // (uniform) one counter update per wave and step
                 uint32_t wb = 0;
-                if (lane == 0) wb = atomicAdd(&L.nb[u], (uint32_t)__popcll(bal));
+                if (lane == 0) wb = atomicAdd(&L.u.t.nb[u], (uint32_t)__popcll(bal));
                 wb = __shfl(wb, 0);
                 if (spk) {
                     const uint32_t rank =
@@ -591,14 +600,14 @@ __device__ void run_update_batch(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint3
     lds_sync();
     const uint64_t T = a.tl.T;
     for (uint32_t u = 0; u < Db; u++) {
-        const uint32_t ns = L.nb[u];
+        const uint32_t ns = L.u.t.nb[u];
         const uint64_t seg = ((t_first + u) % a.spk_slots) * T + tile;
         uint32_t *dst = a.spk_ids + seg * W;
         for (uint32_t k = tid; k < ns; k += kRunThreads) st_ag(dst + k, tile_lo + L.u.t.spk[u * W + k]);
     }
     if (tid < Db) {
         const uint64_t t = t_first + tid;
-        const uint32_t ns = L.nb[tid];
+        const uint32_t ns = L.u.t.nb[tid];
         st_ag(&a.spk_cnt[(t % a.spk_slots) * T + tile], ns);
         if (ns) atomicAdd(&a.counts8[t * kGroups + x], ns);
         const unsigned long long delivered = L.u.t.dlv[tid];
@@ -882,7 +891,10 @@ __device__ __forceinline__ uint64_t raster_advance(const StepArgs &a, uint64_t t
     return ok ? rbase + M : rbase;
 }
 
-template <bool FIXED, bool CMP, bool DIRECT>
+// BATCH: binned delivery of LIF neurons in batches of several steps, whose
+// updates run in registers (run_update_batch); a variant of its own, so that
+// the one-step kernels keep their register allocation.
+template <bool FIXED, bool CMP, bool DIRECT, bool BATCH>
 __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
 {
     __shared__ RunLDS<FIXED, CMP> L;
@@ -980,11 +992,15 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
             // the spike count of the previous step has been read by every thread
             for (uint32_t q = tid; q < Db * tl.W; q += kRunThreads) L.u.t.acc[q] = 0;
             if (tid == 0) L.nspk2[0] = 0;
-            if (tid < Db) L.nb[tid] = 0;
+            if constexpr (BATCH)
+                if (tid < Db) L.u.t.nb[tid] = 0;
             if (!DIRECT) run_drain(a, L, x, r, tile, tile_n, t_first, Db);  // all steps of the batch
-            if (!DIRECT && lif && Db > 1)
-                run_update_batch(ra, L, x, tile, tile_lo, tile_n, t_first, Db);
-            else for (uint32_t u = 0; u < Db; u++) {
+            bool batched = false;
+            if constexpr (BATCH) {
+                batched = lif && Db > 1;
+                if (batched) run_update_batch(ra, L, x, tile, tile_lo, tile_n, t_first, Db);
+            }
+            if (!batched) for (uint32_t u = 0; u < Db; u++) {
                 const uint64_t t = t_first + u;
                 if (u) {  // the spike list of t - 1 (LDS) has been published by every thread
                     if (!lif) run_draws(a, L, tile_lo, tile_n, t, 1);
@@ -1031,16 +1047,41 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
     if (tid == 0 && x == 0 && r == 0) *(uint64_t *)a.t_base = ra.t0 + ra.n_steps;
 }
 
-template <bool FIXED, bool CMP, bool DIRECT>
+template <bool FIXED, bool CMP, bool DIRECT, bool BATCH>
 hipError_t launch_run_t(const RunArgs &ra, hipStream_t s)
 {
     RunArgs arg = ra;
     void *args[] = {&arg};
-    return hipLaunchCooperativeKernel((const void *)k_run<FIXED, CMP, DIRECT>, dim3(kGroups * ra.R),
+    return hipLaunchCooperativeKernel((const void *)k_run<FIXED, CMP, DIRECT, BATCH>, dim3(kGroups * ra.R),
                                       dim3(kRunThreads), args, 0, s);
 }
 
+template <bool FIXED, bool CMP>
+hipError_t launch_run_fc(const RunArgs &ra, hipStream_t s)
+{
+#if SPK_RUN_BATCH
+    return launch_run_t<FIXED, CMP, false, true>(ra, s);
+#else
+    if (ra.s.direct) return launch_run_t<FIXED, CMP, true, false>(ra, s);
+    return launch_run_t<FIXED, CMP, false, false>(ra, s);
+#endif
+}
+
+hipError_t launch_run_any(const RunArgs &ra, hipStream_t s)
+{
+    const bool F = ra.s.m.fixed, C = ra.s.compact;
+    if (F && C) return launch_run_fc<true, true>(ra, s);
+    if (F && !C) return launch_run_fc<true, false>(ra, s);
+    if (!F && C) return launch_run_fc<false, true>(ra, s);
+    return launch_run_fc<false, false>(ra, s);
+}
+
 }  // namespace
+
+#if SPK_RUN_BATCH
+// Binned delivery, LIF neurons, batches of ra.D >= 2 steps.
+hipError_t launch_run_batched(const RunArgs &ra, hipStream_t s) { return launch_run_any(ra, s); }
+#else
 
 bool run_supported(const StepArgs &a, uint32_t R)
 {
@@ -1066,15 +1107,9 @@ hipError_t launch_run(const RunArgs &ra, hipStream_t s)
     const StepArgs &a = ra.s;
     if (a.compact ? !a.syn32 || (!a.direct && !a.pages16) : !a.syn || (!a.direct && !a.pages))
         return hipErrorInvalidValue;
-    const bool F = a.m.fixed, C = a.compact, D = a.direct;
-    if (F && C && D) return launch_run_t<true, true, true>(ra, s);
-    if (F && C && !D) return launch_run_t<true, true, false>(ra, s);
-    if (F && !C && D) return launch_run_t<true, false, true>(ra, s);
-    if (F && !C && !D) return launch_run_t<true, false, false>(ra, s);
-    if (!F && C && D) return launch_run_t<false, true, true>(ra, s);
-    if (!F && C && !D) return launch_run_t<false, true, false>(ra, s);
-    if (!F && !C && D) return launch_run_t<false, false, true>(ra, s);
-    return launch_run_t<false, false, false>(ra, s);
+    if (!a.direct && ra.D > 1 && a.m.kind != SPK_SOURCE) return launch_run_batched(ra, s);
+    return launch_run_any(ra, s);
 }
+#endif
 
 }  // namespace spk
