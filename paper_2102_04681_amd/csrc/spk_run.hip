@@ -140,6 +140,7 @@ struct RunLDS {
     uint32_t mstep[kRunMaxD];   // spikes of each step of the last pushed batch
     uint32_t nspk2[3];          // spike counters of the update, alternating between steps; [2] = 0
     uint32_t pstop[4];          // wait_tiles: a polling wave gave up
+    uint32_t pq[2][4];          // look_tiles: a polling wave saw its words complete (by look parity)
     uint32_t x, r, stop;
     // the neuron model's constants, read by the update from here into vector
     // registers (kept in scalar registers they spill across the long kernel)
@@ -173,6 +174,35 @@ __device__ void run_draws(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t til
             if (m.kind == SPK_SOURCE)
                 L.ref[q] = (uint64_t)hash_hi32(step_hash(m.keys.bern, gi, t)) < m.src_thr ? 1 : 0;
         }
+    }
+}
+
+// The same draws in units of two rounds of one step (unit k: step k / nr2,
+// rounds 2 (k % nr2) and 2 (k % nr2) + 1, nr2 = draw_units_per_step), so
+// that a workgroup can stop between units once its wait is over.
+__device__ __forceinline__ uint32_t draw_units_per_step(uint32_t tile_n)
+{
+    return ((tile_n + kRunThreads - 1) / kRunThreads + 1) / 2;
+}
+template <bool FIXED, bool CMP>
+__device__ void run_draw_unit(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t tile_lo, uint32_t tile_n,
+                              uint64_t t, uint32_t k)
+{
+    const ModelArgs &m = a.m;
+    const uint32_t W = a.tl.W, nr2 = draw_units_per_step(tile_n), u = k / nr2, j = k - u * nr2;
+#pragma unroll
+    for (int h2 = 0; h2 < 2; h2++) {
+        const uint32_t q = (2 * j + h2) * kRunThreads + threadIdx.x;
+        if (q >= tile_n) continue;
+        const uint32_t gi = tile_lo + q;
+        if (m.pois_len) {
+            const uint32_t h = hash_hi32(step_hash(m.keys.pois, gi, t + u));
+            uint32_t kk = L.guide[h >> 24];
+            while ((uint64_t)h >= L.pois[kk]) kk++;
+            L.kp[u * W + q] = (uint8_t)kk;
+        }
+        if (m.kind == SPK_SOURCE)
+            L.ref[q] = (uint64_t)hash_hi32(step_hash(m.keys.bern, gi, t)) < m.src_thr ? 1 : 0;
     }
 }
 
@@ -271,6 +301,31 @@ __device__ bool wait_tiles(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t e,
     uint32_t stop = 0;
     for (uint32_t k = 0; k * kWave < T; k++) stop |= L.pstop[k];
     return stop == 0;
+}
+
+// One look at the tiles' progress words (as wait_tiles, without waiting),
+// with work() done while the loads are in flight: true if every tile has
+// published batch e (and then, with counts, pre[tile] holds the counts).
+template <bool FIXED, bool CMP, class Work>
+__device__ bool look_tiles(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t e, bool counts, uint32_t par,
+                           Work &&work)
+{
+    const uint32_t T = ra.s.tl.T, w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = lane_id();
+    const bool poller = w * kWave < T;
+    const uint32_t n = poller ? (T - w * kWave < kWave ? T - w * kWave : kWave) : 0u;
+    uint32_t v = 0;
+    if (poller) v = ld_ag(&ra.ctl->tilep[e & 1u][w * kWave + (lane < n ? lane : 0u)]);
+    work();
+    if (poller) {
+        const uint32_t want = e & (0xffffffffu >> kTileCntBits);
+        const bool ok = __all(lane >= n || (v >> kTileCntBits) == want);
+        if (counts && ok && lane < n) L.u.p.pre[w * kWave + lane] = v & ((1u << kTileCntBits) - 1u);
+        if (lane == 0) L.pq[par][w] = ok ? 1u : 0u;
+    }
+    __syncthreads();
+    bool all = true;
+    for (uint32_t k = 0; k * kWave < T; k++) all = all && L.pq[par][k] != 0;
+    return all;  // (pq[par] is written again two looks later, after a barrier)
 }
 
 // Start of a tile phase (binned delivery): the first wave waits until every
@@ -972,6 +1027,10 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
     if (ra.n_steps) run_draws(a, L, tile_lo, tile_n, ra.t0, (uint32_t)(ra.n_steps < Dd ? ra.n_steps : Dd));
     uint64_t rbase = a.raster_cap ? a.raster_offs[ra.t0] : 0;
     uint32_t eg = 0, ex = 0;
+    // binned: draws of the next batch left for after its push phase (units
+    // dr_k .. dr_n - 1 of steps from dr_t on)
+    uint64_t dr_t = 0;
+    uint32_t dr_k = 0, dr_n = 0, look = 0;
     __syncthreads();
 
     // Steps run in batches of D (binned delivery with a smallest delay >= D;
@@ -987,6 +1046,8 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
         const bool more = s < ra.n_steps;
         if (has_tile) {
             // binned: every push block of the XCD has filed the previous batch
+            if constexpr (BATCH)
+                for (; dr_k < dr_n; dr_k++) run_draw_unit(a, L, tile_lo, tile_n, dr_t, dr_k);
             if (!DIRECT && !wait_pushes(ra, L, x, ex)) return;
             // the push phase reused this LDS: accumulators restart at zero, and
             // the spike count of the previous step has been read by every thread
@@ -1017,8 +1078,25 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
         } else {  // binned: the tiles' progress words instead of a grid barrier
             ++eg;
             if (has_tile) publish_tile(ra, tile, eg, &L.nspk2[Db == 1 ? 0u : 2u]);
-            if (has_tile && more) run_draws(a, L, tile_lo, tile_n, t_first + Db, Dn);  // while the others finish
-            if (!wait_tiles(ra, L, eg, Db == 1)) return;
+            // the next batch's draws while the others finish.  Batches of
+            // several steps: a unit at a time between looks at the tiles'
+            // words; once every tile has published, the rest waits until after
+            // the push phase (the last tiles to finish would otherwise hold
+            // every push phase up by their draws).  One-step batches draw at
+            // once (measured: the looks between units cost more there).
+            if constexpr (BATCH) {
+                bool ready = false;
+                dr_t = t_first + Db;
+                dr_k = 0;
+                dr_n = has_tile && more ? Dn * draw_units_per_step(tile_n) : 0u;
+                while (!ready && dr_k < dr_n)
+                    ready = look_tiles(ra, L, eg, Db == 1, look++ & 1u,
+                                       [&] { run_draw_unit(a, L, tile_lo, tile_n, dr_t, dr_k++); });
+                if (!ready && !wait_tiles(ra, L, eg, Db == 1)) return;
+            } else {
+                if (has_tile && more) run_draws(a, L, tile_lo, tile_n, t_first + Db, Dn);
+                if (!wait_tiles(ra, L, eg, Db == 1)) return;
+            }
         }
         if (DIRECT) {
             const uint64_t t = t_first;
