@@ -573,10 +573,6 @@ __device__ void run_update(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x,
     }
 }
 
-// Spike counts of the Db steps t_first .. t_first + Db - 1 as one list in
-// (step, tile) order: pre[u * T + tile] = spikes before segment (u, tile),
-// pre[Db * T] = all of them; uslot[u] = the spike-list slot of step u.  A
-// one-step batch finds the counts in pre[tile] already (wait_tiles).
 // Tile phase of a batch of Db >= 2 steps of LIF neurons (binned delivery):
 // the inputs of every step of the batch are in the accumulators already
 // (acc[u * W ...], the smallest delay is at least Db), so each thread takes
@@ -670,6 +666,10 @@ __device__ void run_update_batch(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint3
     }
 }
 
+// Spike counts of the Db steps t_first .. t_first + Db - 1 as one list in
+// (step, tile) order: pre[u * T + tile] = spikes before segment (u, tile),
+// pre[Db * T] = all of them; uslot[u] = the spike-list slot of step u.  A
+// one-step batch finds the counts in pre[tile] already (wait_tiles).
 template <bool FIXED, bool CMP>
 __device__ uint32_t load_spike_batch(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint64_t t_first, uint32_t Db)
 {
