@@ -11,8 +11,9 @@
 //     and (as a push block) the fill counters of the pages it owns;
 //   - the two hand-offs of a step happen inside the kernel instead of at
 //     kernel boundaries, through progress words (binned delivery): a tile
-//     advances its word once it has published its spike list of t, and the
-//     push blocks start once every tile's word has advanced; a push block
+//     advances its word once it has published its spike list of t (for a
+//     one-step batch the word also carries the spike count), and the push
+//     blocks start once every tile's word has advanced; a push block
 //     advances its word once it has filed its events, and a tile starts its
 //     next drain once the 32 words of its XCD have advanced: every page is
 //     written and read on one XCD (its L2 is the point of coherence, so only
@@ -20,8 +21,9 @@
 //     hand-off per step, a grid barrier;
 //   - with binned delivery and a smallest delay of D >= 2 steps, steps run in
 //     batches of D: nothing filed in a batch arrives within it, so the tile
-//     drains the batch's D arrival slots at once and runs its D updates back
-//     to back, and one push phase files the events of all D steps' spikes.
+//     drains the batch's D arrival slots at once and takes each neuron
+//     through the D updates in registers, and one push phase files the
+//     events of all D steps' spikes.
 // Workgroups find their XCD from the hardware register and take a ticket
 // within it, so the group of tiles a workgroup serves is always on the XCD it
 // runs on.  Spike lists cross XCDs through agent-scope loads and stores.
