@@ -170,29 +170,65 @@ __device__ __forceinline__ uint32_t n_buckets(const ConnArgs &c, const RowIndex 
 // Bernoulli rows (one hash per ordered pair) and fixed out-degree rows
 // (k_out uniform targets with replacement): one block per source.
 
-__global__ __launch_bounds__(kBlock) void k_gen_count_rows(ConnArgs c, uint32_t *cnt)
+// With hist (Bernoulli rows), the pass also keeps each row's bucket counts
+// for the placement pass, which then need not draw the row a second time:
+// hist[s * (T + 2 * kGroups) ...] = the row's synapses per target tile
+// (direct delivery's buckets), then per (XCD group, smallest delay or not)
+// (binned delivery's), as u16 (a row longer than kMaxRow is refused before
+// placement).
+__global__ __launch_bounds__(kBlock) void k_gen_count_rows(ConnArgs c, uint32_t *cnt, uint16_t *hist)
 {
     __shared__ uint32_t tot;
+    __shared__ uint32_t hb[kMaxTiles + 2 * kGroups];  // per tile, then per (group, delay class)
+    __shared__ uint32_t hj[kMaxTiles];                  // per tile, smallest delay only (several delays)
     const uint32_t s = blockIdx.x;
     if (c.kind != SPK_CONN_BERNOULLI) {
         if (threadIdx.x == 0) cnt[s] = c.k_out;
         return;
     }
+    const uint32_t T = c.tl.T, HB = T + 2 * kGroups;
     if (threadIdx.x == 0) tot = 0;
+    if (hist)
+        for (uint32_t k = threadIdx.x; k < HB; k += kBlock) {
+            hb[k] = 0;
+            if (k < T) hj[k] = 0;
+        }
     __syncthreads();
     const uint64_t rk = mix64(c.keys.conn ^ (uint64_t)s);
+    const uint64_t rd = mix64(c.keys.delay ^ (uint64_t)s);
     uint32_t mine = 0;
-    for (uint32_t tgt = threadIdx.x; tgt < c.n; tgt += kBlock)
-        mine += (uint64_t)hash_hi32(mix64(rk ^ (uint64_t)tgt)) < c.conn_thr;
+    for (uint32_t tgt = threadIdx.x; tgt < c.n; tgt += kBlock) {
+        const bool hit = (uint64_t)hash_hi32(mix64(rk ^ (uint64_t)tgt)) < c.conn_thr;
+        mine += hit ? 1u : 0u;
+        if (hist && hit) {  // (per-tile counters: few conflicts; the 16 group buckets follow from them)
+            const uint32_t tile = tgt >> c.tl.logW;
+            atomicAdd(&hb[tile], 1u);
+            if (c.lists > 1 && hash_range(mix64(rd ^ (uint64_t)tgt), c.lists) == 0) atomicAdd(&hj[tile], 1u);
+        }
+    }
     for (int o = 32; o > 0; o >>= 1) mine += __shfl_xor(mine, o);
     if (lane_id() == 0 && mine) atomicAdd(&tot, mine);
     __syncthreads();
     if (threadIdx.x == 0) cnt[s] = tot;
+    if (hist && threadIdx.x < kGroups) {  // group g: smallest delay, then the others
+        uint32_t all = 0, j0 = 0;
+        for (uint32_t k = threadIdx.x * c.tl.T8; k < (threadIdx.x + 1) * c.tl.T8; k++) {
+            all += hb[k];
+            j0 += c.lists > 1 ? hj[k] : hb[k];
+        }
+        hb[T + 2 * threadIdx.x] = j0;
+        hb[T + 2 * threadIdx.x + 1] = all - j0;
+    }
+    __syncthreads();
+    if (hist)
+        for (uint32_t k = threadIdx.x; k < HB; k += kBlock)
+            hist[(uint64_t)s * HB + k] = (uint16_t)(hb[k] < 65535u ? hb[k] : 65535u);
 }
 
-// Draw the row twice: once to count per tile, once to place.
+// Draw the row twice: once to count per bucket (unless the count pass kept
+// the counts in hist), once to place.
 __global__ __launch_bounds__(kBlock) void k_gen_fill_rows(ConnArgs c, const uint64_t *row_ptr,
-                                                         void *syn, RowIndex ix)
+                                                         void *syn, RowIndex ix, const uint16_t *hist)
 {
     __shared__ RowLDS L;
     const uint32_t s = blockIdx.x, tid = threadIdx.x;
@@ -204,10 +240,15 @@ __global__ __launch_bounds__(kBlock) void k_gen_fill_rows(ConnArgs c, const uint
     const uint64_t rw = mix64(c.keys.w ^ (uint64_t)s);
     if (c.kind == SPK_CONN_BERNOULLI) {
         const uint64_t rk = mix64(c.keys.conn ^ (uint64_t)s);
-        for (uint32_t tgt = tid; tgt < c.n; tgt += kBlock) {
-            if (!((uint64_t)hash_hi32(mix64(rk ^ (uint64_t)tgt)) < c.conn_thr)) continue;
-            const uint32_t j = c.lists > 1 ? hash_range(mix64(rd ^ (uint64_t)tgt), c.lists) : 0;
-            atomicAdd(&L.cur[bucket_of(c, ix, tgt, j)], 1u);
+        if (hist) {  // the count pass's bucket counts of this row
+            const uint32_t HB = c.tl.T + 2 * kGroups, off = ix.desc ? c.tl.T : 0u;
+            for (uint32_t k = tid; k < nb; k += kBlock) L.cur[k] = hist[(uint64_t)s * HB + off + k];
+        } else {
+            for (uint32_t tgt = tid; tgt < c.n; tgt += kBlock) {
+                if (!((uint64_t)hash_hi32(mix64(rk ^ (uint64_t)tgt)) < c.conn_thr)) continue;
+                const uint32_t j = c.lists > 1 ? hash_range(mix64(rd ^ (uint64_t)tgt), c.lists) : 0;
+                atomicAdd(&L.cur[bucket_of(c, ix, tgt, j)], 1u);
+            }
         }
         scan_tiles(L, nb);
         write_row_index(c, ix, L, s, beg, len);
@@ -568,17 +609,18 @@ int cu_count()
     return cus;
 }
 
-hipError_t gen_count_rows(const ConnArgs &c, uint32_t *cnt, hipStream_t s)
+hipError_t gen_count_rows(const ConnArgs &c, uint32_t *cnt, uint16_t *hist, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_gen_count_rows, dim3(c.n), dim3(kBlock), 0, s, c, cnt);
+    if (c.tl.T > kMaxTiles) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_gen_count_rows, dim3(c.n), dim3(kBlock), 0, s, c, cnt, hist);
     return hipGetLastError();
 }
 
 hipError_t gen_fill_rows(const ConnArgs &c, const uint64_t *row_ptr, void *syn, RowIndex ix,
-                         hipStream_t s)
+                         const uint16_t *hist, hipStream_t s)
 {
     if (c.tl.T > kMaxTiles) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_gen_fill_rows, dim3(c.n), dim3(kBlock), 0, s, c, row_ptr, syn, ix);
+    hipLaunchKernelGGL(k_gen_fill_rows, dim3(c.n), dim3(kBlock), 0, s, c, row_ptr, syn, ix, hist);
     return hipGetLastError();
 }
 

@@ -236,9 +236,11 @@ struct RunArgs {
 constexpr uint32_t kSplitMaxBuckets = 1024;  // split kernel: (delay, tile) buckets and (slot, tile) pages
 
 // spk_gen.hip -- connectivity expansion
-hipError_t gen_count_rows(const ConnArgs &c, uint32_t *cnt, hipStream_t s);
+// hist: optional (Bernoulli rows), n * (T + 2 * kGroups) u16 bucket counts
+// kept for gen_fill_rows, which then draws each row once instead of twice.
+hipError_t gen_count_rows(const ConnArgs &c, uint32_t *cnt, uint16_t *hist, hipStream_t s);
 hipError_t gen_fill_rows(const ConnArgs &c, const uint64_t *row_ptr, void *syn, RowIndex ix,
-                         hipStream_t s);
+                         const uint16_t *hist, hipStream_t s);
 hipError_t gen_in_count(const ConnArgs &c, uint32_t *cnt, hipStream_t s);
 hipError_t gen_in_fill(const ConnArgs &c, const uint64_t *row_ptr, uint32_t *cursor, void *syn,
                        hipStream_t s);

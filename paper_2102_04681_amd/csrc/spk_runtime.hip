@@ -731,10 +731,17 @@ spk_status generate(spk_net *net)
     SPK_HIP(hipMemsetAsync(cnt, 0, (size_t)net->n * 4, s));
     ConnArgs c = conn_args(net);
     const bool in_rows = net->P.conn_kind == SPK_CONN_FIXED_IN;
+    // Bernoulli rows: the count pass keeps every row's bucket counts (u16,
+    // both deliveries' buckets), so the placement pass draws each row once
+    uint16_t *hist = nullptr;
+    const uint64_t hist_elems = (uint64_t)net->n * (net->tl.T + 2 * kGroups);
+    if (net->P.conn_kind == SPK_CONN_BERNOULLI && hist_elems * 2 <= (4ull << 30) &&
+        dalloc(net, &hist, hist_elems) != SPK_OK)
+        hist = nullptr;  // (then the placement pass counts for itself)
     SegTimer tm;
     SPK_HIP(tm.start(s));
     if (in_rows) SPK_HIP(gen_in_count(c, cnt, s));
-    else SPK_HIP(gen_count_rows(c, cnt, s));
+    else SPK_HIP(gen_count_rows(c, cnt, hist, s));
     SPK_HIP(tm.stop(s, &net->gen_ms));
     SPK_TRY(finish_counts(net, cnt));
     RowIndex ix{};
@@ -754,11 +761,12 @@ spk_status generate(spk_net *net)
         dfree(net, tmp);
     } else {        // drawn per source, bucketed while drawn
         SPK_HIP(tm.start(s));
-        SPK_HIP(gen_fill_rows(c, net->row_ptr, syn, ix, s));
+        SPK_HIP(gen_fill_rows(c, net->row_ptr, syn, ix, hist, s));
         SPK_HIP(tm.stop(s, &net->gen_ms));
     }
     SPK_HIP(hipStreamSynchronize(s));
     dfree(net, cnt);
+    dfree(net, hist);
     return finish_rows(net);
 }
 
