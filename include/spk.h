@@ -124,7 +124,10 @@ enum { SPK_STEP_AUTO = 0, SPK_STEP_GRAPH = 1, SPK_STEP_PERSISTENT = 2 };
  *   SPK_PERSISTENT_SPLIT=0 / 1 forces the persistent kernel's variant (see
  *   spk_stats_t.persistent_split; default: split only when the smallest
  *   delay is >= 2 and steps cannot be batched); SPK_BATCH_STEPS caps the
- *   steps per batch (1..16, default 8; spk_stats_t.batch_steps). */
+ *   steps per batch (1..16, default 8; spk_stats_t.batch_steps);
+ *   SPK_GEN_KEYS=0 makes the Bernoulli generator draw every row a second
+ *   time to place it instead of keeping the first pass's synapses (the
+ *   results are the same). */
 typedef struct {
     uint32_t abi_version;      /* must be SPK_ABI_VERSION */
     uint32_t n;

@@ -171,12 +171,16 @@ __device__ __forceinline__ uint32_t n_buckets(const ConnArgs &c, const RowIndex 
 // (k_out uniform targets with replacement): one block per source.
 
 // With hist (Bernoulli rows), the pass also keeps each row's bucket counts
-// for the placement pass, which then need not draw the row a second time:
+// for the placement pass, which then need not count the row again:
 // hist[s * (T + 2 * kGroups) ...] = the row's synapses per target tile
 // (direct delivery's buckets), then per (XCD group, smallest delay or not)
 // (binned delivery's), as u16 (a row longer than kMaxRow is refused before
-// placement).
-__global__ __launch_bounds__(kBlock) void k_gen_count_rows(ConnArgs c, uint32_t *cnt, uint16_t *hist)
+// placement).  With keys as well, it keeps the first cap synapses of the row
+// as keys (j << 24 | target) at keys[s * cap ...], in no particular order:
+// where no row is longer than cap, the placement pass reads them instead of
+// drawing the row again.
+__global__ __launch_bounds__(kBlock) void k_gen_count_rows(ConnArgs c, uint32_t *cnt, uint16_t *hist,
+                                                          uint32_t *keys, uint32_t cap)
 {
     __shared__ uint32_t tot;
     __shared__ uint32_t hb[kMaxTiles + 2 * kGroups];  // per tile, then per (group, delay class)
@@ -196,18 +200,32 @@ __global__ __launch_bounds__(kBlock) void k_gen_count_rows(ConnArgs c, uint32_t 
     __syncthreads();
     const uint64_t rk = mix64(c.keys.conn ^ (uint64_t)s);
     const uint64_t rd = mix64(c.keys.delay ^ (uint64_t)s);
+    const uint32_t lane = lane_id();
     uint32_t mine = 0;
-    for (uint32_t tgt = threadIdx.x; tgt < c.n; tgt += kBlock) {
-        const bool hit = (uint64_t)hash_hi32(mix64(rk ^ (uint64_t)tgt)) < c.conn_thr;
-        mine += hit ? 1u : 0u;
+    for (uint32_t t0 = 0; t0 < c.n; t0 += kBlock) {  // (uniform trip count: ballots below)
+        const uint32_t tgt = t0 + threadIdx.x;
+        const bool hit = tgt < c.n && (uint64_t)hash_hi32(mix64(rk ^ (uint64_t)tgt)) < c.conn_thr;
+        uint32_t j = 0;
         if (hist && hit) {  // (per-tile counters: few conflicts; the 16 group buckets follow from them)
             const uint32_t tile = tgt >> c.tl.logW;
             atomicAdd(&hb[tile], 1u);
-            if (c.lists > 1 && hash_range(mix64(rd ^ (uint64_t)tgt), c.lists) == 0) atomicAdd(&hj[tile], 1u);
+            j = c.lists > 1 ? hash_range(mix64(rd ^ (uint64_t)tgt), c.lists) : 0u;
+            if (c.lists > 1 && j == 0) atomicAdd(&hj[tile], 1u);
+        }
+        if (keys) {  // one position counter update per wave
+            const uint64_t bal = __ballot(hit);
+            uint32_t base = 0;
+            if (lane == 0 && bal) base = atomicAdd(&tot, (uint32_t)__popcll(bal));
+            base = __shfl(base, 0);
+            const uint32_t pos =
+                base + __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+            if (hit && pos < cap) keys[(uint64_t)s * cap + pos] = (j << kTargetBits) | tgt;
+        } else {
+            mine += hit ? 1u : 0u;
         }
     }
     for (int o = 32; o > 0; o >>= 1) mine += __shfl_xor(mine, o);
-    if (lane_id() == 0 && mine) atomicAdd(&tot, mine);
+    if (lane == 0 && mine) atomicAdd(&tot, mine);
     __syncthreads();
     if (threadIdx.x == 0) cnt[s] = tot;
     if (hist && threadIdx.x < kGroups) {  // group g: smallest delay, then the others
@@ -226,9 +244,10 @@ __global__ __launch_bounds__(kBlock) void k_gen_count_rows(ConnArgs c, uint32_t 
 }
 
 // Draw the row twice: once to count per bucket (unless the count pass kept
-// the counts in hist), once to place.
+// the counts in hist), once to place (unless it kept the row's keys).
 __global__ __launch_bounds__(kBlock) void k_gen_fill_rows(ConnArgs c, const uint64_t *row_ptr,
-                                                         void *syn, RowIndex ix, const uint16_t *hist)
+                                                         void *syn, RowIndex ix, const uint16_t *hist,
+                                                         const uint32_t *keys, uint32_t cap)
 {
     __shared__ RowLDS L;
     const uint32_t s = blockIdx.x, tid = threadIdx.x;
@@ -252,6 +271,16 @@ __global__ __launch_bounds__(kBlock) void k_gen_fill_rows(ConnArgs c, const uint
         }
         scan_tiles(L, nb);
         write_row_index(c, ix, L, s, beg, len);
+        if (keys) {  // the row's synapses as the count pass kept them (len <= cap)
+            for (uint32_t k = tid; k < len; k += kBlock) {
+                const uint32_t key = keys[(uint64_t)s * cap + k];
+                const uint32_t tgt = rec_target(key), j = rec_delay(key);
+                const float w = syn_weight(c, s, mix64(rw ^ (uint64_t)tgt));
+                const uint32_t pos = atomicAdd(&L.cur[bucket_of(c, ix, tgt, j)], 1u);
+                put_syn(c, syn, beg + pos, j, tgt, s, w);
+            }
+            return;
+        }
         for (uint32_t tgt = tid; tgt < c.n; tgt += kBlock) {
             if (!((uint64_t)hash_hi32(mix64(rk ^ (uint64_t)tgt)) < c.conn_thr)) continue;
             const uint32_t j = c.lists > 1 ? hash_range(mix64(rd ^ (uint64_t)tgt), c.lists) : 0;
@@ -609,18 +638,19 @@ int cu_count()
     return cus;
 }
 
-hipError_t gen_count_rows(const ConnArgs &c, uint32_t *cnt, uint16_t *hist, hipStream_t s)
+hipError_t gen_count_rows(const ConnArgs &c, uint32_t *cnt, uint16_t *hist, uint32_t *keys, uint32_t cap,
+                          hipStream_t s)
 {
-    if (c.tl.T > kMaxTiles) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_gen_count_rows, dim3(c.n), dim3(kBlock), 0, s, c, cnt, hist);
+    if (c.tl.T > kMaxTiles || (keys && (!hist || c.n > kTargetMask + 1u))) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_gen_count_rows, dim3(c.n), dim3(kBlock), 0, s, c, cnt, hist, keys, cap);
     return hipGetLastError();
 }
 
 hipError_t gen_fill_rows(const ConnArgs &c, const uint64_t *row_ptr, void *syn, RowIndex ix,
-                         const uint16_t *hist, hipStream_t s)
+                         const uint16_t *hist, const uint32_t *keys, uint32_t cap, hipStream_t s)
 {
-    if (c.tl.T > kMaxTiles) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_gen_fill_rows, dim3(c.n), dim3(kBlock), 0, s, c, row_ptr, syn, ix, hist);
+    if (c.tl.T > kMaxTiles || (keys && !hist)) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_gen_fill_rows, dim3(c.n), dim3(kBlock), 0, s, c, row_ptr, syn, ix, hist, keys, cap);
     return hipGetLastError();
 }
 

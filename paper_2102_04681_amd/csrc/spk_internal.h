@@ -237,10 +237,14 @@ constexpr uint32_t kSplitMaxBuckets = 1024;  // split kernel: (delay, tile) buck
 
 // spk_gen.hip -- connectivity expansion
 // hist: optional (Bernoulli rows), n * (T + 2 * kGroups) u16 bucket counts
-// kept for gen_fill_rows, which then draws each row once instead of twice.
-hipError_t gen_count_rows(const ConnArgs &c, uint32_t *cnt, uint16_t *hist, hipStream_t s);
+// kept for gen_fill_rows, which then need not count the rows again; keys
+// (with hist): n * cap u32, the first cap synapses of every row kept as
+// (delay index << 24 | target), so that gen_fill_rows need not draw the rows
+// again either (valid where no row is longer than cap).
+hipError_t gen_count_rows(const ConnArgs &c, uint32_t *cnt, uint16_t *hist, uint32_t *keys, uint32_t cap,
+                          hipStream_t s);
 hipError_t gen_fill_rows(const ConnArgs &c, const uint64_t *row_ptr, void *syn, RowIndex ix,
-                         const uint16_t *hist, hipStream_t s);
+                         const uint16_t *hist, const uint32_t *keys, uint32_t cap, hipStream_t s);
 hipError_t gen_in_count(const ConnArgs &c, uint32_t *cnt, hipStream_t s);
 hipError_t gen_in_fill(const ConnArgs &c, const uint64_t *row_ptr, uint32_t *cursor, void *syn,
                        hipStream_t s);

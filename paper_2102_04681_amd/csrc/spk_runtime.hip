@@ -738,12 +738,30 @@ spk_status generate(spk_net *net)
     if (net->P.conn_kind == SPK_CONN_BERNOULLI && hist_elems * 2 <= (4ull << 30) &&
         dalloc(net, &hist, hist_elems) != SPK_OK)
         hist = nullptr;  // (then the placement pass counts for itself)
+    // ... and keeps each row's synapses, up to cap = mean + 10 sd + 64 per
+    // row, so that the placement pass need not draw the rows again (unless a
+    // row turns out longer, or the keys would take more than 32 GB)
+    uint32_t *keys = nullptr;
+    uint32_t cap = 0;
+    const char *gk = std::getenv("SPK_GEN_KEYS");
+    if (hist && !(gk && std::strcmp(gk, "0") == 0)) {
+        const double p = net->P.p, nn = (double)net->n;
+        const double capd = std::ceil(p * nn + 10.0 * std::sqrt(nn * p * (1.0 - p)) + 64.0);
+        if (capd <= (double)kMaxRow && (double)net->n * capd * 4.0 <= (double)(32ull << 30)) {
+            cap = (uint32_t)capd;
+            if (dalloc(net, &keys, (size_t)net->n * cap) != SPK_OK) keys = nullptr;
+        }
+    }
     SegTimer tm;
     SPK_HIP(tm.start(s));
     if (in_rows) SPK_HIP(gen_in_count(c, cnt, s));
-    else SPK_HIP(gen_count_rows(c, cnt, hist, s));
+    else SPK_HIP(gen_count_rows(c, cnt, hist, keys, cap, s));
     SPK_HIP(tm.stop(s, &net->gen_ms));
     SPK_TRY(finish_counts(net, cnt));
+    if (keys && net->max_row > cap) {  // a row did not fit: placement draws the rows again
+        dfree(net, keys);
+        keys = nullptr;
+    }
     RowIndex ix{};
     SPK_TRY(choose_delivery(net, &ix));
     void *syn = nullptr;
@@ -761,12 +779,13 @@ spk_status generate(spk_net *net)
         dfree(net, tmp);
     } else {        // drawn per source, bucketed while drawn
         SPK_HIP(tm.start(s));
-        SPK_HIP(gen_fill_rows(c, net->row_ptr, syn, ix, hist, s));
+        SPK_HIP(gen_fill_rows(c, net->row_ptr, syn, ix, hist, keys, cap, s));
         SPK_HIP(tm.stop(s, &net->gen_ms));
     }
     SPK_HIP(hipStreamSynchronize(s));
     dfree(net, cnt);
     dfree(net, hist);
+    dfree(net, keys);
     return finish_rows(net);
 }
 

@@ -114,6 +114,22 @@ GEN_CASES = [
 FORMATS = [(1, "full"), (0, "auto")]
 
 
+@pytest.mark.parametrize("name", ["C0", "C1-3000", "bern-delays"])
+def test_generator_two_draws_equals_oracle(spk, name, monkeypatch):
+    """Bernoulli rows placed by drawing every row a second time (the path
+    taken where a row is longer than the first pass can keep) equal the
+    oracle's rows too."""
+    monkeypatch.setenv("SPK_GEN_KEYS", "0")
+    cfg = dict(GEN_CASES)[name]()
+    _say(f"[gen two draws] {name} n={cfg['n']}")
+    g = spk.Net(cfg, max_steps=1)
+    o = oracle.Net(cfg)
+    o_rp, o_col, o_w, o_d = o.csr()
+    assert g.stats()["nnz"] == len(o_col)
+    offs, col, w, d = g.csr()
+    _compare_rows(offs, col, w, d, o_rp, o_col, o_w, o_d, range(cfg["n"]), cfg["acc_mode"] == I.ACC_FIXED)
+
+
 @pytest.mark.parametrize("name,mk", GEN_CASES, ids=[c[0] for c in GEN_CASES])
 @pytest.mark.parametrize("fmt", [f for f, _ in FORMATS], ids=[n for _, n in FORMATS])
 def test_generator_equals_oracle(spk, name, mk, fmt):
