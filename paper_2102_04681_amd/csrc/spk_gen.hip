@@ -310,6 +310,10 @@ __global__ __launch_bounds__(kBlock) void k_gen_fill_rows(ConnArgs c, const uint
 // ------------------------------------------------- fixed in-degree rows
 // One block per target draws its sources; synapses are regrouped by source
 // through global atomic cursors (unordered), then bucketed by bucket_rows.
+// For networks of up to kInRanges * kInRange neurons, blocks of kInThreads
+// take a run of targets each and count their draws per source in LDS, one
+// range of kInRange sources at a time: one global update per (block,
+// source) instead of one per synapse, for a few more passes of hashes.
 __device__ __forceinline__ uint32_t in_source(const ConnArgs &c, uint64_t re, uint64_t ri,
                                               uint32_t q)
 {
@@ -325,6 +329,78 @@ __global__ __launch_bounds__(kBlock) void k_gen_in_count(ConnArgs c, uint32_t *c
     const uint32_t kin = c.k_in_exc + c.k_in_inh;
     for (uint32_t q = threadIdx.x; q < kin; q += kBlock)
         atomicAdd(&cnt[in_source(c, re, ri, q)], 1u);
+}
+
+constexpr uint32_t kInThreads = 1024, kInRange = 32768, kInRanges = 8, kInBlocks = 1024;
+
+// The draws of targets [t0, t1) that land in sources [r0, r0 + rn), counted
+// into h[src - r0].
+__device__ void in_range_counts(const ConnArgs &c, uint32_t t0, uint32_t t1, uint32_t r0, uint32_t rn,
+                                uint32_t *h)
+{
+    const uint32_t kin = c.k_in_exc + c.k_in_inh;
+    for (uint32_t tgt = t0; tgt < t1; tgt++) {
+        const uint64_t re = mix64(c.keys.src_e ^ (uint64_t)tgt);
+        const uint64_t ri = mix64(c.keys.src_i ^ (uint64_t)tgt);
+        for (uint32_t q = threadIdx.x; q < kin; q += kInThreads) {
+            const uint32_t k = in_source(c, re, ri, q) - r0;
+            if (k < rn) atomicAdd(&h[k], 1u);
+        }
+    }
+}
+
+__global__ __launch_bounds__(kInThreads) void k_gen_in_count_lds(ConnArgs c, uint32_t tpb, uint32_t *cnt)
+{
+    __shared__ uint32_t h[kInRange];
+    const uint32_t t0 = blockIdx.x * tpb;
+    if (t0 >= c.n) return;
+    const uint32_t t1 = c.n - t0 < tpb ? c.n : t0 + tpb;
+    for (uint32_t r0 = 0; r0 < c.n; r0 += kInRange) {
+        const uint32_t rn = c.n - r0 < kInRange ? c.n - r0 : kInRange;
+        for (uint32_t k = threadIdx.x; k < rn; k += kInThreads) h[k] = 0;
+        __syncthreads();
+        in_range_counts(c, t0, t1, r0, rn, h);
+        __syncthreads();
+        for (uint32_t k = threadIdx.x; k < rn; k += kInThreads)
+            if (h[k]) atomicAdd(&cnt[r0 + k], h[k]);
+        __syncthreads();
+    }
+}
+
+__global__ __launch_bounds__(kInThreads) void k_gen_in_fill_lds(ConnArgs c, uint32_t tpb, const uint64_t *row_ptr,
+                                                               uint32_t *cursor, void *syn)
+{
+    __shared__ uint32_t h[kInRange];
+    const uint32_t t0 = blockIdx.x * tpb;
+    if (t0 >= c.n) return;
+    const uint32_t t1 = c.n - t0 < tpb ? c.n : t0 + tpb;
+    const uint32_t kin = c.k_in_exc + c.k_in_inh;
+    for (uint32_t r0 = 0; r0 < c.n; r0 += kInRange) {
+        const uint32_t rn = c.n - r0 < kInRange ? c.n - r0 : kInRange;
+        for (uint32_t k = threadIdx.x; k < rn; k += kInThreads) h[k] = 0;
+        __syncthreads();
+        in_range_counts(c, t0, t1, r0, rn, h);
+        __syncthreads();
+        // this block's first position in each row of the range
+        for (uint32_t k = threadIdx.x; k < rn; k += kInThreads)
+            if (h[k]) h[k] = atomicAdd(&cursor[r0 + k], h[k]);
+        __syncthreads();
+        for (uint32_t tgt = t0; tgt < t1; tgt++) {
+            const uint64_t re = mix64(c.keys.src_e ^ (uint64_t)tgt);
+            const uint64_t ri = mix64(c.keys.src_i ^ (uint64_t)tgt);
+            const uint64_t rd = mix64(c.keys.delay ^ (uint64_t)tgt);
+            const uint64_t rw = mix64(c.keys.w ^ (uint64_t)tgt);
+            for (uint32_t q = threadIdx.x; q < kin; q += kInThreads) {
+                const uint32_t src = in_source(c, re, ri, q);
+                if (src - r0 >= rn) continue;
+                const uint32_t j = c.lists > 1 ? hash_range(mix64(rd ^ (uint64_t)q), c.lists) : 0;
+                const float w = syn_weight(c, src, mix64(rw ^ (uint64_t)q));
+                const uint32_t pos = atomicAdd(&h[src - r0], 1u);
+                put_syn(c, syn, row_ptr[src] + pos, j, tgt, src, w);
+            }
+        }
+        __syncthreads();
+    }
 }
 
 __global__ __launch_bounds__(kBlock) void k_gen_in_fill(ConnArgs c, const uint64_t *row_ptr,
@@ -654,16 +730,31 @@ hipError_t gen_fill_rows(const ConnArgs &c, const uint64_t *row_ptr, void *syn, 
     return hipGetLastError();
 }
 
+// block-local counting where the source ranges are few (see above)
+static bool in_rows_lds(const ConnArgs &c) { return c.n <= kInRanges * kInRange; }
+static uint32_t in_rows_tpb(const ConnArgs &c) { return (c.n + kInBlocks - 1) / kInBlocks; }
+
 hipError_t gen_in_count(const ConnArgs &c, uint32_t *cnt, hipStream_t s)
 {
-    hipLaunchKernelGGL(k_gen_in_count, dim3(c.n), dim3(kBlock), 0, s, c, cnt);
+    if (in_rows_lds(c)) {
+        const uint32_t tpb = in_rows_tpb(c);
+        hipLaunchKernelGGL(k_gen_in_count_lds, dim3((c.n + tpb - 1) / tpb), dim3(kInThreads), 0, s, c, tpb, cnt);
+    } else {
+        hipLaunchKernelGGL(k_gen_in_count, dim3(c.n), dim3(kBlock), 0, s, c, cnt);
+    }
     return hipGetLastError();
 }
 
 hipError_t gen_in_fill(const ConnArgs &c, const uint64_t *row_ptr, uint32_t *cursor, void *syn,
                        hipStream_t s)
 {
-    hipLaunchKernelGGL(k_gen_in_fill, dim3(c.n), dim3(kBlock), 0, s, c, row_ptr, cursor, syn);
+    if (in_rows_lds(c)) {
+        const uint32_t tpb = in_rows_tpb(c);
+        hipLaunchKernelGGL(k_gen_in_fill_lds, dim3((c.n + tpb - 1) / tpb), dim3(kInThreads), 0, s, c, tpb, row_ptr,
+                           cursor, syn);
+    } else {
+        hipLaunchKernelGGL(k_gen_in_fill, dim3(c.n), dim3(kBlock), 0, s, c, row_ptr, cursor, syn);
+    }
     return hipGetLastError();
 }
 
