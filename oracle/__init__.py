@@ -100,7 +100,9 @@ def lib():
         L.orc_deliver.restype = i32
         L.orc_deliver.argtypes = [P, P, u64, u32, P, P]
         L.orc_run.restype = i32
-        L.orc_run.argtypes = [P, u64, P, P, P, u64, P]
+        L.orc_run.argtypes = [P, u64, P, P, P, P, u64, P]
+        L.orc_pair.restype = i32
+        L.orc_pair.argtypes = [P, u32, u32, C.POINTER(C.c_int), C.POINTER(C.c_float), C.POINTER(C.c_uint8)]
         L.orc_get_state.restype = i32
         L.orc_get_state.argtypes = [P, P, P]
         L.orc_step_index.restype = u64
@@ -238,14 +240,26 @@ class Net:
         return (out_f, out_q) if fixed else out_f
 
     def run(self, n_steps: int, raster_cap: int | None = None):
+        """Run n_steps; per-step spike counts, events emitted, events
+        delivered (arriving), and the raster (offs, IDs ascending per step).
+        A network made with build_csr=False generates each spike's row when
+        it is delivered (Bernoulli and fixed out-degree)."""
         counts = np.zeros(n_steps, dtype=np.uint32)
         events = np.zeros(n_steps, dtype=np.uint64)
+        delivered = np.zeros(n_steps, dtype=np.uint64)
         offs = np.zeros(n_steps + 1, dtype=np.uint64)
         cap = raster_cap if raster_cap is not None else n_steps * self.n
         raster = np.zeros(max(cap, 1), dtype=np.uint32)
-        _check(lib().orc_run(self._h, n_steps, _ptr(counts), _ptr(events), _ptr(raster), cap,
-                             _ptr(offs)), "run")
-        return dict(counts=counts, events=events, offs=offs, raster=raster[:int(offs[-1])].copy())
+        _check(lib().orc_run(self._h, n_steps, _ptr(counts), _ptr(events), _ptr(delivered), _ptr(raster),
+                             cap, _ptr(offs)), "run")
+        return dict(counts=counts, events=events, delivered=delivered, offs=offs,
+                    raster=raster[:int(offs[-1])].copy())
+
+    def pair(self, s: int, tgt: int):
+        """Bernoulli networks: (connected, weight, delay) of the pair s -> tgt."""
+        c, w, d = C.c_int(), C.c_float(), C.c_uint8()
+        _check(lib().orc_pair(self._h, s, tgt, C.byref(c), C.byref(w), C.byref(d)), "pair")
+        return bool(c.value), np.float32(w.value), int(d.value)
 
     def state(self):
         v = np.zeros(self.n, dtype=np.float32)

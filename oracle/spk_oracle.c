@@ -50,6 +50,7 @@ struct orc_net {
     uint8_t *ref;
     float *slot_f;         /* ring * n, fp32 mode */
     int64_t *slot_q;       /* ring * n, fixed mode */
+    uint64_t *arrive;      /* ring: synapses whose spike arrives at each pending step */
     uint64_t pois_thr[ORC_POIS_CAP];
     uint64_t t;
 };
@@ -216,27 +217,34 @@ static int syn_cmp(const void *a, const void *b)
     return 0;
 }
 
-/* weight of a synapse from source s; h is the W-stream hash of the draw */
-static float syn_weight(const orc_net *net, uint32_t s, uint64_t h)
+/* Weight of a synapse from source s, drawn at coordinates (a, b) of the
+ * W stream: per synapse w_lo + (w_hi - w_lo) * u24 (two fp32 operations),
+ * else the weight of the source's population (Sec. III-A: the static models
+ * keep one weight per population). */
+static float syn_weight(const orc_net *net, uint32_t s, uint64_t a, uint64_t b)
 {
     const orc_params *P = &net->P;
     if (P->w_uniform) {
         float span = P->w_hi - P->w_lo;
-        float t = span * u24(h);
+        float t = span * u24(orc_hash(P->seed, ORC_TAG_W, a, b));
         return P->w_lo + t;
     }
     return s < net->D.n_exc ? P->w_exc : P->w_inh;
 }
 
-static uint8_t syn_delay(const orc_net *net, uint64_t h)
+/* Delay (steps) of the synapse drawn at coordinates (a, b) of the DELAY
+ * stream: uniform over [delay_min, delay_max]. */
+static uint8_t syn_delay(const orc_net *net, uint64_t a, uint64_t b)
 {
     if (net->dspan == 1) return (uint8_t)net->P.delay_min;
-    return (uint8_t)(net->P.delay_min + range_n(h, net->dspan));
+    return (uint8_t)(net->P.delay_min + range_n(orc_hash(net->P.seed, ORC_TAG_DELAY, a, b), net->dspan));
 }
 
 /* Generate the row of source s into buf (cap entries); Bernoulli and fixed
- * out-degree only.  Returns the row length, or -1 if cap is too small. */
-static long long gen_row(const orc_net *net, uint32_t s, orc_syn *buf, uint64_t cap)
+ * out-degree only.  sorted: put the row in canonical order (the stored
+ * rows' order; fixed-point sums do not depend on it).  Returns the row
+ * length, or -1 if cap is too small. */
+static long long gen_row(const orc_net *net, uint32_t s, orc_syn *buf, uint64_t cap, int sorted)
 {
     const orc_params *P = &net->P;
     uint64_t len = 0;
@@ -246,8 +254,8 @@ static long long gen_row(const orc_net *net, uint32_t s, orc_syn *buf, uint64_t 
             if (!(hi32(orc_hash(P->seed, ORC_TAG_CONN, s, tgt)) < net->D.conn_thr)) continue;
             if (len >= cap) return -1;
             buf[len].tgt = tgt;
-            buf[len].d = syn_delay(net, orc_hash(P->seed, ORC_TAG_DELAY, s, tgt));
-            buf[len].w = syn_weight(net, s, orc_hash(P->seed, ORC_TAG_W, s, tgt));
+            buf[len].d = syn_delay(net, s, tgt);
+            buf[len].w = syn_weight(net, s, s, tgt);
             len++;
         }
     } else if (P->conn_kind == ORC_CONN_FIXED_OUT) {
@@ -255,14 +263,14 @@ static long long gen_row(const orc_net *net, uint32_t s, orc_syn *buf, uint64_t 
         if (P->k_out > cap) return -1;
         for (uint32_t j = 0; j < P->k_out; j++) {
             buf[j].tgt = range_n(orc_hash(P->seed, ORC_TAG_TGT, s, j), P->n);
-            buf[j].d = syn_delay(net, orc_hash(P->seed, ORC_TAG_DELAY, s, j));
-            buf[j].w = syn_weight(net, s, orc_hash(P->seed, ORC_TAG_W, s, j));
+            buf[j].d = syn_delay(net, s, j);
+            buf[j].w = syn_weight(net, s, s, j);
         }
         len = P->k_out;
     } else {
         return -2;
     }
-    qsort(buf, (size_t)len, sizeof(orc_syn), syn_cmp);
+    if (sorted) qsort(buf, (size_t)len, sizeof(orc_syn), syn_cmp);
     return (long long)len;
 }
 
@@ -290,7 +298,7 @@ static int build_rows(orc_net *net)
     net->row_ptr[0] = 0;
     for (uint32_t s = 0; s < n; s++) {
         long long L = P->conn_kind == ORC_CONN_FIXED_OUT ? (long long)P->k_out
-                                                           : gen_row(net, s, buf, cap);
+                                                           : gen_row(net, s, buf, cap, 0);
         if (L < 0) { free(buf); return ORC_EINVAL; }
         net->row_ptr[s + 1] = net->row_ptr[s] + (uint64_t)L;
     }
@@ -298,7 +306,7 @@ static int build_rows(orc_net *net)
     if (rc) { free(buf); return rc; }
     /* pass 2: fill */
     for (uint32_t s = 0; s < n; s++) {
-        long long L = gen_row(net, s, buf, cap);
+        long long L = gen_row(net, s, buf, cap, 1);
         uint64_t o = net->row_ptr[s];
         for (long long e = 0; e < L; e++) {
             net->col[o + e] = buf[e].tgt;
@@ -347,8 +355,8 @@ static int build_fixed_in(orc_net *net)
             uint32_t src = fixed_in_src(net, tgt, j);
             uint64_t o = cnt[src]++;
             net->col[o] = tgt;
-            net->delay[o] = syn_delay(net, orc_hash(P->seed, ORC_TAG_DELAY, tgt, j));
-            net->w[o] = syn_weight(net, src, orc_hash(P->seed, ORC_TAG_W, tgt, j));
+            net->delay[o] = syn_delay(net, tgt, j);
+            net->w[o] = syn_weight(net, src, tgt, j);
         }
     free(cnt);
     return ORC_OK;
@@ -436,7 +444,8 @@ static int init_state(orc_net *net)
         net->slot_q = (int64_t *)calloc(slots, sizeof(int64_t));
     else
         net->slot_f = (float *)calloc(slots, sizeof(float));
-    if (!net->V || !net->ref || (!net->slot_q && !net->slot_f)) return ORC_ENOMEM;
+    net->arrive = (uint64_t *)calloc(net->D.ring, sizeof(uint64_t));
+    if (!net->V || !net->ref || (!net->slot_q && !net->slot_f) || !net->arrive) return ORC_ENOMEM;
     /* V0 = v0_lo + (v0_hi - v0_lo) * u, u uniform in [0,1) */
     float span = P->v0_hi - P->v0_lo;
     for (uint32_t i = 0; i < n; i++) {
@@ -516,7 +525,7 @@ void orc_destroy(orc_net *net)
 {
     if (!net) return;
     free(net->row_ptr); free(net->col); free(net->w); free(net->delay); free(net->wq);
-    free(net->V); free(net->ref); free(net->slot_f); free(net->slot_q);
+    free(net->V); free(net->ref); free(net->slot_f); free(net->slot_q); free(net->arrive);
     free(net);
 }
 
@@ -558,7 +567,7 @@ int orc_row(orc_net *net, uint32_t s, uint32_t *tgt, float *w, uint8_t *delay,
     uint64_t bcap = net->P.conn_kind == ORC_CONN_BERNOULLI ? net->P.n : net->P.k_out;
     orc_syn *buf = (orc_syn *)malloc((size_t)(bcap ? bcap : 1) * sizeof(orc_syn));
     if (!buf) return ORC_ENOMEM;
-    long long L = gen_row(net, s, buf, bcap);
+    long long L = gen_row(net, s, buf, bcap, 1);
     if (L < 0) { free(buf); return ORC_EINVAL; }
     *len = (uint64_t)L;
     if ((uint64_t)L > cap) { free(buf); return ORC_EOVERFLOW; }
@@ -583,9 +592,21 @@ int orc_in_row(const orc_net *net, uint32_t tgt, uint32_t *src, float *w, uint8_
     if (kin > cap) return ORC_EOVERFLOW;
     for (uint32_t j = 0; j < kin; j++) {
         src[j] = fixed_in_src(net, tgt, j);
-        delay[j] = syn_delay(net, orc_hash(P->seed, ORC_TAG_DELAY, tgt, j));
-        w[j] = syn_weight(net, src[j], orc_hash(P->seed, ORC_TAG_W, tgt, j));
+        delay[j] = syn_delay(net, tgt, j);
+        w[j] = syn_weight(net, src[j], tgt, j);
     }
+    return ORC_OK;
+}
+
+int orc_pair(const orc_net *net, uint32_t s, uint32_t tgt, int *connected, float *w, uint8_t *delay)
+{
+    const orc_params *P = &net->P;
+    if (P->conn_kind != ORC_CONN_BERNOULLI || s >= P->n || tgt >= P->n) return ORC_EINVAL;
+    /* Sec. III-B: every ordered pair is connected independently with
+     * probability p */
+    *connected = hi32(orc_hash(P->seed, ORC_TAG_CONN, s, tgt)) < net->D.conn_thr;
+    *w = syn_weight(net, s, s, tgt);
+    *delay = syn_delay(net, s, tgt);
     return ORC_OK;
 }
 
@@ -618,7 +639,7 @@ int orc_deliver(orc_net *net, const uint32_t *spikes, uint64_t n_spikes,
                 }
             }
         } else {
-            long long L = gen_row(net, s, buf, bcap);
+            long long L = gen_row(net, s, buf, bcap, 0);
             for (long long e = 0; e < L; e++) {
                 if (delay && buf[e].d != delay) continue;
                 if (out_f) out_f[buf[e].tgt] += (double)buf[e].w;
@@ -694,15 +715,38 @@ int orc_update_one(const orc_net *net, uint64_t t, uint32_t i, float v, uint8_t 
 
 /* ----------------------------------------------------------------- run */
 
-int orc_run(orc_net *net, uint64_t n_steps, uint32_t *counts, uint64_t *events,
-            uint32_t *raster, uint64_t raster_cap, uint64_t *offs)
+/* Add one synapse (target tgt, weight w, delay d) of a spike of step t to
+ * the input of step t + d. */
+static void push_synapse(orc_net *net, uint64_t t, uint32_t tgt, float w, int32_t wq, uint8_t d)
 {
-    if (!net->have_csr) return ORC_EINVAL;
+    uint32_t R = net->D.ring;
+    size_t slot = (size_t)((t + d) % R) * net->P.n + tgt;
+    if (net->P.acc_mode == ORC_ACC_FIXED) net->slot_q[slot] += wq;
+    else                                  net->slot_f[slot] += w;
+    net->arrive[(t + d) % R] += 1;
+}
+
+int orc_run(orc_net *net, uint64_t n_steps, uint32_t *counts, uint64_t *events,
+            uint64_t *delivered, uint32_t *raster, uint64_t raster_cap, uint64_t *offs)
+{
     const orc_params *P = &net->P;
     uint32_t n = P->n, R = net->D.ring;
     int fixed = P->acc_mode == ORC_ACC_FIXED;
+    /* Without the stored CSR (Bernoulli and fixed out-degree networks too
+     * large to store here), the row of every spike is generated when the
+     * spike is delivered: the same rows, in canonical order in fp32 mode
+     * (where the order of the fp32 additions matters) and in draw order in
+     * fixed-point mode (integer sums do not depend on it). */
+    uint64_t bcap = 0;
+    orc_syn *buf = NULL;
+    if (!net->have_csr) {
+        if (P->conn_kind != ORC_CONN_BERNOULLI && P->conn_kind != ORC_CONN_FIXED_OUT) return ORC_EINVAL;
+        bcap = P->conn_kind == ORC_CONN_BERNOULLI ? n : P->k_out;
+        buf = (orc_syn *)malloc((size_t)(bcap ? bcap : 1) * sizeof(orc_syn));
+        if (!buf) return ORC_ENOMEM;
+    }
     uint32_t *S = (uint32_t *)malloc((size_t)n * sizeof(uint32_t));
-    if (!S) return ORC_ENOMEM;
+    if (!S) { free(buf); return ORC_ENOMEM; }
     uint64_t rl = 0;
     if (offs) offs[0] = 0;
     int rc = ORC_OK;
@@ -720,21 +764,32 @@ int orc_run(orc_net *net, uint64_t n_steps, uint32_t *counts, uint64_t *events,
             if (s < 0) { rc = ORC_EOVERFLOW; goto done; }
             if (s) S[ns++] = i;
         }
+        uint64_t arrived = net->arrive[t % R];
+        net->arrive[t % R] = 0;
         /* 2. deliver every spike of step t to all neighbours in its row;
          *    a synapse of delay d feeds the input of step t + d */
         uint64_t ev = 0;
         for (uint32_t k = 0; k < ns; k++) {
             uint32_t s = S[k];
-            for (uint64_t e = net->row_ptr[s]; e < net->row_ptr[s + 1]; e++) {
-                size_t slot = (size_t)((t + net->delay[e]) % R) * n + net->col[e];
-                if (fixed) net->slot_q[slot] += net->wq[e];
-                else       net->slot_f[slot] += net->w[e];
+            if (net->have_csr) {
+                for (uint64_t e = net->row_ptr[s]; e < net->row_ptr[s + 1]; e++)
+                    push_synapse(net, t, net->col[e], net->w[e], fixed ? net->wq[e] : 0, net->delay[e]);
+                ev += net->row_ptr[s + 1] - net->row_ptr[s];
+            } else {
+                long long L = gen_row(net, s, buf, bcap, !fixed);
+                if (L < 0) { rc = ORC_EINVAL; goto done; }
+                for (long long e = 0; e < L; e++) {
+                    int32_t q = 0;
+                    if (fixed && quantise(buf[e].w, P->fixed_shift, &q)) { rc = ORC_EOVERFLOW; goto done; }
+                    push_synapse(net, t, buf[e].tgt, buf[e].w, q, buf[e].d);
+                }
+                ev += (uint64_t)L;
             }
-            ev += net->row_ptr[s + 1] - net->row_ptr[s];
         }
         /* 3. record */
         if (counts) counts[step] = ns;
         if (events) events[step] = ev;
+        if (delivered) delivered[step] = arrived;
         if (raster) {
             if (rl + ns > raster_cap) { rc = ORC_EOVERFLOW; goto done; }
             memcpy(raster + rl, S, (size_t)ns * sizeof(uint32_t));
@@ -745,6 +800,7 @@ int orc_run(orc_net *net, uint64_t n_steps, uint32_t *counts, uint64_t *events,
     }
 done:
     free(S);
+    free(buf);
     return rc;
 }
 

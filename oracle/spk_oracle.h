@@ -113,10 +113,18 @@ int orc_in_row(const orc_net *net, uint32_t tgt, uint32_t *src, float *w, uint8_
  * quantised weight (int64).  Either output may be NULL. */
 int orc_deliver(orc_net *net, const uint32_t *spikes, uint64_t n_spikes,
                 uint32_t delay, double *out_f, int64_t *out_q);
-/* Run n steps.  counts/events: n entries each (may be NULL).  raster: IDs of
- * every step ascending, concatenated; offs: n+1 entries (may be NULL). */
+/* Run n steps.  counts/events/delivered: n entries each (may be NULL):
+ * spikes, synapses of the spikes emitted at the step, synapses whose spike
+ * arrives at the step.  raster: IDs of every step ascending, concatenated;
+ * offs: n+1 entries (may be NULL).  A network created without its CSR
+ * (Bernoulli or fixed out-degree) generates the row of each spike when it
+ * is delivered. */
 int orc_run(orc_net *net, uint64_t n_steps, uint32_t *counts, uint64_t *events,
-            uint32_t *raster, uint64_t raster_cap, uint64_t *offs);
+            uint64_t *delivered, uint32_t *raster, uint64_t raster_cap, uint64_t *offs);
+/* Bernoulli networks: whether source s connects to tgt, and the weight and
+ * delay that synapse has (drawn whether or not it exists). */
+int orc_pair(const orc_net *net, uint32_t s, uint32_t tgt, int *connected, float *w,
+             uint8_t *delay);
 int orc_get_state(const orc_net *net, float *v, uint8_t *ref);
 uint64_t orc_step_index(const orc_net *net);
 /* The update of one neuron in isolation: state (v, ref) at the start of step

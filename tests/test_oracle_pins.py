@@ -436,3 +436,208 @@ def test_driven_workloads_are_active():
     r = net.run(1000)
     rate = r["counts"][200:].sum() / (1000 * 800 * 1e-4)
     assert 5.0 < rate < 100.0
+
+
+# ------------------------------------------------------- pins added later
+
+_GAMMA = 0x9E3779B97F4A7C15
+_M64 = (1 << 64) - 1
+HASH_0100 = 0xD1C0270687984B37  # H(seed 0, tag 1, 0, 0), derived in test_hash_chain_fixed_values
+
+
+def _splitmix_py(z):
+    """SplitMix64's output step on state z, written from its published
+    definition (Steele, Lea & Flood 2014): z += gamma, then
+    z = (z ^ z>>30) * 0xBF58476D1CE4E5B9, z = (z ^ z>>27) * 0x94D049BB133111EB,
+    return z ^ z>>31 (all mod 2^64).  Checked below against the generator's
+    published first outputs, independently of the oracle."""
+    z = (z + _GAMMA) & _M64
+    z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & _M64
+    z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & _M64
+    return z ^ (z >> 31)
+
+
+def test_hash_chain_fixed_values():
+    # The reference generator started from state 0 outputs E220A8397B1DCDAF,
+    # 6E789E6AA1B965F4, 06C45D188009454F: the Python mixer above reproduces
+    # them, so it is SplitMix64.  The hash of every random decision is the
+    # chain H(seed, tag, a, b) = mix(mix(mix(mix(seed) ^ tag) ^ a) ^ b) and
+    # the per-step draw mix(mix(mix(seed) ^ tag) ^ (t << 32 | i)); a wrong
+    # link order, xor or counter packing in the oracle changes these values.
+    assert [_splitmix_py(k * _GAMMA & _M64) for k in range(3)] == \
+        [0xE220A8397B1DCDAF, 0x6E789E6AA1B965F4, 0x06C45D188009454F]
+    cases = [(0, 1, 0, 0), (1, TAG["TGT"], 12345, 7), (3, TAG["W"], 999_999, 999),
+             (2**63 + 5, TAG["DELAY"], 2**40 + 3, 2**33 + 1), (42, TAG["V0"], 1_999_999, 0)]
+    for seed, tag, a, b in cases:
+        want = _splitmix_py(_splitmix_py(_splitmix_py(_splitmix_py(seed) ^ tag) ^ a) ^ b)
+        assert oracle.hash64(seed, tag, a, b) == want, (seed, tag, a, b)
+    for seed, tag, i, t in [(1, TAG["POIS"], 0, 0), (1, TAG["POIS"], 1_999_999, 4999),
+                            (7, TAG["BERN"], 123_456, 77)]:
+        key = _splitmix_py(_splitmix_py(seed) ^ tag)
+        assert oracle.hash_step(seed, tag, i, t) == _splitmix_py(key ^ (t << 32 | i))
+    # one value spelled out: H(0, 1, 0, 0) = mix(mix(mix(E220A8397B1DCDAF ^ 1))),
+    # E220A8397B1DCDAF being the published first output from state 0
+    assert _splitmix_py(_splitmix_py(_splitmix_py(0xE220A8397B1DCDAF ^ 1))) == HASH_0100
+    assert oracle.hash64(0, 1, 0, 0) == HASH_0100
+
+
+def _u24_f32(h):
+    return np.float32(h >> 40) * np.float32(2.0**-24)
+
+
+@pytest.mark.parametrize("lo,hi", [(0.0, 1e-3), (-0.5, 1.5)])
+def test_per_synapse_uniform_weights(lo, hi):
+    # Per-synapse weights (the 1e6-source stress network draws w ~ U[0, 1e-3)):
+    # synapse j of source s has target range(H(seed, TGT, s, j), n) and weight
+    # w_lo + (w_hi - w_lo) * u24(H(seed, W, s, j)), each operation in fp32.
+    # Brute force over every (s, j) against the stored rows, plus the range
+    # and the moments of U[lo, hi).
+    n, k, seed = 300, 60, 5
+    cfg = I.config(3, n=n, k_out=k, seed=seed, w_lo=lo, w_hi=hi)
+    net = oracle.Net(cfg)
+    rp, col, w, d = net.csr()
+    span = np.float32(np.float32(hi) - np.float32(lo))
+    for s in range(n):
+        want = []
+        for j in range(k):
+            t = ((oracle.hash64(seed, TAG["TGT"], s, j) >> 32) * n) >> 32
+            wj = np.float32(np.float32(lo) + np.float32(span * _u24_f32(oracle.hash64(seed, TAG["W"], s, j))))
+            want.append((t, int(wj.view(np.uint32))))
+        a, b = int(rp[s]), int(rp[s + 1])
+        got = sorted(zip(col[a:b].tolist(), w[a:b].view(np.uint32).tolist()))
+        assert got == sorted(want), s
+    wf = w.astype(np.float64)
+    assert wf.min() >= lo and wf.max() < hi
+    m = len(wf)
+    mu, var = (lo + hi) / 2, (hi - lo) ** 2 / 12
+    assert abs(wf.mean() - mu) < 5 * math.sqrt(var / m)
+    assert abs(wf.var() / var - 1) < 5 * math.sqrt(0.8 / m)  # var of U^2-type estimator: 4/5 var^2
+    assert stats.kstest((wf - lo) / (hi - lo), "uniform").pvalue > 1e-3
+    # the lazily generated rows (no CSR) carry the same weights
+    lazy = oracle.Net(cfg, build_csr=False)
+    for s in (0, 17, n - 1):
+        lt, lw, _ = lazy.row(s, cap=k)
+        a, b = int(rp[s]), int(rp[s + 1])
+        assert lt.tolist() == col[a:b].tolist() and lw.view(np.uint32).tolist() == w[a:b].view(np.uint32).tolist()
+
+
+@pytest.mark.parametrize("v0", [-55.0, -40.0, -70.0])
+def test_source_neurons_integrate_without_reset(v0):
+    # Bernoulli source neurons keep integrating their input (no threshold, no
+    # reset, no refractory period): with no input V follows the Euler decay
+    # closed form whatever their firing, and with a constant input I it
+    # converges to V* = V_rest + I/k even above V_th.
+    k = float(np.float32(0.1 / 20.0))
+    bound = (1.0 / k) * 2.0 * np.spacing(np.float32(64.0))
+    for rate in (0.0, 1e4):  # p = rate * dt: never / every step
+        net = _isolated(n=3, neuron_kind=I.SOURCE, v0_lo=v0, v0_hi=v0, src_rate_hz=rate)
+        for n_steps in (1, 50, 2000):
+            while net.t < n_steps:
+                r = net.run(1)
+                assert int(r["counts"][0]) == (3 if rate else 0)
+            v, ref = net.state()
+            exact = -60.0 + (v0 + 60.0) * (1.0 - k) ** n_steps
+            assert np.all(np.abs(v.astype(np.float64) - exact) <= bound), (rate, n_steps, v, exact)
+            assert not ref.any()
+    ib = 0.1  # V* = -60 + 0.1/0.005 = -40 mV, above V_th = -50
+    net = _isolated(n=1, neuron_kind=I.SOURCE, v0_lo=-60.0, v0_hi=-60.0, i_bias=ib, src_rate_hz=1e4)
+    net.run(6000)
+    v, _ = net.state()
+    vstar = -60.0 + ib / k
+    assert v[0] > -50.0 and abs(float(v[0]) - vstar) < 1e-3
+
+
+def _guard_net(w, i_bias=0.0):
+    """Targets 2 receives +w from source 0 and -w from source 1 (fixed point,
+    S = 20): the signed sum is 0, the sum of magnitudes 2 w 2^20."""
+    row_ptr = np.array([0, 1, 2, 2], dtype=np.uint64)
+    col = np.array([2, 2], dtype=np.uint32)
+    wv = np.array([w, -w], dtype=np.float32)
+    cfg = I.explicit_params(3, acc_mode=I.ACC_FIXED, fixed_shift=20, i_bias=i_bias)
+    return oracle.Net(cfg, csr=(row_ptr, col, wv, None))
+
+
+def test_overflow_guard_is_on_magnitudes():
+    # The guard bounds sum |wq| + Kmax |ext_wq| + |bias_q| <= 2^31 - 1: every
+    # in-synapse may arrive in one step with either sign.  Here each weight
+    # alone fits int32 and the signed sum is 0, so only the magnitudes decide:
+    # 2 * 1000 * 2^20 = 2.097e9 fits, 2 * 1100 * 2^20 = 2.307e9 does not; a
+    # bias of -30 mV (3.1e7) still fits, -50 mV (5.2e7) does not.
+    net = _guard_net(1000.0)
+    assert int(net.in_abs_sum_q()[2]) == 2 * 1000 * 2**20
+    _guard_net(1000.0, i_bias=-30.0)
+    for w, ib in ((1100.0, 0.0), (1000.0, -50.0)):
+        with pytest.raises(oracle.OracleError) as e:
+            _guard_net(w, i_bias=ib)
+        assert e.value.code == oracle.EOVERFLOW
+
+
+LAZY_CASES = [
+    ("fixed-out-delays", lambda acc: I.scaled(4, 3000, k_out=300, acc_mode=acc), 150),
+    ("bernoulli", lambda acc: I.config(0, driven=True, seed=2, acc_mode=acc), 200),
+    ("sources", lambda acc: I.scaled(3, 4000, k_out=200, acc_mode=acc, rate_hz=50.0), 40),
+]
+
+
+@pytest.mark.parametrize("name,mk,T", LAZY_CASES, ids=[c[0] for c in LAZY_CASES])
+@pytest.mark.parametrize("acc", [I.ACC_F32, I.ACC_FIXED], ids=["f32", "fixed"])
+def test_lazy_rows_run_equals_stored_rows_run(name, mk, T, acc):
+    # The full-size networks are too large for the oracle to store; it then
+    # generates the row of each spike when delivering it.  That must give the
+    # same simulation bit for bit as the stored rows, split over two calls.
+    cfg = mk(acc)
+    a = oracle.Net(cfg)
+    b = oracle.Net(cfg, build_csr=False)
+    ra = a.run(T)
+    rb1, rb2 = b.run(T // 3), b.run(T - T // 3)
+    assert ra["counts"].sum() > 0
+    for key in ("counts", "events", "delivered"):
+        assert np.array_equal(ra[key], np.concatenate([rb1[key], rb2[key]])), key
+    assert np.array_equal(ra["raster"], np.concatenate([rb1["raster"], rb2["raster"]]))
+    va, fa = a.state()
+    vb, fb = b.state()
+    assert np.array_equal(va.view(np.uint32), vb.view(np.uint32)) and np.array_equal(fa, fb)
+
+
+def test_delivered_record_counts_arrivals():
+    # delivered[t] = synapses whose spike arrives at t: those of delay d of
+    # every spike of t - d, counted here from the stored rows
+    cfg = I.scaled(4, 2000, k_out=200, delay_min=2, delay_max=7, acc_mode=I.ACC_FIXED)
+    net = oracle.Net(cfg)
+    T = 120
+    r = net.run(T)
+    rp, _, _, d = net.csr()
+    want = np.zeros(T, np.int64)
+    for t in range(T):
+        for s in r["raster"][int(r["offs"][t]):int(r["offs"][t + 1])]:
+            arr = t + d[int(rp[s]):int(rp[s + 1])].astype(np.int64)
+            np.add.at(want, arr[arr < T], 1)
+    assert want.sum() > 0
+    assert np.array_equal(r["delivered"].astype(np.int64), want)
+
+
+def test_pair_predicate_matches_rows():
+    cfg = I.config(0, n=200, p=0.1, delay_max=4, seed=8)
+    net = oracle.Net(cfg)
+    rp, col, w, d = net.csr()
+    for s in (0, 57, 199):
+        a, b = int(rp[s]), int(rp[s + 1])
+        got = []
+        for t in range(200):
+            c, wv, dv = net.pair(s, t)
+            if c:
+                got.append((t, dv, int(wv.view(np.uint32))))
+        assert got == list(zip(col[a:b].tolist(), d[a:b].tolist(), w[a:b].view(np.uint32).tolist()))
+
+
+def test_fig_adj_pivot_split():
+    # The figure's thick line splits every row before its first target above
+    # the pivot neuron 4 (the last ID of the first slice, Sec. III-D): the
+    # split positions drawn are 2 3 2 1 2 2 2 3 3 3.  The oracle's rows are
+    # sorted (Sec. III-A), so the split is a lower bound in each row.
+    fx = I.fig_adj()
+    cfg = I.explicit_params(fx["n"])
+    net = oracle.Net(cfg, csr=(fx["row_ptr"], fx["col"], fx["w"], fx["delay"]))
+    piv = fx["pivot"][0]
+    split = [int(np.searchsorted(net.row(s)[0], piv + 1)) for s in range(fx["n"])]
+    assert split == fx["expect_split"]
