@@ -12,12 +12,17 @@ synaptic event happens).
     python bench.py [--steps K] [--warmup W] [--config 4] [--acc f32|fixed]
                     [--mode auto|graph|persistent] [--format auto|full|compact]
 
-Prints one JSON line (the last line of stdout).  Timing: W untimed steps,
-then exactly K steps (one persistent-kernel launch, or graph replays),
-bracketed by torch.cuda.synchronize(); events delivered are read from the
-device counters.  A second pass of K steps runs with HIP events around every
-kernel launch (on the network's stream) to measure the dominant kernel's
-average launch duration for the roofline figure.  The CPU oracle is timed on
+Prints one JSON line (the last line of stdout).  Timing: a fixed number of
+settling steps (past the start-up transient and every pending delay, run
+whatever --warmup says), W untimed warm-up steps, then exactly K steps (one
+persistent-kernel launch, or graph replays) between HIP events on the
+network's stream, bracketed by torch.cuda.synchronize().  `value` counts the
+events of the spikes emitted inside the timed window (the rows read there);
+the events delivered in the window are reported beside it.  For the
+persistent kernel the same launch is also timed by the library's own HIP
+events around it, which gives the dominant kernel's duration for the
+roofline figure over the same window; the graph path times a second pass
+with each step's kernels launched on their own.  The CPU oracle is timed on
 a bounded sample (reduced neuron count, same per-neuron statistics).
 """
 from __future__ import annotations
@@ -79,22 +84,39 @@ def workload(args):
     return cfg
 
 
-def algorithmic_bytes(n, kind, events, spikes, per_event, steps):
-    """Bytes the hot path must move per the method: one stored synapse per
-    delivered event, read once (per_event: 8 B for a 32-bit target + 32-bit
-    weight, 4 B where the network has per-population weights and only the
-    target is stored, as the paper's adjacency list does), 10 B per LIF
-    neuron and step (V read + write, refractory counter read + write; 8 B
-    for a source neuron, which has no counter), 8 B per spike (ID written
-    once, read once).  Accumulators are on chip and cost nothing.  events and
-    spikes are totals over `steps` steps; returns (event bytes, neuron and
-    spike bytes) over those steps."""
+def algorithmic_bytes(n, kind, events, spikes, steps, split=False):
+    """Bytes the hot path must move per the method, over `steps` steps with
+    `events` synaptic events (rows read) and `spikes` spikes in total: per
+    event one synapse record read once (8 B for a 32-bit target + 32-bit
+    weight; also given at 4 B, the record stored where the network has
+    per-population weights and only target and delay are kept, as the paper's
+    adjacency list does), 10 B per LIF neuron and step (V read + write,
+    refractory counter read + write; 8 B for a source neuron, which has no
+    counter), 8 B per spike (ID written once, read once).  Accumulators are
+    on chip and cost nothing.  Returns {bytes per event: total bytes}, or
+    with split=True ({bytes per event: event bytes}, neuron and spike bytes)."""
     per_neuron = 8 if kind == 1 else 10
-    return per_event * events, per_neuron * float(n) * steps + 8.0 * spikes
+    neu = per_neuron * float(n) * steps + 8.0 * spikes
+    ev = {8: 8.0 * events, 4: 4.0 * events}
+    if split:
+        return ev, neu
+    return {b: v + neu for b, v in ev.items()}
 
 
-STEP_SOURCES = ("spk_internal.h", "spk_dev.h", "spk_step.hip", "spk_run.hip", "spk_run_batch.hip", "spk_split.hip",
-                "spk_runtime.hip")
+SETTLE_MS = 30.0
+
+
+def settle_steps(cfg):
+    """Steps every run makes untimed before its warm-up, whatever --warmup
+    says: 30 ms of biological time and at least twice the longest delay.
+    Every neuron starts at a random V below threshold and the drive fires a
+    burst in the first milliseconds whose events arrive over the next delays;
+    after that the network is in its steady state, so that the timed window
+    measures steady-state throughput."""
+    return max(2 * int(cfg["delay_max"]), int(round(SETTLE_MS / cfg["dt_ms"])))
+
+
+STEP_SOURCES = ("spk_internal.h", "spk_dev.h", "spk_step.hip", "spk_run.hip", "spk_run_batch.hip", "spk_runtime.hip")
 
 
 def step_source_sha():
@@ -231,8 +253,9 @@ def main():
 
     cfg = workload(args)
     W, K = args.warmup, args.steps
+    S = settle_steps(cfg)
     t_create = time.perf_counter()
-    net = spk.Net(cfg, stream=stream, max_steps=W + 2 * K)
+    net = spk.Net(cfg, stream=stream, max_steps=S + W + 2 * K)
     torch.cuda.synchronize()
     t_create = time.perf_counter() - t_create
     st = net.stats()
@@ -240,11 +263,17 @@ def main():
     bpe = float(st["bytes_per_synapse"])
     print(f"[bench] {WORKLOAD_NAMES[args.config]}: nnz={st['nnz']} tiles={st['tiles']}x{st['tile_width']} "
           f"delivery={'direct' if st['delivery'] == 1 else 'binned'} "
-          f"steps={'persistent' if persistent else 'graph'} bytes/synapse={bpe:g} create={t_create:.2f}s",
-          file=sys.stderr, flush=True)
+          f"steps={'persistent' if persistent else 'graph'} batch={st['batch_steps']} bytes/synapse={bpe:g} "
+          f"create={t_create:.2f}s settle={S} warmup={W} timed={K}", file=sys.stderr, flush=True)
 
+    net.step(S)  # past the start-up transient and every pending delay
     net.step(W)
     torch.cuda.synchronize()
+    # The persistent kernel runs all K steps in one launch: HIP events around
+    # that launch (on the network's stream) time the dominant kernel over the
+    # same window the wall clock times.
+    if persistent:
+        net.set_profiling(True)
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
     e0.record(stream)
@@ -252,77 +281,84 @@ def main():
     e1.record(stream)
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1)
-    delivered = net.delivered(W, K).astype(float)
-    counts = net.spike_counts(W, K).astype(float)
-    events = float(delivered.sum())
-    spikes = float(counts.sum())
-    value = events / (ms * 1e-3)
+    t0 = S + W
+    emitted = float(net.events(t0, K).astype(float).sum())
+    delivered = float(net.delivered(t0, K).astype(float).sum())
+    spikes = float(net.spike_counts(t0, K).astype(float).sum())
+    # events whose rows were read inside the timed window
+    value = emitted / (ms * 1e-3)
     ms_step = ms / K
 
-    # per-kernel durations, HIP events around every launch (second pass)
-    net.set_profiling(True)
-    net.step(K)
-    km = net.kernel_ms()
-    net.set_profiling(False)
-    nsteps = km["steps"]
-    d2 = float(net.delivered(W + K, K).astype(float).sum())
-    e2 = float(net.events(W + K, K).astype(float).sum())
-    c2 = float(net.spike_counts(W + K, K).astype(float).sum())
-    binned = st["delivery"] == 2
-    if persistent:  # one launch runs all K steps: every byte of the step is its
-        b_ev, b_neu = algorithmic_bytes(cfg["n"], cfg["neuron_kind"], d2, c2, bpe, nsteps)
-        nl = km["run_launches"]
-        kname = "k_split" if st["persistent_split"] else "k_run"
-        kernels = {kname: (km["run_ms"] / nl, (b_ev + b_neu) / nl)}
-    elif binned:  # push kernel reads the fired rows; tile kernel updates the neurons
-        b_push, b_tile = algorithmic_bytes(cfg["n"], cfg["neuron_kind"], e2, c2, bpe, nsteps)
-        kernels = {"k_push": (km["push_ms"] / nsteps, b_push / nsteps),
-                   "k_tile": (km["tile_ms"] / nsteps, b_tile / nsteps)}
-    else:         # tile kernel does both
-        b_ev, b_neu = algorithmic_bytes(cfg["n"], cfg["neuron_kind"], d2, c2, bpe, nsteps)
-        kernels = {"k_tile": (km["tile_ms"] / nsteps, (b_ev + b_neu) / nsteps)}
-    # measured copy bandwidth of this device (the library's streaming copy
-    # kernel, 1 GiB read + 1 GiB written per repetition), for a second ratio
-    probe_ms = net.hbm_copy(1 << 30, reps=10)
-    probe_gbs = 2 * (1 << 30) * 10 / (probe_ms * 1e-3) / 1e9
+    if persistent:
+        km = net.kernel_ms()
+        net.set_profiling(False)
+        assert km["run_launches"] == 1 and km["steps"] == K
+        kernels = {"k_run": (km["run_ms"], algorithmic_bytes(cfg["n"], cfg["neuron_kind"], emitted, spikes, K))}
+        win_ev, win_sp = emitted, spikes
+        spl = K
+    else:  # graph path: a second pass with each step's kernels launched and timed on their own
+        net.set_profiling(True)
+        net.step(K)
+        km = net.kernel_ms()
+        net.set_profiling(False)
+        nsteps = km["steps"]
+        win_ev = float(net.events(t0 + K, K).astype(float).sum())
+        win_sp = float(net.spike_counts(t0 + K, K).astype(float).sum())
+        ev_b, neu_b = algorithmic_bytes(cfg["n"], cfg["neuron_kind"], win_ev, win_sp, nsteps, split=True)
+        if st["delivery"] == 2:  # push kernel reads the fired rows; tile kernel updates the neurons
+            kernels = {"k_push": (km["push_ms"] / nsteps, {b: v / nsteps for b, v in ev_b.items()}),
+                       "k_tile": (km["tile_ms"] / nsteps, {b: neu_b / nsteps for b in ev_b})}
+        else:     # tile kernel does both
+            kernels = {"k_tile": (km["tile_ms"] / nsteps, {b: (v + neu_b) / nsteps for b, v in ev_b.items()})}
+        spl = 1
+    # measured bandwidths of this device: a streaming read (what a synapse
+    # stream can reach) and the library's copy kernel (1 GiB each)
+    read_gbs = (1 << 30) * 10 / (net.hbm_read(1 << 30, reps=10) * 1e-3) / 1e9
+    copy_gbs = 2 * (1 << 30) * 10 / (net.hbm_copy(1 << 30, reps=10) * 1e-3) / 1e9
     dom = max(kernels, key=lambda k: kernels[k][0])
     dom_ms, dom_bytes = kernels[dom]
-    achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
-    b_evt, b_neu = algorithmic_bytes(cfg["n"], cfg["neuron_kind"], events, spikes, bpe, K)
-    step_gbs = (b_evt + b_neu) / (ms * 1e-3) / 1e9
-    spl = nsteps / km["run_launches"] if persistent else 1
+    achieved = dom_bytes[8] / (dom_ms * 1e-3) / 1e9
+    achieved_rec = dom_bytes[bpe] / (dom_ms * 1e-3) / 1e9
     traffic = measured_traffic(args.config, args.acc, dom, spl)
     roofline = {
         "bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
         "frac": round(achieved / PEAK_HBM_GBS, 4),
         "traffic": None if traffic is None else round(traffic),
-        "kernel": dom, "kernel_us": round(dom_ms * 1e3, 2),
-        "kernel_alg_bytes": round(dom_bytes),
-        "step_alg_GBs": round(step_gbs, 1), "step_frac": round(step_gbs / PEAK_HBM_GBS, 4),
-        "events_only_frac": round(value / (PEAK_HBM_GBS * 1e9 / bpe), 4),
-        "bytes_per_event": bpe,
+        "kernel": dom, "kernel_us": round(dom_ms * 1e3, 2), "steps_per_launch": spl,
+        "bytes_per_event": 8.0,
+        "kernel_alg_bytes": round(dom_bytes[8]),
+        "stored_record_bytes_per_event": bpe,
+        "achieved_stored_record": round(achieved_rec, 1),
+        "frac_stored_record": round(achieved_rec / PEAK_HBM_GBS, 4),
+        "events_only_frac": round(value * 8.0 / (PEAK_HBM_GBS * 1e9), 4),
         "per_launch_us": {k: round(v[0] * 1e3, 2) for k, v in kernels.items()},
-        "steps_per_launch": spl,
-        "probe_GBs": round(probe_gbs, 1), "frac_vs_probe": round(achieved / probe_gbs, 4),
+        "probe_read_GBs": round(read_gbs, 1), "frac_vs_read_probe": round(achieved / read_gbs, 4),
+        "probe_copy_GBs": round(copy_gbs, 1),
     }
 
     rate_hz = spikes / (cfg["n"] * K * cfg["dt_ms"] * 1e-3)
+    name = WORKLOAD_NAMES[args.config]
+    if args.config == 3:
+        name += f", {args.rate:g} Hz"
     out = {
         "metric": METRIC, "value": value, "unit": "events/s", "n_gpus": 1, "steps": K,
         "warmup": W, "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f32" if args.acc == "f32" else "i32",
         "data": "synthetic",
         "config": {
-            "workload": WORKLOAD_NAMES[args.config] + (", Poisson drive at twice threshold rate"
-                                                       if cfg["ext_lambda"] and args.config != 2 else ""),
+            "workload": name + (", Poisson drive at twice threshold rate"
+                                if cfg["ext_lambda"] and args.config != 2 else ""),
             "n_neurons": cfg["n"], "synapses": int(st["nnz"]), "dt_ms": cfg["dt_ms"],
             "delivery": "direct" if st["delivery"] == 1 else "binned",
-            "steps": ("one persistent launch" + (" (filing beside the updates)" if st["persistent_split"] else ""))
-                     if persistent else "HIP graphs of 32 steps",
+            "steps": "one persistent launch" if persistent else "HIP graphs of 32 steps",
+            "batch_steps": st["batch_steps"],
             "synapse_bytes": bpe,
             "accumulation": "exact int64 fixed point, rounded once to fp32" if args.acc == "f32"
                             else f"int32 fixed point 2^-{cfg['fixed_shift']}",
-            "mean_rate_hz": round(rate_hz, 3), "events_per_step": round(events / K, 1),
+            "settle_steps": S,
+            "mean_rate_hz": round(rate_hz, 3),
+            "events_emitted_per_step": round(emitted / K, 1),
+            "events_delivered_per_step": round(delivered / K, 1),
             "seed": args.seed, "parallelism": "1 GPU",
         },
         "roofline": roofline,

@@ -45,7 +45,7 @@
 extern "C" {
 #endif
 
-#define SPK_ABI_VERSION 4u
+#define SPK_ABI_VERSION 5u
 #define SPK_MAX_DELAY_LISTS 64u  /* delay_max - delay_min + 1 must not exceed this */
 
 typedef enum {
@@ -121,9 +121,7 @@ enum { SPK_STEP_AUTO = 0, SPK_STEP_GRAPH = 1, SPK_STEP_PERSISTENT = 2 };
  * Tuning (environment, read at creation): SPK_TILES_PER_XCD caps the tiles
  *   per XCD group (1..256, default 32); SPK_PAGE_CAP sets the records per
  *   page of binned delivery (default: an equal share of 2 GiB);
- *   SPK_PERSISTENT_SPLIT=0 / 1 forces the persistent kernel's variant (see
- *   spk_stats_t.persistent_split; default: split only when the smallest
- *   delay is >= 2 and steps cannot be batched); SPK_BATCH_STEPS caps the
+ *   SPK_BATCH_STEPS caps the
  *   steps per batch (1..16, default 8; spk_stats_t.batch_steps);
  *   SPK_GEN_KEYS=0 makes the Bernoulli generator draw every row a second
  *   time to place it instead of keeping the first pass's synapses (the
@@ -168,11 +166,7 @@ typedef struct {
     uint32_t delivery;         /* SPK_DELIVERY_DIRECT or SPK_DELIVERY_BINNED as chosen */
     uint32_t page_cap;         /* binned delivery: records per page (beyond: global atomics) */
     uint32_t step_mode;        /* SPK_STEP_GRAPH or SPK_STEP_PERSISTENT as chosen */
-    uint32_t persistent_split; /* 1: the persistent kernel runs filing and updates side by
-                                  side, the events that arrive at the next step first (binned
-                                  delivery, 4-byte synapses or fixed-point accumulation);
-                                  chosen when the smallest delay is >= 2 steps */
-    uint32_t batch_steps;      /* persistent kernel, binned delivery, unsplit: steps run as
+    uint32_t batch_steps;      /* persistent kernel, binned delivery: steps run as
                                   one batch (tile phases back to back, then one filing pass);
                                   up to the smallest delay (at most 8, or SPK_BATCH_STEPS up
                                   to 16), 1 otherwise */
@@ -288,6 +282,13 @@ spk_status spk_read_kernel_ms(spk_net *net, double *push_ms, double *tile_ms, do
  * library's streaming copy kernel on the network's stream, timed with HIP
  * events: used to calibrate HBM traffic counters.  *ms may be NULL. */
 spk_status spk_hbm_copy(spk_net *net, uint64_t bytes, int reps, double *ms);
+
+/* Plain streaming read of `bytes` bytes (multiple of 16) of a device buffer
+ * the call allocates and fills first, `reps` times, on the network's stream,
+ * timed with HIP events: the read bandwidth the synapse stream can reach.
+ * *ms (summed over reps) may be NULL.  Errors: SPK_EINVAL, SPK_ENOMEM,
+ * SPK_EHIP. */
+spk_status spk_hbm_read(spk_net *net, uint64_t bytes, int reps, double *ms);
 
 void spk_destroy(spk_net *net);                 /* NULL-safe */
 const char *spk_last_error(void);               /* thread-local; never NULL */

@@ -69,13 +69,19 @@ uint64_t orc_splitmix64(uint64_t z)
 }
 
 /* H(seed, tag, a, b): chain the mixer over seed, stream tag and two
- * coordinates.  Used for every random decision of the model. */
-uint64_t orc_hash(uint64_t seed, uint32_t tag, uint64_t a, uint64_t b)
+ * coordinates.  Used for every random decision of the model.  The chain up
+ * to the first coordinate is the prefix of every draw that shares
+ * (seed, tag, a), e.g. all synapses of one source row. */
+static uint64_t hash_prefix(uint64_t seed, uint32_t tag, uint64_t a)
 {
     uint64_t h = orc_splitmix64(seed);
     h = orc_splitmix64(h ^ (uint64_t)tag);
-    h = orc_splitmix64(h ^ a);
-    return orc_splitmix64(h ^ b);
+    return orc_splitmix64(h ^ a);
+}
+
+uint64_t orc_hash(uint64_t seed, uint32_t tag, uint64_t a, uint64_t b)
+{
+    return orc_splitmix64(hash_prefix(seed, tag, a) ^ b);
 }
 
 /* Per-step draws (Poisson drive, Bernoulli firing of neuron i at step t):
@@ -217,27 +223,38 @@ static int syn_cmp(const void *a, const void *b)
     return 0;
 }
 
-/* Weight of a synapse from source s, drawn at coordinates (a, b) of the
- * W stream: per synapse w_lo + (w_hi - w_lo) * u24 (two fp32 operations),
- * else the weight of the source's population (Sec. III-A: the static models
- * keep one weight per population). */
-static float syn_weight(const orc_net *net, uint32_t s, uint64_t a, uint64_t b)
+/* Weight of a synapse from source s: per synapse w_lo + (w_hi - w_lo) * u24
+ * of its W-stream hash h (two fp32 operations), else the weight of the
+ * source's population (Sec. III-A: the static models keep one weight per
+ * population; h is not used). */
+static float weight_of(const orc_net *net, uint32_t s, uint64_t h)
 {
     const orc_params *P = &net->P;
     if (P->w_uniform) {
         float span = P->w_hi - P->w_lo;
-        float t = span * u24(orc_hash(P->seed, ORC_TAG_W, a, b));
+        float t = span * u24(h);
         return P->w_lo + t;
     }
     return s < net->D.n_exc ? P->w_exc : P->w_inh;
 }
 
-/* Delay (steps) of the synapse drawn at coordinates (a, b) of the DELAY
- * stream: uniform over [delay_min, delay_max]. */
-static uint8_t syn_delay(const orc_net *net, uint64_t a, uint64_t b)
+/* Delay (steps) of a synapse from its DELAY-stream hash h: uniform over
+ * [delay_min, delay_max] (h is not used for a single delay). */
+static uint8_t delay_of(const orc_net *net, uint64_t h)
 {
     if (net->dspan == 1) return (uint8_t)net->P.delay_min;
-    return (uint8_t)(net->P.delay_min + range_n(orc_hash(net->P.seed, ORC_TAG_DELAY, a, b), net->dspan));
+    return (uint8_t)(net->P.delay_min + range_n(h, net->dspan));
+}
+
+/* The same for the synapse drawn at coordinates (a, b) of the streams. */
+static float syn_weight(const orc_net *net, uint32_t s, uint64_t a, uint64_t b)
+{
+    return weight_of(net, s, net->P.w_uniform ? orc_hash(net->P.seed, ORC_TAG_W, a, b) : 0);
+}
+
+static uint8_t syn_delay(const orc_net *net, uint64_t a, uint64_t b)
+{
+    return delay_of(net, net->dspan > 1 ? orc_hash(net->P.seed, ORC_TAG_DELAY, a, b) : 0);
 }
 
 /* Generate the row of source s into buf (cap entries); Bernoulli and fixed
@@ -259,12 +276,16 @@ static long long gen_row(const orc_net *net, uint32_t s, orc_syn *buf, uint64_t 
             len++;
         }
     } else if (P->conn_kind == ORC_CONN_FIXED_OUT) {
-        /* k_out independent uniform targets; duplicates are kept */
+        /* k_out independent uniform targets; duplicates are kept.  Draw j of
+         * the row is H(seed, tag, s, j), finished from the row's prefixes. */
         if (P->k_out > cap) return -1;
+        uint64_t pt = hash_prefix(P->seed, ORC_TAG_TGT, s);
+        uint64_t pd = hash_prefix(P->seed, ORC_TAG_DELAY, s);
+        uint64_t pw = hash_prefix(P->seed, ORC_TAG_W, s);
         for (uint32_t j = 0; j < P->k_out; j++) {
-            buf[j].tgt = range_n(orc_hash(P->seed, ORC_TAG_TGT, s, j), P->n);
-            buf[j].d = syn_delay(net, s, j);
-            buf[j].w = syn_weight(net, s, s, j);
+            buf[j].tgt = range_n(orc_splitmix64(pt ^ j), P->n);
+            buf[j].d = delay_of(net, net->dspan > 1 ? orc_splitmix64(pd ^ j) : 0);
+            buf[j].w = weight_of(net, s, P->w_uniform ? orc_splitmix64(pw ^ j) : 0);
         }
         len = P->k_out;
     } else {

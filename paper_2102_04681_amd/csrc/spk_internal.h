@@ -202,17 +202,15 @@ struct StepArgs {
 constexpr uint32_t kCtlStride = 32;
 constexpr uint32_t kRunMaxR = 32;          // workgroups per XCD (one per compute unit)
 constexpr uint32_t kRunMaxFill = 2048;     // pages per push block: arrival slots x tiles of a group
-constexpr uint32_t kRunMaxD = 16;          // steps per batch of the unsplit kernel (binned delivery)
-constexpr uint32_t kRunMaxBuckets = 1024;  // unsplit kernel: (arrival offset, tile) buckets of a push block
+constexpr uint32_t kRunMaxD = 16;          // steps per batch (binned delivery)
+constexpr uint32_t kRunMaxBuckets = 1024;  // (arrival offset, tile) buckets of a push block
 constexpr uint32_t kRunAbortTimeout = 1u;  // a barrier wait gave up
 constexpr uint32_t kRunAbortPlacement = 2u;  // workgroups not spread R per XCD: nothing was run
 struct RunCtl {
     uint32_t ticket[kGroups * kCtlStride];  // workgroups placed on each XCD
     uint32_t gx[kGroups * kCtlStride];      // grid barrier: arrivals per XCD
-    uint32_t critp[kGroups * kRunMaxR];     // split kernel: critical phases finished, per push block
-    uint32_t bulkp[kGroups * kRunMaxR];     // split kernel: bulk phases finished, per push block
-    uint32_t pushp[kGroups * kRunMaxR];     // unsplit kernel: push phases finished, per push block
-    // unsplit kernel, binned: per batch parity and tile, the batch published
+    uint32_t pushp[kGroups * kRunMaxR];     // binned: push phases finished, per push block
+    // binned: per batch parity and tile, the batch published
     // (epoch in bits kTileCntBits and up) with, for a one-step batch, the
     // tile's spike count of that step (bits below)
     uint32_t tilep[2][kGroups * kRunMaxR];
@@ -226,14 +224,8 @@ struct RunArgs {
     RunCtl *ctl;
     uint64_t t0, n_steps;   // steps [t0, t0 + n_steps)
     uint32_t R;             // workgroups per XCD
-    uint32_t D;             // unsplit kernel, binned delivery: steps per batch (1 .. min(d_min, kRunMaxD))
-    // split kernel: critical pages (events of delay 1), one per (XCD group,
-    // push block, tile of the group), page_cap records each, and their fills
-    uint16_t *cpages16;
-    int2 *cpages;
-    uint32_t *cfill;
+    uint32_t D;             // binned delivery: steps per batch (1 .. min(d_min, kRunMaxD))
 };
-constexpr uint32_t kSplitMaxBuckets = 1024;  // split kernel: (delay, tile) buckets and (slot, tile) pages
 
 // spk_gen.hip -- connectivity expansion
 // hist: optional (Bernoulli rows), n * (T + 2 * kGroups) u16 bucket counts
@@ -285,6 +277,7 @@ hipError_t launch_push(const StepArgs &a, uint32_t i, int64_t t_explicit, hipStr
 hipError_t launch_record(const StepArgs &a, uint32_t i, int64_t t_explicit, hipStream_t s);
 hipError_t launch_advance(uint64_t *t_base, uint32_t steps, hipStream_t s);
 hipError_t stream_copy(const void *src, void *dst, uint64_t bytes, hipStream_t s);
+hipError_t stream_read(const void *src, uint64_t bytes, uint32_t *sink, hipStream_t s);
 uint32_t push_blocks_per_group();
 
 // spk_run.hip -- the persistent step kernel (all steps of a call in one launch)
@@ -292,10 +285,5 @@ bool run_supported(const StepArgs &a, uint32_t R);
 bool run_batch_supported(const StepArgs &a, uint32_t D);  // steps per batch D is valid for this network
 hipError_t launch_run(const RunArgs &ra, hipStream_t s);
 hipError_t launch_run_batched(const RunArgs &ra, hipStream_t s);  // spk_run_batch.hip
-
-// spk_split.hip -- the persistent kernel that files each step's delay-1
-// events before the rest (binned delivery)
-bool split_supported(const StepArgs &a, uint32_t R);
-hipError_t launch_split(const RunArgs &ra, hipStream_t s);
 
 }  // namespace spk

@@ -181,14 +181,11 @@ struct spk_net {
     uint64_t device_bytes = 0;
     std::vector<void *> allocs;
     std::map<uint32_t, hipGraphExec_t> graphs;
-    // persistent step kernel; split: the variant that files delay-1 events first
-    bool persistent = false, split = false;
+    // persistent step kernel
+    bool persistent = false;
     uint32_t run_R = 0;
-    uint32_t run_D = 1;  // unsplit persistent kernel, binned delivery: steps per batch
+    uint32_t run_D = 1;  // persistent kernel, binned delivery: steps per batch
     RunCtl *ctl = nullptr;
-    uint16_t *cpages16 = nullptr;
-    int2 *cpages = nullptr;
-    uint32_t *cfill = nullptr;
     // profiling
     bool profiling = false;
     std::vector<hipEvent_t> ev_free;
@@ -570,7 +567,7 @@ spk_status choose_delivery(spk_net *net, RowIndex *ix)
     // With a smallest delay of two steps or more, no event filed at t is
     // needed at t + 1: binned delivery lets the persistent kernel run steps
     // in batches and file a whole batch's events at once (or file them beside
-    // the updates, split kernel), which beats reading the due rows at arrival.
+    // the updates), which beats reading the due rows at arrival.
     if (direct && net->dmin >= 2 && net->P.step_mode != SPK_STEP_GRAPH && binned_ok) direct = false;
     if (!binned_ok || net->P.delivery == SPK_DELIVERY_DIRECT) direct = true;
     if (net->P.delivery == SPK_DELIVERY_BINNED) {
@@ -660,7 +657,7 @@ spk_status finish_rows(spk_net *net)
     }
     class_units(net);
 
-    // Steps per batch of the unsplit persistent kernel (binned delivery): up
+    // Steps per batch of the persistent kernel (binned delivery): up
     // to the smallest delay, so that nothing a batch files arrives within it,
     // and within the bucket, slot and LDS limits.
     const Tiling &tl = net->tl;
@@ -682,8 +679,8 @@ spk_status finish_rows(spk_net *net)
     }
     // Spike lists: direct delivery reads the lists of steps t - dmax .. t - dmin
     // while writing that of t; binned delivery consumes the list of t within t,
-    // but in the persistent kernels one XCD may publish t + 1 (split kernel:
-    // t + 2) while another still reads t, so there are three; with batches of
+    // but in the persistent kernel one XCD may publish t + 1 while another
+    // still reads t, so there are three; with batches of
     // D steps, one XCD may publish the next batch while another reads this one.
     net->spk_slots = net->direct ? net->dmax + 1 : std::max<uint32_t>(3, 2 * net->run_D);
     if (!net->direct) {
@@ -707,12 +704,6 @@ spk_status finish_rows(spk_net *net)
         if (net->compact) SPK_TRY(dalloc(net, &net->pages16, n_pages * cap));
         else SPK_TRY(dalloc(net, &net->pages, n_pages * cap));
         SPK_TRY(dalloc(net, &net->pfill, n_pages));
-        // critical pages of the split persistent kernel: (group, push block, tile)
-        const uint64_t n_cpages = (uint64_t)kGroups * net->pg1 * tl.T8;
-        if (net->compact) SPK_TRY(dalloc(net, &net->cpages16, n_cpages * cap));
-        else SPK_TRY(dalloc(net, &net->cpages, n_cpages * cap));
-        SPK_TRY(dalloc(net, &net->cfill, n_cpages));
-        SPK_HIP(hipMemsetAsync(net->cfill, 0, n_cpages * 4, s));
         SPK_TRY(dalloc(net, &net->ovf_flag, (size_t)net->pslots * tl.T));
         SPK_TRY(dalloc(net, (uint64_t **)&net->acc_ovf, acc_elems));
         SPK_HIP(hipMemsetAsync(net->pfill, 0, n_pages * 4, s));
@@ -857,15 +848,13 @@ RunArgs run_args(const spk_net *net, uint64_t t0, uint64_t n_steps)
     ra.n_steps = n_steps;
     ra.R = net->run_R;
     ra.D = net->direct ? 1u : net->run_D;
-    ra.cpages16 = net->cpages16;
-    ra.cpages = net->cpages;
-    ra.cfill = net->cfill;
     return ra;
 }
 
 hipError_t launch_persistent(const spk_net *net, const RunArgs &ra, hipStream_t s)
 {
-    return net->split ? launch_split(ra, s) : launch_run(ra, s);
+    (void)net;
+    return launch_run(ra, s);
 }
 
 // A zero-step launch of the persistent kernel: checks that the workgroups
@@ -903,16 +892,8 @@ spk_status choose_step_mode(spk_net *net)
     const int cus = cu_count();
     net->run_R = cus > 0 && cus % (int)kGroups == 0 ? (uint32_t)(cus / (int)kGroups) : 0u;
     const StepArgs a = step_args(net);
-    // The split kernel runs filing and updates side by side on half the waves
-    // each: it is taken when nothing filed at t is needed at t + 1 (smallest
-    // delay >= 2) but the unsplit kernel cannot batch steps; with delay-1
-    // events, or with batches of several steps, the unsplit kernel is faster
-    // on MI355X.  SPK_PERSISTENT_SPLIT=0 / 1 forces the choice (a tuning knob).
-    bool want_split = net->dmin >= 2 && net->run_D < 2;
-    if (const char *e = std::getenv("SPK_PERSISTENT_SPLIT")) want_split = std::strcmp(e, "0") != 0;
-    const bool split_fits = coop && want_split && split_supported(a, net->run_R);
     const bool run_fits = coop && run_supported(a, net->run_R) && run_batch_supported(a, net->direct ? 1u : net->run_D);
-    if (!split_fits && !run_fits) {
+    if (!run_fits) {
         if (mode == SPK_STEP_PERSISTENT)
             return fail(SPK_EINVAL, "the persistent step kernel does not apply to this network or device "
                                     "(tiles per XCD, delays, or cooperative launch)");
@@ -920,19 +901,11 @@ spk_status choose_step_mode(spk_net *net)
     }
     SPK_TRY(dalloc(net, &net->ctl, 1));
     bool ok = false;
-    if (split_fits) {
-        net->split = true;
-        SPK_TRY(probe_persistent(net, &ok));
-    }
-    if (!ok && run_fits) {
-        net->split = false;
-        SPK_TRY(probe_persistent(net, &ok));
-    }
+    SPK_TRY(probe_persistent(net, &ok));
     if (ok) {
         net->persistent = true;
         return SPK_OK;
     }
-    net->split = false;
     dfree(net, net->ctl);
     net->ctl = nullptr;
     if (mode == SPK_STEP_PERSISTENT)
@@ -1531,8 +1504,7 @@ spk_status spk_stats(spk_net *net, spk_stats_t *out)
     st.delivery = net->direct ? SPK_DELIVERY_DIRECT : SPK_DELIVERY_BINNED;
     st.page_cap = net->page_cap;
     st.step_mode = net->persistent ? SPK_STEP_PERSISTENT : SPK_STEP_GRAPH;
-    st.persistent_split = net->split ? 1u : 0u;
-    st.batch_steps = net->persistent && !net->split && !net->direct ? net->run_D : 1u;
+    st.batch_steps = net->persistent && !net->direct ? net->run_D : 1u;
     st.setup_ms = net->setup_ms;
     st.gen_ms = net->gen_ms;
     st.range_ms = net->range_ms;
@@ -1591,6 +1563,38 @@ spk_status spk_hbm_copy(spk_net *net, uint64_t bytes, int reps, double *ms)
     if (e1) (void)hipEventDestroy(e1);
     dfree(net, a);
     dfree(net, b);
+    return st;
+}
+
+spk_status spk_hbm_read(spk_net *net, uint64_t bytes, int reps, double *ms)
+{
+    SPK_TRY(check_ready(net));
+    if (bytes == 0 || bytes % 16 || reps < 1) return fail(SPK_EINVAL, "bytes multiple of 16, reps >= 1");
+    hipStream_t s = net->stream;
+    uint8_t *a = nullptr;
+    uint32_t *sink = nullptr;
+    SPK_TRY(dalloc(net, &a, bytes));
+    SPK_TRY(dalloc(net, &sink, 1));
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    spk_status st = SPK_OK;
+    do {
+        hipError_t e = hipMemsetAsync(a, 1, bytes, s);
+        if (e == hipSuccess) e = stream_read(a, bytes, sink, s);  // warm-up
+        if (e == hipSuccess) e = hipEventCreate(&e0);
+        if (e == hipSuccess) e = hipEventCreate(&e1);
+        if (e == hipSuccess) e = hipEventRecord(e0, s);
+        for (int r = 0; r < reps && e == hipSuccess; r++) e = stream_read(a, bytes, sink, s);
+        if (e == hipSuccess) e = hipEventRecord(e1, s);
+        if (e == hipSuccess) e = hipEventSynchronize(e1);
+        float t = 0;
+        if (e == hipSuccess) e = hipEventElapsedTime(&t, e0, e1);
+        if (e != hipSuccess) { st = fail(SPK_EHIP, hipGetErrorString(e)); break; }
+        if (ms) *ms = t;
+    } while (0);
+    if (e0) (void)hipEventDestroy(e0);
+    if (e1) (void)hipEventDestroy(e1);
+    dfree(net, a);
+    dfree(net, sink);
     return st;
 }
 

@@ -548,6 +548,25 @@ __global__ __launch_bounds__(256) void k_stream_copy(const uint4 *src, uint4 *ds
         dst[k] = src[k];
 }
 
+// Streaming read of n16 16-byte words, four loads in flight per thread; the
+// xor of everything read is stored only if it equals a value a memset never
+// produces, so the loads cannot be dropped and nothing is written.
+__global__ __launch_bounds__(256) void k_stream_read(const uint4 *src, uint64_t n16, uint32_t *sink)
+{
+    const uint64_t stride = (uint64_t)gridDim.x * 256;
+    uint64_t k = (uint64_t)blockIdx.x * 256 + threadIdx.x;
+    uint32_t acc = 0;
+    for (; k + 3 * stride < n16; k += 4 * stride) {
+        const uint4 a = src[k], b = src[k + stride], c = src[k + 2 * stride], d = src[k + 3 * stride];
+        acc ^= a.x ^ a.y ^ a.z ^ a.w ^ b.x ^ b.y ^ b.z ^ b.w ^ c.x ^ c.y ^ c.z ^ c.w ^ d.x ^ d.y ^ d.z ^ d.w;
+    }
+    for (; k < n16; k += stride) {
+        const uint4 a = src[k];
+        acc ^= a.x ^ a.y ^ a.z ^ a.w;
+    }
+    if (acc == 0x13579bdfu) sink[0] = acc;
+}
+
 }  // namespace
 
 uint32_t push_blocks_per_group()
@@ -604,6 +623,12 @@ hipError_t launch_record(const StepArgs &a, uint32_t i, int64_t t_explicit, hipS
 hipError_t launch_advance(uint64_t *t_base, uint32_t steps, hipStream_t s)
 {
     hipLaunchKernelGGL(k_advance, dim3(1), dim3(64), 0, s, t_base, steps);
+    return hipGetLastError();
+}
+
+hipError_t stream_read(const void *src, uint64_t bytes, uint32_t *sink, hipStream_t s)
+{
+    hipLaunchKernelGGL(k_stream_read, dim3(cu_count() * 16), dim3(256), 0, s, (const uint4 *)src, bytes / 16, sink);
     return hipGetLastError();
 }
 

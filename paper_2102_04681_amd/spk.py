@@ -19,7 +19,7 @@ import numpy as np
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libspk.so")
 
 SPK_OK, SPK_EINVAL, SPK_ENOMEM, SPK_EHIP, SPK_EOVERFLOW, SPK_ESTATE = 0, -1, -2, -3, -4, -5
-SPK_ABI_VERSION = 4
+SPK_ABI_VERSION = 5
 SPK_LIF, SPK_SOURCE = 0, 1
 SPK_CONN_BERNOULLI, SPK_CONN_FIXED_OUT, SPK_CONN_FIXED_IN, SPK_CONN_EXPLICIT = 0, 1, 2, 3
 SPK_ACC_F32, SPK_ACC_FIXED = 0, 1
@@ -31,7 +31,7 @@ EXPORTED = [
     "spk_preset", "spk_create", "spk_create_from_csr", "spk_step", "spk_sync",
     "spk_read_spike_counts", "spk_read_events", "spk_read_delivered", "spk_read_raster",
     "spk_read_state", "spk_debug_deliver", "spk_export_rows", "spk_poisson_table", "spk_stats",
-    "spk_set_profiling", "spk_read_kernel_ms", "spk_hbm_copy", "spk_destroy", "spk_last_error",
+    "spk_set_profiling", "spk_read_kernel_ms", "spk_hbm_copy", "spk_hbm_read", "spk_destroy", "spk_last_error",
     "spk_abi_version",
 ]
 
@@ -63,7 +63,7 @@ class spk_stats_t(C.Structure):
         ("delay_lists", C.c_uint32), ("max_row", C.c_uint32), ("pois_len", C.c_uint32),
         ("fixed_shift", C.c_int32), ("k", C.c_float), ("bytes_per_synapse", C.c_double),
         ("tile_width", C.c_uint32), ("tiles", C.c_uint32), ("delivery", C.c_uint32),
-        ("page_cap", C.c_uint32), ("step_mode", C.c_uint32), ("persistent_split", C.c_uint32),
+        ("page_cap", C.c_uint32), ("step_mode", C.c_uint32),
         ("batch_steps", C.c_uint32), ("setup_ms", C.c_double), ("gen_ms", C.c_double), ("range_ms", C.c_double),
     ]
 
@@ -99,6 +99,7 @@ def lib():
             "spk_read_kernel_ms": (i32, [P, C.POINTER(C.c_double), C.POINTER(C.c_double),
                                          C.POINTER(C.c_double), C.POINTER(u64), C.POINTER(u64)]),
             "spk_hbm_copy": (i32, [P, u64, i32, C.POINTER(C.c_double)]),
+            "spk_hbm_read": (i32, [P, u64, i32, C.POINTER(C.c_double)]),
             "spk_destroy": (None, [P]),
             "spk_last_error": (C.c_char_p, []),
             "spk_abi_version": (u32, []),
@@ -298,6 +299,11 @@ class Net:
                                         C.byref(nr)), "spk_read_kernel_ms")
         return {"push_ms": d.value, "tile_ms": u.value, "run_ms": r.value, "steps": n.value,
                 "run_launches": nr.value}
+
+    def hbm_read(self, nbytes: int, reps: int = 10) -> float:
+        ms = C.c_double()
+        _check(lib().spk_hbm_read(self._h, nbytes, reps, C.byref(ms)), "spk_hbm_read")
+        return ms.value
 
     def hbm_copy(self, nbytes: int, reps: int = 10) -> float:
         ms = C.c_double()

@@ -47,11 +47,23 @@ def test_step_source_hash_covers_every_step_kernel_source():
 
 
 def test_algorithmic_bytes_of_the_3e9_synapse_workload():
-    with open(os.path.join(ROOT, "profiles", "traffic_c4_f32.json")) as f:
-        k = json.load(f)["kernels"]["k_run"]
-    steps, events = 500, k["events_per_step"] * 500
-    spikes = 2_000_000 * k["mean_rate_hz"] * 1e-4 * steps  # dt = 0.1 ms
-    ev_bytes, other = bench.algorithmic_bytes(2_000_000, 0, events, spikes, 4.0, steps)
-    assert ev_bytes == 4.0 * events
-    assert other == pytest.approx(10.0 * 2_000_000 * steps + 8.0 * spikes)
-    assert (ev_bytes + other) / steps == pytest.approx(32.3e6, rel=2e-3)
+    # per step at 10 Hz: 2,000 spikes x 1,500 events; 8 B per event (a 32-bit
+    # target and a 32-bit weight read once), 10 B per LIF neuron (V and the
+    # refractory counter read and written), 8 B per spike
+    steps, rate = 500, 10.0
+    spikes = 2_000_000 * rate * 1e-4 * steps  # dt = 0.1 ms
+    events = spikes * 1500
+    b = bench.algorithmic_bytes(2_000_000, 0, events, spikes, steps)
+    other = 10.0 * 2_000_000 * steps + 8.0 * spikes
+    assert b[8] == pytest.approx(8.0 * events + other)
+    assert b[4] == pytest.approx(4.0 * events + other)
+    assert b[8] / steps == pytest.approx(44.0e6, rel=1e-3)  # 24 MB of events + 20 MB of neurons
+    ev, neu = bench.algorithmic_bytes(1_000_000, 1, 10.0, 2.0, 3, split=True)
+    assert ev == {8: 80.0, 4: 40.0} and neu == 8.0 * 1_000_000 * 3 + 16.0
+
+
+def test_settle_steps_cover_transient_and_delays():
+    import inputs as I
+    assert bench.settle_steps(I.config(4, driven=True)) == 300
+    assert bench.settle_steps(I.config(3)) == 30
+    assert bench.settle_steps(I.config(0, delay_max=200)) == 400

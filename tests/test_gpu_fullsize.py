@@ -3,7 +3,7 @@
 Workload: 2,000,000 LIF neurons, fixed out-degree 1,500 (3.0e9 synapses),
 delays 1..20 steps, external Poisson drive at twice the threshold rate,
 fp32 accumulation, binned delivery, steps run by the persistent kernel (as
-bench.py times them), by its split variant, and replayed from HIP graphs.  The oracle cannot
+bench.py times them) and replayed from HIP graphs.  The oracle cannot
 simulate this network step by step in test time, so it checks sampled
 outputs it can compute one by one:
 
@@ -42,12 +42,9 @@ def _say(*a):
     sys.stdout.flush()
 
 
-@pytest.mark.parametrize("step_mode,split", [(2, "auto"), (2, "1"), (1, "auto")],
-                         ids=["persist", "persist-split", "graph"])
-def test_full_size_bench_configuration_sampled(spk_full, step_mode, split, monkeypatch):
+@pytest.mark.parametrize("step_mode", [2, 1], ids=["persist", "graph"])
+def test_full_size_bench_configuration_sampled(spk_full, step_mode):
     spk = spk_full
-    if split != "auto":
-        monkeypatch.setenv("SPK_PERSISTENT_SPLIT", split)
     cfg = I.config(4, driven=True, step_mode=step_mode)
     n, K, dmax = cfg["n"], cfg["k_out"], cfg["delay_max"]
     T0 = 300
@@ -55,7 +52,6 @@ def test_full_size_bench_configuration_sampled(spk_full, step_mode, split, monke
     g = spk.Net(cfg, max_steps=T0 + 1, raster_capacity=4_000_000)
     st = g.stats()
     assert st["step_mode"] == step_mode
-    assert st["persistent_split"] == (1 if split == "1" else 0)
     assert st["nnz"] == n * K
     assert st["delivery"] == spk.SPK_DELIVERY_BINNED
     s64 = int(st["fixed_shift"])
@@ -132,7 +128,7 @@ def test_full_size_delay15_batch_sampled(spk_full):
     _say(f"[full c2] create n={n}")
     g = spk.Net(cfg, max_steps=T0 + D, raster_capacity=2_000_000)
     st = g.stats()
-    assert st["step_mode"] == spk.SPK_STEP_PERSISTENT and st["persistent_split"] == 0
+    assert st["step_mode"] == spk.SPK_STEP_PERSISTENT
     assert st["delivery"] == spk.SPK_DELIVERY_BINNED and st["batch_steps"] == D
     assert st["nnz"] == n * (cfg["k_in_exc"] + cfg["k_in_inh"])
     s64 = int(st["fixed_shift"])

@@ -268,14 +268,11 @@ RUN_CASES = [
 
 # how the steps run: graph replay, plain launches with events (profiling),
 # the persistent kernel as chosen (binned delivery with a smallest delay >= 2:
-# the unsplit kernel in batches of up to 8 steps), the same with events
-# around it, the split variant (SPK_PERSISTENT_SPLIT=1), the unsplit kernel,
-# and the unsplit kernel with batches capped at 1, 4 and 16 steps
-# (SPK_BATCH_STEPS)
-MODES = [("graph", 1, False, "auto", None), ("launch", 1, True, "auto", None), ("persist", 2, False, "auto", None),
-         ("persist-prof", 2, True, "auto", None), ("persist-split", 2, False, "1", None),
-         ("persist-unsplit", 2, False, "0", None), ("persist-batch1", 2, False, "0", "1"),
-         ("persist-batch4", 2, False, "0", "4"), ("persist-batch16", 2, False, "0", "16")]
+# batches of up to 8 steps), the same with events around it, and the
+# persistent kernel with batches capped at 1, 4 and 16 steps (SPK_BATCH_STEPS)
+MODES = [("graph", 1, False, None), ("launch", 1, True, None), ("persist", 2, False, None),
+         ("persist-prof", 2, True, None), ("persist-batch1", 2, False, "1"),
+         ("persist-batch4", 2, False, "4"), ("persist-batch16", 2, False, "16")]
 
 
 def _expected_batch(cfg, batch):
@@ -290,9 +287,9 @@ def _persistent_applies(cfg, delivery):
 
 @pytest.mark.parametrize("name,mk,T", RUN_CASES, ids=[c[0] for c in RUN_CASES])
 @pytest.mark.parametrize("delivery", [1, 2], ids=["direct", "binned"])
-@pytest.mark.parametrize("mode,step_mode,profiled,split,batch", MODES, ids=[m[0] for m in MODES])
+@pytest.mark.parametrize("mode,step_mode,profiled,batch", MODES, ids=[m[0] for m in MODES])
 @pytest.mark.parametrize("fmt", [f for f, _ in FORMATS], ids=[n for _, n in FORMATS])
-def test_fixed_point_simulation_bit_identical(spk, name, mk, T, delivery, mode, step_mode, profiled, split, batch,
+def test_fixed_point_simulation_bit_identical(spk, name, mk, T, delivery, mode, step_mode, profiled, batch,
                                               fmt, monkeypatch):
     cfg = mk()
     cfg["acc_mode"] = I.ACC_FIXED
@@ -303,22 +300,16 @@ def test_fixed_point_simulation_bit_identical(spk, name, mk, T, delivery, mode, 
         pytest.skip("profiled paths checked on two shapes")
     if step_mode == 2 and not _persistent_applies(cfg, delivery):
         pytest.skip("the persistent kernel takes direct delivery with one delay only")
-    if split != "auto" and delivery == 1:
-        pytest.skip("direct delivery has no split variant")
     if batch and (delivery == 1 or cfg["delay_min"] < 2):
         pytest.skip("steps are batched only with binned delivery and a smallest delay >= 2")
-    if split != "auto":
-        monkeypatch.setenv("SPK_PERSISTENT_SPLIT", split)
     if batch:
         monkeypatch.setenv("SPK_BATCH_STEPS", batch)
     _say(f"[run] {name} n={cfg['n']} T={T} delivery={delivery} mode={mode} format={fmt}")
     g = spk.Net(cfg, max_steps=T, raster_capacity=cfg["n"] * T)
     st = g.stats()
     assert st["step_mode"] == step_mode
-    want_split = step_mode == 2 and delivery == 2 and split == "1"
-    assert st["persistent_split"] == (1 if want_split else 0)
-    unsplit_binned = step_mode == 2 and delivery == 2 and not want_split
-    assert st["batch_steps"] == (_expected_batch(cfg, batch) if unsplit_binned else 1)
+    persist_binned = step_mode == 2 and delivery == 2
+    assert st["batch_steps"] == (_expected_batch(cfg, batch) if persist_binned else 1)
     g.set_profiling(profiled)
     g.step(T)
     offs, ids = g.raster()
@@ -353,23 +344,22 @@ def test_fixed_point_simulation_bit_identical(spk, name, mk, T, delivery, mode, 
 
 @pytest.mark.parametrize("acc", [I.ACC_F32, I.ACC_FIXED], ids=["f32", "fixed"])
 @pytest.mark.parametrize("fmt", [f for f, _ in FORMATS], ids=[n for _, n in FORMATS])
-@pytest.mark.parametrize("step_mode,split", [(1, "1"), (2, "1"), (2, "0")], ids=["graph", "persist", "unsplit"])
+@pytest.mark.parametrize("step_mode", [1, 2], ids=["graph", "persist"])
 @pytest.mark.parametrize("delays", [(1, 1), (2, 4)], ids=["d1", "d2-4"])
-def test_bin_overflow_fallback(spk, acc, fmt, step_mode, split, delays, monkeypatch):
+def test_bin_overflow_fallback(spk, acc, fmt, step_mode, delays, monkeypatch):
     # 64 neurons, 200 synapses each (multapses), all above threshold at t=0:
     # the one tile receives 12 800 events (delay 1; with delays 2-4, spread
     # over three arrival steps of batches of 2), ~400 per push block, while
     # every page is capped at 64 records, so the global-atomic fallback must
     # deliver the rest (in the simulation and in debug_deliver).
     monkeypatch.setenv("SPK_PAGE_CAP", "64")
-    monkeypatch.setenv("SPK_PERSISTENT_SPLIT", split)
     cfg = I.config(4, n=64, k_out=200, delay_min=delays[0], delay_max=delays[1], v0_lo=-49.0, v0_hi=-49.0,
                    t_ref_ms=0.0, acc_mode=acc, delivery=2, syn_format=fmt, step_mode=step_mode)
     T = 9
     g = spk.Net(cfg, max_steps=T, raster_capacity=64 * T)
     st = g.stats()
     assert st["page_cap"] == 64
-    if step_mode == 2 and split == "0":
+    if step_mode == 2:
         assert st["batch_steps"] == delays[0]
     spikes = np.arange(64, dtype=np.uint32)
     got = g.debug_deliver(spikes)
@@ -393,11 +383,10 @@ def test_bin_overflow_fallback(spk, acc, fmt, step_mode, split, delays, monkeypa
 
 
 @pytest.mark.parametrize("delays", [(1, 20), (3, 9), (15, 15)], ids=["d1-20", "d3-9", "d15"])
-@pytest.mark.parametrize("step_mode,split", [(1, "1"), (2, "1"), (2, "0")], ids=["graph", "persist", "unsplit"])
-def test_resume_matches_single_run(spk, step_mode, split, delays, monkeypatch):
+@pytest.mark.parametrize("step_mode", [1, 2], ids=["graph", "persist"])
+def test_resume_matches_single_run(spk, step_mode, delays):
     # calls of 50 and 70 steps, and of one step each: batches of several steps
     # (smallest delay 3 or 15) end early at the end of a call
-    monkeypatch.setenv("SPK_PERSISTENT_SPLIT", split)
     cfg = I.scaled(4, 5000, k_out=500, acc_mode=I.ACC_FIXED, step_mode=step_mode,
                    delay_min=delays[0], delay_max=delays[1])
     a = spk.Net(cfg, max_steps=120, raster_capacity=5000 * 120)
@@ -618,15 +607,14 @@ def test_persistent_equals_graph_fp32(spk, name, mk, T, fmt, delivery, monkeypat
     cfg["syn_format"] = fmt
     cfg["delivery"] = delivery
     runs = []
-    for step_mode, split in ((1, True), (2, True), (2, False)):
-        monkeypatch.setenv("SPK_PERSISTENT_SPLIT", "1" if split else "0")
-        if step_mode == 1:
-            monkeypatch.delenv("SPK_PERSISTENT_SPLIT")
+    for step_mode, batch in ((1, None), (2, None), (2, "1")):
+        if batch:
+            monkeypatch.setenv("SPK_BATCH_STEPS", batch)
         c = dict(cfg, step_mode=step_mode)
         g = spk.Net(c, max_steps=T, raster_capacity=cfg["n"] * T)
         st = g.stats()
         assert st["step_mode"] == step_mode
-        _say(f"[persist=graph] {name} T={T} mode={step_mode} split={st['persistent_split']} format={fmt}")
+        _say(f"[persist=graph] {name} T={T} mode={step_mode} batch={st['batch_steps']} format={fmt}")
         g.step(T // 3)
         g.step(T - T // 3)
         runs.append((g.spike_counts(), g.raster()[1], g.delivered(), g.events(), g.state()))
@@ -660,41 +648,30 @@ def test_setup_timing_stats(spk):
 def test_step_mode_selection(spk, monkeypatch):
     # AUTO takes the persistent kernel where it applies; asking for it where
     # it does not (direct delivery with several delays) is an error
-    # delay-1 events: the unsplit kernel
+    # delay-1 events: one step per batch
     st = spk.Net(I.scaled(4, 8000, k_out=300), max_steps=1).stats()
-    assert st["step_mode"] == spk.SPK_STEP_PERSISTENT and st["persistent_split"] == 0
-    st = spk.Net(I.scaled(4, 8000, k_out=300), max_steps=1).stats()
-    assert st["batch_steps"] == 1
-    # smallest delay 15: binned delivery and the unsplit kernel in batches of
-    # 8 steps (15 when asked for); the split kernel when asked for, or when
-    # batches are capped at 1
+    assert st["step_mode"] == spk.SPK_STEP_PERSISTENT and st["batch_steps"] == 1
+    # smallest delay 15: binned delivery in batches of 8 steps (15 when
+    # asked for, 1 when batches are capped at 1)
     c2 = I.scaled(2, 8000, k_in_exc=640, k_in_inh=160)
     st = spk.Net(c2, max_steps=1).stats()
-    assert st["step_mode"] == spk.SPK_STEP_PERSISTENT and st["persistent_split"] == 0
+    assert st["step_mode"] == spk.SPK_STEP_PERSISTENT
     assert st["delivery"] == spk.SPK_DELIVERY_BINNED and st["batch_steps"] == 8
     monkeypatch.setenv("SPK_BATCH_STEPS", "16")
     assert spk.Net(c2, max_steps=1).stats()["batch_steps"] == 15
     monkeypatch.setenv("SPK_BATCH_STEPS", "1")
     st = spk.Net(c2, max_steps=1).stats()
-    assert st["persistent_split"] == 1 and st["batch_steps"] == 1
+    assert st["step_mode"] == spk.SPK_STEP_PERSISTENT and st["batch_steps"] == 1
     monkeypatch.delenv("SPK_BATCH_STEPS")
-    monkeypatch.setenv("SPK_PERSISTENT_SPLIT", "1")
-    st = spk.Net(c2, max_steps=1).stats()
-    assert st["persistent_split"] == 1 and st["batch_steps"] == 1
-    monkeypatch.delenv("SPK_PERSISTENT_SPLIT")
     # delays 3..9: batches of 3 steps
     st = spk.Net(I.scaled(4, 8000, k_out=300, delay_min=3, delay_max=9), max_steps=1).stats()
-    assert st["persistent_split"] == 0 and st["batch_steps"] == 3
+    assert st["batch_steps"] == 3
     # ... but direct delivery when steps run as graphs
     st = spk.Net(I.scaled(2, 8000, k_in_exc=640, k_in_inh=160, step_mode=1), max_steps=1).stats()
     assert st["delivery"] == spk.SPK_DELIVERY_DIRECT
-    # fp32 sums with 8-byte synapses: the unsplit kernel even when asked (LDS)
-    monkeypatch.setenv("SPK_PERSISTENT_SPLIT", "1")
+    # fp32 sums with 8-byte synapses: persistent too
     st = spk.Net(I.scaled(4, 8000, k_out=300, syn_format=1), max_steps=1).stats()
-    assert st["step_mode"] == spk.SPK_STEP_PERSISTENT and st["persistent_split"] == 0
-    st = spk.Net(I.scaled(4, 8000, k_out=300), max_steps=1).stats()
-    assert st["persistent_split"] == 1
-    monkeypatch.delenv("SPK_PERSISTENT_SPLIT")
+    assert st["step_mode"] == spk.SPK_STEP_PERSISTENT
     g = spk.Net(I.scaled(4, 8000, k_out=300, step_mode=1), max_steps=1)
     assert g.stats()["step_mode"] == spk.SPK_STEP_GRAPH
     cfg = I.scaled(4, 8000, k_out=300, delivery=1)
