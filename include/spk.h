@@ -47,6 +47,8 @@ extern "C" {
 
 #define SPK_ABI_VERSION 5u
 #define SPK_MAX_DELAY_LISTS 64u  /* delay_max - delay_min + 1 must not exceed this */
+/* Device scratch of spk_deliver_noalloc, per device (bytes). */
+#define SPK_NOALLOC_SCRATCH_BYTES (32ull << 20)
 
 typedef enum {
     SPK_OK = 0,
@@ -251,6 +253,29 @@ spk_status spk_read_state(spk_net *net, float *v, uint8_t *ref);
  * changed. */
 spk_status spk_debug_deliver(spk_net *net, const uint32_t *spikes, uint64_t n_spikes,
                              uint32_t delay, float *out_f32, int32_t *out_i32);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * delivery of spk_debug_deliver with the spike list (d_spikes, n_spikes IDs)
+ * and the output (d_out: n floats in fp32 mode, n int32 in fixed mode, units
+ * of 2^-fixed_shift) in the caller's device memory, enqueued on the
+ * network's stream and not waited for.  The pages, fill counters and
+ * overflow accumulators the delivery needs come from one fixed scratch area
+ * per device (SPK_NOALLOC_SCRATCH_BYTES, a static device array the library
+ * holds until the process ends, cleared by a kernel at the start of every
+ * call); the call allocates nothing, frees nothing, uses no memset and does
+ * not synchronise.  Every call on one device shares that area: calls that
+ * overlap on one device (any network, any stream) race, so the caller
+ * orders them (one stream, or events).  Networks with direct delivery need
+ * no scratch.  Results equal spk_debug_deliver's.  Network state is not
+ * changed.  Errors (returned at once): SPK_EINVAL (null output, bad delay,
+ * n_spikes >= 2^30), SPK_EOVERFLOW (the network's tiles need more overflow
+ * accumulators than the scratch holds: n rounded up to whole tiles x 8
+ * (fp32) or 4 (fixed) bytes, plus pages, must fit), SPK_EHIP.  Spike IDs
+ * >= n are not read through: they deliver nothing, and the next spk_sync
+ * (or read) reports SPK_EINVAL once. */
+spk_status spk_deliver_noalloc(spk_net *net, const uint32_t *d_spikes, uint64_t n_spikes, uint32_t delay,
+                               void *d_out);
 
 /* Export the rows (all synapses of the given source neurons), each row in
  * canonical order (target, delay, weight bits).  offs: n_rows+1 entries;

@@ -266,11 +266,16 @@ __device__ uint32_t gather_direct(const StepArgs &a, typename Acc<FIXED>::T *acc
         uint32_t len = 0;
         uint64_t beg = 0;
         if (p0 + lane < P) {
-            const uint32_t s = a.dbg_spikes ? a.dbg_spikes[p0 + lane] : spike_at<COH>(a, pre, slot, p0 + lane);
+            uint32_t s = a.dbg_spikes ? a.dbg_spikes[p0 + lane] : spike_at<COH>(a, pre, slot, p0 + lane);
+            // a caller's spike list (debug delivery) is checked here: an ID
+            // out of range delivers nothing and raises a flag
+            const bool bad = s >= a.n;
+            if (bad && tile == 0) atomicOr(a.flags, kFlagBadSpike);
+            s = bad ? 0u : s;
             const uint16_t *to = a.toff + (uint64_t)s * T1 + tile;
             const uint32_t b = to[0], e = to[1];
             beg = a.row_ptr[s] + b;
-            len = e - b;
+            len = bad ? 0u : e - b;
         }
         uint32_t inc = len;
         for (int o = 1; o < kWave; o <<= 1) {

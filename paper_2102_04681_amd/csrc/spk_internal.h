@@ -35,6 +35,11 @@ __host__ __device__ __forceinline__ uint32_t rec_class(uint32_t x) { return x >>
 __host__ __device__ __forceinline__ uint32_t rec_key(int2 r) { return (uint32_t)r.x; }
 __host__ __device__ __forceinline__ uint32_t rec_key(uint32_t r) { return r; }
 
+// Device flag bits of a network (StepArgs::flags): bit 1 the raster capacity
+// was exceeded, bit 2 a persistent launch stopped early, bit 3 a spike ID
+// given for debug delivery was out of range.
+constexpr uint32_t kFlagBadSpike = 8u;
+
 // A compact page record (u16): class << 13 | local target (W <= 8192).
 constexpr uint32_t kPageClassShift = 13;
 constexpr uint32_t kPageLocalMask = (1u << kPageClassShift) - 1u;
@@ -278,6 +283,7 @@ hipError_t launch_record(const StepArgs &a, uint32_t i, int64_t t_explicit, hipS
 hipError_t launch_advance(uint64_t *t_base, uint32_t steps, hipStream_t s);
 hipError_t stream_copy(const void *src, void *dst, uint64_t bytes, hipStream_t s);
 hipError_t stream_read(const void *src, uint64_t bytes, uint32_t *sink, hipStream_t s);
+hipError_t zero_words(uint32_t *p, uint64_t n, hipStream_t s);
 uint32_t push_blocks_per_group();
 
 // spk_run.hip -- the persistent step kernel (all steps of a call in one launch)

@@ -21,6 +21,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <map>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -58,6 +59,37 @@ constexpr uint64_t kPageBudget = 256ull << 20;     // page records across all pa
 constexpr uint64_t kDebugPageCap = 4096;           // records per page for spk_debug_deliver
 constexpr uint64_t kRunMaxSteps = 1ull << 24;      // steps per persistent launch (barrier epochs fit u32)
 constexpr uint32_t kFlagRunStopped = 4u;           // device flag: a persistent launch stopped early
+
+// Scratch of spk_deliver_noalloc: one fixed area per device, held until the
+// process ends, shared by every call on that device (the caller orders
+// them).  In host code the array's name stands for a host-side shadow, not a
+// device address: kernels get the address hipGetSymbolAddress returned for
+// the device, looked up once per device when a network is created there.
+constexpr uint64_t kNoAllocScratchBytes = SPK_NOALLOC_SCRATCH_BYTES;
+__device__ __align__(256) uint8_t scratch[kNoAllocScratchBytes];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices];
+
+// Address of this device's scratch (the device is current); looked up once.
+spk_status scratch_lookup(int device)
+{
+    if (device < 0 || device >= kMaxDevices) return fail(SPK_EINVAL, "device index beyond the scratch table");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_ptr[device]) return SPK_OK;
+    void *p = nullptr;
+    SPK_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return fail(SPK_EHIP, "hipGetSymbolAddress returned no address for the scratch area");
+    g_scratch_ptr[device] = p;
+    return SPK_OK;
+}
+
+void *scratch_of(int device)
+{
+    if (device < 0 || device >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    return g_scratch_ptr[device];
+}
 
 uint64_t prob_threshold(double p)
 {
@@ -513,6 +545,7 @@ spk_status derive(spk_net *net, bool explicit_csr)
 spk_status setup_stream(spk_net *net, void *stream)
 {
     SPK_HIP(hipGetDevice(&net->device));
+    SPK_TRY(scratch_lookup(net->device));
     if (stream) {
         net->stream = (hipStream_t)stream;
     } else {
@@ -836,6 +869,12 @@ spk_status sync_flags(spk_net *net, uint32_t *flags_out)
     if (f & kFlagRunStopped)
         return fail(SPK_EHIP, "a persistent step launch stopped early (a barrier wait exceeded its "
                               "bound); the network state is undefined");
+    if (f & kFlagBadSpike) {  // reported once, then cleared: the network is unchanged
+        const uint32_t g = f & ~kFlagBadSpike;
+        SPK_HIP(hipMemcpy(net->flags, &g, 4, hipMemcpyHostToDevice));
+        return fail(SPK_EINVAL, "a spike ID given to spk_deliver_noalloc was >= n; those spikes "
+                                "delivered nothing");
+    }
     return SPK_OK;
 }
 
@@ -1406,6 +1445,58 @@ spk_status spk_debug_deliver(spk_net *net, const uint32_t *spikes, uint64_t n_sp
     (void)hipStreamSynchronize(s);
     for (void *p : tmp) dfree(net, p);
     return st;
+}
+
+spk_status spk_deliver_noalloc(spk_net *net, const uint32_t *d_spikes, uint64_t n_spikes, uint32_t delay,
+                               void *d_out)
+{
+    SPK_TRY(check_ready(net));
+    if (!d_out) return fail(SPK_EINVAL, "output buffer required");
+    if (n_spikes > 0x3fffffffull || (n_spikes && !d_spikes)) return fail(SPK_EINVAL, "spikes");
+    if (delay && (delay < net->dmin || delay >= net->dmin + net->lists))
+        return fail(SPK_EINVAL, "delay not in [delay_min, delay_max]");
+    uint8_t *base = (uint8_t *)scratch_of(net->device);
+    if (!base) return fail(SPK_ESTATE, "no scratch address for the network's device");
+    hipStream_t s = net->stream;
+    const Tiling &tl = net->tl;
+    StepArgs a = step_args(net);
+    a.dbg_spikes = n_spikes ? d_spikes : nullptr;
+    a.dbg_n = (uint32_t)n_spikes;
+    a.dbg_j = delay ? (int32_t)(delay - net->dmin) : -1;
+    a.dbg_out = d_out;  // (no spikes: the tile kernel writes zeros)
+    hipError_t e = hipSuccess;
+    if (!net->direct) {
+        // Carve the scratch: fill counters, overflow flags and overflow
+        // accumulators of one arrival slot, then pages of as many records as
+        // the rest holds (at most the debug capacity; events beyond it take
+        // the overflow accumulators, with the same sums)
+        auto up = [](uint64_t b) { return (b + 255) / 256 * 256; };
+        const uint64_t n_pages = (uint64_t)kGroups * net->pg1 * tl.T8;
+        const uint64_t acc_bytes = (uint64_t)tl.T * tl.W * (net->P.acc_mode == SPK_ACC_FIXED ? 4 : 8);
+        const uint64_t o_fill = 0, o_flag = up(n_pages * 4), o_acc = o_flag + up((uint64_t)tl.T * 4);
+        const uint64_t o_pages = o_acc + up(acc_bytes);
+        const uint64_t rec = net->compact ? 2 : 8;
+        const uint64_t room = o_pages < kNoAllocScratchBytes ? kNoAllocScratchBytes - o_pages : 0;
+        uint64_t cap = std::min<uint64_t>(room / (n_pages * rec), std::min<uint64_t>(kDebugPageCap, net->page_cap));
+        cap = cap / 16 * 16;
+        if (cap < 16)
+            return fail(SPK_EOVERFLOW, "network too large for the fixed scratch of spk_deliver_noalloc (" +
+                                           std::to_string(kNoAllocScratchBytes >> 20) + " MiB per device)");
+        a.pfill = (uint32_t *)(base + o_fill);
+        a.ovf_flag = (uint32_t *)(base + o_flag);
+        a.acc_ovf = base + o_acc;
+        a.pages = net->compact ? nullptr : (int2 *)(base + o_pages);
+        a.pages16 = net->compact ? (uint16_t *)(base + o_pages) : nullptr;
+        a.page_cap = (uint32_t)cap;
+        a.pslots = 1;
+        // counters, flags and accumulators start at zero (a fill kernel: the
+        // last call's contents stay in the scratch)
+        e = zero_words((uint32_t *)base, o_pages / 4, s);
+        if (e == hipSuccess && n_spikes) e = launch_push(a, 0, 0, s);
+    }
+    if (e == hipSuccess) e = launch_tile(a, 0, 0, s);
+    if (e != hipSuccess) return fail(SPK_EHIP, hipGetErrorString(e));
+    return SPK_OK;
 }
 
 spk_status spk_export_rows(spk_net *net, const uint32_t *rows, uint64_t n_rows, uint64_t *offs,

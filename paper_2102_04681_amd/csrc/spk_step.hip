@@ -105,12 +105,17 @@ __global__ __launch_bounds__(kPushThreads) void k_push(StepArgs a, uint32_t i, i
         uint64_t base = 0;
         if (tid < K) {
             const uint32_t k = c0 + tid;
-            const uint32_t s = dbg ? a.dbg_spikes[k] : spike_at(a, L.pre, sslot, k);
+            uint32_t s = dbg ? a.dbg_spikes[k] : spike_at(a, L.pre, sslot, k);
+            // a caller's spike list (debug delivery) is checked here: an ID
+            // out of range delivers nothing and raises a flag
+            const bool bad = s >= a.n;
+            if (bad && x == 0) atomicOr(a.flags, kFlagBadSpike);
+            s = bad ? 0u : s;
             const RowDesc *d = a.desc + s;
             const uint32_t lo = x ? d->gend[x - 1] : 0u, hi = d->gend[x];
-            len = hi - lo;
+            len = bad ? 0u : hi - lo;
             base = d->start + lo;
-            emitted += d->gend[kGroups - 1];
+            emitted += bad ? 0u : d->gend[kGroups - 1];
         }
         // rows are cut into chunks of 64 events; wave w takes chunks w, w + nw,
         // ...: lane l reads event l of the chunk (one uniform lookup per chunk)
@@ -548,6 +553,12 @@ __global__ __launch_bounds__(256) void k_stream_copy(const uint4 *src, uint4 *ds
         dst[k] = src[k];
 }
 
+// Fill n words with zero (a kernel, not a memset: usable in captured graphs).
+__global__ __launch_bounds__(256) void k_zero_u32(uint32_t *p, uint64_t n)
+{
+    for (uint64_t k = (uint64_t)blockIdx.x * 256 + threadIdx.x; k < n; k += (uint64_t)gridDim.x * 256) p[k] = 0;
+}
+
 // Streaming read of n16 16-byte words, four loads in flight per thread; the
 // xor of everything read is stored only if it equals a value a memset never
 // produces, so the loads cannot be dropped and nothing is written.
@@ -623,6 +634,16 @@ hipError_t launch_record(const StepArgs &a, uint32_t i, int64_t t_explicit, hipS
 hipError_t launch_advance(uint64_t *t_base, uint32_t steps, hipStream_t s)
 {
     hipLaunchKernelGGL(k_advance, dim3(1), dim3(64), 0, s, t_base, steps);
+    return hipGetLastError();
+}
+
+hipError_t zero_words(uint32_t *p, uint64_t n, hipStream_t s)
+{
+    if (n == 0) return hipSuccess;
+    uint64_t blocks = (n + 255) / 256;
+    const uint64_t most = (uint64_t)cu_count() * 8;
+    blocks = blocks < most ? blocks : most;
+    hipLaunchKernelGGL(k_zero_u32, dim3((uint32_t)(blocks ? blocks : 1)), dim3(256), 0, s, p, n);
     return hipGetLastError();
 }
 

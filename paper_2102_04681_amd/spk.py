@@ -31,7 +31,8 @@ EXPORTED = [
     "spk_preset", "spk_create", "spk_create_from_csr", "spk_step", "spk_sync",
     "spk_read_spike_counts", "spk_read_events", "spk_read_delivered", "spk_read_raster",
     "spk_read_state", "spk_debug_deliver", "spk_export_rows", "spk_poisson_table", "spk_stats",
-    "spk_set_profiling", "spk_read_kernel_ms", "spk_hbm_copy", "spk_hbm_read", "spk_destroy", "spk_last_error",
+    "spk_set_profiling", "spk_read_kernel_ms", "spk_hbm_copy", "spk_hbm_read", "spk_deliver_noalloc",
+    "spk_destroy", "spk_last_error",
     "spk_abi_version",
 ]
 
@@ -100,6 +101,7 @@ def lib():
                                          C.POINTER(C.c_double), C.POINTER(u64), C.POINTER(u64)]),
             "spk_hbm_copy": (i32, [P, u64, i32, C.POINTER(C.c_double)]),
             "spk_hbm_read": (i32, [P, u64, i32, C.POINTER(C.c_double)]),
+            "spk_deliver_noalloc": (i32, [P, P, u64, u32, P]),
             "spk_destroy": (None, [P]),
             "spk_last_error": (C.c_char_p, []),
             "spk_abi_version": (u32, []),
@@ -258,6 +260,11 @@ class Net:
             _check(lib().spk_debug_deliver(self._h, _ptr(spikes), len(spikes), delay, _ptr(out), None),
                    "spk_debug_deliver")
         return out
+
+    def deliver_noalloc(self, d_spikes: int, n_spikes: int, d_out: int, delay: int = 0):
+        """spk_deliver_noalloc on device pointers (ints); asynchronous."""
+        _check(lib().spk_deliver_noalloc(self._h, C.c_void_p(d_spikes or None), n_spikes, delay,
+                                         C.c_void_p(d_out or None)), "spk_deliver_noalloc")
 
     def export_rows(self, rows, cap: int | None = None):
         rows = np.ascontiguousarray(rows, dtype=np.uint32)

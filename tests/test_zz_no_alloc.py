@@ -1,0 +1,120 @@
+"""spk_deliver_noalloc (the delivery for callers that cannot allocate)
+against spk_debug_deliver, through the C ABI.
+
+Both deliver a given spike list with the network's own kernels and sum
+exactly (integers in fixed mode, exact int64 sums rounded once in fp32
+mode), so their outputs must be equal bit for bit.  Each network takes two
+calls in a row, the second with a smaller spike list, so that anything the
+first call leaves in the shared scratch would show.  Shapes: binned delivery
+(pages carved from the scratch) in both accumulation modes and both synapse
+formats, direct delivery (no scratch), and the 3e9-synapse network at its
+real tiling, where a large spike list overflows the scratch pages into the
+scratch's overflow accumulators.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import inputs as I
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def env():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2102_04681_amd import spk as mod
+    mod.lib()
+    return torch, mod
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _noalloc(torch, g, spikes, delay, fixed):
+    """One call of the allocation-free entry point on device buffers the
+    caller (this test) owns; returns the output as a host array."""
+    d_sp = torch.from_numpy(np.ascontiguousarray(spikes, dtype=np.int32)).cuda() if len(spikes) else None
+    out = torch.full((g.n,), -7, dtype=torch.int32 if fixed else torch.float32, device="cuda")
+    torch.cuda.synchronize()
+    g.deliver_noalloc(d_sp.data_ptr() if d_sp is not None else 0, len(spikes), out.data_ptr(), delay=delay)
+    g.sync()
+    return out.cpu().numpy()
+
+
+CASES = [
+    ("binned-f32-compact", lambda: I.scaled(4, 8000, k_out=700), [0, 7]),
+    ("binned-fixed-compact", lambda: I.scaled(4, 8000, k_out=700, acc_mode=I.ACC_FIXED), [0, 1]),
+    ("binned-f32-full", lambda: I.scaled(4, 6000, k_out=400, syn_format=1), [0, 20]),
+    ("binned-delay15", lambda: I.scaled(2, 5000, k_in_exc=400, k_in_inh=100), [0]),
+    ("direct-f32", lambda: I.scaled(1, 4000), [0]),
+    ("direct-fixed-sources", lambda: I.scaled(3, 8000, k_out=1000, acc_mode=I.ACC_FIXED), [0]),
+]
+
+
+@pytest.mark.parametrize("name,mk,delays", CASES, ids=[c[0] for c in CASES])
+def test_noalloc_equals_debug_deliver(env, name, mk, delays):
+    torch, spk = env
+    cfg = mk()
+    fixed = cfg["acc_mode"] == I.ACC_FIXED
+    g = spk.Net(cfg, max_steps=1)
+    n = cfg["n"]
+    for delay in delays:
+        for count, seed in ((n // 3, 1), (37, 2), (0, 3)):  # two calls, the second smaller, then none
+            spikes = I.spike_set(n, count, seed=seed, unique=True)
+            _say(f"[noalloc] {name} n={n} spikes={len(spikes)} delay={delay}")
+            got = _noalloc(torch, g, spikes, delay, fixed)
+            want = g.debug_deliver(spikes, delay=delay)
+            assert got.dtype == want.dtype
+            assert np.array_equal(got.view(np.uint32), want.view(np.uint32)), "outputs differ"
+            if count == 0:
+                assert not got.any()
+    g.close()
+
+
+def test_noalloc_full_size_network(env):
+    # 2,000,000 neurons in 248 tiles of 8,192: the scratch holds the overflow
+    # accumulators (16 MiB) and pages of 976 records; 20,000 spikes (3e7
+    # events, ~3,800 per page) overflow them, 500 do not
+    torch, spk = env
+    cfg = I.config(4, driven=True)
+    g = spk.Net(cfg, max_steps=1)
+    st = g.stats()
+    assert st["tile_width"] == 8192 and st["delivery"] == spk.SPK_DELIVERY_BINNED
+    for count, seed in ((20000, 4), (500, 5)):
+        spikes = I.spike_set(cfg["n"], count, seed=seed, unique=True)
+        _say(f"[noalloc] full size spikes={count}")
+        got = _noalloc(torch, g, spikes, 0, False)
+        want = g.debug_deliver(spikes)
+        assert np.array_equal(got.view(np.uint32), want.view(np.uint32)), "outputs differ"
+    g.close()
+
+
+def test_noalloc_rejects_and_reports(env):
+    torch, spk = env
+    cfg = I.scaled(4, 8000, k_out=300)
+    g = spk.Net(cfg, max_steps=1)
+    out = torch.zeros(cfg["n"], dtype=torch.float32, device="cuda")
+    sp = torch.tensor([5, 9], dtype=torch.int32, device="cuda")
+    with pytest.raises(spk.SpkError) as e:
+        g.deliver_noalloc(sp.data_ptr(), 2, 0)
+    assert e.value.code == spk.SPK_EINVAL
+    with pytest.raises(spk.SpkError) as e:
+        g.deliver_noalloc(sp.data_ptr(), 2, out.data_ptr(), delay=21)
+    assert e.value.code == spk.SPK_EINVAL
+    # an ID >= n is not read through: it delivers nothing, the next sync
+    # reports it once, and the valid IDs are delivered as usual
+    bad = torch.tensor([5, cfg["n"] + 3, 9], dtype=torch.int32, device="cuda")
+    torch.cuda.synchronize()
+    g.deliver_noalloc(bad.data_ptr(), 3, out.data_ptr())
+    with pytest.raises(spk.SpkError) as e:
+        g.sync()
+    assert e.value.code == spk.SPK_EINVAL
+    g.sync()
+    want = g.debug_deliver(np.array([5, 9], dtype=np.uint32))
+    assert np.array_equal(out.cpu().numpy().view(np.uint32), want.view(np.uint32))
+    g.close()
