@@ -129,12 +129,17 @@ def step_source_sha():
     return h.hexdigest()[:16]
 
 
-def measured_traffic(config, acc, kernel, steps_per_launch):
+def workload_tag(config, rate):
+    """Short name of a workload in profiles/ (the source network carries its rate)."""
+    return f"c{config}" + (f"r{rate:g}" if config == 3 else "")
+
+
+def measured_traffic(tag, acc, kernel, steps_per_launch):
     """HBM bytes per launch from the committed counter summary (calibrated
     FETCH_SIZE + WRITE_SIZE per step of the kernel, times the steps of one
     launch), or None when the summary is missing or the step kernels changed
     since it was taken."""
-    path = os.path.join(ROOT, "profiles", f"traffic_c{config}_{acc}.json")
+    path = os.path.join(ROOT, "profiles", f"traffic_{tag}_{acc}.json")
     try:
         with open(path) as f:
             d = json.load(f)
@@ -319,7 +324,7 @@ def main():
     dom_ms, dom_bytes = kernels[dom]
     achieved = dom_bytes[8] / (dom_ms * 1e-3) / 1e9
     achieved_rec = dom_bytes[bpe] / (dom_ms * 1e-3) / 1e9
-    traffic = measured_traffic(args.config, args.acc, dom, spl)
+    traffic = measured_traffic(workload_tag(args.config, args.rate), args.acc, dom, spl)
     roofline = {
         "bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
         "frac": round(achieved / PEAK_HBM_GBS, 4),

@@ -27,16 +27,17 @@ def test_more_than_one_gpu_is_refused():
     assert "one MI355X" in r.stderr and r.stdout == ""
 
 
-@pytest.mark.parametrize("config", [2, 4])
-def test_traffic_is_used_only_for_the_sources_it_was_taken_on(config, monkeypatch):
-    with open(os.path.join(ROOT, "profiles", f"traffic_c{config}_f32.json")) as f:
+@pytest.mark.parametrize("config,rate", [(2, 10.0), (4, 10.0), (1, 10.0), (3, 10.0), (3, 50.0)])
+def test_traffic_is_used_only_for_the_sources_it_was_taken_on(config, rate, monkeypatch):
+    tag = bench.workload_tag(config, rate)
+    with open(os.path.join(ROOT, "profiles", f"traffic_{tag}_f32.json")) as f:
         d = json.load(f)
     per_step = d["kernels"]["k_run"]["hbm_bytes_per_step"]
     monkeypatch.setattr(bench, "step_source_sha", lambda: d["source_sha"])
-    assert bench.measured_traffic(config, "f32", "k_run", 1000) == per_step * 1000
-    assert bench.measured_traffic(config, "f32", "k_tile", 1000) is None
+    assert bench.measured_traffic(tag, "f32", "k_run", 1000) == per_step * 1000
+    assert bench.measured_traffic(tag, "f32", "k_tile", 1000) is None
     monkeypatch.setattr(bench, "step_source_sha", lambda: "0" * 16)
-    assert bench.measured_traffic(config, "f32", "k_run", 1000) is None
+    assert bench.measured_traffic(tag, "f32", "k_run", 1000) is None
 
 
 def test_step_source_hash_covers_every_step_kernel_source():
