@@ -60,7 +60,7 @@ def parse():
     ap.add_argument("--delivery", choices=["auto", "direct", "binned"], default="auto")
     ap.add_argument("--mode", choices=["auto", "graph", "persistent"], default="auto",
                     help="how steps are launched (spk_params.step_mode)")
-    ap.add_argument("--format", choices=["auto", "full", "compact"], default="auto",
+    ap.add_argument("--format", choices=["auto", "full", "compact", "procedural"], default="auto",
                     help="synapse storage (spk_params.syn_format)")
     ap.add_argument("--seed", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -80,7 +80,7 @@ def workload(args):
     cfg = I.config(args.config, driven=True, seed=args.seed, rate_hz=args.rate, acc_mode=acc)
     cfg["delivery"] = {"auto": 0, "direct": 1, "binned": 2}[args.delivery]
     cfg["step_mode"] = {"auto": 0, "graph": 1, "persistent": 2}[args.mode]
-    cfg["syn_format"] = {"auto": 0, "full": 1, "compact": 2}[args.format]
+    cfg["syn_format"] = {"auto": 0, "full": 1, "compact": 2, "procedural": 3}[args.format]
     return cfg
 
 
@@ -90,14 +90,15 @@ def algorithmic_bytes(n, kind, events, spikes, steps, split=False):
     event one synapse record read once (8 B for a 32-bit target + 32-bit
     weight; also given at 4 B, the record stored where the network has
     per-population weights and only target and delay are kept, as the paper's
-    adjacency list does), 10 B per LIF neuron and step (V read + write,
+    adjacency list does; 0 B where synapses are generated, not stored), 10 B
+    per LIF neuron and step (V read + write,
     refractory counter read + write; 8 B for a source neuron, which has no
     counter), 8 B per spike (ID written once, read once).  Accumulators are
     on chip and cost nothing.  Returns {bytes per event: total bytes}, or
     with split=True ({bytes per event: event bytes}, neuron and spike bytes)."""
     per_neuron = 8 if kind == 1 else 10
     neu = per_neuron * float(n) * steps + 8.0 * spikes
-    ev = {8: 8.0 * events, 4: 4.0 * events}
+    ev = {8: 8.0 * events, 4: 4.0 * events, 0: 0.0}  # (0: procedural synapses, none read)
     if split:
         return ev, neu
     return {b: v + neu for b, v in ev.items()}
@@ -116,7 +117,8 @@ def settle_steps(cfg):
     return max(2 * int(cfg["delay_max"]), int(round(SETTLE_MS / cfg["dt_ms"])))
 
 
-STEP_SOURCES = ("spk_internal.h", "spk_dev.h", "spk_step.hip", "spk_run.hip", "spk_run_batch.hip", "spk_runtime.hip")
+STEP_SOURCES = ("spk_internal.h", "spk_dev.h", "spk_step.hip", "spk_run.hip", "spk_run_batch.hip", "spk_proc.hip",
+                "spk_runtime.hip")
 
 
 def step_source_sha():

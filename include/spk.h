@@ -77,7 +77,14 @@ enum { SPK_DELIVERY_AUTO = 0, SPK_DELIVERY_DIRECT = 1, SPK_DELIVERY_BINNED = 2 }
  * weights: population weights (the paper's static models keep one weight per
  * source population, Sec. III-A), or an explicit adjacency with at most 4
  * distinct weights.  AUTO picks COMPACT whenever it applies. */
-enum { SPK_FORMAT_AUTO = 0, SPK_FORMAT_FULL = 1, SPK_FORMAT_COMPACT = 2 };
+enum { SPK_FORMAT_AUTO = 0, SPK_FORMAT_FULL = 1, SPK_FORMAT_COMPACT = 2, SPK_FORMAT_PROCEDURAL = 3 };
+/* PROCEDURAL (Sec. V, future work: procedural connectivity) stores no
+ * synapses at all: the row of a neuron that fires is generated again from
+ * the network's seed and parameters when its events are filed, the same
+ * synapses the other formats store.  Generated fixed out-degree networks
+ * only; binned delivery, steps run as graphs (SPK_EINVAL otherwise); each
+ * fired row costs one hash per synapse in each of the 8 XCD groups instead
+ * of 4 or 8 bytes per synapse read.  spk_stats_t.bytes_per_synapse is 0. */
 /* How spk_step runs the steps (same results, different speed).  GRAPH: each
  * step is a tile kernel (+ push kernel for binned delivery), batches of steps
  * replayed from captured HIP graphs.  PERSISTENT: all steps of one spk_step
@@ -162,7 +169,7 @@ typedef struct {
     uint32_t pois_len;
     int32_t fixed_shift;       /* fixed mode: S; fp32 mode: the unit 2^-S64 of the exact sums */
     float k;
-    double bytes_per_synapse;  /* synapse storage / nnz: 8 (FULL) or 4 (COMPACT) */
+    double bytes_per_synapse;  /* synapse storage / nnz: 8 (FULL), 4 (COMPACT), 0 (PROCEDURAL) */
     uint32_t tile_width;       /* target neurons per tile (one workgroup each) */
     uint32_t tiles;
     uint32_t delivery;         /* SPK_DELIVERY_DIRECT or SPK_DELIVERY_BINNED as chosen */

@@ -9,7 +9,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libspk.so")
-SOURCES = ["spk_gen.hip", "spk_step.hip", "spk_run.hip", "spk_run_batch.hip", "spk_runtime.hip"]
+SOURCES = ["spk_gen.hip", "spk_step.hip", "spk_run.hip", "spk_run_batch.hip", "spk_proc.hip", "spk_runtime.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

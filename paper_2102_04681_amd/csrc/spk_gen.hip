@@ -18,6 +18,9 @@
 // fp32 operations.
 #include <hip/hip_runtime.h>
 
+#include <cstdlib>
+#include <cstring>
+
 #include "spk_internal.h"
 
 namespace spk {
@@ -636,6 +639,83 @@ __global__ __launch_bounds__(kBlock) void k_bern_in_abs_max(ConnArgs c, uint32_t
     }
 }
 
+// Largest sum of |weight| into one neuron of a fixed out-degree network
+// with population weights, without a global atomic per synapse.  Every
+// synapse is drawn again (the generator's target hash; its term depends only
+// on the class of its source population), counted per target tile by blocks
+// of kFoSrc sources (one global reservation per block and tile), then filed
+// into per-tile buckets as (class << 14 | neuron within the tile); one block
+// per tile counts its neurons' in-synapses per class in LDS and takes the
+// largest sum of class counts x class terms.
+constexpr uint32_t kFoSrc = 256;  // sources per block of the counting and filing passes
+
+__global__ __launch_bounds__(kBlock) void k_fo_count(ConnArgs c, uint32_t *base, uint32_t *tile_total)
+{
+    __shared__ uint32_t cnt[kMaxTiles];
+    const uint32_t T = c.tl.T, tid = threadIdx.x;
+    const uint32_t s0 = blockIdx.x * kFoSrc, s1 = s0 + kFoSrc < c.n ? s0 + kFoSrc : c.n;
+    for (uint32_t k = tid; k < T; k += kBlock) cnt[k] = 0;
+    __syncthreads();
+    for (uint32_t s = s0; s < s1; s++) {
+        const uint64_t rt = mix64(c.keys.tgt ^ (uint64_t)s);
+        for (uint32_t q = tid; q < c.k_out; q += kBlock)
+            atomicAdd(&cnt[hash_range(mix64(rt ^ (uint64_t)q), c.n) >> c.tl.logW], 1u);
+    }
+    __syncthreads();
+    for (uint32_t k = tid; k < T; k += kBlock)
+        base[(uint64_t)blockIdx.x * T + k] = cnt[k] ? atomicAdd(&tile_total[k], cnt[k]) : 0u;
+}
+
+__global__ __launch_bounds__(kBlock) void k_fo_file(ConnArgs c, const uint32_t *base, const uint64_t *tile_start,
+                                                   uint16_t *entries)
+{
+    __shared__ uint32_t cur[kMaxTiles];
+    const uint32_t T = c.tl.T, tid = threadIdx.x;
+    const uint32_t s0 = blockIdx.x * kFoSrc, s1 = s0 + kFoSrc < c.n ? s0 + kFoSrc : c.n;
+    for (uint32_t k = tid; k < T; k += kBlock) cur[k] = base[(uint64_t)blockIdx.x * T + k];
+    __syncthreads();
+    for (uint32_t s = s0; s < s1; s++) {
+        const uint64_t rt = mix64(c.keys.tgt ^ (uint64_t)s);
+        const uint32_t cls = s < c.n_exc ? 0u : 1u;
+        for (uint32_t q = tid; q < c.k_out; q += kBlock) {
+            const uint32_t tgt = hash_range(mix64(rt ^ (uint64_t)q), c.n), tile = tgt >> c.tl.logW;
+            const uint32_t pos = atomicAdd(&cur[tile], 1u);
+            entries[tile_start[tile] + pos] = (uint16_t)((cls << 14) | (tgt & (c.tl.W - 1)));
+        }
+    }
+}
+
+__global__ __launch_bounds__(1024) void k_fo_max(ConnArgs c, const uint64_t *tile_start, const uint16_t *entries,
+                                                ClassTab tab, unsigned long long *out)
+{
+    __shared__ uint32_t cnt[2][kMaxTileW];
+    __shared__ unsigned long long wmax[1024 / kWave];
+    const uint32_t tile = blockIdx.x, tid = threadIdx.x, W = c.tl.W;
+    for (uint32_t k = tid; k < W; k += 1024) cnt[0][k] = cnt[1][k] = 0;
+    __syncthreads();
+    const uint64_t e0 = tile_start[tile], e1 = tile_start[tile + 1];
+    for (uint64_t e = e0 + tid; e < e1; e += 1024) {
+        const uint32_t v = entries[e];
+        atomicAdd(&cnt[v >> 14][v & 0x3fffu], 1u);
+    }
+    __syncthreads();
+    unsigned long long m = 0;
+    for (uint32_t k = tid; k < W; k += 1024) {
+        const unsigned long long x = (unsigned long long)cnt[0][k] * tab.abs[0] + (unsigned long long)cnt[1][k] * tab.abs[1];
+        m = x > m ? x : m;
+    }
+    for (int o = 32; o > 0; o >>= 1) {
+        const unsigned long long y = __shfl_xor(m, o);
+        m = y > m ? y : m;
+    }
+    if ((tid & (kWave - 1)) == 0) wmax[tid / kWave] = m;
+    __syncthreads();
+    if (tid == 0) {
+        for (uint32_t k = 1; k < 1024 / kWave; k++) m = wmax[k] > m ? wmax[k] : m;
+        atomicMax(out, m);
+    }
+}
+
 __global__ __launch_bounds__(kBlock) void k_max_u64(const uint64_t *x, uint64_t m,
                                                    unsigned long long *out)
 {
@@ -730,8 +810,14 @@ hipError_t gen_fill_rows(const ConnArgs &c, const uint64_t *row_ptr, void *syn, 
     return hipGetLastError();
 }
 
-// block-local counting where the source ranges are few (see above)
-static bool in_rows_lds(const ConnArgs &c) { return c.n <= kInRanges * kInRange; }
+// block-local counting where the source ranges are few (see above);
+// SPK_GEN_IN_ATOMICS=1 forces the per-synapse path (a test knob)
+static bool in_rows_lds(const ConnArgs &c)
+{
+    const char *e = std::getenv("SPK_GEN_IN_ATOMICS");
+    if (e && std::strcmp(e, "1") == 0) return false;
+    return c.n <= kInRanges * kInRange;
+}
 static uint32_t in_rows_tpb(const ConnArgs &c) { return (c.n + kInBlocks - 1) / kInBlocks; }
 
 hipError_t gen_in_count(const ConnArgs &c, uint32_t *cnt, hipStream_t s)
@@ -837,6 +923,32 @@ hipError_t bern_in_abs_max(const ConnArgs &c, uint64_t *out, uint64_t *insum, hi
     hipError_t e = hipGetLastError();
     if (e == hipSuccess && Sused > 1) e = max_u64(insum, c.n, out, s);
     return e;
+}
+
+uint32_t fo_blocks(uint32_t n) { return (n + kFoSrc - 1) / kFoSrc; }
+
+hipError_t fo_count(const ConnArgs &c, uint32_t *base, uint32_t *tile_total, hipStream_t s)
+{
+    if (c.kind != SPK_CONN_FIXED_OUT || c.tl.T > kMaxTiles) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_fo_count, dim3(fo_blocks(c.n)), dim3(kBlock), 0, s, c, base, tile_total);
+    return hipGetLastError();
+}
+
+hipError_t fo_file(const ConnArgs &c, const uint32_t *base, const uint64_t *tile_start, uint16_t *entries,
+                   hipStream_t s)
+{
+    if (c.kind != SPK_CONN_FIXED_OUT || c.tl.T > kMaxTiles || c.tl.W > (1u << 14)) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_fo_file, dim3(fo_blocks(c.n)), dim3(kBlock), 0, s, c, base, tile_start, entries);
+    return hipGetLastError();
+}
+
+hipError_t fo_max(const ConnArgs &c, const uint64_t *tile_start, const uint16_t *entries, const ClassTab &tab,
+                  uint64_t *out, hipStream_t s)
+{
+    if (c.tl.W > kMaxTileW || c.tl.T == 0) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_fo_max, dim3(c.tl.T), dim3(1024), 0, s, c, tile_start, entries, tab,
+                       (unsigned long long *)out);
+    return hipGetLastError();
 }
 
 hipError_t max_u64(const uint64_t *x, uint64_t m, uint64_t *out, hipStream_t s)

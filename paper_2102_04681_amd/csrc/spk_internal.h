@@ -152,6 +152,15 @@ struct ModelArgs {
     Keys keys;
 };
 
+// Procedural connectivity (fixed out-degree networks whose synapses are
+// generated again when their source fires, never stored): what the synapse
+// draw needs beyond the stream keys.
+struct ProcArgs {
+    uint32_t k_out, n_exc, w_uniform;
+    float w_lo, w_hi, w_exc, w_inh;
+    float qscale;           // 2^fixed_shift (fixed mode)
+};
+
 // Everything the step kernels touch.
 struct StepArgs {
     ModelArgs m;
@@ -159,6 +168,8 @@ struct StepArgs {
     uint32_t n, lists, dmin;
     uint32_t direct;             // 1: tiles read their runs of the due rows (one delay)
     uint32_t compact;            // 1: u32 synapses and u16 page records, weights from wval
+    uint32_t proc;               // 1: procedural synapses (binned delivery; no rows stored)
+    ProcArgs pr;
     int64_t wval[kMaxClasses];   // compact: weight of each class in accumulator units
     const uint64_t *row_ptr;     // n + 1
     const int2 *syn;             // full: {j << 24 | target, weight bits (fp32 or quantised int32)}
@@ -262,6 +273,18 @@ struct ClassTab {
 hipError_t in_abs_sum(const void *syn, uint64_t nnz, bool fixed, bool compact, const ClassTab &tab,
                       uint64_t *insum, hipStream_t s);
 hipError_t max_u64(const uint64_t *x, uint64_t m, uint64_t *out, hipStream_t s);
+// Fixed out-degree networks with population weights: the largest in_abs_sum
+// from the synapses drawn again and filed by target tile (no atomic per
+// synapse).  fo_count: per (block of sources, tile) reservations base
+// (fo_blocks(n) x T) and tile totals (T, zero on entry); fo_file: entries
+// (class << 14 | neuron in tile) at tile_start[tile] + reservation; fo_max:
+// one block per tile, the largest sum into *out (zero on entry).
+uint32_t fo_blocks(uint32_t n);
+hipError_t fo_count(const ConnArgs &c, uint32_t *base, uint32_t *tile_total, hipStream_t s);
+hipError_t fo_file(const ConnArgs &c, const uint32_t *base, const uint64_t *tile_start, uint16_t *entries,
+                   hipStream_t s);
+hipError_t fo_max(const ConnArgs &c, const uint64_t *tile_start, const uint16_t *entries, const ClassTab &tab,
+                  uint64_t *out, hipStream_t s);
 // Bernoulli networks: the largest in_abs_sum over neurons, by evaluating the
 // pair predicate per target (no atomic per synapse); *out must be zero on
 // entry, and so must insum (n entries), needed when bern_src_ranges(n) > 1.
@@ -281,6 +304,15 @@ hipError_t launch_tile(const StepArgs &a, uint32_t i, int64_t t_explicit, hipStr
 hipError_t launch_push(const StepArgs &a, uint32_t i, int64_t t_explicit, hipStream_t s);
 hipError_t launch_record(const StepArgs &a, uint32_t i, int64_t t_explicit, hipStream_t s);
 hipError_t launch_advance(uint64_t *t_base, uint32_t steps, hipStream_t s);
+
+// spk_proc.hip -- procedural connectivity: the push of a step with every
+// fired row generated again (binned delivery), the rows of given sources as
+// generated (export), and the per-target sum of |weight| terms (range pass,
+// one atomic per generated synapse).
+hipError_t launch_push_proc(const StepArgs &a, uint32_t i, int64_t t_explicit, hipStream_t s);
+hipError_t export_proc(const StepArgs &a, const ClassTab &tab, const uint32_t *rows, uint64_t n_rows,
+                       const uint64_t *out_off, uint32_t *col, uint32_t *wbits, uint8_t *delay, hipStream_t s);
+hipError_t proc_in_abs_sum(const StepArgs &a, uint64_t *insum, hipStream_t s);
 hipError_t stream_copy(const void *src, void *dst, uint64_t bytes, hipStream_t s);
 hipError_t stream_read(const void *src, uint64_t bytes, uint32_t *sink, hipStream_t s);
 hipError_t zero_words(uint32_t *p, uint64_t n, hipStream_t s);

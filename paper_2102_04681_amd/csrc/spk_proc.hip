@@ -1,0 +1,341 @@
+// spk_proc.hip -- procedural connectivity: the synapses of a fixed
+// out-degree network are never stored; the row of every neuron that fires
+// is generated again from the network's parameters when its events are
+// filed (the paper's Sec. V names procedural connectivity as future work:
+// store only the parameters that create the network and generate the
+// adjacency on the fly).
+//
+// A synapse j of source s is the generator's draw: target
+// range(H(seed, TGT, s, j), n), delay index range(H(seed, DELAY, s, j),
+// lists), weight by source population or w_lo + (w_hi - w_lo) u24(H(seed,
+// W, s, j)).  The push kernel here replaces the stored-row push of binned
+// delivery (spk_step.hip): push block (x, g1) takes the same equal share of
+// the step's spikes, generates every synapse of their rows (each XCD group
+// keeps the 1/8 that target it), and files the kept events into the same
+// pages with the same counting sort, so the tile kernel is unchanged.  The
+// cost moves from the synapse stream (no bytes read per event) to hashing
+// (one mixer round per generated synapse, eight synapses generated per kept
+// event); the memory of the synapses (4 or 8 bytes each) is not needed.
+//
+// Generation is wave-local: lanes walk consecutive synapses of the wave's
+// slice of the rows, keep those of the block's group, and compact them with
+// a ballot into a ring of the wave in LDS; every window takes kProcR events
+// per lane from the rings and sorts them by (arrival slot, tile) as the
+// stored-row push does.
+#include <hip/hip_runtime.h>
+
+#include "spk_dev.h"
+
+namespace spk {
+
+namespace {
+
+constexpr int kProcThreads = 1024;
+constexpr int kProcR = 8;                                  // events per lane per window
+constexpr uint32_t kProcWin = kProcR * kProcThreads;       // events sorted at once
+constexpr uint32_t kProcChunk = 1024;                      // spikes generated per chunk
+constexpr uint32_t kProcWaves = kProcThreads / kWave;
+constexpr uint32_t kRing = 128;                            // events a wave holds between windows
+constexpr uint32_t kNoSpike = 0xffffffffu;
+
+template <bool CMP>
+struct ProcLDS {
+    using Rec = typename SynRec<CMP>::T;
+    Rec stage[kProcWin];             // bucket-sorted events {bucket << 16 | local, weight}; compact:
+                                     // u32 bucket << 16 | class << 13 | local
+    Rec ring[kProcWaves][kRing];     // generated events of each wave, not yet taken
+    uint32_t sid[kProcChunk];        // the chunk's spikes (kNoSpike: an ID out of range)
+    uint32_t pre[kMaxTiles + 1];     // prefix of the source tiles' spike counts
+    uint32_t bcnt[kMaxBuckets];      // events per bucket in this window, then rank cursor
+    uint32_t bst[kMaxBuckets];       // bucket starts in the stage
+    uint32_t wb[kMaxBuckets];        // page position of stage entry q is wb[b] + q
+    uint32_t fill[kMaxBuckets];      // records already in the bucket's page
+    uint32_t pidx[kMaxBuckets];      // page of the bucket
+    uint32_t more[kProcWaves];       // the wave has events left to generate or take
+    uint32_t ws[16];
+    unsigned long long ws64[16];
+};
+
+// The stored-format record of synapse j of source s (its target tgt is
+// known): compact {class << 30 | delay index << 24 | target} with class =
+// source population, or full {delay index << 24 | target, weight bits}.
+template <bool CMP>
+__device__ __forceinline__ typename SynRec<CMP>::T proc_record(const StepArgs &a, uint32_t s, uint32_t j,
+                                                              uint32_t tgt, uint32_t jd)
+{
+    const uint32_t key = (jd << kTargetBits) | tgt;
+    if constexpr (CMP) {
+        return key | ((s < a.pr.n_exc ? 0u : 1u) << kClassShift);
+    } else {
+        float w;
+        if (a.pr.w_uniform) {
+            const uint64_t h = key_hash(a.m.keys.w, s, j);
+            const float u = (float)(uint32_t)(h >> 40) * (1.0f / 16777216.0f);
+            w = __fadd_rn(a.pr.w_lo, __fmul_rn(__fsub_rn(a.pr.w_hi, a.pr.w_lo), u));
+        } else {
+            w = s < a.pr.n_exc ? a.pr.w_exc : a.pr.w_inh;
+        }
+        const int32_t wb = a.m.fixed ? (int32_t)__builtin_rintf(__fmul_rn(w, a.pr.qscale)) : __float_as_int(w);
+        return make_int2((int)key, wb);
+    }
+}
+
+template <bool FIXED, bool CMP>
+__global__ __launch_bounds__(kProcThreads) void k_push_proc(StepArgs a, uint32_t i, int64_t t_explicit)
+{
+    using Rec = typename SynRec<CMP>::T;
+    __shared__ ProcLDS<CMP> L;
+    const uint64_t t = step_index(a, i, t_explicit);
+    const uint32_t x = blockIdx.x % kGroups, g1 = blockIdx.x / kGroups, G1 = a.pg1;
+    const uint32_t tid = threadIdx.x, lane = lane_id();
+    const uint32_t w = __builtin_amdgcn_readfirstlane(tid / kWave);
+    const Tiling tl = a.tl;
+    const bool dbg = a.dbg_spikes != nullptr;
+    const uint32_t NB = (dbg ? 1u : a.lists) * tl.T8;
+    const uint32_t sslot = (uint32_t)(t % a.spk_slots);
+    const uint32_t kout = a.pr.k_out;
+
+    for (uint32_t b = tid; b < NB; b += kProcThreads) {
+        const uint32_t p = page_of(a, x, g1, arrival_slot(a, t, b / tl.T8, dbg), b % tl.T8);
+        L.pidx[b] = p;
+        L.fill[b] = a.pfill[p];
+        L.bcnt[b] = 0;
+    }
+    const uint32_t M = dbg ? a.dbg_n : load_spike_set(a, sslot, L.pre, L.ws);
+    const uint32_t k0 = (uint32_t)((uint64_t)M * g1 / G1), k1 = (uint32_t)((uint64_t)M * (g1 + 1) / G1);
+    const uint32_t xlo = x * tl.Gw;
+    const uint64_t cap = a.page_cap;
+    uint64_t emitted = 0;
+    for (uint32_t c0 = k0; c0 < k1 && kout; c0 += kProcChunk) {
+        const uint32_t K = k1 - c0 < kProcChunk ? k1 - c0 : kProcChunk;
+        if (tid < K) {
+            const uint32_t k = c0 + tid;
+            const uint32_t s = dbg ? a.dbg_spikes[k] : spike_at(a, L.pre, sslot, k);
+            // a caller's spike list (debug delivery) is checked here: an ID
+            // out of range generates nothing and raises a flag
+            const bool bad = s >= a.n;
+            if (bad && x == 0) atomicOr(a.flags, kFlagBadSpike);
+            L.sid[tid] = bad ? kNoSpike : s;
+            emitted += bad ? 0u : kout;
+        }
+        lds_sync();
+        // the wave's slice [vb, ve) of the chunk's K * kout synapses; lane l
+        // generates synapse v = vcur + l, i.e. synapse j of spike si
+        const uint32_t V = K * kout;
+        const uint32_t vb = (uint32_t)((uint64_t)V * w / kProcWaves);
+        const uint32_t ve = (uint32_t)((uint64_t)V * (w + 1) / kProcWaves);
+        uint32_t vcur = vb;                      // (wave-uniform)
+        uint32_t si = (vb + lane) / kout, j = (vb + lane) - si * kout;
+        uint32_t scur = kNoSpike;                // the spike whose target-stream prefix pt is held
+        uint64_t pt = 0;
+        uint32_t head = 0, cnt = 0;              // the wave's ring (wave-uniform)
+        for (;;) {
+            Rec rec[kProcR];
+            uint32_t okm = 0;  // bit u: rec[u] is an event
+#pragma unroll
+            for (int u = 0; u < kProcR; u++) {
+                while (cnt < kWave && vcur < ve) {
+                    const bool live = vcur + lane < ve;
+                    bool keep = false;
+                    Rec r{};
+                    if (live) {
+                        const uint32_t s = L.sid[si];
+                        if (s != kNoSpike) {
+                            if (s != scur) {
+                                scur = s;
+                                pt = mix64(a.m.keys.tgt ^ (uint64_t)s);
+                            }
+                            const uint32_t tgt = hash_range(mix64(pt ^ (uint64_t)j), a.n);
+                            if (tgt - xlo < tl.Gw) {  // (unsigned) the target is in group x
+                                const uint32_t jd = a.lists > 1 ? hash_range(key_hash(a.m.keys.delay, s, j), a.lists) : 0u;
+                                keep = !(dbg && a.dbg_j >= 0 && (int32_t)jd != a.dbg_j);
+                                if (keep) r = proc_record<CMP>(a, s, j, tgt, jd);
+                            }
+                        }
+                    }
+                    const uint64_t bal = __ballot(keep);
+                    if (keep) {
+                        const uint32_t rank =
+                            __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+                        L.ring[w][(head + cnt + rank) & (kRing - 1)] = r;
+                    }
+                    cnt += (uint32_t)__popcll(bal);
+                    vcur += kWave;
+                    j += kWave;
+                    while (j >= kout) {
+                        j -= kout;
+                        si++;
+                    }
+                }
+                lds_wave_sync();  // the ring's new entries are visible to every lane
+                const uint32_t avail = cnt < kWave ? cnt : kWave;
+                const bool ok = lane < avail;
+                rec[u] = L.ring[w][(head + lane) & (kRing - 1)];  // (read unconditionally; used if ok)
+                okm |= (uint32_t)ok << u;
+                head += avail;
+                cnt -= avail;
+                lds_wave_sync();  // taken before the ring is written again
+            }
+            if (lane == 0) L.more[w] = cnt > 0 || vcur < ve ? 1u : 0u;
+            // rank every event of the window within its bucket (LDS counters)
+            uint32_t tr[kProcR];
+#pragma unroll
+            for (int q = 0; q < kProcR; q++) {
+                tr[q] = 0xffffffffu;
+                if (!((okm >> q) & 1u)) continue;
+                const uint32_t key = rec_key(rec[q]);
+                const uint32_t local = rec_target(key) - xlo;
+                const uint32_t b = (dbg ? 0u : rec_delay(key)) * tl.T8 + (local >> tl.logW);
+                const uint32_t rank = atomicAdd(&L.bcnt[b], 1u);
+                tr[q] = (b << 16) | rank;
+                const uint32_t sv = (b << 16) | (local & (tl.W - 1));
+                if constexpr (CMP) rec[q] = sv | (rec_class(key) << kPageClassShift);
+                else rec[q].x = (int)sv;
+            }
+            lds_sync();
+            // bucket starts in the stage; the page position of staged event q
+            // of bucket b is wb[b] + q (mod 2^32); the fill counters advance
+            uint32_t staged;
+            {
+                const uint32_t P = (NB + kProcThreads - 1) / kProcThreads;
+                const uint32_t b0 = tid * P;
+                uint32_t sum = 0;
+                for (uint32_t k = 0; k < P; k++)
+                    if (b0 + k < NB) sum += L.bcnt[b0 + k];
+                uint32_t ex = block_scan_u32_open(sum, L.ws, &staged);
+                for (uint32_t k = 0; k < P; k++) {
+                    if (b0 + k < NB) {
+                        const uint32_t bb = b0 + k, c = L.bcnt[bb], f = L.fill[bb];
+                        L.bst[bb] = ex;
+                        L.wb[bb] = f - ex;
+                        L.fill[bb] = f + c;
+                        L.bcnt[bb] = 0;
+                        ex += c;
+                    }
+                }
+            }
+            lds_sync();
+#pragma unroll
+            for (int q = 0; q < kProcR; q++) {
+                if (tr[q] == 0xffffffffu) continue;
+                L.stage[L.bst[tr[q] >> 16] + (tr[q] & 0xffffu)] = rec[q];
+            }
+            lds_sync();
+            // coalesced appends: consecutive staged events of a bucket go to
+            // consecutive page positions
+            for (uint32_t q = tid; q < staged; q += kProcThreads) {
+                const Rec r2 = L.stage[q];
+                const uint32_t key = rec_key(r2);
+                const uint32_t b = key >> 16, low = key & 0xffffu;
+                const uint32_t pos = L.wb[b] + q;
+                if (pos < cap) {
+                    const uint64_t e = (uint64_t)L.pidx[b] * cap + pos;
+                    if constexpr (CMP) a.pages16[e] = (uint16_t)low;
+                    else a.pages[e] = make_int2((int)low, r2.y);
+                } else {
+                    long long units;
+                    uint32_t local;
+                    if constexpr (CMP) {
+                        units = class_units(a, low >> kPageClassShift);
+                        local = low & kPageLocalMask;
+                    } else {
+                        units = units_of<FIXED>(r2.y, a.m.shift64);
+                        local = low;
+                    }
+                    overflow_add<FIXED>(a, arrival_slot(a, t, b / tl.T8, dbg), x * tl.T8 + b % tl.T8, local, units);
+                }
+            }
+            uint32_t any = 0;
+            for (uint32_t k = 0; k < kProcWaves; k++) any |= L.more[k];
+            lds_sync();  // the stage, wb and more[] are read before the next window writes them
+            if (!any) break;
+        }
+    }
+    lds_sync();
+    for (uint32_t b = tid; b < NB; b += kProcThreads) a.pfill[L.pidx[b]] = L.fill[b];
+    if (!dbg && x == 0) {  // events emitted at t, counted once per spike
+        const uint64_t tot = block_sum_u64(emitted, L.ws64);
+        if (tid == 0 && tot) atomicAdd((unsigned long long *)&a.events8[t * kGroups], (unsigned long long)tot);
+    }
+}
+
+// Rows of the given sources as generated, synapse j of row r at out_off[r] + j:
+// target, weight bits as the full format stores them (compact classes: the
+// class's bits from the table), delay.
+__global__ __launch_bounds__(256) void k_export_proc(StepArgs a, ClassTab tab, const uint32_t *rows,
+                                                     const uint64_t *out_off, uint32_t *col, uint32_t *wbits,
+                                                     uint8_t *delay)
+{
+    const uint32_t s = rows[blockIdx.x];
+    const uint64_t o = out_off[blockIdx.x];
+    const uint64_t pt = mix64(a.m.keys.tgt ^ (uint64_t)s);
+    for (uint32_t j = threadIdx.x; j < a.pr.k_out; j += 256) {
+        const uint32_t tgt = hash_range(mix64(pt ^ (uint64_t)j), a.n);
+        const uint32_t jd = a.lists > 1 ? hash_range(key_hash(a.m.keys.delay, s, j), a.lists) : 0u;
+        uint32_t wb;
+        if (a.compact) {
+            wb = tab.bits[s < a.pr.n_exc ? 0 : 1];
+        } else {
+            wb = (uint32_t)proc_record<false>(a, s, j, tgt, jd).y;
+        }
+        col[o + j] = tgt;
+        wbits[o + j] = wb;
+        delay[o + j] = (uint8_t)(a.dmin + jd);
+    }
+}
+
+// Per-target sum of the |weight| terms of every in-synapse (the units of the
+// stored-row range pass: |quantised w| in fixed mode, |w| in units of 2^-24
+// rounded up in fp32 mode), one global atomic per generated synapse.
+__global__ __launch_bounds__(256) void k_proc_in_abs_sum(StepArgs a, unsigned long long *insum)
+{
+    const uint32_t s = blockIdx.x;
+    const uint64_t pt = mix64(a.m.keys.tgt ^ (uint64_t)s);
+    for (uint32_t j = threadIdx.x; j < a.pr.k_out; j += 256) {
+        const uint32_t tgt = hash_range(mix64(pt ^ (uint64_t)j), a.n);
+        const int2 r = proc_record<false>(a, s, j, tgt, 0u);
+        unsigned long long q;
+        if (a.m.fixed) q = (unsigned long long)(r.y < 0 ? -(long long)r.y : (long long)r.y);
+        else q = (unsigned long long)ceil(ldexp((double)fabsf(__int_as_float(r.y)), 24));
+        atomicAdd(&insum[tgt], q);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_push_proc(const StepArgs &a, uint32_t i, int64_t t_explicit, hipStream_t s)
+{
+    const uint32_t nj = a.dbg_spikes ? 1u : a.lists;
+    if (!a.proc || a.direct || a.tl.T > kMaxTiles || a.tl.T != kGroups * a.tl.T8 || nj * a.tl.T8 > kMaxBuckets ||
+        a.tl.W > 8192 || a.pg1 == 0 || a.pslots == 0 || a.page_cap == 0 || a.pr.k_out > kMaxRow)
+        return hipErrorInvalidValue;
+    if (a.compact ? !a.pages16 : !a.pages) return hipErrorInvalidValue;
+    const dim3 grid(kGroups * a.pg1), block(kProcThreads);
+    if (a.compact) {
+        if (a.m.fixed) hipLaunchKernelGGL((k_push_proc<true, true>), grid, block, 0, s, a, i, t_explicit);
+        else hipLaunchKernelGGL((k_push_proc<false, true>), grid, block, 0, s, a, i, t_explicit);
+    } else {
+        if (a.m.fixed) hipLaunchKernelGGL((k_push_proc<true, false>), grid, block, 0, s, a, i, t_explicit);
+        else hipLaunchKernelGGL((k_push_proc<false, false>), grid, block, 0, s, a, i, t_explicit);
+    }
+    return hipGetLastError();
+}
+
+hipError_t export_proc(const StepArgs &a, const ClassTab &tab, const uint32_t *rows, uint64_t n_rows,
+                       const uint64_t *out_off, uint32_t *col, uint32_t *wbits, uint8_t *delay, hipStream_t s)
+{
+    if (!n_rows) return hipSuccess;
+    if (n_rows > 0x7fffffffull || !a.proc) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_export_proc, dim3((uint32_t)n_rows), dim3(256), 0, s, a, tab, rows, out_off, col, wbits,
+                       delay);
+    return hipGetLastError();
+}
+
+hipError_t proc_in_abs_sum(const StepArgs &a, uint64_t *insum, hipStream_t s)
+{
+    if (!a.proc || a.n == 0) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_proc_in_abs_sum, dim3(a.n), dim3(256), 0, s, a, (unsigned long long *)insum);
+    return hipGetLastError();
+}
+
+}  // namespace spk

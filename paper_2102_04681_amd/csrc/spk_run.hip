@@ -1167,7 +1167,7 @@ bool run_supported(const StepArgs &a, uint32_t R)
 {
     const Tiling &tl = a.tl;
     if (R == 0 || R > kRunMaxR || tl.T8 > R || tl.T != kGroups * tl.T8 || tl.W > kMaxTileW) return false;
-    if (a.m.pois_len > 256) return false;
+    if (a.m.pois_len > 256 || a.proc) return false;
     if (a.direct) return a.lists == 1 && a.spk_slots > a.dmin;
     return a.pg1 == R && a.pslots * tl.T8 <= kRunMaxFill && a.lists * tl.T8 <= kRunMaxBuckets && a.spk_slots >= 2 &&
            a.page_cap % 16 == 0 && tl.W <= 65536;

@@ -188,6 +188,7 @@ struct spk_net {
     uint64_t *row_ptr = nullptr;
     // synapses: full (int2) or compact (u32 with a weight class)
     bool compact = false;
+    bool proc = false;  // procedural synapses: generated when their source fires, not stored
     uint32_t n_cls = 0;
     float cls_w[kMaxClasses] = {};
     ClassTab ctab{};
@@ -317,6 +318,15 @@ StepArgs step_args(const spk_net *net)
     a.direct = net->direct ? 1u : 0u;
     a.row_ptr = net->row_ptr;
     a.compact = net->compact ? 1u : 0u;
+    a.proc = net->proc ? 1u : 0u;
+    a.pr.k_out = net->P.k_out;
+    a.pr.n_exc = net->n_exc;
+    a.pr.w_uniform = net->P.w_uniform;
+    a.pr.w_lo = net->P.w_lo;
+    a.pr.w_hi = net->P.w_hi;
+    a.pr.w_exc = net->P.w_exc;
+    a.pr.w_inh = net->P.w_inh;
+    a.pr.qscale = std::ldexp(1.0f, net->P.fixed_shift);
     for (uint32_t k = 0; k < kMaxClasses; k++) a.wval[k] = net->wval[k];
     a.syn = net->syn;
     a.syn32 = net->syn32;
@@ -423,6 +433,59 @@ bool range_by_targets(const spk_net *net)
     return (double)net->nnz * 70.0 > (double)net->n * (double)net->n;
 }
 
+// Fixed out-degree networks with population weights (generated, compact
+// classes = source populations): the range from the synapses drawn again and
+// filed by target tile, counted per class in LDS (no global atomic per
+// synapse).  SPK_RANGE_PASS=atomics forces the per-synapse atomic pass.
+bool range_by_tiles(const spk_net *net)
+{
+    if (net->P.conn_kind != SPK_CONN_FIXED_OUT || !net->compact || net->n_cls > 2) return false;
+    if (const char *e = std::getenv("SPK_RANGE_PASS")) return std::strcmp(e, "atomics") != 0;
+    return true;
+}
+
+// Largest in_abs_sum of a fixed out-degree network by tiles (range_by_tiles);
+// *ok = false (and nothing changed) when its temporary buckets (2 bytes per
+// synapse) cannot be allocated.
+spk_status fo_range(spk_net *net, uint64_t *m, bool *ok)
+{
+    hipStream_t s = net->stream;
+    const ConnArgs c = conn_args(net);
+    const uint32_t T = net->tl.T, nb = fo_blocks(net->n);
+    *ok = false;
+    uint16_t *entries = nullptr;
+    if (dalloc(net, &entries, (size_t)std::max<uint64_t>(net->nnz, 1)) != SPK_OK) {
+        (void)hipGetLastError();  // the failed allocation is not an error of a later call
+        return SPK_OK;
+    }
+    uint32_t *base = nullptr, *tot = nullptr;
+    uint64_t *start = nullptr, *mx = nullptr;
+    SPK_TRY(dalloc(net, &base, (size_t)nb * T));
+    SPK_TRY(dalloc(net, &tot, T));
+    SPK_TRY(dalloc(net, &start, T + 1));
+    SPK_TRY(dalloc(net, &mx, 1));
+    SPK_HIP(hipMemsetAsync(tot, 0, (size_t)T * 4, s));
+    SPK_HIP(hipMemsetAsync(mx, 0, 8, s));
+    SegTimer tm;
+    SPK_HIP(tm.start(s));
+    SPK_HIP(fo_count(c, base, tot, s));
+    std::vector<uint32_t> ht(T);
+    SPK_HIP(hipMemcpyAsync(ht.data(), tot, (size_t)T * 4, hipMemcpyDeviceToHost, s));
+    SPK_HIP(hipStreamSynchronize(s));
+    std::vector<uint64_t> hs(T + 1, 0);
+    for (uint32_t k = 0; k < T; k++) hs[k + 1] = hs[k] + ht[k];
+    if (hs[T] != net->nnz) return fail(SPK_EHIP, "range pass: filed synapses do not add up to nnz");
+    SPK_HIP(hipMemcpyAsync(start, hs.data(), (size_t)(T + 1) * 8, hipMemcpyHostToDevice, s));
+    SPK_HIP(fo_file(c, base, start, entries, s));
+    SPK_HIP(fo_max(c, start, entries, net->ctab, mx, s));
+    SPK_HIP(tm.stop(s, &net->range_ms));
+    SPK_HIP(hipMemcpyAsync(m, mx, 8, hipMemcpyDeviceToHost, s));
+    SPK_HIP(hipStreamSynchronize(s));  // (hs is host memory read by the copy above)
+    dfree(net, entries); dfree(net, base); dfree(net, tot); dfree(net, start); dfree(net, mx);
+    *ok = true;
+    return SPK_OK;
+}
+
 // The term of one synapse of weight w in the accumulator-range bound, as the
 // range pass computes it: |quantised w| (fixed mode) or |w| in units of
 // 2^-24 rounded up (fp32 mode).
@@ -487,7 +550,16 @@ spk_status derive(spk_net *net, bool explicit_csr)
     if (P.neuron_kind > SPK_SOURCE) return fail(SPK_EINVAL, "neuron_kind");
     if (P.acc_mode > SPK_ACC_FIXED) return fail(SPK_EINVAL, "acc_mode");
     if (P.delivery > SPK_DELIVERY_BINNED) return fail(SPK_EINVAL, "delivery");
-    if (P.syn_format > SPK_FORMAT_COMPACT) return fail(SPK_EINVAL, "syn_format");
+    if (P.syn_format > SPK_FORMAT_PROCEDURAL) return fail(SPK_EINVAL, "syn_format");
+    if (P.syn_format == SPK_FORMAT_PROCEDURAL) {
+        if (explicit_csr || P.conn_kind != SPK_CONN_FIXED_OUT || P.k_out == 0)
+            return fail(SPK_EINVAL, "procedural synapses need a generated fixed out-degree network (k_out >= 1)");
+        if (P.delivery == SPK_DELIVERY_DIRECT)
+            return fail(SPK_EINVAL, "procedural synapses are delivered binned (each fired row generated once)");
+        if (P.step_mode == SPK_STEP_PERSISTENT)
+            return fail(SPK_EINVAL, "procedural synapses run as graphs of steps, not in the persistent kernel");
+        net->proc = true;
+    }
     if (P.step_mode > SPK_STEP_PERSISTENT) return fail(SPK_EINVAL, "step_mode");
     if (!explicit_csr && P.conn_kind > SPK_CONN_FIXED_IN) return fail(SPK_EINVAL, "conn_kind");
     if (!(P.p >= 0.0 && P.p <= 1.0)) return fail(SPK_EINVAL, "p in [0,1]");
@@ -626,7 +698,13 @@ spk_status finish_rows(spk_net *net)
 {
     hipStream_t s = net->stream;
     SPK_TRY(dalloc(net, &net->outdeg, net->n));
-    SPK_HIP(out_degree(net->row_ptr, net->n, net->outdeg, s));
+    if (net->proc) {  // every row has k_out synapses
+        const std::vector<uint32_t> deg(net->n, net->P.k_out);
+        SPK_HIP(hipMemcpyAsync(net->outdeg, deg.data(), (size_t)net->n * 4, hipMemcpyHostToDevice, s));
+        SPK_HIP(hipStreamSynchronize(s));
+    } else {
+        SPK_HIP(out_degree(net->row_ptr, net->n, net->outdeg, s));
+    }
 
     // Accumulator range.  Fixed mode: all in-synapses of one neuron at once,
     // plus the largest Poisson count and the bias, must fit in int32.  fp32
@@ -634,7 +712,11 @@ spk_status finish_rows(spk_net *net)
     // possible sum allows.
     const bool fixed = net->P.acc_mode == SPK_ACC_FIXED;
     uint64_t m = 0;
-    if (net->P.conn_kind == SPK_CONN_FIXED_IN && !net->P.w_uniform) {
+    bool done = false;
+    if (range_by_tiles(net)) SPK_TRY(fo_range(net, &m, &done));
+    if (done) {
+        // (the range is known)
+    } else if (net->P.conn_kind == SPK_CONN_FIXED_IN && !net->P.w_uniform) {
         // every neuron has exactly k_in_exc excitatory and k_in_inh
         // inhibitory in-synapses, each with its population's weight: the
         // largest sum is every neuron's, no pass over the synapses needed
@@ -668,7 +750,8 @@ spk_status finish_rows(spk_net *net)
         SPK_HIP(hipMemsetAsync(mx, 0, 8, s));
         SegTimer tm;
         SPK_HIP(tm.start(s));
-        SPK_HIP(in_abs_sum(syn_ptr(net), net->nnz, fixed, net->compact, net->ctab, insum, s));
+        if (net->proc) SPK_HIP(proc_in_abs_sum(step_args(net), insum, s));
+        else SPK_HIP(in_abs_sum(syn_ptr(net), net->nnz, fixed, net->compact, net->ctab, insum, s));
         SPK_HIP(max_u64(insum, net->n, mx, s));
         SPK_HIP(tm.stop(s, &net->range_ms));
         SPK_HIP(hipMemcpyAsync(&m, mx, 8, hipMemcpyDeviceToHost, s));
@@ -747,8 +830,21 @@ spk_status finish_rows(spk_net *net)
     return SPK_OK;
 }
 
+// Procedural synapses: nothing is generated or stored at creation; every
+// row has k_out synapses, drawn when its source fires (binned delivery).
+spk_status generate_proc(spk_net *net)
+{
+    net->nnz = (uint64_t)net->n * net->P.k_out;
+    net->max_row = net->P.k_out;
+    if ((uint64_t)net->lists * net->tl.T8 > kMaxBuckets)
+        return fail(SPK_EINVAL, "binned delivery supports at most 2048 (delay, tile) buckets per XCD group");
+    net->direct = false;
+    return finish_rows(net);
+}
+
 spk_status generate(spk_net *net)
 {
+    if (net->proc) return generate_proc(net);
     hipStream_t s = net->stream;
     uint32_t *cnt = nullptr;
     SPK_TRY(dalloc(net, &cnt, net->n));
@@ -757,11 +853,16 @@ spk_status generate(spk_net *net)
     const bool in_rows = net->P.conn_kind == SPK_CONN_FIXED_IN;
     // Bernoulli rows: the count pass keeps every row's bucket counts (u16,
     // both deliveries' buckets), so the placement pass draws each row once
+    // (SPK_GEN_HIST=0 skips it, as when it cannot be allocated: a test knob)
     uint16_t *hist = nullptr;
     const uint64_t hist_elems = (uint64_t)net->n * (net->tl.T + 2 * kGroups);
-    if (net->P.conn_kind == SPK_CONN_BERNOULLI && hist_elems * 2 <= (4ull << 30) &&
-        dalloc(net, &hist, hist_elems) != SPK_OK)
-        hist = nullptr;  // (then the placement pass counts for itself)
+    const char *gh = std::getenv("SPK_GEN_HIST");
+    const bool want_hist = !(gh && std::strcmp(gh, "0") == 0);
+    if (net->P.conn_kind == SPK_CONN_BERNOULLI && want_hist && hist_elems * 2 <= (4ull << 30) &&
+        dalloc(net, &hist, hist_elems) != SPK_OK) {
+        hist = nullptr;          // (then the placement pass counts for itself)
+        (void)hipGetLastError();  // the failed allocation is not an error of the launches below
+    }
     // ... and keeps each row's synapses, up to cap = mean + 10 sd + 64 per
     // row, so that the placement pass need not draw the rows again (unless a
     // row turns out longer, or the keys would take more than 32 GB)
@@ -773,7 +874,10 @@ spk_status generate(spk_net *net)
         const double capd = std::ceil(p * nn + 10.0 * std::sqrt(nn * p * (1.0 - p)) + 64.0);
         if (capd <= (double)kMaxRow && (double)net->n * capd * 4.0 <= (double)(32ull << 30)) {
             cap = (uint32_t)capd;
-            if (dalloc(net, &keys, (size_t)net->n * cap) != SPK_OK) keys = nullptr;
+            if (dalloc(net, &keys, (size_t)net->n * cap) != SPK_OK) {
+                keys = nullptr;
+                (void)hipGetLastError();
+            }
         }
     }
     SegTimer tm;
@@ -1528,8 +1632,11 @@ spk_status spk_export_rows(spk_net *net, const uint32_t *rows, uint64_t n_rows, 
     SPK_TRY(dalloc(net, &d_del, tot));
     SPK_HIP(hipMemcpyAsync(d_rows, rows, n_rows * 4, hipMemcpyHostToDevice, s));
     SPK_HIP(hipMemcpyAsync(d_off, offs, n_rows * 8, hipMemcpyHostToDevice, s));
-    SPK_HIP(export_gather(net->row_ptr, syn_ptr(net), net->compact, net->ctab, net->dmin, d_rows, n_rows, d_off,
-                          d_col, d_wb, d_del, s));
+    if (net->proc)
+        SPK_HIP(export_proc(step_args(net), net->ctab, d_rows, n_rows, d_off, d_col, d_wb, d_del, s));
+    else
+        SPK_HIP(export_gather(net->row_ptr, syn_ptr(net), net->compact, net->ctab, net->dmin, d_rows, n_rows,
+                              d_off, d_col, d_wb, d_del, s));
     std::vector<uint32_t> hc(tot), hw(tot);
     std::vector<uint8_t> hd(tot);
     if (tot) {
@@ -1589,7 +1696,7 @@ spk_status spk_stats(spk_net *net, spk_stats_t *out)
     st.pois_len = net->pois_len;
     st.fixed_shift = net->P.acc_mode == SPK_ACC_FIXED ? net->P.fixed_shift : net->shift64;
     st.k = net->k;
-    st.bytes_per_synapse = net->compact ? 4.0 : 8.0;
+    st.bytes_per_synapse = net->proc ? 0.0 : net->compact ? 4.0 : 8.0;
     st.tile_width = net->tl.W;
     st.tiles = net->tl.T;
     st.delivery = net->direct ? SPK_DELIVERY_DIRECT : SPK_DELIVERY_BINNED;

@@ -588,6 +588,7 @@ uint32_t push_blocks_per_group()
 
 hipError_t launch_push(const StepArgs &a, uint32_t i, int64_t t_explicit, hipStream_t s)
 {
+    if (a.proc) return launch_push_proc(a, i, t_explicit, s);
     const uint32_t nj = a.dbg_spikes ? 1u : a.lists;
     if (a.direct || a.tl.T > kMaxTiles || a.tl.T != kGroups * a.tl.T8 || nj * a.tl.T8 > kMaxBuckets ||
         a.tl.W > 65536 || a.pg1 == 0 || a.pg1 > kPushThreads || a.pslots == 0 || a.page_cap == 0)
@@ -610,8 +611,11 @@ hipError_t launch_tile(const StepArgs &a, uint32_t i, int64_t t_explicit, hipStr
         (!a.direct && (a.pg1 == 0 || a.pg1 > kTileThreads || a.pslots == 0)) || a.spk_slots == 0 ||
         (a.direct && a.spk_slots <= a.dmin && !a.dbg_out))
         return hipErrorInvalidValue;
-    if (a.compact ? !a.syn32 || (!a.direct && !a.pages16) : !a.syn || (!a.direct && !a.pages))
-        return hipErrorInvalidValue;
+    // rows are read only by direct delivery (procedural synapses are never
+    // stored, and always binned); pages only by binned delivery
+    const bool rows_ok = a.proc ? !a.direct : (a.compact ? a.syn32 != nullptr : a.syn != nullptr);
+    const bool pages_ok = a.direct || (a.compact ? a.pages16 != nullptr : a.pages != nullptr);
+    if (!rows_ok || !pages_ok) return hipErrorInvalidValue;
     if (!a.direct && (a.page_cap % 16)) return hipErrorInvalidValue;  // record pairs stay in their page
     const dim3 grid(a.tl.T), block(kTileThreads);
     if (a.compact) {

@@ -24,7 +24,7 @@ SPK_LIF, SPK_SOURCE = 0, 1
 SPK_CONN_BERNOULLI, SPK_CONN_FIXED_OUT, SPK_CONN_FIXED_IN, SPK_CONN_EXPLICIT = 0, 1, 2, 3
 SPK_ACC_F32, SPK_ACC_FIXED = 0, 1
 SPK_DELIVERY_AUTO, SPK_DELIVERY_DIRECT, SPK_DELIVERY_BINNED = 0, 1, 2
-SPK_FORMAT_AUTO, SPK_FORMAT_FULL, SPK_FORMAT_COMPACT = 0, 1, 2
+SPK_FORMAT_AUTO, SPK_FORMAT_FULL, SPK_FORMAT_COMPACT, SPK_FORMAT_PROCEDURAL = 0, 1, 2, 3
 SPK_STEP_AUTO, SPK_STEP_GRAPH, SPK_STEP_PERSISTENT = 0, 1, 2
 
 EXPORTED = [

@@ -60,7 +60,7 @@ def test_algorithmic_bytes_of_the_3e9_synapse_workload():
     assert b[4] == pytest.approx(4.0 * events + other)
     assert b[8] / steps == pytest.approx(44.0e6, rel=1e-3)  # 24 MB of events + 20 MB of neurons
     ev, neu = bench.algorithmic_bytes(1_000_000, 1, 10.0, 2.0, 3, split=True)
-    assert ev == {8: 80.0, 4: 40.0} and neu == 8.0 * 1_000_000 * 3 + 16.0
+    assert ev == {8: 80.0, 4: 40.0, 0: 0.0} and neu == 8.0 * 1_000_000 * 3 + 16.0
 
 
 def test_settle_steps_cover_transient_and_delays():

@@ -130,6 +130,35 @@ def test_generator_two_draws_equals_oracle(spk, name, monkeypatch):
     _compare_rows(offs, col, w, d, o_rp, o_col, o_w, o_d, range(cfg["n"]), cfg["acc_mode"] == I.ACC_FIXED)
 
 
+def test_generator_without_count_keeping_equals_oracle(spk, monkeypatch):
+    """Bernoulli rows placed without the count pass's per-row bucket counts
+    (the path taken where they cannot be allocated: SPK_GEN_HIST=0) equal the
+    oracle's rows."""
+    monkeypatch.setenv("SPK_GEN_HIST", "0")
+    cfg = I.config(0, n=1500, p=0.05, delay_min=2, delay_max=9, seed=4)
+    g = spk.Net(cfg, max_steps=1)
+    o = oracle.Net(cfg)
+    o_rp, o_col, o_w, o_d = o.csr()
+    offs, col, w, d = g.csr()
+    _compare_rows(offs, col, w, d, o_rp, o_col, o_w, o_d, range(cfg["n"]), False)
+
+
+@pytest.mark.parametrize("atomics", ["0", "1"], ids=["lds", "per-synapse"])
+def test_fixed_in_generator_several_source_ranges(spk, atomics, monkeypatch):
+    """Fixed in-degree rows of a network larger than one LDS source range
+    (70,000 neurons: three ranges of 32,768 sources), counted per block in LDS
+    or (SPK_GEN_IN_ATOMICS=1) with one global atomic per synapse, equal the
+    oracle's rows."""
+    monkeypatch.setenv("SPK_GEN_IN_ATOMICS", atomics)
+    cfg = I.config(2, n=70_000, k_in_exc=40, k_in_inh=10, seed=5)
+    g = spk.Net(cfg, max_steps=1)
+    o = oracle.Net(cfg)
+    o_rp, o_col, o_w, o_d = o.csr()
+    assert g.stats()["nnz"] == len(o_col)
+    offs, col, w, d = g.csr()
+    _compare_rows(offs, col, w, d, o_rp, o_col, o_w, o_d, range(cfg["n"]), False)
+
+
 @pytest.mark.parametrize("name,mk", GEN_CASES, ids=[c[0] for c in GEN_CASES])
 @pytest.mark.parametrize("fmt", [f for f, _ in FORMATS], ids=[n for _, n in FORMATS])
 def test_generator_equals_oracle(spk, name, mk, fmt):
@@ -512,6 +541,36 @@ def test_range_pass_per_target_matches_oracle(spk, w_uniform, monkeypatch):
                 assert e.value.code == spk.SPK_EOVERFLOW
 
 
+@pytest.mark.parametrize("mode", ["tiles", "atomics"])
+def test_range_pass_fixed_out_matches_oracle(spk, mode, monkeypatch):
+    # fixed out-degree networks with population weights: the largest
+    # per-neuron sum of |quantised weights| from the synapses filed by target
+    # tile (default) or one atomic per synapse; both must refuse exactly the
+    # networks the oracle refuses, weights scaled to land just inside and
+    # just outside int32
+    monkeypatch.setenv("SPK_RANGE_PASS", mode)
+    base = dict(n=3000, k_out=300, acc_mode=I.ACC_FIXED, fixed_shift=20, ext_lambda=0.0, ext_w=0.0)
+    unit = I.config(4, **base)
+    m1 = int(oracle.Net(unit).in_abs_sum_q().max())
+    assert m1 > 0
+    for scale, fits in ((0.999, True), (1.001, False)):
+        f = scale * (2**31 - 1) / m1
+        cfg = I.config(4, **dict(base, w_exc=unit["w_exc"] * f, w_inh=unit["w_inh"] * f))
+        try:
+            ok = int(oracle.Net(cfg).in_abs_sum_q().max()) <= 2**31 - 1
+        except oracle.OracleError as e:
+            assert e.code == -4
+            ok = False
+        assert ok == fits
+        if fits:
+            st = spk.Net(cfg, max_steps=1).stats()
+            assert st["range_ms"] > 0
+        else:
+            with pytest.raises(spk.SpkError) as e:
+                spk.Net(cfg, max_steps=1)
+            assert e.value.code == spk.SPK_EOVERFLOW
+
+
 @pytest.mark.parametrize("seed", [1, 2])
 def test_fp32_mode_mean_rate_within_one_percent(spk, seed):
     # fp32 atomics: spike trains diverge after the first rounding
@@ -679,3 +738,103 @@ def test_step_mode_selection(spk, monkeypatch):
     with pytest.raises(spk.SpkError) as e:
         spk.Net(dict(cfg, step_mode=2), max_steps=1)
     assert e.value.code == spk.SPK_EINVAL
+
+
+# ------------------------------------------------ procedural connectivity
+
+PROC_CASES = [
+    ("C4-8000", lambda acc: I.scaled(4, 8000, k_out=700, acc_mode=acc)),
+    ("C4-d3-9", lambda acc: I.scaled(4, 6000, k_out=500, delay_min=3, delay_max=9, acc_mode=acc)),
+    ("C3-8000", lambda acc: I.scaled(3, 8000, k_out=1000, acc_mode=acc)),
+]
+
+
+@pytest.mark.parametrize("name,mk", PROC_CASES, ids=[c[0] for c in PROC_CASES])
+@pytest.mark.parametrize("acc", [I.ACC_F32, I.ACC_FIXED], ids=["f32", "fixed"])
+def test_procedural_rows_and_delivery_equal_oracle(spk, name, mk, acc):
+    # procedural synapses are never stored: the rows the library generates
+    # (exported) equal the oracle's, and delivering a spike set through them
+    # equals the oracle's sums (exact in fixed mode, the rounded exact sum in
+    # fp32 mode) and the stored compact/full format's bit for bit
+    cfg = dict(mk(acc), syn_format=3)
+    g = spk.Net(cfg, max_steps=1)
+    st = g.stats()
+    assert st["bytes_per_synapse"] == 0.0 and st["delivery"] == spk.SPK_DELIVERY_BINNED
+    assert st["step_mode"] == spk.SPK_STEP_GRAPH and st["nnz"] == cfg["n"] * cfg["k_out"]
+    o = _oracle_net(cfg)
+    o_rp, o_col, o_w, o_d = o.csr()
+    rows = np.arange(0, cfg["n"], 13, dtype=np.uint32)
+    offs, col, w, d = g.export_rows(rows)
+    _compare_rows(offs, col, w, d, o_rp, o_col, o_w, o_d, rows, acc == I.ACC_FIXED)
+    stored = spk.Net(dict(cfg, syn_format=0, step_mode=1), max_steps=1)
+    n = cfg["n"]
+    for k, count in enumerate([0, 1, 37, n // 200, n // 3, 3 * n]):
+        spikes = I.spike_set(n, count, seed=30 + k, unique=count <= n)
+        for delay in sorted({0, cfg["delay_min"], cfg["delay_max"]}):
+            _say(f"[proc deliver] {name} acc={acc} spikes={len(spikes)} delay={delay}")
+            got = g.debug_deliver(spikes, delay=delay)
+            if acc == I.ACC_FIXED:
+                _, want = o.deliver(spikes, delay=delay, fixed=True)
+                assert np.array_equal(got.astype(np.int64), want), "fixed-point inputs differ"
+            else:
+                want = o.deliver(spikes, delay=delay)
+                ulp = np.spacing(np.abs(want).astype(np.float32)).astype(np.float64)
+                assert np.all(np.abs(got.astype(np.float64) - want) <= ulp)
+            assert np.array_equal(got.view(np.uint32), stored.debug_deliver(spikes, delay=delay).view(np.uint32))
+
+
+PROC_RUNS = [
+    ("C4-12000", lambda: I.scaled(4, 12000, k_out=1500), 400),
+    ("C4-d3-9", lambda: I.scaled(4, 12000, k_out=1500, delay_min=3, delay_max=9), 300),
+    ("C3-20000", lambda: I.scaled(3, 20000, k_out=1000), 100),
+]
+
+
+@pytest.mark.parametrize("name,mk,T", PROC_RUNS, ids=[c[0] for c in PROC_RUNS])
+def test_procedural_simulation_bit_identical(spk, name, mk, T, monkeypatch):
+    # fixed point: rasters, counts, events, delivered events and final state
+    # equal the oracle's; also with the pages shrunk into the overflow path
+    cfg = dict(mk(), acc_mode=I.ACC_FIXED, syn_format=3)
+    r, ov, orf, (rp, col, w, d) = _oracle_run(cfg, T)
+    assert r["counts"].sum() > 0
+    for cap in (None, "64"):
+        if cap:
+            monkeypatch.setenv("SPK_PAGE_CAP", cap)
+        _say(f"[proc run] {name} T={T} page_cap={cap or 'budget'}")
+        g = spk.Net(cfg, max_steps=T, raster_capacity=cfg["n"] * T)
+        g.step(T // 3)
+        g.step(T - T // 3)
+        offs, ids = g.raster()
+        assert np.array_equal(g.spike_counts(), r["counts"]), "spike counts differ"
+        assert np.array_equal(ids, r["raster"]), "rasters differ"
+        assert np.array_equal(g.events(), r["events"])
+        assert np.array_equal(g.delivered(), r["delivered"])
+        gv, gr = g.state()
+        assert np.array_equal(gv.view(np.uint32), ov.view(np.uint32)), "membrane potentials differ"
+        assert np.array_equal(gr, orf)
+
+
+def test_procedural_fp32_equals_stored(spk):
+    # fp32 mode sums exactly: the procedural network and the stored one step
+    # bit for bit alike (graph path both)
+    cfg = dict(I.scaled(4, 20000, k_out=1500), step_mode=1)
+    T = 600
+    out = []
+    for fmt in (3, 0):
+        g = spk.Net(dict(cfg, syn_format=fmt), max_steps=T, raster_capacity=cfg["n"] * T)
+        g.step(T)
+        out.append((g.raster()[1], g.state()[0], g.delivered()))
+    assert len(out[0][0]) > 0
+    assert np.array_equal(out[0][0], out[1][0])
+    assert np.array_equal(out[0][1].view(np.uint32), out[1][1].view(np.uint32))
+    assert np.array_equal(out[0][2], out[1][2])
+
+
+def test_procedural_rejects_what_it_does_not_take(spk):
+    for cfg in (dict(I.scaled(2, 4000, k_in_exc=300, k_in_inh=75), syn_format=3),
+                dict(I.config(0), syn_format=3),
+                dict(I.scaled(4, 4000, k_out=300), syn_format=3, delivery=1),
+                dict(I.scaled(4, 4000, k_out=300), syn_format=3, step_mode=2)):
+        with pytest.raises(spk.SpkError) as e:
+            spk.Net(cfg, max_steps=1)
+        assert e.value.code == spk.SPK_EINVAL

@@ -12,7 +12,9 @@ sizes and in the launch configuration bench.py times:
     overflow path delivers part of every step's events;
   - the 1e9-synapse source network (1,000,000 Bernoulli sources, fan-out
     1,000, w ~ U[0, 1e-3)) at 10 Hz for 100 steps and at 50 Hz for 20 steps,
-    direct delivery, tiles of 4,096 neurons.
+    direct delivery, tiles of 4,096 neurons;
+  - both networks with procedural synapses (none stored: every fired row is
+    generated again from the hash; binned delivery, steps as graphs).
 
 The oracle simulates these networks step by step with the row of every
 spike generated when it is delivered (it cannot store 3e9 synapses); rasters,
@@ -153,20 +155,25 @@ def _compare(gpu, ref, check_ref=True):
 
 
 @pytest.mark.timeout(900)
-@pytest.mark.parametrize("page_cap", [None, 256], ids=["c4-budget", "c4-overflow"])
-def test_c4_fixed_point_100_steps_bit_identical(spk_mod, page_cap, monkeypatch):
+@pytest.mark.parametrize("page_cap,fmt", [(None, 0), (256, 0), (None, 3)],
+                         ids=["c4-budget", "c4-overflow", "c4-procedural"])
+def test_c4_fixed_point_100_steps_bit_identical(spk_mod, page_cap, fmt, monkeypatch):
     spk = spk_mod
     key = _C4
     start_oracle_jobs([key])
-    cfg = _cfg(key[0])
+    cfg = dict(_cfg(key[0]), syn_format=fmt)
     if page_cap:
         monkeypatch.setenv("SPK_PAGE_CAP", str(page_cap))
-    _say(f"[raster] c4 n={cfg['n']} T={key[1]} page_cap={page_cap or 'budget'}")
+    _say(f"[raster] c4 n={cfg['n']} T={key[1]} page_cap={page_cap or 'budget'} format={fmt}")
     gpu = _run_gpu(spk, cfg, key[1])
     st = gpu["stats"]
     assert st["nnz"] == cfg["n"] * cfg["k_out"]
-    assert st["step_mode"] == spk.SPK_STEP_PERSISTENT and st["delivery"] == spk.SPK_DELIVERY_BINNED
-    assert st["tile_width"] == 8192 and st["tiles"] == 248 and st["bytes_per_synapse"] == 4.0
+    assert st["delivery"] == spk.SPK_DELIVERY_BINNED
+    assert st["tile_width"] == 8192 and st["tiles"] == 248
+    if fmt == 3:  # procedural: no synapse stored, steps as graphs
+        assert st["step_mode"] == spk.SPK_STEP_GRAPH and st["bytes_per_synapse"] == 0.0
+    else:
+        assert st["step_mode"] == spk.SPK_STEP_PERSISTENT and st["bytes_per_synapse"] == 4.0
     if page_cap:
         assert st["page_cap"] == page_cap
     else:
@@ -183,16 +190,20 @@ def test_c4_fixed_point_100_steps_bit_identical(spk_mod, page_cap, monkeypatch):
 
 
 @pytest.mark.timeout(900)
-@pytest.mark.parametrize("key", [_C3_10, _C3_50], ids=["c3-10hz", "c3-50hz"])
-def test_c3_sources_fixed_point_bit_identical(spk_mod, key):
+@pytest.mark.parametrize("key,fmt", [(_C3_10, 0), (_C3_50, 0), (_C3_10, 3)],
+                         ids=["c3-10hz", "c3-50hz", "c3-10hz-procedural"])
+def test_c3_sources_fixed_point_bit_identical(spk_mod, key, fmt):
     spk = spk_mod
     start_oracle_jobs([key])
-    cfg = _cfg(key[0])
-    _say(f"[raster] {key[0]} n={cfg['n']} T={key[1]}")
+    cfg = dict(_cfg(key[0]), syn_format=fmt)
+    _say(f"[raster] {key[0]} n={cfg['n']} T={key[1]} format={fmt}")
     gpu = _run_gpu(spk, cfg, key[1])
     st = gpu["stats"]
     assert st["nnz"] == cfg["n"] * cfg["k_out"]
-    assert st["step_mode"] == spk.SPK_STEP_PERSISTENT and st["delivery"] == spk.SPK_DELIVERY_DIRECT
+    if fmt == 3:
+        assert st["step_mode"] == spk.SPK_STEP_GRAPH and st["delivery"] == spk.SPK_DELIVERY_BINNED
+    else:
+        assert st["step_mode"] == spk.SPK_STEP_PERSISTENT and st["delivery"] == spk.SPK_DELIVERY_DIRECT
     assert st["tile_width"] == 4096
     # every spike of a step emits exactly fan-out events
     assert np.array_equal(gpu["events"], gpu["counts"].astype(np.uint64) * cfg["k_out"])
