@@ -262,10 +262,14 @@ __device__ uint32_t gather_direct(const StepArgs &a, typename Acc<FIXED>::T *acc
     const uint32_t lane = lane_id(), w = threadIdx.x / kWave, nw = blockDim.x / kWave;
     const uint32_t T1 = a.tl.T + 1;
     uint32_t mine = 0;
-    for (uint32_t p0 = w * kWave; p0 < P; p0 += nw * kWave) {
+    // spikes per wave and round: all waves share the spikes (few spikes with
+    // long runs: fewer per wave, so that every wave streams records)
+    uint32_t G = (P + nw - 1) / nw;
+    G = G < 1u ? 1u : (G > (uint32_t)kWave ? (uint32_t)kWave : G);
+    for (uint32_t p0 = w * G; p0 < P; p0 += nw * G) {
         uint32_t len = 0;
         uint64_t beg = 0;
-        if (p0 + lane < P) {
+        if (lane < G && p0 + lane < P) {
             uint32_t s = a.dbg_spikes ? a.dbg_spikes[p0 + lane] : spike_at<COH>(a, pre, slot, p0 + lane);
             // a caller's spike list (debug delivery) is checked here: an ID
             // out of range delivers nothing and raises a flag
