@@ -666,22 +666,86 @@ __global__ __launch_bounds__(kBlock) void k_fo_count(ConnArgs c, uint32_t *base,
         base[(uint64_t)blockIdx.x * T + k] = cnt[k] ? atomicAdd(&tile_total[k], cnt[k]) : 0u;
 }
 
-__global__ __launch_bounds__(kBlock) void k_fo_file(ConnArgs c, const uint32_t *base, const uint64_t *tile_start,
-                                                   uint16_t *entries)
+// Filing: the block's synapses are drawn again kFoStage at a time,
+// counting-sorted by target tile in LDS, and each tile's run is written
+// contiguously after what the block filed there before (its reservation).
+constexpr uint32_t kFoThreads = 1024;
+constexpr uint32_t kFoPer = 32;                          // synapses per thread and round
+constexpr uint32_t kFoStage = kFoPer * kFoThreads;       // synapses sorted at once
+
+__global__ __launch_bounds__(kFoThreads) void k_fo_file(ConnArgs c, const uint32_t *base, const uint64_t *tile_start,
+                                                       uint16_t *entries)
 {
-    __shared__ uint32_t cur[kMaxTiles];
-    const uint32_t T = c.tl.T, tid = threadIdx.x;
+    __shared__ uint16_t stage[kFoStage];   // (class << 14 | neuron in tile), sorted by tile
+    __shared__ uint16_t stile[kFoStage];   // the tile of each staged entry
+    __shared__ uint32_t cnt[kMaxTiles], off[kMaxTiles], cur[kMaxTiles];
+    __shared__ uint32_t ws[kFoThreads / kWave];
+    const uint32_t T = c.tl.T, tid = threadIdx.x, lane = lane_id(), w = tid / kWave;
     const uint32_t s0 = blockIdx.x * kFoSrc, s1 = s0 + kFoSrc < c.n ? s0 + kFoSrc : c.n;
-    for (uint32_t k = tid; k < T; k += kBlock) cur[k] = base[(uint64_t)blockIdx.x * T + k];
-    __syncthreads();
-    for (uint32_t s = s0; s < s1; s++) {
-        const uint64_t rt = mix64(c.keys.tgt ^ (uint64_t)s);
-        const uint32_t cls = s < c.n_exc ? 0u : 1u;
-        for (uint32_t q = tid; q < c.k_out; q += kBlock) {
-            const uint32_t tgt = hash_range(mix64(rt ^ (uint64_t)q), c.n), tile = tgt >> c.tl.logW;
-            const uint32_t pos = atomicAdd(&cur[tile], 1u);
-            entries[tile_start[tile] + pos] = (uint16_t)((cls << 14) | (tgt & (c.tl.W - 1)));
+    const uint64_t V = (uint64_t)(s1 - s0) * c.k_out;
+    for (uint32_t k = tid; k < T; k += kFoThreads) cur[k] = base[(uint64_t)blockIdx.x * T + k];
+    // this thread's next synapse: v = v0 + tid + kFoThreads * u, i.e. synapse j of source s0 + si
+    uint32_t si = tid / c.k_out, j = tid - si * c.k_out;
+    for (uint64_t v0 = 0; v0 < V; v0 += kFoStage) {
+        for (uint32_t k = tid; k < T; k += kFoThreads) cnt[k] = 0;
+        __syncthreads();
+        uint32_t ent[kFoPer];  // tile << 16 | entry, rank in the tile's run of this round in ...
+        uint32_t rnk[kFoPer];
+#pragma unroll
+        for (int u = 0; u < (int)kFoPer; u++) {
+            const uint64_t v = v0 + tid + (uint64_t)kFoThreads * u;
+            ent[u] = 0xffffffffu;
+            if (v < V) {
+                const uint32_t s = s0 + si;
+                const uint32_t tgt = hash_range(key_hash(c.keys.tgt, s, j), c.n), tile = tgt >> c.tl.logW;
+                const uint32_t cls = s < c.n_exc ? 0u : 1u;
+                ent[u] = (tile << 16) | (cls << 14) | (tgt & (c.tl.W - 1));
+                rnk[u] = atomicAdd(&cnt[tile], 1u);
+            }
+            j += kFoThreads;
+            while (j >= c.k_out) {
+                j -= c.k_out;
+                si++;
+            }
         }
+        __syncthreads();
+        // exclusive scan of the round's tile counts (T <= 2048: two per thread)
+        {
+            const uint32_t b = 2 * tid;
+            const uint32_t c0 = b < T ? cnt[b] : 0u, c1 = b + 1 < T ? cnt[b + 1] : 0u;
+            uint32_t inc = c0 + c1;
+            for (int o = 1; o < kWave; o <<= 1) {
+                const uint32_t y = __shfl_up(inc, o);
+                if (lane >= (uint32_t)o) inc += y;
+            }
+            if (lane == kWave - 1) ws[w] = inc;
+            __syncthreads();
+            uint32_t before = 0;
+            for (uint32_t k = 0; k < w; k++) before += ws[k];
+            const uint32_t ex = before + inc - (c0 + c1);
+            if (b < T) off[b] = ex;
+            if (b + 1 < T) off[b + 1] = ex + c0;
+        }
+        __syncthreads();
+        uint32_t staged = 0;
+#pragma unroll
+        for (int u = 0; u < (int)kFoPer; u++) {
+            if (ent[u] == 0xffffffffu) continue;
+            const uint32_t tile = ent[u] >> 16, q = off[tile] + rnk[u];
+            stage[q] = (uint16_t)(ent[u] & 0xffffu);
+            stile[q] = (uint16_t)tile;
+            staged++;
+        }
+        const uint32_t n_round = (uint32_t)(V - v0 < kFoStage ? V - v0 : kFoStage);
+        __syncthreads();
+        // consecutive staged entries of a tile go to consecutive positions
+        for (uint32_t q = tid; q < n_round; q += kFoThreads) {
+            const uint32_t tile = stile[q];
+            entries[tile_start[tile] + cur[tile] + (q - off[tile])] = stage[q];
+        }
+        __syncthreads();
+        for (uint32_t k = tid; k < T; k += kFoThreads) cur[k] += cnt[k];
+        (void)staged;
     }
 }
 
@@ -937,8 +1001,9 @@ hipError_t fo_count(const ConnArgs &c, uint32_t *base, uint32_t *tile_total, hip
 hipError_t fo_file(const ConnArgs &c, const uint32_t *base, const uint64_t *tile_start, uint16_t *entries,
                    hipStream_t s)
 {
-    if (c.kind != SPK_CONN_FIXED_OUT || c.tl.T > kMaxTiles || c.tl.W > (1u << 14)) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(k_fo_file, dim3(fo_blocks(c.n)), dim3(kBlock), 0, s, c, base, tile_start, entries);
+    if (c.kind != SPK_CONN_FIXED_OUT || c.tl.T > kMaxTiles || c.tl.W > (1u << 14) || c.k_out == 0)
+        return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_fo_file, dim3(fo_blocks(c.n)), dim3(kFoThreads), 0, s, c, base, tile_start, entries);
     return hipGetLastError();
 }
 
