@@ -251,7 +251,7 @@ __device__ void publish_tile(const RunArgs &ra, uint32_t tile, uint32_t e, const
 {
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    if (threadIdx.x == 0) st_ag(&ra.ctl->tilep[e & 1u][tile], e << kTileCntBits | *ns);
+    if (threadIdx.x == 0) st_ag(&ra.ctl->tilep[e & 1u][tile * kTileWordStride], e << kTileCntBits | *ns);
 }
 
 // Wait (one wave) until each of the n <= 64 words p[0..n) carries the stamp e
@@ -262,7 +262,7 @@ __device__ bool spin_all_stamp(const uint32_t *p, uint32_t n, uint32_t e, uint32
     const uint32_t lane = lane_id(), want = e & (0xffffffffu >> kTileCntBits);
     const uint64_t t0 = wall_clock64();
     for (uint32_t k = 0;; k++) {
-        *v = ld_ag(p + (lane < n ? lane : 0u));
+        *v = ld_ag(p + (lane < n ? lane : 0u) * kTileWordStride);
         if (__all(lane >= n || (*v >> kTileCntBits) == want)) return true;
         if ((k & 31u) == 31u) {
             if (ld_ag(abort_flag)) return false;
@@ -292,7 +292,7 @@ __device__ bool wait_tiles(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t e,
     if (w * kWave < T) {
         const uint32_t n = T - w * kWave < kWave ? T - w * kWave : kWave, lane = lane_id();
         uint32_t v;
-        const bool ok = spin_all_stamp(&c->tilep[e & 1u][w * kWave], n, e, &c->abort_flag, &v);
+        const bool ok = spin_all_stamp(&c->tilep[e & 1u][w * kWave * kTileWordStride], n, e, &c->abort_flag, &v);
         if (counts && ok && lane < n) L.u.p.pre[w * kWave + lane] = v & ((1u << kTileCntBits) - 1u);
         if (lane == 0) {
             L.pstop[w] = ok ? 0u : 1u;
@@ -316,7 +316,7 @@ __device__ bool look_tiles(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t e,
     const bool poller = w * kWave < T;
     const uint32_t n = poller ? (T - w * kWave < kWave ? T - w * kWave : kWave) : 0u;
     uint32_t v = 0;
-    if (poller) v = ld_ag(&ra.ctl->tilep[e & 1u][w * kWave + (lane < n ? lane : 0u)]);
+    if (poller) v = ld_ag(&ra.ctl->tilep[e & 1u][(w * kWave + (lane < n ? lane : 0u)) * kTileWordStride]);
     work();
     if (poller) {
         const uint32_t want = e & (0xffffffffu >> kTileCntBits);
