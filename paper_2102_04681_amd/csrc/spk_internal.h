@@ -236,7 +236,11 @@ struct RunCtl {
     uint32_t tilep[2][kGroups * kRunMaxR * kTileWordStride];
     uint32_t start, pad0[kCtlStride - 1];   // placement barrier
     uint32_t gcnt, pad1[kCtlStride - 1];    // grid barrier: XCDs complete
-    uint32_t gen, pad2[kCtlStride - 1];     // grid barrier: released epoch
+    // grid barrier: the released epoch, one copy per XCD (kTileWordStride
+    // words apart), each polled by the XCD's workgroups only (measured: 17.08
+    // -> 16.96 us per step on the 250,000-neuron network, 79.6 -> 79.3 on the
+    // 1e6-source one)
+    uint32_t gen[kGroups * kTileWordStride];
     uint32_t abort_flag, pad3[kCtlStride - 1];
 };
 struct RunArgs {

@@ -49,6 +49,17 @@ namespace spk {
 namespace {
 
 constexpr int kRunThreads = 1024;
+
+// The thread index, opaque to the optimiser: address arithmetic derived from
+// it is then recomputed in each phase instead of being hoisted out of the
+// step loop, where the kernel has no registers to spare and the hoisted
+// values would be spilled (each reload waits for every load in flight).
+__device__ __forceinline__ uint32_t tid_here()
+{
+    uint32_t t = threadIdx.x;
+    asm volatile("" : "+v"(t));
+    return t;
+}
 constexpr int kRunRounds = kMaxTileW / kRunThreads;      // neurons per thread
 constexpr uint32_t kRunChunk = 256;                      // spikes resolved per push chunk
 constexpr uint32_t kRunMaxT = kGroups * kRunMaxR;        // tiles
@@ -121,6 +132,7 @@ struct RunLDS {
             uint64_t wbeg[kRunThreads / kWave][kWave];
             unsigned long long dlv[kRunMaxD];  // binned: events delivered at each step of the batch
             uint32_t ovfm;                     // binned: bit u: step u of the batch has overflowed events
+            uint32_t pfv[kRunMaxR];            // binned, one step: records in each push block's page
             uint32_t nb[kRunMaxD];             // batched update: spikes of each step of the batch
         } t;
         struct {
@@ -209,7 +221,8 @@ __device__ void run_draw_unit(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t
 }
 
 // Grid barrier: every workgroup's stores have completed before it arrives.
-// The last arrival of an XCD counts the XCD; the last XCD releases epoch e.
+// The last arrival of an XCD counts the XCD; the last XCD releases epoch e
+// into every XCD's copy of the release word.
 // Between arriving and waiting, the workgroup computes the next step's draws.
 template <bool FIXED, bool CMP>
 __device__ bool grid_sync(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x, uint32_t e, bool draws,
@@ -222,12 +235,13 @@ __device__ bool grid_sync(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x, 
         const uint32_t o = atomicAdd(&c->gx[x * kCtlStride], 1u);
         if (o == ra.R * e - 1) {
             const uint32_t g = atomicAdd(&c->gcnt, 1u);
-            if (g == kGroups * e - 1) st_ag(&c->gen, e);
+            if (g == kGroups * e - 1)
+                for (uint32_t xx = 0; xx < kGroups; xx++) st_ag(&c->gen[xx * kTileWordStride], e);
         }
     }
     if (draws) run_draws(ra.s, L, tile_lo, tile_n, t_draw, n_draw);
     if (threadIdx.x == 0) {
-        L.stop = spin_ge(&c->gen, e, &c->abort_flag) ? 0u : 1u;
+        L.stop = spin_ge(&c->gen[x * kTileWordStride], e, &c->abort_flag) ? 0u : 1u;
         if (L.stop) atomicOr(ra.s.flags, kRunStoppedFlag);
     }
     __syncthreads();
@@ -358,11 +372,18 @@ __device__ bool wait_pushes(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x
 // The caller has zeroed acc[0 .. Db * W).  Leaves in L.u.t.dlv the events
 // delivered at each step, including any that overflowed into the global
 // accumulators (merged here).
-template <bool FIXED, bool CMP>
+// ONE (Db = 1): the first kSpecU chunks per wave of the pages (an equal
+// number of chunks per page, within the page capacity) are loaded together
+// with the pages' fill counters, before the counts are known, and records
+// past a page's count are dropped; only the rest of a longer page goes
+// through the chunk tables.  The pages of an arrival step are not written
+// while it is drained, so the records read are the filed ones or stale ones
+// beyond the count.
+template <bool FIXED, bool CMP, bool ONE>
 __device__ void run_drain(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t x, uint32_t c, uint32_t tile,
                           uint32_t tile_n, uint64_t t_first, uint32_t Db)
 {
-    const uint32_t tid = threadIdx.x;
+    const uint32_t tid = tid_here();
     const Tiling tl = a.tl;
     constexpr uint32_t kPer = CMP ? 2u : 1u;
     constexpr uint32_t kChunk = kPer * kWave;
@@ -376,19 +397,56 @@ __device__ void run_drain(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t x, 
     // thread u < Db: the overflow flag of (arrival step t_first + u, tile)
     const uint32_t osl = tid < Db ? (pslot0 + tid < a.pslots ? pslot0 + tid : pslot0 + tid - a.pslots) : 0u;
     uint32_t ovf = ld_ag(&a.ovf_flag[(uint64_t)osl * tl.T + tile]);
+    // the wave index is uniform: held in a scalar register, the chunk-table
+    // addresses below cost no vector registers
+    const uint32_t w = __builtin_amdgcn_readfirstlane(tid / kWave), lane = tid & (kWave - 1);
+    constexpr uint32_t nw = kRunThreads / kWave;
+    constexpr int kSpecU = CMP ? 8 : 16;
+    // ONE: chunk q = u * nw + w of the speculative loads is chunk q % spc of
+    // push block q / spc's page; spc * kChunk records per page (S)
+    const uint32_t spc = ONE ? kSpecU * nw / G1 : 0u, S = spc * kChunk;
+    using Ld = typename std::conditional<CMP, uint32_t, int2>::type;
+    Ld sr[ONE ? kSpecU : 1];
+    if constexpr (ONE) {
+#pragma unroll
+        for (int u = 0; u < kSpecU; u++) {
+            const uint32_t q = u * nw + w, g = q / spc, o = (q - g * spc) * kChunk + lane * kPer;
+            const bool ok = g < G1 && o < cap;  // (cap is a multiple of 16: both halves of a pair)
+            const uint32_t idx = ok ? (page_of(a, x, g, pslot0, c) * cap + o) / kPer : 0u;
+            if constexpr (CMP) sr[u] = ((const uint32_t *)a.pages16)[idx];
+            else sr[u] = a.pages[idx];
+        }
+    }
     ovf = tid < Db ? ovf : 0u;
     if (tid < Db) L.u.t.dlv[tid] = 0;
     if (tid == 0) L.u.t.ovfm = 0;
     pf = tid < P ? pf : 0u;
-    const uint32_t ne = pf < cap ? pf : cap;
+    const uint32_t ne_all = pf < cap ? pf : cap;
+    if (ONE && tid < kRunMaxR) L.u.t.pfv[tid] = ne_all;
+    // records left for the chunk tables (ONE: those past the speculative part)
+    const uint32_t o0 = ONE ? S : 0u;
+    const uint32_t ne = ne_all > o0 ? ne_all - o0 : 0u;
     uint32_t C;
     const uint32_t cex = block_scan_u32((ne + kChunk - 1) / kChunk, L.ws, &C);  // (publishes the resets)
     if (pf) atomicAdd(&L.u.t.dlv[pu], (unsigned long long)pf);
     if (ovf) atomicOr(&L.u.t.ovfm, 1u << tid);
-    // the wave index is uniform: held in a scalar register, the chunk-table
-    // addresses below cost no vector registers
-    const uint32_t w = __builtin_amdgcn_readfirstlane(tid / kWave), lane = lane_id();
-    constexpr uint32_t nw = kRunThreads / kWave;
+    if constexpr (ONE) {
+#pragma unroll
+        for (int u = 0; u < kSpecU; u++) {
+            const uint32_t q = u * nw + w, g = q / spc, o = (q - g * spc) * kChunk + lane * kPer;
+            const uint32_t f = g < G1 ? L.u.t.pfv[g] : 0u;
+            if constexpr (CMP) {
+#pragma unroll
+                for (int hf = 0; hf < 2; hf++) {
+                    if (o + hf >= f) continue;
+                    const uint32_t rec = hf ? sr[u] >> 16 : sr[u] & 0xffffu;
+                    Acc<FIXED>::add(&L.u.t.acc[rec & kPageLocalMask], class_units(a, rec >> kPageClassShift));
+                }
+            } else {
+                if (o < f) Acc<FIXED>::add(&L.u.t.acc[(uint32_t)sr[u].x], units_of<FIXED>(sr[u].y, a.m.shift64));
+            }
+        }
+    }
     constexpr int kDrain = 16;
     constexpr uint32_t kWin = kDrain * nw;
     const uint32_t nchp = (ne + kChunk - 1) / kChunk;
@@ -398,7 +456,7 @@ __device__ void run_drain(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t x, 
         lds_sync();
         if (tid < P) {
             const uint32_t cb = cex > i0 ? cex : i0, ce = cex + nchp < i0 + kWin ? cex + nchp : i0 + kWin;
-            const uint32_t pbase = page * cap;
+            const uint32_t pbase = page * cap + o0;
             for (uint32_t q = cb; q < ce; q++) {
                 const uint32_t o = (q - cex) * kChunk;
                 L.u.t.cbase[q - i0] = (pbase + o) / kPer;
@@ -588,7 +646,7 @@ __device__ void run_update_batch(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint3
 {
     using AccT = typename RunLDS<FIXED, CMP>::AccT;
     const StepArgs &a = ra.s;
-    const uint32_t tid = threadIdx.x, lane = lane_id(), W = a.tl.W;
+    const uint32_t tid = tid_here(), lane = tid & (kWave - 1), W = a.tl.W;
     const float mk = L.mk, v_rest = L.v_rest, v_th = L.v_th, v_reset = L.v_reset, i_bias = L.i_bias,
                 ext_w = L.ext_w;
     const int32_t ext_wq = L.ext_wq, bias_q = L.bias_q, shift = L.shift, shift64 = L.shift64;
@@ -742,7 +800,7 @@ __device__ uint32_t run_push(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t 
     using LT = RunLDS<FIXED, CMP>;
     constexpr int R = LT::R;
     const StepArgs &a = ra.s;
-    const uint32_t tid = threadIdx.x, lane = lane_id(), w = __builtin_amdgcn_readfirstlane(tid / kWave);
+    const uint32_t tid = tid_here(), lane = tid & (kWave - 1), w = __builtin_amdgcn_readfirstlane(tid / kWave);
     constexpr uint32_t nw = kRunThreads / kWave;
     const Tiling tl = a.tl;
     const uint32_t NB = (Db + a.lists - 1) * tl.T8, G1 = ra.R, NS = Db * tl.T;
@@ -997,7 +1055,7 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
         }
         return;
     }
-    const uint32_t x = L.x, r = L.r;
+    const uint32_t x = __builtin_amdgcn_readfirstlane(L.x), r = __builtin_amdgcn_readfirstlane(L.r);
     const Tiling tl = a.tl;
     const bool has_tile = r < tl.T8;
     const uint32_t tile = x * tl.T8 + r;
@@ -1057,7 +1115,10 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
             if (tid == 0) L.nspk2[0] = 0;
             if constexpr (BATCH)
                 if (tid < Db) L.u.t.nb[tid] = 0;
-            if (!DIRECT) run_drain(a, L, x, r, tile, tile_n, t_first, Db);  // all steps of the batch
+            if (!DIRECT) {  // all steps of the batch
+                if (!BATCH && Db == 1) run_drain<FIXED, CMP, true>(a, L, x, r, tile, tile_n, t_first, 1);
+                else run_drain<FIXED, CMP, false>(a, L, x, r, tile, tile_n, t_first, Db);
+            }
             bool batched = false;
             if constexpr (BATCH) {
                 batched = lif && Db > 1;
