@@ -230,34 +230,51 @@ spk_status spk_create_from_csr(const spk_params *params, uint32_t n, const uint6
  * Errors: SPK_EOVERFLOW if steps would exceed max_steps. */
 spk_status spk_step(spk_net *net, uint64_t n_steps);
 
-/* Wait for all enqueued work; reports device-side overflow flags, and
- * SPK_EHIP if a persistent launch stopped early (a barrier wait exceeded its
- * 10 s bound): the state is then undefined. */
+/* Wait for all enqueued work (the host waits once per call instead of
+ * downloading spike counts every step as the paper's loop does, Sec. III-E,
+ * IV-D).  Reports device-side flags: SPK_EOVERFLOW (raster capacity or
+ * fixed-point range exceeded), SPK_EINVAL once after spk_deliver_noalloc
+ * was given a spike ID >= n, and SPK_EHIP if a persistent launch stopped
+ * early (a barrier wait exceeded its 10 s bound): the state is then
+ * undefined. */
 spk_status spk_sync(spk_net *net);
 
-/* Per-step records for steps [t0, t0+n) (host output buffers of n entries):
- * spike counts |S(t)|, synaptic events emitted at t (sum of the out-degrees
- * of the neurons that spiked at t), synaptic events delivered at t (synapses
- * whose spike arrived at t). */
+/* Per-step records for steps [t0, t0+n) (host output buffers of n entries,
+ * written by the call; the call waits for enqueued work first): spike
+ * counts |S(t)| (the spike arrays of Sec. III-A), synaptic events emitted
+ * at t (sum of the out-degrees of the neurons that spiked at t: one event
+ * per (spike, outgoing synapse), the unit of Sec. IV-A's throughput) and
+ * synaptic events delivered at t (synapses whose spike arrived at t, the
+ * delay of Sec. III-A, V applied); steps not run yet read as 0.  Errors:
+ * SPK_EINVAL if t0 + n exceeds max_steps, or a null buffer with n > 0;
+ * device flags as spk_sync. */
 spk_status spk_read_spike_counts(spk_net *net, uint64_t t0, uint64_t n, uint32_t *out);
 spk_status spk_read_events(spk_net *net, uint64_t t0, uint64_t n, uint64_t *out);
 spk_status spk_read_delivered(spk_net *net, uint64_t t0, uint64_t n, uint64_t *out);
 
-/* Spike raster of steps [t0, t0+n): offs (n+1 entries, offs[0] = 0) and ids
- * (cap entries); IDs of each step ascending.  SPK_EOVERFLOW if the raster
- * capacity was exceeded during the run or cap is too small. */
+/* Spike raster of steps [t0, t0+n) (the IDs each step's spike array holds,
+ * Sec. III-A): host buffers offs (n+1 entries, offs[0] = 0) and ids (cap
+ * entries); IDs of each step ascending.  Requires raster_capacity > 0 at
+ * creation.  Errors: SPK_EOVERFLOW if the raster capacity was exceeded
+ * during the run or cap is too small, SPK_EINVAL if t0 + n exceeds the
+ * steps run or offs is NULL, SPK_ESTATE if recording is off. */
 spk_status spk_read_raster(spk_net *net, uint64_t t0, uint64_t n, uint64_t *offs,
                            uint32_t *ids, uint64_t cap);
 
-/* Membrane potentials and refractory counters (host buffers of n entries;
- * either may be NULL). */
+/* The neuron pool's state after the steps run so far (Sec. III-A: the
+ * per-neuron struct-of-arrays the update reads and writes): membrane
+ * potentials (fp32) and refractory counters (steps left) into host buffers
+ * of n entries; either may be NULL.  Waits for enqueued work first. */
 spk_status spk_read_state(spk_net *net, float *v, uint8_t *ref);
 
-/* Deliver the listed spikes (IDs < n) through the synapses of delay `delay`
- * (0 = every delay) with the same kernel the simulation uses, into a
- * scratch input buffer that is copied to out_f32 (fp32 mode) or out_i32
- * (fixed mode, units of 2^-fixed_shift); n entries.  Network state is not
- * changed. */
+/* Spike transmission alone (Sec. III-C): deliver the listed spikes (host
+ * array of n_spikes IDs < n) through the synapses of delay `delay` (0 =
+ * every delay) with the same kernels the simulation uses, into a scratch
+ * input buffer (allocated and freed by the call) that is copied to the host
+ * buffer out_f32 (fp32 mode) or out_i32 (fixed mode, units of
+ * 2^-fixed_shift); n entries; the other output may be NULL.  Network state
+ * is not changed.  Errors: SPK_EINVAL (ID >= n, bad delay, missing output),
+ * SPK_ENOMEM, SPK_EHIP. */
 spk_status spk_debug_deliver(spk_net *net, const uint32_t *spikes, uint64_t n_spikes,
                              uint32_t delay, float *out_f32, int32_t *out_i32);
 
@@ -284,17 +301,23 @@ spk_status spk_debug_deliver(spk_net *net, const uint32_t *spikes, uint64_t n_sp
 spk_status spk_deliver_noalloc(spk_net *net, const uint32_t *d_spikes, uint64_t n_spikes, uint32_t delay,
                                void *d_out);
 
-/* Export the rows (all synapses of the given source neurons), each row in
- * canonical order (target, delay, weight bits).  offs: n_rows+1 entries;
- * col/delay and w (fp32 mode) or wq (fixed mode) of cap entries; unused
- * outputs may be NULL.  SPK_EOVERFLOW if cap is too small. */
+/* Export the adjacency-list rows (Sec. III-A, Fig. 'adj': all synapses of
+ * the given source neurons; procedural networks generate them, Sec. V), each
+ * row in canonical order (target, delay, weight bits).  Host buffers:
+ * offs: n_rows+1 entries; col/delay and w (fp32 mode) or wq (fixed mode) of
+ * cap entries; unused outputs may be NULL.  Errors: SPK_EOVERFLOW if cap is
+ * too small, SPK_EINVAL for a row >= n. */
 spk_status spk_export_rows(spk_net *net, const uint32_t *rows, uint64_t n_rows, uint64_t *offs,
                            uint32_t *col, float *w, int32_t *wq, uint8_t *delay, uint64_t cap);
 
-/* The Poisson threshold table of the drive: thr[k] = floor(CDF(k) * 2^32),
- * last entry 2^32; *len entries (0 without drive).  cap entries of thr. */
+/* The Poisson threshold table of the external drive (the benchmark models'
+ * Poisson input, Sec. IV): thr[k] = floor(CDF(k) * 2^32), last entry 2^32;
+ * *len entries (0 without drive) into the host buffer thr of cap entries.
+ * Errors: SPK_EOVERFLOW if cap is too small. */
 spk_status spk_poisson_table(spk_net *net, uint64_t *thr, uint32_t cap, uint32_t *len);
 
+/* The network's derived configuration and setup timings (spk_stats_t
+ * above; setup_ms is the creation time of Sec. IV-C) into *out. */
 spk_status spk_stats(spk_net *net, spk_stats_t *out);
 
 /* Kernel timing.  With profiling on, spk_step records HIP events on the
