@@ -18,9 +18,13 @@
 // event); the memory of the synapses (4 or 8 bytes each) is not needed.
 //
 // Generation is wave-local: lanes walk consecutive synapses of the wave's
-// slice of the rows, keep those of the block's group, and compact them with
-// a ballot into a ring of the wave in LDS; every window takes kProcR events
-// per lane from the rings and sorts them by (arrival slot, tile) as the
+// slice of the rows, draw each one's target, keep those of the block's
+// group, and compact them with a ballot into a ring of the wave in LDS as
+// (target, spike, synapse index); the delay (and a per-synapse weight) is
+// drawn when an entry is taken from the ring, where every lane holds a kept
+// synapse (drawn before compaction, one kept lane in eight would make the
+// whole wave run those mixer rounds).  Every window takes kProcR events per
+// lane from the rings and sorts them by (arrival slot, tile) as the
 // stored-row push does.
 #include <hip/hip_runtime.h>
 
@@ -37,13 +41,15 @@ constexpr uint32_t kProcChunk = 1024;                      // spikes generated p
 constexpr uint32_t kProcWaves = kProcThreads / kWave;
 constexpr uint32_t kRing = 128;                            // events a wave holds between windows
 constexpr uint32_t kNoSpike = 0xffffffffu;
+static_assert(kProcChunk <= (1u << 16), "ring entries hold the spike of the chunk in 16 bits");
 
 template <bool CMP>
 struct ProcLDS {
     using Rec = typename SynRec<CMP>::T;
     Rec stage[kProcWin];             // bucket-sorted events {bucket << 16 | local, weight}; compact:
                                      // u32 bucket << 16 | class << 13 | local
-    Rec ring[kProcWaves][kRing];     // generated events of each wave, not yet taken
+    uint2 ring[kProcWaves][kRing];   // kept synapses of each wave, not yet taken: {target,
+                                     // spike of the chunk << 16 | synapse index}
     uint32_t sid[kProcChunk];        // the chunk's spikes (kNoSpike: an ID out of range)
     uint32_t pre[kMaxTiles + 1];     // prefix of the source tiles' spike counts
     uint32_t bcnt[kMaxBuckets];      // events per bucket in this window, then rank cursor
@@ -137,7 +143,7 @@ __global__ __launch_bounds__(kProcThreads) void k_push_proc(StepArgs a, uint32_t
                 while (cnt < kWave && vcur < ve) {
                     const bool live = vcur + lane < ve;
                     bool keep = false;
-                    Rec r{};
+                    uint32_t tgt = 0;
                     if (live) {
                         const uint32_t s = L.sid[si];
                         if (s != kNoSpike) {
@@ -145,19 +151,15 @@ __global__ __launch_bounds__(kProcThreads) void k_push_proc(StepArgs a, uint32_t
                                 scur = s;
                                 pt = mix64(a.m.keys.tgt ^ (uint64_t)s);
                             }
-                            const uint32_t tgt = hash_range(mix64(pt ^ (uint64_t)j), a.n);
-                            if (tgt - xlo < tl.Gw) {  // (unsigned) the target is in group x
-                                const uint32_t jd = a.lists > 1 ? hash_range(key_hash(a.m.keys.delay, s, j), a.lists) : 0u;
-                                keep = !(dbg && a.dbg_j >= 0 && (int32_t)jd != a.dbg_j);
-                                if (keep) r = proc_record<CMP>(a, s, j, tgt, jd);
-                            }
+                            tgt = hash_range(mix64(pt ^ (uint64_t)j), a.n);
+                            keep = tgt - xlo < tl.Gw;  // (unsigned) the target is in group x
                         }
                     }
                     const uint64_t bal = __ballot(keep);
                     if (keep) {
                         const uint32_t rank =
                             __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
-                        L.ring[w][(head + cnt + rank) & (kRing - 1)] = r;
+                        L.ring[w][(head + cnt + rank) & (kRing - 1)] = make_uint2(tgt, si << 16 | j);
                     }
                     cnt += (uint32_t)__popcll(bal);
                     vcur += kWave;
@@ -169,8 +171,15 @@ __global__ __launch_bounds__(kProcThreads) void k_push_proc(StepArgs a, uint32_t
                 }
                 lds_wave_sync();  // the ring's new entries are visible to every lane
                 const uint32_t avail = cnt < kWave ? cnt : kWave;
-                const bool ok = lane < avail;
-                rec[u] = L.ring[w][(head + lane) & (kRing - 1)];  // (read unconditionally; used if ok)
+                bool ok = lane < avail;
+                const uint2 ge = L.ring[w][(head + lane) & (kRing - 1)];  // (read unconditionally; used if ok)
+                rec[u] = Rec{};
+                if (ok) {  // the kept synapse's delay (and weight) draws
+                    const uint32_t s = L.sid[ge.y >> 16], j2 = ge.y & 0xffffu;
+                    const uint32_t jd = a.lists > 1 ? hash_range(key_hash(a.m.keys.delay, s, j2), a.lists) : 0u;
+                    ok = !(dbg && a.dbg_j >= 0 && (int32_t)jd != a.dbg_j);
+                    rec[u] = proc_record<CMP>(a, s, j2, ge.x, jd);
+                }
                 okm |= (uint32_t)ok << u;
                 head += avail;
                 cnt -= avail;
