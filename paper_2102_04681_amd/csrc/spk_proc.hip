@@ -35,8 +35,6 @@ namespace spk {
 namespace {
 
 constexpr int kProcThreads = 1024;
-constexpr int kProcR = 8;                                  // events per lane per window
-constexpr uint32_t kProcWin = kProcR * kProcThreads;       // events sorted at once
 constexpr uint32_t kProcChunk = 1024;                      // spikes generated per chunk
 constexpr uint32_t kProcWaves = kProcThreads / kWave;
 constexpr uint32_t kRing = 128;                            // events a wave holds between windows
@@ -46,7 +44,9 @@ static_assert(kProcChunk <= (1u << 16), "ring entries hold the spike of the chun
 template <bool CMP>
 struct ProcLDS {
     using Rec = typename SynRec<CMP>::T;
-    Rec stage[kProcWin];             // bucket-sorted events {bucket << 16 | local, weight}; compact:
+    static constexpr int R = CMP ? 12 : 8;                    // events per lane per window
+    static constexpr uint32_t kWin = R * kProcThreads;        // events sorted at once
+    Rec stage[kWin];                 // bucket-sorted events {bucket << 16 | local, weight}; compact:
                                      // u32 bucket << 16 | class << 13 | local
     uint2 ring[kProcWaves][kRing];   // kept synapses of each wave, not yet taken: {target,
                                      // spike of the chunk << 16 | synapse index}
@@ -91,6 +91,7 @@ __global__ __launch_bounds__(kProcThreads) void k_push_proc(StepArgs a, uint32_t
 {
     using Rec = typename SynRec<CMP>::T;
     __shared__ ProcLDS<CMP> L;
+    constexpr int kProcR = ProcLDS<CMP>::R;
     const uint64_t t = step_index(a, i, t_explicit);
     const uint32_t x = blockIdx.x % kGroups, g1 = blockIdx.x / kGroups, G1 = a.pg1;
     const uint32_t tid = threadIdx.x, lane = lane_id();
@@ -132,8 +133,8 @@ __global__ __launch_bounds__(kProcThreads) void k_push_proc(StepArgs a, uint32_t
         const uint32_t ve = (uint32_t)((uint64_t)V * (w + 1) / kProcWaves);
         uint32_t vcur = vb;                      // (wave-uniform)
         uint32_t si = (vb + lane) / kout, j = (vb + lane) - si * kout;
-        uint32_t scur = kNoSpike;                // the spike whose target-stream prefix pt is held
-        uint64_t pt = 0;
+        uint32_t sicur = kNoSpike, scur = kNoSpike;  // the lane's spike (index, ID) whose
+        uint64_t pt = 0;                              // target-stream prefix pt is held
         uint32_t head = 0, cnt = 0;              // the wave's ring (wave-uniform)
         for (;;) {
             Rec rec[kProcR];
@@ -145,12 +146,12 @@ __global__ __launch_bounds__(kProcThreads) void k_push_proc(StepArgs a, uint32_t
                     bool keep = false;
                     uint32_t tgt = 0;
                     if (live) {
-                        const uint32_t s = L.sid[si];
-                        if (s != kNoSpike) {
-                            if (s != scur) {
-                                scur = s;
-                                pt = mix64(a.m.keys.tgt ^ (uint64_t)s);
-                            }
+                        if (si != sicur) {  // (once per kout synapses)
+                            sicur = si;
+                            scur = L.sid[si];
+                            pt = mix64(a.m.keys.tgt ^ (uint64_t)scur);
+                        }
+                        if (scur != kNoSpike) {
                             tgt = hash_range(mix64(pt ^ (uint64_t)j), a.n);
                             keep = tgt - xlo < tl.Gw;  // (unsigned) the target is in group x
                         }
