@@ -371,6 +371,48 @@ def test_fixed_point_simulation_bit_identical(spk, name, mk, T, delivery, mode, 
             assert km["tile_ms"] > 0 and km["run_launches"] == 0
 
 
+# degenerate shapes: a single neuron with its autapse, two neurons fully
+# connected, a network with no synapse at all (nnz = 0), one partial tile
+# (n = 37 < the smallest tile), every pair connected, in-degree 1, and 64
+# delay lists (pages for 64 arrival slots)
+DEGENERATE = [
+    ("one-neuron", lambda: I.config(0, n=1, p=1.0, driven=True, v0_lo=-50.5, v0_hi=-50.1), 300),
+    ("two-neurons", lambda: I.config(0, n=2, p=1.0, driven=True, v0_lo=-50.5, v0_hi=-50.1), 300),
+    ("no-synapses", lambda: I.config(0, n=500, p=0.0, driven=True), 100),
+    ("partial-tile", lambda: I.scaled(4, 37, k_out=5), 100),
+    ("all-pairs", lambda: I.config(0, n=200, p=1.0, driven=True, w_exc=0.05, w_inh=-0.2), 100),
+    ("in-degree-1", lambda: I.scaled(2, 300, k_in_exc=1, k_in_inh=0), 100),
+    ("64-delays", lambda: I.scaled(4, 3000, k_out=300, delay_min=1, delay_max=64), 100),
+]
+
+
+@pytest.mark.parametrize("name,mk,T", DEGENERATE, ids=[c[0] for c in DEGENERATE])
+@pytest.mark.parametrize("delivery", [1, 2], ids=["direct", "binned"])
+@pytest.mark.parametrize("step_mode", [1, 2], ids=["graph", "persist"])
+def test_degenerate_networks_bit_identical(spk, name, mk, T, delivery, step_mode):
+    cfg = mk()
+    cfg["acc_mode"] = I.ACC_FIXED
+    cfg["delivery"] = delivery
+    cfg["step_mode"] = step_mode
+    if step_mode == 2 and not _persistent_applies(cfg, delivery):
+        pytest.skip("the persistent kernel takes direct delivery with one delay only")
+    _say(f"[degenerate] {name} n={cfg['n']} T={T} delivery={delivery} step_mode={step_mode}")
+    g = spk.Net(cfg, max_steps=T, raster_capacity=max(1, cfg["n"] * T))
+    assert g.stats()["step_mode"] == step_mode
+    g.step(T)
+    offs, ids = g.raster()
+    r, ov, orf, (rp, col, w, d) = _oracle_run(cfg, T)
+    assert int(g.stats()["nnz"]) == int(rp[-1])
+    assert r["counts"].sum() > 0
+    assert np.array_equal(g.spike_counts(), r["counts"]), "spike counts differ"
+    assert np.array_equal(offs, r["offs"]) and np.array_equal(ids, r["raster"]), "rasters differ"
+    assert np.array_equal(g.events(), r["events"]), "event counts differ"
+    assert np.array_equal(g.delivered(), r["delivered"]), "delivered-event counts differ"
+    gv, gr = g.state()
+    assert np.array_equal(gv.view(np.uint32), ov.view(np.uint32)), "membrane potentials differ"
+    assert np.array_equal(gr, orf)
+
+
 @pytest.mark.parametrize("acc", [I.ACC_F32, I.ACC_FIXED], ids=["f32", "fixed"])
 @pytest.mark.parametrize("fmt", [f for f, _ in FORMATS], ids=[n for _, n in FORMATS])
 @pytest.mark.parametrize("step_mode", [1, 2], ids=["graph", "persist"])

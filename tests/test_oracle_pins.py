@@ -641,3 +641,24 @@ def test_fig_adj_pivot_split():
     piv = fx["pivot"][0]
     split = [int(np.searchsorted(net.row(s)[0], piv + 1)) for s in range(fx["n"])]
     assert split == fx["expect_split"]
+
+
+def test_degenerate_networks_invariants():
+    # a network with no synapse delivers nothing although its neurons fire;
+    # a single neuron with its autapse (p = 1) emits one event per spike,
+    # delivered one step later; every pair connected (p = 1, n = 40): each
+    # spike emits n events
+    r = oracle.Net(I.config(0, n=500, p=0.0, driven=True)).run(100)
+    assert r["counts"].sum() > 0 and r["events"].sum() == 0 and r["delivered"].sum() == 0
+    one = oracle.Net(I.config(0, n=1, p=1.0, driven=True, v0_lo=-50.5, v0_hi=-50.1))
+    rp, col, _, _ = one.csr()
+    assert rp.tolist() == [0, 1] and col.tolist() == [0]
+    r = one.run(300)
+    assert r["counts"].sum() > 0
+    assert np.array_equal(r["events"], r["counts"].astype(np.uint64))
+    assert np.array_equal(r["delivered"][1:], r["events"][:-1])
+    full = oracle.Net(I.config(0, n=40, p=1.0, driven=True, w_exc=0.05, w_inh=-0.2))
+    rp, col, _, _ = full.csr()
+    assert np.all(np.diff(rp) == 40)
+    r = full.run(200)
+    assert r["counts"].sum() > 0 and np.array_equal(r["events"], r["counts"].astype(np.uint64) * 40)
