@@ -50,6 +50,8 @@ CASES = [
     ("binned-f32-compact", lambda: I.scaled(4, 8000, k_out=700), [0, 7]),
     ("binned-fixed-compact", lambda: I.scaled(4, 8000, k_out=700, acc_mode=I.ACC_FIXED), [0, 1]),
     ("binned-f32-full", lambda: I.scaled(4, 6000, k_out=400, syn_format=1), [0, 20]),
+    ("binned-procedural", lambda: I.scaled(4, 8000, k_out=700, syn_format=3), [0, 7]),
+    ("binned-fixed-procedural", lambda: I.scaled(4, 8000, k_out=700, syn_format=3, acc_mode=I.ACC_FIXED), [0, 3]),
     ("binned-delay15", lambda: I.scaled(2, 5000, k_in_exc=400, k_in_inh=100), [0]),
     ("direct-f32", lambda: I.scaled(1, 4000), [0]),
     ("direct-fixed-sources", lambda: I.scaled(3, 8000, k_out=1000, acc_mode=I.ACC_FIXED), [0]),
