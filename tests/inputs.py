@@ -126,6 +126,37 @@ def scaled(index: int, n: int, driven: bool = True, **over) -> dict:
     return c
 
 
+def random_shape(seed: int) -> dict:
+    """A seeded random network shape for broad parity sweeps: n in [40, 6000),
+    Bernoulli, fixed out-degree or fixed in-degree connectivity, smallest
+    delay 1-5 with 1 to 26 delay lists, weights scaled by 80 / (expected
+    in-degree) as in C1 (at most 1x), and the driven variant's Poisson drive."""
+    rng = np.random.default_rng(1000 + seed)
+    n = int(rng.integers(40, 6000))
+    kind = int(rng.choice([BERNOULLI, FIXED_OUT, FIXED_IN]))
+    dmin = int(rng.integers(1, 6))
+    dmax = dmin + int(rng.choice([0, 0, 3, 12, 25]))
+    c = dict(_MEMBRANE, seed=int(seed), n=n, conn_kind=kind, delay_min=dmin, delay_max=dmax, steps=200)
+    if kind == BERNOULLI:
+        c["p"] = float(rng.uniform(0.002, 0.15))
+        deg = c["p"] * n
+    elif kind == FIXED_OUT:
+        c["k_out"] = int(rng.integers(1, min(n, 400) + 1))
+        deg = float(c["k_out"])
+    else:
+        ne = int(round(0.8 * n))
+        c["k_in_exc"] = int(rng.integers(1, max(2, min(ne, 320))))
+        c["k_in_inh"] = int(rng.integers(1, max(2, min(n - ne, 80))))
+        deg = float(c["k_in_exc"] + c["k_in_inh"])
+    sc = min(1.0, 80.0 / max(deg, 1.0))
+    c["w_exc"], c["w_inh"] = _f32(0.27 * sc), _f32(-4.5 * sc)
+    c["ext_w"] = c["w_exc"]
+    c["ext_lambda"] = drive_lambda(c)
+    for k in ("v_rest", "v_th", "v_reset", "v0_lo", "v0_hi", "i_bias", "w_lo", "w_hi"):
+        c[k] = _f32(c[k])
+    return c
+
+
 def spike_set(n: int, count: int, seed: int, unique: bool = True) -> np.ndarray:
     """Seeded random spike IDs in [0, n)."""
     rng = np.random.default_rng(seed)

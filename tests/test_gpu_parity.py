@@ -413,6 +413,55 @@ def test_degenerate_networks_bit_identical(spk, name, mk, T, delivery, step_mode
     assert np.array_equal(gr, orf)
 
 
+# a sweep over seeded random shapes (tests/inputs.random_shape): sizes,
+# connectivity kinds, delays and formats the fixed cases do not hit
+RANDOM_SEEDS = list(range(1, 25))
+
+
+@pytest.mark.parametrize("seed", RANDOM_SEEDS)
+def test_random_shapes_bit_identical(spk, seed):
+    base = I.random_shape(seed)
+    base["acc_mode"] = I.ACC_FIXED
+    base["syn_format"] = FORMATS[seed % len(FORMATS)][0]
+    T = 150
+    r, ov, orf, _ = _oracle_run(base, T)
+    assert r["counts"].sum() > 0
+    runs = [(2, 1), (2, 2)] + ([(1, 1), (1, 2)] if base["delay_min"] == base["delay_max"] else [])
+    for delivery, step_mode in runs:
+        cfg = dict(base, delivery=delivery, step_mode=step_mode)
+        _say(f"[random] seed={seed} n={cfg['n']} kind={cfg['conn_kind']} delays={cfg['delay_min']}-"
+             f"{cfg['delay_max']} format={cfg['syn_format']} delivery={delivery} step_mode={step_mode}")
+        g = spk.Net(cfg, max_steps=T, raster_capacity=cfg["n"] * T)
+        assert g.stats()["step_mode"] == step_mode
+        g.step(T // 3)
+        g.step(T - T // 3)  # (across two calls)
+        offs, ids = g.raster()
+        assert np.array_equal(g.spike_counts(), r["counts"]), "spike counts differ"
+        assert np.array_equal(offs, r["offs"]) and np.array_equal(ids, r["raster"]), "rasters differ"
+        assert np.array_equal(g.events(), r["events"]) and np.array_equal(g.delivered(), r["delivered"])
+        gv, gr = g.state()
+        assert np.array_equal(gv.view(np.uint32), ov.view(np.uint32)) and np.array_equal(gr, orf)
+        g.close()
+
+
+@pytest.mark.parametrize("seed", RANDOM_SEEDS[:12])
+def test_random_shapes_fp32_persistent_equals_graph(spk, seed):
+    # fp32 mode: exact sums, so the two step modes agree bit for bit
+    base = I.random_shape(seed)
+    base["syn_format"] = FORMATS[seed % len(FORMATS)][0]
+    T = 150
+    out = []
+    for step_mode in (1, 2):
+        g = spk.Net(dict(base, delivery=2, step_mode=step_mode), max_steps=T)
+        g.step(T)
+        v, ref = g.state()
+        out.append((g.spike_counts(), g.events(), v.view(np.uint32), ref))
+        g.close()
+    assert out[0][0].sum() > 0
+    for a_, b_ in zip(out[0], out[1]):
+        assert np.array_equal(a_, b_)
+
+
 @pytest.mark.parametrize("acc", [I.ACC_F32, I.ACC_FIXED], ids=["f32", "fixed"])
 @pytest.mark.parametrize("fmt", [f for f, _ in FORMATS], ids=[n for _, n in FORMATS])
 @pytest.mark.parametrize("step_mode", [1, 2], ids=["graph", "persist"])
