@@ -19,6 +19,7 @@ constexpr uint32_t kMaxT8 = 256;       // tiles per group
 constexpr uint32_t kMaxTiles = kGroups * kMaxT8;
 constexpr uint32_t kMaxBuckets = 2048; // (delay, tile) buckets of one group in the push kernel
 constexpr uint32_t kMaxRow = 65535;    // synapses per source row (16-bit run offsets)
+constexpr uint32_t kOnceMaxB = 4992;   // (delay, tile) buckets of the procedural rows-once push
 // Two synapse formats.  Full: int2 {j << 24 | target, weight bits}.  Compact
 // (networks with at most kMaxClasses distinct weights, e.g. one weight per
 // source population, as in the paper's static models): u32
@@ -157,6 +158,7 @@ struct ModelArgs {
 // draw needs beyond the stream keys.
 struct ProcArgs {
     uint32_t k_out, n_exc, w_uniform;
+    uint32_t once;          // rows generated once by one of pg1 push blocks (pages across XCDs)
     float w_lo, w_hi, w_exc, w_inh;
     float qscale;           // 2^fixed_shift (fixed mode)
 };

@@ -65,9 +65,11 @@ struct ProcLDS {
 // The stored-format record of synapse j of source s (its target tgt is
 // known): compact {class << 30 | delay index << 24 | target} with class =
 // source population, or full {delay index << 24 | target, weight bits}.
+// pw: the weight stream's prefix of row s, mix64(keys.w ^ s) (per-synapse
+// weights: the synapse's draw is mix64(pw ^ j), i.e. key_hash(keys.w, s, j)).
 template <bool CMP>
 __device__ __forceinline__ typename SynRec<CMP>::T proc_record(const StepArgs &a, uint32_t s, uint32_t j,
-                                                              uint32_t tgt, uint32_t jd)
+                                                              uint32_t tgt, uint32_t jd, uint64_t pw)
 {
     const uint32_t key = (jd << kTargetBits) | tgt;
     if constexpr (CMP) {
@@ -75,7 +77,7 @@ __device__ __forceinline__ typename SynRec<CMP>::T proc_record(const StepArgs &a
     } else {
         float w;
         if (a.pr.w_uniform) {
-            const uint64_t h = key_hash(a.m.keys.w, s, j);
+            const uint64_t h = mix64(pw ^ (uint64_t)j);
             const float u = (float)(uint32_t)(h >> 40) * (1.0f / 16777216.0f);
             w = __fadd_rn(a.pr.w_lo, __fmul_rn(__fsub_rn(a.pr.w_hi, a.pr.w_lo), u));
         } else {
@@ -84,6 +86,12 @@ __device__ __forceinline__ typename SynRec<CMP>::T proc_record(const StepArgs &a
         const int32_t wb = a.m.fixed ? (int32_t)__builtin_rintf(__fmul_rn(w, a.pr.qscale)) : __float_as_int(w);
         return make_int2((int)key, wb);
     }
+}
+template <bool CMP>
+__device__ __forceinline__ typename SynRec<CMP>::T proc_record(const StepArgs &a, uint32_t s, uint32_t j,
+                                                              uint32_t tgt, uint32_t jd)
+{
+    return proc_record<CMP>(a, s, j, tgt, jd, CMP || !a.pr.w_uniform ? 0ull : mix64(a.m.keys.w ^ (uint64_t)s));
 }
 
 template <bool FIXED, bool CMP>
@@ -269,6 +277,201 @@ __global__ __launch_bounds__(kProcThreads) void k_push_proc(StepArgs a, uint32_t
     }
 }
 
+// Rows generated once (the graph path's default for procedural networks).
+// Between the push and the tile kernels lies a kernel boundary, so pages
+// need not stay on one XCD: push block b of NBLK (= pg1, one per compute
+// unit) takes the b-th equal share of the step's spikes, generates every
+// synapse of their rows once (no group filter: an eighth of the target draws
+// of k_push_proc) and files each event into its own page of the target's
+// tile, page (group of the tile, b, arrival slot, tile of the group); the
+// tile kernel drains the pages of all NBLK push blocks.  Each lane generates
+// consecutive synapses of the block's share (the wave's slice), kOnceR per
+// window, with the target, delay and weight streams' prefixes of the lane's
+// row held in registers; the events are sorted by (delay index, tile) over
+// all T tiles of the network, as k_push_proc does within a group.
+constexpr uint32_t kOnceChunk = 256;  // spikes per chunk
+
+template <bool CMP>
+struct OnceLDS {
+    using Rec = typename SynRec<CMP>::T;
+    static constexpr int R = CMP ? 12 : 6;                    // events per lane per window
+    static constexpr uint32_t kWin = R * kProcThreads;
+    Rec stage[kWin];                 // bucket-sorted events {bucket << 16 | page record}
+    uint32_t sid[kOnceChunk];        // the chunk's spikes (kNoSpike: an ID out of range)
+    uint32_t pre[kMaxTiles + 1];     // prefix of the source tiles' spike counts
+    uint32_t bcnt[kOnceMaxB];        // events per bucket in this window, then rank cursor
+    uint32_t bst[kOnceMaxB];         // bucket starts in the stage
+    uint32_t wb[kOnceMaxB];          // page position of stage entry q is wb[b] + q
+    uint32_t fill[kOnceMaxB];        // records already in the bucket's page
+    uint32_t pidx[kOnceMaxB];        // page of the bucket
+    uint32_t more[kProcWaves];       // the wave has synapses left to generate
+    uint32_t ws[16];
+    unsigned long long ws64[16];
+};
+
+template <bool FIXED, bool CMP>
+__global__ __launch_bounds__(kProcThreads) void k_push_proc_once(StepArgs a, uint32_t i, int64_t t_explicit)
+{
+    using Rec = typename SynRec<CMP>::T;
+    __shared__ OnceLDS<CMP> L;
+    constexpr int kOnceR = OnceLDS<CMP>::R;
+    const uint64_t t = step_index(a, i, t_explicit);
+    const uint32_t b = blockIdx.x, NBLK = gridDim.x;
+    const uint32_t tid = threadIdx.x, lane = lane_id();
+    const uint32_t w = __builtin_amdgcn_readfirstlane(tid / kWave);
+    const Tiling tl = a.tl;
+    const bool dbg = a.dbg_spikes != nullptr;
+    const uint32_t T = tl.T, NB = (dbg ? 1u : a.lists) * T;  // bucket (delay index, tile) = j * T + tile
+    const uint32_t sslot = (uint32_t)(t % a.spk_slots);
+    const uint32_t kout = a.pr.k_out;
+
+    for (uint32_t q = tid; q < NB; q += kProcThreads) {
+        const uint32_t j = q / T, tt = q - j * T, x = tt / tl.T8;
+        const uint32_t p = page_of(a, x, b, arrival_slot(a, t, j, dbg), tt - x * tl.T8);
+        L.pidx[q] = p;
+        L.fill[q] = a.pfill[p];
+        L.bcnt[q] = 0;
+    }
+    const uint32_t M = dbg ? a.dbg_n : load_spike_set(a, sslot, L.pre, L.ws);
+    const uint32_t k0 = (uint32_t)((uint64_t)M * b / NBLK), k1 = (uint32_t)((uint64_t)M * (b + 1) / NBLK);
+    const uint64_t cap = a.page_cap;
+    const bool uniform_w = !CMP && a.pr.w_uniform;
+    uint64_t emitted = 0;
+    for (uint32_t c0 = k0; c0 < k1 && kout; c0 += kOnceChunk) {
+        const uint32_t K = k1 - c0 < kOnceChunk ? k1 - c0 : kOnceChunk;
+        if (tid < K) {
+            const uint32_t k = c0 + tid;
+            const uint32_t s = dbg ? a.dbg_spikes[k] : spike_at(a, L.pre, sslot, k);
+            // a caller's spike list (debug delivery) is checked here: an ID
+            // out of range generates nothing and raises a flag
+            const bool bad = s >= a.n;
+            if (bad && b == 0) atomicOr(a.flags, kFlagBadSpike);
+            L.sid[tid] = bad ? kNoSpike : s;
+            emitted += bad ? 0u : kout;
+        }
+        lds_sync();
+        // the wave's slice [vb, ve) of the chunk's K * kout synapses; lane l
+        // generates synapse v = vcur + l, i.e. synapse j of spike si
+        const uint32_t V = K * kout;
+        const uint32_t vb = (uint32_t)((uint64_t)V * w / kProcWaves);
+        const uint32_t ve = (uint32_t)((uint64_t)V * (w + 1) / kProcWaves);
+        uint32_t vcur = vb;                                // (wave-uniform)
+        uint32_t si = (vb + lane) / kout, j = (vb + lane) - si * kout;
+        uint32_t sicur = kNoSpike, scur = kNoSpike;        // the lane's row (index, ID) and
+        uint64_t pt = 0, pd = 0, pw = 0;                   // its streams' prefixes
+        for (;;) {
+            Rec rec[kOnceR];
+            uint32_t okm = 0;  // bit u: rec[u] is an event
+#pragma unroll
+            for (int u = 0; u < kOnceR; u++) {
+                bool ok = false;
+                rec[u] = Rec{};
+                if (vcur + lane < ve) {
+                    if (si != sicur) {  // (once per kout synapses)
+                        sicur = si;
+                        scur = L.sid[si];
+                        pt = mix64(a.m.keys.tgt ^ (uint64_t)scur);
+                        pd = mix64(a.m.keys.delay ^ (uint64_t)scur);
+                        if (uniform_w) pw = mix64(a.m.keys.w ^ (uint64_t)scur);
+                    }
+                    if (scur != kNoSpike) {
+                        const uint32_t tgt = hash_range(mix64(pt ^ (uint64_t)j), a.n);
+                        const uint32_t jd = a.lists > 1 ? hash_range(mix64(pd ^ (uint64_t)j), a.lists) : 0u;
+                        ok = !(dbg && a.dbg_j >= 0 && (int32_t)jd != a.dbg_j);
+                        rec[u] = proc_record<CMP>(a, scur, j, tgt, jd, pw);
+                    }
+                }
+                okm |= (uint32_t)ok << u;
+                vcur += kWave;
+                j += kWave;
+                while (j >= kout) {
+                    j -= kout;
+                    si++;
+                }
+            }
+            if (lane == 0) L.more[w] = vcur < ve ? 1u : 0u;
+            // rank every event of the window within its bucket (LDS counters)
+            uint32_t tr[kOnceR];
+#pragma unroll
+            for (int q = 0; q < kOnceR; q++) {
+                tr[q] = 0xffffffffu;
+                if (!((okm >> q) & 1u)) continue;
+                const uint32_t key = rec_key(rec[q]);
+                const uint32_t tgt = rec_target(key);
+                const uint32_t bk = (dbg ? 0u : rec_delay(key)) * T + (tgt >> tl.logW);
+                const uint32_t rank = atomicAdd(&L.bcnt[bk], 1u);
+                tr[q] = (bk << 16) | rank;
+                const uint32_t sv = (bk << 16) | (tgt & (tl.W - 1));
+                if constexpr (CMP) rec[q] = sv | (rec_class(key) << kPageClassShift);
+                else rec[q].x = (int)sv;
+            }
+            lds_sync();
+            // bucket starts in the stage; the page position of staged event q
+            // of bucket b is wb[b] + q (mod 2^32); the fill counters advance
+            uint32_t staged;
+            {
+                const uint32_t P = (NB + kProcThreads - 1) / kProcThreads;
+                const uint32_t b0 = tid * P;
+                uint32_t sum = 0;
+                for (uint32_t k = 0; k < P; k++)
+                    if (b0 + k < NB) sum += L.bcnt[b0 + k];
+                uint32_t ex = block_scan_u32_open(sum, L.ws, &staged);
+                for (uint32_t k = 0; k < P; k++) {
+                    if (b0 + k < NB) {
+                        const uint32_t bb = b0 + k, c = L.bcnt[bb], f = L.fill[bb];
+                        L.bst[bb] = ex;
+                        L.wb[bb] = f - ex;
+                        L.fill[bb] = f + c;
+                        L.bcnt[bb] = 0;
+                        ex += c;
+                    }
+                }
+            }
+            lds_sync();
+#pragma unroll
+            for (int q = 0; q < kOnceR; q++) {
+                if (tr[q] == 0xffffffffu) continue;
+                L.stage[L.bst[tr[q] >> 16] + (tr[q] & 0xffffu)] = rec[q];
+            }
+            lds_sync();
+            // coalesced appends: consecutive staged events of a bucket go to
+            // consecutive page positions
+            for (uint32_t q = tid; q < staged; q += kProcThreads) {
+                const Rec r2 = L.stage[q];
+                const uint32_t key = rec_key(r2);
+                const uint32_t bk = key >> 16, low = key & 0xffffu;
+                const uint32_t pos = L.wb[bk] + q;
+                if (pos < cap) {
+                    const uint64_t e = (uint64_t)L.pidx[bk] * cap + pos;
+                    if constexpr (CMP) a.pages16[e] = (uint16_t)low;
+                    else a.pages[e] = make_int2((int)low, r2.y);
+                } else {
+                    long long units;
+                    uint32_t local;
+                    if constexpr (CMP) {
+                        units = class_units(a, low >> kPageClassShift);
+                        local = low & kPageLocalMask;
+                    } else {
+                        units = units_of<FIXED>(r2.y, a.m.shift64);
+                        local = low;
+                    }
+                    overflow_add<FIXED>(a, arrival_slot(a, t, bk / T, dbg), bk % T, local, units);
+                }
+            }
+            uint32_t any = 0;
+            for (uint32_t k = 0; k < kProcWaves; k++) any |= L.more[k];
+            lds_sync();  // the stage, wb and more[] are read before the next window writes them
+            if (!any) break;
+        }
+    }
+    lds_sync();
+    for (uint32_t q = tid; q < NB; q += kProcThreads) a.pfill[L.pidx[q]] = L.fill[q];
+    if (!dbg) {  // events emitted at t (each spike is in one block's share)
+        const uint64_t tot = block_sum_u64(emitted, L.ws64);
+        if (tid == 0 && tot) atomicAdd((unsigned long long *)&a.events8[t * kGroups], (unsigned long long)tot);
+    }
+}
+
 // Rows of the given sources as generated, synapse j of row r at out_off[r] + j:
 // target, weight bits as the full format stores them (compact classes: the
 // class's bits from the table), delay.
@@ -316,6 +519,21 @@ __global__ __launch_bounds__(256) void k_proc_in_abs_sum(StepArgs a, unsigned lo
 hipError_t launch_push_proc(const StepArgs &a, uint32_t i, int64_t t_explicit, hipStream_t s)
 {
     const uint32_t nj = a.dbg_spikes ? 1u : a.lists;
+    if (a.pr.once) {  // rows generated once: pg1 push blocks, pages of every group
+        if (!a.proc || a.direct || a.tl.T > kMaxTiles || a.tl.T != kGroups * a.tl.T8 || nj * a.tl.T > kOnceMaxB ||
+            a.tl.W > 8192 || a.pg1 == 0 || a.pslots == 0 || a.page_cap == 0 || a.pr.k_out > kMaxRow)
+            return hipErrorInvalidValue;
+        if (a.compact ? !a.pages16 : !a.pages) return hipErrorInvalidValue;
+        const dim3 grid(a.pg1), block(kProcThreads);
+        if (a.compact) {
+            if (a.m.fixed) hipLaunchKernelGGL((k_push_proc_once<true, true>), grid, block, 0, s, a, i, t_explicit);
+            else hipLaunchKernelGGL((k_push_proc_once<false, true>), grid, block, 0, s, a, i, t_explicit);
+        } else {
+            if (a.m.fixed) hipLaunchKernelGGL((k_push_proc_once<true, false>), grid, block, 0, s, a, i, t_explicit);
+            else hipLaunchKernelGGL((k_push_proc_once<false, false>), grid, block, 0, s, a, i, t_explicit);
+        }
+        return hipGetLastError();
+    }
     if (!a.proc || a.direct || a.tl.T > kMaxTiles || a.tl.T != kGroups * a.tl.T8 || nj * a.tl.T8 > kMaxBuckets ||
         a.tl.W > 8192 || a.pg1 == 0 || a.pslots == 0 || a.page_cap == 0 || a.pr.k_out > kMaxRow)
         return hipErrorInvalidValue;

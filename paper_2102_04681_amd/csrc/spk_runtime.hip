@@ -189,6 +189,7 @@ struct spk_net {
     // synapses: full (int2) or compact (u32 with a weight class)
     bool compact = false;
     bool proc = false;  // procedural synapses: generated when their source fires, not stored
+    bool proc_once = false;  // ... each fired row generated once (pages of every group per push block)
     uint32_t n_cls = 0;
     float cls_w[kMaxClasses] = {};
     ClassTab ctab{};
@@ -320,6 +321,7 @@ StepArgs step_args(const spk_net *net)
     a.compact = net->compact ? 1u : 0u;
     a.proc = net->proc ? 1u : 0u;
     a.pr.k_out = net->P.k_out;
+    a.pr.once = net->proc_once ? 1u : 0u;
     a.pr.n_exc = net->n_exc;
     a.pr.w_uniform = net->P.w_uniform;
     a.pr.w_lo = net->P.w_lo;
@@ -806,6 +808,13 @@ spk_status finish_rows(spk_net *net)
         // the budget and fall back to global atomics beyond it.
         net->pslots = net->dmax;
         net->pg1 = push_blocks_per_group();
+        // procedural rows are generated once, by one push block per compute
+        // unit, whose pages cover every group (graph path: the kernel boundary
+        // makes them visible on every XCD), where its buckets fit
+        net->proc_once = net->proc && (uint64_t)net->lists * tl.T <= kOnceMaxB;
+        if (const char *e = std::getenv("SPK_PROC_ONCE"))  // 0: the per-group push (tests)
+            if (e[0] == '0') net->proc_once = false;
+        if (net->proc_once) net->pg1 *= kGroups;
         const uint64_t n_pages = (uint64_t)kGroups * net->pg1 * net->pslots * tl.T8;
         uint64_t cap = std::min<uint64_t>(kPageBudget / n_pages, std::max<uint64_t>(net->nnz, 1));
         if (const char *e = std::getenv("SPK_PAGE_CAP")) {

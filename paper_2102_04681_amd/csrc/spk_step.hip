@@ -347,11 +347,6 @@ __global__ __launch_bounds__(kTileThreads) void k_tile(StepArgs a, uint32_t i, i
         const uint32_t ne = pf < cap ? pf : cap;  // records stored in page tid
         uint32_t C;
         const uint32_t cex = block_scan_u32((ne + kChunk - 1) / kChunk, L.ws, &C);
-        uint32_t *pn = L.pre + kTileThreads;      // record counts after the chunk prefix
-        if (tid < G1) {
-            L.pre[tid] = cex;
-            pn[tid] = ne;
-        }
         delivered = block_sum_u64(pf, L.ws64);  // includes events that overflowed
         const uint32_t w = tid / kWave;
         constexpr uint32_t nw = kTileThreads / kWave;

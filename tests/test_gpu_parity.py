@@ -842,11 +842,13 @@ PROC_CASES = [
 
 @pytest.mark.parametrize("name,mk", PROC_CASES, ids=[c[0] for c in PROC_CASES])
 @pytest.mark.parametrize("acc", [I.ACC_F32, I.ACC_FIXED], ids=["f32", "fixed"])
-def test_procedural_rows_and_delivery_equal_oracle(spk, name, mk, acc):
+@pytest.mark.parametrize("once", ["1", "0"], ids=["rows-once", "per-group"])
+def test_procedural_rows_and_delivery_equal_oracle(spk, name, mk, acc, once, monkeypatch):
     # procedural synapses are never stored: the rows the library generates
     # (exported) equal the oracle's, and delivering a spike set through them
     # equals the oracle's sums (exact in fixed mode, the rounded exact sum in
     # fp32 mode) and the stored compact/full format's bit for bit
+    monkeypatch.setenv("SPK_PROC_ONCE", once)
     cfg = dict(mk(acc), syn_format=3)
     g = spk.Net(cfg, max_steps=1)
     st = g.stats()
@@ -882,9 +884,13 @@ PROC_RUNS = [
 
 
 @pytest.mark.parametrize("name,mk,T", PROC_RUNS, ids=[c[0] for c in PROC_RUNS])
-def test_procedural_simulation_bit_identical(spk, name, mk, T, monkeypatch):
+@pytest.mark.parametrize("once", ["1", "0"], ids=["rows-once", "per-group"])
+def test_procedural_simulation_bit_identical(spk, name, mk, T, once, monkeypatch):
     # fixed point: rasters, counts, events, delivered events and final state
-    # equal the oracle's; also with the pages shrunk into the overflow path
+    # equal the oracle's; also with the pages shrunk into the overflow path.
+    # Both push kernels: each fired row generated once (the default where its
+    # buckets fit) and generated by every XCD group (SPK_PROC_ONCE=0)
+    monkeypatch.setenv("SPK_PROC_ONCE", once)
     cfg = dict(mk(), acc_mode=I.ACC_FIXED, syn_format=3)
     r, ov, orf, (rp, col, w, d) = _oracle_run(cfg, T)
     assert r["counts"].sum() > 0

@@ -177,7 +177,9 @@ def test_c4_fixed_point_100_steps_bit_identical(spk_mod, page_cap, fmt, monkeypa
     if page_cap:
         assert st["page_cap"] == page_cap
     else:
-        assert st["page_cap"] == 1696
+        # an equal share of 2^28 records: 8 x 32 x 20 x 31 pages (procedural:
+        # each row generated once by one of 256 push blocks, 8 x 256 x 20 x 31)
+        assert st["page_cap"] == (224 if fmt == 3 else 1696)
     _say(f"[raster] c4 gpu done: {int(gpu['counts'].sum())} spikes")
     ref = _oracle_result(key)
     _compare(gpu, ref)
