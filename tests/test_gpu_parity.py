@@ -445,6 +445,35 @@ def test_random_shapes_bit_identical(spk, seed):
 
 
 @pytest.mark.parametrize("seed", RANDOM_SEEDS[:12])
+def test_random_procedural_shapes_bit_identical(spk, seed, monkeypatch):
+    # procedural synapses on random fixed out-degree shapes (both push
+    # kernels): fixed-point runs bit-identical to the oracle
+    base = I.random_shape(seed)
+    base.update(conn_kind=I.FIXED_OUT, k_out=int(min(base["n"], 50 + 37 * seed)), p=0.0, k_in_exc=0,
+                k_in_inh=0, acc_mode=I.ACC_FIXED, syn_format=3)
+    sc = min(1.0, 80.0 / base["k_out"])
+    base["w_exc"], base["w_inh"] = I._f32(0.27 * sc), I._f32(-4.5 * sc)
+    base["ext_w"] = base["w_exc"]
+    base["ext_lambda"] = I.drive_lambda(base)
+    T = 120
+    r, ov, orf, _ = _oracle_run(base, T)
+    assert r["counts"].sum() > 0
+    for once in ("1", "0"):
+        monkeypatch.setenv("SPK_PROC_ONCE", once)
+        _say(f"[random proc] seed={seed} n={base['n']} k_out={base['k_out']} delays={base['delay_min']}-"
+             f"{base['delay_max']} once={once}")
+        g = spk.Net(base, max_steps=T, raster_capacity=base["n"] * T)
+        g.step(T // 2)
+        g.step(T - T // 2)
+        offs, ids = g.raster()
+        assert np.array_equal(g.spike_counts(), r["counts"]) and np.array_equal(ids, r["raster"]), once
+        assert np.array_equal(g.events(), r["events"]) and np.array_equal(g.delivered(), r["delivered"])
+        gv, gr = g.state()
+        assert np.array_equal(gv.view(np.uint32), ov.view(np.uint32)) and np.array_equal(gr, orf)
+        g.close()
+
+
+@pytest.mark.parametrize("seed", RANDOM_SEEDS[:12])
 def test_random_shapes_fp32_persistent_equals_graph(spk, seed):
     # fp32 mode: exact sums, so the two step modes agree bit for bit
     base = I.random_shape(seed)
