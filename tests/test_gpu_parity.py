@@ -200,14 +200,15 @@ def test_fig_adj_delivery(spk):
 def _abs_sum(o, spikes, delay):
     """Per target: sum of |w| over contributing synapses, and their number."""
     rp, col, w, d = o.csr()
-    out = np.zeros(o.n)
-    cnt = np.zeros(o.n)
-    for s in spikes:
-        a, b = int(rp[s]), int(rp[s + 1])
-        m = slice(a, b)
-        sel = np.ones(b - a, bool) if delay == 0 else d[m] == delay
-        np.add.at(out, col[m][sel], np.abs(w[m][sel].astype(np.float64)))
-        np.add.at(cnt, col[m][sel], 1.0)
+    s = np.asarray(spikes, dtype=np.int64)
+    a, b = rp[s].astype(np.int64), rp[s + 1].astype(np.int64)
+    lens = b - a
+    # the synapse positions of every spike's row, spikes repeated as given
+    idx = np.repeat(a - (np.cumsum(lens) - lens), lens) + np.arange(int(lens.sum()), dtype=np.int64)
+    if delay:
+        idx = idx[d[idx] == delay]
+    out = np.bincount(col[idx], weights=np.abs(w[idx].astype(np.float64)), minlength=o.n)
+    cnt = np.bincount(col[idx], minlength=o.n).astype(np.float64)
     return out, cnt
 
 
@@ -221,6 +222,28 @@ def _fp32_tolerance(want, abs_sum, terms):
     k = np.maximum(terms - 1.0, 0.0)
     gamma = k * u / (1.0 - k * u)
     return np.maximum(1e-5, gamma) * np.maximum(np.abs(want), abs_sum)
+
+
+def _check_deliver(o, got, spikes, delay, acc):
+    """The inputs one delivery of `spikes` leaves (synapses of `delay`, 0 =
+    all) against the oracle's: equal in fixed point; in fp32 within 1e-5
+    relative (widened where fp32 summation cannot promise it) and within one
+    ulp of the double-precision sum, since the library sums exactly and
+    rounds once."""
+    if acc == I.ACC_FIXED:
+        _, want = o.deliver(spikes, delay=delay, fixed=True)
+        assert np.array_equal(got.astype(np.int64), want), "fixed-point inputs differ"
+        return
+    want = o.deliver(spikes, delay=delay)
+    abs_sum, terms = _abs_sum(o, spikes, delay)
+    tol = _fp32_tolerance(want, abs_sum, terms)
+    err = np.abs(got.astype(np.float64) - want)
+    scale = np.maximum(np.abs(want), abs_sum) + 1e-30
+    assert np.all(err <= tol), f"max rel err {np.max(err / scale)}"
+    if terms.max() <= 168:  # the plain 1e-5 relative bar applies
+        assert np.all(err <= 1e-5 * scale)
+    ulp = np.spacing(np.abs(want).astype(np.float32)).astype(np.float64)
+    assert np.all(err <= ulp), f"not the rounded exact sum: {np.max(err / ulp)} ulp"
 
 
 DELIVER_CASES = [
@@ -254,23 +277,7 @@ def test_debug_deliver_matches_oracle(spk, name, mk, delays, acc, delivery, fmt)
         spikes = I.spike_set(n, count, seed=10 + k, unique=uniq)
         for delay in delays:
             _say(f"[deliver] {name} acc={acc} spikes={len(spikes)} delay={delay}")
-            got = g.debug_deliver(spikes, delay=delay)
-            if acc == I.ACC_FIXED:
-                _, want = o.deliver(spikes, delay=delay, fixed=True)
-                assert np.array_equal(got.astype(np.int64), want), "fixed-point inputs differ"
-            else:
-                want = o.deliver(spikes, delay=delay)
-                abs_sum, terms = _abs_sum(o, spikes, delay)
-                tol = _fp32_tolerance(want, abs_sum, terms)
-                err = np.abs(got.astype(np.float64) - want)
-                scale = np.maximum(np.abs(want), abs_sum) + 1e-30
-                assert np.all(err <= tol), f"max rel err {np.max(err / scale)}"
-                if terms.max() <= 168:  # the plain 1e-5 relative bar applies
-                    assert np.all(err <= 1e-5 * scale)
-                # the library sums exactly and rounds once: within one fp32
-                # ulp of the double-precision reference sum
-                ulp = np.spacing(np.abs(want).astype(np.float32)).astype(np.float64)
-                assert np.all(err <= ulp), f"not the rounded exact sum: {np.max(err / ulp)} ulp"
+            _check_deliver(o, g.debug_deliver(spikes, delay=delay), spikes, delay, acc)
 
 
 def test_debug_deliver_rejects_bad_input(spk):
@@ -441,6 +448,28 @@ def test_random_shapes_bit_identical(spk, seed):
         assert np.array_equal(g.events(), r["events"]) and np.array_equal(g.delivered(), r["delivered"])
         gv, gr = g.state()
         assert np.array_equal(gv.view(np.uint32), ov.view(np.uint32)) and np.array_equal(gr, orf)
+        g.close()
+
+
+@pytest.mark.parametrize("seed", RANDOM_SEEDS)
+@pytest.mark.parametrize("acc", [I.ACC_F32, I.ACC_FIXED], ids=["f32", "fixed"])
+def test_random_shapes_deliver_matches_oracle(spk, seed, acc):
+    # one delivery of a given spike set on random shapes (both deliveries,
+    # the shape's format, the smallest, largest and a middle delay and all
+    # delays at once): the inputs equal the oracle's to the bar above
+    base = dict(I.random_shape(seed), acc_mode=acc)
+    base["syn_format"] = FORMATS[seed % len(FORMATS)][0]
+    n, d0, d1 = base["n"], base["delay_min"], base["delay_max"]
+    o = _oracle_net(base)
+    delays = sorted({0, d0, (d0 + d1) // 2, d1})
+    for delivery in (1, 2):
+        g = spk.Net(dict(base, delivery=delivery), max_steps=1)
+        for k, count in enumerate([1, max(1, n // 100), n // 3]):
+            spikes = I.spike_set(n, count, seed=100 * seed + k)
+            for delay in delays:
+                _say(f"[random deliver] seed={seed} n={n} kind={base['conn_kind']} delays={d0}-{d1} "
+                     f"format={base['syn_format']} delivery={delivery} spikes={len(spikes)} delay={delay}")
+                _check_deliver(o, g.debug_deliver(spikes, delay=delay), spikes, delay, acc)
         g.close()
 
 
