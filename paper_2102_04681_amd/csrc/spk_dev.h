@@ -59,15 +59,30 @@ __device__ __forceinline__ uint64_t step_index(const StepArgs &a, uint32_t i, in
     return t_explicit >= 0 ? (uint64_t)t_explicit : *a.t_base + i;
 }
 
+// Inclusive prefix sum of one u32 per lane over a whole wave (every lane
+// active): DPP row shifts by 1, 2, 4 and 8 lanes scan each row of 16 lanes
+// (a lane with no source adds 0), then each row adds the totals of the rows
+// before it, read from lanes 15, 31 and 47.  No LDS traffic, unlike a
+// shuffle (ds_bpermute) per step.
+__device__ __forceinline__ uint32_t wave_scan_incl_u32(uint32_t x)
+{
+    int v = (int)x;
+    v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, true);  // row_shr:1
+    v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, true);  // row_shr:2
+    v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, true);  // row_shr:4
+    v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, true);  // row_shr:8
+    const uint32_t t0 = (uint32_t)__builtin_amdgcn_readlane(v, 15), t1 = (uint32_t)__builtin_amdgcn_readlane(v, 31),
+                   t2 = (uint32_t)__builtin_amdgcn_readlane(v, 47);
+    const uint32_t row = lane_id() >> 4;
+    const uint32_t before = (row >= 1 ? t0 : 0u) + (row >= 2 ? t1 : 0u) + (row >= 3 ? t2 : 0u);
+    return (uint32_t)v + before;
+}
+
 // Block-wide exclusive scan of one u32 per thread (blockDim <= 1024).
 __device__ uint32_t block_scan_u32(uint32_t x, uint32_t *ws /*>=16*/, uint32_t *total)
 {
     const uint32_t lane = lane_id(), w = threadIdx.x / kWave, nw = blockDim.x / kWave;
-    uint32_t inc = x;
-    for (int o = 1; o < kWave; o <<= 1) {
-        const uint32_t y = __shfl_up(inc, o);
-        if (lane >= (uint32_t)o) inc += y;
-    }
+    const uint32_t inc = wave_scan_incl_u32(x);
     if (lane == kWave - 1) ws[w] = inc;
     lds_sync();
     uint32_t before = 0, tot = 0;
@@ -86,11 +101,7 @@ __device__ uint32_t block_scan_u32(uint32_t x, uint32_t *ws /*>=16*/, uint32_t *
 __device__ uint32_t block_scan_u32_open(uint32_t x, uint32_t *ws /*>=16*/, uint32_t *total)
 {
     const uint32_t lane = lane_id(), w = threadIdx.x / kWave, nw = blockDim.x / kWave;
-    uint32_t inc = x;
-    for (int o = 1; o < kWave; o <<= 1) {
-        const uint32_t y = __shfl_up(inc, o);
-        if (lane >= (uint32_t)o) inc += y;
-    }
+    const uint32_t inc = wave_scan_incl_u32(x);
     if (lane == kWave - 1) ws[w] = inc;
     lds_sync();
     uint32_t before = 0, tot = 0;
@@ -281,12 +292,8 @@ __device__ uint32_t gather_direct(const StepArgs &a, typename Acc<FIXED>::T *acc
             beg = a.row_ptr[s] + b;
             len = bad ? 0u : e - b;
         }
-        uint32_t inc = len;
-        for (int o = 1; o < kWave; o <<= 1) {
-            const uint32_t y = __shfl_up(inc, o);
-            if (lane >= (uint32_t)o) inc += y;
-        }
-        const uint32_t tot = __shfl(inc, kWave - 1);
+        const uint32_t inc = wave_scan_incl_u32(len);
+        const uint32_t tot = (uint32_t)__builtin_amdgcn_readlane((int)inc, kWave - 1);
         wpre[w][lane] = inc - len;
         wbeg[w][lane] = beg;
         if (lane == 0) wpre[w][kWave] = tot;

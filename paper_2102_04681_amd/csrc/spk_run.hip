@@ -603,7 +603,7 @@ __device__ void run_update(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x,
     if (nw_spk) {
         uint32_t wb = 0;
         if (lane == 0) wb = atomicAdd(cnt, nw_spk);
-        wb = __shfl(wb, 0);
+        wb = (uint32_t)__builtin_amdgcn_readlane((int)wb, 0);  // (lane 0 took the positions)
 #pragma unroll
         for (int u = 0; u < kRunRounds; u++) {
             const uint64_t mask = bal[u];
@@ -695,7 +695,7 @@ __device__ void run_update_batch(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint3
             if (bal) {  // (uniform) one counter update per wave and step
                 uint32_t wb = 0;
                 if (lane == 0) wb = atomicAdd(&L.u.t.nb[u], (uint32_t)__popcll(bal));
-                wb = __shfl(wb, 0);
+                wb = (uint32_t)__builtin_amdgcn_readlane((int)wb, 0);  // (lane 0 took the positions)
                 if (spk) {
                     const uint32_t rank =
                         __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
