@@ -114,10 +114,38 @@ __device__ uint32_t block_scan_u32_open(uint32_t x, uint32_t *ws /*>=16*/, uint3
     return before + inc - x;
 }
 
+// One step of a 64-bit row scan: x plus the value of the lane C & 0xf below
+// in its row of 16 (0 where there is none), both halves moved by DPP.
+template <int C>
+__device__ __forceinline__ uint64_t dpp_shr_add_u64(uint64_t x)
+{
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)x, C, 0xf, 0xf, true);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(x >> 32), C, 0xf, 0xf, true);
+    return x + (((uint64_t)hi << 32) | lo);
+}
+
+// Sum of one u64 per lane over a whole wave (every lane active), the same in
+// every lane: each row of 16 lanes is scanned with DPP row shifts, and the
+// four row sums are read from lanes 15, 31, 47 and 63.
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t x)
+{
+    x = dpp_shr_add_u64<0x111>(x);  // row_shr:1
+    x = dpp_shr_add_u64<0x112>(x);  // row_shr:2
+    x = dpp_shr_add_u64<0x114>(x);  // row_shr:4
+    x = dpp_shr_add_u64<0x118>(x);  // row_shr:8
+    const int lo = (int)(uint32_t)x, hi = (int)(uint32_t)(x >> 32);
+    uint64_t tot = 0;
+#pragma unroll
+    for (int r = 0; r < kWave / 16; r++)
+        tot += ((uint64_t)(uint32_t)__builtin_amdgcn_readlane(hi, 16 * r + 15) << 32) |
+               (uint32_t)__builtin_amdgcn_readlane(lo, 16 * r + 15);
+    return tot;
+}
+
 __device__ __forceinline__ uint64_t block_sum_u64(uint64_t x, unsigned long long *ws /*>=16*/)
 {
     const uint32_t lane = lane_id(), w = threadIdx.x / kWave, nw = blockDim.x / kWave;
-    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
+    x = wave_sum_u64(x);
     if (lane == 0) ws[w] = x;
     lds_sync();
     uint64_t tot = 0;

@@ -493,7 +493,7 @@ __global__ __launch_bounds__(kTileThreads) void k_tile(StepArgs a, uint32_t i, i
             const int leader = __ffsll((unsigned long long)mask) - 1;
             uint32_t wb = 0;
             if ((int)lane == leader) wb = atomicAdd(&L.nspk, (uint32_t)__popcll(mask));
-            wb = __shfl(wb, leader);
+            wb = (uint32_t)__builtin_amdgcn_readlane((int)wb, leader);
             if (spk) {
                 const uint32_t rank = __builtin_amdgcn_mbcnt_hi(
                     (uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
