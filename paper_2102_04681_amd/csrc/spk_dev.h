@@ -78,19 +78,36 @@ __device__ __forceinline__ uint32_t wave_scan_incl_u32(uint32_t x)
     return (uint32_t)v + before;
 }
 
-// Block-wide exclusive scan of one u32 per thread (blockDim <= 1024).
+// Every kernel that uses the block-wide helpers below runs workgroups of
+// kBlockThreads threads (a constant, so that the per-wave partials are read
+// with all loads at once instead of a loop bounded by blockDim).
+constexpr uint32_t kBlockThreads = 1024;
+constexpr uint32_t kBlockWaves = kBlockThreads / kWave;
+
+// The per-wave partials ws[0 .. kBlockWaves) of a block-wide scan: their sum
+// before wave w and their total.  kBlockWaves is one DPP row: every row of
+// 16 lanes reads the 16 partials (one LDS read per lane) and scans them.
+static_assert(kBlockWaves == 16, "one partial per lane of a DPP row");
+__device__ __forceinline__ void wave_partials(const uint32_t *ws, uint32_t w, uint32_t *before, uint32_t *tot)
+{
+    int v = (int)ws[lane_id() & (kBlockWaves - 1)];
+    v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, true);  // row_shr:1
+    v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, true);  // row_shr:2
+    v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, true);  // row_shr:4
+    v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, true);  // row_shr:8
+    *tot = (uint32_t)__builtin_amdgcn_readlane(v, kBlockWaves - 1);
+    *before = w ? (uint32_t)__builtin_amdgcn_readlane(v, (int)w - 1) : 0u;
+}
+
+// Block-wide exclusive scan of one u32 per thread.
 __device__ uint32_t block_scan_u32(uint32_t x, uint32_t *ws /*>=16*/, uint32_t *total)
 {
-    const uint32_t lane = lane_id(), w = threadIdx.x / kWave, nw = blockDim.x / kWave;
+    const uint32_t lane = lane_id(), w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const uint32_t inc = wave_scan_incl_u32(x);
     if (lane == kWave - 1) ws[w] = inc;
     lds_sync();
-    uint32_t before = 0, tot = 0;
-    for (uint32_t k = 0; k < nw; k++) {
-        const uint32_t v = ws[k];
-        before += k < w ? v : 0u;
-        tot += v;
-    }
+    uint32_t before, tot;
+    wave_partials(ws, w, &before, &tot);
     lds_sync();
     *total = tot;
     return before + inc - x;
@@ -100,16 +117,12 @@ __device__ uint32_t block_scan_u32(uint32_t x, uint32_t *ws /*>=16*/, uint32_t *
 // the caller's next barrier.
 __device__ uint32_t block_scan_u32_open(uint32_t x, uint32_t *ws /*>=16*/, uint32_t *total)
 {
-    const uint32_t lane = lane_id(), w = threadIdx.x / kWave, nw = blockDim.x / kWave;
+    const uint32_t lane = lane_id(), w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     const uint32_t inc = wave_scan_incl_u32(x);
     if (lane == kWave - 1) ws[w] = inc;
     lds_sync();
-    uint32_t before = 0, tot = 0;
-    for (uint32_t k = 0; k < nw; k++) {
-        const uint32_t v = ws[k];
-        before += k < w ? v : 0u;
-        tot += v;
-    }
+    uint32_t before, tot;
+    wave_partials(ws, w, &before, &tot);
     *total = tot;
     return before + inc - x;
 }
@@ -144,32 +157,20 @@ __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t x)
 
 __device__ __forceinline__ uint64_t block_sum_u64(uint64_t x, unsigned long long *ws /*>=16*/)
 {
-    const uint32_t lane = lane_id(), w = threadIdx.x / kWave, nw = blockDim.x / kWave;
+    const uint32_t lane = lane_id(), w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     x = wave_sum_u64(x);
     if (lane == 0) ws[w] = x;
     lds_sync();
-    uint64_t tot = 0;
-    for (uint32_t k = 0; k < nw; k++) tot += ws[k];
+    // each row of 16 lanes sums the 16 partials (one LDS read per lane)
+    uint64_t v = ws[lane & (kBlockWaves - 1)];
+    v = dpp_shr_add_u64<0x111>(v);
+    v = dpp_shr_add_u64<0x112>(v);
+    v = dpp_shr_add_u64<0x114>(v);
+    v = dpp_shr_add_u64<0x118>(v);
+    const uint64_t tot = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), 15) << 32) |
+                         (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, 15);
     lds_sync();
     return tot;
-}
-
-// Block-wide exclusive max-scan of one u32 per thread.
-__device__ uint32_t block_scan_max_u32(uint32_t x, uint32_t *ws)
-{
-    const uint32_t lane = lane_id(), w = threadIdx.x / kWave;
-    uint32_t inc = x;
-    for (int o = 1; o < kWave; o <<= 1) {
-        const uint32_t y = __shfl_up(inc, o);
-        if (lane >= (uint32_t)o) inc = y > inc ? y : inc;
-    }
-    const uint32_t ex_w = __shfl_up(inc, 1);
-    if (lane == kWave - 1) ws[w] = inc;
-    lds_sync();
-    uint32_t before = 0;
-    for (uint32_t k = 0; k < w; k++) before = ws[k] > before ? ws[k] : before;
-    lds_sync();
-    return lane ? (ex_w > before ? ex_w : before) : before;
 }
 
 // The spike list of one slot is spread over per-tile segments: pre[] gets
@@ -298,7 +299,10 @@ __device__ uint32_t gather_direct(const StepArgs &a, typename Acc<FIXED>::T *acc
                                   uint32_t tile_lo, uint32_t P, uint32_t slot, int32_t jf)
 {
     using Rec = typename SynRec<CMP>::T;
-    const uint32_t lane = lane_id(), w = threadIdx.x / kWave, nw = blockDim.x / kWave;
+    // (the wave count as a constant in the persistent kernel; the graph
+    // path's tile kernel, which holds both deliveries, compiles to faster
+    // code with it read from blockDim: measured on both)
+    const uint32_t lane = lane_id(), w = threadIdx.x / kWave, nw = COH ? kBlockWaves : blockDim.x / kWave;
     const uint32_t T1 = a.tl.T + 1;
     uint32_t mine = 0;
     // spikes per wave and round: all waves share the spikes (few spikes with

@@ -35,6 +35,7 @@ namespace spk {
 namespace {
 
 constexpr int kProcThreads = 1024;
+static_assert(kProcThreads == (int)kBlockThreads, "the block-wide helpers assume workgroups of kBlockThreads");
 constexpr uint32_t kProcChunk = 1024;                      // spikes generated per chunk
 constexpr uint32_t kProcWaves = kProcThreads / kWave;
 constexpr uint32_t kRing = 128;                            // events a wave holds between windows

@@ -49,6 +49,7 @@ namespace spk {
 namespace {
 
 constexpr int kRunThreads = 1024;
+static_assert(kRunThreads == (int)kBlockThreads, "the block-wide helpers assume workgroups of kBlockThreads");
 
 // The thread index, opaque to the optimiser: address arithmetic derived from
 // it is then recomputed in each phase instead of being hoisted out of the

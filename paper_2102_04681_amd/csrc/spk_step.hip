@@ -39,6 +39,8 @@ namespace {
 
 constexpr int kPushThreads = 1024;
 constexpr int kTileThreads = 1024;
+static_assert(kPushThreads == (int)kBlockThreads && kTileThreads == (int)kBlockThreads,
+              "the block-wide helpers assume workgroups of kBlockThreads");
 constexpr int kPushR = 16;                                // events per thread per load phase
 constexpr uint32_t kLoadPhase = kPushR * kPushThreads;    // events loaded at once
 constexpr uint32_t kStage = kLoadPhase / 2;               // events bucket-sorted at once
