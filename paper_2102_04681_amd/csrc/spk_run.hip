@@ -1162,9 +1162,9 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
         s += Db;
         const bool more = s < ra.n_steps;
         if (has_tile) {
+            // binned: the draws not made before the last push phase
+            for (; dr_k < dr_n; dr_k++) run_draw_unit(a, L, tile_lo, tile_n, dr_t, dr_k);
             // binned: every push block of the XCD has filed the previous batch
-            if constexpr (BATCH)
-                for (; dr_k < dr_n; dr_k++) run_draw_unit(a, L, tile_lo, tile_n, dr_t, dr_k);
             if (!DIRECT && !wait_pushes(ra, L, x, ex)) return;
             // the push phase reused this LDS: accumulators restart at zero, and
             // the spike count of the previous step has been read by every thread
@@ -1198,13 +1198,12 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
         } else {  // binned: the tiles' progress words instead of a grid barrier
             ++eg;
             if (has_tile) publish_tile(ra, tile, eg, &L.nspk2[Db == 1 ? 0u : 2u]);
-            // the next batch's draws while the others finish.  Batches of
-            // several steps: a unit at a time between looks at the tiles'
-            // words; once every tile has published, the rest waits until after
-            // the push phase (the last tiles to finish would otherwise hold
-            // every push phase up by their draws).  One-step batches draw at
-            // once (measured: the looks between units cost more there).
-            if constexpr (BATCH) {
+            // the next batch's draws while the others finish: a unit at a
+            // time between looks at the tiles' words; once every tile has
+            // published, the rest waits until after the push phase (the last
+            // tiles to finish would otherwise hold every push phase up by
+            // their draws)
+            {
                 bool ready = false;
                 dr_t = t_first + Db;
                 dr_k = 0;
@@ -1213,9 +1212,6 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
                     ready = look_tiles(ra, L, eg, Db == 1, look++ & 1u,
                                        [&] { run_draw_unit(a, L, tile_lo, tile_n, dr_t, dr_k++); });
                 if (!ready && !wait_tiles(ra, L, eg, Db == 1)) return;
-            } else {
-                if (has_tile && more) run_draws(a, L, tile_lo, tile_n, t_first + Db, Dn);
-                if (!wait_tiles(ra, L, eg, Db == 1)) return;
             }
         }
         if (DIRECT) {
