@@ -148,6 +148,7 @@ struct RunLDS {
             uint32_t bcnt[kRunMaxBuckets];  // events per bucket in this window, then rank cursor
             uint32_t bst[kRunMaxBuckets];   // bucket starts in the stage
             uint32_t wb[kRunMaxBuckets];    // page position of stage entry q is wb[b] + q
+            uint32_t pb[kRunMaxBuckets];    // first record of the bucket's page (pages x capacity < 2^32)
         } p;
     } u;
     uint32_t ws[16], ws2[16];
@@ -974,6 +975,7 @@ __device__ uint32_t run_push(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t 
                         uint32_t &f = L.fill[sl * tl.T8 + cc];
                         L.u.p.bst[bb] = ex;
                         L.u.p.wb[bb] = f - ex;
+                        L.u.p.pb[bb] = page_of(a, x, r, sl, cc) * a.page_cap;
                         f += cnt;
                         L.u.p.bcnt[bb] = 0;
                         ex += cnt;
@@ -995,14 +997,14 @@ __device__ uint32_t run_push(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t 
                 const uint32_t key = rec_key(r2);
                 const uint32_t b = key >> 16, low = key & 0xffffu;
                 const uint32_t pos = L.u.p.wb[b] + q;
-                const uint32_t ao = b / tl.T8, cc = b - ao * tl.T8;
-                uint32_t sl = slot_of_a0 + ao;
-                sl = sl >= a.pslots ? sl - a.pslots : sl;
                 if (pos < cap) {
-                    const uint64_t e = (uint64_t)page_of(a, x, r, sl, cc) * cap + pos;
+                    const uint32_t e = L.u.p.pb[b] + pos;
                     if constexpr (CMP) a.pages16[e] = (uint16_t)low;
                     else a.pages[e] = make_int2((int)low, r2.y);
                 } else {
+                    const uint32_t ao = b / tl.T8, cc = b - ao * tl.T8;
+                    uint32_t sl = slot_of_a0 + ao;
+                    sl = sl >= a.pslots ? sl - a.pslots : sl;
                     long long units;
                     uint32_t local;
                     if constexpr (CMP) {
