@@ -383,16 +383,16 @@ __device__ bool wait_pushes(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x
 // beyond the count.
 template <bool FIXED, bool CMP, bool ONE>
 __device__ void run_drain(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t x, uint32_t c, uint32_t tile,
-                          uint32_t tile_n, uint64_t t_first, uint32_t Db)
+                          uint32_t tile_n, uint32_t pslot0, uint32_t Db)
 {
     const uint32_t tid = tid_here();
     const Tiling tl = a.tl;
     constexpr uint32_t kPer = CMP ? 2u : 1u;
     constexpr uint32_t kChunk = kPer * kWave;
     const uint32_t cap = a.page_cap, G1 = a.pg1, P = Db * G1;
-    const uint32_t pslot0 = (uint32_t)(t_first % a.pslots);  // Db <= pslots: one wrap at most
+    // (pslot0: the arrival slot of the first step; Db <= pslots: one wrap at most)
     // thread p < P: page p = u * G1 + g, push block g's page of arrival step t_first + u
-    const uint32_t pu = tid < P ? tid / G1 : 0u, pg = tid < P ? tid - pu * G1 : 0u;
+    const uint32_t pu = ONE || tid >= P ? 0u : tid / G1, pg = tid < P ? tid - pu * G1 : 0u;
     const uint32_t psl = pslot0 + pu < a.pslots ? pslot0 + pu : pslot0 + pu - a.pslots;
     const uint32_t page = page_of(a, x, pg, psl, c);
     uint32_t pf = a.pfill[page];
@@ -406,13 +406,17 @@ __device__ void run_drain(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t x, 
     constexpr int kSpecU = CMP ? 8 : 16;
     // ONE: chunk q = u * nw + w of the speculative loads is chunk q % spc of
     // push block q / spc's page; spc * kChunk records per page (S)
-    const uint32_t spc = ONE ? kSpecU * nw / G1 : 0u, S = spc * kChunk;
+    const uint32_t spc = ONE ? kSpecU * nw / G1 : 1u, S = spc * kChunk;
+    // q / spc for q < 256 as (q * spc_inv) >> 16: exact, since q (spc_inv -
+    // 2^16 / spc) spc < q spc < 2^16 (a division per chunk cost ~0.5 us per
+    // step)
+    const uint32_t spc_inv = (65536u + spc - 1u) / spc;
     using Ld = typename std::conditional<CMP, uint32_t, int2>::type;
     Ld sr[ONE ? kSpecU : 1];
     if constexpr (ONE) {
 #pragma unroll
         for (int u = 0; u < kSpecU; u++) {
-            const uint32_t q = u * nw + w, g = q / spc, o = (q - g * spc) * kChunk + lane * kPer;
+            const uint32_t q = u * nw + w, g = (q * spc_inv) >> 16, o = (q - g * spc) * kChunk + lane * kPer;
             const bool ok = g < G1 && o < cap;  // (cap is a multiple of 16: both halves of a pair)
             const uint32_t idx = ok ? (page_of(a, x, g, pslot0, c) * cap + o) / kPer : 0u;
             if constexpr (CMP) sr[u] = ((const uint32_t *)a.pages16)[idx];
@@ -435,7 +439,7 @@ __device__ void run_drain(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t x, 
     if constexpr (ONE) {
 #pragma unroll
         for (int u = 0; u < kSpecU; u++) {
-            const uint32_t q = u * nw + w, g = q / spc, o = (q - g * spc) * kChunk + lane * kPer;
+            const uint32_t q = u * nw + w, g = (q * spc_inv) >> 16, o = (q - g * spc) * kChunk + lane * kPer;
             const uint32_t f = g < G1 ? L.u.t.pfv[g] : 0u;
             if constexpr (CMP) {
 #pragma unroll
@@ -566,8 +570,8 @@ __device__ __forceinline__ bool lif_step(float &V, uint32_t &r, float I, float m
 // the tile's segment of the spike list of t.
 template <bool FIXED, bool CMP, bool DIRECT>
 __device__ void run_update(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x, uint32_t tile,
-                           uint32_t tile_lo, uint32_t tile_n, uint64_t t, uint64_t delivered, uint32_t aoff,
-                           uint32_t kpoff, uint32_t *cnt, uint32_t *cnt_next)
+                           uint32_t tile_lo, uint32_t tile_n, uint64_t t, uint32_t tslot, uint64_t delivered,
+                           uint32_t aoff, uint32_t kpoff, uint32_t *cnt, uint32_t *cnt_next)
 {
     const StepArgs &a = ra.s;
     const ModelArgs &m = a.m;
@@ -693,7 +697,7 @@ __device__ void run_update(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x,
     // the other counter, last read before the barrier that began this step,
     // restarts at zero for the next step
     if (tid == 0) *cnt_next = 0;
-    const uint64_t seg = (uint64_t)(t % a.spk_slots) * a.tl.T + tile;
+    const uint64_t seg = (uint64_t)tslot * a.tl.T + tile;  // (tslot: the spike-list slot of t)
     uint32_t *dst = a.spk_ids + seg * a.tl.W;
     for (uint32_t q = tid; q < ns; q += kRunThreads) st_ag(dst + q, tile_lo + L.u.t.spk[q]);
     if (tid == 0) {
@@ -714,7 +718,7 @@ __device__ void run_update(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x,
 // Then one barrier, and every step's list is published to its slot.
 template <bool FIXED, bool CMP>
 __device__ void run_update_batch(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x, uint32_t tile,
-                                 uint32_t tile_lo, uint32_t tile_n, uint64_t t_first, uint32_t Db)
+                                 uint32_t tile_lo, uint32_t tile_n, uint64_t t_first, uint32_t ss, uint32_t Db)
 {
     using AccT = typename RunLDS<FIXED, CMP>::AccT;
     const StepArgs &a = ra.s;
@@ -770,14 +774,14 @@ __device__ void run_update_batch(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint3
     const uint64_t T = a.tl.T;
     for (uint32_t u = 0; u < Db; u++) {
         const uint32_t ns = L.u.t.nb[u];
-        const uint64_t seg = ((t_first + u) % a.spk_slots) * T + tile;
+        const uint64_t seg = (uint64_t)(ss + u < a.spk_slots ? ss + u : ss + u - a.spk_slots) * T + tile;
         uint32_t *dst = a.spk_ids + seg * W;
         for (uint32_t k = tid; k < ns; k += kRunThreads) st_ag(dst + k, tile_lo + L.u.t.spk[u * W + k]);
     }
     if (tid < Db) {
         const uint64_t t = t_first + tid;
         const uint32_t ns = L.u.t.nb[tid];
-        st_ag(&a.spk_cnt[(t % a.spk_slots) * T + tile], ns);
+        st_ag(&a.spk_cnt[(uint64_t)(ss + tid < a.spk_slots ? ss + tid : ss + tid - a.spk_slots) * T + tile], ns);
         if (ns) atomicAdd(&a.counts8[t * kGroups + x], ns);
         const unsigned long long delivered = L.u.t.dlv[tid];
         if (delivered) atomicAdd((unsigned long long *)&a.delivered8[t * kGroups + x], delivered);
@@ -789,13 +793,13 @@ __device__ void run_update_batch(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint3
 // pre[Db * T] = all of them; uslot[u] = the spike-list slot of step u.  A
 // one-step batch finds the counts in pre[tile] already (wait_tiles).
 template <bool FIXED, bool CMP>
-__device__ uint32_t load_spike_batch(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint64_t t_first, uint32_t Db)
+__device__ uint32_t load_spike_batch(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t slot0, uint32_t Db)
 {
     const uint32_t T = a.tl.T, W = a.tl.W, NS = Db * T;
     constexpr uint32_t kPerMax = kRunMaxT * kRunMaxD / kRunThreads;  // segments per thread, at most
     const uint32_t per = (NS + kRunThreads - 1) / kRunThreads;
     const uint32_t b0 = threadIdx.x * per;
-    const uint32_t slot0 = (uint32_t)(t_first % a.spk_slots);  // Db <= spk_slots / 2: one wrap at most
+    // (slot0: the spike-list slot of the first step; Db <= spk_slots / 2: one wrap at most)
     uint32_t c[kPerMax], sum = 0;
 #pragma unroll
     for (uint32_t k = 0; k < kPerMax; k++) {  // unconditional loads from clamped indices
@@ -852,7 +856,7 @@ __device__ __forceinline__ uint32_t spike_at_batch(const StepArgs &a, const RunL
 // batches of several steps, leaves each step's count in L.mstep.
 template <bool FIXED, bool CMP>
 __device__ uint32_t run_push(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x, uint32_t r, uint64_t t_first,
-                             uint32_t Db, uint64_t rbase)
+                             uint32_t ps, uint32_t ss, uint32_t Db, uint64_t rbase)
 {
     using Rec = typename SynRec<CMP>::T;
     using LT = RunLDS<FIXED, CMP>;
@@ -862,14 +866,15 @@ __device__ uint32_t run_push(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t 
     constexpr uint32_t nw = kRunThreads / kWave;
     const Tiling tl = a.tl;
     const uint32_t NB = (Db + a.lists - 1) * tl.T8, G1 = ra.R, NS = Db * tl.T;
-    // the pages of the batch's arrival slots were drained in the batch: they restart empty
+    // the pages of the batch's arrival slots were drained in the batch: they
+    // restart empty (ps, ss: the arrival and spike-list slots of t_first)
     for (uint32_t q = tid; q < Db * tl.T8; q += kRunThreads) {
         const uint32_t u = q / tl.T8, c = q - u * tl.T8;
-        L.fill[(uint32_t)((t_first + u) % a.pslots) * tl.T8 + c] = 0;
+        L.fill[(ps + u < a.pslots ? ps + u : ps + u - a.pslots) * tl.T8 + c] = 0;
     }
     for (uint32_t b = tid; b < NB; b += kRunThreads) L.u.p.bcnt[b] = 0;
     if (tid < Db) L.u.p.emit[tid] = 0;
-    const uint32_t M = load_spike_batch(a, L, t_first, Db);  // (its barriers publish the resets)
+    const uint32_t M = load_spike_batch(a, L, ss, Db);  // (its barriers publish the resets)
     if (Db > 1) {
         if (tid == 0) {  // each step's count, and where its spikes go in the raster (if they fit)
             uint64_t rb = rbase;
@@ -892,7 +897,8 @@ __device__ uint32_t run_push(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t 
     const bool rec_raster = a.raster_cap && x == 0;
     const uint32_t xlo = x * tl.Gw;
     const uint64_t cap = a.page_cap;
-    const uint32_t slot_of_a0 = (uint32_t)((t_first + a.dmin) % a.pslots);
+    const uint32_t dm = a.dmin % a.pslots;  // (ps + dm < 2 pslots)
+    const uint32_t slot_of_a0 = ps + dm < a.pslots ? ps + dm : ps + dm - a.pslots;
     for (uint32_t c0 = k0; c0 < k1; c0 += kRunChunk) {
         const uint32_t K = k1 - c0 < kRunChunk ? k1 - c0 : kRunChunk;
         uint32_t len = 0, uo = 0;
@@ -1158,6 +1164,10 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
     // within a batch comes from a spike before it, so it has been filed.
     const uint32_t D = DIRECT ? 1u : ra.D;
     uint64_t s = 0;
+    // the arrival slot and the spike-list slot of t_first, advanced by Db per
+    // batch (Db <= pslots, spk_slots: one wrap at most) instead of a 64-bit
+    // remainder per use
+    uint32_t ps = (uint32_t)(ra.t0 % a.pslots), ss = (uint32_t)(ra.t0 % a.spk_slots);
     while (s < ra.n_steps) {
         const uint32_t Db = (uint32_t)(ra.n_steps - s < D ? ra.n_steps - s : D);
         const uint64_t t_first = ra.t0 + s;
@@ -1175,13 +1185,13 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
             if constexpr (BATCH)
                 if (tid < Db) L.u.t.nb[tid] = 0;
             if (!DIRECT) {  // all steps of the batch
-                if (!BATCH && Db == 1) run_drain<FIXED, CMP, true>(a, L, x, r, tile, tile_n, t_first, 1);
-                else run_drain<FIXED, CMP, false>(a, L, x, r, tile, tile_n, t_first, Db);
+                if (!BATCH && Db == 1) run_drain<FIXED, CMP, true>(a, L, x, r, tile, tile_n, ps, 1);
+                else run_drain<FIXED, CMP, false>(a, L, x, r, tile, tile_n, ps, Db);
             }
             bool batched = false;
             if constexpr (BATCH) {
                 batched = lif && Db > 1;
-                if (batched) run_update_batch(ra, L, x, tile, tile_lo, tile_n, t_first, Db);
+                if (batched) run_update_batch(ra, L, x, tile, tile_lo, tile_n, t_first, ss, Db);
             }
             if (!batched) for (uint32_t u = 0; u < Db; u++) {
                 const uint64_t t = t_first + u;
@@ -1190,7 +1200,8 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
                     __syncthreads();
                 }
                 const uint64_t delivered = DIRECT ? run_gather(a, L, tile, tile_lo, t) : L.u.t.dlv[u];
-                run_update<FIXED, CMP, DIRECT>(ra, L, x, tile, tile_lo, tile_n, t, delivered, u * tl.W,
+                const uint32_t tslot = ss + u < a.spk_slots ? ss + u : ss + u - a.spk_slots;
+                run_update<FIXED, CMP, DIRECT>(ra, L, x, tile, tile_lo, tile_n, t, tslot, delivered, u * tl.W,
                                                lif ? u * tl.W : 0u, &L.nspk2[u & 1u], &L.nspk2[(u + 1u) & 1u]);
             }
         }
@@ -1228,12 +1239,14 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
                 __syncthreads();  // pre[] is the tile's scratch again
             }
         } else {
-            const uint32_t M = run_push(ra, L, x, r, t_first, Db, rbase);
+            const uint32_t M = run_push(ra, L, x, r, t_first, ps, ss, Db, rbase);
             if (a.raster_cap)
                 for (uint32_t u = 0; u < Db; u++)
                     rbase = raster_advance(a, t_first + u, rbase, Db == 1 ? M : L.mstep[u], x == 0 && r == 0);
             publish_push(ra, x, r, ++ex);  // the tiles of the XCD wait for it (wait_pushes)
         }
+        ps = ps + Db < a.pslots ? ps + Db : ps + Db - a.pslots;
+        ss = ss + Db < a.spk_slots ? ss + Db : ss + Db - a.spk_slots;
     }
 
     for (uint32_t q = tid; q < tile_n; q += kRunThreads) {
