@@ -207,6 +207,13 @@ __device__ __forceinline__ uint32_t spike_at(const StepArgs &a, const uint32_t *
     return ld_u32<COH>(a.spk_ids + ((uint64_t)slot * a.tl.T + lo) * a.tl.W + (k - pre[lo]));
 }
 
+// x / T8 for x * T8 < 2^32: the high half of x * ceil(2^32 / T8) (exact:
+// the rounding of the reciprocal adds less than x / 2^32 < 1 / T8).
+__device__ __forceinline__ uint32_t div_t8(const Tiling &tl, uint32_t x)
+{
+    return tl.T8 == 1 ? x : __umulhi(x, tl.T8inv);
+}
+
 // Page (x, g1, slot, c) of the binned delivery; records at page * page_cap.
 __device__ __forceinline__ uint32_t page_of(const StepArgs &a, uint32_t x, uint32_t g1, uint32_t slot,
                                             uint32_t c)

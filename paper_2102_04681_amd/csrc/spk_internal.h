@@ -98,6 +98,7 @@ struct Tiling {
     uint32_t T8;        // tiles per group
     uint32_t T;         // tiles = 8 * T8
     uint32_t Gw;        // group width = T8 * W
+    uint32_t T8inv;     // ceil(2^32 / T8) (0 when T8 = 1): x / T8 by one high multiply
 };
 
 // Where the runs of one source row start, per XCD group (binned delivery):

@@ -804,7 +804,7 @@ __device__ uint32_t load_spike_batch(const StepArgs &a, RunLDS<FIXED, CMP> &L, u
 #pragma unroll
     for (uint32_t k = 0; k < kPerMax; k++) {  // unconditional loads from clamped indices
         const uint32_t seg = b0 + k < NS && k < per ? b0 + k : 0u;
-        const uint32_t u = seg / T, tile = seg - u * T;
+        const uint32_t u = Db == 1 ? 0u : seg / T, tile = seg - u * T;
         const uint32_t slot = slot0 + u < a.spk_slots ? slot0 + u : slot0 + u - a.spk_slots;
         const uint32_t v = Db == 1 ? L.u.p.pre[seg] : ld_u32<true>(a.spk_cnt + (uint64_t)slot * T + tile);
         c[k] = b0 + k < NS && k < per ? (v < W ? v : W) : 0u;
@@ -839,7 +839,7 @@ __device__ __forceinline__ uint32_t spike_at_batch(const StepArgs &a, const RunL
         const uint32_t mid = (lo + hi + 1) >> 1;
         if (pre[mid] <= k) lo = mid; else hi = mid - 1;
     }
-    const uint32_t T = a.tl.T, uu = lo / T, tile = lo - uu * T;
+    const uint32_t T = a.tl.T, uu = NS == T ? 0u : lo / T, tile = lo - uu * T;
     *u = uu;
     return ld_u32<true>(a.spk_ids + ((uint64_t)L.u.p.uslot[uu] * T + tile) * a.tl.W + (k - pre[lo]));
 }
@@ -869,7 +869,7 @@ __device__ uint32_t run_push(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t 
     // the pages of the batch's arrival slots were drained in the batch: they
     // restart empty (ps, ss: the arrival and spike-list slots of t_first)
     for (uint32_t q = tid; q < Db * tl.T8; q += kRunThreads) {
-        const uint32_t u = q / tl.T8, c = q - u * tl.T8;
+        const uint32_t u = div_t8(tl, q), c = q - u * tl.T8;
         L.fill[(ps + u < a.pslots ? ps + u : ps + u - a.pslots) * tl.T8 + c] = 0;
     }
     for (uint32_t b = tid; b < NB; b += kRunThreads) L.u.p.bcnt[b] = 0;
@@ -893,7 +893,9 @@ __device__ uint32_t run_push(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t 
     }
     // one step: its spikes go to the raster from rbase on, if they fit
     const bool one_fits = a.raster_cap && rbase + M <= a.raster_cap;
-    const uint32_t k0 = (uint32_t)((uint64_t)M * r / G1), k1 = (uint32_t)((uint64_t)M * (r + 1) / G1);
+    // [M r / G1, M (r + 1) / G1) in 32-bit arithmetic: M = mq G1 + mr
+    const uint32_t mq = M / G1, mr = M - mq * G1;
+    const uint32_t k0 = mq * r + mr * r / G1, k1 = mq * (r + 1) + mr * (r + 1) / G1;
     const bool rec_raster = a.raster_cap && x == 0;
     const uint32_t xlo = x * tl.Gw;
     const uint64_t cap = a.page_cap;
@@ -975,7 +977,7 @@ __device__ uint32_t run_push(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t 
                 for (uint32_t k = 0; k < P; k++) {
                     if (b0 + k < NB) {
                         const uint32_t bb = b0 + k, cnt = L.u.p.bcnt[bb];
-                        const uint32_t ao = bb / tl.T8, cc = bb - ao * tl.T8;
+                        const uint32_t ao = div_t8(tl, bb), cc = bb - ao * tl.T8;
                         uint32_t sl = slot_of_a0 + ao;
                         sl = sl >= a.pslots ? sl - a.pslots : sl;
                         uint32_t &f = L.fill[sl * tl.T8 + cc];
@@ -1008,7 +1010,7 @@ __device__ uint32_t run_push(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t 
                     if constexpr (CMP) a.pages16[e] = (uint16_t)low;
                     else a.pages[e] = make_int2((int)low, r2.y);
                 } else {
-                    const uint32_t ao = b / tl.T8, cc = b - ao * tl.T8;
+                    const uint32_t ao = div_t8(tl, b), cc = b - ao * tl.T8;
                     uint32_t sl = slot_of_a0 + ao;
                     sl = sl >= a.pslots ? sl - a.pslots : sl;
                     long long units;
@@ -1031,7 +1033,7 @@ __device__ uint32_t run_push(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t 
     // publish the fill counters of all pages of this block
     const uint32_t NF = a.pslots * tl.T8;
     for (uint32_t f = tid; f < NF; f += kRunThreads) {
-        const uint32_t sl = f / tl.T8;
+        const uint32_t sl = div_t8(tl, f);
         a.pfill[page_of(a, x, r, sl, f - sl * tl.T8)] = L.fill[f];
     }
     // events emitted at each step of the batch, counted once per spike (group 0)
@@ -1044,11 +1046,12 @@ __device__ uint32_t run_push(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t 
 // the run of its row that falls into the tile.
 template <bool FIXED, bool CMP>
 __device__ uint64_t run_gather(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t tile, uint32_t tile_lo,
-                               uint64_t t)
+                               uint64_t t, uint32_t tslot)
 {
     uint64_t mine = 0;
     if (t >= a.dmin) {
-        const uint32_t dslot = (uint32_t)((t - a.dmin) % a.spk_slots);
+        // the spike-list slot of t - dmin (tslot: that of t; dmin < spk_slots)
+        const uint32_t dslot = tslot >= a.dmin ? tslot - a.dmin : tslot + a.spk_slots - a.dmin;
         const uint32_t P = load_spike_set<true>(a, dslot, L.u.t.pre, L.ws);
         mine = gather_direct<FIXED, CMP, true>(a, L.u.t.acc, L.u.t.pre, L.u.t.wpre, L.u.t.wbeg, tile, tile_lo, P,
                                                dslot, -1);
@@ -1141,7 +1144,7 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
     if (!DIRECT) {
         const uint32_t NF = a.pslots * tl.T8;
         for (uint32_t f = tid; f < NF; f += kRunThreads) {
-            const uint32_t sl = f / tl.T8;
+            const uint32_t sl = div_t8(tl, f);
             L.fill[f] = a.pfill[page_of(a, x, r, sl, f - sl * tl.T8)];
         }
     }
@@ -1199,8 +1202,8 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
                     if (!lif) run_draws(a, L, tile_lo, tile_n, t, 1);
                     __syncthreads();
                 }
-                const uint64_t delivered = DIRECT ? run_gather(a, L, tile, tile_lo, t) : L.u.t.dlv[u];
                 const uint32_t tslot = ss + u < a.spk_slots ? ss + u : ss + u - a.spk_slots;
+                const uint64_t delivered = DIRECT ? run_gather(a, L, tile, tile_lo, t, tslot) : L.u.t.dlv[u];
                 run_update<FIXED, CMP, DIRECT>(ra, L, x, tile, tile_lo, tile_n, t, tslot, delivered, u * tl.W,
                                                lif ? u * tl.W : 0u, &L.nspk2[u & 1u], &L.nspk2[(u + 1u) & 1u]);
             }

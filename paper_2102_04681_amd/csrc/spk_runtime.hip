@@ -162,6 +162,7 @@ Tiling make_tiling(uint32_t n)
     tl.T8 = (uint32_t)((n + 8ull * W - 1) / (8ull * W));
     tl.T = kGroups * tl.T8;
     tl.Gw = tl.T8 * W;
+    tl.T8inv = tl.T8 > 1 ? (uint32_t)(((1ull << 32) + tl.T8 - 1) / tl.T8) : 0u;
     return tl;
 }
 
