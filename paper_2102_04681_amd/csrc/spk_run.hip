@@ -157,6 +157,7 @@ struct RunLDS {
     uint32_t nspk2[3];          // spike counters of the update, alternating between steps; [2] = 0
     uint32_t pstop[4];          // wait_tiles: a polling wave gave up
     uint32_t pq[2][4];          // look_tiles: a polling wave saw its words complete (by look parity)
+    uint32_t ptot[4];           // one-step batches: the spikes of each polling wave's 64 tiles
     uint32_t x, r, stop;
     // the neuron model's constants, read by the update from here into vector
     // registers (kept in scalar registers they spill across the long kernel)
@@ -291,11 +292,26 @@ __device__ bool spin_all_stamp(const uint32_t *p, uint32_t n, uint32_t e, uint32
     }
 }
 
+// A polling wave's part of a one-step batch's spike prefix, from the words
+// of its tiles w * 64 .. w * 64 + n - 1 (all lanes active): the exclusive
+// prefix of their spike counts (each at most W) at pre[w * 64 + lane], their
+// sum at ptot[w]; load_spike_batch adds the sums of the waves before.
+template <bool FIXED, bool CMP>
+__device__ __forceinline__ void poller_prefix(RunLDS<FIXED, CMP> &L, uint32_t w, uint32_t lane, uint32_t n,
+                                              uint32_t v, uint32_t W)
+{
+    uint32_t cnt = lane < n ? v & ((1u << kTileCntBits) - 1u) : 0u;
+    cnt = cnt < W ? cnt : W;
+    const uint32_t inc = wave_scan_incl_u32(cnt);
+    if (lane < n) L.u.p.pre[w * kWave + lane] = inc - cnt;
+    if (lane == kWave - 1) L.ptot[w] = inc;
+}
+
 // Start of a push phase (binned delivery): waves 0-3 wait until the progress
 // word of every tile (64 per wave) carries batch e: then every spike list of
 // the batch is complete, and every tile has drained the pages of the batch's
 // arrival steps, which this push phase may start to refill.  For a one-step
-// batch the words' spike counts go to pre[tile] (the push phase's LDS).
+// batch the words' spike counts go into the spike prefix (poller_prefix).
 // Words are kept per batch parity: a tile publishes batch e + 1 only after
 // the push phases of batch e of its own XCD, and batch e + 2 only after
 // those of batch e + 1 of every XCD, so the words of parity e & 1 still hold
@@ -309,7 +325,7 @@ __device__ bool wait_tiles(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t e,
         const uint32_t n = T - w * kWave < kWave ? T - w * kWave : kWave, lane = lane_id();
         uint32_t v;
         const bool ok = spin_all_stamp(&c->tilep[e & 1u][w * kWave * kTileWordStride], n, e, &c->abort_flag, &v);
-        if (counts && ok && lane < n) L.u.p.pre[w * kWave + lane] = v & ((1u << kTileCntBits) - 1u);
+        if (counts && ok) poller_prefix(L, w, lane, n, v, ra.s.tl.W);
         if (lane == 0) {
             L.pstop[w] = ok ? 0u : 1u;
             if (!ok) atomicOr(ra.s.flags, kRunStoppedFlag);
@@ -323,7 +339,7 @@ __device__ bool wait_tiles(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t e,
 
 // One look at the tiles' progress words (as wait_tiles, without waiting),
 // with work() done while the loads are in flight: true if every tile has
-// published batch e (and then, with counts, pre[tile] holds the counts).
+// published batch e (and then, with counts, the spike prefix is in place).
 template <bool FIXED, bool CMP, class Work>
 __device__ bool look_tiles(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t e, bool counts, uint32_t par,
                            Work &&work)
@@ -337,7 +353,7 @@ __device__ bool look_tiles(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t e,
     if (poller) {
         const uint32_t want = e & (0xffffffffu >> kTileCntBits);
         const bool ok = __all(lane >= n || (v >> kTileCntBits) == want);
-        if (counts && ok && lane < n) L.u.p.pre[w * kWave + lane] = v & ((1u << kTileCntBits) - 1u);
+        if (counts && ok) poller_prefix(L, w, lane, n, v, ra.s.tl.W);
         if (lane == 0) L.pq[par][w] = ok ? 1u : 0u;
     }
     __syncthreads();
@@ -791,11 +807,30 @@ __device__ void run_update_batch(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint3
 // Spike counts of the Db steps t_first .. t_first + Db - 1 as one list in
 // (step, tile) order: pre[u * T + tile] = spikes before segment (u, tile),
 // pre[Db * T] = all of them; uslot[u] = the spike-list slot of step u.  A
-// one-step batch finds the counts in pre[tile] already (wait_tiles).
+// one-step batch finds each polling wave's part in place already
+// (poller_prefix) and adds the sums of the waves before.
 template <bool FIXED, bool CMP>
 __device__ uint32_t load_spike_batch(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t slot0, uint32_t Db)
 {
     const uint32_t T = a.tl.T, W = a.tl.W, NS = Db * T;
+    if (Db == 1) {
+        // the polling waves left each wave's exclusive prefix in pre[] and
+        // its sum in ptot[] (T <= 256: one tile per thread)
+        uint32_t before = 0, tot = 0;
+#pragma unroll
+        for (uint32_t k = 0; k < kRunMaxT / kWave; k++) {
+            const uint32_t v = k * kWave < T ? L.ptot[k] : 0u;
+            before += k < threadIdx.x / kWave ? v : 0u;
+            tot += v;
+        }
+        if (threadIdx.x < T) L.u.p.pre[threadIdx.x] += before;
+        if (threadIdx.x == 0) {
+            L.u.p.pre[T] = tot;
+            L.u.p.uslot[0] = slot0;
+        }
+        lds_sync();
+        return tot;
+    }
     constexpr uint32_t kPerMax = kRunMaxT * kRunMaxD / kRunThreads;  // segments per thread, at most
     const uint32_t per = (NS + kRunThreads - 1) / kRunThreads;
     const uint32_t b0 = threadIdx.x * per;
@@ -804,9 +839,9 @@ __device__ uint32_t load_spike_batch(const StepArgs &a, RunLDS<FIXED, CMP> &L, u
 #pragma unroll
     for (uint32_t k = 0; k < kPerMax; k++) {  // unconditional loads from clamped indices
         const uint32_t seg = b0 + k < NS && k < per ? b0 + k : 0u;
-        const uint32_t u = Db == 1 ? 0u : seg / T, tile = seg - u * T;
+        const uint32_t u = seg / T, tile = seg - u * T;
         const uint32_t slot = slot0 + u < a.spk_slots ? slot0 + u : slot0 + u - a.spk_slots;
-        const uint32_t v = Db == 1 ? L.u.p.pre[seg] : ld_u32<true>(a.spk_cnt + (uint64_t)slot * T + tile);
+        const uint32_t v = ld_u32<true>(a.spk_cnt + (uint64_t)slot * T + tile);
         c[k] = b0 + k < NS && k < per ? (v < W ? v : W) : 0u;
         sum += c[k];
     }
