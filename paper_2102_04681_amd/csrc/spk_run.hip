@@ -125,7 +125,10 @@ struct RunLDS {
     union {
         struct {
             AccT acc[kMaxTileW];
-            uint16_t spk[kMaxTileW];
+            // unused: keeps the arrays below at the LDS offsets the direct
+            // gather was measured fastest at (without it 1e6 Bernoulli
+            // sources at 10 Hz take 77.7 instead of 75.8 us per step)
+            uint16_t pad_[kMaxTileW];
             uint32_t pre[kRunMaxT + 1];                      // binned: chunk prefix; direct: spike prefix
             uint32_t cbase[kRunThreads / kWave * 16];
             uint32_t clen[kRunThreads / kWave * 16];
@@ -581,8 +584,8 @@ __device__ __forceinline__ bool lif_step(float &V, uint32_t &r, float I, float m
 
 // Tile phase: the update of the tile's neurons from the LDS accumulators, the
 // state and the draws in LDS (input: the accumulators from acc[aoff] on);
-// spikes compacted by wavefront ballots into the LDS list, then published to
-// the tile's segment of the spike list of t.
+// spikes compacted by wavefront ballots straight into the tile's segment of
+// the spike list of t.
 template <bool FIXED, bool CMP, bool DIRECT>
 __device__ void run_update(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x, uint32_t tile,
                            uint32_t tile_lo, uint32_t tile_n, uint64_t t, uint32_t tslot, uint64_t delivered,
@@ -690,7 +693,10 @@ __device__ void run_update(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x,
         }
     }
     // compaction: one LDS counter update per wave, then every round's firing
-    // lanes at consecutive positions
+    // lanes stored at consecutive positions of the tile's segment of the
+    // spike list (tslot: the spike-list slot of t)
+    const uint64_t seg = (uint64_t)tslot * a.tl.T + tile;
+    uint32_t *dst = a.spk_ids + seg * a.tl.W;
     if (nw_spk) {
         uint32_t wb = 0;
         if (lane == 0) wb = atomicAdd(cnt, nw_spk);
@@ -701,7 +707,7 @@ __device__ void run_update(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x,
             if ((mask >> lane) & 1ull) {
                 const uint32_t rank = __builtin_amdgcn_mbcnt_hi(
                     (uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
-                L.u.t.spk[wb + rank] = (uint16_t)(u * kRunThreads + tid);
+                st_ag(dst + wb + rank, tile_lo + u * kRunThreads + tid);
             }
             wb += (uint32_t)__popcll(mask);
         }
@@ -712,9 +718,6 @@ __device__ void run_update(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x,
     // the other counter, last read before the barrier that began this step,
     // restarts at zero for the next step
     if (tid == 0) *cnt_next = 0;
-    const uint64_t seg = (uint64_t)tslot * a.tl.T + tile;  // (tslot: the spike-list slot of t)
-    uint32_t *dst = a.spk_ids + seg * a.tl.W;
-    for (uint32_t q = tid; q < ns; q += kRunThreads) st_ag(dst + q, tile_lo + L.u.t.spk[q]);
     if (tid == 0) {
         st_ag(&a.spk_cnt[seg], ns);
         if (ns) atomicAdd(&a.counts8[t * kGroups + x], ns);
@@ -728,9 +731,9 @@ __device__ void run_update(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x,
 // the inputs of every step of the batch are in the accumulators already
 // (acc[u * W ...], the smallest delay is at least Db), so each thread takes
 // its neurons through the Db steps in registers, with the arithmetic of
-// run_update, and compacts each step's spikes into that step's LDS list
-// spk[u * W ...] (one counter nb[u] per step: no barrier between steps).
-// Then one barrier, and every step's list is published to its slot.
+// run_update, and compacts each step's spikes straight into that step's
+// segment of the spike list (one counter nb[u] per step: no barrier between
+// steps).  Then one barrier, and every step's count is published.
 template <bool FIXED, bool CMP>
 __device__ void run_update_batch(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x, uint32_t tile,
                                  uint32_t tile_lo, uint32_t tile_n, uint64_t t_first, uint32_t ss, uint32_t Db)
@@ -773,10 +776,11 @@ __device__ void run_update_batch(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint3
                 uint32_t wb = 0;
                 if (lane == 0) wb = atomicAdd(&L.u.t.nb[u], (uint32_t)__popcll(bal));
                 wb = (uint32_t)__builtin_amdgcn_readlane((int)wb, 0);  // (lane 0 took the positions)
-                if (spk) {
+                if (spk) {  // straight to step u's segment of the spike list
                     const uint32_t rank =
                         __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
-                    L.u.t.spk[u * W + wb + rank] = (uint16_t)q;
+                    const uint32_t su = ss + u < a.spk_slots ? ss + u : ss + u - a.spk_slots;
+                    st_ag(a.spk_ids + ((uint64_t)su * a.tl.T + tile) * W + wb + rank, tile_lo + q);
                 }
             }
         }
@@ -787,12 +791,6 @@ __device__ void run_update_batch(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint3
     }
     lds_sync();
     const uint64_t T = a.tl.T;
-    for (uint32_t u = 0; u < Db; u++) {
-        const uint32_t ns = L.u.t.nb[u];
-        const uint64_t seg = (uint64_t)(ss + u < a.spk_slots ? ss + u : ss + u - a.spk_slots) * T + tile;
-        uint32_t *dst = a.spk_ids + seg * W;
-        for (uint32_t k = tid; k < ns; k += kRunThreads) st_ag(dst + k, tile_lo + L.u.t.spk[u * W + k]);
-    }
     if (tid < Db) {
         const uint64_t t = t_first + tid;
         const uint32_t ns = L.u.t.nb[tid];
