@@ -201,7 +201,7 @@ __device__ void run_draws(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t til
 // k % nr, nr = draw_units_per_step), so that a workgroup can look at the
 // tiles' words between units and stop once its wait is over (measured:
 // units of one round see the last tile published sooner than units of two
-// or four, C4 27.7 -> 27.1 us per step).
+// or four: 27.7 -> 27.1 us per step on the 3e9-synapse network).
 __device__ __forceinline__ uint32_t draw_units_per_step(uint32_t tile_n)
 {
     return (tile_n + kRunThreads - 1) / kRunThreads;
