@@ -101,3 +101,24 @@ def test_null_safety():
     L.spk_destroy(None)
     assert L.spk_step(None, 1) == spk.SPK_EINVAL
     assert L.spk_preset(7, 0, 0.0, 1, C.byref(spk.spk_params())) == spk.SPK_EINVAL
+
+
+def test_kernel_reciprocal_divisions_are_exact():
+    # The persistent kernel replaces two run-time divisions by multiplies
+    # with precomputed reciprocals; both are exact over the operand ranges
+    # the kernel uses (checked exhaustively here, in exact integers):
+    #  - x / T8 as the high 32 bits of x * ceil(2^32 / T8), for x * T8 < 2^32
+    #    (x: buckets < 1024, fill counters < 2048, resets < 4096; T8 <= 256);
+    #  - q / spc as (q * ceil(2^16 / spc)) >> 16 for q < 256, spc <= 256.
+    import numpy as np
+    x = np.arange(4096, dtype=np.uint64)
+    for t8 in range(2, 257):
+        inv = ((1 << 32) + t8 - 1) // t8
+        assert inv < (1 << 32)
+        got = (x * np.uint64(inv)) >> np.uint64(32)
+        assert np.array_equal(got, x // np.uint64(t8)), t8
+    q = np.arange(256, dtype=np.uint64)
+    for spc in range(1, 257):
+        inv = (65536 + spc - 1) // spc
+        got = (q * np.uint64(inv)) >> np.uint64(16)
+        assert np.array_equal(got, q // np.uint64(spc)), spc
