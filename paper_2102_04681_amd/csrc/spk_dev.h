@@ -226,6 +226,23 @@ __device__ __forceinline__ uint32_t arrival_slot(const StepArgs &a, uint64_t t, 
     return dbg ? 0u : (uint32_t)((t + a.dmin + j) % a.pslots);
 }
 
+// The same from base = arrival_slot(a, t, 0, dbg), without a 64-bit
+// remainder per use (j < lists <= pslots: one wrap at most).
+__device__ __forceinline__ uint32_t arrival_slot_from(const StepArgs &a, uint32_t base, uint32_t j, bool dbg)
+{
+    const uint32_t sl = base + j;
+    return dbg ? 0u : (sl < a.pslots ? sl : sl - a.pslots);
+}
+
+// [M r / G, M (r + 1) / G) in 32-bit arithmetic (M = mq G + mr): the r-th of
+// G equal shares of M items.
+__device__ __forceinline__ void equal_share(uint32_t M, uint32_t r, uint32_t G, uint32_t *k0, uint32_t *k1)
+{
+    const uint32_t mq = M / G, mr = M - mq * G;
+    *k0 = mq * r + mr * r / G;
+    *k1 = mq * (r + 1) + mr * (r + 1) / G;
+}
+
 // Accumulator conversions.  fp32 mode: exact int64 multiple of 2^-S64.
 __device__ __forceinline__ long long to_fixed64(int32_t wbits, int32_t s64)
 {

@@ -111,14 +111,17 @@ __global__ __launch_bounds__(kProcThreads) void k_push_proc(StepArgs a, uint32_t
     const uint32_t sslot = (uint32_t)(t % a.spk_slots);
     const uint32_t kout = a.pr.k_out;
 
+    const uint32_t abase = arrival_slot(a, t, 0, dbg);
     for (uint32_t b = tid; b < NB; b += kProcThreads) {
-        const uint32_t p = page_of(a, x, g1, arrival_slot(a, t, b / tl.T8, dbg), b % tl.T8);
+        const uint32_t j = div_t8(tl, b);
+        const uint32_t p = page_of(a, x, g1, arrival_slot_from(a, abase, j, dbg), b - j * tl.T8);
         L.pidx[b] = p;
         L.fill[b] = a.pfill[p];
         L.bcnt[b] = 0;
     }
     const uint32_t M = dbg ? a.dbg_n : load_spike_set(a, sslot, L.pre, L.ws);
-    const uint32_t k0 = (uint32_t)((uint64_t)M * g1 / G1), k1 = (uint32_t)((uint64_t)M * (g1 + 1) / G1);
+    uint32_t k0, k1;
+    equal_share(M, g1, G1, &k0, &k1);
     const uint32_t xlo = x * tl.Gw;
     const uint64_t cap = a.page_cap;
     uint64_t emitted = 0;
@@ -261,7 +264,9 @@ __global__ __launch_bounds__(kProcThreads) void k_push_proc(StepArgs a, uint32_t
                         units = units_of<FIXED>(r2.y, a.m.shift64);
                         local = low;
                     }
-                    overflow_add<FIXED>(a, arrival_slot(a, t, b / tl.T8, dbg), x * tl.T8 + b % tl.T8, local, units);
+                    const uint32_t jb = div_t8(tl, b);
+                    overflow_add<FIXED>(a, arrival_slot_from(a, abase, jb, dbg), x * tl.T8 + b - jb * tl.T8, local,
+                                        units);
                 }
             }
             uint32_t any = 0;
@@ -326,15 +331,18 @@ __global__ __launch_bounds__(kProcThreads) void k_push_proc_once(StepArgs a, uin
     const uint32_t sslot = (uint32_t)(t % a.spk_slots);
     const uint32_t kout = a.pr.k_out;
 
+    const uint32_t abase = arrival_slot(a, t, 0, dbg);
     for (uint32_t q = tid; q < NB; q += kProcThreads) {
-        const uint32_t j = q / T, tt = q - j * T, x = tt / tl.T8;
-        const uint32_t p = page_of(a, x, b, arrival_slot(a, t, j, dbg), tt - x * tl.T8);
+        // (q / T = (q / 8) / T8: T = 8 T8)
+        const uint32_t j = div_t8(tl, q >> 3), tt = q - j * T, x = div_t8(tl, tt);
+        const uint32_t p = page_of(a, x, b, arrival_slot_from(a, abase, j, dbg), tt - x * tl.T8);
         L.pidx[q] = p;
         L.fill[q] = a.pfill[p];
         L.bcnt[q] = 0;
     }
     const uint32_t M = dbg ? a.dbg_n : load_spike_set(a, sslot, L.pre, L.ws);
-    const uint32_t k0 = (uint32_t)((uint64_t)M * b / NBLK), k1 = (uint32_t)((uint64_t)M * (b + 1) / NBLK);
+    uint32_t k0, k1;
+    equal_share(M, b, NBLK, &k0, &k1);
     const uint64_t cap = a.page_cap;
     const bool uniform_w = !CMP && a.pr.w_uniform;
     uint64_t emitted = 0;
@@ -456,7 +464,8 @@ __global__ __launch_bounds__(kProcThreads) void k_push_proc_once(StepArgs a, uin
                         units = units_of<FIXED>(r2.y, a.m.shift64);
                         local = low;
                     }
-                    overflow_add<FIXED>(a, arrival_slot(a, t, bk / T, dbg), bk % T, local, units);
+                    const uint32_t jb = div_t8(tl, bk >> 3);
+                    overflow_add<FIXED>(a, arrival_slot_from(a, abase, jb, dbg), bk - jb * T, local, units);
                 }
             }
             uint32_t any = 0;

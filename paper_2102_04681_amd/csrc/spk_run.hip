@@ -925,9 +925,8 @@ __device__ uint32_t run_push(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t 
     }
     // one step: its spikes go to the raster from rbase on, if they fit
     const bool one_fits = a.raster_cap && rbase + M <= a.raster_cap;
-    // [M r / G1, M (r + 1) / G1) in 32-bit arithmetic: M = mq G1 + mr
-    const uint32_t mq = M / G1, mr = M - mq * G1;
-    const uint32_t k0 = mq * r + mr * r / G1, k1 = mq * (r + 1) + mr * (r + 1) / G1;
+    uint32_t k0, k1;
+    equal_share(M, r, G1, &k0, &k1);
     const bool rec_raster = a.raster_cap && x == 0;
     const uint32_t xlo = x * tl.Gw;
     const uint64_t cap = a.page_cap;
