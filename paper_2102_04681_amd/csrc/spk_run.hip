@@ -274,14 +274,15 @@ __device__ void publish_tile(const RunArgs &ra, uint32_t tile, uint32_t e, const
 }
 
 // Wait (one wave) until each of the n <= 64 words p[0..n) carries the stamp e
-// in its bits kTileCntBits and up; leaves lane k's word in *v.  False if the
-// wait gave up or another workgroup did.
+// in its bits kTileCntBits and up; leaves lane k's word in *v.  On entry *v
+// holds the lane's word as last seen: a lane whose word already carries e
+// loads it no more.  False if the wait gave up or another workgroup did.
 __device__ bool spin_all_stamp(const uint32_t *p, uint32_t n, uint32_t e, uint32_t *abort_flag, uint32_t *v)
 {
     const uint32_t lane = lane_id(), want = e & (0xffffffffu >> kTileCntBits);
     const uint64_t t0 = wall_clock64();
     for (uint32_t k = 0;; k++) {
-        *v = ld_ag(p + (lane < n ? lane : 0u) * kTileWordStride);
+        if (lane < n && (*v >> kTileCntBits) != want) *v = ld_ag(p + lane * kTileWordStride);
         if (__all(lane >= n || (*v >> kTileCntBits) == want)) return true;
         if ((k & 31u) == 31u) {
             if (ld_ag(abort_flag)) return false;
@@ -318,16 +319,16 @@ __device__ __forceinline__ void poller_prefix(RunLDS<FIXED, CMP> &L, uint32_t w,
 // the push phases of batch e of its own XCD, and batch e + 2 only after
 // those of batch e + 1 of every XCD, so the words of parity e & 1 still hold
 // batch e for every push block that waits for it.
+// pv: the polling lane's word as last seen (look_tiles), updated here.
 template <bool FIXED, bool CMP>
-__device__ bool wait_tiles(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t e, bool counts)
+__device__ bool wait_tiles(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t e, bool counts, uint32_t &pv)
 {
     RunCtl *c = ra.ctl;
     const uint32_t T = ra.s.tl.T, w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     if (w * kWave < T) {
         const uint32_t n = T - w * kWave < kWave ? T - w * kWave : kWave, lane = lane_id();
-        uint32_t v;
-        const bool ok = spin_all_stamp(&c->tilep[e & 1u][w * kWave * kTileWordStride], n, e, &c->abort_flag, &v);
-        if (counts && ok) poller_prefix(L, w, lane, n, v, ra.s.tl.W);
+        const bool ok = spin_all_stamp(&c->tilep[e & 1u][w * kWave * kTileWordStride], n, e, &c->abort_flag, &pv);
+        if (counts && ok) poller_prefix(L, w, lane, n, pv, ra.s.tl.W);
         if (lane == 0) {
             L.pstop[w] = ok ? 0u : 1u;
             if (!ok) atomicOr(ra.s.flags, kRunStoppedFlag);
@@ -342,20 +343,23 @@ __device__ bool wait_tiles(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t e,
 // One look at the tiles' progress words (as wait_tiles, without waiting),
 // with work() done while the loads are in flight: true if every tile has
 // published batch e (and then, with counts, the spike prefix is in place).
+// pv: the polling lane's word as last seen; a lane whose word already
+// carries batch e loads it no more (fewer loads from every workgroup while
+// the last tiles finish).
 template <bool FIXED, bool CMP, class Work>
 __device__ bool look_tiles(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t e, bool counts, uint32_t par,
-                           Work &&work)
+                           uint32_t &pv, Work &&work)
 {
     const uint32_t T = ra.s.tl.T, w = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave), lane = lane_id();
     const bool poller = w * kWave < T;
     const uint32_t n = poller ? (T - w * kWave < kWave ? T - w * kWave : kWave) : 0u;
-    uint32_t v = 0;
-    if (poller) v = ld_ag(&ra.ctl->tilep[e & 1u][(w * kWave + (lane < n ? lane : 0u)) * kTileWordStride]);
+    const uint32_t want = e & (0xffffffffu >> kTileCntBits);
+    if (lane < n && (pv >> kTileCntBits) != want)
+        pv = ld_ag(&ra.ctl->tilep[e & 1u][(w * kWave + lane) * kTileWordStride]);
     work();
     if (poller) {
-        const uint32_t want = e & (0xffffffffu >> kTileCntBits);
-        const bool ok = __all(lane >= n || (v >> kTileCntBits) == want);
-        if (counts && ok) poller_prefix(L, w, lane, n, v, ra.s.tl.W);
+        const bool ok = __all(lane >= n || (pv >> kTileCntBits) == want);
+        if (counts && ok) poller_prefix(L, w, lane, n, pv, ra.s.tl.W);
         if (lane == 0) L.pq[par][w] = ok ? 1u : 0u;
     }
     __syncthreads();
@@ -978,18 +982,20 @@ __device__ uint32_t run_push(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t 
                 uom |= (uint64_t)(lw >> 8) << (4 * u);
                 rec[u] = SynRec<CMP>::load(a, idx);  // unconditional load from a clamped index
             }
-            // rank every event of the window within its bucket (LDS counters)
-            uint32_t tr[R];
+            // rank every event of the window within its bucket (LDS counters);
+            // no rank is used before the loop ends, so that the atomics are in
+            // flight together rather than one LDS round trip each.  The
+            // record becomes (bucket << 16) | page entry.
+            uint32_t rk[R];
 #pragma unroll
             for (int q = 0; q < R; q++) {
-                tr[q] = 0xffffffffu;
+                rk[q] = 0;
                 if (!((okm >> q) & 1u)) continue;
                 const uint32_t key = rec_key(rec[q]);
                 const uint32_t ao = rec_delay(key) + (uint32_t)((uom >> (4 * q)) & 0xfu);
                 const uint32_t local = rec_target(key) - xlo;
                 const uint32_t b = ao * tl.T8 + (local >> tl.logW);
-                const uint32_t rank = atomicAdd(&L.u.p.bcnt[b], 1u);
-                tr[q] = (b << 16) | rank;
+                rk[q] = atomicAdd(&L.u.p.bcnt[b], 1u);
                 const uint32_t sv = (b << 16) | (local & (tl.W - 1));
                 if constexpr (CMP) rec[q] = sv | (rec_class(key) << kPageClassShift);
                 else rec[q].x = (int)sv;
@@ -1024,10 +1030,8 @@ __device__ uint32_t run_push(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t 
             lds_sync();
             Rec *stage = L.u.p.stage;
 #pragma unroll
-            for (int q = 0; q < R; q++) {
-                if (tr[q] == 0xffffffffu) continue;
-                stage[L.u.p.bst[tr[q] >> 16] + (tr[q] & 0xffffu)] = rec[q];
-            }
+            for (int q = 0; q < R; q++)
+                if ((okm >> q) & 1u) stage[L.u.p.bst[rec_key(rec[q]) >> 16] + rk[q]] = rec[q];
             lds_sync();
             // coalesced appends: consecutive staged events of a bucket go to
             // consecutive page positions
@@ -1255,10 +1259,12 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
                 dr_t = t_first + Db;
                 dr_k = 0;
                 dr_n = has_tile && more ? Dn * draw_units_per_step(tile_n) : 0u;
+                // a polling lane's word as last seen: none yet (a stamp other than eg's)
+                uint32_t pv = ((eg ^ 1u) & (0xffffffffu >> kTileCntBits)) << kTileCntBits;
                 while (!ready && dr_k < dr_n)
-                    ready = look_tiles(ra, L, eg, Db == 1, look++ & 1u,
+                    ready = look_tiles(ra, L, eg, Db == 1, look++ & 1u, pv,
                                        [&] { run_draw_unit(a, L, tile_lo, tile_n, dr_t, dr_k++); });
-                if (!ready && !wait_tiles(ra, L, eg, Db == 1)) return;
+                if (!ready && !wait_tiles(ra, L, eg, Db == 1, pv)) return;
             }
         }
         if (DIRECT) {
