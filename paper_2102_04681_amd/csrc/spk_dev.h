@@ -315,12 +315,13 @@ __device__ __forceinline__ void overflow_add(const StepArgs &a, uint32_t slot, u
 // jf >= 0 only synapses of delay index jf are delivered.  Returns the number
 // of events this thread delivered.
 //   acc: the tile's LDS accumulators; pre: the spike-count prefix of the slot
-//   (load_spike_set); wpre, wbeg: per-wave scratch.  COH: spike IDs are read
-//   with agent-scope loads (persistent kernel).
+//   (load_spike_set); wpre, wbeg: per-wave scratch; wtab: the accumulator
+//   units of each weight class (compact records) in LDS.  COH: spike IDs are
+//   read with agent-scope loads (persistent kernel).
 template <bool FIXED, bool CMP, bool COH>
 __device__ uint32_t gather_direct(const StepArgs &a, typename Acc<FIXED>::T *acc, const uint32_t *pre,
                                   uint32_t (*wpre)[kWave + 1], uint64_t (*wbeg)[kWave], uint32_t tile,
-                                  uint32_t tile_lo, uint32_t P, uint32_t slot, int32_t jf)
+                                  uint32_t tile_lo, uint32_t P, uint32_t slot, int32_t jf, const long long *wtab)
 {
     using Rec = typename SynRec<CMP>::T;
     // (the wave count as a constant in the persistent kernel; the graph
@@ -377,7 +378,7 @@ __device__ uint32_t gather_direct(const StepArgs &a, typename Acc<FIXED>::T *acc
                 const uint32_t key = rec_key(r[u]);
                 if (jf >= 0 && (int32_t)rec_delay(key) != jf) continue;
                 long long units;
-                if constexpr (CMP) units = class_units(a, rec_class(key));
+                if constexpr (CMP) units = wtab[rec_class(key)];
                 else units = units_of<FIXED>(r[u].y, a.m.shift64);
                 Acc<FIXED>::add(&acc[rec_target(key) - tile_lo], units);
                 mine++;

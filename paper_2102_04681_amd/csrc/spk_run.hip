@@ -167,6 +167,10 @@ struct RunLDS {
     float mk, v_rest, v_th, v_reset, i_bias, ext_w;
     int32_t ext_wq, bias_q, shift, shift64;
     uint32_t ref_steps, pois_len;
+    // compact records: accumulator units of each weight class, read by the
+    // drain with one LDS load per record instead of a chain of selects among
+    // kernel arguments
+    long long wtab[kMaxClasses];
 };
 
 // Per-step draws of the tile's neurons for steps t .. t + nsteps - 1: the
@@ -464,12 +468,12 @@ __device__ void run_drain(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t x, 
             const uint32_t q = u * nw + w, g = (q * spc_inv) >> 16, o = (q - g * spc) * kChunk + lane * kPer;
             const uint32_t f = g < G1 ? L.u.t.pfv[g] : 0u;
             if constexpr (CMP) {
-#pragma unroll
-                for (int hf = 0; hf < 2; hf++) {
-                    if (o + hf >= f) continue;
-                    const uint32_t rec = hf ? sr[u] >> 16 : sr[u] & 0xffffu;
-                    Acc<FIXED>::add(&L.u.t.acc[rec & kPageLocalMask], class_units(a, rec >> kPageClassShift));
-                }
+                // both records' units read before either add
+                const uint32_t r0 = sr[u] & 0xffffu, r1 = sr[u] >> 16;
+                const long long u0 = L.wtab[(r0 >> kPageClassShift) & (kMaxClasses - 1)];
+                const long long u1 = L.wtab[(r1 >> kPageClassShift) & (kMaxClasses - 1)];
+                if (o < f) Acc<FIXED>::add(&L.u.t.acc[r0 & kPageLocalMask], u0);
+                if (o + 1 < f) Acc<FIXED>::add(&L.u.t.acc[r1 & kPageLocalMask], u1);
             } else {
                 if (o < f) Acc<FIXED>::add(&L.u.t.acc[(uint32_t)sr[u].x], units_of<FIXED>(sr[u].y, a.m.shift64));
             }
@@ -507,13 +511,12 @@ __device__ void run_drain(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t x, 
             }
 #pragma unroll
             for (int u = 0; u < kDrain; u++) {
-                const uint32_t ao = (L.u.t.clen[u * nw + w] >> 8) * W;
-#pragma unroll
-                for (int hf = 0; hf < 2; hf++) {
-                    if (!((okm >> (2 * u + hf)) & 1u)) continue;
-                    const uint32_t rec = hf ? rr[u] >> 16 : rr[u] & 0xffffu;
-                    Acc<FIXED>::add(&L.u.t.acc[ao + (rec & kPageLocalMask)], class_units(a, rec >> kPageClassShift));
-                }
+                const uint32_t ao = (L.u.t.clen[u * nw + w] >> 8) << tl.logW;
+                const uint32_t r0 = rr[u] & 0xffffu, r1 = rr[u] >> 16;
+                const long long u0 = L.wtab[(r0 >> kPageClassShift) & (kMaxClasses - 1)];
+                const long long u1 = L.wtab[(r1 >> kPageClassShift) & (kMaxClasses - 1)];
+                if ((okm >> (2 * u)) & 1u) Acc<FIXED>::add(&L.u.t.acc[ao + (r0 & kPageLocalMask)], u0);
+                if ((okm >> (2 * u + 1)) & 1u) Acc<FIXED>::add(&L.u.t.acc[ao + (r1 & kPageLocalMask)], u1);
             }
         } else {
             int2 rr[kDrain];
@@ -530,7 +533,7 @@ __device__ void run_drain(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t x, 
 #pragma unroll
             for (int u = 0; u < kDrain; u++)
                 if ((okm >> u) & 1u) {
-                    const uint32_t ao = (L.u.t.clen[u * nw + w] >> 8) * W;
+                    const uint32_t ao = (L.u.t.clen[u * nw + w] >> 8) << tl.logW;
                     Acc<FIXED>::add(&L.u.t.acc[ao + (uint32_t)rr[u].x], units_of<FIXED>(rr[u].y, a.m.shift64));
                 }
         }
@@ -994,7 +997,7 @@ __device__ uint32_t run_push(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t 
                 const uint32_t key = rec_key(rec[q]);
                 const uint32_t ao = rec_delay(key) + (uint32_t)((uom >> (4 * q)) & 0xfu);
                 const uint32_t local = rec_target(key) - xlo;
-                const uint32_t b = ao * tl.T8 + (local >> tl.logW);
+                const uint32_t b = __umul24(ao, tl.T8) + (local >> tl.logW);  // (ao, T8 < 2^24)
                 rk[q] = atomicAdd(&L.u.p.bcnt[b], 1u);
                 const uint32_t sv = (b << 16) | (local & (tl.W - 1));
                 if constexpr (CMP) rec[q] = sv | (rec_class(key) << kPageClassShift);
@@ -1089,7 +1092,7 @@ __device__ uint64_t run_gather(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_
         const uint32_t dslot = tslot >= a.dmin ? tslot - a.dmin : tslot + a.spk_slots - a.dmin;
         const uint32_t P = load_spike_set<true>(a, dslot, L.u.t.pre, L.ws);
         mine = gather_direct<FIXED, CMP, true>(a, L.u.t.acc, L.u.t.pre, L.u.t.wpre, L.u.t.wbeg, tile, tile_lo, P,
-                                               dslot, -1);
+                                               dslot, -1, L.wtab);
     }
     const uint64_t tot = block_sum_u64(mine, L.ws64);
     return tot;
@@ -1135,6 +1138,7 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
         L.shift64 = mm.shift64;
         L.ref_steps = mm.ref_steps;
         L.pois_len = mm.pois_len;
+        for (uint32_t k = 0; k < kMaxClasses; k++) L.wtab[k] = a.wval[k];
         const uint32_t raw = xcc_id();
         const uint32_t x = raw & (kGroups - 1);
         if (raw >= kGroups) atomicOr(&ctl->abort_flag, kRunAbortPlacement);

@@ -266,6 +266,9 @@ struct TileLDS {
     uint32_t nspk;
     uint64_t pois[256];
     uint16_t guide[256];
+    // compact records: accumulator units of each weight class (one LDS load
+    // per record instead of a chain of selects among the kernel arguments)
+    long long wtab[kMaxClasses];
 };
 
 template <bool FIXED, bool CMP>
@@ -314,7 +317,10 @@ __global__ __launch_bounds__(kTileThreads) void k_tile(StepArgs a, uint32_t i, i
         if (tid < m.pois_len) L.pois[tid] = pz;
         if (tid < 256) L.guide[tid] = gz;
     }
-    if (tid == 0) L.nspk = 0;
+    if (tid == 0) {
+        L.nspk = 0;
+        for (uint32_t k = 0; k < kMaxClasses; k++) L.wtab[k] = a.wval[k];
+    }
 
     // 1. accumulate every event arriving at t (the state loads above stay
     //    in flight: the barriers below order LDS traffic only)
@@ -325,7 +331,8 @@ __global__ __launch_bounds__(kTileThreads) void k_tile(StepArgs a, uint32_t i, i
         // rows in this tile (only the synapses of delay d when there are several)
         uint64_t mine = 0;
         if (debug) {
-            mine = gather_direct<FIXED, CMP, false>(a, L.acc, L.pre, L.wpre, L.wbeg, tile, tile_lo, a.dbg_n, 0, a.dbg_j);
+            mine = gather_direct<FIXED, CMP, false>(a, L.acc, L.pre, L.wpre, L.wbeg, tile, tile_lo, a.dbg_n, 0, a.dbg_j,
+                                                   L.wtab);
         } else {
             for (uint32_t j = 0; j < a.lists; j++) {
                 const uint64_t d = (uint64_t)a.dmin + j;
@@ -333,7 +340,7 @@ __global__ __launch_bounds__(kTileThreads) void k_tile(StepArgs a, uint32_t i, i
                 const uint32_t dslot = (uint32_t)((t - d) % a.spk_slots);
                 const uint32_t P = load_spike_set(a, dslot, L.pre, L.ws);
                 mine += gather_direct<FIXED, CMP, false>(a, L.acc, L.pre, L.wpre, L.wbeg, tile, tile_lo, P, dslot,
-                                                         a.lists > 1 ? (int32_t)j : -1);
+                                                         a.lists > 1 ? (int32_t)j : -1, L.wtab);
                 lds_sync();
             }
         }
@@ -384,12 +391,12 @@ __global__ __launch_bounds__(kTileThreads) void k_tile(StepArgs a, uint32_t i, i
                 }
 #pragma unroll
                 for (int u = 0; u < kDrain; u++) {
-#pragma unroll
-                    for (int hf = 0; hf < 2; hf++) {
-                        if (!((okm >> (2 * u + hf)) & 1u)) continue;
-                        const uint32_t rec = hf ? r[u] >> 16 : r[u] & 0xffffu;
-                        Acc<FIXED>::add(&L.acc[rec & kPageLocalMask], class_units(a, rec >> kPageClassShift));
-                    }
+                    // both records' units read before either add
+                    const uint32_t r0 = r[u] & 0xffffu, r1 = r[u] >> 16;
+                    const long long u0 = L.wtab[(r0 >> kPageClassShift) & (kMaxClasses - 1)];
+                    const long long u1 = L.wtab[(r1 >> kPageClassShift) & (kMaxClasses - 1)];
+                    if ((okm >> (2 * u)) & 1u) Acc<FIXED>::add(&L.acc[r0 & kPageLocalMask], u0);
+                    if ((okm >> (2 * u + 1)) & 1u) Acc<FIXED>::add(&L.acc[r1 & kPageLocalMask], u1);
                 }
             } else {
                 int2 r[kDrain];
