@@ -400,11 +400,10 @@ __device__ bool wait_pushes(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x
 // The caller has zeroed acc[0 .. Db * W).  Leaves in L.u.t.dlv the events
 // delivered at each step, including any that overflowed into the global
 // accumulators (merged here).
-// ONE (Db = 1): the first kSpecU chunks per wave of the pages (an equal
-// number of chunks per page, within the page capacity) are loaded together
-// with the pages' fill counters, before the counts are known, and records
-// past a page's count are dropped; only the rest of a longer page goes
-// through the chunk tables.  The pages of an arrival step are not written
+// ONE (Db = 1): the first part of every page (an equal number of records per
+// page, within the page capacity) is loaded together with the pages' fill
+// counters, before the counts are known, and records past a page's count are
+// dropped; only the rest of a longer page goes through the chunk tables.  The pages of an arrival step are not written
 // while it is drained, so the records read are the filed ones or stale ones
 // beyond the count.
 template <bool FIXED, bool CMP, bool ONE>
@@ -429,24 +428,35 @@ __device__ void run_drain(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t x, 
     // addresses below cost no vector registers
     const uint32_t w = __builtin_amdgcn_readfirstlane(tid / kWave), lane = tid & (kWave - 1);
     constexpr uint32_t nw = kRunThreads / kWave;
-    constexpr int kSpecU = CMP ? 8 : 16;
-    // ONE: chunk q = u * nw + w of the speculative loads is chunk q % spc of
-    // push block q / spc's page; spc * kChunk records per page (S)
-    const uint32_t spc = ONE ? kSpecU * nw / G1 : 1u, S = spc * kChunk;
+    // ONE, full records: chunk q = u * nw + w of the speculative loads is
+    // chunk q % spc of push block q / spc's page.  Compact records: 2 nw load
+    // slots of 512 records (one 16-byte load per lane: the same bytes in a
+    // quarter of the load instructions, which the compute unit's queue of
+    // loads in flight admits at once), two per wave; slot v = 2 w + j is part
+    // v % lpp of push block v / lpp's page.  spc * kChunk records per page (S)
+    constexpr int kSpecU = CMP ? 2 : 16;
+    constexpr uint32_t kSlotRec = 8u * kWave;  // compact: records per load slot
+    const uint32_t lpp = CMP ? kSpecU * nw / G1 : 1u;
+    const uint32_t spc = ONE ? (CMP ? lpp * (kSlotRec / kChunk) : kSpecU * nw / G1) : 1u, S = spc * kChunk;
     // q / spc for q < 256 as (q * spc_inv) >> 16: exact, since q (spc_inv -
     // 2^16 / spc) spc < q spc < 2^16 (a division per chunk cost ~0.5 us per
-    // step)
-    const uint32_t spc_inv = (65536u + spc - 1u) / spc;
-    using Ld = typename std::conditional<CMP, uint32_t, int2>::type;
+    // step); v / lpp the same way
+    const uint32_t spc_inv = (65536u + spc - 1u) / spc, lpp_inv = (65536u + lpp - 1u) / lpp;
+    using Ld = typename std::conditional<CMP, uint4, int2>::type;
     Ld sr[ONE ? kSpecU : 1];
     if constexpr (ONE) {
 #pragma unroll
         for (int u = 0; u < kSpecU; u++) {
-            const uint32_t q = u * nw + w, g = (q * spc_inv) >> 16, o = (q - g * spc) * kChunk + lane * kPer;
-            const bool ok = g < G1 && o < cap;  // (cap is a multiple of 16: both halves of a pair)
-            const uint32_t idx = ok ? (page_of(a, x, g, pslot0, c) * cap + o) / kPer : 0u;
-            if constexpr (CMP) sr[u] = ((const uint32_t *)a.pages16)[idx];
-            else sr[u] = a.pages[idx];
+            if constexpr (CMP) {
+                const uint32_t v = kSpecU * w + u, g = (v * lpp_inv) >> 16, o = (v - g * lpp) * kSlotRec + lane * 8u;
+                const bool ok = g < G1 && o < cap;  // (cap is a multiple of 16: all 8 records of a lane)
+                const uint32_t idx = ok ? (page_of(a, x, g, pslot0, c) * cap + o) / 8u : 0u;
+                sr[u] = ((const uint4 *)a.pages16)[idx];
+            } else {
+                const uint32_t q = u * nw + w, g = (q * spc_inv) >> 16, o = (q - g * spc) * kChunk + lane * kPer;
+                const bool ok = g < G1 && o < cap;
+                sr[u] = a.pages[ok ? page_of(a, x, g, pslot0, c) * cap + o : 0u];
+            }
         }
     }
     ovf = tid < Db ? ovf : 0u;
@@ -465,16 +475,22 @@ __device__ void run_drain(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t x, 
     if constexpr (ONE) {
 #pragma unroll
         for (int u = 0; u < kSpecU; u++) {
-            const uint32_t q = u * nw + w, g = (q * spc_inv) >> 16, o = (q - g * spc) * kChunk + lane * kPer;
-            const uint32_t f = g < G1 ? L.u.t.pfv[g] : 0u;
             if constexpr (CMP) {
-                // both records' units read before either add
-                const uint32_t r0 = sr[u] & 0xffffu, r1 = sr[u] >> 16;
-                const long long u0 = L.wtab[(r0 >> kPageClassShift) & (kMaxClasses - 1)];
-                const long long u1 = L.wtab[(r1 >> kPageClassShift) & (kMaxClasses - 1)];
-                if (o < f) Acc<FIXED>::add(&L.u.t.acc[r0 & kPageLocalMask], u0);
-                if (o + 1 < f) Acc<FIXED>::add(&L.u.t.acc[r1 & kPageLocalMask], u1);
+                const uint32_t v = kSpecU * w + u, g = (v * lpp_inv) >> 16, o = (v - g * lpp) * kSlotRec + lane * 8u;
+                const uint32_t f = g < G1 ? L.u.t.pfv[g] : 0u;
+                const uint32_t wd[4] = {sr[u].x, sr[u].y, sr[u].z, sr[u].w};
+#pragma unroll
+                for (int k = 0; k < 4; k++) {
+                    // both records' units read before either add
+                    const uint32_t r0 = wd[k] & 0xffffu, r1 = wd[k] >> 16;
+                    const long long u0 = L.wtab[(r0 >> kPageClassShift) & (kMaxClasses - 1)];
+                    const long long u1 = L.wtab[(r1 >> kPageClassShift) & (kMaxClasses - 1)];
+                    if (o + 2 * k < f) Acc<FIXED>::add(&L.u.t.acc[r0 & kPageLocalMask], u0);
+                    if (o + 2 * k + 1 < f) Acc<FIXED>::add(&L.u.t.acc[r1 & kPageLocalMask], u1);
+                }
             } else {
+                const uint32_t q = u * nw + w, g = (q * spc_inv) >> 16, o = (q - g * spc) * kChunk + lane * kPer;
+                const uint32_t f = g < G1 ? L.u.t.pfv[g] : 0u;
                 if (o < f) Acc<FIXED>::add(&L.u.t.acc[(uint32_t)sr[u].x], units_of<FIXED>(sr[u].y, a.m.shift64));
             }
         }
