@@ -1234,14 +1234,16 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
         if (has_tile) {
             // binned: the draws not made before the last push phase
             for (; dr_k < dr_n; dr_k++) run_draw_unit(a, L, tile_lo, tile_n, dr_t, dr_k);
-            // binned: every push block of the XCD has filed the previous batch
-            if (!DIRECT && !wait_pushes(ra, L, x, ex)) return;
             // the push phase reused this LDS: accumulators restart at zero, and
-            // the spike count of the previous step has been read by every thread
+            // the spike count of the previous step has been read by every
+            // thread (binned: while the other push blocks finish; the barrier
+            // of the wait orders these stores before the drain)
             for (uint32_t q = tid; q < Db * tl.W; q += kRunThreads) L.u.t.acc[q] = 0;
             if (tid == 0) L.nspk2[0] = 0;
             if constexpr (BATCH)
                 if (tid < Db) L.u.t.nb[tid] = 0;
+            // binned: every push block of the XCD has filed the previous batch
+            if (!DIRECT && !wait_pushes(ra, L, x, ex)) return;
             if (!DIRECT) {  // all steps of the batch
                 if (!BATCH && Db == 1) run_drain<FIXED, CMP, true>(a, L, x, r, tile, tile_n, ps, 1);
                 else run_drain<FIXED, CMP, false>(a, L, x, r, tile, tile_n, ps, Db);
