@@ -469,7 +469,10 @@ __device__ void run_drain(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t x, 
     const uint32_t o0 = ONE ? S : 0u;
     const uint32_t ne = ne_all > o0 ? ne_all - o0 : 0u;
     uint32_t C;
-    const uint32_t cex = block_scan_u32((ne + kChunk - 1) / kChunk, L.ws, &C);  // (publishes the resets)
+    // chunks of the chunk tables: compact records 512 (one 16-byte load per
+    // lane), full records 64 (one 8-byte load per lane)
+    constexpr uint32_t kPerL = CMP ? 8u : 1u, kChunkL = kPerL * kWave;
+    const uint32_t cex = block_scan_u32((ne + kChunkL - 1) / kChunkL, L.ws, &C);  // (publishes the resets)
     if (pf) atomicAdd(&L.u.t.dlv[pu], (unsigned long long)pf);
     if (ovf) atomicOr(&L.u.t.ovfm, 1u << tid);
     if constexpr (ONE) {
@@ -495,44 +498,50 @@ __device__ void run_drain(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t x, 
             }
         }
     }
-    constexpr int kDrain = 16;
+    // chunks per wave and window: the same registers for both formats
+    constexpr int kDrain = CMP ? 4 : 16;
     constexpr uint32_t kWin = kDrain * nw;
-    const uint32_t nchp = (ne + kChunk - 1) / kChunk;
-    const uint32_t W = tl.W;
+    const uint32_t nchp = (ne + kChunkL - 1) / kChunkL;
     for (uint32_t i0 = 0; i0 < C; i0 += kWin) {
         for (uint32_t q = tid; q < kWin; q += kRunThreads) L.u.t.clen[q] = 0;
         lds_sync();
         if (tid < P) {
             const uint32_t cb = cex > i0 ? cex : i0, ce = cex + nchp < i0 + kWin ? cex + nchp : i0 + kWin;
+            // (16-byte aligned for compact records: cap is a multiple of 16, o0 of 8)
             const uint32_t pbase = page * cap + o0;
             for (uint32_t q = cb; q < ce; q++) {
-                const uint32_t o = (q - cex) * kChunk;
-                L.u.t.cbase[q - i0] = (pbase + o) / kPer;
-                L.u.t.clen[q - i0] = (ne - o < kChunk ? ne - o : kChunk) | (pu << 8);
+                const uint32_t o = (q - cex) * kChunkL;
+                L.u.t.cbase[q - i0] = (pbase + o) / kPerL;
+                L.u.t.clen[q - i0] = (ne - o < kChunkL ? ne - o : kChunkL) | (pu << 16);
             }
         }
         lds_sync();
         if constexpr (CMP) {
-            const uint32_t *pw = (const uint32_t *)a.pages16;
-            uint32_t rr[kDrain];
-            uint32_t okm = 0;
+            const uint4 *pq = (const uint4 *)a.pages16;
+            uint4 rr[kDrain];
+            uint32_t okm = 0;  // bit 8u + i: record i of the lane's 8 in chunk u
 #pragma unroll
             for (int u = 0; u < kDrain; u++) {
                 const uint32_t cw = u * nw + w;
-                const uint32_t len = L.u.t.clen[cw] & 0xffu, cb = L.u.t.cbase[cw];
-                const bool ok = 2 * lane < len;
-                const uint32_t idx = ok ? cb + lane : 0u;
-                okm |= ((uint32_t)ok | (uint32_t)(2 * lane + 1 < len) << 1) << (2 * u);
-                rr[u] = pw[idx];  // unconditional load from a clamped index
+                const uint32_t len = L.u.t.clen[cw] & 0xffffu, cb = L.u.t.cbase[cw];
+                const uint32_t o = lane * kPerL;
+                const uint32_t nv = o < len ? (len - o < kPerL ? len - o : kPerL) : 0u;
+                okm |= ((1u << nv) - 1u) << (8 * u);
+                rr[u] = pq[nv ? cb + lane : 0u];  // unconditional load from a clamped index
             }
 #pragma unroll
             for (int u = 0; u < kDrain; u++) {
-                const uint32_t ao = (L.u.t.clen[u * nw + w] >> 8) << tl.logW;
-                const uint32_t r0 = rr[u] & 0xffffu, r1 = rr[u] >> 16;
-                const long long u0 = L.wtab[(r0 >> kPageClassShift) & (kMaxClasses - 1)];
-                const long long u1 = L.wtab[(r1 >> kPageClassShift) & (kMaxClasses - 1)];
-                if ((okm >> (2 * u)) & 1u) Acc<FIXED>::add(&L.u.t.acc[ao + (r0 & kPageLocalMask)], u0);
-                if ((okm >> (2 * u + 1)) & 1u) Acc<FIXED>::add(&L.u.t.acc[ao + (r1 & kPageLocalMask)], u1);
+                const uint32_t ao = (L.u.t.clen[u * nw + w] >> 16) << tl.logW;
+                const uint32_t wd[4] = {rr[u].x, rr[u].y, rr[u].z, rr[u].w};
+#pragma unroll
+                for (int k = 0; k < 4; k++) {
+                    const uint32_t r0 = wd[k] & 0xffffu, r1 = wd[k] >> 16;
+                    const long long u0 = L.wtab[(r0 >> kPageClassShift) & (kMaxClasses - 1)];
+                    const long long u1 = L.wtab[(r1 >> kPageClassShift) & (kMaxClasses - 1)];
+                    if ((okm >> (8 * u + 2 * k)) & 1u) Acc<FIXED>::add(&L.u.t.acc[ao + (r0 & kPageLocalMask)], u0);
+                    if ((okm >> (8 * u + 2 * k + 1)) & 1u)
+                        Acc<FIXED>::add(&L.u.t.acc[ao + (r1 & kPageLocalMask)], u1);
+                }
             }
         } else {
             int2 rr[kDrain];
@@ -540,7 +549,7 @@ __device__ void run_drain(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t x, 
 #pragma unroll
             for (int u = 0; u < kDrain; u++) {
                 const uint32_t cw = u * nw + w;
-                const uint32_t len = L.u.t.clen[cw] & 0xffu, cb = L.u.t.cbase[cw];
+                const uint32_t len = L.u.t.clen[cw] & 0xffffu, cb = L.u.t.cbase[cw];
                 const bool ok = lane < len;
                 const uint32_t idx = ok ? cb + lane : 0u;
                 okm |= (uint32_t)ok << u;
@@ -549,7 +558,7 @@ __device__ void run_drain(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t x, 
 #pragma unroll
             for (int u = 0; u < kDrain; u++)
                 if ((okm >> u) & 1u) {
-                    const uint32_t ao = (L.u.t.clen[u * nw + w] >> 8) << tl.logW;
+                    const uint32_t ao = (L.u.t.clen[u * nw + w] >> 16) << tl.logW;
                     Acc<FIXED>::add(&L.u.t.acc[ao + (uint32_t)rr[u].x], units_of<FIXED>(rr[u].y, a.m.shift64));
                 }
         }
@@ -566,11 +575,11 @@ __device__ void run_drain(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t x, 
                 const uint64_t gi = st * tl.W + q;
                 if (FIXED) {
                     int32_t *o = (int32_t *)a.acc_ovf + gi;
-                    L.u.t.acc[u * W + q] += (int32_t)ld_ag((const uint32_t *)o);
+                    L.u.t.acc[u * tl.W + q] += (int32_t)ld_ag((const uint32_t *)o);
                     st_ag((uint32_t *)o, 0u);
                 } else {
                     unsigned long long *o = (unsigned long long *)a.acc_ovf + gi;
-                    L.u.t.acc[u * W + q] += __hip_atomic_load(o, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    L.u.t.acc[u * tl.W + q] += __hip_atomic_load(o, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                     __hip_atomic_store(o, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 }
             }
