@@ -378,6 +378,43 @@ def test_fixed_point_simulation_bit_identical(spk, name, mk, T, delivery, mode, 
             assert km["tile_ms"] > 0 and km["run_launches"] == 0
 
 
+# long pages in the persistent kernel's one-step drain, which loads the
+# first part of every page before the fill counts are known and the rest
+# through its chunk tables: 16,384 Bernoulli sources firing with
+# probability 0.5 per step (256 tiles), fan-out 800, delays 1-4, one weight
+# (compact records) or full records: ~800 records per page and step, within
+# the page capacity, and two sorting windows per push block; fixed point,
+# bit-identical to the oracle
+@pytest.mark.parametrize("fmt", [f for f, _ in FORMATS], ids=[n for _, n in FORMATS])
+def test_long_pages_one_step_drain_bit_identical(spk, fmt):
+    cfg = I.scaled(3, 16384, rate_hz=500.0, k_out=800, delay_min=1, delay_max=4, w_uniform=0, w_exc=1e-3)
+    cfg["acc_mode"] = I.ACC_FIXED
+    cfg["delivery"] = 2
+    cfg["syn_format"] = fmt
+    cfg["step_mode"] = 2
+    T = 40
+    _say(f"[long pages] n={cfg['n']} T={T} format={fmt}")
+    g = spk.Net(cfg, max_steps=T, raster_capacity=cfg["n"] * T)
+    st = g.stats()
+    assert st["step_mode"] == 2 and st["batch_steps"] == 1 and st["delivery"] == 2
+    if fmt == 0:
+        assert st["bytes_per_synapse"] == 4.0  # compact records
+    g.step(T)
+    offs, ids = g.raster()
+    r, ov, orf, _ = _oracle_run(cfg, T)
+    # records per page and step once every delay contributes: a step's events
+    # over the tiles and the push blocks of each group (32 on MI355X)
+    per_page = float(np.mean(r["events"][8:])) / (st["tiles"] * 32)
+    assert 600 < per_page and 1.2 * per_page < st["page_cap"], (per_page, st["page_cap"])
+    assert np.array_equal(g.spike_counts(), r["counts"]), "spike counts differ"
+    assert np.array_equal(offs, r["offs"]) and np.array_equal(ids, r["raster"]), "rasters differ"
+    assert np.array_equal(g.events(), r["events"]), "event counts differ"
+    assert np.array_equal(g.delivered(), r["delivered"]), "delivered-event counts differ"
+    gv, gr = g.state()
+    assert np.array_equal(gv.view(np.uint32), ov.view(np.uint32)), "membrane potentials differ"
+    assert np.array_equal(gr, orf)
+
+
 # degenerate shapes: a single neuron with its autapse, two neurons fully
 # connected, a network with no synapse at all (nnz = 0), one partial tile
 # (n = 37 < the smallest tile), every pair connected, in-degree 1, and 64
