@@ -171,6 +171,11 @@ struct RunLDS {
     // drain with one LDS load per record instead of a chain of selects among
     // kernel arguments
     long long wtab[kMaxClasses];
+    // the per-step statistics of the tile's last step (thread 0's), added to
+    // the global counters after the tile's publication, which then does
+    // not wait for these atomics (nothing orders them with it)
+    uint32_t st_ns;
+    unsigned long long st_ev, st_dlv;
 };
 
 // Per-step draws of the tile's neurons for steps t .. t + nsteps - 1: the
@@ -588,6 +593,16 @@ __device__ void run_drain(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t x, 
     }
 }
 
+// A step's spike, event and delivery counts of one tile added to the
+// group's global counters (global atomics, thread 0).
+__device__ __forceinline__ void step_stats(const StepArgs &a, uint32_t x, uint64_t t, uint32_t ns,
+                                           unsigned long long ev, unsigned long long dlv)
+{
+    if (ns) atomicAdd(&a.counts8[t * kGroups + x], ns);
+    if (ev) atomicAdd((unsigned long long *)&a.events8[t * kGroups + x], ev);
+    if (dlv) atomicAdd((unsigned long long *)&a.delivered8[t * kGroups + x], dlv);
+}
+
 // Forward Euler step of the membrane in single precision (Sec. IV-A; the
 // delta-current LIF reading, each operation rounded on its own):
 // (V + k (v_rest - V)) + I.
@@ -621,7 +636,7 @@ __device__ __forceinline__ bool lif_step(float &V, uint32_t &r, float I, float m
 template <bool FIXED, bool CMP, bool DIRECT>
 __device__ void run_update(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x, uint32_t tile,
                            uint32_t tile_lo, uint32_t tile_n, uint64_t t, uint32_t tslot, uint64_t delivered,
-                           uint32_t aoff, uint32_t kpoff, uint32_t *cnt, uint32_t *cnt_next)
+                           uint32_t aoff, uint32_t kpoff, uint32_t *cnt, uint32_t *cnt_next, bool late)
 {
     const StepArgs &a = ra.s;
     const ModelArgs &m = a.m;
@@ -752,10 +767,13 @@ __device__ void run_update(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x,
     if (tid == 0) *cnt_next = 0;
     if (tid == 0) {
         st_ag(&a.spk_cnt[seg], ns);
-        if (ns) atomicAdd(&a.counts8[t * kGroups + x], ns);
-        if (ev) atomicAdd((unsigned long long *)&a.events8[t * kGroups + x], (unsigned long long)ev);
-        if (delivered)
-            atomicAdd((unsigned long long *)&a.delivered8[t * kGroups + x], (unsigned long long)delivered);
+        if (late) {  // (step_stats, after the publication)
+            L.st_ns = ns;
+            L.st_ev = ev;
+            L.st_dlv = delivered;
+        } else {
+            step_stats(a, x, t, ns, ev, delivered);
+        }
     }
 }
 
@@ -1240,6 +1258,11 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
         const uint64_t t_first = ra.t0 + s;
         s += Db;
         const bool more = s < ra.n_steps;
+        // binned: the last step's statistics wait in LDS until the tile has
+        // published (step_stats); direct delivery adds them at once (measured:
+        // deferred past the grid barrier, 1e6 sources at 10 Hz took 76.2
+        // instead of 74.8 us per step)
+        bool late = false;
         if (has_tile) {
             // binned: the draws not made before the last push phase
             for (; dr_k < dr_n; dr_k++) run_draw_unit(a, L, tile_lo, tile_n, dr_t, dr_k);
@@ -1262,6 +1285,7 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
                 batched = lif && Db > 1;
                 if (batched) run_update_batch(ra, L, x, tile, tile_lo, tile_n, t_first, ss, Db);
             }
+            late = !DIRECT && !batched;
             if (!batched) for (uint32_t u = 0; u < Db; u++) {
                 const uint64_t t = t_first + u;
                 if (u) {  // the spike list of t - 1 (LDS) has been published by every thread
@@ -1271,7 +1295,8 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
                 const uint32_t tslot = ss + u < a.spk_slots ? ss + u : ss + u - a.spk_slots;
                 const uint64_t delivered = DIRECT ? run_gather(a, L, tile, tile_lo, t, tslot) : L.u.t.dlv[u];
                 run_update<FIXED, CMP, DIRECT>(ra, L, x, tile, tile_lo, tile_n, t, tslot, delivered, u * tl.W,
-                                               lif ? u * tl.W : 0u, &L.nspk2[u & 1u], &L.nspk2[(u + 1u) & 1u]);
+                                               lif ? u * tl.W : 0u, &L.nspk2[u & 1u], &L.nspk2[(u + 1u) & 1u],
+                                               late && u + 1 == Db);
             }
         }
         const uint32_t Dn = (uint32_t)(ra.n_steps - s < Dd ? ra.n_steps - s : Dd);  // (0 after the last batch)
@@ -1280,6 +1305,7 @@ __global__ __launch_bounds__(kRunThreads) void k_run(RunArgs ra)
         } else {  // binned: the tiles' progress words instead of a grid barrier
             ++eg;
             if (has_tile) publish_tile(ra, tile, eg, &L.nspk2[Db == 1 ? 0u : 2u]);
+            if (late && tid == 0) step_stats(a, x, t_first + Db - 1, L.st_ns, L.st_ev, L.st_dlv);
             // the next batch's draws while the others finish: a unit at a
             // time between looks at the tiles' words; once every tile has
             // published, the rest waits until after the push phase (the last
