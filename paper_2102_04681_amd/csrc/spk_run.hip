@@ -408,9 +408,9 @@ __device__ bool wait_pushes(const RunArgs &ra, RunLDS<FIXED, CMP> &L, uint32_t x
 // ONE (Db = 1): the first part of every page (an equal number of records per
 // page, within the page capacity) is loaded together with the pages' fill
 // counters, before the counts are known, and records past a page's count are
-// dropped; only the rest of a longer page goes through the chunk tables.  The pages of an arrival step are not written
-// while it is drained, so the records read are the filed ones or stale ones
-// beyond the count.
+// dropped; only the rest of a longer page goes through the chunk tables.
+// The pages of an arrival step are not written while it is drained, so the
+// records read are the filed ones or stale ones beyond the count.
 template <bool FIXED, bool CMP, bool ONE>
 __device__ void run_drain(const StepArgs &a, RunLDS<FIXED, CMP> &L, uint32_t x, uint32_t c, uint32_t tile,
                           uint32_t tile_n, uint32_t pslot0, uint32_t Db)
